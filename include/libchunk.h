@@ -1,0 +1,240 @@
+/*
+ * libchunk — one device's share of Piper's data-parallel training hot path
+ * on an AMD Instinct MI355X (gfx950).
+ *
+ * Piper lowers a training program to a DAG of Chunk (compute) and Comm
+ * (communication) nodes; each Chunk has an exec run on an assigned stream
+ * for one pass, F (forward) or B (backward) (Piper Section 4.1, "IR" and
+ * the PASS dimension). Split replicates Chunks per microbatch and Order
+ * sequences them (Section 4.1, "Scheduling directives"). The worker keeps
+ * forward activations until the matching backward consumes them and
+ * accumulates gradients into one flat buffer per model-state bucket
+ * (Section 4.3.2, "Memory management"); under ZeRO-1 each rank updates the
+ * optimizer state of its own shard (Section 6.2).
+ *
+ * This library implements that share for one transformer-decoder pipeline
+ * stage: Chunk F / Chunk B of every microbatch in an Order, fp32 gradient
+ * accumulation into the stage's flat bucket, and a fused AdamW step with a
+ * bf16 cast over a flat shard.
+ *
+ * Conventions shared by every entry point
+ *   - C ABI, never throws. Every function returns an lc_status; a negative
+ *     value means failure and lc_last_error() gives a message.
+ *   - Argument, descriptor and Order errors are detected on the host before
+ *     anything is enqueued: such a call has no side effects.
+ *   - "device" pointers are HIP device allocations owned by the caller; the
+ *     library allocates no device memory. Work is enqueued on `stream`
+ *     (a hipStream_t; NULL is the default stream) and nothing synchronises
+ *     the host: results are ready once the caller synchronises the stream.
+ *     LC_ERR_HIP reports a failed launch; faults surface at that sync.
+ *   - Device pointers must be 16-byte aligned (else LC_ERR_INVALID_ARG).
+ *   - Sizes and offsets are 64-bit.
+ *   - Thread-compatible: one lc_stage must not be used by two host threads
+ *     at once.
+ */
+#ifndef LIBCHUNK_H
+#define LIBCHUNK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum lc_status {
+  LC_OK = 0,
+  LC_ERR_INVALID_ARG = -1,  /* bad pointer, size, alignment or descriptor field */
+  LC_ERR_UNSUPPORTED = -2,  /* a valid shape this build does not implement      */
+  LC_ERR_BAD_ORDER = -3,    /* an Order that breaks the Order rules below        */
+  LC_ERR_STASH_FULL = -4,   /* more microbatches in flight than stash slots      */
+  LC_ERR_STATE = -5,        /* F twice for one microbatch, or B without its F    */
+  LC_ERR_WORKSPACE = -6,    /* workspace smaller than lc_workspace_bytes()       */
+  LC_ERR_HIP = -7           /* a HIP runtime call or kernel launch failed        */
+} lc_status;
+
+typedef enum lc_dtype { LC_FP32 = 0, LC_BF16 = 1 } lc_dtype;
+
+/* Piper's PASS dimension: F = forward, B = full backward (Section 4.1). */
+typedef enum lc_pass { LC_PASS_F = 0, LC_PASS_B = 1 } lc_pass;
+
+/* One pipeline stage: n_layers pre-norm decoder layers. Every layer is
+ *   n1 = RMSNorm(x; g1); q,k,v = n1 Wq^T, n1 Wk^T, n1 Wv^T; rotate-half RoPE
+ *   on q and k (positions 0..seq_len-1 per sequence, angle p*base^(-2i/hd));
+ *   o = causal softmax(q k^T / sqrt(hd)) v per head; h = x + o Wo^T;
+ *   n2 = RMSNorm(h; g2); y = h + FFN(n2)
+ * with FFN the SwiGLU (silu(n2 W1^T) * (n2 W3^T)) W2^T when n_experts == 0,
+ * else a top-k (k = 2) softmax-routed mixture of SwiGLU experts whose gate
+ * weights are renormalised over the selected experts (ties pick the lower
+ * expert index). Activations are token-major [micro_batch, seq_len,
+ * d_model]; weights are [out, in] row-major. */
+typedef struct lc_stage_desc {
+  int32_t n_layers;
+  int32_t d_model;       /* == n_heads * head_dim */
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t d_ff;          /* dense FFN width (ignored when n_experts > 0) */
+  int32_t n_experts;     /* 0 = dense SwiGLU FFN */
+  int32_t top_k;         /* experts per token (must be 2 when n_experts > 0) */
+  int32_t d_ff_expert;   /* FFN width of each expert */
+  int32_t seq_len;
+  int32_t micro_batch;   /* sequences per microbatch */
+  float rms_eps;         /* RMSNorm epsilon, inside the square root */
+  float rope_base;       /* RoPE base (10000) */
+  int32_t causal;        /* must be 1 */
+  int32_t compute_dtype; /* lc_dtype of weights and activations; gradients
+                            are always accumulated in fp32 */
+} lc_stage_desc;
+
+/* Tensor ids of the canonical flat layout (one bucket per stage). Per layer,
+ * in this order: WQ, WK, WV, WO [d,d]; G1 [d]; dense: W1 (gate) [f,d],
+ * W3 (up) [f,d], W2 (down) [d,f]; MoE: WR (router) [E,d], then for each
+ * expert e: W1 [fe,d], W3 [fe,d], W2 [d,fe]; finally G2 [d]. The gradient,
+ * master, m and v buffers use the same layout. */
+typedef enum lc_tensor_id {
+  LC_T_WQ = 0, LC_T_WK = 1, LC_T_WV = 2, LC_T_WO = 3, LC_T_G1 = 4,
+  LC_T_W1 = 5, LC_T_W3 = 6, LC_T_W2 = 7, LC_T_G2 = 8, LC_T_WR = 9
+} lc_tensor_id;
+
+/* One Order entry: run pass `pass` (lc_pass) of microbatch `mb`. */
+typedef struct lc_order_entry {
+  int32_t mb;
+  int32_t pass;
+} lc_order_entry;
+
+/* An Order over num_microbatches microbatches (Piper Section 4.1, Order).
+ * Rules (checked by lc_order_validate and again by lc_run_order):
+ *   - each (mb, F) and (mb, B) with 0 <= mb < num_microbatches appears
+ *     exactly once, and F(mb) precedes B(mb);
+ *   - the F entries and the B entries are each in increasing mb order:
+ *     a pipeline stage must consume microbatches in the order its
+ *     neighbour produced them, and Piper rejects schedules that do not
+ *     (Section 4.3.2, "Communication management");
+ *   - at most max_in_flight microbatches sit between their F and their B
+ *     (else LC_ERR_STASH_FULL). */
+typedef struct lc_order {
+  int32_t num_microbatches;
+  int32_t n_entries;
+  const lc_order_entry *entries; /* host memory, n_entries long */
+} lc_order;
+
+/* One microbatch's activations, all device pointers, [micro_batch, seq_len,
+ * d_model] in compute_dtype. `x` is read by F and again by B: it must stay
+ * valid and unchanged until B of this microbatch has been enqueued and has
+ * run. F writes `y`; B reads `dy` and writes `dx`. Unused fields may be NULL
+ * (F needs x and y; B needs x, dy and dx). */
+typedef struct lc_microbatch_desc {
+  int32_t mb;
+  int32_t reserved;
+  const void *x;
+  void *y;
+  const void *dy;
+  void *dx;
+} lc_microbatch_desc;
+
+/* The stage's bucket: compute weights in the canonical layout and the fp32
+ * gradient accumulator with the same layout. The caller zeroes `grad` (+0.0)
+ * before the first backward of a step; every backward adds its microbatch's
+ * gradient (no 1/M scaling). */
+typedef struct lc_param_bufs {
+  const void *w;   /* device, compute_dtype */
+  float *grad;     /* device, fp32 */
+} lc_param_bufs;
+
+/* AdamW hyper-parameters for shard_adam_step. step >= 1 counts optimizer
+ * steps (bias correction uses beta^step). */
+typedef struct lc_adam_hparams {
+  float lr;
+  float beta1;
+  float beta2;
+  float eps;
+  float weight_decay;
+  int32_t reserved;
+  int64_t step;
+} lc_adam_hparams;
+
+typedef struct lc_stage lc_stage; /* opaque, host memory */
+
+/* ---------------------------------------------------------------- host-only
+ * These make no HIP call and may be used without a GPU. */
+
+/* Number of elements of the stage's flat bucket. */
+lc_status lc_param_count(const lc_stage_desc *desc, size_t *n_elems);
+
+/* Offset (elements) and shape of tensor `tensor_id` of layer `layer`
+ * (expert `expert` for MoE W1/W3/W2, else pass 0). shape[1] is 1 for
+ * vectors. */
+lc_status lc_param_offset(const lc_stage_desc *desc, int32_t layer, int32_t tensor_id,
+                          int32_t expert, size_t *offset, int64_t shape[2]);
+
+/* The 1F1B Order of stage s of a P-stage pipeline over M microbatches:
+ * W = min(P-s-1, M) forwards, then M-W (forward, backward) pairs, then W
+ * backwards. `out` holds `capacity` entries (needs 2M); *n receives 2M. */
+lc_status lc_order_1f1b(int32_t M, int32_t P, int32_t s, lc_order_entry *out,
+                        int32_t capacity, int32_t *n);
+
+/* Checks an Order against the rules above for at most max_in_flight
+ * stashed microbatches. *peak (nullable) receives the largest number in
+ * flight. Returns LC_OK, LC_ERR_BAD_ORDER or LC_ERR_STASH_FULL. */
+lc_status lc_order_validate(const lc_order *order, int32_t max_in_flight, int32_t *peak);
+
+/* Device workspace a stage needs for max_in_flight stashed microbatches
+ * (activation stash + backward scratch + RoPE table). */
+lc_status lc_workspace_bytes(const lc_stage_desc *desc, int32_t max_in_flight, size_t *bytes);
+
+/* ---------------------------------------------------------------- stage
+ * lc_stage_create validates the descriptor, carves the caller's workspace
+ * (device, >= lc_workspace_bytes, 256-byte aligned) into stash slots and
+ * scratch, and enqueues the upload of the RoPE cos/sin table on `stream`.
+ * The handle owns host memory only; lc_stage_destroy frees it (synchronise
+ * the stream first). */
+lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_bytes,
+                          int32_t max_in_flight, void *stream, lc_stage **out);
+lc_status lc_stage_destroy(lc_stage *stage);
+
+/* Chunk F of one microbatch: Y = stage(X). Stashes the activations the
+ * backward needs in a free slot (LC_ERR_STATE if this microbatch is already
+ * stashed, LC_ERR_STASH_FULL if no slot is free). */
+lc_status chunk_forward(lc_stage *stage, const lc_param_bufs *params,
+                        const lc_microbatch_desc *mb, void *stream);
+
+/* Chunk B of one microbatch: dX = (dY/dX)^T dY and grad += dL/dW for
+ * L = sum(dY * Y), using the slot stashed by chunk_forward of the same mb
+ * (LC_ERR_STATE if none), which is released afterwards. Gradients are added
+ * to params->grad in fp32, one addition per element. */
+lc_status chunk_backward(lc_stage *stage, const lc_param_bufs *params,
+                         const lc_microbatch_desc *mb, void *stream);
+
+/* Runs a whole Order: validates it (no side effects on failure), then
+ * enqueues chunk_forward / chunk_backward in entry order. mbs[i] describes
+ * microbatch i (num_microbatches entries). */
+lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
+                       const lc_microbatch_desc *mbs, void *stream);
+
+/* ---------------------------------------------------------------- buffers */
+
+/* accum[i] += g[i] for i < n, in fp32 (g is fp32 or bf16 per g_dtype); each
+ * element is read and written exactly once. accum and g must not overlap. */
+lc_status chunk_accumulate_grad(float *accum, const void *g, int32_t g_dtype, size_t n,
+                                void *stream);
+
+/* AdamW over a flat shard of n elements (decoupled weight decay, bias
+ * correction). With host scalars c_wd = 1 - lr*wd, step_size =
+ * lr/(1-beta1^t) and bc2s = sqrt(1-beta2^t) (computed in double, rounded
+ * once to float), every element does, one fp32 rounding per operation:
+ *   p = p*c_wd; m = b1*m + (1-b1)*g; v = b2*v + (1-b2)*(g*g);
+ *   p = p - step_size * (m / (sqrt(v)/bc2s + eps));
+ *   out_bf16 = round-to-nearest-even(p)   (if out_bf16 != NULL)
+ * grad is fp32 or bf16 per grad_dtype. master, m, v are updated in place. */
+lc_status shard_adam_step(float *master, float *m, float *v, const void *grad,
+                          int32_t grad_dtype, uint16_t *out_bf16, size_t n,
+                          const lc_adam_hparams *hp, void *stream);
+
+/* Message for the last non-OK status returned on this thread. */
+const char *lc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBCHUNK_H */

@@ -1,0 +1,319 @@
+"""Pins for the stage oracle (oracle/stage.py) against facts fixed by the
+mathematics, independent of the oracle's own code:
+
+* finite differences of L = sum(dY*Y) in float64 (whole stage, dense and MoE)
+* softmax rows sum to one, exact zeros above the causal diagonal
+* identical keys -> causal prefix mean of V; identical values -> v0; S=1 -> v
+* causality of Y and of dX
+* accumulated microbatch gradients == full-batch gradient
+* closed forms of RMSNorm, RoPE, SwiGLU and the top-2 router
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import stage as O
+from oracle import order as OO
+
+F64 = np.float64
+
+
+def tiny_cfg(**kw):
+    base = dict(name="fd", n_layers=2, d_model=16, n_heads=2, head_dim=8, d_ff=40,
+                seq_len=8, micro_batch=2, num_microbatches=2, bf16=False)
+    base.update(kw)
+    return synth.StageConfig(**base)
+
+
+def tiny_moe_cfg(**kw):
+    base = dict(name="fdmoe", n_layers=1, d_model=16, n_heads=2, head_dim=8, d_ff=0,
+                seq_len=6, micro_batch=2, num_microbatches=2, bf16=False,
+                n_experts=4, top_k=2, d_ff_expert=24)
+    base.update(kw)
+    return synth.StageConfig(**base)
+
+
+def flat_and_loss(cfg, flat, X, dY):
+    layers = O.layer_params(cfg, flat)
+    return O.stage_loss(cfg, layers, X, dY)
+
+
+def grads(cfg, flat, X, dY):
+    layers = O.layer_params(cfg, flat)
+    Y, caches = O.stage_forward(cfg, layers, X)
+    dX, G = O.stage_backward(cfg, layers, caches, dY)
+    return Y, dX, G
+
+
+def fd_check(cfg, flat, X, dY, u_p, u_x, tol=1e-6):
+    _, dX, G = grads(cfg, flat, X, dY)
+    analytic = float(np.dot(G, u_p) + np.sum(dX * u_x))
+    norm_theta = np.sqrt(np.sum(flat ** 2) + np.sum(X ** 2))
+    norm_u = np.sqrt(np.sum(u_p ** 2) + np.sum(u_x ** 2))
+    h = 1e-5 * norm_theta / norm_u
+    lp = flat_and_loss(cfg, flat + h * u_p, X + h * u_x, dY)
+    lm = flat_and_loss(cfg, flat - h * u_p, X - h * u_x, dY)
+    numeric = (lp - lm) / (2 * h)
+    rel = abs(numeric - analytic) / max(abs(analytic), 1e-30)
+    assert rel <= tol, (numeric, analytic, rel)
+
+
+def random_inputs(cfg, seed):
+    rng = np.random.default_rng(seed)
+    flat = synth.stage_params(cfg, seed=seed, random_gains=True).astype(F64)
+    # larger weights than the workload's 0.02 so every term matters
+    flat = flat * 10.0
+    for name, off, shape in synth.layout(cfg):
+        if name.endswith(".g1") or name.endswith(".g2"):
+            flat[off:off + int(np.prod(shape))] /= 10.0
+    X = rng.standard_normal((cfg.micro_batch, cfg.seq_len, cfg.d_model))
+    dY = rng.standard_normal(X.shape)
+    return flat, X, dY
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_fd_dense_joint(seed):
+    cfg = tiny_cfg()
+    flat, X, dY = random_inputs(cfg, seed)
+    rng = np.random.default_rng(100 + seed)
+    fd_check(cfg, flat, X, dY, rng.standard_normal(flat.shape), rng.standard_normal(X.shape))
+
+
+def test_fd_dense_per_tensor():
+    """A direction confined to one tensor at a time (and to X alone)."""
+    cfg = tiny_cfg(n_layers=1)
+    flat, X, dY = random_inputs(cfg, 3)
+    rng = np.random.default_rng(7)
+    for name, off, shape in synth.layout(cfg):
+        u = np.zeros_like(flat)
+        sz = int(np.prod(shape))
+        u[off:off + sz] = rng.standard_normal(sz)
+        fd_check(cfg, flat, X, dY, u, np.zeros_like(X))
+    fd_check(cfg, flat, X, dY, np.zeros_like(flat), rng.standard_normal(X.shape))
+
+
+def _moe_inputs_with_margin(cfg, margin=1e-3):
+    for seed in range(50):
+        flat, X, dY = random_inputs(cfg, seed)
+        layers = O.layer_params(cfg, flat)
+        # routing margins at every layer input of the forward pass
+        ok = True
+        x = X
+        tabs = O.rope_tables(cfg.seq_len, cfg.head_dim, cfg.rope_base)
+        for p in layers:
+            y, c = O.layer_forward(p, x, cfg, tabs)
+            pi = np.sort(c["moe"]["pi"], axis=1)[:, ::-1]
+            if np.min(pi[:, cfg.top_k - 1] - pi[:, cfg.top_k]) < margin:
+                ok = False
+                break
+            x = y
+        if ok:
+            return flat, X, dY
+    raise AssertionError("no seed with clear routing margins")
+
+
+def test_fd_moe_joint_and_per_tensor():
+    cfg = tiny_moe_cfg()
+    flat, X, dY = _moe_inputs_with_margin(cfg)
+    rng = np.random.default_rng(11)
+    fd_check(cfg, flat, X, dY, rng.standard_normal(flat.shape), rng.standard_normal(X.shape))
+    for name, off, shape in synth.layout(cfg):
+        u = np.zeros_like(flat)
+        sz = int(np.prod(shape))
+        u[off:off + sz] = rng.standard_normal(sz)
+        fd_check(cfg, flat, X, dY, u, np.zeros_like(X))
+
+
+def test_softmax_rows_and_causal_zeros():
+    rng = np.random.default_rng(0)
+    q = rng.standard_normal((33, 16)) * 3
+    k = rng.standard_normal((33, 16)) * 3
+    P = O.attention_probs(q, k)
+    assert np.max(np.abs(P.sum(axis=1) - 1.0)) <= 1e-12
+    assert np.all(P[np.triu_indices(33, 1)] == 0.0)
+    assert np.all(P[np.tril_indices(33)] > 0.0)
+
+
+def test_identical_keys_give_causal_prefix_mean():
+    rng = np.random.default_rng(1)
+    b, S, h, hd = 2, 17, 3, 8
+    q = rng.standard_normal((b, S, h, hd))
+    k = np.broadcast_to(rng.standard_normal((b, 1, h, hd)), (b, S, h, hd)).copy()
+    v = rng.standard_normal((b, S, h, hd))
+    o = O.attention_forward(q, k, v)
+    prefix_mean = np.cumsum(v, axis=1) / np.arange(1, S + 1)[None, :, None, None]
+    assert np.max(np.abs(o - prefix_mean)) <= 1e-12
+
+
+def test_identical_values_and_single_position():
+    rng = np.random.default_rng(2)
+    b, S, h, hd = 1, 9, 2, 8
+    q, k = rng.standard_normal((2, b, S, h, hd))
+    v = np.broadcast_to(rng.standard_normal((b, 1, h, hd)), (b, S, h, hd)).copy()
+    o = O.attention_forward(q, k, v)
+    assert np.max(np.abs(o - v)) <= 1e-12
+    q1, k1, v1 = rng.standard_normal((3, b, 1, h, hd))
+    assert np.max(np.abs(O.attention_forward(q1, k1, v1) - v1)) <= 1e-15
+
+
+def test_causality_forward_and_backward():
+    cfg = tiny_cfg()
+    flat, X, dY = random_inputs(cfg, 5)
+    Y, _, _ = grads(cfg, flat, X, dY)
+    p = 5
+    X2 = X.copy()
+    X2[:, p] += 1.0
+    Y2, _, _ = grads(cfg, flat, X2, dY)
+    assert np.array_equal(Y[:, :p], Y2[:, :p])
+    assert not np.allclose(Y[:, p], Y2[:, p])
+    i = 3
+    dY1 = np.zeros_like(dY)
+    dY1[:, i] = dY[:, i]
+    _, dX1, _ = grads(cfg, flat, X, dY1)
+    assert np.all(dX1[:, i + 1:] == 0.0)
+    assert np.any(dX1[:, :i + 1] != 0.0)
+
+
+def test_microbatch_sum_equals_full_batch():
+    cfg = tiny_cfg(micro_batch=1)
+    full = tiny_cfg(micro_batch=3)
+    flat, _, _ = random_inputs(cfg, 9)
+    rng = np.random.default_rng(9)
+    X = rng.standard_normal((3, cfg.seq_len, cfg.d_model))
+    dY = rng.standard_normal(X.shape)
+    Yf, dXf, Gf = grads(full, flat, X, dY)
+    G = np.zeros_like(Gf)
+    for mb in range(3):
+        Ym, dXm, Gm = grads(cfg, flat, X[mb:mb + 1], dY[mb:mb + 1])
+        G += Gm
+        assert np.max(np.abs(Ym - Yf[mb:mb + 1])) <= 1e-12
+        assert np.max(np.abs(dXm - dXf[mb:mb + 1])) <= 1e-12
+    assert np.max(np.abs(G - Gf)) <= 1e-10 * np.max(np.abs(Gf))
+
+
+def test_order_invariance_of_results():
+    cfg = tiny_cfg(micro_batch=1, num_microbatches=4)
+    flat, _, _ = random_inputs(cfg, 4)
+    rng = np.random.default_rng(4)
+    Xs = [rng.standard_normal((1, cfg.seq_len, cfg.d_model)) for _ in range(4)]
+    dYs = [rng.standard_normal((1, cfg.seq_len, cfg.d_model)) for _ in range(4)]
+    a = O.run_order(cfg, flat, Xs, dYs, OO.one_f_one_b(4, 3, 0))
+    b = O.run_order(cfg, flat, Xs, dYs, OO.gpipe(4))
+    assert np.array_equal(a[2], b[2])
+    for i in range(4):
+        assert np.array_equal(a[0][i], b[0][i]) and np.array_equal(a[1][i], b[1][i])
+
+
+# ---------------------------------------------------------------- RMSNorm
+
+def test_rmsnorm_constant_row():
+    d, eps = 32, 1e-5
+    g = np.linspace(0.5, 1.5, d)
+    for c in (-3.0, 0.25, 7.0):
+        n, rstd = O.rmsnorm_forward(np.full((2, d), c), g, eps)
+        assert np.allclose(n, c / np.sqrt(c * c + eps) * g, rtol=1e-14, atol=0)
+
+
+def test_rmsnorm_scale_invariance_and_radial_gradient():
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((5, 24))
+    g = rng.standard_normal(24)
+    n1, _ = O.rmsnorm_forward(x, g, 0.0)
+    n2, _ = O.rmsnorm_forward(3.7 * x, g, 0.0)
+    assert np.max(np.abs(n1 - n2)) <= 1e-13
+    # with eps = 0 the output does not change along x itself: sum_k x_k dx_k = 0
+    _, rstd = O.rmsnorm_forward(x, g, 0.0)
+    dx, _ = O.rmsnorm_backward(rng.standard_normal(x.shape), x, rstd, g)
+    assert np.max(np.abs(np.sum(x * dx, axis=1))) <= 1e-12
+
+
+# ---------------------------------------------------------------- RoPE
+
+def test_rope_rotate_half_convention_on_unit_vectors():
+    S, hd, base = 7, 8, 10000.0
+    cos, sin = O.rope_tables(S, hd, base)
+    for i in range(hd // 2):
+        theta = base ** (-2.0 * i / hd)
+        e = np.zeros((1, S, 1, hd))
+        e[..., i] = 1.0
+        r = O.rope_apply(e, cos, sin)
+        p = np.arange(S)
+        assert np.allclose(r[0, :, 0, i], np.cos(p * theta), atol=1e-7)
+        assert np.allclose(r[0, :, 0, i + hd // 2], np.sin(p * theta), atol=1e-7)
+
+
+def test_rope_identity_at_zero_norms_inverse_and_relative():
+    rng = np.random.default_rng(6)
+    S, hd, h = 12, 16, 2
+    cos, sin = O.rope_tables(S + 5, hd, 10000.0)
+    t = rng.standard_normal((1, S, h, hd))
+    r = O.rope_apply(t, cos[:S], sin[:S])
+    assert np.array_equal(r[:, 0], t[:, 0])
+    half = hd // 2
+    pair = lambda z: z[..., :half] ** 2 + z[..., half:] ** 2
+    assert np.max(np.abs(pair(r) - pair(t))) <= 1e-6  # table is fp32-rounded
+    back = O.rope_apply(r, cos[:S], sin[:S], inverse=True)
+    assert np.max(np.abs(back - t)) <= 1e-6
+    # <R_p q, R_p' k> depends only on p - p': shift both positions by 5
+    q = rng.standard_normal((1, S, 1, hd))
+    k = rng.standard_normal((1, S, 1, hd))
+    s0 = np.einsum("bihd,bjhd->ij", O.rope_apply(q, cos[:S], sin[:S]),
+                   O.rope_apply(k, cos[:S], sin[:S]))
+    s5 = np.einsum("bihd,bjhd->ij", O.rope_apply(q, cos[5:], sin[5:]),
+                   O.rope_apply(k, cos[5:], sin[5:]))
+    assert np.max(np.abs(s0 - s5)) <= 1e-5
+
+
+# ---------------------------------------------------------------- SwiGLU
+
+def test_silu_closed_forms_and_derivative():
+    assert O.silu(np.array(0.0)) == 0.0
+    z = np.linspace(-6, 6, 101)
+    h = 1e-6
+    fd = (O.silu(z + h) - O.silu(z - h)) / (2 * h)
+    s = O.sigmoid(z)
+    assert np.max(np.abs(fd - s * (1 + z * (1 - s)))) <= 1e-8
+    rng = np.random.default_rng(0)
+    n = rng.standard_normal((4, 8))
+    out, gt, u, a = O.swiglu_ffn_forward(n, np.zeros((6, 8)), rng.standard_normal((6, 8)),
+                                         rng.standard_normal((8, 6)))
+    assert np.all(a == 0.0) and np.all(out == 0.0)
+
+
+# ---------------------------------------------------------------- MoE
+
+def test_moe_identical_experts_equal_dense():
+    cfg = tiny_moe_cfg()
+    rng = np.random.default_rng(8)
+    d, fe = cfg.d_model, cfg.d_ff_expert
+    w1, w3, w2 = rng.standard_normal((fe, d)), rng.standard_normal((fe, d)), rng.standard_normal((d, fe))
+    p = {"wr": rng.standard_normal((cfg.n_experts, d))}
+    for e in range(cfg.n_experts):
+        p[f"e{e}.w1"], p[f"e{e}.w3"], p[f"e{e}.w2"] = w1, w3, w2
+    n2 = rng.standard_normal((10, d))
+    out, mc = O.moe_forward(n2, p, cfg)
+    dense, _, _, _ = O.swiglu_ffn_forward(n2, w1, w3, w2)
+    assert np.max(np.abs(out - dense)) <= 1e-12 * np.max(np.abs(dense))
+
+
+def test_moe_zero_router_ties_to_lowest_experts():
+    cfg = tiny_moe_cfg()
+    rng = np.random.default_rng(9)
+    n2 = rng.standard_normal((10, cfg.d_model))
+    _, pi, sel, w = O.moe_route(n2, np.zeros((cfg.n_experts, cfg.d_model)), 2)
+    assert np.all(pi == 1.0 / cfg.n_experts)
+    assert np.all(sel == np.array([0, 1]))
+    assert np.all(w == 0.5)
+
+
+def test_moe_each_token_two_distinct_experts():
+    cfg = tiny_moe_cfg()
+    rng = np.random.default_rng(10)
+    n2 = rng.standard_normal((50, cfg.d_model))
+    _, pi, sel, w = O.moe_route(n2, rng.standard_normal((cfg.n_experts, cfg.d_model)), 2)
+    assert np.all(sel[:, 0] != sel[:, 1])
+    assert np.allclose(w.sum(axis=1), 1.0, atol=1e-15)
+    # the selected experts are the two largest probabilities
+    srt = np.sort(pi, axis=1)
+    assert np.all(pi[np.arange(50), sel[:, 0]] == srt[:, -1])
+    assert np.all(pi[np.arange(50), sel[:, 1]] == srt[:, -2])

@@ -1,0 +1,244 @@
+"""Benchmark: one GPU's share of the pipeline-stage training step.
+
+Workload (default): the 7B-shaped stage — 4 decoder layers, d_model 4096,
+32 heads x 128, SwiGLU FFN 11008, causal sequence 4096, microbatch 1, 16
+microbatches in the 1F1B Order of stage 0 of an 8-stage pipeline, bf16
+compute with fp32 gradient accumulation, then one AdamW step (with the bf16
+cast of the updated weights) over the whole stage bucket. A step is one pass
+of all of it; inputs are resident in HBM before timing starts.
+
+Reported: algorithmic TFLOP/s of the step (GEMMs 2MNK; causal attention
+S(S+1)/2 pairs per head for each of QK^T and PV; backward = 2x forward;
+attention recompute excluded), its fraction of the MI355X bf16 dense peak,
+the roofline of the dominant kernel measured with HIP events, the AdamW
+shard step on a 1.6e9-element shard in GB/s, and the CPU oracle timed on a
+bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 2516.6   # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+METRIC = ("stage fwd+bwd TFLOP/s + MFMA util (7B-shaped 4-layer stage); Adam shard GB/s")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def stage_flops_per_mb(cfg) -> float:
+    T, d, f, H, hd, S, b = (cfg.tokens, cfg.d_model, cfg.d_ff, cfg.n_heads, cfg.head_dim,
+                            cfg.seq_len, cfg.micro_batch)
+    gemm = 2.0 * T * d * (3 * d + d + 2 * f + f)
+    attn = 4.0 * (S * (S + 1) / 2) * hd * H * b
+    return 3.0 * cfg.n_layers * (gemm + attn)
+
+
+def desc_of(cfg, lc):
+    return lc.make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
+                        cfg.seq_len, cfg.micro_batch, cfg.bf16, rms_eps=cfg.rms_eps,
+                        rope_base=cfg.rope_base)
+
+
+def time_launches(torch, stream, fns, reps):
+    """Per-launch HIP event timing; returns (total ms, launches)."""
+    total, count = 0.0, 0
+    for _ in range(reps):
+        for fn in fns:
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            fn()
+            e.record(stream)
+            e.synchronize()
+            total += s.elapsed_time(e)
+            count += 1
+    return total, count
+
+
+def wgrad_roofline(torch, lc, cfg, stream):
+    """The weight-gradient GEMM (both operands token-major, fp32 accumulate
+    into the bucket) at the four shapes of one layer's backward: the kernel
+    with the largest share of the step's FLOPs. Returns the roofline dict."""
+    T, d, f = cfg.tokens, cfg.d_model, cfg.d_ff
+    dev = "cuda"
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    big = max(3 * d, 2 * f)
+    dy = torch.randn((T, big), generator=g, device=dev).to(torch.bfloat16)
+    x = torch.randn((T, max(d, f)), generator=g, device=dev).to(torch.bfloat16)
+    C = torch.zeros(big * max(d, f), dtype=torch.float32, device=dev)
+    shapes = [(3 * d, d), (d, d), (2 * f, d), (d, f)]  # (rows of dW, cols of dW)
+    fns, flops = [], 0.0
+    for (M, N) in shapes:
+        def fn(M=M, N=N):
+            lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ACCUM_F32, M, N, T, dy, big, 0, x, max(d, f), 0, C,
+                       N, stream=stream)
+        fns.append(fn)
+        flops += 2.0 * M * N * T
+    for fn in fns:  # warm
+        fn()
+    torch.cuda.synchronize()
+    ms, n = time_launches(torch, stream, fns, 5)
+    avg_ms = ms / n
+    avg_flops = flops / len(shapes)
+    achieved = avg_flops / (avg_ms * 1e-3) / 1e12
+    return {"bound": "mfma", "kernel": "gemm_bf16_kernel<false,false,LC_EPI_ACCUM_F32>",
+            "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+            "avg_launch_ms": round(avg_ms, 4), "flop_per_launch": avg_flops}
+
+
+def adam_shard(torch, lc, shard, stream, reps=10):
+    n = shard.n
+    dev = "cuda"
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    p = torch.randn(n, generator=g, device=dev).mul_(shard.p_std)
+    m = torch.zeros_like(p)
+    v = torch.zeros_like(p)
+    gr = torch.randn(n, generator=g, device=dev).mul_(shard.g_std).to(torch.bfloat16)
+    out = torch.empty(n, dtype=torch.bfloat16, device=dev)
+
+    def step(t):
+        lc.shard_adam_step(p, m, v, gr, lc.LC_BF16, out, n, shard.lr, shard.beta1, shard.beta2,
+                           shard.eps, shard.weight_decay, t, stream=stream)
+    step(1)
+    step(2)
+    torch.cuda.synchronize()
+    ms, cnt = time_launches(torch, stream, [lambda i=i: step(3 + i) for i in range(reps)], 1)
+    avg = ms / cnt
+    gbs = 28.0 * n / (avg * 1e-3) / 1e9
+    del p, m, v, gr, out
+    torch.cuda.empty_cache()
+    return {"workload": shard.name, "n": n, "bytes_per_elem": 28, "ms": round(avg, 3),
+            "value": round(gbs, 1), "unit": "GB/s", "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def cpu_baseline(cfg, tokens: int):
+    """The oracle, as it stands, on one layer of the workload truncated to
+    `tokens` positions of one sequence: Chunk F then Chunk B."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import synth
+    from oracle import stage as OS
+    sample = synth.scaled(cfg, n_layers=1, seq_len=tokens, micro_batch=1, bf16=False)
+    flat = synth.stage_params(sample, 0)
+    X = synth.activation(sample, 0, 0, "x")
+    dY = synth.activation(sample, 0, 0, "dy")
+    layers = OS.layer_params(sample, flat)
+    t0 = time.perf_counter()
+    Y, caches = OS.stage_forward(sample, layers, X)
+    dX, G = OS.stage_backward(sample, layers, caches, dY)
+    dt = time.perf_counter() - t0
+    flops = stage_flops_per_mb(sample)
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                   if i.get("internal_api") == "openblas"] or [1])
+    return {"value": round(flops / dt / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"1 of {cfg.n_layers} layers, first {tokens} of {cfg.seq_len} tokens of one "
+                      f"microbatch, Chunk F + Chunk B in float64 numpy ({flops / 1e12:.3f} TFLOP)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-adam-shard", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=1024)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's share of the stage; --gpus {args.gpus} is not "
+              "supported (this build runs on a single GPU).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2606_11169_amd import libchunk as lc
+    from paper_2606_11169_amd.runner import random_stage, require_gpu
+
+    require_gpu()
+    cfg = synth.STAGE_7B
+    M = cfg.num_microbatches
+    stream = torch.cuda.current_stream()
+    order = lc.lc_order_1f1b(M, cfg.pp_size, cfg.pp_rank)
+    _, peak = lc.lc_order_validate(order, M, M)
+    log(f"[bench] {cfg.name}: {M} microbatches, 1F1B(P={cfg.pp_size}, s={cfg.pp_rank}), "
+        f"{peak} in flight")
+    r = random_stage(desc_of(cfg, lc), peak, seed=0, stream=stream)
+    r.alloc_random_microbatches(M, seed=1)
+    log(f"[bench] params {r.n_params}, workspace {r.ws_bytes / 2**30:.1f} GiB")
+
+    def step():
+        r.zero_grad()
+        r.run_order(order)
+        r.adam_step(cfg.lr, cfg.beta1, cfg.beta2, cfg.adam_eps, cfg.weight_decay)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    flops = stage_flops_per_mb(cfg) * M
+    tflops = flops / (ms * 1e-3) / 1e12
+    log(f"[bench] {ms:.1f} ms/step, {tflops:.1f} TFLOP/s ({100 * tflops / BF16_PEAK_TFLOPS:.1f}% of bf16 peak)")
+    finite = bool(torch.isfinite(r.Y[M - 1].float()).all().item())
+    r.close()
+    del r
+    torch.cuda.empty_cache()
+
+    roof = wgrad_roofline(torch, lc, cfg, stream)
+    log(f"[bench] roofline {roof}")
+    adam = None if args.no_adam_shard else adam_shard(torch, lc, synth.ADAM_1P6B, stream)
+    if adam:
+        log(f"[bench] adam shard {adam}")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, args.cpu_tokens)
+        log(f"[bench] cpu baseline {cpu}")
+
+    out = {
+        "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 2),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
+                   "heads": cfg.n_heads, "head_dim": cfg.head_dim, "d_ff": cfg.d_ff,
+                   "seq_len": cfg.seq_len, "micro_batch": cfg.micro_batch,
+                   "num_microbatches": M, "order": f"1F1B(P={cfg.pp_size},s={cfg.pp_rank})",
+                   "optimizer": "AdamW over the stage bucket + bf16 cast",
+                   "parallelism": "one GPU's share (no collectives)",
+                   "algorithmic_tflop_per_step": round(flops / 1e12, 2)},
+        "mfma_util": round(tflops / BF16_PEAK_TFLOPS, 4),
+        "roofline": roof,
+        "adam_shard": adam,
+        "cpu_baseline": cpu,
+        "outputs_finite": finite,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,313 @@
+// Host-only core of libchunk (see host_core.hpp). Built with the host C++
+// compiler; makes no HIP call.
+#include "host_core.hpp"
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+namespace lc {
+
+static thread_local char g_err[512] = "";
+
+lc_status fail(lc_status st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+static inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+lc_status validate_desc(const lc_stage_desc *d) {
+  if (!d) return fail(LC_ERR_INVALID_ARG, "null stage descriptor");
+  if (d->n_layers <= 0 || d->d_model <= 0 || d->n_heads <= 0 || d->head_dim <= 0 ||
+      d->seq_len <= 0 || d->micro_batch <= 0)
+    return fail(LC_ERR_INVALID_ARG, "stage dimensions must be positive");
+  if ((int64_t)d->n_heads * d->head_dim != d->d_model)
+    return fail(LC_ERR_INVALID_ARG, "d_model (%d) != n_heads (%d) * head_dim (%d)", d->d_model,
+                d->n_heads, d->head_dim);
+  if (d->head_dim % 2 != 0) return fail(LC_ERR_INVALID_ARG, "head_dim must be even");
+  if (d->causal != 1) return fail(LC_ERR_UNSUPPORTED, "only causal attention is implemented");
+  if (!(d->rms_eps >= 0.0f) || !(d->rope_base > 0.0f))
+    return fail(LC_ERR_INVALID_ARG, "rms_eps must be >= 0 and rope_base > 0");
+  if (d->compute_dtype != LC_FP32 && d->compute_dtype != LC_BF16)
+    return fail(LC_ERR_INVALID_ARG, "compute_dtype must be LC_FP32 or LC_BF16");
+  if (d->n_experts < 0) return fail(LC_ERR_INVALID_ARG, "n_experts must be >= 0");
+  if (d->n_experts == 0) {
+    if (d->d_ff <= 0) return fail(LC_ERR_INVALID_ARG, "d_ff must be positive");
+  } else {
+    if (d->top_k != 2) return fail(LC_ERR_UNSUPPORTED, "MoE stages route to top_k == 2 experts");
+    if (d->n_experts < 2) return fail(LC_ERR_INVALID_ARG, "MoE needs at least 2 experts");
+    if (d->d_ff_expert <= 0) return fail(LC_ERR_INVALID_ARG, "d_ff_expert must be positive");
+  }
+  // limits of the kernels in this build
+  if (d->compute_dtype == LC_BF16) {
+    if (d->head_dim != 128)
+      return fail(LC_ERR_UNSUPPORTED, "bf16 attention kernels need head_dim == 128");
+    if (d->d_model % 64 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs d_model % 64 == 0");
+    int64_t f = d->n_experts ? d->d_ff_expert : d->d_ff;
+    if (f % 64 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs the FFN width % 64 == 0");
+    if (d->seq_len % 128 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs seq_len % 128 == 0");
+  } else {
+    if (d->head_dim > 128) return fail(LC_ERR_UNSUPPORTED, "fp32 attention needs head_dim <= 128");
+    if (d->d_model % 4 != 0) return fail(LC_ERR_UNSUPPORTED, "fp32 needs d_model % 4 == 0");
+  }
+  if (d->n_experts > 64) return fail(LC_ERR_UNSUPPORTED, "at most 64 experts");
+  return LC_OK;
+}
+
+ParamPlan param_plan(const lc_stage_desc &d) {
+  ParamPlan p{};
+  const size_t D = (size_t)d.d_model;
+  size_t off = 0;
+  p.wq = off; off += D * D;
+  p.wk = off; off += D * D;
+  p.wv = off; off += D * D;
+  p.wo = off; off += D * D;
+  p.g1 = off; off += D;
+  if (d.n_experts == 0) {
+    const size_t F = (size_t)d.d_ff;
+    p.w1 = off; off += F * D;
+    p.w3 = off; off += F * D;
+    p.w2 = off; off += D * F;
+  } else {
+    const size_t FE = (size_t)d.d_ff_expert, E = (size_t)d.n_experts;
+    p.wr = off; off += E * D;
+    p.expert0 = off;
+    p.expert_stride = 3 * FE * D;
+    off += E * p.expert_stride;
+  }
+  p.g2 = off; off += D;
+  p.per_layer = off;
+  p.total = off * (size_t)d.n_layers;
+  return p;
+}
+
+lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *out) {
+  lc_status st = validate_desc(&d);
+  if (st != LC_OK) return st;
+  if (max_in_flight <= 0) return fail(LC_ERR_INVALID_ARG, "max_in_flight must be positive");
+  StagePlan p{};
+  const size_t es = d.compute_dtype == LC_BF16 ? 2 : 4;
+  const int64_t T = (int64_t)d.micro_batch * d.seq_len;
+  const size_t D = (size_t)d.d_model, H = (size_t)d.n_heads;
+  const bool moe = d.n_experts > 0;
+  const size_t F = moe ? (size_t)d.d_ff_expert : (size_t)d.d_ff;
+  const size_t R = moe ? 2 * (size_t)T : (size_t)T;  // FFN rows (routed rows for MoE)
+  p.elem = es;
+  p.T = T;
+  size_t off = 0;
+  const size_t half = (size_t)d.head_dim / 2;
+  p.rope_cos = off; off = align256(off + (size_t)d.seq_len * half * 4);
+  p.rope_sin = off; off = align256(off + (size_t)d.seq_len * half * 4);
+
+  // one layer block of the stash
+  size_t lo = 0;
+  auto take = [&](size_t bytes) { size_t r = lo; lo = align256(lo + bytes); return r; };
+  p.xin = take((size_t)T * D * es);
+  p.rstd1 = take((size_t)T * 4);
+  p.n1 = take((size_t)T * D * es);
+  p.qkv = take((size_t)T * 3 * D * es);
+  p.o = take((size_t)T * D * es);
+  p.lse = take((size_t)T * H * 4);
+  p.h = take((size_t)T * D * es);
+  p.rstd2 = take((size_t)T * 4);
+  p.n2 = take((size_t)T * D * es);
+  p.gate = take(R * F * es);
+  p.up = take(R * F * es);
+  p.act = take(R * F * es);
+  if (moe) {
+    const size_t E = (size_t)d.n_experts;
+    p.moe_sel = take((size_t)T * 2 * 4);
+    p.moe_w = take((size_t)T * 2 * 4);
+    p.moe_perm = take(R * 4);
+    p.moe_rowpos = take((size_t)T * 2 * 4);
+    p.moe_off = take((E + 1) * 4 + 256);
+    p.moe_xp = take(R * D * es);
+    p.moe_eo = take(R * D * es);
+  }
+  p.layer_bytes = lo;
+  p.slot_bytes = lo * (size_t)d.n_layers;
+  p.slot0 = off;
+  off = align256(off + p.slot_bytes * (size_t)max_in_flight);
+
+  auto stake = [&](size_t bytes) { size_t r = off; off = align256(off + bytes); return r; };
+  p.s_dy0 = stake((size_t)T * D * es);
+  p.s_dy1 = stake((size_t)T * D * es);
+  p.s_da = stake(R * 2 * F * es);
+  p.s_dn = stake((size_t)T * D * es);
+  p.s_do = stake((size_t)T * D * es);
+  p.s_dqkv = stake((size_t)T * 3 * D * es);
+  p.s_dh = stake((size_t)T * D * es);
+  p.s_attn_bytes = attn_scratch_size(d.micro_batch, d.seq_len, d.n_heads);
+  p.s_attn = stake(p.s_attn_bytes);
+  p.s_norm_bytes = rmsnorm_scratch_size(T, d.d_model);
+  p.s_norm = stake(p.s_norm_bytes);
+  if (moe) {
+    // gradient of the routed rows' expert outputs and of the gate weights
+    p.s_moe = stake(R * D * es + (size_t)T * 2 * 4 * 2 + 4096);
+  }
+  p.total = off;
+  *out = p;
+  return LC_OK;
+}
+
+size_t rmsnorm_scratch_size(int64_t T, int64_t d) {
+  const int64_t blocks = (T + kNormRowsPerBlock - 1) / kNormRowsPerBlock;
+  return (size_t)(blocks * d) * sizeof(float);
+}
+
+size_t attn_scratch_size(int64_t B, int64_t S, int64_t H) {
+  return (size_t)(B * S * H) * sizeof(float);
+}
+
+}  // namespace lc
+
+using namespace lc;
+
+extern "C" {
+
+const char *lc_last_error(void) { return g_err; }
+
+lc_status lc_param_count(const lc_stage_desc *desc, size_t *n_elems) {
+  lc_status st = validate_desc(desc);
+  if (st != LC_OK) return st;
+  if (!n_elems) return fail(LC_ERR_INVALID_ARG, "null output pointer");
+  *n_elems = param_plan(*desc).total;
+  return LC_OK;
+}
+
+lc_status lc_param_offset(const lc_stage_desc *desc, int32_t layer, int32_t tensor_id,
+                          int32_t expert, size_t *offset, int64_t shape[2]) {
+  lc_status st = validate_desc(desc);
+  if (st != LC_OK) return st;
+  if (!offset || !shape) return fail(LC_ERR_INVALID_ARG, "null output pointer");
+  if (layer < 0 || layer >= desc->n_layers) return fail(LC_ERR_INVALID_ARG, "layer out of range");
+  const ParamPlan p = param_plan(*desc);
+  const int64_t D = desc->d_model;
+  const bool moe = desc->n_experts > 0;
+  size_t base = (size_t)layer * p.per_layer, o = 0;
+  int64_t r = 0, c = 1;
+  if (tensor_id != LC_T_W1 && tensor_id != LC_T_W3 && tensor_id != LC_T_W2 && expert != 0)
+    return fail(LC_ERR_INVALID_ARG, "expert index only applies to W1/W3/W2");
+  switch (tensor_id) {
+    case LC_T_WQ: o = p.wq; r = D; c = D; break;
+    case LC_T_WK: o = p.wk; r = D; c = D; break;
+    case LC_T_WV: o = p.wv; r = D; c = D; break;
+    case LC_T_WO: o = p.wo; r = D; c = D; break;
+    case LC_T_G1: o = p.g1; r = D; break;
+    case LC_T_G2: o = p.g2; r = D; break;
+    case LC_T_WR:
+      if (!moe) return fail(LC_ERR_INVALID_ARG, "dense stage has no router");
+      o = p.wr; r = desc->n_experts; c = D; break;
+    case LC_T_W1: case LC_T_W3: case LC_T_W2: {
+      if (!moe) {
+        if (expert != 0) return fail(LC_ERR_INVALID_ARG, "dense stage has no experts");
+        const int64_t F = desc->d_ff;
+        if (tensor_id == LC_T_W1) { o = p.w1; r = F; c = D; }
+        if (tensor_id == LC_T_W3) { o = p.w3; r = F; c = D; }
+        if (tensor_id == LC_T_W2) { o = p.w2; r = D; c = F; }
+      } else {
+        if (expert < 0 || expert >= desc->n_experts)
+          return fail(LC_ERR_INVALID_ARG, "expert out of range");
+        const int64_t FE = desc->d_ff_expert;
+        size_t e0 = p.expert0 + (size_t)expert * p.expert_stride;
+        if (tensor_id == LC_T_W1) { o = e0; r = FE; c = D; }
+        if (tensor_id == LC_T_W3) { o = e0 + (size_t)(FE * D); r = FE; c = D; }
+        if (tensor_id == LC_T_W2) { o = e0 + (size_t)(2 * FE * D); r = D; c = FE; }
+      }
+      break;
+    }
+    default: return fail(LC_ERR_INVALID_ARG, "unknown tensor id %d", tensor_id);
+  }
+  *offset = base + o;
+  shape[0] = r;
+  shape[1] = c;
+  return LC_OK;
+}
+
+lc_status lc_order_1f1b(int32_t M, int32_t P, int32_t s, lc_order_entry *out, int32_t capacity,
+                        int32_t *n) {
+  if (M <= 0 || P <= 0 || s < 0 || s >= P)
+    return fail(LC_ERR_INVALID_ARG, "need M > 0, P > 0 and 0 <= s < P");
+  if (!out || !n) return fail(LC_ERR_INVALID_ARG, "null output pointer");
+  if (capacity < 2 * M) return fail(LC_ERR_INVALID_ARG, "capacity %d < 2M = %d", capacity, 2 * M);
+  const int32_t W = (P - s - 1) < M ? (P - s - 1) : M;
+  int32_t k = 0;
+  for (int32_t i = 0; i < W; ++i) out[k++] = lc_order_entry{i, LC_PASS_F};
+  for (int32_t i = 0; i < M - W; ++i) {
+    out[k++] = lc_order_entry{W + i, LC_PASS_F};
+    out[k++] = lc_order_entry{i, LC_PASS_B};
+  }
+  for (int32_t i = M - W; i < M; ++i) out[k++] = lc_order_entry{i, LC_PASS_B};
+  *n = k;
+  return LC_OK;
+}
+
+lc_status lc_order_validate(const lc_order *order, int32_t max_in_flight, int32_t *peak) {
+  if (peak) *peak = 0;
+  if (!order) return fail(LC_ERR_INVALID_ARG, "null order");
+  if (max_in_flight <= 0) return fail(LC_ERR_INVALID_ARG, "max_in_flight must be positive");
+  const int32_t M = order->num_microbatches;
+  if (M <= 0) return fail(LC_ERR_BAD_ORDER, "num_microbatches must be positive");
+  if (order->n_entries != 2 * M)
+    return fail(LC_ERR_BAD_ORDER, "an Order over %d microbatches has %d entries, not 2M", M,
+                order->n_entries);
+  if (!order->entries) return fail(LC_ERR_INVALID_ARG, "null entries");
+  std::vector<uint8_t> seen_f((size_t)M, 0), seen_b((size_t)M, 0);
+  int32_t last_f = -1, last_b = -1, live = 0, pk = 0;
+  for (int32_t i = 0; i < order->n_entries; ++i) {
+    const lc_order_entry e = order->entries[i];
+    if (e.mb < 0 || e.mb >= M)
+      return fail(LC_ERR_BAD_ORDER, "entry %d: microbatch %d out of range", i, e.mb);
+    if (e.pass == LC_PASS_F) {
+      if (seen_f[e.mb]) return fail(LC_ERR_BAD_ORDER, "entry %d: F%d appears twice", i, e.mb);
+      if (e.mb <= last_f)
+        return fail(LC_ERR_BAD_ORDER, "entry %d: F%d after F%d (forwards must be in order)", i,
+                    e.mb, last_f);
+      seen_f[e.mb] = 1;
+      last_f = e.mb;
+      ++live;
+      if (live > pk) pk = live;
+      if (peak) *peak = pk;
+      if (live > max_in_flight)
+        return fail(LC_ERR_STASH_FULL, "entry %d: %d microbatches in flight > %d slots", i, live,
+                    max_in_flight);
+    } else if (e.pass == LC_PASS_B) {
+      if (seen_b[e.mb]) return fail(LC_ERR_BAD_ORDER, "entry %d: B%d appears twice", i, e.mb);
+      if (!seen_f[e.mb]) return fail(LC_ERR_BAD_ORDER, "entry %d: B%d before F%d", i, e.mb, e.mb);
+      if (e.mb <= last_b)
+        return fail(LC_ERR_BAD_ORDER, "entry %d: B%d after B%d (backwards must be in order)", i,
+                    e.mb, last_b);
+      seen_b[e.mb] = 1;
+      last_b = e.mb;
+      --live;
+    } else {
+      return fail(LC_ERR_BAD_ORDER, "entry %d: unknown pass %d", i, e.pass);
+    }
+  }
+  if (peak) *peak = pk;
+  return LC_OK;
+}
+
+lc_status lc_workspace_bytes(const lc_stage_desc *desc, int32_t max_in_flight, size_t *bytes) {
+  if (!bytes) return fail(LC_ERR_INVALID_ARG, "null output pointer");
+  StagePlan p;
+  lc_status st = validate_desc(desc);
+  if (st != LC_OK) return st;
+  st = stage_plan(*desc, max_in_flight, &p);
+  if (st != LC_OK) return st;
+  *bytes = p.total;
+  return LC_OK;
+}
+
+size_t lc_rmsnorm_scratch_bytes(int64_t T, int64_t d) { return rmsnorm_scratch_size(T, d); }
+size_t lc_attention_scratch_bytes(int32_t B, int32_t S, int32_t H) {
+  return attn_scratch_size(B, S, H);
+}
+
+}  // extern "C"

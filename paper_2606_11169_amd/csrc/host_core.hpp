@@ -1,0 +1,61 @@
+// Host-only core of libchunk: descriptor validation, the canonical parameter
+// layout, Order generation/validation and the workspace plan. No HIP calls,
+// so it builds with the plain host compiler and is testable without a GPU.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "libchunk.h"
+
+namespace lc {
+
+lc_status fail(lc_status st, const char *fmt, ...);
+
+// Rows per block of the RMSNorm backward's gain-gradient partial sums.
+constexpr int kNormRowsPerBlock = 32;
+size_t rmsnorm_scratch_size(int64_t T, int64_t d);
+size_t attn_scratch_size(int64_t B, int64_t S, int64_t H);
+
+// Validates a stage descriptor (shapes, dtype, limits of this build).
+lc_status validate_desc(const lc_stage_desc *d);
+
+// Per-layer sizes of the canonical flat bucket.
+struct ParamPlan {
+  size_t per_layer;                 // elements per layer
+  size_t wq, wk, wv, wo, g1;        // offsets inside a layer
+  size_t w1, w3, w2;                // dense FFN
+  size_t wr, expert0, expert_stride;  // MoE: router, first expert's W1, stride per expert
+  size_t g2;
+  size_t total;
+};
+ParamPlan param_plan(const lc_stage_desc &d);
+
+// Where every stashed activation and scratch buffer lives in the caller's
+// workspace. Offsets are bytes from the workspace base, 256-byte aligned.
+struct StagePlan {
+  size_t elem;          // bytes per activation element (2 or 4)
+  int64_t T;            // tokens per microbatch
+  // RoPE table: cos then sin, fp32 [seq_len, head_dim/2]
+  size_t rope_cos, rope_sin;
+  // stash: max_in_flight slots of n_layers layer blocks
+  size_t slot0, slot_bytes, layer_bytes;
+  // offsets inside one layer block
+  size_t xin, rstd1, n1, qkv, o, lse, h, rstd2, n2, gate, up, act;
+  // MoE per-layer extras (0 when dense)
+  size_t moe_sel, moe_w, moe_perm, moe_rowpos, moe_off, moe_xp, moe_eo;
+  // backward scratch (one set, reused by every microbatch)
+  size_t s_dy0, s_dy1;  // residual-stream gradient ping-pong [T, d]
+  size_t s_da;          // dgate|dup [T, 2f] (or MoE rows [2T, 2fe])
+  size_t s_dn;          // [T, d] gradient at a norm output
+  size_t s_do;          // [T, d] gradient at attention output
+  size_t s_dqkv;        // [T, 3d]
+  size_t s_dh;          // [T, d]
+  size_t s_attn, s_attn_bytes;  // attention backward scratch
+  size_t s_norm, s_norm_bytes;  // RMSNorm backward scratch
+  size_t s_moe;         // MoE backward extras
+  size_t total;
+};
+lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *out);
+
+}  // namespace lc

@@ -1,0 +1,371 @@
+// Stage composer: Chunk F / Chunk B of a decoder pipeline stage as a sequence
+// of kernel launches on the caller's stream, the activation stash, and the
+// Order runner.
+//
+// Piper's worker runs the tasks of its sub-DAG in order on their streams,
+// keeps a forward's outputs in local storage until the last consumer (the
+// matching backward) has been scheduled, then frees them (Piper Section
+// 4.3.2, scheduling loop and "Memory management"). Here one stage runs on one
+// stream, so stream order alone makes reuse of a freed stash slot safe: a slot
+// is taken by chunk_forward(mb) and returned by chunk_backward(mb) as soon as
+// its launches are enqueued. Gradients of every backward are added into the
+// bucket's flat fp32 buffer (Section 4.3.2; accumulated across microbatches,
+// Section 6.2).
+#include "common.hpp"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+struct lc_stage {
+  lc_stage_desc d;
+  lc::StagePlan plan;
+  lc::ParamPlan pp;
+  char *ws;
+  int32_t slots;
+  std::vector<int32_t> owner;      // microbatch stashed in each slot, -1 if free
+  std::vector<const void *> xin0;  // the caller's X of that microbatch
+  std::vector<float> rope_host;    // cos table then sin table (fp32)
+};
+
+namespace lc {
+
+lc_status hip_fail(hipError_t e, const char *what) {
+  return fail(LC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+namespace {
+
+struct LayerBufs {
+  char *base;
+  const StagePlan *p;
+  void *at(size_t off) const { return base + off; }
+};
+
+struct W {  // weight pointers of one layer (compute dtype) and grad pointers (fp32)
+  const char *w;
+  float *g;
+  size_t es;
+  const void *wp(size_t off) const { return w + off * es; }
+  float *gp(size_t off) const { return g + off; }
+};
+
+lc_gemm_args gemm_base(int dtype, int epi, int64_t M, int64_t N, int64_t K) {
+  lc_gemm_args a;
+  memset(&a, 0, sizeof a);
+  a.dtype = dtype;
+  a.epilogue = epi;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  return a;
+}
+
+}  // namespace
+
+static LayerBufs layer_bufs(lc_stage *st, int slot, int l) {
+  LayerBufs b;
+  b.base = st->ws + st->plan.slot0 + (size_t)slot * st->plan.slot_bytes +
+           (size_t)l * st->plan.layer_bytes;
+  b.p = &st->plan;
+  return b;
+}
+
+static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const void *x, void *y,
+                                int slot, hipStream_t s) {
+  const lc_stage_desc &d = st->d;
+  const StagePlan &P = st->plan;
+  const ParamPlan &pp = st->pp;
+  const int dt = d.compute_dtype;
+  const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
+  const float *rs = reinterpret_cast<const float *>(st->ws + P.rope_sin);
+  for (int l = 0; l < d.n_layers; ++l) {
+    const LayerBufs L = layer_bufs(st, slot, l);
+    const W w{static_cast<const char *>(pb->w) + (size_t)l * pp.per_layer * P.elem, nullptr, P.elem};
+    const void *xin = l == 0 ? x : L.at(P.xin);
+    void *out = l == d.n_layers - 1 ? y : layer_bufs(st, slot, l + 1).at(P.xin);
+    // n1 = RMSNorm(x; g1)
+    LC_TRY(rmsnorm_fwd_launch(dt, T, D, xin, w.wp(pp.g1), d.rms_eps, L.at(P.n1),
+                              static_cast<float *>(L.at(P.rstd1)), s));
+    // [q|k|v] = n1 [Wq;Wk;Wv]^T, RoPE on q and k
+    lc_gemm_args a = gemm_base(dt, LC_EPI_ROPE, T, 3 * D, D);
+    a.A = L.at(P.n1); a.lda = D; a.a_kmajor = 1;
+    a.B = w.wp(pp.wq); a.ldb = D; a.b_kmajor = 1;
+    a.C = L.at(P.qkv); a.ldc = 3 * D;
+    a.rope_cos = rc; a.rope_sin = rs; a.rope_seq = d.seq_len; a.rope_cols = (int)(2 * D);
+    a.head_dim = d.head_dim;
+    LC_TRY(gemm_launch(a, s));
+    // o = causal attention
+    char *qkv = static_cast<char *>(L.at(P.qkv));
+    LC_TRY(attn_fwd_launch(dt, d.micro_batch, d.seq_len, d.n_heads, d.head_dim, qkv,
+                           qkv + D * P.elem, qkv + 2 * D * P.elem, 3 * D, L.at(P.o), D,
+                           static_cast<float *>(L.at(P.lse)), s));
+    // h = x + o Wo^T
+    a = gemm_base(dt, LC_EPI_RESIDUAL, T, D, D);
+    a.A = L.at(P.o); a.lda = D; a.a_kmajor = 1;
+    a.B = w.wp(pp.wo); a.ldb = D; a.b_kmajor = 1;
+    a.C = L.at(P.h); a.ldc = D;
+    a.R = xin; a.ldr = D;
+    LC_TRY(gemm_launch(a, s));
+    // n2 = RMSNorm(h; g2)
+    LC_TRY(rmsnorm_fwd_launch(dt, T, D, L.at(P.h), w.wp(pp.g2), d.rms_eps, L.at(P.n2),
+                              static_cast<float *>(L.at(P.rstd2)), s));
+    if (d.n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
+    // gate, up = n2 W1^T, n2 W3^T; act = silu(gate) * up
+    a = gemm_base(dt, LC_EPI_SWIGLU, T, F, D);
+    a.A = L.at(P.n2); a.lda = D; a.a_kmajor = 1;
+    a.B = w.wp(pp.w1); a.ldb = D; a.b_kmajor = 1;
+    a.C = L.at(P.act); a.ldc = F;
+    a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = F;
+    LC_TRY(gemm_launch(a, s));
+    // y = h + act W2^T
+    a = gemm_base(dt, LC_EPI_RESIDUAL, T, D, F);
+    a.A = L.at(P.act); a.lda = F; a.a_kmajor = 1;
+    a.B = w.wp(pp.w2); a.ldb = F; a.b_kmajor = 1;
+    a.C = out; a.ldc = D;
+    a.R = L.at(P.h); a.ldr = D;
+    LC_TRY(gemm_launch(a, s));
+  }
+  return LC_OK;
+}
+
+static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const void *x0,
+                                 const void *dy_in, void *dx_out, int slot, hipStream_t s) {
+  const lc_stage_desc &d = st->d;
+  const StagePlan &P = st->plan;
+  const ParamPlan &pp = st->pp;
+  const int dt = d.compute_dtype;
+  const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
+  const float *rs = reinterpret_cast<const float *>(st->ws + P.rope_sin);
+  char *ws = st->ws;
+  const void *dy = dy_in;
+  for (int l = d.n_layers - 1; l >= 0; --l) {
+    const LayerBufs L = layer_bufs(st, slot, l);
+    const size_t lw = (size_t)l * pp.per_layer;
+    const W w{static_cast<const char *>(pb->w) + lw * P.elem, pb->grad + lw, P.elem};
+    const void *xin = l == 0 ? x0 : L.at(P.xin);
+    void *dx = l == 0 ? dx_out : ws + ((d.n_layers - 1 - l) % 2 == 0 ? P.s_dy0 : P.s_dy1);
+    void *da = ws + P.s_da, *dn = ws + P.s_dn, *dh = ws + P.s_dh, *dO = ws + P.s_do;
+    char *dqkv = ws + P.s_dqkv;
+    if (d.n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
+    // [dgate | dup] = SwiGLU'(dy W2)
+    lc_gemm_args a = gemm_base(dt, LC_EPI_SWIGLU_BWD, T, F, D);
+    a.A = dy; a.lda = D; a.a_kmajor = 1;
+    a.B = w.wp(pp.w2); a.ldb = F; a.b_kmajor = 0;
+    a.C = da; a.ldc = 2 * F;
+    a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = F;
+    LC_TRY(gemm_launch(a, s));
+    // G[W2] += dy^T act
+    a = gemm_base(dt, LC_EPI_ACCUM_F32, D, F, T);
+    a.A = dy; a.lda = D; a.a_kmajor = 0;
+    a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
+    a.C = w.gp(pp.w2); a.ldc = F;
+    LC_TRY(gemm_launch(a, s));
+    // dn2 = [dgate | dup] [W1; W3]
+    a = gemm_base(dt, LC_EPI_STORE, T, D, 2 * F);
+    a.A = da; a.lda = 2 * F; a.a_kmajor = 1;
+    a.B = w.wp(pp.w1); a.ldb = D; a.b_kmajor = 0;
+    a.C = dn; a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    // G[W1; W3] += [dgate | dup]^T n2
+    a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * F, D, T);
+    a.A = da; a.lda = 2 * F; a.a_kmajor = 0;
+    a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
+    a.C = w.gp(pp.w1); a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    // dh = dy + RMSNorm2'(dn2); G[g2] += ...
+    LC_TRY(rmsnorm_bwd_launch(dt, T, D, dn, L.at(P.h), static_cast<const float *>(L.at(P.rstd2)),
+                              w.wp(pp.g2), dy, dh, w.gp(pp.g2), ws + P.s_norm, P.s_norm_bytes, s));
+    // do = dh Wo
+    a = gemm_base(dt, LC_EPI_STORE, T, D, D);
+    a.A = dh; a.lda = D; a.a_kmajor = 1;
+    a.B = w.wp(pp.wo); a.ldb = D; a.b_kmajor = 0;
+    a.C = dO; a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    // G[Wo] += dh^T o
+    a = gemm_base(dt, LC_EPI_ACCUM_F32, D, D, T);
+    a.A = dh; a.lda = D; a.a_kmajor = 0;
+    a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
+    a.C = w.gp(pp.wo); a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    // dq, dk, dv (dq, dk rotated back)
+    char *qkv = static_cast<char *>(L.at(P.qkv));
+    LC_TRY(attn_bwd_launch(dt, d.micro_batch, d.seq_len, d.n_heads, d.head_dim, qkv,
+                           qkv + D * P.elem, qkv + 2 * D * P.elem, 3 * D, L.at(P.o), dO, D,
+                           static_cast<const float *>(L.at(P.lse)), dqkv, dqkv + D * P.elem,
+                           dqkv + 2 * D * P.elem, 3 * D, rc, rs, ws + P.s_attn, P.s_attn_bytes, s));
+    // dn1 = [dq|dk|dv] [Wq;Wk;Wv]
+    a = gemm_base(dt, LC_EPI_STORE, T, D, 3 * D);
+    a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 1;
+    a.B = w.wp(pp.wq); a.ldb = D; a.b_kmajor = 0;
+    a.C = dn; a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
+    a = gemm_base(dt, LC_EPI_ACCUM_F32, 3 * D, D, T);
+    a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 0;
+    a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
+    a.C = w.gp(pp.wq); a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    // dx = dh + RMSNorm1'(dn1); G[g1] += ...
+    LC_TRY(rmsnorm_bwd_launch(dt, T, D, dn, xin, static_cast<const float *>(L.at(P.rstd1)),
+                              w.wp(pp.g1), dh, dx, w.gp(pp.g1), ws + P.s_norm, P.s_norm_bytes, s));
+    dy = dx;
+  }
+  return LC_OK;
+}
+
+static lc_status check_params(const lc_stage *st, const lc_param_bufs *pb, bool need_grad) {
+  if (!st) return fail(LC_ERR_INVALID_ARG, "null stage");
+  if (!pb || !pb->w) return fail(LC_ERR_INVALID_ARG, "null parameter buffers");
+  if (!aligned16(pb->w)) return fail(LC_ERR_INVALID_ARG, "weights must be 16-byte aligned");
+  if (need_grad && (!pb->grad || !aligned16(pb->grad)))
+    return fail(LC_ERR_INVALID_ARG, "gradient buffer must be non-null and 16-byte aligned");
+  return LC_OK;
+}
+
+static lc_status check_mb(const lc_microbatch_desc *mb, bool fwd) {
+  if (!mb) return fail(LC_ERR_INVALID_ARG, "null microbatch descriptor");
+  if (fwd) {
+    if (!mb->x || !mb->y || !aligned16(mb->x) || !aligned16(mb->y))
+      return fail(LC_ERR_INVALID_ARG, "microbatch %d: x and y must be non-null and aligned", mb->mb);
+  } else {
+    if (!mb->dy || !mb->dx || !aligned16(mb->dy) || !aligned16(mb->dx))
+      return fail(LC_ERR_INVALID_ARG, "microbatch %d: dy and dx must be non-null and aligned",
+                  mb->mb);
+  }
+  return LC_OK;
+}
+
+static int find_slot(const lc_stage *st, int32_t mb) {
+  for (int i = 0; i < st->slots; ++i)
+    if (st->owner[i] == mb) return i;
+  return -1;
+}
+
+static lc_status do_forward(lc_stage *st, const lc_param_bufs *pb, const lc_microbatch_desc *mb,
+                            hipStream_t s) {
+  int slot = find_slot(st, -1);
+  st->owner[slot] = mb->mb;
+  st->xin0[slot] = mb->x;
+  return forward_layers(st, pb, mb->x, mb->y, slot, s);
+}
+
+static lc_status do_backward(lc_stage *st, const lc_param_bufs *pb, const lc_microbatch_desc *mb,
+                             hipStream_t s) {
+  const int slot = find_slot(st, mb->mb);
+  lc_status r = backward_layers(st, pb, st->xin0[slot], mb->dy, mb->dx, slot, s);
+  st->owner[slot] = -1;
+  st->xin0[slot] = nullptr;
+  return r;
+}
+
+}  // namespace lc
+
+using namespace lc;
+
+extern "C" {
+
+lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_bytes,
+                          int32_t max_in_flight, void *stream, lc_stage **out) {
+  if (!out) return fail(LC_ERR_INVALID_ARG, "null output handle");
+  *out = nullptr;
+  StagePlan plan;
+  LC_TRY(validate_desc(desc));
+  LC_TRY(stage_plan(*desc, max_in_flight, &plan));
+  if (desc->n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
+  if (!workspace) return fail(LC_ERR_INVALID_ARG, "null workspace");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(LC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (ws_bytes < plan.total)
+    return fail(LC_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, plan.total);
+  lc_stage *st = new (std::nothrow) lc_stage();
+  if (!st) return fail(LC_ERR_INVALID_ARG, "out of host memory");
+  st->d = *desc;
+  st->plan = plan;
+  st->pp = param_plan(*desc);
+  st->ws = static_cast<char *>(workspace);
+  st->slots = max_in_flight;
+  st->owner.assign((size_t)max_in_flight, -1);
+  st->xin0.assign((size_t)max_in_flight, nullptr);
+  // RoPE angles p * base^(-2i/hd) in double, tables rounded once to float
+  const int half = desc->head_dim / 2, S = desc->seq_len;
+  st->rope_host.resize((size_t)2 * S * half);
+  for (int pos = 0; pos < S; ++pos)
+    for (int i = 0; i < half; ++i) {
+      const double theta = pow((double)desc->rope_base, -2.0 * i / (double)desc->head_dim);
+      const double ang = (double)pos * theta;
+      st->rope_host[(size_t)pos * half + i] = (float)cos(ang);
+      st->rope_host[(size_t)S * half + (size_t)pos * half + i] = (float)sin(ang);
+    }
+  const size_t tb = (size_t)S * half * sizeof(float);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(st->ws + plan.rope_cos, st->rope_host.data(), tb,
+                                hipMemcpyHostToDevice, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(st->ws + plan.rope_sin, st->rope_host.data() + (size_t)S * half, tb,
+                       hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) {
+    delete st;
+    return hip_fail(e, "uploading the RoPE table");
+  }
+  *out = st;
+  return LC_OK;
+}
+
+lc_status lc_stage_destroy(lc_stage *stage) {
+  delete stage;
+  return LC_OK;
+}
+
+lc_status chunk_forward(lc_stage *stage, const lc_param_bufs *params, const lc_microbatch_desc *mb,
+                        void *stream) {
+  LC_TRY(check_params(stage, params, false));
+  LC_TRY(check_mb(mb, true));
+  if (find_slot(stage, mb->mb) >= 0)
+    return fail(LC_ERR_STATE, "microbatch %d is already stashed", mb->mb);
+  if (mb->mb < 0) return fail(LC_ERR_INVALID_ARG, "negative microbatch index");
+  if (find_slot(stage, -1) < 0)
+    return fail(LC_ERR_STASH_FULL, "all %d stash slots are in use", stage->slots);
+  return do_forward(stage, params, mb, static_cast<hipStream_t>(stream));
+}
+
+lc_status chunk_backward(lc_stage *stage, const lc_param_bufs *params, const lc_microbatch_desc *mb,
+                         void *stream) {
+  LC_TRY(check_params(stage, params, true));
+  LC_TRY(check_mb(mb, false));
+  if (mb->mb < 0 || find_slot(stage, mb->mb) < 0)
+    return fail(LC_ERR_STATE, "microbatch %d has no stashed forward", mb->mb);
+  return do_backward(stage, params, mb, static_cast<hipStream_t>(stream));
+}
+
+lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
+                       const lc_microbatch_desc *mbs, void *stream) {
+  LC_TRY(check_params(stage, params, true));
+  LC_TRY(lc_order_validate(order, stage->slots, nullptr));
+  if (!mbs) return fail(LC_ERR_INVALID_ARG, "null microbatch array");
+  for (int i = 0; i < order->num_microbatches; ++i) {
+    if (mbs[i].mb != i) return fail(LC_ERR_INVALID_ARG, "mbs[%d].mb = %d, expected %d", i, mbs[i].mb, i);
+    LC_TRY(check_mb(&mbs[i], true));
+    LC_TRY(check_mb(&mbs[i], false));
+  }
+  for (int i = 0; i < stage->slots; ++i)
+    if (stage->owner[i] != -1)
+      return fail(LC_ERR_STATE, "lc_run_order needs an empty stash (microbatch %d is stashed)",
+                  stage->owner[i]);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int i = 0; i < order->n_entries; ++i) {
+    const lc_order_entry e = order->entries[i];
+    const lc_microbatch_desc *mb = &mbs[e.mb];
+    lc_status r = e.pass == LC_PASS_F ? do_forward(stage, params, mb, s)
+                                      : do_backward(stage, params, mb, s);
+    if (r != LC_OK) return r;
+  }
+  return LC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,356 @@
+"""ctypes binding of libchunk (include/libchunk.h, include/libchunk_ops.h).
+
+Argument marshalling only: every function forwards to the C entry point of
+the same name; all computation happens in the HIP kernels behind it. Device
+buffers are passed as integers (device addresses) or as torch tensors (their
+data_ptr()); streams as integers (a hipStream_t) or torch streams. A negative
+status raises LibchunkError carrying lc_last_error().
+
+The shared library must have been built (``python -m
+paper_2606_11169_amd.build``); importing works without it, the first call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import List, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_lib", "libchunk.so")
+
+LC_OK = 0
+LC_ERR_INVALID_ARG = -1
+LC_ERR_UNSUPPORTED = -2
+LC_ERR_BAD_ORDER = -3
+LC_ERR_STASH_FULL = -4
+LC_ERR_STATE = -5
+LC_ERR_WORKSPACE = -6
+LC_ERR_HIP = -7
+STATUS_NAMES = {0: "OK", -1: "INVALID_ARG", -2: "UNSUPPORTED", -3: "BAD_ORDER",
+                -4: "STASH_FULL", -5: "STATE", -6: "WORKSPACE", -7: "HIP"}
+
+LC_FP32, LC_BF16 = 0, 1
+LC_PASS_F, LC_PASS_B = 0, 1
+(LC_T_WQ, LC_T_WK, LC_T_WV, LC_T_WO, LC_T_G1, LC_T_W1, LC_T_W3, LC_T_W2, LC_T_G2,
+ LC_T_WR) = range(10)
+(LC_EPI_STORE, LC_EPI_STORE_F32, LC_EPI_ACCUM_F32, LC_EPI_RESIDUAL, LC_EPI_ROPE,
+ LC_EPI_SWIGLU, LC_EPI_SWIGLU_BWD) = range(7)
+
+
+class LibchunkError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"libchunk {STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class lc_stage_desc(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("d_ff", C.c_int32), ("n_experts", C.c_int32),
+                ("top_k", C.c_int32), ("d_ff_expert", C.c_int32), ("seq_len", C.c_int32),
+                ("micro_batch", C.c_int32), ("rms_eps", C.c_float), ("rope_base", C.c_float),
+                ("causal", C.c_int32), ("compute_dtype", C.c_int32)]
+
+
+class lc_order_entry(C.Structure):
+    _fields_ = [("mb", C.c_int32), ("pass_", C.c_int32)]
+
+
+class lc_order(C.Structure):
+    _fields_ = [("num_microbatches", C.c_int32), ("n_entries", C.c_int32),
+                ("entries", C.POINTER(lc_order_entry))]
+
+
+class lc_microbatch_desc(C.Structure):
+    _fields_ = [("mb", C.c_int32), ("reserved", C.c_int32), ("x", C.c_void_p),
+                ("y", C.c_void_p), ("dy", C.c_void_p), ("dx", C.c_void_p)]
+
+
+class lc_param_bufs(C.Structure):
+    _fields_ = [("w", C.c_void_p), ("grad", C.c_void_p)]
+
+
+class lc_adam_hparams(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float),
+                ("eps", C.c_float), ("weight_decay", C.c_float), ("reserved", C.c_int32),
+                ("step", C.c_int64)]
+
+
+class lc_gemm_args(C.Structure):
+    _fields_ = [("dtype", C.c_int32), ("epilogue", C.c_int32),
+                ("M", C.c_int64), ("N", C.c_int64), ("K", C.c_int64),
+                ("A", C.c_void_p), ("lda", C.c_int64), ("a_kmajor", C.c_int32),
+                ("b_kmajor", C.c_int32), ("B", C.c_void_p), ("ldb", C.c_int64),
+                ("C", C.c_void_p), ("ldc", C.c_int64),
+                ("R", C.c_void_p), ("ldr", C.c_int64),
+                ("aux0", C.c_void_p), ("aux1", C.c_void_p), ("ld_aux", C.c_int64),
+                ("rope_cos", C.c_void_p), ("rope_sin", C.c_void_p),
+                ("rope_seq", C.c_int32), ("rope_cols", C.c_int32), ("head_dim", C.c_int32),
+                ("reserved", C.c_int32)]
+
+
+# name -> (restype, argtypes)
+_SIGS = {
+    "lc_last_error": (C.c_char_p, []),
+    "lc_param_count": (C.c_int, [C.POINTER(lc_stage_desc), C.POINTER(C.c_size_t)]),
+    "lc_param_offset": (C.c_int, [C.POINTER(lc_stage_desc), C.c_int32, C.c_int32, C.c_int32,
+                                  C.POINTER(C.c_size_t), C.POINTER(C.c_int64)]),
+    "lc_order_1f1b": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.POINTER(lc_order_entry),
+                                C.c_int32, C.POINTER(C.c_int32)]),
+    "lc_order_validate": (C.c_int, [C.POINTER(lc_order), C.c_int32, C.POINTER(C.c_int32)]),
+    "lc_workspace_bytes": (C.c_int, [C.POINTER(lc_stage_desc), C.c_int32, C.POINTER(C.c_size_t)]),
+    "lc_stage_create": (C.c_int, [C.POINTER(lc_stage_desc), C.c_void_p, C.c_size_t, C.c_int32,
+                                  C.c_void_p, C.POINTER(C.c_void_p)]),
+    "lc_stage_destroy": (C.c_int, [C.c_void_p]),
+    "chunk_forward": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
+                                C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "chunk_backward": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
+                                 C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "lc_run_order": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs), C.POINTER(lc_order),
+                               C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "chunk_accumulate_grad": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_size_t,
+                                        C.c_void_p]),
+    "shard_adam_step": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                  C.c_void_p, C.c_size_t, C.POINTER(lc_adam_hparams),
+                                  C.c_void_p]),
+    "lc_gemm": (C.c_int, [C.POINTER(lc_gemm_args), C.c_void_p]),
+    "lc_rmsnorm_forward": (C.c_int, [C.c_int32, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p,
+                                     C.c_float, C.c_void_p, C.c_void_p, C.c_void_p]),
+    "lc_rmsnorm_backward": (C.c_int, [C.c_int32, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p,
+                                      C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                      C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "lc_rmsnorm_scratch_bytes": (C.c_size_t, [C.c_int64, C.c_int64]),
+    "lc_attention_forward": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                       C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
+                                       C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]),
+    "lc_attention_backward": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
+                                        C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p,
+                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
+                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                        C.c_void_p]),
+    "lc_attention_scratch_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32]),
+    "lc_cast_bf16": (C.c_int, [C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+}
+
+EXPORTED = tuple(_SIGS)
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2606_11169_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(st: int) -> int:
+    if st < 0:
+        raise LibchunkError(st, lib().lc_last_error().decode(errors="replace"))
+    return st
+
+
+def ptr(x) -> int:
+    """Device address of a torch tensor, or an int / None passed through."""
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def stream_ptr(s) -> int:
+    if s is None:
+        return 0
+    if isinstance(s, int):
+        return s
+    return int(s.cuda_stream)
+
+
+def _vp(x):
+    return C.c_void_p(ptr(x) or None)
+
+
+# ------------------------------------------------------------------ host-only
+
+def make_desc(n_layers, d_model, n_heads, head_dim, d_ff, seq_len, micro_batch, bf16,
+              n_experts=0, top_k=0, d_ff_expert=0, rms_eps=1e-5, rope_base=10000.0,
+              causal=1) -> lc_stage_desc:
+    return lc_stage_desc(n_layers, d_model, n_heads, head_dim, d_ff, n_experts, top_k,
+                         d_ff_expert, seq_len, micro_batch, rms_eps, rope_base, causal,
+                         LC_BF16 if bf16 else LC_FP32)
+
+
+def lc_param_count(desc: lc_stage_desc) -> int:
+    n = C.c_size_t()
+    _check(lib().lc_param_count(C.byref(desc), C.byref(n)))
+    return n.value
+
+
+def lc_param_offset(desc, layer, tensor_id, expert=0) -> Tuple[int, Tuple[int, int]]:
+    off = C.c_size_t()
+    shape = (C.c_int64 * 2)()
+    _check(lib().lc_param_offset(C.byref(desc), layer, tensor_id, expert, C.byref(off), shape))
+    return off.value, (shape[0], shape[1])
+
+
+def lc_order_1f1b(M, P, s) -> List[Tuple[int, int]]:
+    buf = (lc_order_entry * max(1, 2 * M))()
+    n = C.c_int32()
+    _check(lib().lc_order_1f1b(M, P, s, buf, 2 * M, C.byref(n)))
+    return [(buf[i].mb, buf[i].pass_) for i in range(n.value)]
+
+
+def make_order(entries: Sequence[Tuple[int, int]], M: int):
+    arr = (lc_order_entry * max(1, len(entries)))(*[lc_order_entry(m, p) for m, p in entries])
+    o = lc_order(M, len(entries), C.cast(arr, C.POINTER(lc_order_entry)))
+    o._keep = arr
+    return o
+
+
+def lc_order_validate(entries, M, max_in_flight) -> Tuple[int, int]:
+    """Returns (status, peak) without raising for Order errors."""
+    o = make_order(entries, M)
+    pk = C.c_int32()
+    st = lib().lc_order_validate(C.byref(o), max_in_flight, C.byref(pk))
+    if st not in (LC_OK, LC_ERR_BAD_ORDER, LC_ERR_STASH_FULL):
+        _check(st)
+    return st, pk.value
+
+
+def lc_workspace_bytes(desc, max_in_flight) -> int:
+    n = C.c_size_t()
+    _check(lib().lc_workspace_bytes(C.byref(desc), max_in_flight, C.byref(n)))
+    return n.value
+
+
+def lc_rmsnorm_scratch_bytes(T, d) -> int:
+    return int(lib().lc_rmsnorm_scratch_bytes(T, d))
+
+
+def lc_attention_scratch_bytes(B, S, H) -> int:
+    return int(lib().lc_attention_scratch_bytes(B, S, H))
+
+
+# ------------------------------------------------------------------ stage
+
+class Stage:
+    """Owns an lc_stage handle (host memory); the workspace belongs to the caller."""
+
+    def __init__(self, desc, workspace, ws_bytes, max_in_flight, stream=None):
+        h = C.c_void_p()
+        _check(lib().lc_stage_create(C.byref(desc), _vp(workspace), ws_bytes, max_in_flight,
+                                     C.c_void_p(stream_ptr(stream) or None), C.byref(h)))
+        self.handle = h
+        self.desc = desc
+
+    def close(self):
+        if self.handle:
+            lib().lc_stage_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def lc_stage_create(desc, workspace, ws_bytes, max_in_flight, stream=None) -> Stage:
+    return Stage(desc, workspace, ws_bytes, max_in_flight, stream)
+
+
+def _mb(mb, x=None, y=None, dy=None, dx=None):
+    return lc_microbatch_desc(mb, 0, _vp(x), _vp(y), _vp(dy), _vp(dx))
+
+
+def chunk_forward(stage: Stage, w, grad, mb, x, y, stream=None):
+    pb = lc_param_bufs(_vp(w), _vp(grad))
+    d = _mb(mb, x=x, y=y)
+    return _check(lib().chunk_forward(stage.handle, C.byref(pb), C.byref(d),
+                                      C.c_void_p(stream_ptr(stream) or None)))
+
+
+def chunk_backward(stage: Stage, w, grad, mb, dy, dx, stream=None):
+    pb = lc_param_bufs(_vp(w), _vp(grad))
+    d = _mb(mb, dy=dy, dx=dx)
+    return _check(lib().chunk_backward(stage.handle, C.byref(pb), C.byref(d),
+                                       C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_run_order(stage: Stage, w, grad, entries, xs, ys, dys, dxs, stream=None):
+    M = len(xs)
+    o = make_order(entries, M)
+    arr = (lc_microbatch_desc * M)(*[_mb(i, xs[i], ys[i], dys[i], dxs[i]) for i in range(M)])
+    pb = lc_param_bufs(_vp(w), _vp(grad))
+    return _check(lib().lc_run_order(stage.handle, C.byref(pb), C.byref(o), arr,
+                                     C.c_void_p(stream_ptr(stream) or None)))
+
+
+# ------------------------------------------------------------------ buffers
+
+def chunk_accumulate_grad(accum, g, g_dtype, n, stream=None):
+    return _check(lib().chunk_accumulate_grad(_vp(accum), _vp(g), g_dtype, n,
+                                              C.c_void_p(stream_ptr(stream) or None)))
+
+
+def shard_adam_step(master, m, v, grad, grad_dtype, out_bf16, n, lr, beta1, beta2, eps,
+                    weight_decay, step, stream=None):
+    hp = lc_adam_hparams(lr, beta1, beta2, eps, weight_decay, 0, step)
+    return _check(lib().shard_adam_step(_vp(master), _vp(m), _vp(v), _vp(grad), grad_dtype,
+                                        _vp(out_bf16), n, C.byref(hp),
+                                        C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_cast_bf16(inp, out, n, stream=None):
+    return _check(lib().lc_cast_bf16(_vp(inp), _vp(out), n,
+                                     C.c_void_p(stream_ptr(stream) or None)))
+
+
+# ------------------------------------------------------------------ ops
+
+def lc_gemm(dtype, epilogue, M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, Cm, ldc, R=None,
+            ldr=0, aux0=None, aux1=None, ld_aux=0, rope_cos=None, rope_sin=None, rope_seq=0,
+            rope_cols=0, head_dim=0, stream=None):
+    a = lc_gemm_args(dtype, epilogue, M, N, K, ptr(A) or None, lda, int(a_kmajor),
+                     int(b_kmajor), ptr(B) or None, ldb, ptr(Cm) or None, ldc, ptr(R) or None,
+                     ldr, ptr(aux0) or None, ptr(aux1) or None, ld_aux, ptr(rope_cos) or None,
+                     ptr(rope_sin) or None, rope_seq, rope_cols, head_dim, 0)
+    return _check(lib().lc_gemm(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_rmsnorm_forward(dtype, T, d, x, g, eps, n, rstd, stream=None):
+    return _check(lib().lc_rmsnorm_forward(dtype, T, d, _vp(x), _vp(g), eps, _vp(n), _vp(rstd),
+                                           C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_rmsnorm_backward(dtype, T, d, dn, x, rstd, g, dres, dx, dg_accum, scratch,
+                        scratch_bytes, stream=None):
+    return _check(lib().lc_rmsnorm_backward(dtype, T, d, _vp(dn), _vp(x), _vp(rstd), _vp(g),
+                                            _vp(dres), _vp(dx), _vp(dg_accum), _vp(scratch),
+                                            scratch_bytes,
+                                            C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_attention_forward(dtype, B, S, H, hd, q, k, v, ld_qkv, o, ld_o, lse, stream=None):
+    return _check(lib().lc_attention_forward(dtype, B, S, H, hd, _vp(q), _vp(k), _vp(v), ld_qkv,
+                                             _vp(o), ld_o, _vp(lse),
+                                             C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_attention_backward(dtype, B, S, H, hd, q, k, v, ld_qkv, o, dout, ld_o, lse, dq, dk, dv,
+                          ld_dqkv, rope_cos, rope_sin, scratch, scratch_bytes, stream=None):
+    return _check(lib().lc_attention_backward(dtype, B, S, H, hd, _vp(q), _vp(k), _vp(v), ld_qkv,
+                                              _vp(o), _vp(dout), ld_o, _vp(lse), _vp(dq),
+                                              _vp(dk), _vp(dv), ld_dqkv, _vp(rope_cos),
+                                              _vp(rope_sin), _vp(scratch), scratch_bytes,
+                                              C.c_void_p(stream_ptr(stream) or None)))

@@ -1,0 +1,395 @@
+"""Parity of the individual HIP kernels (through the C-ABI) with the oracle.
+
+Bit-exact: gradient accumulation, AdamW + bf16 cast, the cast itself, and
+GEMMs on integer-valued operands (every partial sum is an exact integer in
+fp32). Within tolerance: GEMM on random operands, the fused epilogues,
+RMSNorm and attention (fp32 path 1e-4, bf16 path 2e-2, max-normwise).
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import optim as OP
+from oracle import stage as OS
+from paper_2606_11169_amd import libchunk as lc
+from paper_2606_11169_amd.runner import require_gpu
+from tests.gpu_util import (DEV, banner, bf16, bf16_round, bits16, bits32, dev, f32, host, ints,
+                            rel_err)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- accumulation
+
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
+@pytest.mark.parametrize("n", [1, 3, 255, 4097, (1 << 20) + 5])
+def test_accumulate_bit_exact_and_covering(n, gdt):
+    banner(f"accumulate n={n} g={gdt}")
+    rng = np.random.default_rng(n)
+    G0 = rng.standard_normal(n).astype(np.float32)
+    g = rng.standard_normal(n).astype(np.float32)
+    if gdt == "bf16":
+        g = bf16_round(g)
+    pad = 64
+    Gd = f32(np.concatenate([G0, np.full(pad, 7.0, np.float32)]))
+    gd = dev(np.concatenate([g, np.full(pad, 3.0, np.float32)]), gdt == "bf16")
+    lc.chunk_accumulate_grad(Gd, gd, lc.LC_BF16 if gdt == "bf16" else lc.LC_FP32, n)
+    torch.cuda.synchronize()
+    got = bits32(Gd)
+    want = OP.accumulate(G0, g).view(np.uint32)
+    assert np.array_equal(got[:n], want)
+    assert np.all(host(Gd)[n:] == 7.0)  # canary words untouched
+    # sentinel: G = 0, g[i] = i  -> each element updated exactly once
+    idx = (np.arange(n) % 256).astype(np.float32)
+    Z = f32(np.zeros(n, np.float32))
+    lc.chunk_accumulate_grad(Z, dev(idx, gdt == "bf16"), lc.LC_BF16 if gdt == "bf16" else lc.LC_FP32, n)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(Z), idx)
+
+
+def test_accumulate_disjoint_shards_leave_each_other_intact():
+    banner("accumulate shards")
+    n = 10_000
+    G = f32(np.zeros(2 * n, np.float32))
+    g = f32(np.ones(2 * n, np.float32))
+    lc.chunk_accumulate_grad(G, g, lc.LC_FP32, n)
+    lc.chunk_accumulate_grad(G.data_ptr() + 4 * n, g.data_ptr() + 4 * n, lc.LC_FP32, n)
+    lc.chunk_accumulate_grad(G, g, lc.LC_FP32, n)
+    torch.cuda.synchronize()
+    h = host(G)
+    assert np.all(h[:n] == 2.0) and np.all(h[n:] == 1.0)
+
+
+# ---------------------------------------------------------------- AdamW
+
+ADAM_CASES = [
+    # (lr, b1, b2, eps, wd)
+    (1e-3, 0.9, 0.999, 1e-8, 0.0),
+    (3e-4, 0.9, 0.95, 1e-8, 0.1),
+]
+
+
+@pytest.mark.parametrize("hp", ADAM_CASES)
+@pytest.mark.parametrize("state,step", [("zero", 1), ("warm", 10)])
+@pytest.mark.parametrize("gdt", ["bf16", "f32"])
+@pytest.mark.parametrize("n", [1, 7, 4099, (1 << 20) + 3])
+def test_adam_bit_exact(n, gdt, state, step, hp):
+    banner(f"adam n={n} g={gdt} {state} t={step} hp={hp}")
+    p, m, v, g = synth.adam_inputs(n, seed=1, state=state)
+    if gdt == "f32":
+        g = synth.normal(1, 777, n, 1e-3)
+    lr, b1, b2, eps, wd = hp
+    p1, m1, v1 = OP.adamw(p, m, v, g, lr, b1, b2, eps, wd, step)
+    out_ref = OP.bf16_rne_bits(p1)
+    P, Mo, V = f32(p), f32(m), f32(v)
+    Gd = dev(g, gdt == "bf16")
+    out = torch.zeros(n + 8, dtype=torch.int16, device=DEV)
+    lc.shard_adam_step(P, Mo, V, Gd, lc.LC_BF16 if gdt == "bf16" else lc.LC_FP32, out, n, lr, b1,
+                       b2, eps, wd, step)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits32(P), p1.view(np.uint32))
+    assert np.array_equal(bits32(Mo), m1.view(np.uint32))
+    assert np.array_equal(bits32(V), v1.view(np.uint32))
+    ob = bits16(out)
+    assert np.array_equal(ob[:n], out_ref)
+    assert np.all(ob[n:] == 0)
+
+
+def test_adam_without_cast_and_nonfinite_propagation():
+    banner("adam no-cast + nan")
+    n = 1000
+    p, m, v, g = synth.adam_inputs(n, seed=2, state="warm")
+    g = g.copy()
+    g[5] = np.nan
+    g[6] = np.inf
+    p1, m1, v1 = OP.adamw(p, m, v, g, 3e-4, 0.9, 0.95, 1e-8, 0.1, 3)
+    P, Mo, V = f32(p), f32(m), f32(v)
+    lc.shard_adam_step(P, Mo, V, f32(g), lc.LC_FP32, None, n, 3e-4, 0.9, 0.95, 1e-8, 0.1, 3)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits32(P), p1.view(np.uint32))
+    assert np.isnan(host(P)[5]) and np.isnan(host(P)[6])
+
+
+# ---------------------------------------------------------------- cast
+
+def test_cast_bf16_every_bf16_value_and_random_patterns():
+    banner("cast bf16")
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0x0000, 0x0001, 0x3FFF, 0x7FFF, 0x8000, 0x8001, 0xC000, 0xFFFF], np.uint32)
+    rng = np.random.default_rng(0)
+    bits = np.concatenate([(hi[:, None] | lows[None, :]).reshape(-1),
+                           rng.integers(0, 1 << 32, size=3_000_001, dtype=np.uint64).astype(np.uint32)])
+    x = bits.view(np.float32)
+    xin = torch.from_numpy(bits.view(np.int32).copy()).to(DEV).view(torch.float32)
+    out = torch.empty(x.size, dtype=torch.int16, device=DEV)
+    lc.lc_cast_bf16(xin, out, x.size)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits16(out), OP.bf16_rne_bits(x))
+
+
+# ---------------------------------------------------------------- GEMM
+
+LAYOUTS = [(True, True), (True, False), (False, False)]
+
+
+def operands(rng, M, N, K, a_k, b_k, integer, brows=None):
+    brows = brows or N
+    if integer:
+        A, B = ints(rng, (M, K)), ints(rng, (brows, K))
+    else:
+        A = bf16_round(rng.standard_normal((M, K)).astype(np.float32))
+        B = bf16_round(rng.standard_normal((brows, K)).astype(np.float32))
+    Am = A if a_k else np.ascontiguousarray(A.T)
+    Bm = B if b_k else np.ascontiguousarray(B.T)
+    return A, B, bf16(Am), bf16(Bm), (K if a_k else M), (K if b_k else brows)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS, ids=["NT", "NN", "TN"])
+@pytest.mark.parametrize("shape", [(256, 256, 64), (304, 264, 200), (512, 768, 1024), (8, 8, 8),
+                                   (1024, 256, 4096)])
+def test_gemm_integer_operands_bit_exact(shape, layout):
+    M, N, K = shape
+    a_k, b_k = layout
+    banner(f"gemm int {shape} layout={layout}")
+    rng = np.random.default_rng(M + N + K)
+    A, B, Ad, Bd, lda, ldb = operands(rng, M, N, K, a_k, b_k, True)
+    exact = (A.astype(np.int64) @ B.astype(np.int64).T).astype(np.float32)
+    C = torch.full((M, N), -1.0, dtype=torch.float32, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE_F32, M, N, K, Ad, lda, a_k, Bd, ldb, b_k, C, N)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(C), exact)
+    if not (a_k and not b_k):
+        C0 = ints(rng, (M, N), -1000, 1000)
+        Cacc = f32(C0)
+        lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ACCUM_F32, M, N, K, Ad, lda, a_k, Bd, ldb, b_k, Cacc, N)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(Cacc), C0 + exact)
+    Cb = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE, M, N, K, Ad, lda, a_k, Bd, ldb, b_k, Cb, N)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits16(Cb).reshape(M, N), OP.bf16_rne_bits(exact))
+
+
+@pytest.mark.parametrize("layout", LAYOUTS, ids=["NT", "NN", "TN"])
+def test_gemm_random_operands(layout):
+    a_k, b_k = layout
+    M, N, K = 520, 384, 1032
+    banner(f"gemm random layout={layout}")
+    rng = np.random.default_rng(5)
+    A, B, Ad, Bd, lda, ldb = operands(rng, M, N, K, a_k, b_k, False)
+    ref = A.astype(np.float64) @ B.astype(np.float64).T
+    C = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE_F32, M, N, K, Ad, lda, a_k, Bd, ldb, b_k, C, N)
+    torch.cuda.synchronize()
+    assert rel_err(host(C), ref) <= 1e-5
+
+
+def test_gemm_residual_epilogue():
+    banner("gemm residual")
+    rng = np.random.default_rng(6)
+    M, N, K = 384, 512, 256
+    A, B, Ad, Bd, lda, ldb = operands(rng, M, N, K, True, True, False)
+    R = bf16_round(rng.standard_normal((M, N)).astype(np.float32))
+    C = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_RESIDUAL, M, N, K, Ad, lda, 1, Bd, ldb, 1, C, N, R=bf16(R), ldr=N)
+    torch.cuda.synchronize()
+    ref = R + A.astype(np.float64) @ B.astype(np.float64).T
+    assert rel_err(host(C), ref) <= 8e-3
+
+
+def test_gemm_rope_epilogue():
+    banner("gemm rope")
+    rng = np.random.default_rng(7)
+    H, hd, S, b = 2, 128, 256, 2
+    d = H * hd
+    T, N, K = b * S, 3 * d, d
+    A, B, Ad, Bd, lda, ldb = operands(rng, T, N, K, True, True, False)
+    cos, sin = OS.rope_tables(S, hd, 10000.0)
+    C = torch.empty((T, N), dtype=torch.bfloat16, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ROPE, T, N, K, Ad, lda, 1, Bd, ldb, 1, C, N,
+               rope_cos=f32(cos), rope_sin=f32(sin), rope_seq=S, rope_cols=2 * d, head_dim=hd)
+    torch.cuda.synchronize()
+    prod = (A.astype(np.float64) @ B.astype(np.float64).T).reshape(b, S, 3, H, hd)
+    q = OS.rope_apply(prod[:, :, 0], cos, sin)
+    k = OS.rope_apply(prod[:, :, 1], cos, sin)
+    ref = np.stack([q, k, prod[:, :, 2]], axis=2).reshape(T, N)
+    assert rel_err(host(C), ref) <= 8e-3
+
+
+def test_gemm_swiglu_epilogues():
+    banner("gemm swiglu fwd/bwd")
+    rng = np.random.default_rng(8)
+    T, F, D = 384, 320, 256
+    A, B13, Ad, Bd, lda, ldb = operands(rng, T, F, D, True, True, False, brows=2 * F)
+    act = torch.empty((T, F), dtype=torch.bfloat16, device=DEV)
+    gate = torch.empty_like(act)
+    up = torch.empty_like(act)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_SWIGLU, T, F, D, Ad, lda, 1, Bd, ldb, 1, act, F,
+               aux0=gate, aux1=up, ld_aux=F)
+    torch.cuda.synchronize()
+    prod = A.astype(np.float64) @ B13.astype(np.float64).T
+    g_ref, u_ref = prod[:, :F], prod[:, F:]
+    assert rel_err(host(gate), g_ref) <= 8e-3
+    assert rel_err(host(up), u_ref) <= 8e-3
+    assert rel_err(host(act), OS.silu(g_ref) * u_ref) <= 1e-2
+    # backward: da = dy W2 (W2 [D, F] read with k = D not contiguous)
+    dy = bf16_round(rng.standard_normal((T, D)).astype(np.float32))
+    W2 = bf16_round(rng.standard_normal((D, F)).astype(np.float32) * 0.05)
+    gv, uv = host(gate), host(up)
+    dgu = torch.empty((T, 2 * F), dtype=torch.bfloat16, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_SWIGLU_BWD, T, F, D, bf16(dy), D, 1, bf16(W2), F, 0, dgu,
+               2 * F, aux0=gate, aux1=up, ld_aux=F)
+    torch.cuda.synchronize()
+    da = dy.astype(np.float64) @ W2.astype(np.float64)
+    s = OS.sigmoid(gv)
+    ref = np.concatenate([da * uv * s * (1 + gv * (1 - s)), da * OS.silu(gv)], axis=1)
+    assert rel_err(host(dgu), ref) <= 1e-2
+
+
+@pytest.mark.parametrize("layout", LAYOUTS, ids=["NT", "NN", "TN"])
+def test_gemm_fp32_path(layout):
+    a_k, b_k = layout
+    banner(f"gemm fp32 layout={layout}")
+    rng = np.random.default_rng(9)
+    M, N, K = 130, 90, 70
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = rng.standard_normal((N, K)).astype(np.float32)
+    Am = A if a_k else np.ascontiguousarray(A.T)
+    Bm = B if b_k else np.ascontiguousarray(B.T)
+    C = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    lc.lc_gemm(lc.LC_FP32, lc.LC_EPI_STORE, M, N, K, f32(Am), K if a_k else M, a_k, f32(Bm),
+               K if b_k else N, b_k, C, N)
+    torch.cuda.synchronize()
+    assert rel_err(host(C), A.astype(np.float64) @ B.astype(np.float64).T) <= 1e-5
+
+
+# ---------------------------------------------------------------- RMSNorm
+
+@pytest.mark.parametrize("is_bf16", [False, True], ids=["fp32", "bf16"])
+def test_rmsnorm_forward_backward(is_bf16):
+    banner(f"rmsnorm bf16={is_bf16}")
+    rng = np.random.default_rng(10)
+    T, d, eps = 300, 512, 1e-5
+    rnd = (lambda a: bf16_round(a)) if is_bf16 else (lambda a: a)
+    x = rnd(rng.standard_normal((T, d)).astype(np.float32))
+    g = rnd((1 + 0.1 * rng.standard_normal(d)).astype(np.float32))
+    dn = rnd(rng.standard_normal((T, d)).astype(np.float32))
+    dres = rnd(rng.standard_normal((T, d)).astype(np.float32))
+    dt = lc.LC_BF16 if is_bf16 else lc.LC_FP32
+    xd, gd = dev(x, is_bf16), dev(g, is_bf16)
+    n = torch.empty_like(xd)
+    rstd = torch.empty(T, dtype=torch.float32, device=DEV)
+    lc.lc_rmsnorm_forward(dt, T, d, xd, gd, eps, n, rstd)
+    n_ref, r_ref = OS.rmsnorm_forward(x.astype(np.float64), g.astype(np.float64), eps)
+    torch.cuda.synchronize()
+    tol = 8e-3 if is_bf16 else 1e-5
+    assert rel_err(host(n), n_ref) <= tol
+    assert rel_err(host(rstd), r_ref[:, 0]) <= 1e-5
+    dx = torch.empty_like(xd)
+    dg0 = rng.standard_normal(d).astype(np.float32)
+    dg = f32(dg0)
+    sb = lc.lc_rmsnorm_scratch_bytes(T, d)
+    scratch = torch.empty(sb, dtype=torch.uint8, device=DEV)
+    lc.lc_rmsnorm_backward(dt, T, d, dev(dn, is_bf16), xd, rstd, gd, dev(dres, is_bf16), dx, dg,
+                           scratch, sb)
+    torch.cuda.synchronize()
+    dx_ref, dg_ref = OS.rmsnorm_backward(dn.astype(np.float64), x.astype(np.float64),
+                                         host(rstd)[:, None], g.astype(np.float64))
+    assert rel_err(host(dx), dres + dx_ref) <= (1e-2 if is_bf16 else 1e-5)
+    assert rel_err(host(dg), dg0 + dg_ref) <= 1e-5
+
+
+# ---------------------------------------------------------------- attention
+
+def packed_qkv(rng, B, S, H, hd, is_bf16, identical_keys=False):
+    d = H * hd
+    qkv = rng.standard_normal((B, S, 3, H, hd)).astype(np.float32)
+    if identical_keys:
+        qkv[:, :, 1] = qkv[:, :1, 1]
+    if is_bf16:
+        qkv = bf16_round(qkv)
+    return qkv, dev(qkv.reshape(B * S, 3 * d), is_bf16)
+
+
+def attn_case(B, S, H, hd, is_bf16, seed, rope):
+    banner(f"attention B={B} S={S} H={H} hd={hd} bf16={is_bf16} rope={rope}")
+    rng = np.random.default_rng(seed)
+    d = H * hd
+    qkv, qkvd = packed_qkv(rng, B, S, H, hd, is_bf16)
+    dt = lc.LC_BF16 if is_bf16 else lc.LC_FP32
+    esz = 2 if is_bf16 else 4
+    base = qkvd.data_ptr()
+    o = torch.empty((B * S, d), dtype=qkvd.dtype, device=DEV)
+    lse = torch.empty(B * H * S, dtype=torch.float32, device=DEV)
+    lc.lc_attention_forward(dt, B, S, H, hd, base, base + d * esz, base + 2 * d * esz, 3 * d, o, d, lse)
+    q, k, v = (qkv[:, :, i].astype(np.float64) for i in range(3))
+    o_ref = OS.attention_forward(q, k, v)
+    s = np.einsum("bihe,bjhe->bhij", q, k) / np.sqrt(hd)
+    s = np.where(np.triu(np.ones((S, S), bool), 1)[None, None], -np.inf, s)
+    mx = s.max(-1, keepdims=True)
+    lse_ref = (mx + np.log(np.exp(s - mx).sum(-1, keepdims=True)))[..., 0]
+    torch.cuda.synchronize()
+    tol = 2e-2 if is_bf16 else 1e-4
+    assert rel_err(host(o).reshape(B, S, H, hd), o_ref) <= tol / 2
+    assert np.max(np.abs(host(lse).reshape(B, H, S) - lse_ref)) <= (1e-2 if is_bf16 else 1e-5)
+    do = rng.standard_normal((B, S, H, hd)).astype(np.float32)
+    if is_bf16:
+        do = bf16_round(do)
+    dqkv = torch.zeros((B * S, 3 * d), dtype=qkvd.dtype, device=DEV)
+    cos = sin = None
+    if rope:
+        cos, sin = OS.rope_tables(S, hd, 10000.0)
+    sb = lc.lc_attention_scratch_bytes(B, S, H)
+    scratch = torch.empty(sb, dtype=torch.uint8, device=DEV)
+    g0 = dqkv.data_ptr()
+    lc.lc_attention_backward(dt, B, S, H, hd, base, base + d * esz, base + 2 * d * esz, 3 * d, o,
+                             dev(do.reshape(B * S, d), is_bf16), d, lse, g0, g0 + d * esz,
+                             g0 + 2 * d * esz, 3 * d, None if cos is None else f32(cos),
+                             None if sin is None else f32(sin), scratch, sb)
+    # reference uses the kernel's own (rounded) O only through D = rowsum(dO*O): use exact O
+    dq, dk, dv = OS.attention_backward(do.astype(np.float64), q, k, v)
+    if rope:
+        dq = OS.rope_apply(dq, cos, sin, inverse=True)
+        dk = OS.rope_apply(dk, cos, sin, inverse=True)
+    torch.cuda.synchronize()
+    got = host(dqkv).reshape(B, S, 3, H, hd)
+    for i, ref in enumerate((dq, dk, dv)):
+        assert rel_err(got[:, :, i], ref) <= tol, ("dq", "dk", "dv")[i]
+
+
+@pytest.mark.parametrize("rope", [False, True])
+def test_attention_bf16(rope):
+    attn_case(2, 256, 2, 128, True, 11, rope)
+
+
+def test_attention_bf16_longer():
+    attn_case(1, 512, 1, 128, True, 12, True)
+
+
+@pytest.mark.parametrize("hd", [32, 8])
+def test_attention_fp32(hd):
+    attn_case(2, 64, 4, hd, False, 13, True)
+
+
+def test_attention_identical_keys_prefix_mean():
+    banner("attention identical keys")
+    rng = np.random.default_rng(14)
+    B, S, H, hd = 1, 256, 2, 128
+    d = H * hd
+    qkv, qkvd = packed_qkv(rng, B, S, H, hd, True, identical_keys=True)
+    base = qkvd.data_ptr()
+    o = torch.empty((B * S, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty(B * H * S, dtype=torch.float32, device=DEV)
+    lc.lc_attention_forward(lc.LC_BF16, B, S, H, hd, base, base + 2 * d, base + 4 * d, 3 * d, o, d, lse)
+    torch.cuda.synchronize()
+    v = qkv[:, :, 2].astype(np.float64)
+    prefix_mean = np.cumsum(v, axis=1) / np.arange(1, S + 1)[None, :, None, None]
+    assert rel_err(host(o).reshape(B, S, H, hd), prefix_mean) <= 1e-2

@@ -1,0 +1,179 @@
+"""Host-side checks of the libchunk C-ABI (no GPU needed):
+
+* the built library loads and exports every function the headers declare
+* the canonical parameter layout equals the input recipe's layout
+* 1F1B generation and Order validation agree with the Order oracle
+  (hand-listed cases, the paper's listing, random permutations)
+* descriptor, workspace and argument errors come back as status codes
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import order as OO
+from paper_2606_11169_amd import libchunk as lc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in ("libchunk.h", "libchunk_ops.h"):
+        txt = open(os.path.join(ROOT, "include", h)).read()
+        txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+        for m in re.finditer(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*([a-z_][a-z0-9_]*)\s*\(",
+                             txt, flags=re.M):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+def test_library_exports_every_declared_function():
+    L = lc.lib()
+    names = declared_functions()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(lc.EXPORTED)
+
+
+def desc_of(cfg):
+    return lc.make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
+                        cfg.seq_len, cfg.micro_batch, cfg.bf16, n_experts=cfg.n_experts,
+                        top_k=cfg.top_k, d_ff_expert=cfg.d_ff_expert, rms_eps=cfg.rms_eps,
+                        rope_base=cfg.rope_base)
+
+
+TID = {"wq": lc.LC_T_WQ, "wk": lc.LC_T_WK, "wv": lc.LC_T_WV, "wo": lc.LC_T_WO,
+       "g1": lc.LC_T_G1, "w1": lc.LC_T_W1, "w3": lc.LC_T_W3, "w2": lc.LC_T_W2,
+       "g2": lc.LC_T_G2, "wr": lc.LC_T_WR}
+
+
+@pytest.mark.parametrize("cfg", list(synth.STAGES.values()), ids=list(synth.STAGES))
+def test_param_layout_matches_recipe(cfg):
+    d = desc_of(cfg)
+    assert lc.lc_param_count(d) == synth.param_count(cfg)
+    for name, off, shape in synth.layout(cfg):
+        parts = name.split(".")
+        layer = int(parts[0][1:])
+        expert = int(parts[1][1:]) if len(parts) == 3 else 0
+        o, sh = lc.lc_param_offset(d, layer, TID[parts[-1]], expert)
+        assert o == off, name
+        assert sh == (shape + (1,))[:2], name
+
+
+def test_param_counts_of_the_workloads():
+    assert synth.param_count(synth.TINY_FP32) == 395_776
+    assert synth.param_count(synth.LLAMA_2K) == 411_074_560
+    assert synth.param_count(synth.STAGE_7B) == 809_533_440
+    assert synth.param_count(synth.MOE_2K) == 344_014_848
+
+
+@pytest.mark.parametrize("M,P,s", [(4, 2, 0), (16, 8, 0), (16, 8, 7), (3, 5, 1), (1, 1, 0),
+                                   (8, 4, 2), (5, 8, 0)])
+def test_1f1b_matches_oracle(M, P, s):
+    got = lc.lc_order_1f1b(M, P, s)
+    want = [(mb, lc.LC_PASS_F if ps == "F" else lc.LC_PASS_B) for mb, ps in OO.one_f_one_b(M, P, s)]
+    assert got == want
+
+
+def to_c(entries):
+    return [(mb, lc.LC_PASS_F if ps == "F" else lc.LC_PASS_B) for mb, ps in entries]
+
+
+STATUS = {"OK": lc.LC_OK, "BAD_ORDER": lc.LC_ERR_BAD_ORDER, "STASH_FULL": lc.LC_ERR_STASH_FULL}
+
+
+def test_validate_matches_oracle_on_fixture_and_random_orders():
+    from tests.test_oracle_order import golden_cases
+    for M, status, peak, body in golden_cases():
+        st, pk = lc.lc_order_validate(to_c(OO.parse(body)), M, M)
+        assert st == STATUS[status], body
+        if status == "OK":
+            assert pk == peak
+    rng = np.random.default_rng(0)
+    for trial in range(3000):
+        M = int(rng.integers(1, 6))
+        base = [(i, "F") for i in range(M)] + [(i, "B") for i in range(M)]
+        kind = trial % 3
+        if kind == 0:
+            seq = [base[i] for i in rng.permutation(len(base))]
+        elif kind == 1:
+            seq = OO.one_f_one_b(M, int(rng.integers(1, 6)), 0)
+        else:
+            seq = list(base)
+            if len(seq) > 1:
+                i, j = rng.integers(0, len(seq), size=2)
+                seq[i] = seq[j]
+        cap = int(rng.integers(1, M + 2))
+        st_o, pk_o = OO.validate(seq, M, cap)
+        st_c, pk_c = lc.lc_order_validate(to_c(seq), M, cap)
+        assert st_c == STATUS[st_o], (seq, cap)
+        if st_o == "OK":
+            assert pk_c == pk_o
+
+
+def test_workspace_grows_with_stash_slots():
+    d = desc_of(synth.STAGE_7B)
+    w1 = lc.lc_workspace_bytes(d, 1)
+    w8 = lc.lc_workspace_bytes(d, 8)
+    slot = (w8 - w1) // 7
+    T, D, F, L = 4096, 4096, 11008, 4
+    # per layer: x, n1, qkv(3), o, h, n2 (bf16 [T,d]) + gate, up, act ([T,f]) + fp32 rows
+    approx = L * (2 * T * D * 8 + 2 * T * F * 3 + 4 * T * (2 + 32))
+    assert approx <= slot <= approx + L * 16 * 256
+
+
+def test_descriptor_errors():
+    base = dict(n_layers=1, d_model=256, n_heads=2, head_dim=128, d_ff=512, seq_len=128,
+                micro_batch=1, bf16=True)
+    assert lc.lc_param_count(lc.make_desc(**base)) > 0
+    bad = [dict(d_model=250), dict(n_layers=0), dict(head_dim=64, n_heads=4),
+           dict(seq_len=100), dict(d_ff=-1)]
+    for kw in bad:
+        with pytest.raises(lc.LibchunkError) as e:
+            lc.lc_param_count(lc.make_desc(**{**base, **kw}))
+        assert e.value.status in (lc.LC_ERR_INVALID_ARG, lc.LC_ERR_UNSUPPORTED)
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.lc_param_count(lc.make_desc(**base, causal=0))
+    assert e.value.status == lc.LC_ERR_UNSUPPORTED
+    with pytest.raises(lc.LibchunkError):
+        lc.lc_param_offset(lc.make_desc(**base), 1, lc.LC_T_WQ)
+    with pytest.raises(lc.LibchunkError):
+        lc.lc_param_offset(lc.make_desc(**base), 0, lc.LC_T_WR)
+
+
+def test_stage_create_argument_errors_before_any_device_work():
+    d = lc.make_desc(1, 256, 2, 128, 512, 128, 1, True)
+    need = lc.lc_workspace_bytes(d, 2)
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.lc_stage_create(d, 0, need, 2)
+    assert e.value.status == lc.LC_ERR_INVALID_ARG
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.lc_stage_create(d, 1 << 20, need - 1, 2)
+    assert e.value.status == lc.LC_ERR_WORKSPACE
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.lc_stage_create(d, (1 << 20) + 16, need, 2)
+    assert e.value.status == lc.LC_ERR_INVALID_ARG
+
+
+def test_buffer_entry_points_reject_bad_arguments():
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.chunk_accumulate_grad(0, 0, lc.LC_FP32, 10)
+    assert e.value.status == lc.LC_ERR_INVALID_ARG
+    with pytest.raises(lc.LibchunkError):
+        lc.chunk_accumulate_grad(4096, 4096 + 16, lc.LC_FP32, 10)  # overlap
+    with pytest.raises(lc.LibchunkError):
+        lc.chunk_accumulate_grad(4096 + 4, 1 << 20, lc.LC_FP32, 10)  # unaligned
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.shard_adam_step(4096, 8192, 12288, 16384, lc.LC_BF16, 0, 8, 1e-3, 0.9, 0.999, 1e-8,
+                           0.0, 0)
+    assert e.value.status == lc.LC_ERR_INVALID_ARG
+    assert lc.chunk_accumulate_grad(0, 0, lc.LC_FP32, 0) == lc.LC_OK  # n = 0 is a no-op
+    with pytest.raises(lc.LibchunkError):
+        lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE, 0, 8, 8, 4096, 8, 1, 4096, 8, 1, 4096, 8)
+    with pytest.raises(lc.LibchunkError):
+        lc.lc_attention_forward(lc.LC_BF16, 1, 128, 2, 64, 4096, 4096, 4096, 256, 4096, 256, 4096)

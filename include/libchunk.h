@@ -53,7 +53,10 @@ typedef enum lc_status {
   LC_ERR_HIP = -7           /* a HIP runtime call or kernel launch failed        */
 } lc_status;
 
-typedef enum lc_dtype { LC_FP32 = 0, LC_BF16 = 1 } lc_dtype;
+/* Element types. A stage's compute_dtype is LC_FP32 or LC_BF16; LC_FP16
+ * appears only in the per-tensor types of libchunk_ops.h (a bf16 stage keeps
+ * its attention q, k, v in fp16, see lc_stage_desc). */
+typedef enum lc_dtype { LC_FP32 = 0, LC_BF16 = 1, LC_FP16 = 2 } lc_dtype;
 
 /* Piper's PASS dimension: F = forward, B = full backward (Section 4.1). */
 typedef enum lc_pass { LC_PASS_F = 0, LC_PASS_B = 1 } lc_pass;
@@ -67,7 +70,17 @@ typedef enum lc_pass { LC_PASS_F = 0, LC_PASS_B = 1 } lc_pass;
  * else a top-k (k = 2) softmax-routed mixture of SwiGLU experts whose gate
  * weights are renormalised over the selected experts (ties pick the lower
  * expert index). Activations are token-major [micro_batch, seq_len,
- * d_model]; weights are [out, in] row-major. */
+ * d_model]; weights are [out, in] row-major.
+ *
+ * Precision of a bf16 stage: every matrix product takes bf16 operands (the
+ * weights, the normalised activations, the attention output, the SwiGLU
+ * output and every gradient operand) with fp32 accumulation; attention's
+ * q, k, v and softmax probabilities use fp16 operands (values of bounded
+ * range, three more mantissa bits, same matrix-core rate); the residual
+ * stream between and inside layers, the SwiGLU gate/up values kept for the
+ * backward, the residual-stream gradient and all norm inputs are fp32.
+ * X, Y, dY and dX at the stage boundary are bf16. An fp32 stage computes
+ * everything in fp32. */
 typedef struct lc_stage_desc {
   int32_t n_layers;
   int32_t d_model;       /* == n_heads * head_dim */

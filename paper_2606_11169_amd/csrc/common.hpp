@@ -18,6 +18,8 @@ inline lc_status check_launch(const char *what) {
   return e == hipSuccess ? LC_OK : hip_fail(e, what);
 }
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline size_t dtype_size(int dt) { return dt == LC_FP32 ? 4 : 2; }
+inline bool valid_dtype(int dt) { return dt == LC_FP32 || dt == LC_BF16 || dt == LC_FP16; }
 
 #define LC_TRY(expr)                 \
   do {                               \
@@ -26,16 +28,19 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
   } while (0)
 
 // ------------------------------------------------------------------ types
-typedef uint16_t bf16_t;  // storage of a bfloat16 value
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;   // MFMA operand
-typedef __attribute__((ext_vector_type(16))) float f32x16_v;   // 32x32 MFMA accumulator
+typedef uint16_t bf16_t;  // storage of a bfloat16 value (bit-exact paths)
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;     // MFMA operand
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_v;    // MFMA operand
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_v;
+typedef __attribute__((ext_vector_type(4))) _Float16 f16x4_v;
+typedef __attribute__((ext_vector_type(16))) float f32x16_v;     // 32x32 MFMA accumulator
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
 // float -> bf16, round to nearest even; NaN keeps sign and high payload and is
-// made quiet. Written out on the bit pattern so that every caller gets the same
-// rounding on every target.
+// made quiet. Written out on the bit pattern: the bit-exact kernels (AdamW's
+// cast, lc_cast_bf16) use this one.
 __device__ __forceinline__ bf16_t f2bf(float f) {
   uint32_t u = __float_as_uint(f);
   if ((u & 0x7FFFFFFFu) > 0x7F800000u) return bf16_t((u >> 16) | 0x0040u);
@@ -55,6 +60,43 @@ template <typename T> __device__ __forceinline__ void st_elem(T *p, float v);
 template <> __device__ __forceinline__ void st_elem<float>(float *p, float v) { *p = v; }
 template <> __device__ __forceinline__ void st_elem<bf16_t>(bf16_t *p, float v) { *p = f2bf(v); }
 
+// Four consecutive elements of a tensor whose type is known at run time
+// (uniform across the wave): 8 bytes for bf16/fp16 (hardware round-to-nearest-
+// even conversions), 16 bytes for fp32.
+__device__ __forceinline__ void store4_dt(void *base, int64_t idx, int dt, float a, float b,
+                                          float c, float d) {
+  if (dt == LC_FP32) {
+    *reinterpret_cast<float4 *>(static_cast<float *>(base) + idx) = make_float4(a, b, c, d);
+  } else if (dt == LC_BF16) {
+    bf16x4_v v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+    *reinterpret_cast<bf16x4_v *>(static_cast<__bf16 *>(base) + idx) = v;
+  } else {
+    f16x4_v v = {(_Float16)a, (_Float16)b, (_Float16)c, (_Float16)d};
+    *reinterpret_cast<f16x4_v *>(static_cast<_Float16 *>(base) + idx) = v;
+  }
+}
+
+__device__ __forceinline__ float4 load4_dt(const void *base, int64_t idx, int dt) {
+  if (dt == LC_FP32) return *reinterpret_cast<const float4 *>(static_cast<const float *>(base) + idx);
+  if (dt == LC_BF16) {
+    const bf16x4_v v = *reinterpret_cast<const bf16x4_v *>(static_cast<const __bf16 *>(base) + idx);
+    return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+  }
+  const f16x4_v v = *reinterpret_cast<const f16x4_v *>(static_cast<const _Float16 *>(base) + idx);
+  return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+}
+
+// Eight consecutive elements as floats / from floats (16 or 32 bytes).
+__device__ __forceinline__ void load8_dt(const void *base, int64_t idx, int dt, float (&x)[8]) {
+  const float4 a = load4_dt(base, idx, dt), b = load4_dt(base, idx + 4, dt);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ __forceinline__ void store8_dt(void *base, int64_t idx, int dt, const float (&x)[8]) {
+  store4_dt(base, idx, dt, x[0], x[1], x[2], x[3]);
+  store4_dt(base, idx + 4, dt, x[4], x[5], x[6], x[7]);
+}
+
 // logistic sigmoid with the hardware reciprocal (about 1 ulp); used in
 // activation epilogues whose results are rounded to bf16 or checked at 1e-4
 __device__ __forceinline__ float sigmoidf_(float z) {
@@ -73,19 +115,10 @@ inline unsigned ceil_div(size_t a, size_t b) { return unsigned((a + b - 1) / b);
 // ------------------------------------------------------------------ internal launchers
 // Defined in the kernel translation units; used by the stage composer.
 lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s);
-lc_status rmsnorm_fwd_launch(int dtype, int64_t T, int64_t d, const void *x, const void *g,
-                             float eps, void *n, float *rstd, hipStream_t s);
-lc_status rmsnorm_bwd_launch(int dtype, int64_t T, int64_t d, const void *dn, const void *x,
-                             const float *rstd, const void *g, const void *dres, void *dx,
-                             float *dg_accum, void *scratch, size_t scratch_bytes, hipStream_t s);
-lc_status attn_fwd_launch(int dtype, int B, int S, int H, int hd, const void *q, const void *k,
-                          const void *v, int64_t ld_qkv, void *o, int64_t ld_o, float *lse,
-                          hipStream_t s);
-lc_status attn_bwd_launch(int dtype, int B, int S, int H, int hd, const void *q, const void *k,
-                          const void *v, int64_t ld_qkv, const void *o, const void *dout,
-                          int64_t ld_o, const float *lse, void *dq, void *dk, void *dv,
-                          int64_t ld_dqkv, const float *rcos, const float *rsin, void *scratch,
-                          size_t scratch_bytes, hipStream_t s);
+lc_status rmsnorm_fwd_launch(const lc_norm_args &a, hipStream_t s);
+lc_status rmsnorm_bwd_launch(const lc_norm_args &a, hipStream_t s);
+lc_status attn_fwd_launch(const lc_attn_args &a, hipStream_t s);
+lc_status attn_bwd_launch(const lc_attn_args &a, hipStream_t s);
 lc_status accumulate_launch(float *acc, const void *g, int g_dtype, size_t n, hipStream_t s);
 lc_status adam_launch(float *p, float *m, float *v, const void *g, int g_dtype, uint16_t *out,
                       size_t n, const lc_adam_hparams &hp, hipStream_t s);

@@ -48,13 +48,13 @@ lc_status validate_desc(const lc_stage_desc *d) {
   if (d->compute_dtype == LC_BF16) {
     if (d->head_dim != 128)
       return fail(LC_ERR_UNSUPPORTED, "bf16 attention kernels need head_dim == 128");
-    if (d->d_model % 64 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs d_model % 64 == 0");
+    if (d->d_model % 64 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs d_model %% 64 == 0");
     int64_t f = d->n_experts ? d->d_ff_expert : d->d_ff;
-    if (f % 64 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs the FFN width % 64 == 0");
-    if (d->seq_len % 128 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs seq_len % 128 == 0");
+    if (f % 64 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs the FFN width %% 64 == 0");
+    if (d->seq_len % 128 != 0) return fail(LC_ERR_UNSUPPORTED, "bf16 needs seq_len %% 128 == 0");
   } else {
     if (d->head_dim > 128) return fail(LC_ERR_UNSUPPORTED, "fp32 attention needs head_dim <= 128");
-    if (d->d_model % 4 != 0) return fail(LC_ERR_UNSUPPORTED, "fp32 needs d_model % 4 == 0");
+    if (d->d_model % 4 != 0) return fail(LC_ERR_UNSUPPORTED, "fp32 needs d_model %% 4 == 0");
   }
   if (d->n_experts > 64) return fail(LC_ERR_UNSUPPORTED, "at most 64 experts");
   return LC_OK;
@@ -87,12 +87,27 @@ ParamPlan param_plan(const lc_stage_desc &d) {
   return p;
 }
 
+StageTypes stage_types(const lc_stage_desc &d) {
+  StageTypes t;
+  if (d.compute_dtype == LC_BF16) {
+    t.op = LC_BF16;
+    t.att = LC_FP16;
+    t.res = LC_FP32;
+  } else {
+    t.op = t.att = t.res = LC_FP32;
+  }
+  return t;
+}
+
+static size_t bytes_of(int dt) { return dt == LC_FP32 ? 4 : 2; }
+
 lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *out) {
   lc_status st = validate_desc(&d);
   if (st != LC_OK) return st;
   if (max_in_flight <= 0) return fail(LC_ERR_INVALID_ARG, "max_in_flight must be positive");
   StagePlan p{};
-  const size_t es = d.compute_dtype == LC_BF16 ? 2 : 4;
+  p.ty = stage_types(d);
+  const size_t es = bytes_of(p.ty.op), ea = bytes_of(p.ty.att), er = bytes_of(p.ty.res);
   const int64_t T = (int64_t)d.micro_batch * d.seq_len;
   const size_t D = (size_t)d.d_model, H = (size_t)d.n_heads;
   const bool moe = d.n_experts > 0;
@@ -108,17 +123,17 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *o
   // one layer block of the stash
   size_t lo = 0;
   auto take = [&](size_t bytes) { size_t r = lo; lo = align256(lo + bytes); return r; };
-  p.xin = take((size_t)T * D * es);
+  p.xin = take((size_t)T * D * er);
   p.rstd1 = take((size_t)T * 4);
   p.n1 = take((size_t)T * D * es);
-  p.qkv = take((size_t)T * 3 * D * es);
+  p.qkv = take((size_t)T * 3 * D * ea);
   p.o = take((size_t)T * D * es);
   p.lse = take((size_t)T * H * 4);
-  p.h = take((size_t)T * D * es);
+  p.h = take((size_t)T * D * er);
   p.rstd2 = take((size_t)T * 4);
   p.n2 = take((size_t)T * D * es);
-  p.gate = take(R * F * es);
-  p.up = take(R * F * es);
+  p.gate = take(R * F * er);
+  p.up = take(R * F * er);
   p.act = take(R * F * es);
   if (moe) {
     const size_t E = (size_t)d.n_experts;
@@ -136,13 +151,15 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *o
   off = align256(off + p.slot_bytes * (size_t)max_in_flight);
 
   auto stake = [&](size_t bytes) { size_t r = off; off = align256(off + bytes); return r; };
-  p.s_dy0 = stake((size_t)T * D * es);
-  p.s_dy1 = stake((size_t)T * D * es);
+  p.s_dy0 = stake((size_t)T * D * er);
+  p.s_dy1 = stake((size_t)T * D * er);
+  p.s_dy16 = stake((size_t)T * D * es);
   p.s_da = stake(R * 2 * F * es);
-  p.s_dn = stake((size_t)T * D * es);
+  p.s_dn = stake((size_t)T * D * er);
   p.s_do = stake((size_t)T * D * es);
   p.s_dqkv = stake((size_t)T * 3 * D * es);
-  p.s_dh = stake((size_t)T * D * es);
+  p.s_dh = stake((size_t)T * D * er);
+  p.s_dh16 = stake((size_t)T * D * es);
   p.s_attn_bytes = attn_scratch_size(d.micro_batch, d.seq_len, d.n_heads);
   p.s_attn = stake(p.s_attn_bytes);
   p.s_norm_bytes = rmsnorm_scratch_size(T, d.d_model);

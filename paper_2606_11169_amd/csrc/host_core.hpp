@@ -10,7 +10,7 @@
 
 namespace lc {
 
-lc_status fail(lc_status st, const char *fmt, ...);
+lc_status fail(lc_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 
 // Rows per block of the RMSNorm backward's gain-gradient partial sums.
 constexpr int kNormRowsPerBlock = 32;
@@ -33,8 +33,19 @@ ParamPlan param_plan(const lc_stage_desc &d);
 
 // Where every stashed activation and scratch buffer lives in the caller's
 // workspace. Offsets are bytes from the workspace base, 256-byte aligned.
+// Element types of a stage's internal tensors (see lc_stage_desc's precision
+// note): GEMM operands in the compute dtype, attention q/k/v in fp16 for bf16
+// stages, residual stream / gate-up stash / norm inputs in fp32.
+struct StageTypes {
+  int op;    // GEMM operand activations and gradients (n1, o, n2, act, dgu, dqkv, ...)
+  int att;   // attention q, k, v
+  int res;   // residual stream, its gradient, gate/up stash, norm-input gradients
+};
+StageTypes stage_types(const lc_stage_desc &d);
+
 struct StagePlan {
-  size_t elem;          // bytes per activation element (2 or 4)
+  size_t elem;          // bytes per GEMM-operand element (2 or 4)
+  StageTypes ty;
   int64_t T;            // tokens per microbatch
   // RoPE table: cos then sin, fp32 [seq_len, head_dim/2]
   size_t rope_cos, rope_sin;
@@ -45,12 +56,14 @@ struct StagePlan {
   // MoE per-layer extras (0 when dense)
   size_t moe_sel, moe_w, moe_perm, moe_rowpos, moe_off, moe_xp, moe_eo;
   // backward scratch (one set, reused by every microbatch)
-  size_t s_dy0, s_dy1;  // residual-stream gradient ping-pong [T, d]
+  size_t s_dy0, s_dy1;  // residual-stream gradient ping-pong [T, d] (res type)
+  size_t s_dy16;        // operand copy of the current layer's dy [T, d] (op type)
   size_t s_da;          // dgate|dup [T, 2f] (or MoE rows [2T, 2fe])
-  size_t s_dn;          // [T, d] gradient at a norm output
+  size_t s_dn;          // [T, d] gradient at a norm output (res type)
   size_t s_do;          // [T, d] gradient at attention output
   size_t s_dqkv;        // [T, 3d]
-  size_t s_dh;          // [T, d]
+  size_t s_dh;          // [T, d] (res type)
+  size_t s_dh16;        // operand copy of dh [T, d] (op type)
   size_t s_attn, s_attn_bytes;  // attention backward scratch
   size_t s_norm, s_norm_bytes;  // RMSNorm backward scratch
   size_t s_moe;         // MoE backward extras

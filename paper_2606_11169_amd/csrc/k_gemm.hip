@@ -23,6 +23,8 @@
 // runs of four consecutive columns n = 8g + 4(l / 32) + e: epilogues store 8 or
 // 16 contiguous bytes per lane, and the column pairs (c, c + 64) that RoPE and
 // SwiGLU combine sit in the same lane (blocks j and j + 2 of a 128-wide wave).
+// Output, residual and gate/up element types are run-time values (uniform
+// branches in the epilogue only).
 #include "common.hpp"
 
 namespace lc {
@@ -38,7 +40,7 @@ struct GemmP {
   const bf16_t *A;
   const bf16_t *B;
   void *C;
-  const bf16_t *R;
+  const void *R;
   void *aux0;
   void *aux1;
   const float *rcos;
@@ -47,6 +49,7 @@ struct GemmP {
   int M, N, K;  // N: output columns (SwiGLU: gate/up width)
   int tiles_m, tiles_n;
   int rope_seq, rope_cols;
+  int c_dt, r_dt, aux_dt;
 };
 
 __device__ __forceinline__ int lds_off(int row, int chunk) {
@@ -142,19 +145,6 @@ struct TileLoader {
     }
   }
 };
-
-__device__ __forceinline__ void store_bf16x4(bf16_t *p, float a, float b, float c, float d) {
-  uint2 w;
-  w.x = pack_bf2(a, b);
-  w.y = pack_bf2(c, d);
-  *reinterpret_cast<uint2 *>(p) = w;
-}
-
-__device__ __forceinline__ float4 load_bf16x4(const bf16_t *p) {
-  const uint2 w = *reinterpret_cast<const uint2 *>(p);
-  return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u),
-                     __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xFFFF0000u));
-}
 
 template <bool A_K, bool B_K, int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
@@ -257,10 +247,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
             a[e] = gt[e] * sigmoidf_(gt[e]) * up[e];
           }
           const int64_t oa = (int64_t)m * p.ld_aux + n;
-          store_bf16x4(reinterpret_cast<bf16_t *>(p.aux0) + oa, gt[0], gt[1], gt[2], gt[3]);
-          store_bf16x4(reinterpret_cast<bf16_t *>(p.aux1) + oa, up[0], up[1], up[2], up[3]);
-          store_bf16x4(reinterpret_cast<bf16_t *>(p.C) + (int64_t)m * p.ldc + n, a[0], a[1], a[2],
-                       a[3]);
+          store4_dt(p.aux0, oa, p.aux_dt, gt[0], gt[1], gt[2], gt[3]);
+          store4_dt(p.aux1, oa, p.aux_dt, up[0], up[1], up[2], up[3]);
+          store4_dt(p.C, (int64_t)m * p.ldc + n, p.c_dt, a[0], a[1], a[2], a[3]);
         }
       }
     } else if constexpr (EPI == LC_EPI_ROPE) {
@@ -291,9 +280,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
               x2[e] = a * sv[e] + b * cv[e];
             }
           }
-          bf16_t *row = reinterpret_cast<bf16_t *>(p.C) + (int64_t)m * p.ldc + hbase;
-          store_bf16x4(row + c, x1[0], x1[1], x1[2], x1[3]);
-          store_bf16x4(row + c + 64, x2[0], x2[1], x2[2], x2[3]);
+          const int64_t row = (int64_t)m * p.ldc + hbase;
+          store4_dt(p.C, row + c, p.c_dt, x1[0], x1[1], x1[2], x1[3]);
+          store4_dt(p.C, row + c + 64, p.c_dt, x2[0], x2[1], x2[2], x2[3]);
         }
       }
     } else {
@@ -305,18 +294,14 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
           if (n >= p.N) continue;
           float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
           float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+          const int64_t oc = (int64_t)m * p.ldc + n;
           if constexpr (EPI == LC_EPI_STORE) {
-            store_bf16x4(reinterpret_cast<bf16_t *>(p.C) + (int64_t)m * p.ldc + n, v0, v1, v2, v3);
+            store4_dt(p.C, oc, p.c_dt, v0, v1, v2, v3);
           } else if constexpr (EPI == LC_EPI_RESIDUAL) {
-            const float4 r = load_bf16x4(p.R + (int64_t)m * p.ldr + n);
-            store_bf16x4(reinterpret_cast<bf16_t *>(p.C) + (int64_t)m * p.ldc + n, r.x + v0,
-                         r.y + v1, r.z + v2, r.w + v3);
-          } else if constexpr (EPI == LC_EPI_STORE_F32) {
-            *reinterpret_cast<float4 *>(reinterpret_cast<float *>(p.C) + (int64_t)m * p.ldc + n) =
-                make_float4(v0, v1, v2, v3);
+            const float4 r = load4_dt(p.R, (int64_t)m * p.ldr + n, p.r_dt);
+            store4_dt(p.C, oc, p.c_dt, r.x + v0, r.y + v1, r.z + v2, r.w + v3);
           } else if constexpr (EPI == LC_EPI_ACCUM_F32) {
-            float4 *cp =
-                reinterpret_cast<float4 *>(reinterpret_cast<float *>(p.C) + (int64_t)m * p.ldc + n);
+            float4 *cp = reinterpret_cast<float4 *>(static_cast<float *>(p.C) + oc);
             float4 c = *cp;
             c.x += v0;
             c.y += v1;
@@ -325,8 +310,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
             *cp = c;
           } else if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
             const int64_t oa = (int64_t)m * p.ld_aux + n;
-            const float4 gt = load_bf16x4(reinterpret_cast<const bf16_t *>(p.aux0) + oa);
-            const float4 up = load_bf16x4(reinterpret_cast<const bf16_t *>(p.aux1) + oa);
+            const float4 gt = load4_dt(p.aux0, oa, p.aux_dt);
+            const float4 up = load4_dt(p.aux1, oa, p.aux_dt);
             const float gv[4] = {gt.x, gt.y, gt.z, gt.w};
             const float uv[4] = {up.x, up.y, up.z, up.w};
             const float dv[4] = {v0, v1, v2, v3};
@@ -337,9 +322,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
               dg[e] = dv[e] * uv[e] * s * (1.0f + gv[e] * (1.0f - s));
               du[e] = dv[e] * gv[e] * s;
             }
-            bf16_t *row = reinterpret_cast<bf16_t *>(p.C) + (int64_t)m * p.ldc;
-            store_bf16x4(row + n, dg[0], dg[1], dg[2], dg[3]);
-            store_bf16x4(row + p.N + n, du[0], du[1], du[2], du[3]);
+            store4_dt(p.C, oc, p.c_dt, dg[0], dg[1], dg[2], dg[3]);
+            store4_dt(p.C, oc + p.N, p.c_dt, du[0], du[1], du[2], du[3]);
           }
         }
       }
@@ -366,6 +350,11 @@ lc_status launch_t(const GemmP &p, hipStream_t s) {
 
 lc_status gemm_f32_launch(const lc_gemm_args &a, hipStream_t s);  // k_gemm_f32.hip
 
+// the epilogue types this call uses (STORE_F32 and ACCUM_F32 imply fp32 C)
+static int c_type(const lc_gemm_args &a) {
+  return (a.epilogue == LC_EPI_STORE_F32 || a.epilogue == LC_EPI_ACCUM_F32) ? LC_FP32 : a.c_dtype;
+}
+
 static lc_status check_gemm_args(const lc_gemm_args &a) {
   if (a.M <= 0 || a.N <= 0 || a.K <= 0) return fail(LC_ERR_INVALID_ARG, "gemm: M, N, K must be > 0");
   if (a.M > INT32_MAX / 2 || a.N > INT32_MAX / 4 || a.K > INT32_MAX / 2)
@@ -375,18 +364,21 @@ static lc_status check_gemm_args(const lc_gemm_args &a) {
     return fail(LC_ERR_INVALID_ARG, "gemm: operands must be 16-byte aligned");
   if (a.epilogue < LC_EPI_STORE || a.epilogue > LC_EPI_SWIGLU_BWD)
     return fail(LC_ERR_INVALID_ARG, "gemm: unknown epilogue %d", a.epilogue);
-  if (a.lda % 8 || a.ldb % 8 || a.ldc % 8) return fail(LC_ERR_INVALID_ARG, "gemm: ld % 8 != 0");
+  if (!valid_dtype(c_type(a))) return fail(LC_ERR_INVALID_ARG, "gemm: unknown c_dtype");
+  const bool bf = a.dtype == LC_BF16;
+  if (bf && (a.lda % 8 || a.ldb % 8 || a.ldc % 8))
+    return fail(LC_ERR_INVALID_ARG, "gemm: ld %% 8 != 0");
   const int64_t acols = a.a_kmajor ? a.K : a.M;
   const int64_t brows = a.epilogue == LC_EPI_SWIGLU ? 2 * a.N : a.N;
   const int64_t bcols = a.b_kmajor ? a.K : brows;
   if (a.lda < acols || a.ldb < bcols) return fail(LC_ERR_INVALID_ARG, "gemm: ld too small");
   if (a.epilogue == LC_EPI_RESIDUAL) {
-    if (!a.R || !aligned16(a.R) || a.ldr % 8 || a.ldr < a.N)
+    if (!a.R || !aligned16(a.R) || (bf && a.ldr % 8) || a.ldr < a.N || !valid_dtype(a.r_dtype))
       return fail(LC_ERR_INVALID_ARG, "gemm: bad residual operand");
   }
   if (a.epilogue == LC_EPI_SWIGLU || a.epilogue == LC_EPI_SWIGLU_BWD) {
-    if (!a.aux0 || !a.aux1 || !aligned16(a.aux0) || !aligned16(a.aux1) || a.ld_aux % 8 ||
-        a.ld_aux < a.N)
+    if (!a.aux0 || !a.aux1 || !aligned16(a.aux0) || !aligned16(a.aux1) ||
+        (bf && a.ld_aux % 8) || a.ld_aux < a.N || !valid_dtype(a.aux_dtype))
       return fail(LC_ERR_INVALID_ARG, "gemm: bad gate/up operands");
     if (a.epilogue == LC_EPI_SWIGLU_BWD && a.ldc < 2 * a.N)
       return fail(LC_ERR_INVALID_ARG, "gemm: ldc < 2N for SWIGLU_BWD");
@@ -403,24 +395,30 @@ static lc_status check_gemm_args(const lc_gemm_args &a) {
 
 lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
   LC_TRY(check_gemm_args(a));
-  if (a.dtype == LC_FP32) return gemm_f32_launch(a, s);
-  if (a.dtype != LC_BF16) return fail(LC_ERR_INVALID_ARG, "gemm: unknown dtype");
+  if (a.dtype == LC_FP32) {
+    if (c_type(a) != LC_FP32 || (a.epilogue == LC_EPI_RESIDUAL && a.r_dtype != LC_FP32) ||
+        ((a.epilogue == LC_EPI_SWIGLU || a.epilogue == LC_EPI_SWIGLU_BWD) &&
+         a.aux_dtype != LC_FP32))
+      return fail(LC_ERR_UNSUPPORTED, "gemm fp32: every tensor must be fp32");
+    return gemm_f32_launch(a, s);
+  }
+  if (a.dtype != LC_BF16) return fail(LC_ERR_INVALID_ARG, "gemm: A/B dtype must be fp32 or bf16");
   // layout limits of the bf16 kernel: 16-byte rows along every contiguous extent
-  if (a.N % 8) return fail(LC_ERR_UNSUPPORTED, "gemm bf16: N % 8 != 0");
-  if ((a.a_kmajor || a.b_kmajor) && a.K % 8) return fail(LC_ERR_UNSUPPORTED, "gemm bf16: K % 8");
-  if (!a.a_kmajor && a.M % 8) return fail(LC_ERR_UNSUPPORTED, "gemm bf16: M % 8 (A not k-major)");
+  if (a.N % 8) return fail(LC_ERR_UNSUPPORTED, "gemm bf16: N %% 8 != 0");
+  if ((a.a_kmajor || a.b_kmajor) && a.K % 8) return fail(LC_ERR_UNSUPPORTED, "gemm bf16: K %% 8 != 0");
+  if (!a.a_kmajor && a.M % 8) return fail(LC_ERR_UNSUPPORTED, "gemm bf16: M %% 8 != 0 (A not k-major)");
   if (a.epilogue == LC_EPI_ROPE && a.head_dim != 128)
     return fail(LC_ERR_UNSUPPORTED, "gemm bf16: RoPE epilogue needs head_dim 128");
   if (a.epilogue == LC_EPI_SWIGLU && (a.N % 64 || !a.b_kmajor))
-    return fail(LC_ERR_UNSUPPORTED, "gemm bf16: SwiGLU needs N % 64 == 0 and k-major B");
-  if (a.epilogue == LC_EPI_ROPE && !aligned16(a.rope_cos))
+    return fail(LC_ERR_UNSUPPORTED, "gemm bf16: SwiGLU needs N %% 64 == 0 and k-major B");
+  if (a.epilogue == LC_EPI_ROPE && (!aligned16(a.rope_cos) || !aligned16(a.rope_sin)))
     return fail(LC_ERR_INVALID_ARG, "gemm: RoPE tables must be 16-byte aligned");
 
   GemmP p{};
   p.A = static_cast<const bf16_t *>(a.A);
   p.B = static_cast<const bf16_t *>(a.B);
   p.C = a.C;
-  p.R = static_cast<const bf16_t *>(a.R);
+  p.R = a.R;
   p.aux0 = a.aux0;
   p.aux1 = a.aux1;
   p.rcos = a.rope_cos;
@@ -438,18 +436,17 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
                                           : (int)((a.N + BN - 1) / BN);
   p.rope_seq = a.rope_seq;
   p.rope_cols = a.rope_cols;
+  p.c_dt = c_type(a);
+  p.r_dt = a.r_dtype;
+  p.aux_dt = a.aux_dtype;
 
   const bool ak = a.a_kmajor != 0, bk = a.b_kmajor != 0;
   switch (a.epilogue) {
     case LC_EPI_STORE:
+    case LC_EPI_STORE_F32:
       if (ak && bk) return launch_t<true, true, LC_EPI_STORE>(p, s);
       if (ak && !bk) return launch_t<true, false, LC_EPI_STORE>(p, s);
       if (!ak && !bk) return launch_t<false, false, LC_EPI_STORE>(p, s);
-      break;
-    case LC_EPI_STORE_F32:
-      if (ak && bk) return launch_t<true, true, LC_EPI_STORE_F32>(p, s);
-      if (ak && !bk) return launch_t<true, false, LC_EPI_STORE_F32>(p, s);
-      if (!ak && !bk) return launch_t<false, false, LC_EPI_STORE_F32>(p, s);
       break;
     case LC_EPI_ACCUM_F32:
       if (ak && bk) return launch_t<true, true, LC_EPI_ACCUM_F32>(p, s);

@@ -10,8 +10,9 @@
 // (two float4 per fp32 stream, one uint4 per bf16 stream) in a grid-stride
 // loop, and a scalar loop covers the tail. This file is compiled with
 // -ffp-contract=off: every multiply and add below is its own IEEE fp32
-// operation, and sqrt and divide are the correctly rounded ones, so the
-// results are bitwise those of the written-out operation sequence.
+// operation, the divide is the correctly rounded one and the square root is
+// made correctly rounded by sqrt_rn, so the results are bitwise those of the
+// written-out operation sequence.
 #include "common.hpp"
 
 #include <math.h>
@@ -71,6 +72,28 @@ struct AdamS {
   float c_wd, b1, b2, omb1, omb2, step_size, bc2s, eps;
 };
 
+// Correctly rounded fp32 square root. The hardware estimate s (v_sqrt_f32,
+// within 1 ulp) is compared with its two neighbours s-, s+ through exact fma
+// residuals: sqrt(x) lies below the midpoint of (s-, s) iff x - s- * s <= 0,
+// and above the midpoint of (s, s+) iff x - s+ * s > 0 (x - s+- * s is an
+// integer multiple of ulp(s)^2, so it can never fall strictly between 0 and
+// the midpoint gap). Inputs below 2^-64 are scaled by 2^64 first so that the
+// residuals stay normal; the result is scaled back by 2^-32 exactly.
+__device__ __forceinline__ float sqrt_rn(float x) {
+  const bool tiny = x < 0x1.0p-64f;
+  const float xs = tiny ? x * 0x1.0p+64f : x;
+  float s = __builtin_amdgcn_sqrtf(xs);
+  if (xs > 0.0f && xs < INFINITY) {
+    const float dn = __int_as_float(__float_as_int(s) - 1);
+    const float up = __int_as_float(__float_as_int(s) + 1);
+    const float rdn = __builtin_fmaf(-dn, s, xs);
+    const float rup = __builtin_fmaf(-up, s, xs);
+    if (rdn <= 0.0f) s = dn;
+    if (rup > 0.0f) s = up;
+  }
+  return tiny ? s * 0x1.0p-32f : s;
+}
+
 __device__ __forceinline__ void adam_elem(float &p, float &m, float &v, float g, const AdamS &s) {
   p = p * s.c_wd;
   const float m1 = s.b1 * m;
@@ -80,7 +103,7 @@ __device__ __forceinline__ void adam_elem(float &p, float &m, float &v, float g,
   const float v1 = s.b2 * v;
   const float v2 = s.omb2 * gg;
   v = v1 + v2;
-  const float den = __fadd_rn(__fdiv_rn(__fsqrt_rn(v), s.bc2s), s.eps);
+  const float den = __fadd_rn(__fdiv_rn(sqrt_rn(v), s.bc2s), s.eps);
   const float upd = s.step_size * __fdiv_rn(m, den);
   p = p - upd;
 }

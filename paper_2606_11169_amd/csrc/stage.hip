@@ -11,6 +11,11 @@
 // its launches are enqueued. Gradients of every backward are added into the
 // bucket's flat fp32 buffer (Section 4.3.2; accumulated across microbatches,
 // Section 6.2).
+//
+// Tensor element types follow StageTypes: matrix-product operands in the
+// compute dtype, attention q/k/v in fp16 for a bf16 stage, and the residual
+// stream (inside and between layers), its gradient, the gate/up values kept
+// for the backward and every norm input in fp32.
 #include "common.hpp"
 
 #include <math.h>
@@ -41,7 +46,6 @@ namespace {
 
 struct LayerBufs {
   char *base;
-  const StagePlan *p;
   void *at(size_t off) const { return base + off; }
 };
 
@@ -58,9 +62,19 @@ lc_gemm_args gemm_base(int dtype, int epi, int64_t M, int64_t N, int64_t K) {
   memset(&a, 0, sizeof a);
   a.dtype = dtype;
   a.epilogue = epi;
+  a.c_dtype = dtype;
   a.M = M;
   a.N = N;
   a.K = K;
+  return a;
+}
+
+lc_norm_args norm_base(int64_t T, int64_t d, float eps) {
+  lc_norm_args a;
+  memset(&a, 0, sizeof a);
+  a.T = T;
+  a.d = d;
+  a.eps = eps;
   return a;
 }
 
@@ -70,7 +84,6 @@ static LayerBufs layer_bufs(lc_stage *st, int slot, int l) {
   LayerBufs b;
   b.base = st->ws + st->plan.slot0 + (size_t)slot * st->plan.slot_bytes +
            (size_t)l * st->plan.layer_bytes;
-  b.p = &st->plan;
   return b;
 }
 
@@ -80,54 +93,69 @@ static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const voi
   const StagePlan &P = st->plan;
   const ParamPlan &pp = st->pp;
   const int dt = d.compute_dtype;
+  const StageTypes ty = P.ty;
   const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const size_t ea = dtype_size(ty.att);
   const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
   const float *rs = reinterpret_cast<const float *>(st->ws + P.rope_sin);
   for (int l = 0; l < d.n_layers; ++l) {
     const LayerBufs L = layer_bufs(st, slot, l);
     const W w{static_cast<const char *>(pb->w) + (size_t)l * pp.per_layer * P.elem, nullptr, P.elem};
-    const void *xin = l == 0 ? x : L.at(P.xin);
-    void *out = l == d.n_layers - 1 ? y : layer_bufs(st, slot, l + 1).at(P.xin);
+    const bool first = l == 0, last = l == d.n_layers - 1;
+    const void *xin = first ? x : L.at(P.xin);
+    const int x_dt = first ? dt : ty.res;
+    void *out = last ? y : layer_bufs(st, slot, l + 1).at(P.xin);
     // n1 = RMSNorm(x; g1)
-    LC_TRY(rmsnorm_fwd_launch(dt, T, D, xin, w.wp(pp.g1), d.rms_eps, L.at(P.n1),
-                              static_cast<float *>(L.at(P.rstd1)), s));
+    lc_norm_args na = norm_base(T, D, d.rms_eps);
+    na.x = xin; na.x_dtype = x_dt;
+    na.g = w.wp(pp.g1); na.w_dtype = dt;
+    na.n = L.at(P.n1); na.out_dtype = ty.op;
+    na.rstd = static_cast<float *>(L.at(P.rstd1));
+    LC_TRY(rmsnorm_fwd_launch(na, s));
     // [q|k|v] = n1 [Wq;Wk;Wv]^T, RoPE on q and k
     lc_gemm_args a = gemm_base(dt, LC_EPI_ROPE, T, 3 * D, D);
     a.A = L.at(P.n1); a.lda = D; a.a_kmajor = 1;
     a.B = w.wp(pp.wq); a.ldb = D; a.b_kmajor = 1;
-    a.C = L.at(P.qkv); a.ldc = 3 * D;
+    a.C = L.at(P.qkv); a.ldc = 3 * D; a.c_dtype = ty.att;
     a.rope_cos = rc; a.rope_sin = rs; a.rope_seq = d.seq_len; a.rope_cols = (int)(2 * D);
     a.head_dim = d.head_dim;
     LC_TRY(gemm_launch(a, s));
     // o = causal attention
     char *qkv = static_cast<char *>(L.at(P.qkv));
-    LC_TRY(attn_fwd_launch(dt, d.micro_batch, d.seq_len, d.n_heads, d.head_dim, qkv,
-                           qkv + D * P.elem, qkv + 2 * D * P.elem, 3 * D, L.at(P.o), D,
-                           static_cast<float *>(L.at(P.lse)), s));
+    lc_attn_args at;
+    memset(&at, 0, sizeof at);
+    at.dtype = ty.att; at.o_dtype = ty.op;
+    at.B = d.micro_batch; at.S = d.seq_len; at.H = d.n_heads; at.hd = d.head_dim;
+    at.q = qkv; at.k = qkv + D * ea; at.v = qkv + 2 * D * ea; at.ld_qkv = 3 * D;
+    at.o = L.at(P.o); at.ld_o = D; at.lse = static_cast<float *>(L.at(P.lse));
+    LC_TRY(attn_fwd_launch(at, s));
     // h = x + o Wo^T
     a = gemm_base(dt, LC_EPI_RESIDUAL, T, D, D);
     a.A = L.at(P.o); a.lda = D; a.a_kmajor = 1;
     a.B = w.wp(pp.wo); a.ldb = D; a.b_kmajor = 1;
-    a.C = L.at(P.h); a.ldc = D;
-    a.R = xin; a.ldr = D;
+    a.C = L.at(P.h); a.ldc = D; a.c_dtype = ty.res;
+    a.R = xin; a.ldr = D; a.r_dtype = x_dt;
     LC_TRY(gemm_launch(a, s));
     // n2 = RMSNorm(h; g2)
-    LC_TRY(rmsnorm_fwd_launch(dt, T, D, L.at(P.h), w.wp(pp.g2), d.rms_eps, L.at(P.n2),
-                              static_cast<float *>(L.at(P.rstd2)), s));
+    na.x = L.at(P.h); na.x_dtype = ty.res;
+    na.g = w.wp(pp.g2);
+    na.n = L.at(P.n2);
+    na.rstd = static_cast<float *>(L.at(P.rstd2));
+    LC_TRY(rmsnorm_fwd_launch(na, s));
     if (d.n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
     // gate, up = n2 W1^T, n2 W3^T; act = silu(gate) * up
     a = gemm_base(dt, LC_EPI_SWIGLU, T, F, D);
     a.A = L.at(P.n2); a.lda = D; a.a_kmajor = 1;
     a.B = w.wp(pp.w1); a.ldb = D; a.b_kmajor = 1;
-    a.C = L.at(P.act); a.ldc = F;
-    a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = F;
+    a.C = L.at(P.act); a.ldc = F; a.c_dtype = ty.op;
+    a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = F; a.aux_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // y = h + act W2^T
     a = gemm_base(dt, LC_EPI_RESIDUAL, T, D, F);
     a.A = L.at(P.act); a.lda = F; a.a_kmajor = 1;
     a.B = w.wp(pp.w2); a.ldb = F; a.b_kmajor = 1;
-    a.C = out; a.ldc = D;
-    a.R = L.at(P.h); a.ldr = D;
+    a.C = out; a.ldc = D; a.c_dtype = last ? dt : ty.res;
+    a.R = L.at(P.h); a.ldr = D; a.r_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
   }
   return LC_OK;
@@ -139,30 +167,38 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
   const StagePlan &P = st->plan;
   const ParamPlan &pp = st->pp;
   const int dt = d.compute_dtype;
+  const StageTypes ty = P.ty;
+  const bool copies = ty.op != ty.res;  // bf16 operand copies of fp32 gradients
   const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const size_t ea = dtype_size(ty.att), es = P.elem;
   const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
   const float *rs = reinterpret_cast<const float *>(st->ws + P.rope_sin);
   char *ws = st->ws;
-  const void *dy = dy_in;
+  // gradient flowing into the current layer: residual version and operand version
+  const void *dy_res = dy_in, *dy_op = dy_in;
+  int dy_dt = dt;
   for (int l = d.n_layers - 1; l >= 0; --l) {
     const LayerBufs L = layer_bufs(st, slot, l);
     const size_t lw = (size_t)l * pp.per_layer;
     const W w{static_cast<const char *>(pb->w) + lw * P.elem, pb->grad + lw, P.elem};
-    const void *xin = l == 0 ? x0 : L.at(P.xin);
-    void *dx = l == 0 ? dx_out : ws + ((d.n_layers - 1 - l) % 2 == 0 ? P.s_dy0 : P.s_dy1);
+    const bool first = l == 0;
+    const void *xin = first ? x0 : L.at(P.xin);
+    const int x_dt = first ? dt : ty.res;
+    void *dx = first ? dx_out : ws + ((d.n_layers - 1 - l) % 2 == 0 ? P.s_dy0 : P.s_dy1);
     void *da = ws + P.s_da, *dn = ws + P.s_dn, *dh = ws + P.s_dh, *dO = ws + P.s_do;
+    void *dh_op = copies ? ws + P.s_dh16 : dh;
     char *dqkv = ws + P.s_dqkv;
     if (d.n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
     // [dgate | dup] = SwiGLU'(dy W2)
     lc_gemm_args a = gemm_base(dt, LC_EPI_SWIGLU_BWD, T, F, D);
-    a.A = dy; a.lda = D; a.a_kmajor = 1;
+    a.A = dy_op; a.lda = D; a.a_kmajor = 1;
     a.B = w.wp(pp.w2); a.ldb = F; a.b_kmajor = 0;
-    a.C = da; a.ldc = 2 * F;
-    a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = F;
+    a.C = da; a.ldc = 2 * F; a.c_dtype = ty.op;
+    a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = F; a.aux_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // G[W2] += dy^T act
     a = gemm_base(dt, LC_EPI_ACCUM_F32, D, F, T);
-    a.A = dy; a.lda = D; a.a_kmajor = 0;
+    a.A = dy_op; a.lda = D; a.a_kmajor = 0;
     a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
     a.C = w.gp(pp.w2); a.ldc = F;
     LC_TRY(gemm_launch(a, s));
@@ -170,7 +206,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a = gemm_base(dt, LC_EPI_STORE, T, D, 2 * F);
     a.A = da; a.lda = 2 * F; a.a_kmajor = 1;
     a.B = w.wp(pp.w1); a.ldb = D; a.b_kmajor = 0;
-    a.C = dn; a.ldc = D;
+    a.C = dn; a.ldc = D; a.c_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // G[W1; W3] += [dgate | dup]^T n2
     a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * F, D, T);
@@ -179,31 +215,47 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a.C = w.gp(pp.w1); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
     // dh = dy + RMSNorm2'(dn2); G[g2] += ...
-    LC_TRY(rmsnorm_bwd_launch(dt, T, D, dn, L.at(P.h), static_cast<const float *>(L.at(P.rstd2)),
-                              w.wp(pp.g2), dy, dh, w.gp(pp.g2), ws + P.s_norm, P.s_norm_bytes, s));
+    lc_norm_args nb = norm_base(T, D, d.rms_eps);
+    nb.dn = dn; nb.dn_dtype = ty.res;
+    nb.x = L.at(P.h); nb.x_dtype = ty.res;
+    nb.rstd = static_cast<float *>(L.at(P.rstd2));
+    nb.g = w.wp(pp.g2); nb.w_dtype = dt;
+    nb.dres = dy_res; nb.dres_dtype = dy_dt;
+    nb.dx = dh; nb.out_dtype = ty.res;
+    nb.dx_copy = copies ? dh_op : nullptr;
+    nb.dg_accum = w.gp(pp.g2);
+    nb.scratch = ws + P.s_norm; nb.scratch_bytes = P.s_norm_bytes;
+    LC_TRY(rmsnorm_bwd_launch(nb, s));
     // do = dh Wo
     a = gemm_base(dt, LC_EPI_STORE, T, D, D);
-    a.A = dh; a.lda = D; a.a_kmajor = 1;
+    a.A = dh_op; a.lda = D; a.a_kmajor = 1;
     a.B = w.wp(pp.wo); a.ldb = D; a.b_kmajor = 0;
-    a.C = dO; a.ldc = D;
+    a.C = dO; a.ldc = D; a.c_dtype = ty.op;
     LC_TRY(gemm_launch(a, s));
     // G[Wo] += dh^T o
     a = gemm_base(dt, LC_EPI_ACCUM_F32, D, D, T);
-    a.A = dh; a.lda = D; a.a_kmajor = 0;
+    a.A = dh_op; a.lda = D; a.a_kmajor = 0;
     a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.wo); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
     // dq, dk, dv (dq, dk rotated back)
     char *qkv = static_cast<char *>(L.at(P.qkv));
-    LC_TRY(attn_bwd_launch(dt, d.micro_batch, d.seq_len, d.n_heads, d.head_dim, qkv,
-                           qkv + D * P.elem, qkv + 2 * D * P.elem, 3 * D, L.at(P.o), dO, D,
-                           static_cast<const float *>(L.at(P.lse)), dqkv, dqkv + D * P.elem,
-                           dqkv + 2 * D * P.elem, 3 * D, rc, rs, ws + P.s_attn, P.s_attn_bytes, s));
+    lc_attn_args at;
+    memset(&at, 0, sizeof at);
+    at.dtype = ty.att; at.o_dtype = ty.op;
+    at.B = d.micro_batch; at.S = d.seq_len; at.H = d.n_heads; at.hd = d.head_dim;
+    at.q = qkv; at.k = qkv + D * ea; at.v = qkv + 2 * D * ea; at.ld_qkv = 3 * D;
+    at.o = L.at(P.o); at.ld_o = D; at.lse = static_cast<float *>(L.at(P.lse));
+    at.dout = dO;
+    at.dq = dqkv; at.dk = dqkv + D * es; at.dv = dqkv + 2 * D * es; at.ld_dqkv = 3 * D;
+    at.rope_cos = rc; at.rope_sin = rs;
+    at.scratch = ws + P.s_attn; at.scratch_bytes = P.s_attn_bytes;
+    LC_TRY(attn_bwd_launch(at, s));
     // dn1 = [dq|dk|dv] [Wq;Wk;Wv]
     a = gemm_base(dt, LC_EPI_STORE, T, D, 3 * D);
     a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 1;
     a.B = w.wp(pp.wq); a.ldb = D; a.b_kmajor = 0;
-    a.C = dn; a.ldc = D;
+    a.C = dn; a.ldc = D; a.c_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
     a = gemm_base(dt, LC_EPI_ACCUM_F32, 3 * D, D, T);
@@ -212,9 +264,18 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a.C = w.gp(pp.wq); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
     // dx = dh + RMSNorm1'(dn1); G[g1] += ...
-    LC_TRY(rmsnorm_bwd_launch(dt, T, D, dn, xin, static_cast<const float *>(L.at(P.rstd1)),
-                              w.wp(pp.g1), dh, dx, w.gp(pp.g1), ws + P.s_norm, P.s_norm_bytes, s));
-    dy = dx;
+    nb.dn = dn; nb.dn_dtype = ty.res;
+    nb.x = xin; nb.x_dtype = x_dt;
+    nb.rstd = static_cast<float *>(L.at(P.rstd1));
+    nb.g = w.wp(pp.g1);
+    nb.dres = dh; nb.dres_dtype = ty.res;
+    nb.dx = dx; nb.out_dtype = first ? dt : ty.res;
+    nb.dx_copy = (copies && !first) ? ws + P.s_dy16 : nullptr;
+    nb.dg_accum = w.gp(pp.g1);
+    LC_TRY(rmsnorm_bwd_launch(nb, s));
+    dy_res = dx;
+    dy_op = copies ? ws + P.s_dy16 : dx;
+    dy_dt = ty.res;
   }
   return LC_OK;
 }

@@ -30,7 +30,7 @@ LC_ERR_HIP = -7
 STATUS_NAMES = {0: "OK", -1: "INVALID_ARG", -2: "UNSUPPORTED", -3: "BAD_ORDER",
                 -4: "STASH_FULL", -5: "STATE", -6: "WORKSPACE", -7: "HIP"}
 
-LC_FP32, LC_BF16 = 0, 1
+LC_FP32, LC_BF16, LC_FP16 = 0, 1, 2
 LC_PASS_F, LC_PASS_B = 0, 1
 (LC_T_WQ, LC_T_WK, LC_T_WV, LC_T_WO, LC_T_G1, LC_T_W1, LC_T_W3, LC_T_W2, LC_T_G2,
  LC_T_WR) = range(10)
@@ -78,6 +78,8 @@ class lc_adam_hparams(C.Structure):
 
 class lc_gemm_args(C.Structure):
     _fields_ = [("dtype", C.c_int32), ("epilogue", C.c_int32),
+                ("c_dtype", C.c_int32), ("r_dtype", C.c_int32), ("aux_dtype", C.c_int32),
+                ("reserved0", C.c_int32),
                 ("M", C.c_int64), ("N", C.c_int64), ("K", C.c_int64),
                 ("A", C.c_void_p), ("lda", C.c_int64), ("a_kmajor", C.c_int32),
                 ("b_kmajor", C.c_int32), ("B", C.c_void_p), ("ldb", C.c_int64),
@@ -86,7 +88,27 @@ class lc_gemm_args(C.Structure):
                 ("aux0", C.c_void_p), ("aux1", C.c_void_p), ("ld_aux", C.c_int64),
                 ("rope_cos", C.c_void_p), ("rope_sin", C.c_void_p),
                 ("rope_seq", C.c_int32), ("rope_cols", C.c_int32), ("head_dim", C.c_int32),
-                ("reserved", C.c_int32)]
+                ("reserved1", C.c_int32)]
+
+
+class lc_norm_args(C.Structure):
+    _fields_ = [("T", C.c_int64), ("d", C.c_int64), ("eps", C.c_float),
+                ("x_dtype", C.c_int32), ("w_dtype", C.c_int32), ("out_dtype", C.c_int32),
+                ("dn_dtype", C.c_int32), ("dres_dtype", C.c_int32),
+                ("x", C.c_void_p), ("g", C.c_void_p), ("n", C.c_void_p), ("rstd", C.c_void_p),
+                ("dn", C.c_void_p), ("dres", C.c_void_p), ("dx", C.c_void_p),
+                ("dx_copy", C.c_void_p), ("dg_accum", C.c_void_p),
+                ("scratch", C.c_void_p), ("scratch_bytes", C.c_size_t)]
+
+
+class lc_attn_args(C.Structure):
+    _fields_ = [("dtype", C.c_int32), ("o_dtype", C.c_int32),
+                ("B", C.c_int32), ("S", C.c_int32), ("H", C.c_int32), ("hd", C.c_int32),
+                ("q", C.c_void_p), ("k", C.c_void_p), ("v", C.c_void_p), ("ld_qkv", C.c_int64),
+                ("o", C.c_void_p), ("ld_o", C.c_int64), ("lse", C.c_void_p),
+                ("dout", C.c_void_p), ("dq", C.c_void_p), ("dk", C.c_void_p), ("dv", C.c_void_p),
+                ("ld_dqkv", C.c_int64), ("rope_cos", C.c_void_p), ("rope_sin", C.c_void_p),
+                ("scratch", C.c_void_p), ("scratch_bytes", C.c_size_t)]
 
 
 # name -> (restype, argtypes)
@@ -114,21 +136,11 @@ _SIGS = {
                                   C.c_void_p, C.c_size_t, C.POINTER(lc_adam_hparams),
                                   C.c_void_p]),
     "lc_gemm": (C.c_int, [C.POINTER(lc_gemm_args), C.c_void_p]),
-    "lc_rmsnorm_forward": (C.c_int, [C.c_int32, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p,
-                                     C.c_float, C.c_void_p, C.c_void_p, C.c_void_p]),
-    "lc_rmsnorm_backward": (C.c_int, [C.c_int32, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p,
-                                      C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                                      C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "lc_rmsnorm_forward": (C.c_int, [C.POINTER(lc_norm_args), C.c_void_p]),
+    "lc_rmsnorm_backward": (C.c_int, [C.POINTER(lc_norm_args), C.c_void_p]),
     "lc_rmsnorm_scratch_bytes": (C.c_size_t, [C.c_int64, C.c_int64]),
-    "lc_attention_forward": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                       C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
-                                       C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]),
-    "lc_attention_backward": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
-                                        C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p,
-                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
-                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
-                                        C.c_void_p]),
+    "lc_attention_forward": (C.c_int, [C.POINTER(lc_attn_args), C.c_void_p]),
+    "lc_attention_backward": (C.c_int, [C.POINTER(lc_attn_args), C.c_void_p]),
     "lc_attention_scratch_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32]),
     "lc_cast_bf16": (C.c_int, [C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
 }
@@ -320,37 +332,64 @@ def lc_cast_bf16(inp, out, n, stream=None):
 
 def lc_gemm(dtype, epilogue, M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, Cm, ldc, R=None,
             ldr=0, aux0=None, aux1=None, ld_aux=0, rope_cos=None, rope_sin=None, rope_seq=0,
-            rope_cols=0, head_dim=0, stream=None):
-    a = lc_gemm_args(dtype, epilogue, M, N, K, ptr(A) or None, lda, int(a_kmajor),
-                     int(b_kmajor), ptr(B) or None, ldb, ptr(Cm) or None, ldc, ptr(R) or None,
-                     ldr, ptr(aux0) or None, ptr(aux1) or None, ld_aux, ptr(rope_cos) or None,
-                     ptr(rope_sin) or None, rope_seq, rope_cols, head_dim, 0)
+            rope_cols=0, head_dim=0, c_dtype=None, r_dtype=None, aux_dtype=None, stream=None):
+    """C = A.B^T with an epilogue (lc_gemm_args); c/r/aux dtypes default to `dtype`."""
+    a = lc_gemm_args()
+    a.dtype, a.epilogue = dtype, epilogue
+    a.c_dtype = dtype if c_dtype is None else c_dtype
+    a.r_dtype = dtype if r_dtype is None else r_dtype
+    a.aux_dtype = dtype if aux_dtype is None else aux_dtype
+    a.M, a.N, a.K = M, N, K
+    a.A, a.lda, a.a_kmajor = ptr(A) or None, lda, int(a_kmajor)
+    a.B, a.ldb, a.b_kmajor = ptr(B) or None, ldb, int(b_kmajor)
+    a.C, a.ldc = ptr(Cm) or None, ldc
+    a.R, a.ldr = ptr(R) or None, ldr
+    a.aux0, a.aux1, a.ld_aux = ptr(aux0) or None, ptr(aux1) or None, ld_aux
+    a.rope_cos, a.rope_sin = ptr(rope_cos) or None, ptr(rope_sin) or None
+    a.rope_seq, a.rope_cols, a.head_dim = rope_seq, rope_cols, head_dim
     return _check(lib().lc_gemm(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
 
 
-def lc_rmsnorm_forward(dtype, T, d, x, g, eps, n, rstd, stream=None):
-    return _check(lib().lc_rmsnorm_forward(dtype, T, d, _vp(x), _vp(g), eps, _vp(n), _vp(rstd),
-                                           C.c_void_p(stream_ptr(stream) or None)))
+def _fill(struct, **kw):
+    for k, v in kw.items():
+        if isinstance(v, (int, float)) or v is None:
+            setattr(struct, k, v if not (k in _PTR_FIELDS and v == 0) else None)
+        else:
+            setattr(struct, k, ptr(v))
+    return struct
 
 
-def lc_rmsnorm_backward(dtype, T, d, dn, x, rstd, g, dres, dx, dg_accum, scratch,
-                        scratch_bytes, stream=None):
-    return _check(lib().lc_rmsnorm_backward(dtype, T, d, _vp(dn), _vp(x), _vp(rstd), _vp(g),
-                                            _vp(dres), _vp(dx), _vp(dg_accum), _vp(scratch),
-                                            scratch_bytes,
-                                            C.c_void_p(stream_ptr(stream) or None)))
+_PTR_FIELDS = {"x", "g", "n", "rstd", "dn", "dres", "dx", "dx_copy", "dg_accum", "scratch", "q",
+               "k", "v", "o", "lse", "dout", "dq", "dk", "dv", "rope_cos", "rope_sin"}
 
 
-def lc_attention_forward(dtype, B, S, H, hd, q, k, v, ld_qkv, o, ld_o, lse, stream=None):
-    return _check(lib().lc_attention_forward(dtype, B, S, H, hd, _vp(q), _vp(k), _vp(v), ld_qkv,
-                                             _vp(o), ld_o, _vp(lse),
-                                             C.c_void_p(stream_ptr(stream) or None)))
+def lc_rmsnorm_forward(T, d, x, g, eps, n, rstd, x_dtype, w_dtype, out_dtype, stream=None):
+    a = _fill(lc_norm_args(), T=T, d=d, eps=eps, x=x, g=g, n=n, rstd=rstd, x_dtype=x_dtype,
+              w_dtype=w_dtype, out_dtype=out_dtype)
+    return _check(lib().lc_rmsnorm_forward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
 
 
-def lc_attention_backward(dtype, B, S, H, hd, q, k, v, ld_qkv, o, dout, ld_o, lse, dq, dk, dv,
-                          ld_dqkv, rope_cos, rope_sin, scratch, scratch_bytes, stream=None):
-    return _check(lib().lc_attention_backward(dtype, B, S, H, hd, _vp(q), _vp(k), _vp(v), ld_qkv,
-                                              _vp(o), _vp(dout), ld_o, _vp(lse), _vp(dq),
-                                              _vp(dk), _vp(dv), ld_dqkv, _vp(rope_cos),
-                                              _vp(rope_sin), _vp(scratch), scratch_bytes,
-                                              C.c_void_p(stream_ptr(stream) or None)))
+def lc_rmsnorm_backward(T, d, dn, x, rstd, g, dres, dx, dg_accum, scratch, scratch_bytes,
+                        dn_dtype, x_dtype, w_dtype, dres_dtype, out_dtype, dx_copy=None,
+                        stream=None):
+    a = _fill(lc_norm_args(), T=T, d=d, dn=dn, x=x, rstd=rstd, g=g, dres=dres, dx=dx,
+              dx_copy=dx_copy, dg_accum=dg_accum, scratch=scratch, scratch_bytes=scratch_bytes,
+              dn_dtype=dn_dtype, x_dtype=x_dtype, w_dtype=w_dtype, dres_dtype=dres_dtype,
+              out_dtype=out_dtype)
+    return _check(lib().lc_rmsnorm_backward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_attention_forward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, ld_o, lse, stream=None):
+    a = _fill(lc_attn_args(), dtype=dtype, o_dtype=o_dtype, B=B, S=S, H=H, hd=hd, q=q, k=k, v=v,
+              ld_qkv=ld_qkv, o=o, ld_o=ld_o, lse=lse)
+    return _check(lib().lc_attention_forward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_attention_backward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, dout, ld_o, lse, dq,
+                          dk, dv, ld_dqkv, rope_cos, rope_sin, scratch, scratch_bytes,
+                          stream=None):
+    a = _fill(lc_attn_args(), dtype=dtype, o_dtype=o_dtype, B=B, S=S, H=H, hd=hd, q=q, k=k, v=v,
+              ld_qkv=ld_qkv, o=o, ld_o=ld_o, lse=lse, dout=dout, dq=dq, dk=dk, dv=dv,
+              ld_dqkv=ld_dqkv, rope_cos=rope_cos, rope_sin=rope_sin, scratch=scratch,
+              scratch_bytes=scratch_bytes)
+    return _check(lib().lc_attention_backward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))

@@ -61,6 +61,11 @@ def gpu_run(cfg, order, flat, Xs, dYs, max_in_flight=None):
     return r
 
 
+def report(errs, k=6):
+    top = sorted(errs.items(), key=lambda kv: -kv[1])[:k]
+    print("worst tensors: " + ", ".join(f"{n}={e:.2e}" for n, e in top), flush=True)
+
+
 def per_tensor_errors(cfg, got, ref):
     out = {}
     for name, off, shape in synth.layout(cfg):
@@ -83,9 +88,13 @@ def test_stage_matches_oracle(cfg, tol):
     r = gpu_run(cfg, order, flat, Xs, dYs)
     Ys, dXs, G = OS.run_order(cfg, flat, Xs, dYs, order)
     for mb in range(cfg.num_microbatches):
+        print(f"mb {mb}: Y err {rel_err(host(r.Y[mb]), Ys[mb]):.2e}, "
+              f"dX err {rel_err(host(r.dX[mb]), dXs[mb]):.2e}")
         assert rel_err(host(r.Y[mb]), Ys[mb]) <= tol, f"Y[{mb}]"
         assert rel_err(host(r.dX[mb]), dXs[mb]) <= tol, f"dX[{mb}]"
-    errs = per_tensor_errors(cfg, host(r.grad), G)
+    Gg = host(r.grad)
+    errs = per_tensor_errors(cfg, Gg, G)
+    report(errs)
     worst = max(errs, key=errs.get)
     assert errs[worst] <= tol, (worst, errs[worst])
     # one AdamW step on the accumulated gradient
@@ -98,10 +107,11 @@ def test_stage_matches_oracle(cfg, tol):
                                    cfg.adam_eps, cfg.weight_decay, 1)
     assert rel_err(host(r.m), m_ref) <= tol
     assert rel_err(host(r.v), v_ref) <= 2 * tol
-    # at t = 1 the update is ~ -lr*sign(g): skip elements whose gradient is
-    # within the tolerated difference of zero (their sign is not determined)
-    keep = np.abs(g_ref) > 1e-4 * np.max(np.abs(g_ref)) if tol <= 1e-4 else \
-        np.abs(g_ref) > 4 * tol * np.max(np.abs(g_ref))
+    # at t = 1 the update is ~ -lr*sign(g): an element whose gradient sign
+    # differs between the two sides (|g| within the tolerated error of 0)
+    # moves the other way; compare the elements whose signs agree
+    keep = np.sign(Gg.astype(np.float32)) == np.sign(g_ref)
+    print(f"adam: {int((~keep).sum())} of {keep.size} elements with opposite gradient signs")
     assert keep.mean() > 0.9
     assert rel_err(host(r.master)[keep], p_ref[keep]) <= tol
     r.close()
@@ -159,8 +169,10 @@ def test_stage_error_paths_have_no_side_effects():
     r.close()
 
 
-@pytest.mark.parametrize("cfg", [synth.STAGE_7B], ids=["stage7b"])
-def test_full_size_stage_on_a_prefix(cfg):
+@pytest.mark.parametrize("cfg,tol", [(synth.STAGE_7B, 2e-2),
+                                     (synth.scaled(synth.STAGE_7B, bf16=False), 1e-4)],
+                         ids=["stage7b_bf16", "stage7b_fp32"])
+def test_full_size_stage_on_a_prefix(cfg, tol):
     P = 128
     banner(f"full-size {cfg.name} prefix {P}")
     flat = synth.stage_params(cfg, 0)
@@ -181,9 +193,11 @@ def test_full_size_stage_on_a_prefix(cfg):
     layers = OS.layer_params(cfg, flat)
     Yp, caches = OS.stage_forward(cfg, layers, X[:, :P])
     dXp, Gp = OS.stage_backward(cfg, layers, caches, dY[:, :P])
-    assert rel_err(Yg[:, :P], Yp) <= 2e-2
-    assert rel_err(dXg[:, :P], dXp) <= 2e-2
+    print(f"Y prefix err {rel_err(Yg[:, :P], Yp):.2e}, dX prefix err {rel_err(dXg[:, :P], dXp):.2e}")
+    assert rel_err(Yg[:, :P], Yp) <= tol
+    assert rel_err(dXg[:, :P], dXp) <= tol
     assert np.all(dXg[:, P:] == 0.0)
     errs = per_tensor_errors(cfg, Gg, Gp)
+    report(errs, 12)
     worst = max(errs, key=errs.get)
-    assert errs[worst] <= 2e-2, (worst, errs[worst])
+    assert errs[worst] <= tol, (worst, errs[worst])

@@ -122,8 +122,10 @@ def test_workspace_grows_with_stash_slots():
     w8 = lc.lc_workspace_bytes(d, 8)
     slot = (w8 - w1) // 7
     T, D, F, L = 4096, 4096, 11008, 4
-    # per layer: x, n1, qkv(3), o, h, n2 (bf16 [T,d]) + gate, up, act ([T,f]) + fp32 rows
-    approx = L * (2 * T * D * 8 + 2 * T * F * 3 + 4 * T * (2 + 32))
+    # per layer: x, h (fp32 [T,d]); n1, o, n2 (bf16 [T,d]); q, k, v (fp16 [T,d]);
+    # gate, up (fp32 [T,f]); act (bf16 [T,f]); rstd1, rstd2, lse (fp32 rows)
+    approx = L * (4 * T * D * 2 + 2 * T * D * 3 + 2 * T * D * 3 + 4 * T * F * 2 + 2 * T * F
+                  + 4 * T * (2 + 32))
     assert approx <= slot <= approx + L * 16 * 256
 
 
@@ -176,4 +178,13 @@ def test_buffer_entry_points_reject_bad_arguments():
     with pytest.raises(lc.LibchunkError):
         lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE, 0, 8, 8, 4096, 8, 1, 4096, 8, 1, 4096, 8)
     with pytest.raises(lc.LibchunkError):
-        lc.lc_attention_forward(lc.LC_BF16, 1, 128, 2, 64, 4096, 4096, 4096, 256, 4096, 256, 4096)
+        lc.lc_attention_forward(lc.LC_BF16, lc.LC_BF16, 1, 128, 2, 64, 4096, 4096, 4096, 256,
+                                4096, 256, 4096)
+    with pytest.raises(lc.LibchunkError):  # fp16 q/k/v need bf16 outputs
+        lc.lc_attention_forward(lc.LC_FP16, lc.LC_FP16, 1, 128, 2, 128, 4096, 4096, 4096, 768,
+                                4096, 256, 4096)
+    with pytest.raises(lc.LibchunkError):  # gemm fp32 operands with a bf16 output
+        lc.lc_gemm(lc.LC_FP32, lc.LC_EPI_STORE, 8, 8, 8, 4096, 8, 1, 4096, 8, 1, 4096, 8,
+                   c_dtype=lc.LC_BF16)
+    with pytest.raises(lc.LibchunkError):  # norm with an unknown dtype
+        lc.lc_rmsnorm_forward(4, 8, 4096, 4096, 1e-5, 4096, 4096, 7, lc.LC_BF16, lc.LC_BF16)

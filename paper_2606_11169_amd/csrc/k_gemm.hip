@@ -5,18 +5,43 @@
 //   A(m, k) = A_K ? A[m*lda + k] : A[k*lda + m]      (A_K: k is contiguous)
 //   B(n, k) = B_K ? B[n*ldb + k] : B[k*ldb + n]
 //
-// Tile: 256 x 256 x 64 per workgroup of 256 threads (4 waves, 2 x 2), each wave
-// owns 128 x 128 = 4 x 4 MFMA blocks of 32 x 32. Operand tiles live in LDS as
-// [row][64 k] bf16 rows of 128 bytes whose eight 16-byte chunks are XOR-swizzled
-// by (row & 7), so that the MFMA fragment reads (16 bytes per lane, 32 rows at
-// the same k-chunk) and the tile writes are bank-conflict free. Two LDS stages:
-// the global loads of k-tile t+1 are in flight while tile t is multiplied.
+// Tile: 256 x 256 per workgroup of 512 threads (8 waves, 4 along m x 2 along
+// n); each wave owns 64 x 128 = 2 x 4 MFMA blocks of 32 x 32. K is walked in
+// halves of 32: LDS is a ring of four 32 KiB slots, each holding one half
+// (A 256 x 32 | B 256 x 32), so three halves (96 KiB per CU) are always in
+// flight from HBM/L2 while the fourth is being multiplied. Latency of the
+// global->LDS path, not LDS or matrix-core throughput, is what bounds this
+// kernel, and the ring is sized for it.
 //
-// An operand whose k is not contiguous in memory (a weight read as dX = dY W,
-// or both operands of a weight gradient dW = dY^T X) is loaded as 8 x 8 blocks
-// (eight 16-byte rows along m, one per k) and transposed in registers, so the
-// LDS image and the MFMA path are identical for every layout and no transposed
-// copy is ever materialised in HBM.
+// The eight waves form two groups of four (waves 0-3 and 4-7; one wave of
+// each on every SIMD) that run one phase apart ("ping-pong"): while one group
+// multiplies a half out of registers, the other reads its fragments of that
+// half from LDS, so every SIMD's matrix core always has a wave to serve.
+//   phase 2j:   group 0 reads half j,     group 1 multiplies half j-1
+//   phase 2j+1: group 0 multiplies half j, group 1 reads half j
+// Half j+3 goes into the slot of half j-1, which is free after phase 2j-1:
+// group 0 starts its A part at the start of phase 2j, group 1 its B part at
+// the start of phase 2j+1, and each group waits (vmcnt) for its part of half
+// j+1 before the barrier that ends phase 2j+1.
+//
+// Operand tiles go from HBM straight into LDS (buffer_load_dwordx4 ... lds:
+// lane l of a wave's load fills bytes [16 l, 16 l + 16) of a 1 KiB LDS run),
+// so no register staging is needed; each lane picks the global 16 bytes that
+// belong at its LDS slot, which is how the tiles are swizzled. Buffer
+// descriptors make out-of-range lanes (matrix edges, K tail) read zeros.
+//   k-major operand: LDS rows of 32 k (64 B); 16-byte chunk c of row r sits
+//     at chunk c ^ ((r >> 2) & 3). A fragment (32 rows at one k chunk, 16
+//     bytes per lane) is one ds_read_b128 and every 16-lane phase touches all
+//     64 banks once.
+//   m/n-major operand (a weight read as dX = dY W, both operands of a weight
+//     gradient dW = dY^T X): LDS rows of one k and 256 m (512 B), chunk c of
+//     row k at chunk c ^ (4 (k & 3)). The fragment is read with the CDNA4
+//     transposing load ds_read_b64_tr_b16: in each group of 16 lanes, lane j
+//     receives element j % 4 of the 8 bytes addressed by lane 4e + j / 4 as its
+//     element e, so lanes addressing four consecutive k rows at four 4-element
+//     column runs receive one column's four k values each. Two such loads
+//     give the 8 k values of the MFMA operand; no transposed copy exists in
+//     HBM and no register shuffles are spent.
 //
 // The MFMA is issued with B's fragment in the instruction's first operand and
 // A's in the second, which leaves lane l holding output row m = l % 32 and four
@@ -30,11 +55,22 @@
 namespace lc {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int NT = 256;            // threads per workgroup
-constexpr int WM = 128, WN = 128;  // wave tile
+constexpr int BM = 256, BN = 256;
+constexpr int KH = 32;             // k per half (one LDS ring slot)
+constexpr int NSLOT = 4;           // ring slots
+constexpr int NT = 512;            // threads per workgroup (8 waves)
+constexpr int WM = 64, WN = 128;   // wave tile
 constexpr int FM = WM / 32, FN = WN / 32;
-constexpr int TILE_BYTES = BM * BK * 2;  // one operand tile in LDS (32 KiB)
+constexpr int HALF_BYTES = BM * KH * 2;       // one operand's half in LDS (16 KiB)
+constexpr int SLOT_BYTES = 2 * HALF_BYTES;    // A half | B half
+constexpr uint32_t OOB = 0x80000000u;    // buffer offset beyond every operand: reads 0
+
+typedef __attribute__((ext_vector_type(4))) short s16x4_v;
+// LDS addresses stay 32-bit LDS-space pointers throughout (no generic pointers)
+typedef __attribute__((address_space(3))) char lds_t;
+typedef __attribute__((address_space(3))) bf16x8_v lds_v8;
+typedef __attribute__((address_space(3))) s16x4_v lds_v4;
+#define LDS_AS(T, ptr) ((__attribute__((address_space(3))) T *)(ptr))
 
 struct GemmP {
   const bf16_t *A;
@@ -46,117 +82,143 @@ struct GemmP {
   const float *rcos;
   const float *rsin;
   int64_t lda, ldb, ldc, ldr, ld_aux;
+  uint32_t a_bytes, b_bytes;  // byte extent of each operand (< 2^31)
   int M, N, K;  // N: output columns (SwiGLU: gate/up width)
   int tiles_m, tiles_n;
   int rope_seq, rope_cols;
   int c_dt, r_dt, aux_dt;
 };
 
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * 128 + ((chunk ^ (row & 7)) << 4);
+typedef __attribute__((ext_vector_type(4))) int i32x4_v;
+
+// Raw buffer descriptor (CDNA: dword3 = 0x00020000, stride 0): offsets past
+// `bytes` read as zero.
+__device__ __forceinline__ i32x4_v make_rsrc(const void *base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4_v r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
 }
 
-// 8x8 transpose of bf16 held as 8 rows of uint4 (row r = 8 consecutive m at k r)
-// into 8 rows of uint4 (row mm = 8 consecutive k at m mm).
-__device__ __forceinline__ void transpose8x8(const uint4 (&r)[8], uint4 (&t)[8]) {
-  const uint32_t *rw = reinterpret_cast<const uint32_t *>(r);
-  uint32_t *tw = reinterpret_cast<uint32_t *>(t);
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {      // m pair (2p, 2p+1) = dword p of every row
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {    // k pair (2q, 2q+1) = dword q of the output
-      const uint32_t lo = rw[(2 * q) * 4 + p];
-      const uint32_t hi = rw[(2 * q + 1) * 4 + p];
-      tw[(2 * p) * 4 + q] = (lo & 0xFFFFu) | (hi << 16);
-      tw[(2 * p + 1) * 4 + q] = (lo >> 16) | (hi & 0xFFFF0000u);
-    }
-  }
+// 16 bytes per lane from the buffer at byte offset `off` into LDS at
+// lds + 16 * lane. Issued as inline assembly: the compiler then does not track
+// the load, so it inserts no wait for it before LDS reads of the other stage;
+// the step's explicit wait before its barrier is what orders it.
+__device__ __forceinline__ void dma16(i32x4_v rs, lds_t *lds, uint32_t off) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t) reinterpret_cast<uintptr_t>(lds));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(off), "s"(rs), "s"(m0)
+               : "memory", "m0");
 }
 
-// Loads of one 256 x 64 operand tile into registers.
-// KMAJ: thread t covers rows (t>>3) + 32i, chunk t&7, i < 8.
-// !KMAJ: thread t covers the 8x8 block (m-block t&31, k-block t>>5).
+// One wave's share of an operand's loads: 4 of the 16 1-KiB LDS runs of a
+// 256 x 32 half (the four waves of a group load one operand).
+//   k-major: run q = rows 16q .. 16q+15; lane l -> row 16q + l/4, LDS chunk
+//     l%4 holding global k chunk (l%4) ^ ((row >> 2) & 3).
+//     ROWMAP 0: tile row r -> operand row base + r (valid below lim)
+//     ROWMAP 1 (SwiGLU B rows): tile row r -> gate row ob + (r>>7)*64 + (r&63)
+//       for (r&127) < 64, else up row lim + ob + (r>>7)*64 + (r&63); valid
+//       while the output column ob + (r>>7)*64 + (r&63) < lim.
+//   m/n-major: run q = k rows 2q, 2q+1; lane l -> k row 2q + l/32, LDS chunk
+//     l%32 holding global columns 8 ((l%32) ^ (4 (krow & 3))) .. +7.
+// Run t of wave w is q = 4w + t: consecutive runs are a fixed byte distance
+// apart in the operand. For k-major runs the swizzle term (row >> 2) & 3 is
+// (l >> 4) & 3 for every run; for m/n-major runs (krow & 3) depends on the
+// parity of t (2 k rows on flip bit 1). The per-lane state is a row offset,
+// the two parity variants of the in-row offset, a validity mask and a k
+// position; everything else is wave-uniform.
 template <bool KMAJ, int ROWMAP>
-struct TileLoader {
-  uint4 v[8];
+struct Stream {
+  uint32_t base;     // byte offset of run 0's row (k-major) or k row (m/n-major)
+  uint32_t col[2];   // byte offset inside the row for even / odd runs
+  uint32_t run;      // byte distance between consecutive runs
+  uint32_t kb;       // bytes per unit of k
+  uint32_t rows;     // bit t set when run t's row / columns are inside the operand
+  int kl;            // k-major: first k of this lane's chunk; m/n-major: k row of run 0
 
-  // ROWMAP 0: tile row r -> operand row base + r (valid below lim)
-  // ROWMAP 1 (SwiGLU B rows): tile row r -> gate row ob + (r>>7)*64 + (r&63) for
-  //           (r&127) < 64, else up row N + ob + (r>>7)*64 + (r&63); valid while
-  //           the output column ob + (r>>7)*64 + (r&63) < N.
-  __device__ __forceinline__ void load(const bf16_t *__restrict__ X, int64_t ld, int base,
-                                       int lim, int k0, int K, int tid) {
+  __device__ __forceinline__ void init(int64_t ld, int base_row, int lim, int wave, int lane) {
     if constexpr (KMAJ) {
-      const int ch = tid & 7;
-      const int gk = k0 + ch * 8;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int r = (tid >> 3) + 32 * i;
-        int grow;
-        bool ok;
-        if constexpr (ROWMAP == 0) {
-          grow = base + r;
-          ok = grow < lim;
-        } else {
-          const int oc = base + (r >> 7) * 64 + (r & 63);
-          ok = oc < lim;
-          grow = ((r & 127) < 64) ? oc : lim + oc;
-        }
-        ok = ok && (gk < K);
-        if (ok) {
-          v[i] = *reinterpret_cast<const uint4 *>(X + (int64_t)grow * ld + gk);
-        } else {
-          v[i] = make_uint4(0, 0, 0, 0);
-        }
+      const int r0 = 64 * wave + (lane >> 2);  // tile row of run 0; (r >> 2) & 3 == (lane >> 4) & 3
+      kl = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+      int grow0, oc0;
+      if constexpr (ROWMAP == 0) {
+        grow0 = base_row + r0;
+        oc0 = grow0;
+      } else {
+        oc0 = base_row + (r0 >> 7) * 64 + (r0 & 63);
+        grow0 = ((r0 & 127) < 64) ? oc0 : lim + oc0;
       }
+      rows = 0;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) rows |= (oc0 + 16 * t < lim ? 1u : 0u) << t;
+      base = rows ? (uint32_t)((int64_t)grow0 * ld * 2) : 0u;
+      col[0] = col[1] = (uint32_t)(kl * 2);
+      run = (uint32_t)(16 * ld * 2);
+      kb = 2;
     } else {
       static_assert(ROWMAP == 0, "row remap needs a k-major operand");
-      const int mb = tid & 31, kb = tid >> 5;
-      const int gm = base + mb * 8;
-      const bool mok = gm < lim;
+      const int kr0 = 8 * wave + (lane >> 5);         // k row of run 0; kr0 & 3 == lane >> 5
+      const int c0 = (lane & 31) ^ (4 * (lane >> 5));  // odd runs: c0 ^ 8
+      const int gm0 = base_row + 8 * c0, gm1 = base_row + 8 * (c0 ^ 8);
+      kl = kr0;
+      rows = 0;
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk) {
-        const int gk = k0 + kb * 8 + kk;
-        if (mok && gk < K) {
-          v[kk] = *reinterpret_cast<const uint4 *>(X + (int64_t)gk * ld + gm);
-        } else {
-          v[kk] = make_uint4(0, 0, 0, 0);
-        }
-      }
+      for (int t = 0; t < 4; ++t) rows |= (((t & 1) ? gm1 : gm0) < lim ? 1u : 0u) << t;
+      base = (uint32_t)((int64_t)kr0 * ld * 2);
+      col[0] = gm0 < lim ? (uint32_t)(gm0 * 2) : 0u;
+      col[1] = gm1 < lim ? (uint32_t)(gm1 * 2) : 0u;
+      run = (uint32_t)(2 * ld * 2);
+      kb = (uint32_t)(ld * 2);
     }
   }
 
-  __device__ __forceinline__ void store(char *lds, int tid) const {
-    if constexpr (KMAJ) {
-      const int ch = tid & 7;
+  // the wave's 4 runs of the half starting at k0, into `lds` (the operand's half)
+  __device__ __forceinline__ void load(i32x4_v rs, lds_t *lds, int wave, int k0, int K) const {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int r = (tid >> 3) + 32 * i;
-        *reinterpret_cast<uint4 *>(lds + lds_off(r, ch)) = v[i];
-      }
-    } else {
-      const int mb = tid & 31, kb = tid >> 5;
-      uint4 t[8];
-      transpose8x8(v, t);
-#pragma unroll
-      for (int mm = 0; mm < 8; ++mm) {
-        *reinterpret_cast<uint4 *>(lds + lds_off(mb * 8 + mm, kb)) = t[mm];
-      }
+    for (int t = 0; t < 4; ++t) {
+      bool ok = (rows >> t) & 1u;
+      if constexpr (KMAJ) ok = ok && k0 + kl < K;
+      else ok = ok && k0 + kl + 2 * t < K;
+      const uint32_t off = ok ? base + t * run + col[t & 1] + (uint32_t)k0 * kb : OOB;
+      dma16(rs, lds + (4 * wave + t) * 1024, off);
     }
   }
 };
 
+// MFMA operand of 32 rows (row0 .. row0+31) at k = 16 s + 8 (lane / 32) + [0, 8)
+// of the half stored at t
+template <bool KMAJ>
+__device__ __forceinline__ bf16x8_v frag(const lds_t *t, int row0, int s, int lane) {
+  if constexpr (KMAJ) {
+    const int row = row0 + (lane & 31);
+    const int c = 2 * s + (lane >> 5);
+    return *reinterpret_cast<const lds_v8 *>(t + row * 64 + ((c ^ ((row >> 2) & 3)) << 4));
+  } else {
+    const int i16 = lane & 15, g = lane >> 4;
+    const int m = row0 + 16 * (g & 1) + 4 * (i16 & 3);
+    const int k = 16 * s + 8 * (g >> 1) + (i16 >> 2);
+    const int cb = ((m >> 3) ^ (4 * (i16 >> 2))) << 4;  // k & 3 == i16 >> 2
+    const lds_t *p0 = t + k * 512 + cb + (m & 7) * 2;
+    const s16x4_v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(p0));
+    const s16x4_v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(p0 + 4 * 512));
+    const s16x4_v v[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8_v, v);
+  }
+}
+
 template <bool A_K, bool B_K, int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
-  extern __shared__ __align__(16) char smem[];
-  // LDS: A stage 0, A stage 1, B stage 0, B stage 1
-  auto ldsA = [&](int st) { return smem + st * TILE_BYTES; };
-  auto ldsB = [&](int st) { return smem + (2 + st) * TILE_BYTES; };
+  __shared__ __align__(16) char ring[NSLOT * SLOT_BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int grp = wave >> 2, w4 = wave & 3;
+  const int wm = w4, wn = grp;  // group g owns output columns [128 g, 128 g + 128)
 
   // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
   // contiguous run of tiles, then walk tiles in groups of 8 tile-rows so that
@@ -174,9 +236,6 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   constexpr bool SWI = (EPI == LC_EPI_SWIGLU);
   const int n0 = SWI ? tn * (BN / 2) : tn * BN;  // first output column
 
-  TileLoader<A_K, 0> la;
-  TileLoader<B_K, SWI ? 1 : 0> lb;
-
   f32x16_v acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -185,47 +244,80 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = (p.K + BK - 1) / BK;
-  la.load(p.A, p.lda, m0, p.M, 0, p.K, tid);
-  lb.load(p.B, p.ldb, n0, p.N, 0, p.K, tid);
-  la.store(ldsA(0), tid);
-  lb.store(ldsB(0), tid);
+  lds_t *const R0 = LDS_AS(char, ring);
+  const int nh = (p.K + KH - 1) / KH;  // halves
+  // group 0 streams the A halves, group 1 the B halves
+  const i32x4_v rs = grp == 0 ? make_rsrc(p.A, p.a_bytes) : make_rsrc(p.B, p.b_bytes);
+  Stream<A_K, 0> sa_;
+  Stream<B_K, SWI ? 1 : 0> sb_;
+  if (grp == 0) sa_.init(p.lda, m0, p.M, w4, lane);
+  else sb_.init(p.ldb, n0, p.N, w4, lane);
+  auto load = [&](int j) {  // this group's operand of half j
+    lds_t *slot = R0 + (j & (NSLOT - 1)) * SLOT_BYTES;
+    if (grp == 0) sa_.load(rs, slot, w4, j * KH, p.K);
+    else sb_.load(rs, slot + HALF_BYTES, w4, j * KH, p.K);
+  };
+  // wait until this wave's loads of half j+1 have landed (loads retire in
+  // order; the younger halves j+2, j+3 may stay in flight)
+  auto wait_next = [&](int j) {
+    if (j + 3 < nh) __builtin_amdgcn_s_waitcnt(0x0F78);       // vmcnt(8)
+    else if (j + 2 < nh) __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt(4)
+    else __builtin_amdgcn_s_waitcnt(0x0F70);                  // vmcnt(0)
+  };
+
+  typedef bf16x8_v FragA[2][FM];
+  typedef bf16x8_v FragB[2][FN];
+  auto read_half = [&](int j, FragA &af, FragB &bfr) {
+    const lds_t *slot = R0 + (j & (NSLOT - 1)) * SLOT_BYTES;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[s][i] = frag<A_K>(slot, wm * WM + i * 32, s, lane);
+#pragma unroll
+      for (int jj = 0; jj < FN; ++jj)
+        bfr[s][jj] = frag<B_K>(slot + HALF_BYTES, wn * WN + jj * 32, s, lane);
+    }
+  };
+  auto multiply = [&](const FragA &af, const FragB &bfr) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int jj = 0; jj < FN; ++jj)
+          acc[i][jj] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[s][jj], af[s][i], acc[i][jj], 0, 0, 0);
+  };
+  // A phase boundary: no instruction moves across it; both groups meet at it.
+  auto barrier = [&]() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // prologue: halves 0, 1, 2 in flight, half 0 landed everywhere
+  for (int j = 0; j < 3 && j < nh; ++j) load(j);
+  if (nh > 2) __builtin_amdgcn_s_waitcnt(0x0F78);       // vmcnt(8)
+  else if (nh > 1) __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt(4)
+  else __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
+  if (grp == 1) barrier();
+  for (int j = 0; j < nh; ++j) {
+    FragA af;
+    FragB bfr;
+    if (j + 3 < nh) load(j + 3);  // into the slot of half j-1
+    read_half(j, af, bfr);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments in registers
+    if (grp == 1) wait_next(j);
+    barrier();
+    multiply(af, bfr);
+    if (grp == 0) wait_next(j);
+    barrier();
+  }
+  if (grp == 0) barrier();
 
   const int frow = lane & 31;
   const int fhalf = lane >> 5;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load(p.A, p.lda, m0, p.M, (kt + 1) * BK, p.K, tid);
-      lb.load(p.B, p.ldb, n0, p.N, (kt + 1) * BK, p.K, tid);
-    }
-    const char *sa = ldsA(cur);
-    const char *sb = ldsB(cur);
-#pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      const int ch = s * 2 + fhalf;
-      bf16x8_v af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_v *>(sa + lds_off(wm * WM + i * 32 + frow, ch));
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_v *>(sb + lds_off(wn * WN + j * 32 + frow, ch));
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      la.store(ldsA(cur ^ 1), tid);
-      lb.store(ldsB(cur ^ 1), tid);
-    }
-    __syncthreads();
-  }
-
   // ------------------------------------------------------------ epilogue
   const int h4 = 4 * fhalf;
 #pragma unroll
@@ -334,15 +426,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
 template <bool A_K, bool B_K, int EPI>
 lc_status launch_t(const GemmP &p, hipStream_t s) {
   const unsigned grid = (unsigned)p.tiles_m * (unsigned)p.tiles_n;
-  const size_t lds = 4 * TILE_BYTES;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<A_K, B_K, EPI>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return hip_fail(e, "gemm: setting the LDS size");
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((gemm_bf16_kernel<A_K, B_K, EPI>), dim3(grid), dim3(NT), lds, s, p);
+  hipLaunchKernelGGL((gemm_bf16_kernel<A_K, B_K, EPI>), dim3(grid), dim3(NT), 0, s, p);
   return check_launch("gemm_bf16_kernel");
 }
 
@@ -431,6 +515,14 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
   p.M = (int)a.M;
   p.N = (int)a.N;
   p.K = (int)a.K;
+  // byte extents for the buffer descriptors (offsets are 32-bit)
+  const int64_t brows = a.epilogue == LC_EPI_SWIGLU ? 2 * a.N : a.N;
+  const int64_t a_ext = a.a_kmajor ? (a.M - 1) * a.lda + a.K : (a.K - 1) * a.lda + a.M;
+  const int64_t b_ext = a.b_kmajor ? (brows - 1) * a.ldb + a.K : (a.K - 1) * a.ldb + brows;
+  if (a_ext * 2 >= (int64_t)OOB || b_ext * 2 >= (int64_t)OOB)
+    return fail(LC_ERR_UNSUPPORTED, "gemm bf16: an operand spans 2 GiB or more");
+  p.a_bytes = (uint32_t)(a_ext * 2);
+  p.b_bytes = (uint32_t)(b_ext * 2);
   p.tiles_m = (int)((a.M + BM - 1) / BM);
   p.tiles_n = a.epilogue == LC_EPI_SWIGLU ? (int)((a.N + BN / 2 - 1) / (BN / 2))
                                           : (int)((a.N + BN - 1) / BN);

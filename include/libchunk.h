@@ -224,6 +224,16 @@ lc_status chunk_backward(lc_stage *stage, const lc_param_bufs *params,
 lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
                        const lc_microbatch_desc *mbs, void *stream);
 
+/* Routing of a mixture-of-experts stage: copies the two experts chosen for
+ * every token of layer `layer` of microbatch `mb` (int32 [micro_batch *
+ * seq_len, 2], the order of lc_moe_route's sel) into the caller's device
+ * buffer `sel_out`. Valid between chunk_forward(mb) and chunk_backward(mb)
+ * (LC_ERR_STATE otherwise); LC_ERR_INVALID_ARG for a dense stage or a layer
+ * out of range. Enqueued on `stream`; for tests and monitoring (routing
+ * statistics), not needed to train. */
+lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32_t *sel_out,
+                               void *stream);
+
 /* ---------------------------------------------------------------- buffers */
 
 /* accum[i] += g[i] for i < n, in fp32 (g is fp32 or bf16 per g_dtype); each

@@ -61,6 +61,20 @@ extern "C" {
  * k-major; 16-byte aligned pointers. Other dimensions may be any positive
  * size (edges are masked).
  */
+/* Grouped modes (n_groups groups; group_offsets is a device array of
+ * n_groups + 1 nondecreasing offsets written by an earlier kernel, such as the
+ * expert offsets of lc_moe_dispatch; values are clamped to [0, M] or [0, K]):
+ *   LC_GROUP_NONE  one product as above.
+ *   LC_GROUP_ROWS  rows [off[g], off[g+1]) of A and C are multiplied with
+ *                  B_g = B + g * group_stride_b (an expert's weights); rows at
+ *                  or beyond off[n_groups] are not written. M bounds the rows.
+ *   LC_GROUP_K     C_g = C + g * group_stride_c receives the epilogue of
+ *                  sum over k in [off[g], off[g+1]) of A(m, k) B(n, k) (an
+ *                  expert's weight gradient over its routed rows); both
+ *                  operands must not be k-major. K bounds the offsets.
+ */
+typedef enum lc_gemm_group { LC_GROUP_NONE = 0, LC_GROUP_ROWS = 1, LC_GROUP_K = 2 } lc_gemm_group;
+
 typedef enum lc_gemm_epilogue {
   LC_EPI_STORE = 0,
   LC_EPI_STORE_F32 = 1,
@@ -86,6 +100,12 @@ typedef struct lc_gemm_args {
   void *aux0; void *aux1; int64_t ld_aux;
   const float *rope_cos; const float *rope_sin;
   int32_t rope_seq; int32_t rope_cols; int32_t head_dim; int32_t reserved1;
+  /* grouped products (the experts of a mixture-of-experts FFN); see below */
+  int32_t group_mode;              /* lc_gemm_group */
+  int32_t n_groups;                /* 1 .. 64 */
+  const int32_t *group_offsets;    /* device, n_groups + 1 entries */
+  int64_t group_stride_b;          /* LC_GROUP_ROWS: elements from B_g to B_(g+1) */
+  int64_t group_stride_c;          /* LC_GROUP_K: elements from C_g to C_(g+1) */
 } lc_gemm_args;
 
 lc_status lc_gemm(const lc_gemm_args *args, void *stream);
@@ -153,6 +173,51 @@ typedef struct lc_attn_args {
 lc_status lc_attention_forward(const lc_attn_args *args, void *stream);
 lc_status lc_attention_backward(const lc_attn_args *args, void *stream);
 size_t lc_attention_scratch_bytes(int32_t B, int32_t S, int32_t H);
+
+/* ------------------------------------------------------------------ MoE routing
+ * Router and dispatch of a top-2 mixture-of-experts FFN over T tokens of d
+ * features and E experts (2 <= E <= 64); the expert FFNs themselves are
+ * grouped products (lc_gemm with LC_GROUP_ROWS / LC_GROUP_K).
+ *
+ * lc_moe_route reads n [T, d] and the router weights wr [E, d] (element types
+ * n_dtype, w_dtype) and writes, per token t:
+ *   l[t, e] = sum_i n[t, i] wr[e, i]                    (fp32 accumulation)
+ *   sel[t, 0], sel[t, 1] = the two experts of largest softmax(l[t]); equal
+ *                          probabilities go to the lower expert index; a NaN
+ *                          logit ranks below every number
+ *   w[t, k] = softmax(l[t])[sel_k] / (softmax(l[t])[sel_0] + softmax(l[t])[sel_1])
+ *           (computed as w0 = 1 / (1 + exp(l1 - l0)), w1 = exp(l1 - l0) w0)
+ * sel is int32 [T, 2] and w fp32 [T, 2], device.
+ *
+ * lc_moe_dispatch groups the 2T (token, expert) pairs of sel/w by expert with
+ * a stable counting sort (expert-major, token-minor order; the same result on
+ * every run) and writes (device, int32 unless noted):
+ *   offsets[E + 1]  offsets[e] = number of pairs routed to experts below e
+ *   perm[2T]        token of sorted row r
+ *   wrow[2T]        fp32 gate weight w[perm[r], k] of sorted row r
+ *   rowpos[T, 2]    sorted row of pair (t, sel[t, k])
+ * A pair whose expert is outside [0, E), or repeats the token's first expert,
+ * is not placed (rowpos -1); rows past offsets[E] then hold token 0 with
+ * weight 0. One workgroup does the whole sort (tokens in chunks of 1024).
+ */
+typedef struct lc_moe_args {
+  int64_t T;
+  int32_t d;
+  int32_t E;
+  int32_t n_dtype;
+  int32_t w_dtype;
+  const void *n;          /* [T, d] */
+  const void *wr;         /* [E, d] */
+  int32_t *sel;           /* [T, 2] */
+  float *w;               /* [T, 2] */
+  int32_t *offsets;       /* [E + 1] */
+  int32_t *perm;          /* [2T] */
+  float *wrow;            /* [2T] */
+  int32_t *rowpos;        /* [T, 2] */
+} lc_moe_args;
+
+lc_status lc_moe_route(const lc_moe_args *args, void *stream);
+lc_status lc_moe_dispatch(const lc_moe_args *args, void *stream);
 
 /* ------------------------------------------------------------------ casts */
 

@@ -205,6 +205,29 @@ def moe_route(n2, wr, top_k: int):
     return logits, pi, sel, w
 
 
+def moe_dispatch(sel, n_experts: int):
+    """Order in which the grouped expert products take their rows: the
+    (token, expert) pairs grouped by expert, and within an expert by token
+    (the row order in which moe_forward lists each expert's tokens).
+
+    Returns offsets [E + 1] (offsets[e] = pairs routed to experts below e),
+    perm [2T] (token of each grouped row) and rowpos [T, k] (grouped row of
+    pair (t, sel[t, k])). Plain loops over the definition.
+    """
+    sel = np.asarray(sel)
+    T, K = sel.shape
+    perm, offsets = [], [0]
+    rowpos = np.full((T, K), -1, dtype=np.int64)
+    for e in range(n_experts):
+        for t in range(T):
+            for k in range(K):
+                if sel[t, k] == e:
+                    rowpos[t, k] = len(perm)
+                    perm.append(t)
+        offsets.append(len(perm))
+    return np.array(offsets, np.int64), np.array(perm, np.int64), rowpos
+
+
 def moe_forward(n2, p, cfg, route_override=None):
     """sum_k w_k FFN_{e_k}(n2_t) per token t; n2 is [T, d].
 

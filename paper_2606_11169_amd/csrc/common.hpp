@@ -123,5 +123,22 @@ lc_status accumulate_launch(float *acc, const void *g, int g_dtype, size_t n, hi
 lc_status adam_launch(float *p, float *m, float *v, const void *g, int g_dtype, uint16_t *out,
                       size_t n, const lc_adam_hparams &hp, hipStream_t s);
 lc_status cast_bf16_launch(const float *in, uint16_t *out, size_t n, hipStream_t s);
+lc_status moe_route_launch(const lc_moe_args &a, hipStream_t s);
+lc_status moe_dispatch_launch(const lc_moe_args &a, hipStream_t s);
+lc_status moe_gather_launch(const void *src, void *dst, const int32_t *idx, int64_t rows,
+                            int64_t row_bytes, hipStream_t s);
+lc_status moe_combine_launch(const void *h, int h_dt, const float *eo, const float *w,
+                             const int32_t *rowpos, void *out, int out_dt, int64_t T, int d,
+                             hipStream_t s);
+lc_status moe_bwd_gather_launch(const void *dy, int dy_dt, const float *eo, const int32_t *perm,
+                                const float *wrow, void *dys, int dys_dt, float *dw,
+                                int64_t rows, int d, hipStream_t s);
+lc_status moe_bwd_combine_launch(const float *dns, const float *dw, const float *w,
+                                 const int32_t *sel, const int32_t *rowpos, const void *wr,
+                                 int w_dt, float *dl, float *dn, int64_t T, int d,
+                                 hipStream_t s);
+lc_status moe_router_grad_launch(const void *n, int n_dt, const int32_t *sel, const float *dl,
+                                 float *scratch, size_t scratch_bytes, float *g, int64_t T,
+                                 int d, int E, hipStream_t s);
 
 }  // namespace lc

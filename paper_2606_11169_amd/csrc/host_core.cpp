@@ -43,6 +43,8 @@ lc_status validate_desc(const lc_stage_desc *d) {
     if (d->top_k != 2) return fail(LC_ERR_UNSUPPORTED, "MoE stages route to top_k == 2 experts");
     if (d->n_experts < 2) return fail(LC_ERR_INVALID_ARG, "MoE needs at least 2 experts");
     if (d->d_ff_expert <= 0) return fail(LC_ERR_INVALID_ARG, "d_ff_expert must be positive");
+    if (d->compute_dtype != LC_BF16)
+      return fail(LC_ERR_UNSUPPORTED, "MoE stages need compute_dtype LC_BF16 (grouped matrix-core products)");
   }
   // limits of the kernels in this build
   if (d->compute_dtype == LC_BF16) {
@@ -140,10 +142,11 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *o
     p.moe_sel = take((size_t)T * 2 * 4);
     p.moe_w = take((size_t)T * 2 * 4);
     p.moe_perm = take(R * 4);
+    p.moe_wrow = take(R * 4);
     p.moe_rowpos = take((size_t)T * 2 * 4);
-    p.moe_off = take((E + 1) * 4 + 256);
+    p.moe_off = take((E + 1) * 4);
     p.moe_xp = take(R * D * es);
-    p.moe_eo = take(R * D * es);
+    p.moe_eo = take(R * D * 4);
   }
   p.layer_bytes = lo;
   p.slot_bytes = lo * (size_t)d.n_layers;
@@ -165,8 +168,12 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *o
   p.s_norm_bytes = rmsnorm_scratch_size(T, d.d_model);
   p.s_norm = stake(p.s_norm_bytes);
   if (moe) {
-    // gradient of the routed rows' expert outputs and of the gate weights
-    p.s_moe = stake(R * D * es + (size_t)T * 2 * 4 * 2 + 4096);
+    p.s_moe_dys = stake(R * D * es);
+    p.s_moe_dns = stake(R * D * 4);
+    p.s_moe_dw = stake(R * 4);
+    p.s_moe_dl = stake((size_t)T * 2 * 4);
+    p.s_moe_part_bytes = moe_router_scratch_size(T, d.d_model, d.n_experts);
+    p.s_moe_part = stake(p.s_moe_part_bytes);
   }
   p.total = off;
   *out = p;
@@ -176,6 +183,11 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *o
 size_t rmsnorm_scratch_size(int64_t T, int64_t d) {
   const int64_t blocks = (T + kNormRowsPerBlock - 1) / kNormRowsPerBlock;
   return (size_t)(blocks * d) * sizeof(float);
+}
+
+size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E) {
+  const int64_t nblk = (T + kRouterTokensPerBlock - 1) / kRouterTokensPerBlock;
+  return (size_t)(nblk * E * d) * sizeof(float);
 }
 
 size_t attn_scratch_size(int64_t B, int64_t S, int64_t H) {

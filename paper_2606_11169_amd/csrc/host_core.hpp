@@ -16,6 +16,9 @@ lc_status fail(lc_status st, const char *fmt, ...) __attribute__((format(printf,
 constexpr int kNormRowsPerBlock = 32;
 size_t rmsnorm_scratch_size(int64_t T, int64_t d);
 size_t attn_scratch_size(int64_t B, int64_t S, int64_t H);
+// Tokens per block of the MoE router weight gradient's partial sums.
+constexpr int kRouterTokensPerBlock = 128;
+size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E);
 
 // Validates a stage descriptor (shapes, dtype, limits of this build).
 lc_status validate_desc(const lc_stage_desc *d);
@@ -53,8 +56,10 @@ struct StagePlan {
   size_t slot0, slot_bytes, layer_bytes;
   // offsets inside one layer block
   size_t xin, rstd1, n1, qkv, o, lse, h, rstd2, n2, gate, up, act;
-  // MoE per-layer extras (0 when dense)
-  size_t moe_sel, moe_w, moe_perm, moe_rowpos, moe_off, moe_xp, moe_eo;
+  // MoE per-layer extras (0 when dense): routing (sel, w [T, 2]), dispatch
+  // (perm, wrow [2T], rowpos [T, 2], expert offsets [E + 1]), the gathered
+  // expert inputs xp [2T, d] (op type) and expert outputs eo [2T, d] (fp32)
+  size_t moe_sel, moe_w, moe_perm, moe_wrow, moe_rowpos, moe_off, moe_xp, moe_eo;
   // backward scratch (one set, reused by every microbatch)
   size_t s_dy0, s_dy1;  // residual-stream gradient ping-pong [T, d] (res type)
   size_t s_dy16;        // operand copy of the current layer's dy [T, d] (op type)
@@ -66,7 +71,10 @@ struct StagePlan {
   size_t s_dh16;        // operand copy of dh [T, d] (op type)
   size_t s_attn, s_attn_bytes;  // attention backward scratch
   size_t s_norm, s_norm_bytes;  // RMSNorm backward scratch
-  size_t s_moe;         // MoE backward extras
+  // MoE backward: weighted expert-output gradients dys [2T, d] (op type),
+  // expert-input gradients dns [2T, d] (fp32), gate-weight gradients dw [2T],
+  // router-logit gradients dl [T, 2], router weight-gradient partial sums
+  size_t s_moe_dys, s_moe_dns, s_moe_dw, s_moe_dl, s_moe_part, s_moe_part_bytes;
   size_t total;
 };
 lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *out);

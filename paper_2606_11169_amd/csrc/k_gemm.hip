@@ -85,6 +85,9 @@ struct GemmP {
   uint32_t a_bytes, b_bytes;  // byte extent of each operand (< 2^31)
   int M, N, K;  // N: output columns (SwiGLU: gate/up width)
   int tiles_m, tiles_n;
+  int gmode, ngroups;
+  const int32_t *goff;
+  int64_t gstride_b, gstride_c;
   int rope_seq, rope_cols;
   int c_dt, r_dt, aux_dt;
 };
@@ -226,14 +229,42 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   int wg = blockIdx.x;
   const int nwg = gridDim.x;
   if ((nwg & 7) == 0) wg = (wg & 7) * (nwg >> 3) + (wg >> 3);
-  constexpr int GROUP = 8;
-  const int per_group = GROUP * p.tiles_n;
-  const int first_m = (wg / per_group) * GROUP;
-  const int gsz = min(p.tiles_m - first_m, GROUP);
-  const int tm = first_m + (wg % per_group) % gsz;
-  const int tn = (wg % per_group) / gsz;
-  const int m0 = tm * BM;
   constexpr bool SWI = (EPI == LC_EPI_SWIGLU);
+  int m0, tn, m_lim = p.M, kbeg = 0, kend = p.K;
+  const bf16_t *Bp = p.B;
+  void *Cp = p.C;
+  if (p.gmode == LC_GROUP_ROWS) {
+    // tile slot wg / tiles_n walks the groups' row tiles in order; slots past
+    // the last group's tiles have nothing to do (the grid is an upper bound)
+    tn = wg % p.tiles_n;
+    int slot = wg / p.tiles_n, g = 0, lo = 0, hi = 0;
+    for (; g < p.ngroups; ++g) {
+      lo = min(max(p.goff[g], 0), p.M);
+      hi = min(max(p.goff[g + 1], lo), p.M);
+      const int nt = (hi - lo + BM - 1) / BM;
+      if (slot < nt) break;
+      slot -= nt;
+    }
+    if (g == p.ngroups) return;  // uniform across the workgroup, before any barrier
+    m0 = lo + slot * BM;
+    m_lim = hi;
+    Bp = p.B + (int64_t)g * p.gstride_b;
+  } else {
+    int t = wg;
+    if (p.gmode == LC_GROUP_K) {
+      const int per = p.tiles_m * p.tiles_n, g = t / per;
+      t -= g * per;
+      kbeg = min(max(p.goff[g], 0), p.K);
+      kend = min(max(p.goff[g + 1], kbeg), p.K);
+      Cp = static_cast<char *>(p.C) + (int64_t)g * p.gstride_c * (p.c_dt == LC_FP32 ? 4 : 2);
+    }
+    constexpr int GROUP = 8;
+    const int per_group = GROUP * p.tiles_n;
+    const int first_m = (t / per_group) * GROUP;
+    const int gsz = min(p.tiles_m - first_m, GROUP);
+    m0 = (first_m + (t % per_group) % gsz) * BM;
+    tn = (t % per_group) / gsz;
+  }
   const int n0 = SWI ? tn * (BN / 2) : tn * BN;  // first output column
 
   f32x16_v acc[FM][FN];
@@ -245,17 +276,17 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   lds_t *const R0 = LDS_AS(char, ring);
-  const int nh = (p.K + KH - 1) / KH;  // halves
+  const int nh = (kend - kbeg + KH - 1) / KH;  // halves
   // group 0 streams the A halves, group 1 the B halves
-  const i32x4_v rs = grp == 0 ? make_rsrc(p.A, p.a_bytes) : make_rsrc(p.B, p.b_bytes);
+  const i32x4_v rs = grp == 0 ? make_rsrc(p.A, p.a_bytes) : make_rsrc(Bp, p.b_bytes);
   Stream<A_K, 0> sa_;
   Stream<B_K, SWI ? 1 : 0> sb_;
-  if (grp == 0) sa_.init(p.lda, m0, p.M, w4, lane);
+  if (grp == 0) sa_.init(p.lda, m0, m_lim, w4, lane);
   else sb_.init(p.ldb, n0, p.N, w4, lane);
   auto load = [&](int j) {  // this group's operand of half j
     lds_t *slot = R0 + (j & (NSLOT - 1)) * SLOT_BYTES;
-    if (grp == 0) sa_.load(rs, slot, w4, j * KH, p.K);
-    else sb_.load(rs, slot + HALF_BYTES, w4, j * KH, p.K);
+    if (grp == 0) sa_.load(rs, slot, w4, kbeg + j * KH, kend);
+    else sb_.load(rs, slot + HALF_BYTES, w4, kbeg + j * KH, kend);
   };
   // wait until this wave's loads of half j+1 have landed (loads retire in
   // order; the younger halves j+2, j+3 may stay in flight)
@@ -323,7 +354,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     const int m = m0 + wm * WM + i * 32 + frow;
-    if (m >= p.M) continue;
+    if (m >= m_lim) continue;
     if constexpr (EPI == LC_EPI_SWIGLU) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
@@ -341,7 +372,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
           const int64_t oa = (int64_t)m * p.ld_aux + n;
           store4_dt(p.aux0, oa, p.aux_dt, gt[0], gt[1], gt[2], gt[3]);
           store4_dt(p.aux1, oa, p.aux_dt, up[0], up[1], up[2], up[3]);
-          store4_dt(p.C, (int64_t)m * p.ldc + n, p.c_dt, a[0], a[1], a[2], a[3]);
+          store4_dt(Cp, (int64_t)m * p.ldc + n, p.c_dt, a[0], a[1], a[2], a[3]);
         }
       }
     } else if constexpr (EPI == LC_EPI_ROPE) {
@@ -373,8 +404,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
             }
           }
           const int64_t row = (int64_t)m * p.ldc + hbase;
-          store4_dt(p.C, row + c, p.c_dt, x1[0], x1[1], x1[2], x1[3]);
-          store4_dt(p.C, row + c + 64, p.c_dt, x2[0], x2[1], x2[2], x2[3]);
+          store4_dt(Cp, row + c, p.c_dt, x1[0], x1[1], x1[2], x1[3]);
+          store4_dt(Cp, row + c + 64, p.c_dt, x2[0], x2[1], x2[2], x2[3]);
         }
       }
     } else {
@@ -388,12 +419,12 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
           float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
           const int64_t oc = (int64_t)m * p.ldc + n;
           if constexpr (EPI == LC_EPI_STORE) {
-            store4_dt(p.C, oc, p.c_dt, v0, v1, v2, v3);
+            store4_dt(Cp, oc, p.c_dt, v0, v1, v2, v3);
           } else if constexpr (EPI == LC_EPI_RESIDUAL) {
             const float4 r = load4_dt(p.R, (int64_t)m * p.ldr + n, p.r_dt);
-            store4_dt(p.C, oc, p.c_dt, r.x + v0, r.y + v1, r.z + v2, r.w + v3);
+            store4_dt(Cp, oc, p.c_dt, r.x + v0, r.y + v1, r.z + v2, r.w + v3);
           } else if constexpr (EPI == LC_EPI_ACCUM_F32) {
-            float4 *cp = reinterpret_cast<float4 *>(static_cast<float *>(p.C) + oc);
+            float4 *cp = reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc);
             float4 c = *cp;
             c.x += v0;
             c.y += v1;
@@ -414,8 +445,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
               dg[e] = dv[e] * uv[e] * s * (1.0f + gv[e] * (1.0f - s));
               du[e] = dv[e] * gv[e] * s;
             }
-            store4_dt(p.C, oc, p.c_dt, dg[0], dg[1], dg[2], dg[3]);
-            store4_dt(p.C, oc + p.N, p.c_dt, du[0], du[1], du[2], du[3]);
+            store4_dt(Cp, oc, p.c_dt, dg[0], dg[1], dg[2], dg[3]);
+            store4_dt(Cp, oc + p.N, p.c_dt, du[0], du[1], du[2], du[3]);
           }
         }
       }
@@ -425,7 +456,11 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
 
 template <bool A_K, bool B_K, int EPI>
 lc_status launch_t(const GemmP &p, hipStream_t s) {
-  const unsigned grid = (unsigned)p.tiles_m * (unsigned)p.tiles_n;
+  // LC_GROUP_ROWS: an upper bound on the groups' row tiles (each group adds at
+  // most one partial tile); LC_GROUP_K: every group has the full output grid
+  unsigned grid = (unsigned)p.tiles_m * (unsigned)p.tiles_n;
+  if (p.gmode == LC_GROUP_ROWS) grid = (unsigned)(p.tiles_m + p.ngroups) * (unsigned)p.tiles_n;
+  if (p.gmode == LC_GROUP_K) grid *= (unsigned)p.ngroups;
   hipLaunchKernelGGL((gemm_bf16_kernel<A_K, B_K, EPI>), dim3(grid), dim3(NT), 0, s, p);
   return check_launch("gemm_bf16_kernel");
 }
@@ -469,6 +504,19 @@ static lc_status check_gemm_args(const lc_gemm_args &a) {
   } else if (a.ldc < a.N) {
     return fail(LC_ERR_INVALID_ARG, "gemm: ldc < N");
   }
+  if (a.group_mode != LC_GROUP_NONE) {
+    if (a.group_mode != LC_GROUP_ROWS && a.group_mode != LC_GROUP_K)
+      return fail(LC_ERR_INVALID_ARG, "gemm: unknown group mode %d", a.group_mode);
+    if (a.n_groups < 1 || a.n_groups > 64) return fail(LC_ERR_INVALID_ARG, "gemm: n_groups must be 1..64");
+    if (!a.group_offsets || (reinterpret_cast<uintptr_t>(a.group_offsets) & 3))
+      return fail(LC_ERR_INVALID_ARG, "gemm: group offsets must be a 4-byte aligned device array");
+    if (a.epilogue == LC_EPI_ROPE || a.epilogue == LC_EPI_RESIDUAL)
+      return fail(LC_ERR_UNSUPPORTED, "gemm: grouped products take STORE, ACCUM or SwiGLU epilogues");
+    if (a.group_mode == LC_GROUP_ROWS && a.group_stride_b < 0)
+      return fail(LC_ERR_INVALID_ARG, "gemm: negative group_stride_b");
+    if (a.group_mode == LC_GROUP_K && (a.a_kmajor || a.b_kmajor || a.group_stride_c < 0))
+      return fail(LC_ERR_UNSUPPORTED, "gemm: LC_GROUP_K needs m/n-major operands and group_stride_c >= 0");
+  }
   if (a.epilogue == LC_EPI_ROPE) {
     if (!a.rope_cos || !a.rope_sin || a.rope_seq <= 0 || a.rope_cols < 0 ||
         a.head_dim <= 0 || a.head_dim % 2 || a.rope_cols % a.head_dim || a.N % a.head_dim)
@@ -479,6 +527,8 @@ static lc_status check_gemm_args(const lc_gemm_args &a) {
 
 lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
   LC_TRY(check_gemm_args(a));
+  if (a.dtype == LC_FP32 && a.group_mode != LC_GROUP_NONE)
+    return fail(LC_ERR_UNSUPPORTED, "gemm fp32: grouped products need bf16 operands");
   if (a.dtype == LC_FP32) {
     if (c_type(a) != LC_FP32 || (a.epilogue == LC_EPI_RESIDUAL && a.r_dtype != LC_FP32) ||
         ((a.epilogue == LC_EPI_SWIGLU || a.epilogue == LC_EPI_SWIGLU_BWD) &&
@@ -526,6 +576,11 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
   p.tiles_m = (int)((a.M + BM - 1) / BM);
   p.tiles_n = a.epilogue == LC_EPI_SWIGLU ? (int)((a.N + BN / 2 - 1) / (BN / 2))
                                           : (int)((a.N + BN - 1) / BN);
+  p.gmode = a.group_mode;
+  p.ngroups = a.group_mode == LC_GROUP_NONE ? 1 : a.n_groups;
+  p.goff = a.group_offsets;
+  p.gstride_b = a.group_stride_b;
+  p.gstride_c = a.group_stride_c;
   p.rope_seq = a.rope_seq;
   p.rope_cols = a.rope_cols;
   p.c_dt = c_type(a);

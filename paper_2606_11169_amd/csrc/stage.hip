@@ -87,6 +87,119 @@ static LayerBufs layer_bufs(lc_stage *st, int slot, int l) {
   return b;
 }
 
+// MoE FFN of one layer (Chunk F): route, dispatch, gather, two grouped
+// expert products, weighted combine with the residual h.
+static lc_status moe_forward(lc_stage *st, const W &w, const LayerBufs &L, void *out, int out_dt,
+                             hipStream_t s) {
+  const lc_stage_desc &d = st->d;
+  const StagePlan &P = st->plan;
+  const ParamPlan &pp = st->pp;
+  const int dt = d.compute_dtype;
+  const StageTypes ty = P.ty;
+  const int64_t T = P.T, D = d.d_model, FE = d.d_ff_expert, R = 2 * T;
+  const int E = d.n_experts;
+  lc_moe_args ma;
+  memset(&ma, 0, sizeof ma);
+  ma.T = T; ma.d = (int32_t)D; ma.E = E; ma.n_dtype = ty.op; ma.w_dtype = dt;
+  ma.n = L.at(P.n2); ma.wr = w.wp(pp.wr);
+  ma.sel = static_cast<int32_t *>(L.at(P.moe_sel));
+  ma.w = static_cast<float *>(L.at(P.moe_w));
+  ma.offsets = static_cast<int32_t *>(L.at(P.moe_off));
+  ma.perm = static_cast<int32_t *>(L.at(P.moe_perm));
+  ma.wrow = static_cast<float *>(L.at(P.moe_wrow));
+  ma.rowpos = static_cast<int32_t *>(L.at(P.moe_rowpos));
+  LC_TRY(moe_route_launch(ma, s));
+  LC_TRY(moe_dispatch_launch(ma, s));
+  LC_TRY(moe_gather_launch(L.at(P.n2), L.at(P.moe_xp), ma.perm, R, D * (int64_t)P.elem, s));
+  // gate, up = xp [W1_e; W3_e]^T per expert; act = silu(gate) * up
+  lc_gemm_args a = gemm_base(dt, LC_EPI_SWIGLU, R, FE, D);
+  a.A = L.at(P.moe_xp); a.lda = D; a.a_kmajor = 1;
+  a.B = w.wp(pp.expert0); a.ldb = D; a.b_kmajor = 1;
+  a.C = L.at(P.act); a.ldc = FE; a.c_dtype = ty.op;
+  a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = FE; a.aux_dtype = ty.res;
+  a.group_mode = LC_GROUP_ROWS; a.n_groups = E; a.group_offsets = ma.offsets;
+  a.group_stride_b = (int64_t)pp.expert_stride;
+  LC_TRY(gemm_launch(a, s));
+  // eo = act W2_e^T per expert (fp32)
+  a = gemm_base(dt, LC_EPI_STORE_F32, R, D, FE);
+  a.A = L.at(P.act); a.lda = FE; a.a_kmajor = 1;
+  a.B = w.wp(pp.expert0 + 2 * FE * D); a.ldb = FE; a.b_kmajor = 1;
+  a.C = L.at(P.moe_eo); a.ldc = D;
+  a.group_mode = LC_GROUP_ROWS; a.n_groups = E; a.group_offsets = ma.offsets;
+  a.group_stride_b = (int64_t)pp.expert_stride;
+  LC_TRY(gemm_launch(a, s));
+  // out = h + w0 eo[rowpos0] + w1 eo[rowpos1]
+  return moe_combine_launch(L.at(P.h), ty.res, static_cast<const float *>(L.at(P.moe_eo)), ma.w,
+                            ma.rowpos, out, out_dt, T, (int)D, s);
+}
+
+// MoE FFN of one layer (Chunk B): given dy (the gradient at the layer output),
+// writes dn = dL/dn2 (fp32, P.s_dn) and adds the expert and router weight
+// gradients into the bucket.
+static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, const void *dy,
+                              int dy_dt, hipStream_t s) {
+  const lc_stage_desc &d = st->d;
+  const StagePlan &P = st->plan;
+  const ParamPlan &pp = st->pp;
+  const int dt = d.compute_dtype;
+  const StageTypes ty = P.ty;
+  const int64_t T = P.T, D = d.d_model, FE = d.d_ff_expert, R = 2 * T;
+  const int E = d.n_experts;
+  char *ws = st->ws;
+  const int32_t *off = static_cast<const int32_t *>(L.at(P.moe_off));
+  const float *eo = static_cast<const float *>(L.at(P.moe_eo));
+  void *dys = ws + P.s_moe_dys;
+  float *dns = reinterpret_cast<float *>(ws + P.s_moe_dns);
+  float *dw = reinterpret_cast<float *>(ws + P.s_moe_dw);
+  float *dl = reinterpret_cast<float *>(ws + P.s_moe_dl);
+  void *da = ws + P.s_da;
+  // dys[r] = wrow[r] dy[perm[r]], dw[r] = dy[perm[r]] . eo[r]
+  LC_TRY(moe_bwd_gather_launch(dy, dy_dt, eo, static_cast<const int32_t *>(L.at(P.moe_perm)),
+                               static_cast<const float *>(L.at(P.moe_wrow)), dys, ty.op, dw, R,
+                               (int)D, s));
+  // [dgate | dup] = SwiGLU'(dys W2_e) per expert
+  lc_gemm_args a = gemm_base(dt, LC_EPI_SWIGLU_BWD, R, FE, D);
+  a.A = dys; a.lda = D; a.a_kmajor = 1;
+  a.B = w.wp(pp.expert0 + 2 * FE * D); a.ldb = FE; a.b_kmajor = 0;
+  a.C = da; a.ldc = 2 * FE; a.c_dtype = ty.op;
+  a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = FE; a.aux_dtype = ty.res;
+  a.group_mode = LC_GROUP_ROWS; a.n_groups = E; a.group_offsets = off;
+  a.group_stride_b = (int64_t)pp.expert_stride;
+  LC_TRY(gemm_launch(a, s));
+  // G[W2_e] += dys_e^T act_e over each expert's rows
+  a = gemm_base(dt, LC_EPI_ACCUM_F32, D, FE, R);
+  a.A = dys; a.lda = D; a.a_kmajor = 0;
+  a.B = L.at(P.act); a.ldb = FE; a.b_kmajor = 0;
+  a.C = w.gp(pp.expert0 + 2 * FE * D); a.ldc = FE;
+  a.group_mode = LC_GROUP_K; a.n_groups = E; a.group_offsets = off;
+  a.group_stride_c = (int64_t)pp.expert_stride;
+  LC_TRY(gemm_launch(a, s));
+  // dns = [dgate | dup] [W1_e; W3_e] per expert (fp32)
+  a = gemm_base(dt, LC_EPI_STORE_F32, R, D, 2 * FE);
+  a.A = da; a.lda = 2 * FE; a.a_kmajor = 1;
+  a.B = w.wp(pp.expert0); a.ldb = D; a.b_kmajor = 0;
+  a.C = dns; a.ldc = D;
+  a.group_mode = LC_GROUP_ROWS; a.n_groups = E; a.group_offsets = off;
+  a.group_stride_b = (int64_t)pp.expert_stride;
+  LC_TRY(gemm_launch(a, s));
+  // G[W1_e; W3_e] += [dgate | dup]_e^T xp_e
+  a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * FE, D, R);
+  a.A = da; a.lda = 2 * FE; a.a_kmajor = 0;
+  a.B = L.at(P.moe_xp); a.ldb = D; a.b_kmajor = 0;
+  a.C = w.gp(pp.expert0); a.ldc = D;
+  a.group_mode = LC_GROUP_K; a.n_groups = E; a.group_offsets = off;
+  a.group_stride_c = (int64_t)pp.expert_stride;
+  LC_TRY(gemm_launch(a, s));
+  // dn = dns[rowpos0] + dns[rowpos1] + dl Wr; then G[Wr] += dl^T n2
+  const int32_t *sel = static_cast<const int32_t *>(L.at(P.moe_sel));
+  LC_TRY(moe_bwd_combine_launch(dns, dw, static_cast<const float *>(L.at(P.moe_w)), sel,
+                                static_cast<const int32_t *>(L.at(P.moe_rowpos)), w.wp(pp.wr), dt,
+                                dl, reinterpret_cast<float *>(ws + P.s_dn), T, (int)D, s));
+  return moe_router_grad_launch(L.at(P.n2), ty.op, sel, dl,
+                                reinterpret_cast<float *>(ws + P.s_moe_part), P.s_moe_part_bytes,
+                                w.gp(pp.wr), T, (int)D, E, s);
+}
+
 static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const void *x, void *y,
                                 int slot, hipStream_t s) {
   const lc_stage_desc &d = st->d;
@@ -142,7 +255,10 @@ static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const voi
     na.n = L.at(P.n2);
     na.rstd = static_cast<float *>(L.at(P.rstd2));
     LC_TRY(rmsnorm_fwd_launch(na, s));
-    if (d.n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
+    if (d.n_experts > 0) {
+      LC_TRY(moe_forward(st, w, L, out, last ? dt : ty.res, s));
+      continue;
+    }
     // gate, up = n2 W1^T, n2 W3^T; act = silu(gate) * up
     a = gemm_base(dt, LC_EPI_SWIGLU, T, F, D);
     a.A = L.at(P.n2); a.lda = D; a.a_kmajor = 1;
@@ -188,9 +304,12 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     void *da = ws + P.s_da, *dn = ws + P.s_dn, *dh = ws + P.s_dh, *dO = ws + P.s_do;
     void *dh_op = copies ? ws + P.s_dh16 : dh;
     char *dqkv = ws + P.s_dqkv;
-    if (d.n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
+    lc_gemm_args a;
+    if (d.n_experts > 0) {
+      LC_TRY(moe_backward(st, w, L, dy_res, dy_dt, s));
+    } else {
     // [dgate | dup] = SwiGLU'(dy W2)
-    lc_gemm_args a = gemm_base(dt, LC_EPI_SWIGLU_BWD, T, F, D);
+    a = gemm_base(dt, LC_EPI_SWIGLU_BWD, T, F, D);
     a.A = dy_op; a.lda = D; a.a_kmajor = 1;
     a.B = w.wp(pp.w2); a.ldb = F; a.b_kmajor = 0;
     a.C = da; a.ldc = 2 * F; a.c_dtype = ty.op;
@@ -214,6 +333,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.w1); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
+    }
     // dh = dy + RMSNorm2'(dn2); G[g2] += ...
     lc_norm_args nb = norm_base(T, D, d.rms_eps);
     nb.dn = dn; nb.dn_dtype = ty.res;
@@ -338,7 +458,6 @@ lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_
   StagePlan plan;
   LC_TRY(validate_desc(desc));
   LC_TRY(stage_plan(*desc, max_in_flight, &plan));
-  if (desc->n_experts > 0) return fail(LC_ERR_UNSUPPORTED, "MoE stages are not built yet");
   if (!workspace) return fail(LC_ERR_INVALID_ARG, "null workspace");
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(LC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
@@ -402,6 +521,20 @@ lc_status chunk_backward(lc_stage *stage, const lc_param_bufs *params, const lc_
   if (mb->mb < 0 || find_slot(stage, mb->mb) < 0)
     return fail(LC_ERR_STATE, "microbatch %d has no stashed forward", mb->mb);
   return do_backward(stage, params, mb, static_cast<hipStream_t>(stream));
+}
+
+lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32_t *sel_out,
+                               void *stream) {
+  if (!stage || !sel_out) return fail(LC_ERR_INVALID_ARG, "null stage or output");
+  if (stage->d.n_experts <= 0) return fail(LC_ERR_INVALID_ARG, "dense stage has no routing");
+  if (layer < 0 || layer >= stage->d.n_layers) return fail(LC_ERR_INVALID_ARG, "layer out of range");
+  const int slot = mb < 0 ? -1 : find_slot(stage, mb);
+  if (slot < 0) return fail(LC_ERR_STATE, "microbatch %d is not stashed", mb);
+  const LayerBufs L = layer_bufs(stage, slot, layer);
+  const size_t bytes = (size_t)stage->plan.T * 2 * sizeof(int32_t);
+  hipError_t e = hipMemcpyAsync(sel_out, L.at(stage->plan.moe_sel), bytes, hipMemcpyDeviceToDevice,
+                                static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LC_OK : hip_fail(e, "copying the routing");
 }
 
 lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,

@@ -36,6 +36,7 @@ LC_PASS_F, LC_PASS_B = 0, 1
  LC_T_WR) = range(10)
 (LC_EPI_STORE, LC_EPI_STORE_F32, LC_EPI_ACCUM_F32, LC_EPI_RESIDUAL, LC_EPI_ROPE,
  LC_EPI_SWIGLU, LC_EPI_SWIGLU_BWD) = range(7)
+LC_GROUP_NONE, LC_GROUP_ROWS, LC_GROUP_K = 0, 1, 2
 
 
 class LibchunkError(RuntimeError):
@@ -88,7 +89,18 @@ class lc_gemm_args(C.Structure):
                 ("aux0", C.c_void_p), ("aux1", C.c_void_p), ("ld_aux", C.c_int64),
                 ("rope_cos", C.c_void_p), ("rope_sin", C.c_void_p),
                 ("rope_seq", C.c_int32), ("rope_cols", C.c_int32), ("head_dim", C.c_int32),
-                ("reserved1", C.c_int32)]
+                ("reserved1", C.c_int32),
+                ("group_mode", C.c_int32), ("n_groups", C.c_int32),
+                ("group_offsets", C.c_void_p), ("group_stride_b", C.c_int64),
+                ("group_stride_c", C.c_int64)]
+
+
+class lc_moe_args(C.Structure):
+    _fields_ = [("T", C.c_int64), ("d", C.c_int32), ("E", C.c_int32),
+                ("n_dtype", C.c_int32), ("w_dtype", C.c_int32),
+                ("n", C.c_void_p), ("wr", C.c_void_p), ("sel", C.c_void_p), ("w", C.c_void_p),
+                ("offsets", C.c_void_p), ("perm", C.c_void_p), ("wrow", C.c_void_p),
+                ("rowpos", C.c_void_p)]
 
 
 class lc_norm_args(C.Structure):
@@ -143,6 +155,10 @@ _SIGS = {
     "lc_attention_backward": (C.c_int, [C.POINTER(lc_attn_args), C.c_void_p]),
     "lc_attention_scratch_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32]),
     "lc_cast_bf16": (C.c_int, [C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "lc_moe_route": (C.c_int, [C.POINTER(lc_moe_args), C.c_void_p]),
+    "lc_moe_dispatch": (C.c_int, [C.POINTER(lc_moe_args), C.c_void_p]),
+    "lc_stage_moe_routing": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                                       C.c_void_p]),
 }
 
 EXPORTED = tuple(_SIGS)
@@ -332,7 +348,8 @@ def lc_cast_bf16(inp, out, n, stream=None):
 
 def lc_gemm(dtype, epilogue, M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, Cm, ldc, R=None,
             ldr=0, aux0=None, aux1=None, ld_aux=0, rope_cos=None, rope_sin=None, rope_seq=0,
-            rope_cols=0, head_dim=0, c_dtype=None, r_dtype=None, aux_dtype=None, stream=None):
+            rope_cols=0, head_dim=0, c_dtype=None, r_dtype=None, aux_dtype=None, stream=None,
+            group_mode=0, n_groups=0, group_offsets=None, group_stride_b=0, group_stride_c=0):
     """C = A.B^T with an epilogue (lc_gemm_args); c/r/aux dtypes default to `dtype`."""
     a = lc_gemm_args()
     a.dtype, a.epilogue = dtype, epilogue
@@ -347,6 +364,9 @@ def lc_gemm(dtype, epilogue, M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, Cm, ld
     a.aux0, a.aux1, a.ld_aux = ptr(aux0) or None, ptr(aux1) or None, ld_aux
     a.rope_cos, a.rope_sin = ptr(rope_cos) or None, ptr(rope_sin) or None
     a.rope_seq, a.rope_cols, a.head_dim = rope_seq, rope_cols, head_dim
+    a.group_mode, a.n_groups = group_mode, n_groups
+    a.group_offsets = ptr(group_offsets) or None
+    a.group_stride_b, a.group_stride_c = group_stride_b, group_stride_c
     return _check(lib().lc_gemm(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
 
 
@@ -393,3 +413,26 @@ def lc_attention_backward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, dout,
               ld_dqkv=ld_dqkv, rope_cos=rope_cos, rope_sin=rope_sin, scratch=scratch,
               scratch_bytes=scratch_bytes)
     return _check(lib().lc_attention_backward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_moe_route(T, d, E, n, wr, sel, w, n_dtype, w_dtype, stream=None):
+    """Router: top-2 experts and renormalised gate weights per token."""
+    a = _fill(lc_moe_args(), T=T, d=d, E=E, n_dtype=n_dtype, w_dtype=w_dtype)
+    a.n, a.wr, a.sel, a.w = ptr(n) or None, ptr(wr) or None, ptr(sel) or None, ptr(w) or None
+    return _check(lib().lc_moe_route(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_moe_dispatch(T, E, sel, w, offsets, perm, wrow, rowpos, stream=None):
+    """Stable grouping of the (token, expert) pairs by expert."""
+    a = _fill(lc_moe_args(), T=T, d=8, E=E, n_dtype=LC_BF16, w_dtype=LC_BF16)
+    a.sel, a.w = ptr(sel) or None, ptr(w) or None
+    a.offsets, a.perm = ptr(offsets) or None, ptr(perm) or None
+    a.wrow, a.rowpos = ptr(wrow) or None, ptr(rowpos) or None
+    return _check(lib().lc_moe_dispatch(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_stage_moe_routing(stage, mb, layer, sel_out, stream=None):
+    """Copies the routing of a stashed microbatch's layer into `sel_out` [T, 2] int32."""
+    return _check(lib().lc_stage_moe_routing(stage.handle, C.c_int32(mb), C.c_int32(layer),
+                                             C.c_void_p(ptr(sel_out)),
+                                             C.c_void_p(stream_ptr(stream) or None)))

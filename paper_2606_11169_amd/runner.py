@@ -79,6 +79,13 @@ class StageRunner:
         lc.chunk_backward(self.stage, self.w, self.grad, mb, self.dY[mb], self.dX[mb],
                           self.stream)
 
+    def moe_routing(self, mb: int, layer: int) -> np.ndarray:
+        """The experts chosen for each token of a stashed microbatch's layer, [T, 2]."""
+        out = torch.empty((self.T, 2), dtype=torch.int32, device=self.device)
+        lc.lc_stage_moe_routing(self.stage, mb, layer, out, self.stream)
+        torch.cuda.synchronize()
+        return out.cpu().numpy()
+
     def run_order(self, entries: Sequence[Tuple[int, int]]):
         lc.lc_run_order(self.stage, self.w, self.grad, entries, self.X, self.Y, self.dY, self.dX,
                         self.stream)

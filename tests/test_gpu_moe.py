@@ -1,0 +1,271 @@
+"""Parity of the mixture-of-experts path (router, dispatch, grouped expert
+products, the whole MoE stage) with the oracle.
+
+* router: the selected experts agree with the oracle's top-2 of its float64
+  softmax on the same bf16 inputs except where the two candidates' oracle
+  probabilities are within 1e-4 (near-ties fp32 logits may order either
+  way); gate weights within 1e-5; the zero-router closed form (ties to
+  experts 0 and 1, weights exactly 1/2)
+* dispatch: offsets, permutation, row positions and row weights bit-exact
+  against the oracle's grouping of the GPU's own routing (integer work)
+* grouped products: integer-valued operands make every sum exact, so each
+  group's rows / k range are compared bit for bit, with empty groups and
+  groups that end inside a tile
+* MoE stage: Y, dX and every gradient tensor within 2e-2 of the oracle run
+  with the GPU's routing as a routing override (the gate weights still come
+  from the oracle's own logits); the GPU routing differs from the oracle's
+  own routing only at near-ties (probability gap below 1e-2)
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import stage as OS
+from paper_2606_11169_amd import libchunk as lc
+from paper_2606_11169_amd.runner import StageRunner, require_gpu
+from tests.gpu_util import DEV, banner, bf16, f32, host, rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+def bf16_round(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).float().numpy()
+
+
+def i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(DEV)
+
+
+def random_routing(rng, T, E):
+    sel = np.stack([rng.choice(E, size=2, replace=False) for _ in range(T)]).astype(np.int32)
+    w0 = rng.uniform(0.5, 1.0, size=T).astype(np.float32)
+    return sel, np.stack([w0, 1.0 - w0], axis=1).astype(np.float32)
+
+
+# ---------------------------------------------------------------- router
+
+@pytest.mark.parametrize("T,d,E", [(1000, 256, 8), (129, 512, 2), (64, 128, 64)])
+def test_router_matches_oracle(T, d, E):
+    banner(f"moe route T={T} d={d} E={E}")
+    rng = np.random.default_rng(T + d + E)
+    n = bf16_round(rng.standard_normal((T, d)))
+    wr = bf16_round(0.02 * rng.standard_normal((E, d)))
+    sel = torch.empty((T, 2), dtype=torch.int32, device=DEV)
+    w = torch.empty((T, 2), dtype=torch.float32, device=DEV)
+    lc.lc_moe_route(T, d, E, bf16(n), bf16(wr), sel, w, lc.LC_BF16, lc.LC_BF16)
+    torch.cuda.synchronize()
+    gs, gw = sel.cpu().numpy(), host(w)
+    _, pi, osel, ow = OS.moe_route(n.astype(np.float64), wr.astype(np.float64), 2)
+    assert np.all(gs[:, 0] != gs[:, 1])
+    rows = np.arange(T)
+    same = np.all(gs == osel, axis=1)
+    for t in np.nonzero(~same)[0]:
+        gap = np.max(np.abs(pi[t, gs[t]] - pi[t, osel[t]]))
+        assert gap < 1e-4, f"token {t}: GPU {gs[t]} vs oracle {osel[t]}, probability gap {gap}"
+    assert np.max(np.abs(gw[same] - ow[same])) <= 1e-5
+    assert same.mean() > 0.99
+    del rows
+
+
+def test_router_zero_weights_tie_to_lowest_experts():
+    banner("moe route zero router")
+    T, d, E = 300, 256, 8
+    n = bf16_round(np.random.default_rng(1).standard_normal((T, d)))
+    sel = torch.empty((T, 2), dtype=torch.int32, device=DEV)
+    w = torch.empty((T, 2), dtype=torch.float32, device=DEV)
+    lc.lc_moe_route(T, d, E, bf16(n), bf16(np.zeros((E, d))), sel, w, lc.LC_BF16, lc.LC_BF16)
+    torch.cuda.synchronize()
+    assert np.all(sel.cpu().numpy() == np.array([0, 1]))
+    assert np.all(host(w) == 0.5)
+
+
+# ---------------------------------------------------------------- dispatch
+
+@pytest.mark.parametrize("T,E", [(1, 2), (1000, 8), (3000, 8), (2500, 64), (1024, 3)])
+def test_dispatch_bit_exact(T, E):
+    banner(f"moe dispatch T={T} E={E}")
+    rng = np.random.default_rng(7 * T + E)
+    sel, w = random_routing(rng, T, E)
+    off = torch.full((E + 1,), -7, dtype=torch.int32, device=DEV)
+    perm = torch.full((2 * T,), -7, dtype=torch.int32, device=DEV)
+    wrow = torch.full((2 * T,), -7.0, dtype=torch.float32, device=DEV)
+    rowpos = torch.full((T, 2), -7, dtype=torch.int32, device=DEV)
+    lc.lc_moe_dispatch(T, E, i32(sel), f32(w), off, perm, wrow, rowpos)
+    torch.cuda.synchronize()
+    ooff, operm, orowpos = OS.moe_dispatch(sel, E)
+    assert np.array_equal(off.cpu().numpy(), ooff)
+    assert np.array_equal(perm.cpu().numpy(), operm)
+    assert np.array_equal(rowpos.cpu().numpy(), orowpos)
+    slot = np.zeros(2 * T, np.int64)
+    for k in range(2):
+        slot[orowpos[:, k]] = k
+    want = w[operm, slot]
+    assert np.array_equal(wrow.cpu().numpy().view(np.uint32), want.view(np.uint32))
+
+
+def test_dispatch_skips_invalid_pairs():
+    """A repeated or out-of-range expert is not placed (rowpos -1); the rows
+    past the placed ones read token 0 with weight 0."""
+    banner("moe dispatch invalid pairs")
+    T, E = 5, 4
+    sel = np.array([[0, 1], [2, 2], [3, 9], [1, 0], [-1, 3]], np.int32)
+    w = np.full((T, 2), 0.5, np.float32)
+    off = torch.empty(E + 1, dtype=torch.int32, device=DEV)
+    perm = torch.full((2 * T,), -7, dtype=torch.int32, device=DEV)
+    wrow = torch.full((2 * T,), -7.0, dtype=torch.float32, device=DEV)
+    rowpos = torch.full((T, 2), -7, dtype=torch.int32, device=DEV)
+    lc.lc_moe_dispatch(T, E, i32(sel), f32(w), off, perm, wrow, rowpos)
+    torch.cuda.synchronize()
+    assert off.cpu().numpy().tolist() == [0, 2, 4, 5, 7]
+    assert perm.cpu().numpy().tolist() == [0, 3, 0, 3, 1, 2, 4, 0, 0, 0]
+    assert rowpos.cpu().numpy().tolist() == [[0, 2], [4, -1], [5, -1], [3, 1], [-1, 6]]
+    assert host(wrow).tolist()[7:] == [0.0, 0.0, 0.0]
+
+
+# ---------------------------------------------------------------- grouped products
+
+def ints(rng, shape, lo=-8, hi=8):
+    return rng.integers(lo, hi + 1, size=shape).astype(np.float32)
+
+
+@pytest.mark.parametrize("b_kmajor", [True, False], ids=["NT", "NN"])
+def test_grouped_rows_bit_exact(b_kmajor):
+    banner(f"grouped rows b_kmajor={b_kmajor}")
+    rng = np.random.default_rng(3)
+    sizes = [300, 0, 17, 512, 256, 1]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    G, R, N, K = len(sizes), int(off[-1]) + 40, 264, 200
+    A = ints(rng, (R, K))
+    Bs = [ints(rng, (N, K)) for _ in range(G)]
+    stride = N * K
+    Bflat = np.concatenate([(b if b_kmajor else b.T.copy()).ravel() for b in Bs])
+    C = torch.full((R, N), -1.0, dtype=torch.float32, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE_F32, R, N, K, bf16(A), K, 1, bf16(Bflat),
+               K if b_kmajor else N, int(b_kmajor), C, N, group_mode=lc.LC_GROUP_ROWS,
+               n_groups=G, group_offsets=i32(off), group_stride_b=stride)
+    torch.cuda.synchronize()
+    got = host(C)
+    for g in range(G):
+        rows = slice(off[g], off[g + 1])
+        want = A[rows].astype(np.int64) @ Bs[g].astype(np.int64).T
+        assert np.array_equal(got[rows], want.astype(np.float64)), f"group {g}"
+    assert np.all(got[off[-1]:] == -1.0)  # rows past the last group untouched
+
+
+def test_grouped_swiglu_rows_matches_per_group():
+    banner("grouped rows swiglu")
+    rng = np.random.default_rng(4)
+    sizes = [130, 0, 400]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    G, R, F, D = len(sizes), int(off[-1]), 128, 256
+    A = bf16_round(rng.standard_normal((R, D)))
+    W = [bf16_round(0.05 * rng.standard_normal((2 * F, D))) for _ in range(G)]
+    act = torch.empty((R, F), dtype=torch.bfloat16, device=DEV)
+    gate = torch.empty((R, F), dtype=torch.float32, device=DEV)
+    up = torch.empty_like(gate)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_SWIGLU, R, F, D, bf16(A), D, 1,
+               bf16(np.concatenate([w.ravel() for w in W])), D, 1, act, F, aux0=gate, aux1=up,
+               ld_aux=F, aux_dtype=lc.LC_FP32, group_mode=lc.LC_GROUP_ROWS, n_groups=G,
+               group_offsets=i32(off), group_stride_b=2 * F * D)
+    torch.cuda.synchronize()
+    for g in range(G):
+        rows = slice(off[g], off[g + 1])
+        gt = A[rows].astype(np.float64) @ W[g][:F].T.astype(np.float64)
+        u = A[rows].astype(np.float64) @ W[g][F:].T.astype(np.float64)
+        if sizes[g] == 0:
+            continue
+        assert rel_err(host(gate)[rows], gt) <= 1e-5
+        assert rel_err(host(up)[rows], u) <= 1e-5
+        a = gt / (1.0 + np.exp(-gt)) * u
+        assert rel_err(host(act)[rows], a) <= 1e-2
+
+
+def test_grouped_k_bit_exact():
+    banner("grouped k")
+    rng = np.random.default_rng(5)
+    sizes = [70, 0, 300, 1, 257]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    G, Ktot, M, N = len(sizes), int(off[-1]) + 9, 264, 136
+    A = ints(rng, (Ktot, M))   # A(m, k) = A[k, m]
+    B = ints(rng, (Ktot, N))   # B(n, k) = B[k, n]
+    C0 = ints(rng, (G, M, N), -1000, 1000)
+    C = f32(C0.reshape(-1))
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ACCUM_F32, M, N, Ktot, bf16(A), M, 0, bf16(B), N, 0, C, N,
+               group_mode=lc.LC_GROUP_K, n_groups=G, group_offsets=i32(off),
+               group_stride_c=M * N)
+    torch.cuda.synchronize()
+    got = host(C).reshape(G, M, N)
+    for g in range(G):
+        ks = slice(off[g], off[g + 1])
+        want = C0[g] + (A[ks].astype(np.int64).T @ B[ks].astype(np.int64))
+        assert np.array_equal(got[g], want.astype(np.float64)), f"group {g}"
+
+
+# ---------------------------------------------------------------- stage
+
+SMALL_MOE = synth.StageConfig(
+    name="small_moe", n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ff=0, seq_len=256,
+    micro_batch=2, num_microbatches=2, bf16=True, n_experts=4, top_k=2, d_ff_expert=128,
+    pp_size=2, pp_rank=0)
+
+
+def desc_of(cfg):
+    return lc.make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
+                        cfg.seq_len, cfg.micro_batch, cfg.bf16, n_experts=cfg.n_experts,
+                        top_k=cfg.top_k, d_ff_expert=cfg.d_ff_expert, rms_eps=cfg.rms_eps,
+                        rope_base=cfg.rope_base)
+
+
+def test_moe_stage_matches_oracle_with_gpu_routing():
+    cfg = SMALL_MOE
+    banner(f"moe stage {cfg.name}")
+    M = cfg.num_microbatches
+    flat = synth.stage_params(cfg, 0)
+    Xs = [synth.activation(cfg, 0, mb, "x") for mb in range(M)]
+    dYs = [synth.activation(cfg, 0, mb, "dy") for mb in range(M)]
+    r = StageRunner(desc_of(cfg), flat, M)
+    r.alloc_microbatches(Xs, dYs)
+    routes = []
+    for mb in range(M):
+        r.forward(mb)
+        routes.append([r.moe_routing(mb, l) for l in range(cfg.n_layers)])
+    for mb in range(M):
+        r.backward(mb)
+    torch.cuda.synchronize()
+    layers = OS.layer_params(cfg, flat)
+    G = np.zeros(synth.param_count(cfg))
+    errs = {}
+    near_tie_mismatches = 0
+    for mb in range(M):
+        Y, caches = OS.stage_forward(cfg, layers, Xs[mb], route_overrides=routes[mb])
+        for l in range(cfg.n_layers):
+            pi = caches[l]["moe"]["pi"]
+            own = np.argsort(-pi, axis=1, kind="stable")[:, :2]
+            g = routes[mb][l]
+            diff = ~np.all(own == g, axis=1)
+            for t in np.nonzero(diff)[0]:
+                gap = np.max(np.abs(pi[t, g[t]] - pi[t, own[t]]))
+                assert gap < 1e-2, f"mb {mb} layer {l} token {t}: routing gap {gap}"
+            near_tie_mismatches += int(diff.sum())
+        dX, gmb = OS.stage_backward(cfg, layers, caches, dYs[mb])
+        G += gmb
+        errs[f"Y{mb}"] = rel_err(host(r.Y[mb]), Y)
+        errs[f"dX{mb}"] = rel_err(host(r.dX[mb]), dX)
+    got = host(r.grad)
+    for name, off, shape in synth.layout(cfg):
+        sz = int(np.prod(shape))
+        errs[name] = rel_err(got[off:off + sz], G[off:off + sz])
+    top = sorted(errs.items(), key=lambda kv: -kv[1])[:6]
+    print("worst tensors: " + ", ".join(f"{n}={e:.2e}" for n, e in top)
+          + f"; routing differs from the oracle's own at {near_tie_mismatches} near-ties",
+          flush=True)
+    assert max(errs.values()) <= 2e-2
+    r.close()

@@ -317,3 +317,38 @@ def test_moe_each_token_two_distinct_experts():
     srt = np.sort(pi, axis=1)
     assert np.all(pi[np.arange(50), sel[:, 0]] == srt[:, -1])
     assert np.all(pi[np.arange(50), sel[:, 1]] == srt[:, -2])
+
+
+@pytest.mark.parametrize("T,E", [(1, 2), (37, 4), (1500, 8), (300, 64)])
+def test_moe_dispatch_groups_by_expert_then_token(T, E):
+    """The grouping is fixed by two properties that determine it uniquely:
+    rows of one expert are contiguous and in expert order, and within an
+    expert the tokens increase. Checked directly on the definition's output
+    for random routings (two distinct experts per token)."""
+    rng = np.random.default_rng(T + E)
+    sel = np.stack([rng.choice(E, size=2, replace=False) for _ in range(T)])
+    off, perm, rowpos = O.moe_dispatch(sel, E)
+    assert off[0] == 0 and off[-1] == 2 * T and np.all(np.diff(off) >= 0)
+    assert np.array_equal(np.diff(off), np.bincount(sel.ravel(), minlength=E))
+    for e in range(E):
+        rows = perm[off[e]:off[e + 1]]
+        assert np.all(np.diff(rows) > 0)                     # tokens increase
+        assert np.all((sel[rows] == e).any(axis=1))          # each row really routes to e
+    assert np.array_equal(np.sort(perm), np.repeat(np.arange(T), 2))  # every token twice
+    for k in range(2):
+        assert np.array_equal(perm[rowpos[:, k]], np.arange(T))
+        rows_of_expert = np.searchsorted(off, rowpos[:, k], side="right") - 1
+        assert np.array_equal(rows_of_expert, sel[:, k])
+
+
+def test_moe_dispatch_matches_forward_row_order():
+    """moe_forward lists expert e's rows as np.nonzero(sel == e): the same
+    rows, in the same order, as the dispatch's group e."""
+    rng = np.random.default_rng(11)
+    T, E = 200, 8
+    sel = np.stack([rng.choice(E, size=2, replace=False) for _ in range(T)])
+    off, perm, rowpos = O.moe_dispatch(sel, E)
+    for e in range(E):
+        rows, slot = np.nonzero(sel == e)
+        assert np.array_equal(perm[off[e]:off[e + 1]], rows)
+        assert np.array_equal(rowpos[rows, slot], np.arange(off[e], off[e + 1]))

@@ -37,17 +37,65 @@ def log(*a):
 
 
 def stage_flops_per_mb(cfg) -> float:
+    """Algorithmic FLOP of Chunk F + Chunk B of one microbatch: projection
+    GEMMs 2MNK (a MoE layer's experts counted over the 2T routed rows, the
+    tiny router product excluded), causal attention S(S+1)/2 pairs per head
+    for each of QK^T and PV, backward = 2x forward."""
     T, d, f, H, hd, S, b = (cfg.tokens, cfg.d_model, cfg.d_ff, cfg.n_heads, cfg.head_dim,
                             cfg.seq_len, cfg.micro_batch)
-    gemm = 2.0 * T * d * (3 * d + d + 2 * f + f)
+    if cfg.moe:
+        ffn = 2.0 * (cfg.top_k * T) * d * (3 * cfg.d_ff_expert)
+    else:
+        ffn = 2.0 * T * d * (3 * f)
+    gemm = 2.0 * T * d * (3 * d + d) + ffn
     attn = 4.0 * (S * (S + 1) / 2) * hd * H * b
     return 3.0 * cfg.n_layers * (gemm + attn)
 
 
 def desc_of(cfg, lc):
     return lc.make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
-                        cfg.seq_len, cfg.micro_batch, cfg.bf16, rms_eps=cfg.rms_eps,
+                        cfg.seq_len, cfg.micro_batch, cfg.bf16, n_experts=cfg.n_experts,
+                        top_k=cfg.top_k, d_ff_expert=cfg.d_ff_expert, rms_eps=cfg.rms_eps,
                         rope_base=cfg.rope_base)
+
+
+def time_stage(torch, lc, cfg, stream, steps, warmup, tag):
+    """Time steps of (zero G, the Order, AdamW over the bucket) on `cfg`;
+    returns (ms per step, TFLOP/s, outputs finite)."""
+    from paper_2606_11169_amd.runner import random_stage
+    M = cfg.num_microbatches
+    order = lc.lc_order_1f1b(M, cfg.pp_size, cfg.pp_rank)
+    _, peak = lc.lc_order_validate(order, M, M)
+    log(f"[bench] {cfg.name}: {M} microbatches, 1F1B(P={cfg.pp_size}, s={cfg.pp_rank}), "
+        f"{peak} in flight")
+    r = random_stage(desc_of(cfg, lc), peak, seed=0, stream=stream)
+    r.alloc_random_microbatches(M, seed=1)
+    log(f"[bench] params {r.n_params}, workspace {r.ws_bytes / 2**30:.1f} GiB")
+
+    def step():
+        r.zero_grad()
+        r.run_order(order)
+        r.adam_step(cfg.lr, cfg.beta1, cfg.beta2, cfg.adam_eps, cfg.weight_decay)
+
+    for i in range(warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] {tag} warmup {i + 1}/{warmup} done")
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    tflops = stage_flops_per_mb(cfg) * M / (ms * 1e-3) / 1e12
+    finite = bool(torch.isfinite(r.Y[M - 1].float()).all().item())
+    r.close()
+    del r
+    torch.cuda.empty_cache()
+    return ms, tflops, finite
 
 
 def time_launches(torch, stream, fns, reps):
@@ -158,6 +206,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-adam-shard", action="store_true")
+    ap.add_argument("--no-moe", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -175,42 +224,22 @@ def main():
     cfg = synth.STAGE_7B
     M = cfg.num_microbatches
     stream = torch.cuda.current_stream()
-    order = lc.lc_order_1f1b(M, cfg.pp_size, cfg.pp_rank)
-    _, peak = lc.lc_order_validate(order, M, M)
-    log(f"[bench] {cfg.name}: {M} microbatches, 1F1B(P={cfg.pp_size}, s={cfg.pp_rank}), "
-        f"{peak} in flight")
-    r = random_stage(desc_of(cfg, lc), peak, seed=0, stream=stream)
-    r.alloc_random_microbatches(M, seed=1)
-    log(f"[bench] params {r.n_params}, workspace {r.ws_bytes / 2**30:.1f} GiB")
-
-    def step():
-        r.zero_grad()
-        r.run_order(order)
-        r.adam_step(cfg.lr, cfg.beta1, cfg.beta2, cfg.adam_eps, cfg.weight_decay)
-
-    for i in range(args.warmup):
-        step()
-        torch.cuda.synchronize()
-        log(f"[bench] warmup {i + 1}/{args.warmup} done")
-    torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for i in range(args.steps):
-        step()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms = t0.elapsed_time(t1) / args.steps
+    ms, tflops, finite = time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "7b")
     flops = stage_flops_per_mb(cfg) * M
-    tflops = flops / (ms * 1e-3) / 1e12
     log(f"[bench] {ms:.1f} ms/step, {tflops:.1f} TFLOP/s ({100 * tflops / BF16_PEAK_TFLOPS:.1f}% of bf16 peak)")
-    finite = bool(torch.isfinite(r.Y[M - 1].float()).all().item())
-    r.close()
-    del r
-    torch.cuda.empty_cache()
 
     roof = wgrad_roofline(torch, lc, cfg, stream)
     log(f"[bench] roofline {roof}")
+    moe = None
+    if not args.no_moe:
+        mcfg = synth.MOE_2K
+        mms, mtf, mfin = time_stage(torch, lc, mcfg, stream, args.steps, args.warmup, "moe")
+        moe = {"workload": mcfg.name, "value": round(mtf, 2), "unit": "TFLOP/s",
+               "ms_per_step": round(mms, 2), "frac": round(mtf / BF16_PEAK_TFLOPS, 4),
+               "algorithmic_tflop_per_step":
+                   round(stage_flops_per_mb(mcfg) * mcfg.num_microbatches / 1e12, 3),
+               "outputs_finite": mfin}
+        log(f"[bench] moe stage {moe}")
     adam = None if args.no_adam_shard else adam_shard(torch, lc, synth.ADAM_1P6B, stream)
     if adam:
         log(f"[bench] adam shard {adam}")
@@ -234,6 +263,7 @@ def main():
         "mfma_util": round(tflops / BF16_PEAK_TFLOPS, 4),
         "roofline": roof,
         "adam_shard": adam,
+        "moe_stage": moe,
         "cpu_baseline": cpu,
         "outputs_finite": finite,
     }

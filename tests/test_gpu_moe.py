@@ -269,3 +269,42 @@ def test_moe_stage_matches_oracle_with_gpu_routing():
           flush=True)
     assert max(errs.values()) <= 2e-2
     r.close()
+
+
+def test_full_size_moe_stage_on_a_prefix():
+    """The MoE workload at full size (4 layers, d 2048, 8 experts x 1408,
+    2 x 2048 tokens): outputs and gradients on a 128-token prefix of each
+    sequence against the oracle run on that prefix with the GPU's routing of
+    those tokens (routing is per token, and causality keeps the prefix
+    self-contained); dY is zero past the prefix, so the full-size backward
+    is checked too and dX past the prefix must be exactly 0."""
+    cfg = synth.MOE_2K
+    P, S = 128, cfg.seq_len
+    banner(f"full-size {cfg.name} prefix {P}")
+    flat = synth.stage_params(cfg, 0)
+    X = synth.activation(cfg, 0, 0, "x")
+    dY = synth.activation(cfg, 0, 0, "dy")
+    dY[:, P:] = 0.0
+    r = StageRunner(desc_of(cfg), flat, 1)
+    r.alloc_microbatches([X], [dY])
+    r.forward(0)
+    route = [r.moe_routing(0, l) for l in range(cfg.n_layers)]
+    r.backward(0)
+    torch.cuda.synchronize()
+    Yg, dXg, Gg = host(r.Y[0]), host(r.dX[0]), host(r.grad)
+    r.close()
+    del r
+    torch.cuda.empty_cache()
+    rows = np.concatenate([np.arange(b * S, b * S + P) for b in range(cfg.micro_batch)])
+    override = [rt[rows] for rt in route]
+    layers = OS.layer_params(cfg, flat)
+    Yp, caches = OS.stage_forward(cfg, layers, X[:, :P], route_overrides=override)
+    dXp, Gp = OS.stage_backward(cfg, layers, caches, dY[:, :P])
+    errs = {"Y": rel_err(Yg[:, :P], Yp), "dX": rel_err(dXg[:, :P], dXp)}
+    assert np.all(dXg[:, P:] == 0.0)
+    for name, off, shape in synth.layout(cfg):
+        sz = int(np.prod(shape))
+        errs[name] = rel_err(Gg[off:off + sz], Gp[off:off + sz])
+    top = sorted(errs.items(), key=lambda kv: -kv[1])[:8]
+    print("worst tensors: " + ", ".join(f"{n}={e:.2e}" for n, e in top), flush=True)
+    assert max(errs.values()) <= 2e-2

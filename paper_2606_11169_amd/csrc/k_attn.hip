@@ -2,28 +2,35 @@
 // q/k/v operands, fp32 softmax and accumulation), plus a plain fp32 path.
 //
 // Forward (written from the FlashAttention-2 algorithm of Dao, 2023): a
-// workgroup owns 128 queries of one (batch row, head); each of its 4 waves owns
-// 32 queries and walks the visible keys in blocks of 64 staged in LDS, keeping
-// a running row maximum and row sum (online softmax) and the output
-// accumulator in registers. The score block is computed transposed,
-// S^T = K Q^T, so each lane holds one query's scores: the row max and row
-// sum need only lane-local work plus one swap with the partner lane
-// (lane ^ 32) that holds the other half of the keys. The output is likewise
-// accumulated transposed, O^T += V^T P^T, so the per-query rescale factor is a
-// lane-local scalar, and the P^T accumulator registers are fed straight back
-// as the MFMA B operand: the keys a lane holds define the k-slots, and the
-// V^T fragment is read from LDS in the same key order. Products use the q/k/v
+// workgroup of 8 waves owns 256 queries of one (batch row, head); each wave
+// owns 32 queries and walks the visible keys in blocks of 64, keeping a
+// running row maximum and row sum (online softmax) and the output in
+// registers. K and V blocks stream from HBM straight into a two-stage LDS ring
+// (buffer_load_dwordx4 ... lds, one 1 KiB run of 4 rows per wave
+// instruction). The score block is computed transposed, S^T = K Q^T, so each
+// lane holds one query's scores: the row max and row sum need lane-local work
+// plus one swap with the partner lane (lane ^ 32). The output is accumulated
+// transposed, O^T += V^T P^T, so the rescale is a lane-local scalar (skipped
+// when no query's maximum moved), and the P^T accumulator registers feed the
+// MFMA directly: the keys a lane holds define the k slots, and the V^T
+// fragment is read in that key order with the transposing LDS load
+// ds_read_b64_tr_b16 from V's key-major rows. Forward products use the q/k/v
 // element type (P is rounded to it too).
 //
-// Backward (deterministic, no atomics): D = rowsum(dO * O) first; then one
-// kernel per query block recomputes P^T from the saved log-sum-exp (with the
-// forward's q/k type, so P matches the forward) and accumulates
-// dQ^T = K^T dS^T over keys, and one kernel per key block accumulates
-// dV^T = dO^T P and dK^T = Q^T dS over queries (S computed untransposed there
-// so the key is the lane index). Every gradient product is bf16 x bf16 (q, k,
-// v are converted while they are staged). RoPE's inverse rotation of dq/dk is
-// applied in the epilogue. LDS tiles are filled from 8 x 8 blocks read once
-// from HBM and written both row-major and transposed.
+// Backward (deterministic, no atomics): a prep pass computes D = rowsum(dO*O)
+// and bf16 copies of q, k, v; then one kernel per 256 keys accumulates
+// dV^T = dO^T P and dK^T = Q^T dS over the query blocks at or after the
+// diagonal, and one kernel per 256 queries accumulates dQ^T = K^T dS^T over
+// the visible key blocks. Both recompute P from the forward's log-sum-exp with
+// the forward's q/k element type (so P matches the forward) and take every
+// gradient product in bf16. RoPE's inverse rotation of dq/dk is applied in
+// the epilogues.
+//
+// Every LDS tile is [64 rows][128 columns] of 2-byte elements (256-byte rows
+// of 16 chunks); chunk c of row r sits at chunk c ^ f(r) with
+// f(r) = ((r & 3) << 2) | ((r >> 2) & 3). A 128-bit fragment read (16
+// consecutive rows, one chunk) and a transposing read (4 consecutive rows,
+// four chunks) both touch every bank once per phase.
 #include "common.hpp"
 
 #include <math.h>
@@ -34,13 +41,18 @@ namespace lc {
 namespace {
 
 constexpr int HD = 128;
-constexpr int QB = 128;  // queries (or keys) per workgroup
-constexpr int KB = 64;   // keys (or queries) per inner step
+constexpr int QB = 128;    // granularity of seq_len accepted by the matrix-core path
+constexpr int ROWS = 256;  // queries (or keys) per workgroup: 8 waves x 32
+constexpr int KB = 64;     // keys (or queries) per inner block
+constexpr int NT = 512;
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 constexpr int TILE = KB * HD * 2;  // 16 KiB: one [64][128] tile of 2-byte elements
 
-typedef __attribute__((ext_vector_type(4))) unsigned u32x4_v;
+typedef __attribute__((ext_vector_type(4))) int i32x4_v;
+typedef __attribute__((ext_vector_type(4))) short s16x4_v;
+typedef __attribute__((address_space(3))) char lds_t;
+#define LDS_AS(T, ptr) ((__attribute__((address_space(3))) T *)(ptr))
 
 template <typename E> struct V8;
 template <> struct V8<__bf16> { typedef bf16x8_v type; };
@@ -53,81 +65,76 @@ __device__ __forceinline__ f32x16_v mfma(f16x8_v a, f16x8_v b, f32x16_v c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
-// 8 elements of type E (16 bytes) -> 8 bf16
-template <typename E>
-__device__ __forceinline__ uint4 to_bf16(uint4 v) {
-  if constexpr (std::is_same<E, __bf16>::value) {
-    return v;
-  } else {
-    const f16x8_v h = __builtin_bit_cast(f16x8_v, v);
-    bf16x8_v b;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) b[e] = (__bf16)(float)h[e];
-    return __builtin_bit_cast(uint4, b);
-  }
+// ---------------------------------------------------------------- tiles
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int tile_off(int r, int c) { return r * 256 + ((c ^ swz(r)) << 4); }
+
+__device__ __forceinline__ i32x4_v make_rsrc(const void *base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4_v r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
 }
 
-// [64 rows][128 cols] tile: 256-byte rows of 16 chunks, chunk XOR (row & 7)
-__device__ __forceinline__ int rowt(int row, int c) { return row * 256 + ((c ^ (row & 7)) << 4); }
-// [128 rows][64 cols] tile: 128-byte rows of 8 chunks, chunk XOR (row & 7)
-__device__ __forceinline__ int colt(int row, int c) { return row * 128 + ((c ^ (row & 7)) << 4); }
-
-__device__ __forceinline__ void transpose8x8(const uint4 (&r)[8], uint4 (&t)[8]) {
-  const uint32_t *rw = reinterpret_cast<const uint32_t *>(r);
-  uint32_t *tw = reinterpret_cast<uint32_t *>(t);
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t lo = rw[(2 * q) * 4 + p];
-      const uint32_t hi = rw[(2 * q + 1) * 4 + p];
-      tw[(2 * p) * 4 + q] = (lo & 0xFFFFu) | (hi << 16);
-      tw[(2 * p + 1) * 4 + q] = (lo >> 16) | (hi & 0xFFFF0000u);
-    }
-  }
+// 16 bytes per lane from byte offset `off` of the buffer into LDS at
+// lds + 16 * lane (inline assembly: the compiler does not track it; the
+// block loop's explicit wait before its barrier orders it)
+__device__ __forceinline__ void dma16(i32x4_v rs, lds_t *lds, uint32_t off) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t) reinterpret_cast<uintptr_t>(lds));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(off), "s"(rs), "s"(m0)
+               : "memory", "m0");
+}
+// 4 bytes per lane into lds + 4 * lane
+__device__ __forceinline__ void dma4(i32x4_v rs, lds_t *lds, uint32_t off) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t) reinterpret_cast<uintptr_t>(lds));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dword %0, %1, 0 offen lds"
+               :
+               : "v"(off), "s"(rs), "s"(m0)
+               : "memory", "m0");
 }
 
-// One 8 x 8 block of a [64][128] tile of 2-byte elements: rows rb*8 .. +7,
-// columns eb*8 .. +7; stored row-major or transposed, optionally converted
-// from element type E to bf16 on the way.
-struct Blk {
-  uint4 v[8];
-  __device__ __forceinline__ void load(const void *base, int64_t ld, int64_t row0, int rb,
-                                       int eb) {
-    const uint16_t *b = static_cast<const uint16_t *>(base);
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk)
-      v[kk] = *reinterpret_cast<const uint4 *>(b + (row0 + rb * 8 + kk) * ld + eb * 8);
-  }
-  template <typename E>
-  __device__ __forceinline__ void store_rows(char *t, int rb, int eb, bool to_bf) const {
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk)
-      *reinterpret_cast<uint4 *>(t + rowt(rb * 8 + kk, eb)) = to_bf ? to_bf16<E>(v[kk]) : v[kk];
-  }
-  template <typename E>
-  __device__ __forceinline__ void store_cols(char *t, int rb, int eb, bool to_bf) const {
-    uint4 tr[8];
-    transpose8x8(v, tr);
-#pragma unroll
-    for (int ee = 0; ee < 8; ++ee)
-      *reinterpret_cast<uint4 *>(t + colt(eb * 8 + ee, rb)) = to_bf ? to_bf16<E>(tr[ee]) : tr[ee];
-  }
-};
+// Run `run` (0..15) of a [64][128] tile: rows 4 run .. 4 run + 3 of the block
+// whose row 0 is global row `grow0` of a matrix with `ld` elements per row,
+// columns col0 .. col0 + 127.
+__device__ __forceinline__ void tile_run(i32x4_v rs, lds_t *tile, int run, int64_t grow0,
+                                         int64_t ld, int col0, int lane) {
+  const int r = 4 * run + (lane >> 4);
+  const int c = (lane & 15) ^ swz(r);
+  const uint32_t off = (uint32_t)(((grow0 + r) * ld + col0 + 8 * c) * 2);
+  dma16(rs, tile + run * 1024, off);
+}
 
-// fragment of 8 elements from a [128][64] transposed tile: columns c..c+3 and
-// c+8..c+11 of row `row` (c = 16*step + 4*half, so both runs sit in adjacent chunks)
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// MFMA operand of 32 tile rows row0 .. row0+31 at columns 16 s + 8 (lane / 32) + [0, 8)
 template <typename VT>
-__device__ __forceinline__ VT frag_cols(const char *t, int row, int c) {
-  const uint2 lo = *reinterpret_cast<const uint2 *>(t + colt(row, c >> 3) + (c & 7) * 2);
-  const uint2 hi = *reinterpret_cast<const uint2 *>(t + colt(row, (c >> 3) + 1) + (c & 7) * 2);
-  const u32x4_v w = {lo.x, lo.y, hi.x, hi.y};
-  return __builtin_bit_cast(VT, w);
+__device__ __forceinline__ VT frag_rows(const lds_t *t, int row0, int s, int lane) {
+  const int r = row0 + (lane & 31);
+  return *reinterpret_cast<const __attribute__((address_space(3))) VT *>(
+      t + tile_off(r, 2 * s + (lane >> 5)));
 }
 
+// MFMA operand of 32 tile columns col0 .. col0+31 (lane l: column col0 + l % 32)
+// whose 8 k values are tile rows c .. c+3 and c+8 .. c+11, c = kbase + 4 (lane / 32):
+// the key (or query) order of a 32 x 32 accumulator's registers 8t .. 8t+7
+// (rows 16t + 4 hf + [0, 4) and 16t + 8 + 4 hf + [0, 4)), kbase = 32 j + 16 t.
 template <typename VT>
-__device__ __forceinline__ VT frag_rows(const char *t, int row, int chunk) {
-  return *reinterpret_cast<const VT *>(t + rowt(row, chunk));
+__device__ __forceinline__ VT frag_cols(const lds_t *t, int col0, int kbase, int lane) {
+  const int i16 = lane & 15;
+  const int r = kbase + 4 * (lane >> 5) + (i16 >> 2);
+  const int col = col0 + 16 * ((lane >> 4) & 1) + 4 * (i16 & 3);
+  const lds_t *p0 = t + tile_off(r, col >> 3) + (col & 7) * 2;
+  const lds_t *p1 = t + tile_off(r + 8, col >> 3) + (col & 7) * 2;
+  typedef __attribute__((address_space(3))) s16x4_v lds_v4;
+  const s16x4_v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)p0);
+  const s16x4_v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)p1);
+  const s16x4_v v[2] = {lo, hi};
+  return __builtin_bit_cast(VT, v);
 }
 
 template <typename E>
@@ -141,6 +148,27 @@ __device__ __forceinline__ typename V8<E>::type pack8(const f32x16_v &a, int bas
 // row index inside a 32-row MFMA output block held by register r of a lane in half hf
 __device__ __forceinline__ int out_row(int r, int hf) { return (r & 3) + 8 * (r >> 2) + 4 * hf; }
 
+__device__ __forceinline__ f32x16_v zero16() {
+  f32x16_v z;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) z[r] = 0.0f;
+  return z;
+}
+
+// 8 elements of type E (16 bytes) as 8 bf16
+template <typename E>
+__device__ __forceinline__ bf16x8_v to_bf16x8(uint4 v) {
+  if constexpr (std::is_same<E, __bf16>::value) {
+    return __builtin_bit_cast(bf16x8_v, v);
+  } else {
+    const f16x8_v h = __builtin_bit_cast(f16x8_v, v);
+    bf16x8_v b;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b[e] = (__bf16)(float)h[e];
+    return b;
+  }
+}
+
 struct AttnP {
   const void *q, *k, *v;   // q/k/v element type (template)
   __bf16 *o;
@@ -148,114 +176,111 @@ struct AttnP {
   const __bf16 *dout;
   __bf16 *dq, *dk, *dv;
   float *D;
+  __bf16 *qkvb;            // bf16 copies of q, k, v (backward): [B*S, 3*H*hd]
   const float *rcos, *rsin;
-  int64_t ld_qkv, ld_o, ld_d;
-  int S, H;
+  int64_t ld_qkv, ld_o, ld_d, ld_b;
+  uint32_t qkv_bytes, o_bytes, b_bytes, lse_bytes;  // buffer extents (q/k/v from p.q)
+  int S, H, B;
   float scale;  // 1/sqrt(hd)
 };
 
 // ---------------------------------------------------------------- forward
 template <typename QE>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(AttnP p) {
+__global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
-  extern __shared__ __align__(16) char smem[];  // 2 stages x (K rows | V^T)
-  const int nqb = p.S / QB;
+  __shared__ __align__(16) char smem[2 * 2 * TILE];  // stage s: K tile | V tile
+  lds_t *const L = LDS_AS(char, smem);
+  const int nqb = (p.S + ROWS - 1) / ROWS;
   const int qb = nqb - 1 - (int)blockIdx.x;  // heaviest blocks first
   const int h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hf = lane >> 5;
   const int64_t row0 = (int64_t)b * p.S;
-  const QE *Q = static_cast<const QE *>(p.q) + h * HD;
-  const QE *K = static_cast<const QE *>(p.k) + h * HD;
-  const QE *V = static_cast<const QE *>(p.v) + h * HD;
-  const int q0 = qb * QB + w * 32;
+  const int q0 = qb * ROWS + w * 32;
+  const bool active = q0 < p.S;
   const int myq = q0 + l32;
   const float sc = p.scale * LOG2E;
+  const QE *Q = static_cast<const QE *>(p.q) + h * HD;
 
   QV qf[8];
 #pragma unroll
-  for (int es = 0; es < 8; ++es)
-    qf[es] = *reinterpret_cast<const QV *>(Q + (row0 + myq) * p.ld_qkv + es * 16 + hf * 8);
-
+  for (int es = 0; es < 8; ++es) {
+    if (active) qf[es] = *reinterpret_cast<const QV *>(Q + (row0 + myq) * p.ld_qkv + es * 16 + hf * 8);
+    else qf[es] = QV{};
+  }
   f32x16_v o[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[i][r] = 0.0f;
-  float m = -1e30f, l = 0.0f;
+  for (int i = 0; i < 4; ++i) o[i] = zero16();
+  float m = -INFINITY, l = 0.0f;
 
-  const bool isK = tid < 128;
-  const int bt = tid & 127, rb = bt >> 4, eb = bt & 15;
-  Blk blk;
-  const int nkb = (qb + 1) * QB / KB;
-  blk.load(isK ? (const void *)K : (const void *)V, p.ld_qkv, row0, rb, eb);
-  if (isK) blk.store_rows<QE>(smem, rb, eb, false); else blk.store_cols<QE>(smem + TILE, rb, eb, false);
+  // waves 0-3 stream K (runs 4 (w & 3) .. + 3), waves 4-7 stream V
+  const bool isK = w < 4;
+  const i32x4_v rs = make_rsrc(isK ? p.k : p.v, p.qkv_bytes);
+  auto load = [&](int kb, lds_t *st) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      tile_run(rs, st + (isK ? 0 : TILE), 4 * (w & 3) + t, row0 + (int64_t)kb * KB, p.ld_qkv,
+               h * HD, lane);
+  };
+  const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
+  load(0, L);
+  wait_vm0();
   __syncthreads();
-
   for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
-    const bool more = kb + 1 < nkb;
-    if (more) blk.load(isK ? (const void *)K : (const void *)V, p.ld_qkv, row0 + (kb + 1) * KB, rb, eb);
-    const char *sK = smem + cur * 2 * TILE;
-    const char *sVt = sK + TILE;
+    const lds_t *cur = L + (kb & 1) * 2 * TILE;
+    if (kb + 1 < nkb) load(kb + 1, L + ((kb + 1) & 1) * 2 * TILE);
     const int k0 = kb * KB;
-    if (k0 <= q0 + 31) {
-      f32x16_v s[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[j][r] = 0.0f;
+    if (active && k0 <= q0 + 31) {
+      f32x16_v s[2] = {zero16(), zero16()};
 #pragma unroll
       for (int es = 0; es < 8; ++es)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          s[j] = mfma(frag_rows<QV>(sK, j * 32 + l32, es * 2 + hf), qf[es], s[j]);
+        for (int j = 0; j < 2; ++j) s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), qf[es], s[j]);
       const bool diag = k0 + KB - 1 > q0;
       float mx = -INFINITY;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float v = s[j][r] * sc;
-          if (diag && k0 + j * 32 + out_row(r, hf) > myq) v = -INFINITY;
-          s[j][r] = v;
-          mx = fmaxf(mx, v);
+          if (diag && k0 + j * 32 + out_row(r, hf) > myq) s[j][r] = -INFINITY;
+          mx = fmaxf(mx, s[j][r]);
         }
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m, mx);
-      const float alpha = exp2f(m - mn);
-      m = mn;
+      const float mn = fmaxf(m, mx * sc);
+      if (__any(mn > m)) {  // rescale only when some query's maximum moved
+        const float alpha = mn > m ? exp2f(m - mn) : 1.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+        l *= alpha;
+        m = mn;
+      }
       float ls = 0.0f;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float pv = exp2f(s[j][r] - mn);
+          const float pv = exp2f(__builtin_fmaf(s[j][r], sc, -m));
           s[j][r] = pv;
           ls += pv;
         }
-      l = l * alpha + ls;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+      l += ls;
+      const lds_t *vt = cur + TILE;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const QV pf = pack8<QE>(s[j], 8 * t);
-          const int kc = j * 32 + 16 * t + 4 * hf;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o[i] = mfma(frag_cols<QV>(sVt, i * 32 + l32, kc), pf, o[i]);
+          for (int i = 0; i < 4; ++i) o[i] = mfma(frag_cols<QV>(vt, i * 32, j * 32 + 16 * t, lane), pf, o[i]);
         }
     }
-    if (more) {
-      char *nb = smem + (cur ^ 1) * 2 * TILE;
-      if (isK) blk.store_rows<QE>(nb, rb, eb, false); else blk.store_cols<QE>(nb + TILE, rb, eb, false);
-    }
+    wait_vm0();
     __syncthreads();
   }
-
+  if (!active) return;
   const float lt = l + __shfl_xor(l, 32, 64);
   const float inv = 1.0f / lt;
   __bf16 *orow = p.o + (row0 + myq) * p.ld_o + h * HD;
@@ -271,7 +296,9 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnP p) {
 }
 
 // ---------------------------------------------------------------- backward
-// D[b,h,i] = sum_e dO[i,e] O[i,e]; one workgroup per token row, 16 lanes per head
+// D[b,h,i] = sum_e dO[i,e] O[i,e] (16 lanes per head), and, for fp16 q/k/v,
+// bf16 copies of the token row's q, k, v. One workgroup per token row.
+template <typename QE>
 __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p, int d) {
   const int64_t row = blockIdx.x;  // b*S + s
   const int b = (int)(row / p.S), s = (int)(row % p.S);
@@ -284,6 +311,16 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p, int d) {
 #pragma unroll
     for (int o2 = 8; o2 > 0; o2 >>= 1) acc += __shfl_xor(acc, o2, 64);
     if ((threadIdx.x & 15) == 0) p.D[((int64_t)b * p.H + c / HD) * p.S + s] = acc;
+  }
+  if constexpr (!std::is_same<QE, __bf16>::value) {
+    const void *src[3] = {p.q, p.k, p.v};
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(static_cast<const QE *>(src[t]) +
+                                                         row * p.ld_qkv + c);
+        *reinterpret_cast<bf16x8_v *>(p.qkvb + row * p.ld_b + t * d + c) = to_bf16x8<QE>(v);
+      }
   }
 }
 
@@ -313,100 +350,110 @@ __device__ __forceinline__ void store_row_t(__bf16 *row, const f32x16_v (&acc)[4
     }
 }
 
-// dQ: one workgroup per 128 queries; LDS stage = K rows (QE) | K^T (bf16) | V rows (bf16)
+// the bf16 versions of q, k, v read by the gradient products
 template <typename QE>
-__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnP p) {
+__device__ __forceinline__ const __bf16 *bf_qkv(const AttnP &p, int t) {
+  if constexpr (std::is_same<QE, __bf16>::value)
+    return static_cast<const __bf16 *>(t == 0 ? p.q : t == 1 ? p.k : p.v);
+  else
+    return p.qkvb + t * (int64_t)p.H * HD;
+}
+
+// dQ: one workgroup per 256 queries; LDS stage = K (QE) | K (bf16) | V (bf16)
+template <typename QE>
+__global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
-  extern __shared__ __align__(16) char smem[];
-  const int nqb = p.S / QB;
+  __shared__ __align__(16) char smem[2 * 3 * TILE];
+  lds_t *const L = LDS_AS(char, smem);
+  const int nqb = (p.S + ROWS - 1) / ROWS;
   const int qb = nqb - 1 - (int)blockIdx.x;
   const int h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hf = lane >> 5;
   const int64_t row0 = (int64_t)b * p.S;
-  const QE *K = static_cast<const QE *>(p.k) + h * HD;
-  const QE *V = static_cast<const QE *>(p.v) + h * HD;
-  const int q0 = qb * QB + w * 32;
+  const int q0 = qb * ROWS + w * 32;
+  const bool active = q0 < p.S;
   const int myq = q0 + l32;
   const float sc = p.scale * LOG2E;
+  const int64_t ldb = std::is_same<QE, __bf16>::value ? p.ld_qkv : p.ld_b;
 
   QV qf[8];
   bf16x8_v df[8];
 #pragma unroll
   for (int es = 0; es < 8; ++es) {
-    qf[es] = *reinterpret_cast<const QV *>(static_cast<const QE *>(p.q) + h * HD +
-                                           (row0 + myq) * p.ld_qkv + es * 16 + hf * 8);
-    df[es] = *reinterpret_cast<const bf16x8_v *>(p.dout + h * HD + (row0 + myq) * p.ld_o +
-                                                 es * 16 + hf * 8);
+    if (active) {
+      qf[es] = *reinterpret_cast<const QV *>(static_cast<const QE *>(p.q) + h * HD +
+                                             (row0 + myq) * p.ld_qkv + es * 16 + hf * 8);
+      df[es] = *reinterpret_cast<const bf16x8_v *>(p.dout + h * HD + (row0 + myq) * p.ld_o +
+                                                   es * 16 + hf * 8);
+    } else {
+      qf[es] = QV{};
+      df[es] = bf16x8_v{};
+    }
   }
-  const int64_t si = ((int64_t)b * p.H + h) * p.S + myq;
+  const int64_t si = ((int64_t)b * p.H + h) * p.S + (active ? myq : 0);
   const float lse2 = p.lse[si] * LOG2E;
   const float Dq = p.D[si];
-
   f32x16_v acc[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[i][r] = 0.0f;
+  for (int i = 0; i < 4; ++i) acc[i] = zero16();
 
-  const bool isK = tid < 128;
-  const int bt = tid & 127, rb = bt >> 4, eb = bt & 15;
-  constexpr int STAGE = 3 * TILE;
-  Blk blk;
-  const int nkb = (qb + 1) * QB / KB;
-  auto put = [&](char *st) {
-    if (isK) {
-      blk.store_rows<QE>(st, rb, eb, false);
-      blk.store_cols<QE>(st + TILE, rb, eb, true);
-    } else {
-      blk.store_rows<QE>(st + 2 * TILE, rb, eb, true);
+  // 48 runs per block: K (QE) runs 0-15, K (bf16) 16-31, V (bf16) 32-47; 6 per wave
+  const i32x4_v rk = make_rsrc(p.k, p.qkv_bytes);
+  const i32x4_v rkb = make_rsrc(bf_qkv<QE>(p, 1), std::is_same<QE, __bf16>::value ? p.qkv_bytes : p.b_bytes);
+  const i32x4_v rvb = make_rsrc(bf_qkv<QE>(p, 2), std::is_same<QE, __bf16>::value ? p.qkv_bytes : p.b_bytes);
+  auto load = [&](int kb, lds_t *st) {
+    const int64_t g0 = row0 + (int64_t)kb * KB;
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+      const int run = 6 * w + t, which = run >> 4;
+      if (which == 0) tile_run(rk, st, run & 15, g0, p.ld_qkv, h * HD, lane);
+      else if (which == 1) tile_run(rkb, st + TILE, run & 15, g0, ldb, h * HD, lane);
+      else tile_run(rvb, st + 2 * TILE, run & 15, g0, ldb, h * HD, lane);
     }
   };
-  blk.load(isK ? (const void *)K : (const void *)V, p.ld_qkv, row0, rb, eb);
-  put(smem);
+  const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
+  load(0, L);
+  wait_vm0();
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
-    const bool more = kb + 1 < nkb;
-    if (more) blk.load(isK ? (const void *)K : (const void *)V, p.ld_qkv, row0 + (kb + 1) * KB, rb, eb);
-    const char *sK = smem + cur * STAGE, *sKt = sK + TILE, *sV = sK + 2 * TILE;
+    const lds_t *cur = L + (kb & 1) * 3 * TILE;
+    if (kb + 1 < nkb) load(kb + 1, L + ((kb + 1) & 1) * 3 * TILE);
     const int k0 = kb * KB;
-    if (k0 <= q0 + 31) {
-      f32x16_v s[2], dp[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[j][r] = dp[j][r] = 0.0f;
+    if (active && k0 <= q0 + 31) {
+      f32x16_v s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
 #pragma unroll
       for (int es = 0; es < 8; ++es)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          s[j] = mfma(frag_rows<QV>(sK, j * 32 + l32, es * 2 + hf), qf[es], s[j]);
-          dp[j] = mfma(frag_rows<bf16x8_v>(sV, j * 32 + l32, es * 2 + hf), df[es], dp[j]);
+          s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), qf[es], s[j]);
+          dp[j] = mfma(frag_rows<bf16x8_v>(cur + 2 * TILE, j * 32, es, lane), df[es], dp[j]);
         }
       const bool diag = k0 + KB - 1 > q0;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float pv = exp2f(s[j][r] * sc - lse2);
+          float pv = exp2f(__builtin_fmaf(s[j][r], sc, -lse2));
           if (diag && k0 + j * 32 + out_row(r, hf) > myq) pv = 0.0f;
           dp[j][r] = pv * (dp[j][r] - Dq);
         }
+      const lds_t *kt = cur + TILE;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          const bf16x8_v pf = pack8<__bf16>(dp[j], 8 * t);
-          const int kc = j * 32 + 16 * t + 4 * hf;
+          const bf16x8_v sf = pack8<__bf16>(dp[j], 8 * t);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            acc[i] = mfma(frag_cols<bf16x8_v>(sKt, i * 32 + l32, kc), pf, acc[i]);
+            acc[i] = mfma(frag_cols<bf16x8_v>(kt, i * 32, j * 32 + 16 * t, lane), sf, acc[i]);
         }
     }
-    if (more) put(smem + (cur ^ 1) * STAGE);
+    wait_vm0();
     __syncthreads();
   }
+  if (!active) return;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -415,82 +462,86 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnP p) {
   store_row_t(p.dq + h * HD + (row0 + myq) * p.ld_d, acc, 1.0f, hf);
 }
 
-// dK, dV: one workgroup per 128 keys; LDS stage = Q rows (QE) | Q^T (bf16) |
-// dO rows | dO^T | lse | D
+// dK, dV: one workgroup of 4 waves per 128 keys (each wave keeps its keys' K
+// and V operands and both accumulators, 256+ registers, so one wave per
+// SIMD); LDS stage = Q (QE) | Q (bf16) | dO | lse | D
+constexpr int KV_WAVES = 4, KV_ROWS = KV_WAVES * 32;
 template <typename QE>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(AttnP p) {
+__global__ __launch_bounds__(KV_WAVES * 64) void attn_bwd_dkdv_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
-  extern __shared__ __align__(16) char smem[];
-  const int kblk = blockIdx.x;
+  constexpr int STAGE = 3 * TILE + 512;
+  __shared__ __align__(16) char smem[2 * STAGE];
+  lds_t *const L = LDS_AS(char, smem);
+  const int kblk = blockIdx.x;  // heaviest (earliest keys) first
   const int h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hf = lane >> 5;
   const int64_t row0 = (int64_t)b * p.S;
-  const QE *Q = static_cast<const QE *>(p.q) + h * HD;
-  const __bf16 *dO = p.dout + h * HD;
-  const int k0w = kblk * QB + w * 32;
+  const int k0w = kblk * KV_ROWS + w * 32;
+  const bool active = k0w < p.S;
   const int myk = k0w + l32;
   const float sc = p.scale * LOG2E;
+  const int64_t ldb = std::is_same<QE, __bf16>::value ? p.ld_qkv : p.ld_b;
 
   QV kf[8];
   bf16x8_v vf[8];
 #pragma unroll
   for (int es = 0; es < 8; ++es) {
-    const int64_t off = h * HD + (row0 + myk) * p.ld_qkv + es * 16 + hf * 8;
-    kf[es] = *reinterpret_cast<const QV *>(static_cast<const QE *>(p.k) + off);
-    const uint4 raw = *reinterpret_cast<const uint4 *>(static_cast<const QE *>(p.v) + off);
-    vf[es] = __builtin_bit_cast(bf16x8_v, to_bf16<QE>(raw));
+    if (active) {
+      const int64_t off = h * HD + (row0 + myk) * p.ld_qkv + es * 16 + hf * 8;
+      kf[es] = *reinterpret_cast<const QV *>(static_cast<const QE *>(p.k) + off);
+      vf[es] = to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(static_cast<const QE *>(p.v) + off));
+    } else {
+      kf[es] = QV{};
+      vf[es] = bf16x8_v{};
+    }
   }
   f32x16_v dk[4], dv[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dk[i][r] = dv[i][r] = 0.0f;
+  for (int i = 0; i < 4; ++i) dk[i] = dv[i] = zero16();
 
-  const bool isQ = tid < 128;
-  const int bt = tid & 127, rb = bt >> 4, eb = bt & 15;
-  constexpr int STAGE = 4 * TILE + 512;
+  // 48 runs per block: Q (QE) 0-15, Q (bf16) 16-31, dO 32-47 (12 per wave);
+  // the last wave also brings the block's lse and D (64 floats each)
+  const i32x4_v rq = make_rsrc(p.q, p.qkv_bytes);
+  const i32x4_v rqb = make_rsrc(bf_qkv<QE>(p, 0), std::is_same<QE, __bf16>::value ? p.qkv_bytes : p.b_bytes);
+  const i32x4_v rdo = make_rsrc(p.dout, p.o_bytes);
+  const i32x4_v rl = make_rsrc(p.lse, p.lse_bytes);
+  const i32x4_v rd = make_rsrc(p.D, p.lse_bytes);
   const int64_t sbase = ((int64_t)b * p.H + h) * p.S;
-  Blk blk;
-  float sv = 0.0f;  // lse (threads 0..63) or D (threads 64..127) of the staged block
-  auto fetch = [&](int qbi) {
-    blk.load(isQ ? (const void *)Q : (const void *)dO, isQ ? p.ld_qkv : p.ld_o, row0 + qbi * KB, rb, eb);
-    if (tid < 64) sv = p.lse[sbase + qbi * KB + tid] * LOG2E;
-    else if (tid < 128) sv = p.D[sbase + qbi * KB + tid - 64];
-  };
-  auto put = [&](char *st) {
-    if (isQ) {
-      blk.store_rows<QE>(st, rb, eb, false);
-      blk.store_cols<QE>(st + TILE, rb, eb, true);
-    } else {
-      blk.store_rows<__bf16>(st + 2 * TILE, rb, eb, false);
-      blk.store_cols<__bf16>(st + 3 * TILE, rb, eb, false);
+  auto load = [&](int qbi, lds_t *st) {
+    const int64_t g0 = row0 + (int64_t)qbi * KB;
+#pragma unroll
+    for (int t = 0; t < 12; ++t) {
+      const int run = 12 * w + t, which = run >> 4;
+      if (which == 0) tile_run(rq, st, run & 15, g0, p.ld_qkv, h * HD, lane);
+      else if (which == 1) tile_run(rqb, st + TILE, run & 15, g0, ldb, h * HD, lane);
+      else tile_run(rdo, st + 2 * TILE, run & 15, g0, p.ld_o, h * HD, lane);
     }
-    if (tid < 128) reinterpret_cast<float *>(st + 4 * TILE)[tid] = sv;
+    if (w == KV_WAVES - 1) {
+      const uint32_t off = (uint32_t)((sbase + (int64_t)qbi * KB + lane) * 4);
+      dma4(rl, st + 3 * TILE, off);
+      dma4(rd, st + 3 * TILE + 256, off);
+    }
   };
-  const int qfirst = kblk * QB / KB, nqblk = p.S / KB;
-  fetch(qfirst);
-  put(smem);
+  const int qfirst = kblk * KV_ROWS / KB, nqblk = p.S / KB;
+  load(qfirst, L);
+  wait_vm0();
   __syncthreads();
   for (int qbi = qfirst; qbi < nqblk; ++qbi) {
-    const int cur = (qbi - qfirst) & 1;
-    const bool more = qbi + 1 < nqblk;
-    if (more) fetch(qbi + 1);
-    const char *sQ = smem + cur * STAGE, *sQt = sQ + TILE, *sD = sQ + 2 * TILE, *sDt = sQ + 3 * TILE;
-    const float *sL = reinterpret_cast<const float *>(sQ + 4 * TILE);
+    const int cur_i = (qbi - qfirst) & 1;
+    const lds_t *cur = L + cur_i * STAGE;
+    if (qbi + 1 < nqblk) load(qbi + 1, L + (cur_i ^ 1) * STAGE);
+    const float *sL = reinterpret_cast<const float *>(smem + cur_i * STAGE + 3 * TILE);
     const int q0 = qbi * KB;
-    if (q0 + KB - 1 >= k0w) {
-      f32x16_v s[2], dp[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[j][r] = dp[j][r] = 0.0f;
+    if (active && q0 + KB - 1 >= k0w) {
+      f32x16_v s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
 #pragma unroll
       for (int es = 0; es < 8; ++es)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          s[j] = mfma(frag_rows<QV>(sQ, j * 32 + l32, es * 2 + hf), kf[es], s[j]);
-          dp[j] = mfma(frag_rows<bf16x8_v>(sD, j * 32 + l32, es * 2 + hf), vf[es], dp[j]);
+          s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), kf[es], s[j]);
+          dp[j] = mfma(frag_rows<bf16x8_v>(cur + 2 * TILE, j * 32, es, lane), vf[es], dp[j]);
         }
       const bool diag = q0 < k0w + 31;
 #pragma unroll
@@ -498,28 +549,29 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(AttnP p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int qi = j * 32 + out_row(r, hf);
-          float pv = exp2f(s[j][r] * sc - sL[qi]);
+          float pv = exp2f(__builtin_fmaf(s[j][r], sc, -sL[qi] * LOG2E));
           if (diag && q0 + qi < myk) pv = 0.0f;
           s[j][r] = pv;
           dp[j][r] = pv * (dp[j][r] - sL[64 + qi]);
         }
+      const lds_t *qt = cur + TILE, *dot = cur + 2 * TILE;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const bf16x8_v pf = pack8<__bf16>(s[j], 8 * t);
           const bf16x8_v sf = pack8<__bf16>(dp[j], 8 * t);
-          const int qc = j * 32 + 16 * t + 4 * hf;
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            dv[i] = mfma(frag_cols<bf16x8_v>(sDt, i * 32 + l32, qc), pf, dv[i]);
-            dk[i] = mfma(frag_cols<bf16x8_v>(sQt, i * 32 + l32, qc), sf, dk[i]);
+            dv[i] = mfma(frag_cols<bf16x8_v>(dot, i * 32, j * 32 + 16 * t, lane), pf, dv[i]);
+            dk[i] = mfma(frag_cols<bf16x8_v>(qt, i * 32, j * 32 + 16 * t, lane), sf, dk[i]);
           }
         }
     }
-    if (more) put(smem + (cur ^ 1) * STAGE);
+    wait_vm0();
     __syncthreads();
   }
+  if (!active) return;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -652,11 +704,6 @@ __global__ void attn_bwd_kv_f32_kernel(AttnF p) {
   }
 }
 
-lc_status set_lds(const void *fn, size_t bytes) {
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  return e == hipSuccess ? LC_OK : hip_fail(e, "attention: setting the LDS size");
-}
-
 lc_status check_common(const lc_attn_args &a, bool bwd) {
   if (a.B <= 0 || a.S <= 0 || a.H <= 0 || a.hd <= 0)
     return fail(LC_ERR_INVALID_ARG, "attention: dimensions must be positive");
@@ -704,15 +751,34 @@ AttnP mc_params(const lc_attn_args &a) {
   p.dk = static_cast<__bf16 *>(a.dk);
   p.dv = static_cast<__bf16 *>(a.dv);
   p.D = static_cast<float *>(a.scratch);
+  const int64_t rows = (int64_t)a.B * a.S, d = (int64_t)a.H * HD;
+  const size_t dbytes = ((size_t)rows * a.H * sizeof(float) + 255) / 256 * 256;
+  p.qkvb = a.scratch ? reinterpret_cast<__bf16 *>(static_cast<char *>(a.scratch) + dbytes) : nullptr;
   p.rcos = a.rope_cos;
   p.rsin = a.rope_sin;
   p.ld_qkv = a.ld_qkv;
   p.ld_o = a.ld_o;
   p.ld_d = a.ld_dqkv;
+  p.ld_b = 3 * d;
+  p.qkv_bytes = (uint32_t)(((rows - 1) * a.ld_qkv + d) * 2);
+  p.o_bytes = (uint32_t)(((rows - 1) * a.ld_o + d) * 2);
+  p.b_bytes = (uint32_t)(((rows - 1) * p.ld_b + d) * 2);
+  p.lse_bytes = (uint32_t)(rows * a.H * sizeof(float));
   p.S = a.S;
   p.H = a.H;
+  p.B = a.B;
   p.scale = 1.0f / sqrtf((float)a.hd);
   return p;
+}
+
+// buffer offsets are 32-bit: every matrix the kernels stream must span less than 2 GiB
+lc_status check_extents(const lc_attn_args &a) {
+  const int64_t rows = (int64_t)a.B * a.S, d = (int64_t)a.H * HD;
+  const int64_t lim = (int64_t)1 << 31;
+  if (((rows - 1) * a.ld_qkv + d) * 2 >= lim || ((rows - 1) * a.ld_o + d) * 2 >= lim ||
+      ((rows - 1) * 3 * d + d) * 2 >= lim)
+    return fail(LC_ERR_UNSUPPORTED, "attention: a q/k/v/o matrix spans 2 GiB or more");
+  return LC_OK;
 }
 
 AttnF f32_params(const lc_attn_args &a) {
@@ -739,29 +805,24 @@ AttnF f32_params(const lc_attn_args &a) {
 
 template <typename QE>
 lc_status fwd_mc(const lc_attn_args &a, hipStream_t s) {
-  const size_t lds = 2 * 2 * TILE;
-  static bool once = false;
-  if (!once) { LC_TRY(set_lds((const void *)attn_fwd_kernel<QE>, lds)); once = true; }
-  hipLaunchKernelGGL(attn_fwd_kernel<QE>, dim3(a.S / QB, a.H, a.B), dim3(256), lds, s, mc_params(a));
+  LC_TRY(check_extents(a));
+  const unsigned nqb = (unsigned)((a.S + ROWS - 1) / ROWS);
+  hipLaunchKernelGGL(attn_fwd_kernel<QE>, dim3(nqb, a.H, a.B), dim3(NT), 0, s, mc_params(a));
   return check_launch("attn_fwd_kernel");
 }
 
 template <typename QE>
 lc_status bwd_mc(const lc_attn_args &a, hipStream_t s) {
+  LC_TRY(check_extents(a));
   const AttnP p = mc_params(a);
-  hipLaunchKernelGGL(attn_bwd_prep_kernel, dim3((unsigned)((int64_t)a.B * a.S)), dim3(256), 0, s, p,
-                     a.H * HD);
+  hipLaunchKernelGGL(attn_bwd_prep_kernel<QE>, dim3((unsigned)((int64_t)a.B * a.S)), dim3(256), 0,
+                     s, p, a.H * HD);
   LC_TRY(check_launch("attn_bwd_prep_kernel"));
-  const size_t lds_dq = 2 * 3 * TILE, lds_kv = 2 * (4 * TILE + 512);
-  static bool once = false;
-  if (!once) {
-    LC_TRY(set_lds((const void *)attn_bwd_dq_kernel<QE>, lds_dq));
-    LC_TRY(set_lds((const void *)attn_bwd_dkdv_kernel<QE>, lds_kv));
-    once = true;
-  }
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<QE>, dim3(a.S / QB, a.H, a.B), dim3(256), lds_kv, s, p);
+  const unsigned nb = (unsigned)((a.S + ROWS - 1) / ROWS);
+  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<QE>, dim3((unsigned)((a.S + KV_ROWS - 1) / KV_ROWS), a.H, a.B),
+                     dim3(KV_WAVES * 64), 0, s, p);
   LC_TRY(check_launch("attn_bwd_dkdv_kernel"));
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(a.S / QB, a.H, a.B), dim3(256), lds_dq, s, p);
+  hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(nb, a.H, a.B), dim3(NT), 0, s, p);
   return check_launch("attn_bwd_dq_kernel");
 }
 

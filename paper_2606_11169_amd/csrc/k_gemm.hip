@@ -7,32 +7,24 @@
 //
 // Tile: 256 x 256 per workgroup of 512 threads (8 waves, 4 along m x 2 along
 // n); each wave owns 64 x 128 = 2 x 4 MFMA blocks of 32 x 32. K is walked in
-// halves of 32: LDS is a ring of four 32 KiB slots, each holding one half
-// (A 256 x 32 | B 256 x 32), so three halves (96 KiB per CU) are always in
-// flight from HBM/L2 while the fourth is being multiplied. Latency of the
-// global->LDS path, not LDS or matrix-core throughput, is what bounds this
-// kernel, and the ring is sized for it.
-//
-// The eight waves form two groups of four (waves 0-3 and 4-7; one wave of
-// each on every SIMD) that run one phase apart ("ping-pong"): while one group
-// multiplies a half out of registers, the other reads its fragments of that
-// half from LDS, so every SIMD's matrix core always has a wave to serve.
-//   phase 2j:   group 0 reads half j,     group 1 multiplies half j-1
-//   phase 2j+1: group 0 multiplies half j, group 1 reads half j
-// Half j+3 goes into the slot of half j-1, which is free after phase 2j-1:
-// group 0 starts its A part at the start of phase 2j, group 1 its B part at
-// the start of phase 2j+1, and each group waits (vmcnt) for its part of half
-// j+1 before the barrier that ends phase 2j+1.
+// stages of 64: LDS holds two 64 KiB stages (A 256 x 64 | B 256 x 64); while
+// the waves multiply stage s, stage s + 1 streams in from HBM/L2, and one
+// barrier per stage both publishes the new stage and frees the old one.
+// Waves 0-3 stream A, waves 4-7 stream B (8 loads of 1 KiB per wave per
+// stage). A stage is multiplied in two halves of k = 32 (fragments of one
+// half in registers at a time).
 //
 // Operand tiles go from HBM straight into LDS (buffer_load_dwordx4 ... lds:
 // lane l of a wave's load fills bytes [16 l, 16 l + 16) of a 1 KiB LDS run),
 // so no register staging is needed; each lane picks the global 16 bytes that
 // belong at its LDS slot, which is how the tiles are swizzled. Buffer
 // descriptors make out-of-range lanes (matrix edges, K tail) read zeros.
-//   k-major operand: LDS rows of 32 k (64 B); 16-byte chunk c of row r sits
-//     at chunk c ^ ((r >> 2) & 3). A fragment (32 rows at one k chunk, 16
-//     bytes per lane) is one ds_read_b128 and every 16-lane phase touches all
-//     64 banks once.
+//   k-major operand: LDS rows of 64 k (128 B, one full cache line of the
+//     operand row per load lane group); 16-byte chunk c of row r sits at
+//     chunk c ^ ((r >> 1) & 7). A fragment (32 rows at one k chunk, 16 bytes
+//     per lane) is one ds_read_b128, and every 16 lanes touch all 64 banks
+//     once. (Rows of 32 k, i.e. half cache lines per load, cost a third of
+//     the throughput of the global->LDS path.)
 //   m/n-major operand (a weight read as dX = dY W, both operands of a weight
 //     gradient dW = dY^T X): LDS rows of one k and 256 m (512 B), chunk c of
 //     row k at chunk c ^ (4 (k & 3)). The fragment is read with the CDNA4
@@ -56,13 +48,12 @@ namespace lc {
 namespace {
 
 constexpr int BM = 256, BN = 256;
-constexpr int KH = 32;             // k per half (one LDS ring slot)
-constexpr int NSLOT = 4;           // ring slots
+constexpr int KS = 64;             // k per stage
 constexpr int NT = 512;            // threads per workgroup (8 waves)
 constexpr int WM = 64, WN = 128;   // wave tile
 constexpr int FM = WM / 32, FN = WN / 32;
-constexpr int HALF_BYTES = BM * KH * 2;       // one operand's half in LDS (16 KiB)
-constexpr int SLOT_BYTES = 2 * HALF_BYTES;    // A half | B half
+constexpr int OPND_BYTES = BM * KS * 2;       // one operand's stage in LDS (32 KiB)
+constexpr int STAGE_BYTES = 2 * OPND_BYTES;   // A | B
 constexpr uint32_t OOB = 0x80000000u;    // buffer offset beyond every operand: reads 0
 
 typedef __attribute__((ext_vector_type(4))) short s16x4_v;
@@ -118,22 +109,23 @@ __device__ __forceinline__ void dma16(i32x4_v rs, lds_t *lds, uint32_t off) {
                : "memory", "m0");
 }
 
-// One wave's share of an operand's loads: 4 of the 16 1-KiB LDS runs of a
-// 256 x 32 half (the four waves of a group load one operand).
-//   k-major: run q = rows 16q .. 16q+15; lane l -> row 16q + l/4, LDS chunk
-//     l%4 holding global k chunk (l%4) ^ ((row >> 2) & 3).
+// One wave's share of an operand's loads: 8 of the 32 1-KiB LDS runs of a
+// 256 x 64 stage (the four waves of a group load one operand).
+//   k-major: run q = rows 8q .. 8q+7; lane l -> row 8q + l/8, LDS chunk l%8
+//     holding global k chunk (l%8) ^ ((row >> 1) & 7).
 //     ROWMAP 0: tile row r -> operand row base + r (valid below lim)
 //     ROWMAP 1 (SwiGLU B rows): tile row r -> gate row ob + (r>>7)*64 + (r&63)
 //       for (r&127) < 64, else up row lim + ob + (r>>7)*64 + (r&63); valid
 //       while the output column ob + (r>>7)*64 + (r&63) < lim.
 //   m/n-major: run q = k rows 2q, 2q+1; lane l -> k row 2q + l/32, LDS chunk
 //     l%32 holding global columns 8 ((l%32) ^ (4 (krow & 3))) .. +7.
-// Run t of wave w is q = 4w + t: consecutive runs are a fixed byte distance
-// apart in the operand. For k-major runs the swizzle term (row >> 2) & 3 is
-// (l >> 4) & 3 for every run; for m/n-major runs (krow & 3) depends on the
-// parity of t (2 k rows on flip bit 1). The per-lane state is a row offset,
-// the two parity variants of the in-row offset, a validity mask and a k
-// position; everything else is wave-uniform.
+// Run t of wave w is q = 8w + t: consecutive runs are a fixed byte distance
+// apart in the operand, and the swizzle term of a run depends only on the
+// parity of t ((row >> 1) & 7 = (l >> 4) + 4 (t & 1) for k-major runs,
+// krow & 3 = (2t + l/32) & 3 for m/n-major ones). The per-lane state is a row
+// offset, the two parity variants of the in-row offset (and, k-major, of the
+// lane's k position), a validity mask and a k position; everything else is
+// wave-uniform.
 template <bool KMAJ, int ROWMAP>
 struct Stream {
   uint32_t base;     // byte offset of run 0's row (k-major) or k row (m/n-major)
@@ -141,36 +133,40 @@ struct Stream {
   uint32_t run;      // byte distance between consecutive runs
   uint32_t kb;       // bytes per unit of k
   uint32_t rows;     // bit t set when run t's row / columns are inside the operand
-  int kl;            // k-major: first k of this lane's chunk; m/n-major: k row of run 0
+  int kl[2];         // k-major: first k of this lane's chunk (even / odd runs);
+                     // m/n-major: k row of run 0 (both entries)
 
   __device__ __forceinline__ void init(int64_t ld, int base_row, int lim, int wave, int lane) {
     if constexpr (KMAJ) {
-      const int r0 = 64 * wave + (lane >> 2);  // tile row of run 0; (r >> 2) & 3 == (lane >> 4) & 3
-      kl = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+      const int sw = lane >> 4;  // (row >> 1) & 7 of even runs; odd runs add 4
+      kl[0] = 8 * ((lane & 7) ^ sw);
+      kl[1] = 8 * ((lane & 7) ^ (sw + 4));
       int grow0, oc0;
       if constexpr (ROWMAP == 0) {
-        grow0 = base_row + r0;
+        grow0 = base_row + 64 * wave + (lane >> 3);
         oc0 = grow0;
       } else {
-        oc0 = base_row + (r0 >> 7) * 64 + (r0 & 63);
-        grow0 = ((r0 & 127) < 64) ? oc0 : lim + oc0;
+        // tile rows 64 w .. 64 w + 63: gate rows for even w, up rows for odd w
+        oc0 = base_row + (wave >> 1) * 64 + (lane >> 3);
+        grow0 = (wave & 1) ? lim + oc0 : oc0;
       }
       rows = 0;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) rows |= (oc0 + 16 * t < lim ? 1u : 0u) << t;
+      for (int t = 0; t < 8; ++t) rows |= (oc0 + 8 * t < lim ? 1u : 0u) << t;
       base = rows ? (uint32_t)((int64_t)grow0 * ld * 2) : 0u;
-      col[0] = col[1] = (uint32_t)(kl * 2);
-      run = (uint32_t)(16 * ld * 2);
+      col[0] = (uint32_t)(kl[0] * 2);
+      col[1] = (uint32_t)(kl[1] * 2);
+      run = (uint32_t)(8 * ld * 2);
       kb = 2;
     } else {
       static_assert(ROWMAP == 0, "row remap needs a k-major operand");
-      const int kr0 = 8 * wave + (lane >> 5);         // k row of run 0; kr0 & 3 == lane >> 5
+      const int kr0 = 16 * wave + (lane >> 5);        // k row of run 0; kr0 & 3 == lane >> 5
       const int c0 = (lane & 31) ^ (4 * (lane >> 5));  // odd runs: c0 ^ 8
       const int gm0 = base_row + 8 * c0, gm1 = base_row + 8 * (c0 ^ 8);
-      kl = kr0;
+      kl[0] = kl[1] = kr0;
       rows = 0;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) rows |= (((t & 1) ? gm1 : gm0) < lim ? 1u : 0u) << t;
+      for (int t = 0; t < 8; ++t) rows |= (((t & 1) ? gm1 : gm0) < lim ? 1u : 0u) << t;
       base = (uint32_t)((int64_t)kr0 * ld * 2);
       col[0] = gm0 < lim ? (uint32_t)(gm0 * 2) : 0u;
       col[1] = gm1 < lim ? (uint32_t)(gm1 * 2) : 0u;
@@ -179,27 +175,27 @@ struct Stream {
     }
   }
 
-  // the wave's 4 runs of the half starting at k0, into `lds` (the operand's half)
+  // the wave's 8 runs of the stage starting at k0, into `lds` (the operand's stage)
   __device__ __forceinline__ void load(i32x4_v rs, lds_t *lds, int wave, int k0, int K) const {
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < 8; ++t) {
       bool ok = (rows >> t) & 1u;
-      if constexpr (KMAJ) ok = ok && k0 + kl < K;
-      else ok = ok && k0 + kl + 2 * t < K;
+      if constexpr (KMAJ) ok = ok && k0 + kl[t & 1] < K;
+      else ok = ok && k0 + kl[0] + 2 * t < K;
       const uint32_t off = ok ? base + t * run + col[t & 1] + (uint32_t)k0 * kb : OOB;
-      dma16(rs, lds + (4 * wave + t) * 1024, off);
+      dma16(rs, lds + (8 * wave + t) * 1024, off);
     }
   }
 };
 
 // MFMA operand of 32 rows (row0 .. row0+31) at k = 16 s + 8 (lane / 32) + [0, 8)
-// of the half stored at t
+// of the stage stored at t (s = 0 .. 3)
 template <bool KMAJ>
 __device__ __forceinline__ bf16x8_v frag(const lds_t *t, int row0, int s, int lane) {
   if constexpr (KMAJ) {
     const int row = row0 + (lane & 31);
     const int c = 2 * s + (lane >> 5);
-    return *reinterpret_cast<const lds_v8 *>(t + row * 64 + ((c ^ ((row >> 2) & 3)) << 4));
+    return *reinterpret_cast<const lds_v8 *>(t + row * 128 + ((c ^ ((row >> 1) & 7)) << 4));
   } else {
     const int i16 = lane & 15, g = lane >> 4;
     const int m = row0 + 16 * (g & 1) + 4 * (i16 & 3);
@@ -213,9 +209,21 @@ __device__ __forceinline__ bf16x8_v frag(const lds_t *t, int row0, int s, int la
   }
 }
 
+// Scheduling pattern for one k-step: the NRD LDS reads of the next k-step
+// spread over the NMF MFMAs of this one (reads first, as evenly as possible).
+template <int NRD, int NMF, int I = 0>
+__device__ __forceinline__ void interleave_steps() {
+  if constexpr (I < NMF) {
+    constexpr int r = NRD / NMF + (I < NRD % NMF ? 1 : 0);
+    if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // one MFMA
+    interleave_steps<NRD, NMF, I + 1>();
+  }
+}
+
 template <bool A_K, bool B_K, int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
-  __shared__ __align__(16) char ring[NSLOT * SLOT_BYTES];
+  __shared__ __align__(16) char ring[2 * STAGE_BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -276,76 +284,72 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   lds_t *const R0 = LDS_AS(char, ring);
-  const int nh = (kend - kbeg + KH - 1) / KH;  // halves
-  // group 0 streams the A halves, group 1 the B halves
+  const int ns = (kend - kbeg + KS - 1) / KS;  // stages
+  // group 0 streams A, group 1 streams B
   const i32x4_v rs = grp == 0 ? make_rsrc(p.A, p.a_bytes) : make_rsrc(Bp, p.b_bytes);
   Stream<A_K, 0> sa_;
   Stream<B_K, SWI ? 1 : 0> sb_;
   if (grp == 0) sa_.init(p.lda, m0, m_lim, w4, lane);
   else sb_.init(p.ldb, n0, p.N, w4, lane);
-  auto load = [&](int j) {  // this group's operand of half j
-    lds_t *slot = R0 + (j & (NSLOT - 1)) * SLOT_BYTES;
-    if (grp == 0) sa_.load(rs, slot, w4, kbeg + j * KH, kend);
-    else sb_.load(rs, slot + HALF_BYTES, w4, kbeg + j * KH, kend);
-  };
-  // wait until this wave's loads of half j+1 have landed (loads retire in
-  // order; the younger halves j+2, j+3 may stay in flight)
-  auto wait_next = [&](int j) {
-    if (j + 3 < nh) __builtin_amdgcn_s_waitcnt(0x0F78);       // vmcnt(8)
-    else if (j + 2 < nh) __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt(4)
-    else __builtin_amdgcn_s_waitcnt(0x0F70);                  // vmcnt(0)
+  auto load = [&](int st) {  // this group's operand of stage st
+    lds_t *stage = R0 + (st & 1) * STAGE_BYTES;
+    if (grp == 0) sa_.load(rs, stage, w4, kbeg + st * KS, kend);
+    else sb_.load(rs, stage + OPND_BYTES, w4, kbeg + st * KS, kend);
   };
 
-  typedef bf16x8_v FragA[2][FM];
-  typedef bf16x8_v FragB[2][FN];
-  auto read_half = [&](int j, FragA &af, FragB &bfr) {
-    const lds_t *slot = R0 + (j & (NSLOT - 1)) * SLOT_BYTES;
+  typedef bf16x8_v FragA[FM];
+  typedef bf16x8_v FragB[FN];
+  // fragments of k-step q (k 16q .. 16q + 15) of stage st
+  auto read_step = [&](int st, int q, FragA &af, FragB &bfr) {
+    const lds_t *stage = R0 + (st & 1) * STAGE_BYTES;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int i = 0; i < FM; ++i) af[i] = frag<A_K>(stage, wm * WM + i * 32, q, lane);
 #pragma unroll
-      for (int i = 0; i < FM; ++i) af[s][i] = frag<A_K>(slot, wm * WM + i * 32, s, lane);
-#pragma unroll
-      for (int jj = 0; jj < FN; ++jj)
-        bfr[s][jj] = frag<B_K>(slot + HALF_BYTES, wn * WN + jj * 32, s, lane);
-    }
+    for (int jj = 0; jj < FN; ++jj) bfr[jj] = frag<B_K>(stage + OPND_BYTES, wn * WN + jj * 32, q, lane);
   };
   auto multiply = [&](const FragA &af, const FragB &bfr) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int jj = 0; jj < FN; ++jj)
-          acc[i][jj] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[s][jj], af[s][i], acc[i][jj], 0, 0, 0);
+      for (int jj = 0; jj < FN; ++jj)
+        acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[jj], af[i], acc[i][jj], 0, 0, 0);
   };
-  // A phase boundary: no instruction moves across it; both groups meet at it.
-  auto barrier = [&]() {
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_barrier();
+  // LDS reads of one k-step: one per k-major fragment, two per m/n-major one
+  constexpr int NRD = (A_K ? FM : 2 * FM) + (B_K ? FN : 2 * FN);
+  constexpr int NMF = FM * FN;
+  auto interleave = [&]() {
+    interleave_steps<NRD, NMF>();
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  // prologue: halves 0, 1, 2 in flight, half 0 landed everywhere
-  for (int j = 0; j < 3 && j < nh; ++j) load(j);
-  if (nh > 2) __builtin_amdgcn_s_waitcnt(0x0F78);       // vmcnt(8)
-  else if (nh > 1) __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt(4)
-  else __builtin_amdgcn_s_waitcnt(0x0F70);
+  // Software pipeline over k-steps: the fragments of step q + 1 are read
+  // while step q multiplies (two fragment sets in registers). Stage s + 1 goes
+  // into the buffer of stage s - 1, whose last fragments every wave has read
+  // before the barrier that published stage s. The barrier that publishes
+  // stage s + 1 (after each wave's wait for its own loads and reads) sits
+  // before the last k-step of stage s, so the first reads of stage s + 1
+  // overlap that k-step's MFMAs.
+  FragA fa[2];
+  FragB fb[2];
+  if (ns > 0) load(0);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   __syncthreads();
-  if (grp == 1) barrier();
-  for (int j = 0; j < nh; ++j) {
-    FragA af;
-    FragB bfr;
-    if (j + 3 < nh) load(j + 3);  // into the slot of half j-1
-    read_half(j, af, bfr);
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments in registers
-    if (grp == 1) wait_next(j);
-    barrier();
-    multiply(af, bfr);
-    if (grp == 0) wait_next(j);
-    barrier();
+  if (ns > 0) read_step(0, 0, fa[0], fb[0]);
+  for (int st = 0; st < ns; ++st) {
+    if (st + 1 < ns) load(st + 1);
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      read_step(st, q + 1, fa[(q + 1) & 1], fb[(q + 1) & 1]);
+      multiply(fa[q & 1], fb[q & 1]);
+      interleave();
+    }
+    __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0)
+    __syncthreads();
+    // (after the last stage this reads the other buffer's stale data, unused)
+    read_step(st + 1, 0, fa[0], fb[0]);
+    multiply(fa[1], fb[1]);
+    interleave();
   }
-  if (grp == 0) barrier();
 
   const int frow = lane & 31;
   const int fhalf = lane >> 5;

@@ -46,6 +46,11 @@ constexpr int ROWS = 256;  // queries (or keys) per workgroup: 8 waves x 32
 constexpr int KB = 64;     // keys (or queries) per inner block
 constexpr int NT = 512;
 constexpr float LOG2E = 1.4426950408889634f;
+
+// 2^x by the hardware instruction (v_exp_f32): no range reduction for results
+// below the normal range, which only ever go into softmax weights that are
+// rounded to 16 bits (where they are zero anyway); 2^-inf = 0.
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 constexpr float LN2 = 0.6931471805599453f;
 constexpr int TILE = KB * HD * 2;  // 16 KiB: one [64][128] tile of 2-byte elements
 
@@ -237,19 +242,22 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
       for (int es = 0; es < 8; ++es)
 #pragma unroll
         for (int j = 0; j < 2; ++j) s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), qf[es], s[j]);
-      const bool diag = k0 + KB - 1 > q0;
+      if (k0 + KB - 1 > q0) {  // diagonal block (wave-uniform): mask keys after the query
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (k0 + j * 32 + out_row(r, hf) > myq) s[j][r] = -INFINITY;
+      }
       float mx = -INFINITY;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if (diag && k0 + j * 32 + out_row(r, hf) > myq) s[j][r] = -INFINITY;
-          mx = fmaxf(mx, s[j][r]);
-        }
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[j][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float mn = fmaxf(m, mx * sc);
       if (__any(mn > m)) {  // rescale only when some query's maximum moved
-        const float alpha = mn > m ? exp2f(m - mn) : 1.0f;
+        const float alpha = mn > m ? ex2(m - mn) : 1.0f;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -262,7 +270,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float pv = exp2f(__builtin_fmaf(s[j][r], sc, -m));
+          const float pv = ex2(__builtin_fmaf(s[j][r], sc, -m));
           s[j][r] = pv;
           ls += pv;
         }
@@ -430,13 +438,18 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
           s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), qf[es], s[j]);
           dp[j] = mfma(frag_rows<bf16x8_v>(cur + 2 * TILE, j * 32, es, lane), df[es], dp[j]);
         }
-      const bool diag = k0 + KB - 1 > q0;
+      if (k0 + KB - 1 > q0) {  // diagonal block (wave-uniform): P = 0 for keys after the query
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (k0 + j * 32 + out_row(r, hf) > myq) s[j][r] = -INFINITY;
+      }
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float pv = exp2f(__builtin_fmaf(s[j][r], sc, -lse2));
-          if (diag && k0 + j * 32 + out_row(r, hf) > myq) pv = 0.0f;
+          const float pv = ex2(__builtin_fmaf(s[j][r], sc, -lse2));
           dp[j][r] = pv * (dp[j][r] - Dq);
         }
       const lds_t *kt = cur + TILE;
@@ -543,14 +556,19 @@ __global__ __launch_bounds__(KV_WAVES * 64) void attn_bwd_dkdv_kernel(AttnP p) {
           s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), kf[es], s[j]);
           dp[j] = mfma(frag_rows<bf16x8_v>(cur + 2 * TILE, j * 32, es, lane), vf[es], dp[j]);
         }
-      const bool diag = q0 < k0w + 31;
+      if (q0 < k0w + 31) {  // diagonal block (wave-uniform): P = 0 for queries before the key
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (q0 + j * 32 + out_row(r, hf) < myk) s[j][r] = -INFINITY;
+      }
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int qi = j * 32 + out_row(r, hf);
-          float pv = exp2f(__builtin_fmaf(s[j][r], sc, -sL[qi] * LOG2E));
-          if (diag && q0 + qi < myk) pv = 0.0f;
+          const float pv = ex2(__builtin_fmaf(s[j][r], sc, -sL[qi] * LOG2E));
           s[j][r] = pv;
           dp[j][r] = pv * (dp[j][r] - sL[64 + qi]);
         }

@@ -35,6 +35,13 @@ HIP_FLAGS = [
 ]
 # kernels whose results are defined operation by operation (bit-exact paths)
 NO_CONTRACT = {"k_optim.hip"}
+# per-file code generation options
+EXTRA_FLAGS = {
+    # keep MFMA results in VGPRs: the attention kernels apply the softmax to
+    # them with vector instructions, and accumulation-register copies cost more
+    # than they save
+    "k_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
 
 
 def _run(cmd):
@@ -62,6 +69,7 @@ def build(verbose: bool = False) -> str:
         flags = list(HIP_FLAGS)
         if f in NO_CONTRACT:
             flags.append("-ffp-contract=off")
+        flags.extend(EXTRA_FLAGS.get(f, []))
         jobs.append([HIPCC, *flags, "-c", os.path.join(CSRC, f), "-o", o])
         objs.append(o)
     workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))

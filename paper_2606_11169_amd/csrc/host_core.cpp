@@ -191,10 +191,10 @@ size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E) {
 }
 
 size_t attn_scratch_size(int64_t B, int64_t S, int64_t H) {
-  // D (fp32 [B, H, S]), then bf16 copies of q, k, v ([B*S, 3*H*128]) for the
-  // matrix-core backward
+  // D (fp32 [B, H, S]), then for the matrix-core backward bf16 rows of v
+  // ([B*S, H*128]) and bf16 transposes of q, k, dO ([B][H][128][S] each)
   const size_t dbytes = ((size_t)(B * S * H) * sizeof(float) + 255) / 256 * 256;
-  return dbytes + (size_t)(B * S) * 3 * (size_t)H * 128 * 2;
+  return dbytes + (size_t)(B * S) * 4 * (size_t)H * 128 * 2;
 }
 
 }  // namespace lc

@@ -18,19 +18,26 @@
 // element type (P is rounded to it too).
 //
 // Backward (deterministic, no atomics): a prep pass computes D = rowsum(dO*O)
-// and bf16 copies of q, k, v; then one kernel per 256 keys accumulates
-// dV^T = dO^T P and dK^T = Q^T dS over the query blocks at or after the
-// diagonal, and one kernel per 256 queries accumulates dQ^T = K^T dS^T over
-// the visible key blocks. Both recompute P from the forward's log-sum-exp with
-// the forward's q/k element type (so P matches the forward) and take every
-// gradient product in bf16. RoPE's inverse rotation of dq/dk is applied in
-// the epilogues.
+// and writes bf16 transposes of q, k and dO (per head, [head dim][position])
+// plus, for fp16 inputs, a bf16 copy of v; then one kernel per 128 keys
+// accumulates dV^T = dO^T P and dK^T = Q^T dS over the query blocks at or
+// after the diagonal, and one kernel per 256 queries accumulates
+// dQ^T = K^T dS^T over the visible key blocks. Both recompute P from the
+// forward's log-sum-exp with the forward's q/k element type (so P matches the
+// forward) and take every gradient product in bf16. RoPE's inverse rotation
+// of dq/dk is applied in the epilogues.
 //
-// Every LDS tile is [64 rows][128 columns] of 2-byte elements (256-byte rows
-// of 16 chunks); chunk c of row r sits at chunk c ^ f(r) with
+// Row tiles are [64 rows][128 columns] of 2-byte elements (256-byte rows of 16
+// chunks); chunk c of row r sits at chunk c ^ f(r) with
 // f(r) = ((r & 3) << 2) | ((r >> 2) & 3). A 128-bit fragment read (16
 // consecutive rows, one chunk) and a transposing read (4 consecutive rows,
 // four chunks) both touch every bank once per phase.
+// Transposed tiles (backward) are [128 head-dim rows][64 positions] (128-byte
+// rows of 8 chunks, chunk c of row r at c ^ ((r >> 1) & 7)). The prep pass
+// stores the positions of every 16-group in the order 0-3, 8-11, 4-7, 12-15:
+// the order in which a 32 x 32 accumulator's registers 8t .. 8t+7 hold their
+// rows, so the k values of a gradient product's fragment are 16 contiguous
+// bytes (one ds_read_b128) instead of two transposing reads.
 #include "common.hpp"
 
 #include <math.h>
@@ -142,6 +149,30 @@ __device__ __forceinline__ VT frag_cols(const lds_t *t, int col0, int kbase, int
   return __builtin_bit_cast(VT, v);
 }
 
+// Run `run` (0..15) of a transposed [128][64] tile: head-dim rows 8 run ..
+// 8 run + 7, positions pos0 .. pos0 + 63 of the [128][S] matrix of one head
+// that starts at element `hbase` of its buffer.
+__device__ __forceinline__ void tt_run(i32x4_v rs, lds_t *tile, int run, int64_t hbase, int S,
+                                       int pos0, int lane) {
+  const int r = 8 * run + (lane >> 3);
+  const int c = (lane & 7) ^ ((r >> 1) & 7);
+  const uint32_t off = (uint32_t)((hbase + (int64_t)r * S + pos0 + 8 * c) * 2);
+  dma16(rs, tile + run * 1024, off);
+}
+
+// MFMA operand of transposed-tile rows row0 .. row0+31 (lane l: row row0 + l % 32)
+// whose 8 k values are the stored positions 32 j + 16 t + 8 (lane / 32) + [0, 8):
+// in the prep pass's order these are the positions a 32 x 32 accumulator's
+// registers 8t .. 8t+7 hold (rows 16t + 4 hf + [0, 4) and 16t + 8 + 4 hf + [0, 4)
+// of block j).
+template <typename VT>
+__device__ __forceinline__ VT frag_t(const lds_t *t, int row0, int j, int tt, int lane) {
+  const int r = row0 + (lane & 31);
+  const int c = 4 * j + 2 * tt + (lane >> 5);
+  return *reinterpret_cast<const __attribute__((address_space(3))) VT *>(t + r * 128 +
+                                                                         ((c ^ ((r >> 1) & 7)) << 4));
+}
+
 template <typename E>
 __device__ __forceinline__ typename V8<E>::type pack8(const f32x16_v &a, int base) {
   typename V8<E>::type r;
@@ -181,10 +212,13 @@ struct AttnP {
   const __bf16 *dout;
   __bf16 *dq, *dk, *dv;
   float *D;
-  __bf16 *qkvb;            // bf16 copies of q, k, v (backward): [B*S, 3*H*hd]
+  // backward: bf16 rows of v (p.v itself for bf16 inputs), and bf16 transposes
+  // [B][H][128][S] of q, k and dO (positions permuted within 16-groups)
+  const __bf16 *vb;
+  __bf16 *vb_w, *qt, *kt, *dot;
   const float *rcos, *rsin;
-  int64_t ld_qkv, ld_o, ld_d, ld_b;
-  uint32_t qkv_bytes, o_bytes, b_bytes, lse_bytes;  // buffer extents (q/k/v from p.q)
+  int64_t ld_qkv, ld_o, ld_d, ld_vb;
+  uint32_t qkv_bytes, o_bytes, vb_bytes, t_bytes, lse_bytes;  // buffer extents (q/k/v from p.q)
   int S, H, B;
   float scale;  // 1/sqrt(hd)
 };
@@ -304,31 +338,71 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
 }
 
 // ---------------------------------------------------------------- backward
-// D[b,h,i] = sum_e dO[i,e] O[i,e] (16 lanes per head), and, for fp16 q/k/v,
-// bf16 copies of the token row's q, k, v. One workgroup per token row.
+// One workgroup per (64-position block, head, batch row): D[b,h,i] =
+// sum_e dO[i,e] O[i,e]; the block's columns of dO, q and k transposed into
+// [B][H][128][S] bf16 (positions of each 16-group in the order 0-3, 8-11,
+// 4-7, 12-15) through an LDS tile; for fp16 q/k/v, the bf16 rows of v.
 template <typename QE>
-__global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p, int d) {
-  const int64_t row = blockIdx.x;  // b*S + s
-  const int b = (int)(row / p.S), s = (int)(row % p.S);
-  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
-    const bf16x8_v a = *reinterpret_cast<const bf16x8_v *>(p.dout + row * p.ld_o + c);
-    const bf16x8_v o = *reinterpret_cast<const bf16x8_v *>(p.o + row * p.ld_o + c);
-    float acc = 0.0f;
+__global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p) {
+  constexpr int W = 130;  // tile row stride (65 words): conflict-free fills and gathers
+  __shared__ __align__(16) __bf16 tile[64 * W];
+  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int t = threadIdx.x, r = t >> 2, qtr = t & 3;  // row, 32-column quarter
+  const int pos0 = blk * 64;
+  const int64_t grow = (int64_t)b * p.S + pos0 + r;
+  const int col = h * HD + qtr * 32;
+  const int64_t hbase = ((int64_t)b * p.H + h) * HD * p.S;
+
+  auto put = [&](int u, bf16x8_v v) {  // columns 32 qtr + 8u .. +7 of row r
+    uint32_t *w = reinterpret_cast<uint32_t *>(tile + r * W + qtr * 32 + 8 * u);
+    const uint4 x = __builtin_bit_cast(uint4, v);
+    w[0] = x.x;
+    w[1] = x.y;
+    w[2] = x.z;
+    w[3] = x.w;
+  };
+  auto write_t = [&](__bf16 *dst) {  // 1024 chunks of 8 stored positions
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int idx = t + 256 * it, c = idx & 7, n = idx >> 3;
+      const int rb = 16 * (c >> 1) + 4 * (c & 1);
+      bf16x8_v v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = tile[(rb + (e & 3) + 8 * (e >> 2)) * W + n];
+      *reinterpret_cast<bf16x8_v *>(dst + hbase + (int64_t)n * p.S + pos0 + 8 * c) = v;
+    }
+  };
+
+  float acc = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const bf16x8_v a = *reinterpret_cast<const bf16x8_v *>(p.dout + grow * p.ld_o + col + 8 * u);
+    const bf16x8_v o = *reinterpret_cast<const bf16x8_v *>(p.o + grow * p.ld_o + col + 8 * u);
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc += (float)a[i] * (float)o[i];
+    put(u, a);
+  }
+  acc += __shfl_xor(acc, 1, 64);
+  acc += __shfl_xor(acc, 2, 64);
+  if (qtr == 0) p.D[((int64_t)b * p.H + h) * p.S + pos0 + r] = acc;
+  __syncthreads();
+  write_t(p.dot);
 #pragma unroll
-    for (int o2 = 8; o2 > 0; o2 >>= 1) acc += __shfl_xor(acc, o2, 64);
-    if ((threadIdx.x & 15) == 0) p.D[((int64_t)b * p.H + c / HD) * p.S + s] = acc;
+  for (int src = 0; src < 2; ++src) {
+    __syncthreads();
+    const QE *X = static_cast<const QE *>(src == 0 ? p.q : p.k);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      put(u, to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(X + grow * p.ld_qkv + col + 8 * u)));
+    __syncthreads();
+    write_t(src == 0 ? p.qt : p.kt);
   }
   if constexpr (!std::is_same<QE, __bf16>::value) {
-    const void *src[3] = {p.q, p.k, p.v};
+    const QE *V = static_cast<const QE *>(p.v);
 #pragma unroll
-    for (int t = 0; t < 3; ++t)
-      for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(static_cast<const QE *>(src[t]) +
-                                                         row * p.ld_qkv + c);
-        *reinterpret_cast<bf16x8_v *>(p.qkvb + row * p.ld_b + t * d + c) = to_bf16x8<QE>(v);
-      }
+    for (int u = 0; u < 4; ++u)
+      *reinterpret_cast<bf16x8_v *>(p.vb_w + grow * p.ld_vb + col + 8 * u) =
+          to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(V + grow * p.ld_qkv + col + 8 * u));
   }
 }
 
@@ -358,16 +432,7 @@ __device__ __forceinline__ void store_row_t(__bf16 *row, const f32x16_v (&acc)[4
     }
 }
 
-// the bf16 versions of q, k, v read by the gradient products
-template <typename QE>
-__device__ __forceinline__ const __bf16 *bf_qkv(const AttnP &p, int t) {
-  if constexpr (std::is_same<QE, __bf16>::value)
-    return static_cast<const __bf16 *>(t == 0 ? p.q : t == 1 ? p.k : p.v);
-  else
-    return p.qkvb + t * (int64_t)p.H * HD;
-}
-
-// dQ: one workgroup per 256 queries; LDS stage = K (QE) | K (bf16) | V (bf16)
+// dQ: one workgroup per 256 queries; LDS stage = K (QE) | V (bf16) | K^T (bf16)
 template <typename QE>
 __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
@@ -384,7 +449,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   const bool active = q0 < p.S;
   const int myq = q0 + l32;
   const float sc = p.scale * LOG2E;
-  const int64_t ldb = std::is_same<QE, __bf16>::value ? p.ld_qkv : p.ld_b;
+  const int64_t hbase = ((int64_t)b * p.H + h) * HD * p.S;
 
   QV qf[8];
   bf16x8_v df[8];
@@ -407,18 +472,18 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc[i] = zero16();
 
-  // 48 runs per block: K (QE) runs 0-15, K (bf16) 16-31, V (bf16) 32-47; 6 per wave
+  // 48 runs per block: K (QE) runs 0-15, V (bf16) 16-31, K^T (bf16) 32-47; 6 per wave
   const i32x4_v rk = make_rsrc(p.k, p.qkv_bytes);
-  const i32x4_v rkb = make_rsrc(bf_qkv<QE>(p, 1), std::is_same<QE, __bf16>::value ? p.qkv_bytes : p.b_bytes);
-  const i32x4_v rvb = make_rsrc(bf_qkv<QE>(p, 2), std::is_same<QE, __bf16>::value ? p.qkv_bytes : p.b_bytes);
+  const i32x4_v rvb = make_rsrc(p.vb, p.vb_bytes);
+  const i32x4_v rkt = make_rsrc(p.kt, p.t_bytes);
   auto load = [&](int kb, lds_t *st) {
     const int64_t g0 = row0 + (int64_t)kb * KB;
 #pragma unroll
     for (int t = 0; t < 6; ++t) {
       const int run = 6 * w + t, which = run >> 4;
       if (which == 0) tile_run(rk, st, run & 15, g0, p.ld_qkv, h * HD, lane);
-      else if (which == 1) tile_run(rkb, st + TILE, run & 15, g0, ldb, h * HD, lane);
-      else tile_run(rvb, st + 2 * TILE, run & 15, g0, ldb, h * HD, lane);
+      else if (which == 1) tile_run(rvb, st + TILE, run & 15, g0, p.ld_vb, h * HD, lane);
+      else tt_run(rkt, st + 2 * TILE, run & 15, hbase, p.S, kb * KB, lane);
     }
   };
   const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
@@ -436,7 +501,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), qf[es], s[j]);
-          dp[j] = mfma(frag_rows<bf16x8_v>(cur + 2 * TILE, j * 32, es, lane), df[es], dp[j]);
+          dp[j] = mfma(frag_rows<bf16x8_v>(cur + TILE, j * 32, es, lane), df[es], dp[j]);
         }
       if (k0 + KB - 1 > q0) {  // diagonal block (wave-uniform): P = 0 for keys after the query
 #pragma unroll
@@ -452,15 +517,14 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
           const float pv = ex2(__builtin_fmaf(s[j][r], sc, -lse2));
           dp[j][r] = pv * (dp[j][r] - Dq);
         }
-      const lds_t *kt = cur + TILE;
+      const lds_t *kt = cur + 2 * TILE;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const bf16x8_v sf = pack8<__bf16>(dp[j], 8 * t);
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            acc[i] = mfma(frag_cols<bf16x8_v>(kt, i * 32, j * 32 + 16 * t, lane), sf, acc[i]);
+          for (int i = 0; i < 4; ++i) acc[i] = mfma(frag_t<bf16x8_v>(kt, i * 32, j, t, lane), sf, acc[i]);
         }
     }
     wait_vm0();
@@ -475,66 +539,82 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   store_row_t(p.dq + h * HD + (row0 + myq) * p.ld_d, acc, 1.0f, hf);
 }
 
-// dK, dV: one workgroup of 4 waves per 128 keys (each wave keeps its keys' K
-// and V operands and both accumulators, 256+ registers, so one wave per
-// SIMD); LDS stage = Q (QE) | Q (bf16) | dO | lse | D
-constexpr int KV_WAVES = 4, KV_ROWS = KV_WAVES * 32;
+// dK, dV: one workgroup of 8 waves per 128 keys. Waves w and w + 4 own the
+// same 32 keys (their K and V fragments stay in registers) and take the first
+// and the second 32 queries of every 64-query block at or after the diagonal;
+// at the end wave w + 4 hands its partial dK, dV to wave w through LDS, which
+// adds them (fixed order: deterministic). LDS stage (two of them) =
+// Q (QE) | dO | Q^T | dO^T | lse | D of one 64-query block.
+constexpr int KV_ROWS = 128;
 template <typename QE>
-__global__ __launch_bounds__(KV_WAVES * 64) void attn_bwd_dkdv_kernel(AttnP p) {
+__global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
-  constexpr int STAGE = 3 * TILE + 512;
+  constexpr int STAGE = 4 * TILE + 512;
   __shared__ __align__(16) char smem[2 * STAGE];
   lds_t *const L = LDS_AS(char, smem);
-  const int kblk = blockIdx.x;  // heaviest (earliest keys) first
-  const int h = blockIdx.y, b = blockIdx.z;
+  const int kblk = (int)blockIdx.x / p.H, h = (int)blockIdx.x % p.H;  // earliest (heaviest) keys first
+  const int b = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int pw = w & 3, hq = w >> 2;  // key block of the pair, query half
   const int l32 = lane & 31, hf = lane >> 5;
   const int64_t row0 = (int64_t)b * p.S;
-  const int k0w = kblk * KV_ROWS + w * 32;
-  const bool active = k0w < p.S;
+  const int k0w = kblk * KV_ROWS + pw * 32;
   const int myk = k0w + l32;
   const float sc = p.scale * LOG2E;
-  const int64_t ldb = std::is_same<QE, __bf16>::value ? p.ld_qkv : p.ld_b;
+  const int64_t hbase = ((int64_t)b * p.H + h) * HD * p.S;
 
   QV kf[8];
   bf16x8_v vf[8];
 #pragma unroll
   for (int es = 0; es < 8; ++es) {
-    if (active) {
-      const int64_t off = h * HD + (row0 + myk) * p.ld_qkv + es * 16 + hf * 8;
-      kf[es] = *reinterpret_cast<const QV *>(static_cast<const QE *>(p.k) + off);
-      vf[es] = to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(static_cast<const QE *>(p.v) + off));
-    } else {
-      kf[es] = QV{};
-      vf[es] = bf16x8_v{};
-    }
+    const int64_t off = h * HD + (row0 + myk) * p.ld_qkv + es * 16 + hf * 8;
+    kf[es] = *reinterpret_cast<const QV *>(static_cast<const QE *>(p.k) + off);
+    vf[es] = to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(static_cast<const QE *>(p.v) + off));
   }
   f32x16_v dk[4], dv[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) dk[i] = dv[i] = zero16();
 
-  // 48 runs per block: Q (QE) 0-15, Q (bf16) 16-31, dO 32-47 (12 per wave);
-  // the last wave also brings the block's lse and D (64 floats each)
-  const i32x4_v rq = make_rsrc(p.q, p.qkv_bytes);
-  const i32x4_v rqb = make_rsrc(bf_qkv<QE>(p, 0), std::is_same<QE, __bf16>::value ? p.qkv_bytes : p.b_bytes);
-  const i32x4_v rdo = make_rsrc(p.dout, p.o_bytes);
+  // 64 runs per block: wave w brings runs 8 (w & 1) .. + 7 of tile w >> 1
+  // (Q (QE), dO, Q^T, dO^T); the last wave also brings lse and D (64 floats each)
+  const int tl = w >> 1;
+  const i32x4_v rs = tl == 0 ? make_rsrc(p.q, p.qkv_bytes)
+                   : tl == 1 ? make_rsrc(p.dout, p.o_bytes)
+                   : tl == 2 ? make_rsrc(p.qt, p.t_bytes)
+                             : make_rsrc(p.dot, p.t_bytes);
   const i32x4_v rl = make_rsrc(p.lse, p.lse_bytes);
   const i32x4_v rd = make_rsrc(p.D, p.lse_bytes);
   const int64_t sbase = ((int64_t)b * p.H + h) * p.S;
-  auto load = [&](int qbi, lds_t *st) {
-    const int64_t g0 = row0 + (int64_t)qbi * KB;
+  // Byte offset of run t (0..15) of block qbi = ublk * qbi + urun * t + lbase
+  // + lcol[t & 3]: the same element addresses as tile_run / tt_run, with one
+  // per-lane base and four per-lane column variants (row tiles: the swizzle of
+  // row 4t + lane/16 depends on t & 3; transposed tiles: on t & 1).
+  uint32_t lbase, lcol[4], urun, ublk, u0;
+  if (tl < 2) {
+    const int64_t ld = tl == 0 ? p.ld_qkv : p.ld_o;
+    lbase = (uint32_t)(((row0 + (lane >> 4)) * ld + h * HD) * 2);
 #pragma unroll
-    for (int t = 0; t < 12; ++t) {
-      const int run = 12 * w + t, which = run >> 4;
-      if (which == 0) tile_run(rq, st, run & 15, g0, p.ld_qkv, h * HD, lane);
-      else if (which == 1) tile_run(rqb, st + TILE, run & 15, g0, ldb, h * HD, lane);
-      else tile_run(rdo, st + 2 * TILE, run & 15, g0, p.ld_o, h * HD, lane);
-    }
-    if (w == KV_WAVES - 1) {
+    for (int v = 0; v < 4; ++v) lcol[v] = (uint32_t)(16 * ((lane & 15) ^ ((((lane >> 4) & 3) << 2) | v)));
+    urun = (uint32_t)(4 * ld * 2);
+    ublk = (uint32_t)(KB * ld * 2);
+  } else {
+    lbase = (uint32_t)((hbase + (int64_t)(lane >> 3) * p.S) * 2);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) lcol[v] = (uint32_t)(16 * ((lane & 7) ^ ((4 * (v & 1) + (lane >> 4)) & 7)));
+    urun = (uint32_t)(8 * p.S * 2);
+    ublk = (uint32_t)(KB * 2);
+  }
+  u0 = urun * (uint32_t)(8 * (w & 1));
+  auto load = [&](int qbi, lds_t *st) {
+    lds_t *const tile = st + tl * TILE + (w & 1) * 8 * 1024;
+    const uint32_t ub = ublk * (uint32_t)qbi + u0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) dma16(rs, tile + t * 1024, ub + urun * t + lbase + lcol[t & 3]);
+    if (w == NT / 64 - 1) {
       const uint32_t off = (uint32_t)((sbase + (int64_t)qbi * KB + lane) * 4);
-      dma4(rl, st + 3 * TILE, off);
-      dma4(rd, st + 3 * TILE + 256, off);
+      dma4(rl, st + 4 * TILE, off);
+      dma4(rd, st + 4 * TILE + 256, off);
     }
   };
   const int qfirst = kblk * KV_ROWS / KB, nqblk = p.S / KB;
@@ -545,55 +625,66 @@ __global__ __launch_bounds__(KV_WAVES * 64) void attn_bwd_dkdv_kernel(AttnP p) {
     const int cur_i = (qbi - qfirst) & 1;
     const lds_t *cur = L + cur_i * STAGE;
     if (qbi + 1 < nqblk) load(qbi + 1, L + (cur_i ^ 1) * STAGE);
-    const float *sL = reinterpret_cast<const float *>(smem + cur_i * STAGE + 3 * TILE);
-    const int q0 = qbi * KB;
-    if (active && q0 + KB - 1 >= k0w) {
-      f32x16_v s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
+    const float *sL = reinterpret_cast<const float *>(smem + cur_i * STAGE + 4 * TILE) + 32 * hq;
+    const int q0 = qbi * KB + 32 * hq;  // this wave's 32 queries
+    if (q0 + 31 >= k0w) {
+      f32x16_v s = zero16(), dp = zero16();
 #pragma unroll
-      for (int es = 0; es < 8; ++es)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), kf[es], s[j]);
-          dp[j] = mfma(frag_rows<bf16x8_v>(cur + 2 * TILE, j * 32, es, lane), vf[es], dp[j]);
-        }
+      for (int es = 0; es < 8; ++es) {
+        s = mfma(frag_rows<QV>(cur, 32 * hq, es, lane), kf[es], s);
+        dp = mfma(frag_rows<bf16x8_v>(cur + TILE, 32 * hq, es, lane), vf[es], dp);
+        // at most two k-steps of fragments in flight (registers are the limit)
+        if (es & 1) __builtin_amdgcn_sched_barrier(0);
+      }
       if (q0 < k0w + 31) {  // diagonal block (wave-uniform): P = 0 for queries before the key
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (q0 + j * 32 + out_row(r, hf) < myk) s[j][r] = -INFINITY;
+        for (int r = 0; r < 16; ++r)
+          if (q0 + out_row(r, hf) < myk) s[r] = -INFINITY;
       }
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int r = 0; r < 16; ++r) {
+        const int qi = out_row(r, hf);
+        const float pv = ex2(__builtin_fmaf(s[r], sc, -sL[qi] * LOG2E));
+        s[r] = pv;
+        dp[r] = pv * (dp[r] - sL[64 + qi]);
+      }
+      const lds_t *qt = cur + 2 * TILE, *dot = cur + 3 * TILE;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int qi = j * 32 + out_row(r, hf);
-          const float pv = ex2(__builtin_fmaf(s[j][r], sc, -sL[qi] * LOG2E));
-          s[j][r] = pv;
-          dp[j][r] = pv * (dp[j][r] - sL[64 + qi]);
+      for (int t = 0; t < 2; ++t) {
+        const bf16x8_v pf = pack8<__bf16>(s, 8 * t);
+        const bf16x8_v sf = pack8<__bf16>(dp, 8 * t);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          dv[i] = mfma(frag_t<bf16x8_v>(dot, i * 32, hq, t, lane), pf, dv[i]);
+          dk[i] = mfma(frag_t<bf16x8_v>(qt, i * 32, hq, t, lane), sf, dk[i]);
+          if (i & 1) __builtin_amdgcn_sched_barrier(0);
         }
-      const lds_t *qt = cur + TILE, *dot = cur + 2 * TILE;
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const bf16x8_v pf = pack8<__bf16>(s[j], 8 * t);
-          const bf16x8_v sf = pack8<__bf16>(dp[j], 8 * t);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            dv[i] = mfma(frag_cols<bf16x8_v>(dot, i * 32, j * 32 + 16 * t, lane), pf, dv[i]);
-            dk[i] = mfma(frag_cols<bf16x8_v>(qt, i * 32, j * 32 + 16 * t, lane), sf, dk[i]);
-          }
-        }
+      }
     }
     wait_vm0();
     __syncthreads();
   }
-  if (!active) return;
+  // waves 4-7 hand their partial sums to waves 0-3 (the stages are free now)
+  typedef __attribute__((address_space(3))) float lds_f;
+  lds_f *const red = reinterpret_cast<lds_f *>(L) + pw * (128 * 64) + lane;
+  if (hq == 1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        red[(i * 16 + r) * 64] = dk[i][r];
+        red[(64 + i * 16 + r) * 64] = dv[i][r];
+      }
+  }
+  __syncthreads();
+  if (hq == 1) return;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) dk[i][r] *= p.scale;
+    for (int r = 0; r < 16; ++r) {
+      dk[i][r] = (dk[i][r] + red[(i * 16 + r) * 64]) * p.scale;
+      dv[i][r] += red[(64 + i * 16 + r) * 64];
+    }
   if (p.rcos) rope_inverse_pairs(dk, p.rcos, p.rsin, myk, hf);
   store_row_t(p.dk + h * HD + (row0 + myk) * p.ld_d, dk, 1.0f, hf);
   store_row_t(p.dv + h * HD + (row0 + myk) * p.ld_d, dv, 1.0f, hf);
@@ -770,17 +861,26 @@ AttnP mc_params(const lc_attn_args &a) {
   p.dv = static_cast<__bf16 *>(a.dv);
   p.D = static_cast<float *>(a.scratch);
   const int64_t rows = (int64_t)a.B * a.S, d = (int64_t)a.H * HD;
+  // scratch: D (fp32 [B, H, S], 256-byte aligned), v rows (bf16), then the
+  // transposes of q, k, dO (bf16 [B][H][128][S] each)
   const size_t dbytes = ((size_t)rows * a.H * sizeof(float) + 255) / 256 * 256;
-  p.qkvb = a.scratch ? reinterpret_cast<__bf16 *>(static_cast<char *>(a.scratch) + dbytes) : nullptr;
+  __bf16 *const cp = a.scratch ? reinterpret_cast<__bf16 *>(static_cast<char *>(a.scratch) + dbytes) : nullptr;
+  const bool bf = a.dtype == LC_BF16;
+  p.vb_w = cp;
+  p.vb = bf ? static_cast<const __bf16 *>(a.v) : cp;
+  p.ld_vb = bf ? a.ld_qkv : d;
+  p.qt = cp ? cp + rows * d : nullptr;
+  p.kt = cp ? cp + 2 * rows * d : nullptr;
+  p.dot = cp ? cp + 3 * rows * d : nullptr;
   p.rcos = a.rope_cos;
   p.rsin = a.rope_sin;
   p.ld_qkv = a.ld_qkv;
   p.ld_o = a.ld_o;
   p.ld_d = a.ld_dqkv;
-  p.ld_b = 3 * d;
   p.qkv_bytes = (uint32_t)(((rows - 1) * a.ld_qkv + d) * 2);
   p.o_bytes = (uint32_t)(((rows - 1) * a.ld_o + d) * 2);
-  p.b_bytes = (uint32_t)(((rows - 1) * p.ld_b + d) * 2);
+  p.vb_bytes = (uint32_t)(((rows - 1) * p.ld_vb + d) * 2);
+  p.t_bytes = (uint32_t)(rows * d * 2);
   p.lse_bytes = (uint32_t)(rows * a.H * sizeof(float));
   p.S = a.S;
   p.H = a.H;
@@ -794,7 +894,7 @@ lc_status check_extents(const lc_attn_args &a) {
   const int64_t rows = (int64_t)a.B * a.S, d = (int64_t)a.H * HD;
   const int64_t lim = (int64_t)1 << 31;
   if (((rows - 1) * a.ld_qkv + d) * 2 >= lim || ((rows - 1) * a.ld_o + d) * 2 >= lim ||
-      ((rows - 1) * 3 * d + d) * 2 >= lim)
+      rows * d * 2 >= lim)
     return fail(LC_ERR_UNSUPPORTED, "attention: a q/k/v/o matrix spans 2 GiB or more");
   return LC_OK;
 }
@@ -833,12 +933,12 @@ template <typename QE>
 lc_status bwd_mc(const lc_attn_args &a, hipStream_t s) {
   LC_TRY(check_extents(a));
   const AttnP p = mc_params(a);
-  hipLaunchKernelGGL(attn_bwd_prep_kernel<QE>, dim3((unsigned)((int64_t)a.B * a.S)), dim3(256), 0,
-                     s, p, a.H * HD);
+  hipLaunchKernelGGL(attn_bwd_prep_kernel<QE>, dim3((unsigned)(a.S / 64), a.H, a.B), dim3(256), 0,
+                     s, p);
   LC_TRY(check_launch("attn_bwd_prep_kernel"));
   const unsigned nb = (unsigned)((a.S + ROWS - 1) / ROWS);
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<QE>, dim3((unsigned)((a.S + KV_ROWS - 1) / KV_ROWS), a.H, a.B),
-                     dim3(KV_WAVES * 64), 0, s, p);
+  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<QE>, dim3((unsigned)(a.S / KV_ROWS * a.H), a.B), dim3(NT), 0,
+                     s, p);
   LC_TRY(check_launch("attn_bwd_dkdv_kernel"));
   hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(nb, a.H, a.B), dim3(NT), 0, s, p);
   return check_launch("attn_bwd_dq_kernel");

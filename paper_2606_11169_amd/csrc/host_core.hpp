@@ -13,7 +13,7 @@ namespace lc {
 lc_status fail(lc_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 
 // Rows per block of the RMSNorm backward's gain-gradient partial sums.
-constexpr int kNormRowsPerBlock = 32;
+constexpr int kNormRowsPerBlock = 16;
 size_t rmsnorm_scratch_size(int64_t T, int64_t d);
 size_t attn_scratch_size(int64_t B, int64_t S, int64_t H);
 // Tokens per block of the MoE router weight gradient's partial sums.

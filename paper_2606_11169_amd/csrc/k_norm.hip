@@ -6,18 +6,23 @@
 //             dg_k += sum_t dn_tk xh_tk
 //
 // Row kernels: one wave per row, 8 elements per lane per step (16- or 32-byte
-// accesses); a row is read once for its reduction and again for the write
-// (the second read hits L2). Every tensor's element type is a run-time value
+// accesses). Rows of up to 4096 elements stay in registers between the
+// row's reduction and its write (one read); longer rows are read twice (the
+// second read hits L2). Every tensor's element type is a run-time value
 // (uniform branches). The gain gradient is a column reduction over rows:
-// blocks of kNormRowsPerBlock rows write fp32 partial sums, then one thread
-// per column adds the partials in block order into dg — the same order on
-// every run, no atomics.
+// each workgroup of the backward kernel handles kNormRowsPerBlock rows (wave
+// w: rows w, w + 4, ...) and writes the fp32 partial sums of its rows (each
+// wave's rows in order, then the waves in order), then the final kernel adds the partials of each column: sixteen
+// slices of consecutive blocks, each summed in block order, then the slices
+// in order — the same order on every run, no atomics.
 #include "common.hpp"
 
 namespace lc {
 namespace {
 
-constexpr int ROWS_PER_BLOCK = 4;  // one wave per row
+constexpr int ROWS_PER_BLOCK = 4;  // forward: one wave per row
+constexpr int MAXU = 8;            // 8-element chunks per lane held in registers
+constexpr int MAXD = 64 * 8 * MAXU;
 
 struct NormP {
   const void *x, *g, *dn, *dres;
@@ -37,6 +42,33 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(NormP p) {
   if (row >= p.rows) return;
   const int64_t base = row * p.d;
   float ss = 0.0f;
+  if (p.d <= MAXD) {
+    float v[MAXU][8];
+#pragma unroll
+    for (int u = 0; u < MAXU; ++u) {
+      const int c = lane * 8 + 512 * u;
+      if (c < p.d) {
+        load8_dt(p.x, base + c, p.x_dt, v[u]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += v[u][e] * v[u][e];
+      }
+    }
+    ss = wave_sum(ss);
+    const float r = 1.0f / sqrtf(ss / (float)p.d + p.eps);
+    if (lane == 0) p.rstd[row] = r;
+#pragma unroll
+    for (int u = 0; u < MAXU; ++u) {
+      const int c = lane * 8 + 512 * u;
+      if (c < p.d) {
+        float gv[8];
+        load8_dt(p.g, c, p.w_dt, gv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[u][e] = v[u][e] * r * gv[e];
+        store8_dt(p.n, base + c, p.out_dt, v[u]);
+      }
+    }
+    return;
+  }
   for (int c = lane * 8; c < p.d; c += 64 * 8) {
     float v[8];
     load8_dt(p.x, base + c, p.x_dt, v);
@@ -56,13 +88,57 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(NormP p) {
   }
 }
 
-__global__ __launch_bounds__(256) void rmsnorm_bwd_rows_kernel(NormP p) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * ROWS_PER_BLOCK + (threadIdx.x >> 6);
-  if (row >= p.rows) return;
+// dx for one row held by one wave (a: dn, b: x of the lane's chunks), and the
+// row's gain-gradient terms dn * x * rstd added into the lane's accumulators
+__device__ __forceinline__ void bwd_row_regs(const NormP &p, int64_t row, int lane,
+                                             float (&acc)[MAXU][8]) {
   const int64_t base = row * p.d;
   const float r = p.rstd[row];
+  float a[MAXU][8], b[MAXU][8];
   float dot = 0.0f;  // sum_k dn*g*x
+#pragma unroll
+  for (int u = 0; u < MAXU; ++u) {
+    const int c = lane * 8 + 512 * u;
+    if (c < p.d) {
+      float gv[8];
+      load8_dt(p.dn, base + c, p.dn_dt, a[u]);
+      load8_dt(p.x, base + c, p.x_dt, b[u]);
+      load8_dt(p.g, c, p.w_dt, gv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dot += a[u][e] * gv[e] * b[u][e];
+    }
+  }
+  dot = wave_sum(dot);
+  const float mean = dot * r / (float)p.d;  // mean_k(dxh * xh)
+  const float r2m = r * mean;
+#pragma unroll
+  for (int u = 0; u < MAXU; ++u) {
+    const int c = lane * 8 + 512 * u;
+    if (c < p.d) {
+      float gv[8], o[8];
+      load8_dt(p.g, c, p.w_dt, gv);
+      if (p.dres) {
+        load8_dt(p.dres, base + c, p.dres_dt, o);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = 0.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        o[e] += r * (a[u][e] * gv[e] - b[u][e] * r2m);
+        acc[u][e] += a[u][e] * (b[u][e] * r);
+      }
+      store8_dt(p.dx, base + c, p.out_dt, o);
+      if (p.dx_copy) store8_dt(p.dx_copy, base + c, LC_BF16, o);
+    }
+  }
+}
+
+// rows longer than MAXD: the row is read twice, the gain gradient is not formed here
+__device__ __forceinline__ void bwd_row_long(const NormP &p, int64_t row, int lane) {
+  const int64_t base = row * p.d;
+  const float r = p.rstd[row];
+  float dot = 0.0f;
   for (int c = lane * 8; c < p.d; c += 64 * 8) {
     float a[8], b[8], gv[8];
     load8_dt(p.dn, base + c, p.dn_dt, a);
@@ -72,7 +148,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_rows_kernel(NormP p) {
     for (int e = 0; e < 8; ++e) dot += a[e] * gv[e] * b[e];
   }
   dot = wave_sum(dot);
-  const float mean = dot * r / (float)p.d;  // mean_k(dxh * xh)
+  const float mean = dot * r / (float)p.d;
   const float r2m = r * mean;
   for (int c = lane * 8; c < p.d; c += 64 * 8) {
     float a[8], b[8], gv[8], o[8];
@@ -92,13 +168,49 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_rows_kernel(NormP p) {
   }
 }
 
+// One workgroup per kNormRowsPerBlock rows (wave w: rows w, w + 4, ...); for
+// d <= MAXD it also writes partial[blk][k] = sum over the block's rows of
+// dn * x * rstd (each wave's rows in order, then wave 0's sum, wave 1's, ...).
+__global__ __launch_bounds__(256) void rmsnorm_bwd_rows_kernel(NormP p) {
+  __shared__ float red[MAXD];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * kNormRowsPerBlock;
+  const int64_t r1 = min(p.rows, r0 + kNormRowsPerBlock);
+  if (p.d > MAXD) {
+    for (int64_t row = r0 + wv; row < r1; row += 4) bwd_row_long(p, row, lane);
+    return;
+  }
+  float acc[MAXU][8];
+#pragma unroll
+  for (int u = 0; u < MAXU; ++u)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
+  for (int64_t row = r0 + wv; row < r1; row += 4) bwd_row_regs(p, row, lane, acc);
+  if (!p.dg) return;  // uniform: no gain gradient requested
+#pragma unroll 1
+  for (int w = 0; w < 4; ++w) {
+    if (wv == w) {
+#pragma unroll
+      for (int u = 0; u < MAXU; ++u) {
+        const int c = lane * 8 + 512 * u;
+        if (c < p.d) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) red[c + e] = (w == 0 ? 0.0f : red[c + e]) + acc[u][e];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  for (int k = threadIdx.x; k < p.d; k += 256) p.partial[(int64_t)blockIdx.x * p.d + k] = red[k];
+}
+
 __device__ __forceinline__ float ld1_dt(const void *base, int64_t i, int dt) {
   if (dt == LC_FP32) return static_cast<const float *>(base)[i];
   if (dt == LC_BF16) return (float)static_cast<const __bf16 *>(base)[i];
   return (float)static_cast<const _Float16 *>(base)[i];
 }
 
-// partial[blk][k] = sum over rows of block blk of dn[t,k] * x[t,k] * rstd[t]
+// rows longer than MAXD: partial[blk][k] = sum over rows of block blk of dn[t,k] * x[t,k] * rstd[t]
 __global__ __launch_bounds__(256) void rmsnorm_dg_partial_kernel(NormP p) {
   const int k = blockIdx.x * 256 + threadIdx.x;
   if (k >= p.d) return;
@@ -110,12 +222,35 @@ __global__ __launch_bounds__(256) void rmsnorm_dg_partial_kernel(NormP p) {
   p.partial[(int64_t)blockIdx.y * p.d + k] = s;
 }
 
-__global__ __launch_bounds__(256) void rmsnorm_dg_final_kernel(NormP p) {
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  if (k >= p.d) return;
+// dg[k] += sum of partial[b][k] over blocks b: sixteen slices of consecutive
+// blocks (each summed in block order), then the slices in order
+constexpr int DG_SLICES = 16;
+__global__ __launch_bounds__(1024) void rmsnorm_dg_final_kernel(NormP p) {
+  __shared__ float sl[DG_SLICES][64];
+  const int t = threadIdx.x, sidx = t >> 6, kc = t & 63;
+  const int k = blockIdx.x * 64 + kc;
+  const int per = (p.nblk + DG_SLICES - 1) / DG_SLICES;
+  const int b0 = sidx * per, b1 = min(p.nblk, b0 + per);
   float s = 0.0f;
-  for (int b = 0; b < p.nblk; ++b) s += p.partial[(int64_t)b * p.d + k];
-  p.dg[k] = p.dg[k] + s;
+  if (k < p.d) {
+    int b = b0;
+    for (; b + 8 <= b1; b += 8) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = p.partial[(int64_t)(b + i) * p.d + k];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += v[i];
+    }
+    for (; b < b1; ++b) s += p.partial[(int64_t)b * p.d + k];
+  }
+  sl[sidx][kc] = s;
+  __syncthreads();
+  if (sidx == 0 && k < p.d) {
+    float tot = sl[0][kc];
+#pragma unroll
+    for (int i = 1; i < DG_SLICES; ++i) tot += sl[i][kc];
+    p.dg[k] = p.dg[k] + tot;
+  }
 }
 
 lc_status check_common(const lc_norm_args &a, bool bwd) {
@@ -177,14 +312,15 @@ lc_status rmsnorm_fwd_launch(const lc_norm_args &a, hipStream_t s) {
 lc_status rmsnorm_bwd_launch(const lc_norm_args &a, hipStream_t s) {
   LC_TRY(check_common(a, true));
   const NormP p = make_params(a);
-  hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel,
-                     dim3((unsigned)((a.T + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK)), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel, dim3((unsigned)p.nblk), dim3(256), 0, s, p);
   LC_TRY(check_launch("rmsnorm_bwd_rows_kernel"));
   if (!a.dg_accum) return LC_OK;
-  hipLaunchKernelGGL(rmsnorm_dg_partial_kernel, dim3((unsigned)((a.d + 255) / 256), (unsigned)p.nblk),
-                     dim3(256), 0, s, p);
-  LC_TRY(check_launch("rmsnorm_dg_partial_kernel"));
-  hipLaunchKernelGGL(rmsnorm_dg_final_kernel, dim3((unsigned)((a.d + 255) / 256)), dim3(256), 0, s, p);
+  if (a.d > MAXD) {
+    hipLaunchKernelGGL(rmsnorm_dg_partial_kernel, dim3((unsigned)((a.d + 255) / 256), (unsigned)p.nblk),
+                       dim3(256), 0, s, p);
+    LC_TRY(check_launch("rmsnorm_dg_partial_kernel"));
+  }
+  hipLaunchKernelGGL(rmsnorm_dg_final_kernel, dim3((unsigned)((a.d + 63) / 64)), dim3(1024), 0, s, p);
   return check_launch("rmsnorm_dg_final_kernel");
 }
 

@@ -44,6 +44,8 @@
 // branches in the epilogue only).
 #include "common.hpp"
 
+#include <type_traits>
+
 namespace lc {
 namespace {
 
@@ -209,6 +211,41 @@ __device__ __forceinline__ bf16x8_v frag(const lds_t *t, int row0, int s, int la
   }
 }
 
+// Four consecutive elements of type T at base[idx] as floats (epilogue loads)
+template <typename T>
+__device__ __forceinline__ float4 ld4(const void *base, int64_t idx) {
+  if constexpr (std::is_same<T, float>::value) {
+    return *reinterpret_cast<const float4 *>(static_cast<const float *>(base) + idx);
+  } else {
+    typedef __attribute__((ext_vector_type(4))) T t4;
+    const t4 v = *reinterpret_cast<const t4 *>(static_cast<const T *>(base) + idx);
+    return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+  }
+}
+
+// The epilogue's loads of one 32-row block: NJ column blocks j0 .. j0+NJ-1 of
+// 4 x 4 columns each, at row m of `base` (ld elements per row); columns past
+// the last one read the last four columns instead (never used), so the loads
+// carry no per-lane condition and issue back to back.
+template <typename T, int NJ>
+__device__ __forceinline__ void ld_block(float4 (&dst)[NJ][4], const void *base, int64_t ld, int m,
+                                         int nb, int N) {
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int n = nb + j * 32 + 8 * g;
+      dst[j][g] = ld4<T>(base, (int64_t)m * ld + (n < N ? n : N - 4));
+    }
+}
+template <int NJ>
+__device__ __forceinline__ void ld_block_dt(float4 (&dst)[NJ][4], const void *base, int64_t ld, int m,
+                                            int nb, int N, int dt) {
+  if (dt == LC_FP32) ld_block<float, NJ>(dst, base, ld, m, nb, N);
+  else if (dt == LC_BF16) ld_block<__bf16, NJ>(dst, base, ld, m, nb, N);
+  else ld_block<_Float16, NJ>(dst, base, ld, m, nb, N);
+}
+
 // Scheduling pattern for one k-step: the NRD LDS reads of the next k-step
 // spread over the NMF MFMAs of this one (reads first, as evenly as possible).
 template <int NRD, int NMF, int I = 0>
@@ -354,6 +391,10 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   const int frow = lane & 31;
   const int fhalf = lane >> 5;
   // ------------------------------------------------------------ epilogue
+  // Every epilogue that reads memory first issues all loads of a 32-row block
+  // (or half of it), then computes and stores: loads and stores of different
+  // pointers cannot be reordered by the compiler, so a load-compute-store
+  // chain per element would wait out one memory round trip per element.
   const int h4 = 4 * fhalf;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
@@ -384,11 +425,22 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
       if (hbase >= p.N) continue;
       const bool rot = hbase < p.rope_cols;
       const int pos = m % p.rope_seq;
+      float4 cs[2][4], sn[2][4];
+      if (rot) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int c = j * 32 + 8 * g + h4;  // column inside the head, < 64
+            cs[j][g] = *reinterpret_cast<const float4 *>(p.rcos + (int64_t)pos * 64 + c);
+            sn[j][g] = *reinterpret_cast<const float4 *>(p.rsin + (int64_t)pos * 64 + c);
+          }
+      }
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int c = j * 32 + 8 * g + h4;  // column inside the head, < 64
+          const int c = j * 32 + 8 * g + h4;
           float x1[4], x2[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -396,10 +448,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
             x2[e] = acc[i][j + 2][4 * g + e];
           }
           if (rot) {
-            const float4 cs = *reinterpret_cast<const float4 *>(p.rcos + (int64_t)pos * 64 + c);
-            const float4 sn = *reinterpret_cast<const float4 *>(p.rsin + (int64_t)pos * 64 + c);
-            const float cv[4] = {cs.x, cs.y, cs.z, cs.w};
-            const float sv[4] = {sn.x, sn.y, sn.z, sn.w};
+            const float cv[4] = {cs[j][g].x, cs[j][g].y, cs[j][g].z, cs[j][g].w};
+            const float sv[4] = {sn[j][g].x, sn[j][g].y, sn[j][g].z, sn[j][g].w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float a = x1[e], b = x2[e];
@@ -412,7 +462,41 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
           store4_dt(Cp, row + c + 64, p.c_dt, x2[0], x2[1], x2[2], x2[3]);
         }
       }
+    } else if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
+#pragma unroll
+      for (int jp = 0; jp < 2; ++jp) {  // blocks j = 2 jp, 2 jp + 1
+        float4 gt[2][4], up[2][4];
+        const int nb = n0 + wn * WN + 2 * jp * 32 + h4;
+        ld_block_dt<2>(gt, p.aux0, p.ld_aux, m, nb, p.N, p.aux_dt);
+        ld_block_dt<2>(up, p.aux1, p.ld_aux, m, nb, p.N, p.aux_dt);
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int j = 2 * jp + jj;
+            const int n = n0 + wn * WN + j * 32 + 8 * g + h4;
+            if (n >= p.N) continue;
+            const float gv[4] = {gt[jj][g].x, gt[jj][g].y, gt[jj][g].z, gt[jj][g].w};
+            const float uv[4] = {up[jj][g].x, up[jj][g].y, up[jj][g].z, up[jj][g].w};
+            float dg[4], du[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float dv = acc[i][j][4 * g + e];
+              const float sg = sigmoidf_(gv[e]);
+              dg[e] = dv * uv[e] * sg * (1.0f + gv[e] * (1.0f - sg));
+              du[e] = dv * gv[e] * sg;
+            }
+            const int64_t oc = (int64_t)m * p.ldc + n;
+            store4_dt(Cp, oc, p.c_dt, dg[0], dg[1], dg[2], dg[3]);
+            store4_dt(Cp, oc + p.N, p.c_dt, du[0], du[1], du[2], du[3]);
+          }
+      }
     } else {
+      // STORE, RESIDUAL (C = R + acc), ACCUM_F32 (C += acc)
+      float4 src[FN][4];
+      const int nb = n0 + wn * WN + h4;
+      if constexpr (EPI == LC_EPI_RESIDUAL) ld_block_dt<FN>(src, p.R, p.ldr, m, nb, p.N, p.r_dt);
+      if constexpr (EPI == LC_EPI_ACCUM_F32) ld_block<float, FN>(src, Cp, p.ldc, m, nb, p.N);
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
 #pragma unroll
@@ -421,37 +505,17 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
           if (n >= p.N) continue;
           float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
           float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-          const int64_t oc = (int64_t)m * p.ldc + n;
-          if constexpr (EPI == LC_EPI_STORE) {
-            store4_dt(Cp, oc, p.c_dt, v0, v1, v2, v3);
-          } else if constexpr (EPI == LC_EPI_RESIDUAL) {
-            const float4 r = load4_dt(p.R, (int64_t)m * p.ldr + n, p.r_dt);
-            store4_dt(Cp, oc, p.c_dt, r.x + v0, r.y + v1, r.z + v2, r.w + v3);
-          } else if constexpr (EPI == LC_EPI_ACCUM_F32) {
-            float4 *cp = reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc);
-            float4 c = *cp;
-            c.x += v0;
-            c.y += v1;
-            c.z += v2;
-            c.w += v3;
-            *cp = c;
-          } else if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
-            const int64_t oa = (int64_t)m * p.ld_aux + n;
-            const float4 gt = load4_dt(p.aux0, oa, p.aux_dt);
-            const float4 up = load4_dt(p.aux1, oa, p.aux_dt);
-            const float gv[4] = {gt.x, gt.y, gt.z, gt.w};
-            const float uv[4] = {up.x, up.y, up.z, up.w};
-            const float dv[4] = {v0, v1, v2, v3};
-            float dg[4], du[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float s = sigmoidf_(gv[e]);
-              dg[e] = dv[e] * uv[e] * s * (1.0f + gv[e] * (1.0f - s));
-              du[e] = dv[e] * gv[e] * s;
-            }
-            store4_dt(Cp, oc, p.c_dt, dg[0], dg[1], dg[2], dg[3]);
-            store4_dt(Cp, oc + p.N, p.c_dt, du[0], du[1], du[2], du[3]);
+          if constexpr (EPI == LC_EPI_RESIDUAL || EPI == LC_EPI_ACCUM_F32) {
+            v0 = src[j][g].x + v0;
+            v1 = src[j][g].y + v1;
+            v2 = src[j][g].z + v2;
+            v3 = src[j][g].w + v3;
           }
+          const int64_t oc = (int64_t)m * p.ldc + n;
+          if constexpr (EPI == LC_EPI_ACCUM_F32)
+            *reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc) = make_float4(v0, v1, v2, v3);
+          else
+            store4_dt(Cp, oc, p.c_dt, v0, v1, v2, v3);
         }
       }
     }

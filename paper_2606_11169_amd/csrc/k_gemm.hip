@@ -211,41 +211,6 @@ __device__ __forceinline__ bf16x8_v frag(const lds_t *t, int row0, int s, int la
   }
 }
 
-// Four consecutive elements of type T at base[idx] as floats (epilogue loads)
-template <typename T>
-__device__ __forceinline__ float4 ld4(const void *base, int64_t idx) {
-  if constexpr (std::is_same<T, float>::value) {
-    return *reinterpret_cast<const float4 *>(static_cast<const float *>(base) + idx);
-  } else {
-    typedef __attribute__((ext_vector_type(4))) T t4;
-    const t4 v = *reinterpret_cast<const t4 *>(static_cast<const T *>(base) + idx);
-    return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
-  }
-}
-
-// The epilogue's loads of one 32-row block: NJ column blocks j0 .. j0+NJ-1 of
-// 4 x 4 columns each, at row m of `base` (ld elements per row); columns past
-// the last one read the last four columns instead (never used), so the loads
-// carry no per-lane condition and issue back to back.
-template <typename T, int NJ>
-__device__ __forceinline__ void ld_block(float4 (&dst)[NJ][4], const void *base, int64_t ld, int m,
-                                         int nb, int N) {
-#pragma unroll
-  for (int j = 0; j < NJ; ++j)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int n = nb + j * 32 + 8 * g;
-      dst[j][g] = ld4<T>(base, (int64_t)m * ld + (n < N ? n : N - 4));
-    }
-}
-template <int NJ>
-__device__ __forceinline__ void ld_block_dt(float4 (&dst)[NJ][4], const void *base, int64_t ld, int m,
-                                            int nb, int N, int dt) {
-  if (dt == LC_FP32) ld_block<float, NJ>(dst, base, ld, m, nb, N);
-  else if (dt == LC_BF16) ld_block<__bf16, NJ>(dst, base, ld, m, nb, N);
-  else ld_block<_Float16, NJ>(dst, base, ld, m, nb, N);
-}
-
 // Scheduling pattern for one k-step: the NRD LDS reads of the next k-step
 // spread over the NMF MFMAs of this one (reads first, as evenly as possible).
 template <int NRD, int NMF, int I = 0>
@@ -388,134 +353,136 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
     interleave();
   }
 
-  const int frow = lane & 31;
-  const int fhalf = lane >> 5;
   // ------------------------------------------------------------ epilogue
-  // Every epilogue that reads memory first issues all loads of a 32-row block
-  // (or half of it), then computes and stores: loads and stores of different
-  // pointers cannot be reordered by the compiler, so a load-compute-store
-  // chain per element would wait out one memory round trip per element.
-  const int h4 = 4 * fhalf;
+  // Each wave stages its 64 x 128 fp32 results through its own 16 KiB of the
+  // (now idle) LDS ring, one 32-row block at a time: written in the MFMA
+  // layout (lane = row, registers = columns), read back row-contiguous (16-byte
+  // chunk c of row r at chunk c ^ (r & 15): both directions conflict-free), so
+  // that every global access of the epilogue covers whole cache lines (two
+  // rows of 128 columns, or four rows of two 64-column halves, per
+  // instruction). Loads of a group of rows are issued before its stores.
+  __syncthreads();  // every wave's last fragment reads are done
+  const int frow = lane & 31, fhalf = lane >> 5;
+  lds_t *const E = R0 + wave * 16384;
+  typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+  typedef __attribute__((address_space(3))) f32x4_t lds_f4;
+  const int ncol0 = n0 + wn * WN;  // first of the wave's 128 accumulator columns (non-SwiGLU)
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
-    const int m = m0 + wm * WM + i * 32 + frow;
-    if (m >= m_lim) continue;
-    if constexpr (EPI == LC_EPI_SWIGLU) {
+    const int mrow0 = m0 + wm * WM + i * 32;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int n = n0 + wn * 64 + j * 32 + 8 * g + h4;
-          if (n >= p.N) continue;
-          float gt[4], up[4], a[4];
+      for (int g = 0; g < 4; ++g) {
+        const int c = 8 * j + 2 * g + fhalf;
+        const f32x4_t w = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+        *reinterpret_cast<lds_f4 *>(E + frow * 512 + ((c ^ (frow & 15)) << 4)) = w;
+      }
+    auto chunk = [&](int r, int c) -> float4 {
+      const f32x4_t v = *reinterpret_cast<const lds_f4 *>(E + r * 512 + ((c ^ (r & 15)) << 4));
+      return make_float4(v[0], v[1], v[2], v[3]);
+    };
+    if constexpr (EPI == LC_EPI_ROPE || EPI == LC_EPI_SWIGLU) {
+      // lane: row 4 s + lane / 16, column quads q and q + 16 (columns 4q and 64 + 4q)
+      const int q = lane & 15;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            gt[e] = acc[i][j][4 * g + e];
-            up[e] = acc[i][j + 2][4 * g + e];
-            a[e] = gt[e] * sigmoidf_(gt[e]) * up[e];
+      for (int s0 = 0; s0 < 8; s0 += 4) {
+        float4 x1[4], x2[4], cs[4], sn[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int rl = 4 * (s0 + u) + (lane >> 4);
+          x1[u] = chunk(rl, q);
+          x2[u] = chunk(rl, q + 16);
+          if constexpr (EPI == LC_EPI_ROPE) {
+            const int m = min(mrow0 + rl, m_lim - 1);
+            const int pos = m % p.rope_seq;
+            cs[u] = *reinterpret_cast<const float4 *>(p.rcos + (int64_t)pos * 64 + 4 * q);
+            sn[u] = *reinterpret_cast<const float4 *>(p.rsin + (int64_t)pos * 64 + 4 * q);
           }
-          const int64_t oa = (int64_t)m * p.ld_aux + n;
-          store4_dt(p.aux0, oa, p.aux_dt, gt[0], gt[1], gt[2], gt[3]);
-          store4_dt(p.aux1, oa, p.aux_dt, up[0], up[1], up[2], up[3]);
-          store4_dt(Cp, (int64_t)m * p.ldc + n, p.c_dt, a[0], a[1], a[2], a[3]);
         }
-      }
-    } else if constexpr (EPI == LC_EPI_ROPE) {
-      const int hbase = n0 + wn * WN;  // first column of this wave's head (head_dim 128)
-      if (hbase >= p.N) continue;
-      const bool rot = hbase < p.rope_cols;
-      const int pos = m % p.rope_seq;
-      float4 cs[2][4], sn[2][4];
-      if (rot) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int u = 0; u < 4; ++u) {
+          const int rl = 4 * (s0 + u) + (lane >> 4);
+          const int m = mrow0 + rl;
+          if (m >= m_lim) continue;
+          float a[4] = {x1[u].x, x1[u].y, x1[u].z, x1[u].w};
+          float b[4] = {x2[u].x, x2[u].y, x2[u].z, x2[u].w};
+          if constexpr (EPI == LC_EPI_ROPE) {
+            if (ncol0 >= p.N) continue;  // head past the output (uniform)
+            if (ncol0 < p.rope_cols) {
+              const float cv[4] = {cs[u].x, cs[u].y, cs[u].z, cs[u].w};
+              const float sv[4] = {sn[u].x, sn[u].y, sn[u].z, sn[u].w};
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int c = j * 32 + 8 * g + h4;  // column inside the head, < 64
-            cs[j][g] = *reinterpret_cast<const float4 *>(p.rcos + (int64_t)pos * 64 + c);
-            sn[j][g] = *reinterpret_cast<const float4 *>(p.rsin + (int64_t)pos * 64 + c);
-          }
-      }
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c = j * 32 + 8 * g + h4;
-          float x1[4], x2[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            x1[e] = acc[i][j][4 * g + e];
-            x2[e] = acc[i][j + 2][4 * g + e];
-          }
-          if (rot) {
-            const float cv[4] = {cs[j][g].x, cs[j][g].y, cs[j][g].z, cs[j][g].w};
-            const float sv[4] = {sn[j][g].x, sn[j][g].y, sn[j][g].z, sn[j][g].w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float a = x1[e], b = x2[e];
-              x1[e] = a * cv[e] - b * sv[e];
-              x2[e] = a * sv[e] + b * cv[e];
+              for (int e = 0; e < 4; ++e) {
+                const float x = a[e], y = b[e];
+                a[e] = x * cv[e] - y * sv[e];
+                b[e] = x * sv[e] + y * cv[e];
+              }
             }
+            const int64_t row = (int64_t)m * p.ldc + ncol0 + 4 * q;
+            store4_dt(Cp, row, p.c_dt, a[0], a[1], a[2], a[3]);
+            store4_dt(Cp, row + 64, p.c_dt, b[0], b[1], b[2], b[3]);
+          } else {
+            const int n = n0 + wn * 64 + 4 * q;  // output column of the gate/up pair
+            if (n >= p.N) continue;
+            float act[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) act[e] = a[e] * sigmoidf_(a[e]) * b[e];
+            const int64_t oa = (int64_t)m * p.ld_aux + n;
+            store4_dt(p.aux0, oa, p.aux_dt, a[0], a[1], a[2], a[3]);
+            store4_dt(p.aux1, oa, p.aux_dt, b[0], b[1], b[2], b[3]);
+            store4_dt(Cp, (int64_t)m * p.ldc + n, p.c_dt, act[0], act[1], act[2], act[3]);
           }
-          const int64_t row = (int64_t)m * p.ldc + hbase;
-          store4_dt(Cp, row + c, p.c_dt, x1[0], x1[1], x1[2], x1[3]);
-          store4_dt(Cp, row + c + 64, p.c_dt, x2[0], x2[1], x2[2], x2[3]);
         }
       }
-    } else if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
+    } else {
+      // lane: row 2 s + lane / 32, column quad lane % 32
+      const int q = lane & 31;
+      const int n = ncol0 + 4 * q;
+      const int ncl = n < p.N ? n : p.N - 4;  // loads of columns past N read valid data (unused)
 #pragma unroll
-      for (int jp = 0; jp < 2; ++jp) {  // blocks j = 2 jp, 2 jp + 1
-        float4 gt[2][4], up[2][4];
-        const int nb = n0 + wn * WN + 2 * jp * 32 + h4;
-        ld_block_dt<2>(gt, p.aux0, p.ld_aux, m, nb, p.N, p.aux_dt);
-        ld_block_dt<2>(up, p.aux1, p.ld_aux, m, nb, p.N, p.aux_dt);
+      for (int s0 = 0; s0 < 16; s0 += 8) {
+        float4 v[8], x[8], y[8];
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj)
+        for (int u = 0; u < 8; ++u) {
+          const int rl = 2 * (s0 + u) + (lane >> 5);
+          const int mc = min(mrow0 + rl, m_lim - 1);
+          v[u] = chunk(rl, q);
+          if constexpr (EPI == LC_EPI_RESIDUAL) x[u] = load4_dt(p.R, (int64_t)mc * p.ldr + ncl, p.r_dt);
+          if constexpr (EPI == LC_EPI_ACCUM_F32)
+            x[u] = *reinterpret_cast<const float4 *>(static_cast<const float *>(Cp) + (int64_t)mc * p.ldc + ncl);
+          if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
+            x[u] = load4_dt(p.aux0, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
+            y[u] = load4_dt(p.aux1, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
+          }
+        }
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int j = 2 * jp + jj;
-            const int n = n0 + wn * WN + j * 32 + 8 * g + h4;
-            if (n >= p.N) continue;
-            const float gv[4] = {gt[jj][g].x, gt[jj][g].y, gt[jj][g].z, gt[jj][g].w};
-            const float uv[4] = {up[jj][g].x, up[jj][g].y, up[jj][g].z, up[jj][g].w};
+        for (int u = 0; u < 8; ++u) {
+          const int rl = 2 * (s0 + u) + (lane >> 5);
+          const int m = mrow0 + rl;
+          if (m >= m_lim || n >= p.N) continue;
+          const int64_t oc = (int64_t)m * p.ldc + n;
+          float o[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+          if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
+            const float gv[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+            const float uv[4] = {y[u].x, y[u].y, y[u].z, y[u].w};
             float dg[4], du[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const float dv = acc[i][j][4 * g + e];
               const float sg = sigmoidf_(gv[e]);
-              dg[e] = dv * uv[e] * sg * (1.0f + gv[e] * (1.0f - sg));
-              du[e] = dv * gv[e] * sg;
+              dg[e] = o[e] * uv[e] * sg * (1.0f + gv[e] * (1.0f - sg));
+              du[e] = o[e] * gv[e] * sg;
             }
-            const int64_t oc = (int64_t)m * p.ldc + n;
             store4_dt(Cp, oc, p.c_dt, dg[0], dg[1], dg[2], dg[3]);
             store4_dt(Cp, oc + p.N, p.c_dt, du[0], du[1], du[2], du[3]);
+          } else if constexpr (EPI == LC_EPI_ACCUM_F32) {
+            *reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc) =
+                make_float4(x[u].x + o[0], x[u].y + o[1], x[u].z + o[2], x[u].w + o[3]);
+          } else if constexpr (EPI == LC_EPI_RESIDUAL) {
+            store4_dt(Cp, oc, p.c_dt, x[u].x + o[0], x[u].y + o[1], x[u].z + o[2], x[u].w + o[3]);
+          } else {
+            store4_dt(Cp, oc, p.c_dt, o[0], o[1], o[2], o[3]);
           }
-      }
-    } else {
-      // STORE, RESIDUAL (C = R + acc), ACCUM_F32 (C += acc)
-      float4 src[FN][4];
-      const int nb = n0 + wn * WN + h4;
-      if constexpr (EPI == LC_EPI_RESIDUAL) ld_block_dt<FN>(src, p.R, p.ldr, m, nb, p.N, p.r_dt);
-      if constexpr (EPI == LC_EPI_ACCUM_F32) ld_block<float, FN>(src, Cp, p.ldc, m, nb, p.N);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int n = n0 + wn * WN + j * 32 + 8 * g + h4;
-          if (n >= p.N) continue;
-          float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
-          float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-          if constexpr (EPI == LC_EPI_RESIDUAL || EPI == LC_EPI_ACCUM_F32) {
-            v0 = src[j][g].x + v0;
-            v1 = src[j][g].y + v1;
-            v2 = src[j][g].z + v2;
-            v3 = src[j][g].w + v3;
-          }
-          const int64_t oc = (int64_t)m * p.ldc + n;
-          if constexpr (EPI == LC_EPI_ACCUM_F32)
-            *reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc) = make_float4(v0, v1, v2, v3);
-          else
-            store4_dt(Cp, oc, p.c_dt, v0, v1, v2, v3);
         }
       }
     }

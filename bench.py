@@ -59,16 +59,24 @@ def desc_of(cfg, lc):
                         rope_base=cfg.rope_base)
 
 
-def time_stage(torch, lc, cfg, stream, steps, warmup, tag):
+def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None):
     """Time steps of (zero G, the Order, AdamW over the bucket) on `cfg`;
-    returns (ms per step, TFLOP/s, outputs finite)."""
+    returns (ms per step, TFLOP/s, outputs finite). With w_delay set the
+    Order is 1F1B with split backwards (Bi, then Bw w_delay backwards later)."""
     from paper_2606_11169_amd.runner import random_stage
     M = cfg.num_microbatches
-    order = lc.lc_order_1f1b(M, cfg.pp_size, cfg.pp_rank)
-    _, peak = lc.lc_order_validate(order, M, M)
-    log(f"[bench] {cfg.name}: {M} microbatches, 1F1B(P={cfg.pp_size}, s={cfg.pp_rank}), "
-        f"{peak} in flight")
-    r = random_stage(desc_of(cfg, lc), peak, seed=0, stream=stream)
+    if w_delay is None:
+        order = lc.lc_order_1f1b(M, cfg.pp_size, cfg.pp_rank)
+        wp = 0
+    else:
+        order = lc.lc_order_1f1b_split(M, cfg.pp_size, cfg.pp_rank, w_delay)
+        wp = min(w_delay + 1, M)
+    st, peak, peak_w = lc.lc_order_validate_split(order, M, M, M)
+    assert st == lc.LC_OK
+    log(f"[bench] {cfg.name}: {M} microbatches, 1F1B(P={cfg.pp_size}, s={cfg.pp_rank})"
+        f"{'' if w_delay is None else f' split, w_delay {w_delay}'}, {peak} in flight, "
+        f"{peak_w} weight passes pending")
+    r = random_stage(desc_of(cfg, lc), peak, seed=0, stream=stream, max_w_pending=wp)
     r.alloc_random_microbatches(M, seed=1)
     log(f"[bench] params {r.n_params}, workspace {r.ws_bytes / 2**30:.1f} GiB")
 
@@ -267,6 +275,9 @@ def main():
                     help="only the MoE stage timing (kernel profiles of that workload)")
     ap.add_argument("--roofline-only", action="store_true",
                     help="only the roofline kernel replay and the calibration copy (PMC runs)")
+    ap.add_argument("--split-only", type=int, default=None, metavar="W_DELAY",
+                    help="only the 7B-shaped stage with split backwards (Bw W_DELAY "
+                         "backwards after its Bi)")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -289,6 +300,14 @@ def main():
         mms, mtf, _ = time_stage(torch, lc, mcfg, stream, args.steps, args.warmup, "moe")
         print(json.dumps({"moe_stage": {"workload": mcfg.name, "value": round(mtf, 2),
                                         "unit": "TFLOP/s", "ms_per_step": round(mms, 2)}}))
+        return
+    if args.split_only is not None:
+        sms, stf, sfin = time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "split",
+                                    w_delay=args.split_only)
+        print(json.dumps({"split_stage": {"workload": cfg.name, "w_delay": args.split_only,
+                                          "value": round(stf, 2), "unit": "TFLOP/s",
+                                          "ms_per_step": round(sms, 2),
+                                          "outputs_finite": sfin}}))
         return
     if args.roofline_only:
         calibration_copy(torch, lc, stream)

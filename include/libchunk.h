@@ -58,8 +58,11 @@ typedef enum lc_status {
  * its attention q, k, v in fp16, see lc_stage_desc). */
 typedef enum lc_dtype { LC_FP32 = 0, LC_BF16 = 1, LC_FP16 = 2 } lc_dtype;
 
-/* Piper's PASS dimension: F = forward, B = full backward (Section 4.1). */
-typedef enum lc_pass { LC_PASS_F = 0, LC_PASS_B = 1 } lc_pass;
+/* Piper's PASS dimension (Section 4.1): F = forward, B = full backward,
+ * BI = backward for the inputs (dX only), BW = backward for the weights (the
+ * parameter gradient only). BI and BW split B for schedules that defer the
+ * weight-gradient work into pipeline bubbles (ZeroBubble). */
+typedef enum lc_pass { LC_PASS_F = 0, LC_PASS_B = 1, LC_PASS_BI = 2, LC_PASS_BW = 3 } lc_pass;
 
 /* One pipeline stage: n_layers pre-norm decoder layers. Every layer is
  *   n1 = RMSNorm(x; g1); q,k,v = n1 Wq^T, n1 Wk^T, n1 Wv^T; rotate-half RoPE
@@ -117,14 +120,18 @@ typedef struct lc_order_entry {
 
 /* An Order over num_microbatches microbatches (Piper Section 4.1, Order).
  * Rules (checked by lc_order_validate and again by lc_run_order):
- *   - each (mb, F) and (mb, B) with 0 <= mb < num_microbatches appears
- *     exactly once, and F(mb) precedes B(mb);
- *   - the F entries and the B entries are each in increasing mb order:
- *     a pipeline stage must consume microbatches in the order its
- *     neighbour produced them, and Piper rejects schedules that do not
- *     (Section 4.3.2, "Communication management");
+ *   - for each 0 <= mb < num_microbatches, (mb, F) appears exactly once,
+ *     and so does either (mb, B) or the pair (mb, BI), (mb, BW); F(mb)
+ *     precedes B(mb) or BI(mb), and BI(mb) precedes BW(mb);
+ *   - the F entries are in increasing mb order, and so are the B and BI
+ *     entries taken together (both hand dX to the upstream stage): a
+ *     pipeline stage must consume microbatches in the order its neighbour
+ *     produced them, and Piper rejects schedules that do not (Section
+ *     4.3.2, "Communication management"). BW entries only add into the
+ *     local gradient accumulator and may come in any order;
  *   - at most max_in_flight microbatches sit between their F and their B
- *     (else LC_ERR_STASH_FULL). */
+ *     or BW, and at most max_w_pending between their BI and BW (else
+ *     LC_ERR_STASH_FULL). */
 typedef struct lc_order {
   int32_t num_microbatches;
   int32_t n_entries;
@@ -132,10 +139,11 @@ typedef struct lc_order {
 } lc_order;
 
 /* One microbatch's activations, all device pointers, [micro_batch, seq_len,
- * d_model] in compute_dtype. `x` is read by F and again by B: it must stay
- * valid and unchanged until B of this microbatch has been enqueued and has
- * run. F writes `y`; B reads `dy` and writes `dx`. Unused fields may be NULL
- * (F needs x and y; B needs x, dy and dx). */
+ * d_model] in compute_dtype. `x` is read by F and again by B (or BI): it
+ * must stay valid and unchanged until B (or BI) of this microbatch has been
+ * enqueued and has run. F writes `y`; B and BI read `dy` and write `dx`; BW
+ * reads none of them. Unused fields may be NULL (F needs x and y; B and BI
+ * need dy and dx). */
 typedef struct lc_microbatch_desc {
   int32_t mb;
   int32_t reserved;
@@ -186,13 +194,37 @@ lc_status lc_param_offset(const lc_stage_desc *desc, int32_t layer, int32_t tens
 lc_status lc_order_1f1b(int32_t M, int32_t P, int32_t s, lc_order_entry *out,
                         int32_t capacity, int32_t *n);
 
+/* The 1F1B Order above with every B split into BI then BW: BW(j) is placed
+ * right after BI(j + w_delay) (after the last BI when there is none), and
+ * the BW entries keep microbatch order. w_delay = 0 gives BI(j) BW(j)
+ * pairs; larger values defer weight passes, up to min(w_delay + 1, M) of
+ * them pending at once. `out` holds `capacity` entries (needs 3M). */
+lc_status lc_order_1f1b_split(int32_t M, int32_t P, int32_t s, int32_t w_delay,
+                              lc_order_entry *out, int32_t capacity, int32_t *n);
+
 /* Checks an Order against the rules above for at most max_in_flight
- * stashed microbatches. *peak (nullable) receives the largest number in
- * flight. Returns LC_OK, LC_ERR_BAD_ORDER or LC_ERR_STASH_FULL. */
+ * stashed microbatches and max_w_pending pending weight passes. *peak and
+ * *peak_w (nullable) receive the largest numbers of each seen. Returns
+ * LC_OK, LC_ERR_BAD_ORDER or LC_ERR_STASH_FULL. */
+lc_status lc_order_validate_split(const lc_order *order, int32_t max_in_flight,
+                                  int32_t max_w_pending, int32_t *peak, int32_t *peak_w);
+
+/* lc_order_validate_split with max_w_pending = max_in_flight (a microbatch
+ * whose weight pass is pending still holds its stash slot, so this is no
+ * extra bound). */
 lc_status lc_order_validate(const lc_order *order, int32_t max_in_flight, int32_t *peak);
 
-/* Device workspace a stage needs for max_in_flight stashed microbatches
- * (activation stash + backward scratch + RoPE table). */
+/* Device workspace a stage needs for max_in_flight stashed microbatches and
+ * max_w_pending weight-pass slots (0 <= max_w_pending <= max_in_flight; > 0
+ * only for dense stages): activation stash, weight-pass slots, backward
+ * scratch and RoPE table. A weight-pass slot holds, per layer, the gradient
+ * operands of the weight products ([T, d], [T, 2 d_ff], [T, d], [T, 3d] in
+ * the compute dtype, T = micro_batch * seq_len) and the two norms' fp32
+ * gain-gradient partial sums. */
+lc_status lc_workspace_bytes_split(const lc_stage_desc *desc, int32_t max_in_flight,
+                                   int32_t max_w_pending, size_t *bytes);
+
+/* lc_workspace_bytes_split with no weight-pass slots. */
 lc_status lc_workspace_bytes(const lc_stage_desc *desc, int32_t max_in_flight, size_t *bytes);
 
 /* ---------------------------------------------------------------- stage
@@ -203,6 +235,14 @@ lc_status lc_workspace_bytes(const lc_stage_desc *desc, int32_t max_in_flight, s
  * the stream first). */
 lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_bytes,
                           int32_t max_in_flight, void *stream, lc_stage **out);
+
+/* lc_stage_create with max_w_pending weight-pass slots (workspace >=
+ * lc_workspace_bytes_split): the stage can then run chunk_backward_input /
+ * chunk_backward_weight. lc_stage_create has none (LC_ERR_STASH_FULL on
+ * the first chunk_backward_input). */
+lc_status lc_stage_create_split(const lc_stage_desc *desc, void *workspace, size_t ws_bytes,
+                                int32_t max_in_flight, int32_t max_w_pending, void *stream,
+                                lc_stage **out);
 lc_status lc_stage_destroy(lc_stage *stage);
 
 /* Chunk F of one microbatch: Y = stage(X). Stashes the activations the
@@ -218,9 +258,29 @@ lc_status chunk_forward(lc_stage *stage, const lc_param_bufs *params,
 lc_status chunk_backward(lc_stage *stage, const lc_param_bufs *params,
                          const lc_microbatch_desc *mb, void *stream);
 
+/* Chunk BI of one microbatch (dense stages): dX = (dY/dX)^T dY exactly as
+ * chunk_backward computes it, without the parameter gradient. Reads dy now
+ * (and x, for the first layer's norm); writes the weight products' gradient
+ * operands and the norms' gain partial sums into a free weight-pass slot
+ * (LC_ERR_STASH_FULL if none). The stash slot stays taken until BW.
+ * LC_ERR_STATE if mb has no stashed forward or already ran BI;
+ * LC_ERR_UNSUPPORTED for mixture-of-experts stages. */
+lc_status chunk_backward_input(lc_stage *stage, const lc_param_bufs *params,
+                               const lc_microbatch_desc *mb, void *stream);
+
+/* Chunk BW of one microbatch: grad += dL/dW from the operands BI left,
+ * then releases the microbatch's weight-pass and stash slots. Only mb->mb
+ * is read from the descriptor. Per element the addition is the one
+ * chunk_backward makes, so BI + BW in the same microbatch order as the B
+ * entries of an Order gives a bit-identical gradient. LC_ERR_STATE if mb
+ * has no pending BI. */
+lc_status chunk_backward_weight(lc_stage *stage, const lc_param_bufs *params,
+                                const lc_microbatch_desc *mb, void *stream);
+
 /* Runs a whole Order: validates it (no side effects on failure), then
- * enqueues chunk_forward / chunk_backward in entry order. mbs[i] describes
- * microbatch i (num_microbatches entries). */
+ * enqueues chunk_forward / chunk_backward / chunk_backward_input /
+ * chunk_backward_weight in entry order. mbs[i] describes microbatch i
+ * (num_microbatches entries). */
 lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
                        const lc_microbatch_desc *mbs, void *stream);
 

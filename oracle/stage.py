@@ -407,10 +407,12 @@ def stage_loss(cfg, layers, X, dY, route_overrides=None) -> float:
 
 def run_order(cfg, flat_params, Xs: Sequence[np.ndarray], dYs: Sequence[np.ndarray],
               order: Sequence[Tuple[int, str]]):
-    """Execute an Order of (mb, 'F'|'B') entries (Piper Section 4.1, Split and
-    Order). F(mb) keeps its activations until B(mb); B(mb) adds the
-    microbatch's gradient into the flat accumulator G (initially +0, no 1/M
-    scaling) in the Order's B sequence.
+    """Execute an Order of (mb, 'F'|'B'|'Bi'|'Bw') entries (Piper Section 4.1,
+    Split and Order). F(mb) keeps its activations until B(mb) or Bi(mb).
+    B(mb) adds the microbatch's gradient into the flat accumulator G
+    (initially +0, no 1/M scaling); Bi(mb) produces dX(mb) and Bw(mb) adds the
+    microbatch's gradient into G, so G receives the microbatches' gradients in
+    the Order's sequence of B and Bw entries.
 
     Returns (Ys, dXs, G) with G in float64.
     """
@@ -419,13 +421,18 @@ def run_order(cfg, flat_params, Xs: Sequence[np.ndarray], dYs: Sequence[np.ndarr
     Ys: List[Optional[np.ndarray]] = [None] * M
     dXs: List[Optional[np.ndarray]] = [None] * M
     stash = {}
+    held = {}  # microbatch -> gradient computed by Bi, added by Bw
     G = np.zeros(synth.param_count(cfg), F64)
     for mb, ps in order:
         if ps == "F":
             Ys[mb], stash[mb] = stage_forward(cfg, layers, Xs[mb])
-        else:
+        elif ps == "B":
             dXs[mb], gmb = stage_backward(cfg, layers, stash.pop(mb), dYs[mb])
             G += gmb
+        elif ps == "Bi":
+            dXs[mb], held[mb] = stage_backward(cfg, layers, stash.pop(mb), dYs[mb])
+        else:
+            G += held.pop(mb)
     return Ys, dXs, G
 
 

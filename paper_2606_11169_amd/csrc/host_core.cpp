@@ -103,10 +103,15 @@ StageTypes stage_types(const lc_stage_desc &d) {
 
 static size_t bytes_of(int dt) { return dt == LC_FP32 ? 4 : 2; }
 
-lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *out) {
+lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_w_pending,
+                     StagePlan *out) {
   lc_status st = validate_desc(&d);
   if (st != LC_OK) return st;
   if (max_in_flight <= 0) return fail(LC_ERR_INVALID_ARG, "max_in_flight must be positive");
+  if (max_w_pending < 0 || max_w_pending > max_in_flight)
+    return fail(LC_ERR_INVALID_ARG, "max_w_pending must be in [0, max_in_flight]");
+  if (max_w_pending > 0 && d.n_experts > 0)
+    return fail(LC_ERR_UNSUPPORTED, "split backward of mixture-of-experts stages");
   StagePlan p{};
   p.ty = stage_types(d);
   const size_t es = bytes_of(p.ty.op), ea = bytes_of(p.ty.att), er = bytes_of(p.ty.res);
@@ -152,6 +157,21 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *o
   p.slot_bytes = lo * (size_t)d.n_layers;
   p.slot0 = off;
   off = align256(off + p.slot_bytes * (size_t)max_in_flight);
+
+  // one layer block of a weight-pass slot
+  size_t wo = 0;
+  auto wtake = [&](size_t bytes) { size_t r = wo; wo = align256(wo + bytes); return r; };
+  p.w_dy = wtake((size_t)T * D * es);
+  p.w_da = wtake(R * 2 * F * es);
+  p.w_dh = wtake((size_t)T * D * es);
+  p.w_dqkv = wtake((size_t)T * 3 * D * es);
+  p.w_p2 = wtake(rmsnorm_scratch_size(T, d.d_model));
+  p.w_p1 = wtake(rmsnorm_scratch_size(T, d.d_model));
+  p.wlayer_bytes = wo;
+  p.wslot_bytes = wo * (size_t)d.n_layers;
+  p.w_slots = max_w_pending;
+  p.wslot0 = off;
+  off = align256(off + p.wslot_bytes * (size_t)max_w_pending);
 
   auto stake = [&](size_t bytes) { size_t r = off; off = align256(off + bytes); return r; };
   p.s_dy0 = stake((size_t)T * D * er);
@@ -280,61 +300,142 @@ lc_status lc_order_1f1b(int32_t M, int32_t P, int32_t s, lc_order_entry *out, in
   return LC_OK;
 }
 
-lc_status lc_order_validate(const lc_order *order, int32_t max_in_flight, int32_t *peak) {
-  if (peak) *peak = 0;
-  if (!order) return fail(LC_ERR_INVALID_ARG, "null order");
-  if (max_in_flight <= 0) return fail(LC_ERR_INVALID_ARG, "max_in_flight must be positive");
-  const int32_t M = order->num_microbatches;
-  if (M <= 0) return fail(LC_ERR_BAD_ORDER, "num_microbatches must be positive");
-  if (order->n_entries != 2 * M)
-    return fail(LC_ERR_BAD_ORDER, "an Order over %d microbatches has %d entries, not 2M", M,
-                order->n_entries);
-  if (!order->entries) return fail(LC_ERR_INVALID_ARG, "null entries");
-  std::vector<uint8_t> seen_f((size_t)M, 0), seen_b((size_t)M, 0);
-  int32_t last_f = -1, last_b = -1, live = 0, pk = 0;
-  for (int32_t i = 0; i < order->n_entries; ++i) {
-    const lc_order_entry e = order->entries[i];
-    if (e.mb < 0 || e.mb >= M)
-      return fail(LC_ERR_BAD_ORDER, "entry %d: microbatch %d out of range", i, e.mb);
+lc_status lc_order_1f1b_split(int32_t M, int32_t P, int32_t s, int32_t w_delay,
+                              lc_order_entry *out, int32_t capacity, int32_t *n) {
+  if (w_delay < 0) return fail(LC_ERR_INVALID_ARG, "w_delay must be >= 0");
+  if (!out || !n) return fail(LC_ERR_INVALID_ARG, "null output pointer");
+  if (M > 0 && capacity < 3 * M)
+    return fail(LC_ERR_INVALID_ARG, "capacity %d < 3M = %d", capacity, 3 * M);
+  std::vector<lc_order_entry> base((size_t)(M > 0 ? 2 * M : 0));
+  int32_t nb = 0;
+  lc_status st = lc_order_1f1b(M, P, s, base.data(), 2 * M, &nb);
+  if (st != LC_OK) return st;
+  int32_t k = 0, oldest = 0;  // Bw entries leave in microbatch order
+  for (int32_t i = 0; i < nb; ++i) {
+    const lc_order_entry e = base[(size_t)i];
     if (e.pass == LC_PASS_F) {
-      if (seen_f[e.mb]) return fail(LC_ERR_BAD_ORDER, "entry %d: F%d appears twice", i, e.mb);
-      if (e.mb <= last_f)
-        return fail(LC_ERR_BAD_ORDER, "entry %d: F%d after F%d (forwards must be in order)", i,
-                    e.mb, last_f);
-      seen_f[e.mb] = 1;
-      last_f = e.mb;
-      ++live;
-      if (live > pk) pk = live;
-      if (peak) *peak = pk;
-      if (live > max_in_flight)
-        return fail(LC_ERR_STASH_FULL, "entry %d: %d microbatches in flight > %d slots", i, live,
-                    max_in_flight);
-    } else if (e.pass == LC_PASS_B) {
-      if (seen_b[e.mb]) return fail(LC_ERR_BAD_ORDER, "entry %d: B%d appears twice", i, e.mb);
-      if (!seen_f[e.mb]) return fail(LC_ERR_BAD_ORDER, "entry %d: B%d before F%d", i, e.mb, e.mb);
-      if (e.mb <= last_b)
-        return fail(LC_ERR_BAD_ORDER, "entry %d: B%d after B%d (backwards must be in order)", i,
-                    e.mb, last_b);
-      seen_b[e.mb] = 1;
-      last_b = e.mb;
-      --live;
-    } else {
-      return fail(LC_ERR_BAD_ORDER, "entry %d: unknown pass %d", i, e.pass);
+      out[k++] = e;
+      continue;
     }
+    out[k++] = lc_order_entry{e.mb, LC_PASS_BI};
+    if (e.mb - oldest >= w_delay) out[k++] = lc_order_entry{oldest++, LC_PASS_BW};
   }
-  if (peak) *peak = pk;
+  while (oldest < M) out[k++] = lc_order_entry{oldest++, LC_PASS_BW};
+  *n = k;
   return LC_OK;
 }
 
-lc_status lc_workspace_bytes(const lc_stage_desc *desc, int32_t max_in_flight, size_t *bytes) {
+lc_status lc_order_validate_split(const lc_order *order, int32_t max_in_flight,
+                                  int32_t max_w_pending, int32_t *peak, int32_t *peak_w) {
+  if (peak) *peak = 0;
+  if (peak_w) *peak_w = 0;
+  if (!order) return fail(LC_ERR_INVALID_ARG, "null order");
+  if (max_in_flight <= 0) return fail(LC_ERR_INVALID_ARG, "max_in_flight must be positive");
+  if (max_w_pending < 0) return fail(LC_ERR_INVALID_ARG, "max_w_pending must be >= 0");
+  const int32_t M = order->num_microbatches;
+  if (M <= 0) return fail(LC_ERR_BAD_ORDER, "num_microbatches must be positive");
+  if (order->n_entries < 2 * M || (int64_t)order->n_entries > 3 * (int64_t)M)
+    return fail(LC_ERR_BAD_ORDER, "an Order over %d microbatches has %d entries, not 2M to 3M", M,
+                order->n_entries);
+  if (!order->entries) return fail(LC_ERR_INVALID_ARG, "null entries");
+  // seen[mb] bit p: pass p of mb has appeared
+  std::vector<uint8_t> seen((size_t)M, 0);
+  static const char *const kName[4] = {"F", "B", "Bi", "Bw"};
+  int32_t last_f = -1, last_b = -1, live = 0, pk = 0, wlive = 0, pkw = 0;
+  lc_status res = LC_OK;
+  for (int32_t i = 0; i < order->n_entries && res == LC_OK; ++i) {
+    const lc_order_entry e = order->entries[i];
+    if (e.mb < 0 || e.mb >= M) {
+      res = fail(LC_ERR_BAD_ORDER, "entry %d: microbatch %d out of range", i, e.mb);
+      break;
+    }
+    if (e.pass < LC_PASS_F || e.pass > LC_PASS_BW) {
+      res = fail(LC_ERR_BAD_ORDER, "entry %d: unknown pass %d", i, e.pass);
+      break;
+    }
+    uint8_t &sn = seen[(size_t)e.mb];
+    const uint8_t bit = (uint8_t)(1u << e.pass);
+    if (sn & bit) {
+      res = fail(LC_ERR_BAD_ORDER, "entry %d: %s%d appears twice", i, kName[e.pass], e.mb);
+      break;
+    }
+    switch (e.pass) {
+      case LC_PASS_F:
+        if (e.mb <= last_f) {
+          res = fail(LC_ERR_BAD_ORDER, "entry %d: F%d after F%d (forwards must be in order)", i,
+                     e.mb, last_f);
+          break;
+        }
+        last_f = e.mb;
+        if (++live > pk) pk = live;
+        if (live > max_in_flight)
+          res = fail(LC_ERR_STASH_FULL, "entry %d: %d microbatches in flight > %d slots", i, live,
+                     max_in_flight);
+        break;
+      case LC_PASS_B:
+      case LC_PASS_BI:
+        if (!(sn & (1u << LC_PASS_F))) {
+          res = fail(LC_ERR_BAD_ORDER, "entry %d: %s%d before F%d", i, kName[e.pass], e.mb, e.mb);
+          break;
+        }
+        if (e.mb <= last_b || (sn & ((1u << LC_PASS_B) | (1u << LC_PASS_BI)))) {
+          res = fail(LC_ERR_BAD_ORDER,
+                     "entry %d: %s%d after the backward of microbatch %d (B and Bi entries "
+                     "must be in order, one per microbatch)",
+                     i, kName[e.pass], e.mb, last_b);
+          break;
+        }
+        last_b = e.mb;
+        if (e.pass == LC_PASS_B) {
+          --live;
+        } else {
+          if (++wlive > pkw) pkw = wlive;
+          if (wlive > max_w_pending)
+            res = fail(LC_ERR_STASH_FULL, "entry %d: %d weight passes pending > %d slots", i,
+                       wlive, max_w_pending);
+        }
+        break;
+      default:  // LC_PASS_BW
+        if (!(sn & (1u << LC_PASS_BI))) {
+          res = fail(LC_ERR_BAD_ORDER, "entry %d: Bw%d before Bi%d", i, e.mb, e.mb);
+          break;
+        }
+        --live;
+        --wlive;
+        break;
+    }
+    sn |= bit;
+  }
+  if (peak) *peak = pk;
+  if (peak_w) *peak_w = pkw;
+  if (res != LC_OK) return res;
+  for (int32_t mb = 0; mb < M; ++mb) {
+    const uint8_t sn = seen[(size_t)mb];
+    const bool has_b = sn & (1u << LC_PASS_B), has_bw = sn & (1u << LC_PASS_BW);
+    if (!(sn & (1u << LC_PASS_F)) || has_b == has_bw)
+      return fail(LC_ERR_BAD_ORDER, "microbatch %d lacks its F, or its B (or Bi and Bw)", mb);
+  }
+  return LC_OK;
+}
+
+lc_status lc_order_validate(const lc_order *order, int32_t max_in_flight, int32_t *peak) {
+  return lc_order_validate_split(order, max_in_flight, max_in_flight, peak, nullptr);
+}
+
+lc_status lc_workspace_bytes_split(const lc_stage_desc *desc, int32_t max_in_flight,
+                                   int32_t max_w_pending, size_t *bytes) {
   if (!bytes) return fail(LC_ERR_INVALID_ARG, "null output pointer");
   StagePlan p;
   lc_status st = validate_desc(desc);
   if (st != LC_OK) return st;
-  st = stage_plan(*desc, max_in_flight, &p);
+  st = stage_plan(*desc, max_in_flight, max_w_pending, &p);
   if (st != LC_OK) return st;
   *bytes = p.total;
   return LC_OK;
+}
+
+lc_status lc_workspace_bytes(const lc_stage_desc *desc, int32_t max_in_flight, size_t *bytes) {
+  return lc_workspace_bytes_split(desc, max_in_flight, 0, bytes);
 }
 
 size_t lc_rmsnorm_scratch_bytes(int64_t T, int64_t d) { return rmsnorm_scratch_size(T, d); }

@@ -56,6 +56,15 @@ struct StagePlan {
   size_t slot0, slot_bytes, layer_bytes;
   // offsets inside one layer block
   size_t xin, rstd1, n1, qkv, o, lse, h, rstd2, n2, gate, up, act;
+  // weight-pass slots (split backward): max_w_pending slots of n_layers
+  // blocks, each holding the gradient operands a backward-for-inputs pass
+  // leaves for the backward-for-weights pass of the same microbatch: the
+  // layer-output gradient dy [T, d], dgate|dup [T, 2f], dh [T, d] and
+  // dq|dk|dv [T, 3d] (op type), and the fp32 gain-gradient partial sums of
+  // both norms (rmsnorm_scratch_size each)
+  int32_t w_slots;
+  size_t wslot0, wslot_bytes, wlayer_bytes;
+  size_t w_dy, w_da, w_dh, w_dqkv, w_p2, w_p1;
   // MoE per-layer extras (0 when dense): routing (sel, w [T, 2]), dispatch
   // (perm, wrow [2T], rowpos [T, 2], expert offsets [E + 1]), the gathered
   // expert inputs xp [2T, d] (op type) and expert outputs eo [2T, d] (fp32)
@@ -77,6 +86,7 @@ struct StagePlan {
   size_t s_moe_dys, s_moe_dns, s_moe_dw, s_moe_dl, s_moe_part, s_moe_part_bytes;
   size_t total;
 };
-lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, StagePlan *out);
+lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_w_pending,
+                     StagePlan *out);
 
 }  // namespace lc

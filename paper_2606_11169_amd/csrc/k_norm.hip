@@ -29,6 +29,7 @@ struct NormP {
   void *n, *dx, *dx_copy;
   float *rstd;
   float *partial, *dg;
+  int part;  // write the gain-gradient partial sums
   int64_t rows;
   int d;
   float eps;
@@ -186,7 +187,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_rows_kernel(NormP p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
   for (int64_t row = r0 + wv; row < r1; row += 4) bwd_row_regs(p, row, lane, acc);
-  if (!p.dg) return;  // uniform: no gain gradient requested
+  if (!p.part) return;  // uniform: no gain gradient requested
 #pragma unroll 1
   for (int w = 0; w < 4; ++w) {
     if (wv == w) {
@@ -287,6 +288,7 @@ NormP make_params(const lc_norm_args &a) {
   p.rstd = a.rstd;
   p.partial = static_cast<float *>(a.scratch);
   p.dg = a.dg_accum;
+  p.part = a.dg_accum != nullptr;
   p.rows = a.T;
   p.d = (int)a.d;
   p.eps = a.eps;
@@ -309,19 +311,55 @@ lc_status rmsnorm_fwd_launch(const lc_norm_args &a, hipStream_t s) {
   return check_launch("rmsnorm_fwd_kernel");
 }
 
+namespace {
+
+// Row kernel, plus the separate partial-sum kernel for rows longer than MAXD
+// when p.part is set.
+lc_status bwd_rows(const NormP &p, hipStream_t s) {
+  hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel, dim3((unsigned)p.nblk), dim3(256), 0, s, p);
+  LC_TRY(check_launch("rmsnorm_bwd_rows_kernel"));
+  if (!p.part || p.d <= MAXD) return LC_OK;
+  hipLaunchKernelGGL(rmsnorm_dg_partial_kernel, dim3((unsigned)((p.d + 255) / 256), (unsigned)p.nblk),
+                     dim3(256), 0, s, p);
+  return check_launch("rmsnorm_dg_partial_kernel");
+}
+
+lc_status dg_final(const NormP &p, hipStream_t s) {
+  hipLaunchKernelGGL(rmsnorm_dg_final_kernel, dim3((unsigned)((p.d + 63) / 64)), dim3(1024), 0, s, p);
+  return check_launch("rmsnorm_dg_final_kernel");
+}
+
+}  // namespace
+
 lc_status rmsnorm_bwd_launch(const lc_norm_args &a, hipStream_t s) {
   LC_TRY(check_common(a, true));
   const NormP p = make_params(a);
-  hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel, dim3((unsigned)p.nblk), dim3(256), 0, s, p);
-  LC_TRY(check_launch("rmsnorm_bwd_rows_kernel"));
-  if (!a.dg_accum) return LC_OK;
-  if (a.d > MAXD) {
-    hipLaunchKernelGGL(rmsnorm_dg_partial_kernel, dim3((unsigned)((a.d + 255) / 256), (unsigned)p.nblk),
-                       dim3(256), 0, s, p);
-    LC_TRY(check_launch("rmsnorm_dg_partial_kernel"));
-  }
-  hipLaunchKernelGGL(rmsnorm_dg_final_kernel, dim3((unsigned)((a.d + 63) / 64)), dim3(1024), 0, s, p);
-  return check_launch("rmsnorm_dg_final_kernel");
+  LC_TRY(bwd_rows(p, s));
+  return a.dg_accum ? dg_final(p, s) : LC_OK;
+}
+
+lc_status rmsnorm_bwd_partials_launch(const lc_norm_args &a, hipStream_t s) {
+  lc_norm_args b = a;
+  b.dg_accum = nullptr;
+  LC_TRY(check_common(b, true));
+  if (!a.scratch || a.scratch_bytes < rmsnorm_scratch_size(a.T, a.d))
+    return fail(LC_ERR_WORKSPACE, "rmsnorm: scratch smaller than lc_rmsnorm_scratch_bytes");
+  NormP p = make_params(b);
+  p.part = 1;
+  return bwd_rows(p, s);
+}
+
+lc_status rmsnorm_dg_final_launch(const float *partial, float *dg, int64_t T, int64_t d,
+                                  hipStream_t s) {
+  if (!partial || !dg || T <= 0 || d <= 0 || d > INT32_MAX)
+    return fail(LC_ERR_INVALID_ARG, "rmsnorm: bad gain-gradient sum arguments");
+  NormP p{};
+  p.partial = const_cast<float *>(partial);
+  p.dg = dg;
+  p.rows = T;
+  p.d = (int)d;
+  p.nblk = (int)((T + kNormRowsPerBlock - 1) / kNormRowsPerBlock);
+  return dg_final(p, s);
 }
 
 }  // namespace lc

@@ -12,6 +12,16 @@
 // bucket's flat fp32 buffer (Section 4.3.2; accumulated across microbatches,
 // Section 6.2).
 //
+// Split backward (Section 4.1, PASS values Bi and Bw): the backward for the
+// inputs runs every input-gradient launch of Chunk B and leaves the operands
+// of the weight-gradient products (per layer: the layer-output gradient,
+// dgate|dup, dh, dq|dk|dv, all in the operand type, and both norms' gain
+// partial sums) in a weight-pass slot; the backward for the weights runs the
+// weight-gradient products and the gain sums from there, then frees the
+// weight-pass slot and the stash slot (the products also read n1, o, n2 and
+// act from the stash). The same kernels in the same per-element order make
+// the gradient bit-identical to Chunk B's.
+//
 // Tensor element types follow StageTypes: matrix-product operands in the
 // compute dtype, attention q/k/v in fp16 for a bf16 stage, and the residual
 // stream (inside and between layers), its gradient, the gate/up values kept
@@ -33,6 +43,7 @@ struct lc_stage {
   int32_t slots;
   std::vector<int32_t> owner;      // microbatch stashed in each slot, -1 if free
   std::vector<const void *> xin0;  // the caller's X of that microbatch
+  std::vector<int32_t> wowner;     // microbatch whose weight pass is pending, per weight-pass slot
   std::vector<float> rope_host;    // cos table then sin table (fp32)
 };
 
@@ -84,6 +95,13 @@ static LayerBufs layer_bufs(lc_stage *st, int slot, int l) {
   LayerBufs b;
   b.base = st->ws + st->plan.slot0 + (size_t)slot * st->plan.slot_bytes +
            (size_t)l * st->plan.layer_bytes;
+  return b;
+}
+
+static LayerBufs wlayer_bufs(lc_stage *st, int wslot, int l) {
+  LayerBufs b;
+  b.base = st->ws + st->plan.wslot0 + (size_t)wslot * st->plan.wslot_bytes +
+           (size_t)l * st->plan.wlayer_bytes;
   return b;
 }
 
@@ -277,14 +295,19 @@ static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const voi
   return LC_OK;
 }
 
+// Chunk B (wslot < 0), or the backward for the inputs (wslot >= 0: weight
+// products skipped, their operands and the gain partial sums left in weight-
+// pass slot wslot).
 static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const void *x0,
-                                 const void *dy_in, void *dx_out, int slot, hipStream_t s) {
+                                 const void *dy_in, void *dx_out, int slot, int wslot,
+                                 hipStream_t s) {
   const lc_stage_desc &d = st->d;
   const StagePlan &P = st->plan;
   const ParamPlan &pp = st->pp;
   const int dt = d.compute_dtype;
   const StageTypes ty = P.ty;
   const bool copies = ty.op != ty.res;  // bf16 operand copies of fp32 gradients
+  const bool split = wslot >= 0;
   const int64_t T = P.T, D = d.d_model, F = d.d_ff;
   const size_t ea = dtype_size(ty.att), es = P.elem;
   const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
@@ -293,17 +316,34 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
   // gradient flowing into the current layer: residual version and operand version
   const void *dy_res = dy_in, *dy_op = dy_in;
   int dy_dt = dt;
+  if (split) {
+    // the weight pass reads the top layer's dy after the caller may have reused it
+    void *top = wlayer_bufs(st, wslot, d.n_layers - 1).at(P.w_dy);
+    hipError_t e = hipMemcpyAsync(top, dy_in, (size_t)T * D * es, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "saving dy for the weight pass");
+    dy_op = top;
+  }
   for (int l = d.n_layers - 1; l >= 0; --l) {
     const LayerBufs L = layer_bufs(st, slot, l);
+    const LayerBufs WL = split ? wlayer_bufs(st, wslot, l) : LayerBufs{nullptr};
     const size_t lw = (size_t)l * pp.per_layer;
-    const W w{static_cast<const char *>(pb->w) + lw * P.elem, pb->grad + lw, P.elem};
+    const W w{static_cast<const char *>(pb->w) + lw * P.elem, split ? nullptr : pb->grad + lw,
+              P.elem};
     const bool first = l == 0;
     const void *xin = first ? x0 : L.at(P.xin);
     const int x_dt = first ? dt : ty.res;
-    void *dx = first ? dx_out : ws + ((d.n_layers - 1 - l) % 2 == 0 ? P.s_dy0 : P.s_dy1);
-    void *da = ws + P.s_da, *dn = ws + P.s_dn, *dh = ws + P.s_dh, *dO = ws + P.s_do;
-    void *dh_op = copies ? ws + P.s_dh16 : dh;
-    char *dqkv = ws + P.s_dqkv;
+    // operand copy of the gradient handed to layer l - 1
+    void *dy_next_op = first ? nullptr
+                       : split ? wlayer_bufs(st, wslot, l - 1).at(P.w_dy)
+                               : ws + P.s_dy16;
+    void *dx = first ? dx_out
+               : (split && !copies) ? dy_next_op
+                                    : ws + ((d.n_layers - 1 - l) % 2 == 0 ? P.s_dy0 : P.s_dy1);
+    void *dn = ws + P.s_dn, *dO = ws + P.s_do;
+    void *da = split ? WL.at(P.w_da) : ws + P.s_da;
+    void *dh = (split && !copies) ? WL.at(P.w_dh) : ws + P.s_dh;
+    void *dh_op = !copies ? dh : split ? WL.at(P.w_dh) : ws + P.s_dh16;
+    char *dqkv = split ? static_cast<char *>(WL.at(P.w_dqkv)) : ws + P.s_dqkv;
     lc_gemm_args a;
     if (d.n_experts > 0) {
       LC_TRY(moe_backward(st, w, L, dy_res, dy_dt, s));
@@ -316,11 +356,13 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a.aux0 = L.at(P.gate); a.aux1 = L.at(P.up); a.ld_aux = F; a.aux_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // G[W2] += dy^T act
-    a = gemm_base(dt, LC_EPI_ACCUM_F32, D, F, T);
-    a.A = dy_op; a.lda = D; a.a_kmajor = 0;
-    a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
-    a.C = w.gp(pp.w2); a.ldc = F;
-    LC_TRY(gemm_launch(a, s));
+    if (!split) {
+      a = gemm_base(dt, LC_EPI_ACCUM_F32, D, F, T);
+      a.A = dy_op; a.lda = D; a.a_kmajor = 0;
+      a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
+      a.C = w.gp(pp.w2); a.ldc = F;
+      LC_TRY(gemm_launch(a, s));
+    }
     // dn2 = [dgate | dup] [W1; W3]
     a = gemm_base(dt, LC_EPI_STORE, T, D, 2 * F);
     a.A = da; a.lda = 2 * F; a.a_kmajor = 1;
@@ -328,13 +370,15 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a.C = dn; a.ldc = D; a.c_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // G[W1; W3] += [dgate | dup]^T n2
-    a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * F, D, T);
-    a.A = da; a.lda = 2 * F; a.a_kmajor = 0;
-    a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
-    a.C = w.gp(pp.w1); a.ldc = D;
-    LC_TRY(gemm_launch(a, s));
+    if (!split) {
+      a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * F, D, T);
+      a.A = da; a.lda = 2 * F; a.a_kmajor = 0;
+      a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
+      a.C = w.gp(pp.w1); a.ldc = D;
+      LC_TRY(gemm_launch(a, s));
     }
-    // dh = dy + RMSNorm2'(dn2); G[g2] += ...
+    }
+    // dh = dy + RMSNorm2'(dn2); G[g2] += ... (or its partial sums)
     lc_norm_args nb = norm_base(T, D, d.rms_eps);
     nb.dn = dn; nb.dn_dtype = ty.res;
     nb.x = L.at(P.h); nb.x_dtype = ty.res;
@@ -343,9 +387,14 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     nb.dres = dy_res; nb.dres_dtype = dy_dt;
     nb.dx = dh; nb.out_dtype = ty.res;
     nb.dx_copy = copies ? dh_op : nullptr;
-    nb.dg_accum = w.gp(pp.g2);
-    nb.scratch = ws + P.s_norm; nb.scratch_bytes = P.s_norm_bytes;
-    LC_TRY(rmsnorm_bwd_launch(nb, s));
+    if (split) {
+      nb.scratch = WL.at(P.w_p2); nb.scratch_bytes = rmsnorm_scratch_size(T, D);
+      LC_TRY(rmsnorm_bwd_partials_launch(nb, s));
+    } else {
+      nb.dg_accum = w.gp(pp.g2);
+      nb.scratch = ws + P.s_norm; nb.scratch_bytes = P.s_norm_bytes;
+      LC_TRY(rmsnorm_bwd_launch(nb, s));
+    }
     // do = dh Wo
     a = gemm_base(dt, LC_EPI_STORE, T, D, D);
     a.A = dh_op; a.lda = D; a.a_kmajor = 1;
@@ -353,11 +402,13 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a.C = dO; a.ldc = D; a.c_dtype = ty.op;
     LC_TRY(gemm_launch(a, s));
     // G[Wo] += dh^T o
-    a = gemm_base(dt, LC_EPI_ACCUM_F32, D, D, T);
-    a.A = dh_op; a.lda = D; a.a_kmajor = 0;
-    a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
-    a.C = w.gp(pp.wo); a.ldc = D;
-    LC_TRY(gemm_launch(a, s));
+    if (!split) {
+      a = gemm_base(dt, LC_EPI_ACCUM_F32, D, D, T);
+      a.A = dh_op; a.lda = D; a.a_kmajor = 0;
+      a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
+      a.C = w.gp(pp.wo); a.ldc = D;
+      LC_TRY(gemm_launch(a, s));
+    }
     // dq, dk, dv (dq, dk rotated back)
     char *qkv = static_cast<char *>(L.at(P.qkv));
     lc_attn_args at;
@@ -378,24 +429,76 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     a.C = dn; a.ldc = D; a.c_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
-    a = gemm_base(dt, LC_EPI_ACCUM_F32, 3 * D, D, T);
-    a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 0;
-    a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
-    a.C = w.gp(pp.wq); a.ldc = D;
-    LC_TRY(gemm_launch(a, s));
-    // dx = dh + RMSNorm1'(dn1); G[g1] += ...
+    if (!split) {
+      a = gemm_base(dt, LC_EPI_ACCUM_F32, 3 * D, D, T);
+      a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 0;
+      a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
+      a.C = w.gp(pp.wq); a.ldc = D;
+      LC_TRY(gemm_launch(a, s));
+    }
+    // dx = dh + RMSNorm1'(dn1); G[g1] += ... (or its partial sums)
     nb.dn = dn; nb.dn_dtype = ty.res;
     nb.x = xin; nb.x_dtype = x_dt;
     nb.rstd = static_cast<float *>(L.at(P.rstd1));
     nb.g = w.wp(pp.g1);
     nb.dres = dh; nb.dres_dtype = ty.res;
     nb.dx = dx; nb.out_dtype = first ? dt : ty.res;
-    nb.dx_copy = (copies && !first) ? ws + P.s_dy16 : nullptr;
-    nb.dg_accum = w.gp(pp.g1);
-    LC_TRY(rmsnorm_bwd_launch(nb, s));
+    nb.dx_copy = (copies && !first) ? dy_next_op : nullptr;
+    if (split) {
+      nb.scratch = WL.at(P.w_p1); nb.scratch_bytes = rmsnorm_scratch_size(T, D);
+      LC_TRY(rmsnorm_bwd_partials_launch(nb, s));
+    } else {
+      nb.dg_accum = w.gp(pp.g1);
+      LC_TRY(rmsnorm_bwd_launch(nb, s));
+    }
     dy_res = dx;
-    dy_op = copies ? ws + P.s_dy16 : dx;
+    dy_op = copies ? dy_next_op : dx;
     dy_dt = ty.res;
+  }
+  return LC_OK;
+}
+
+// The backward for the weights: every weight-gradient product and gain sum of
+// Chunk B, from the operands the backward for the inputs left in weight-pass
+// slot wslot and the activations in stash slot `slot`.
+static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, int wslot,
+                               hipStream_t s) {
+  const lc_stage_desc &d = st->d;
+  const StagePlan &P = st->plan;
+  const ParamPlan &pp = st->pp;
+  const int dt = d.compute_dtype;
+  const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  for (int l = d.n_layers - 1; l >= 0; --l) {
+    const LayerBufs L = layer_bufs(st, slot, l);
+    const LayerBufs WL = wlayer_bufs(st, wslot, l);
+    const size_t lw = (size_t)l * pp.per_layer;
+    const W w{static_cast<const char *>(pb->w) + lw * P.elem, pb->grad + lw, P.elem};
+    // G[W2] += dy^T act
+    lc_gemm_args a = gemm_base(dt, LC_EPI_ACCUM_F32, D, F, T);
+    a.A = WL.at(P.w_dy); a.lda = D; a.a_kmajor = 0;
+    a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
+    a.C = w.gp(pp.w2); a.ldc = F;
+    LC_TRY(gemm_launch(a, s));
+    // G[W1; W3] += [dgate | dup]^T n2
+    a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * F, D, T);
+    a.A = WL.at(P.w_da); a.lda = 2 * F; a.a_kmajor = 0;
+    a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
+    a.C = w.gp(pp.w1); a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p2)), w.gp(pp.g2), T, D, s));
+    // G[Wo] += dh^T o
+    a = gemm_base(dt, LC_EPI_ACCUM_F32, D, D, T);
+    a.A = WL.at(P.w_dh); a.lda = D; a.a_kmajor = 0;
+    a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
+    a.C = w.gp(pp.wo); a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
+    a = gemm_base(dt, LC_EPI_ACCUM_F32, 3 * D, D, T);
+    a.A = WL.at(P.w_dqkv); a.lda = 3 * D; a.a_kmajor = 0;
+    a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
+    a.C = w.gp(pp.wq); a.ldc = D;
+    LC_TRY(gemm_launch(a, s));
+    LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p1)), w.gp(pp.g1), T, D, s));
   }
   return LC_OK;
 }
@@ -428,6 +531,12 @@ static int find_slot(const lc_stage *st, int32_t mb) {
   return -1;
 }
 
+static int find_wslot(const lc_stage *st, int32_t mb) {
+  for (int i = 0; i < (int)st->wowner.size(); ++i)
+    if (st->wowner[i] == mb) return i;
+  return -1;
+}
+
 static lc_status do_forward(lc_stage *st, const lc_param_bufs *pb, const lc_microbatch_desc *mb,
                             hipStream_t s) {
   int slot = find_slot(st, -1);
@@ -436,12 +545,32 @@ static lc_status do_forward(lc_stage *st, const lc_param_bufs *pb, const lc_micr
   return forward_layers(st, pb, mb->x, mb->y, slot, s);
 }
 
+static void release(lc_stage *st, int slot) {
+  st->owner[slot] = -1;
+  st->xin0[slot] = nullptr;
+}
+
 static lc_status do_backward(lc_stage *st, const lc_param_bufs *pb, const lc_microbatch_desc *mb,
                              hipStream_t s) {
   const int slot = find_slot(st, mb->mb);
-  lc_status r = backward_layers(st, pb, st->xin0[slot], mb->dy, mb->dx, slot, s);
-  st->owner[slot] = -1;
-  st->xin0[slot] = nullptr;
+  lc_status r = backward_layers(st, pb, st->xin0[slot], mb->dy, mb->dx, slot, -1, s);
+  release(st, slot);
+  return r;
+}
+
+static lc_status do_backward_input(lc_stage *st, const lc_param_bufs *pb,
+                                   const lc_microbatch_desc *mb, hipStream_t s) {
+  const int slot = find_slot(st, mb->mb), wslot = find_wslot(st, -1);
+  st->wowner[wslot] = mb->mb;
+  return backward_layers(st, pb, st->xin0[slot], mb->dy, mb->dx, slot, wslot, s);
+}
+
+static lc_status do_backward_weight(lc_stage *st, const lc_param_bufs *pb, int32_t mb,
+                                    hipStream_t s) {
+  const int slot = find_slot(st, mb), wslot = find_wslot(st, mb);
+  lc_status r = weight_layers(st, pb, slot, wslot, s);
+  st->wowner[wslot] = -1;
+  release(st, slot);
   return r;
 }
 
@@ -451,13 +580,14 @@ using namespace lc;
 
 extern "C" {
 
-lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_bytes,
-                          int32_t max_in_flight, void *stream, lc_stage **out) {
+lc_status lc_stage_create_split(const lc_stage_desc *desc, void *workspace, size_t ws_bytes,
+                                int32_t max_in_flight, int32_t max_w_pending, void *stream,
+                                lc_stage **out) {
   if (!out) return fail(LC_ERR_INVALID_ARG, "null output handle");
   *out = nullptr;
   StagePlan plan;
   LC_TRY(validate_desc(desc));
-  LC_TRY(stage_plan(*desc, max_in_flight, &plan));
+  LC_TRY(stage_plan(*desc, max_in_flight, max_w_pending, &plan));
   if (!workspace) return fail(LC_ERR_INVALID_ARG, "null workspace");
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(LC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
@@ -472,6 +602,7 @@ lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_
   st->slots = max_in_flight;
   st->owner.assign((size_t)max_in_flight, -1);
   st->xin0.assign((size_t)max_in_flight, nullptr);
+  st->wowner.assign((size_t)max_w_pending, -1);
   // RoPE angles p * base^(-2i/hd) in double, tables rounded once to float
   const int half = desc->head_dim / 2, S = desc->seq_len;
   st->rope_host.resize((size_t)2 * S * half);
@@ -497,6 +628,11 @@ lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_
   return LC_OK;
 }
 
+lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_bytes,
+                          int32_t max_in_flight, void *stream, lc_stage **out) {
+  return lc_stage_create_split(desc, workspace, ws_bytes, max_in_flight, 0, stream, out);
+}
+
 lc_status lc_stage_destroy(lc_stage *stage) {
   delete stage;
   return LC_OK;
@@ -520,7 +656,34 @@ lc_status chunk_backward(lc_stage *stage, const lc_param_bufs *params, const lc_
   LC_TRY(check_mb(mb, false));
   if (mb->mb < 0 || find_slot(stage, mb->mb) < 0)
     return fail(LC_ERR_STATE, "microbatch %d has no stashed forward", mb->mb);
+  if (find_wslot(stage, mb->mb) >= 0)
+    return fail(LC_ERR_STATE, "microbatch %d already ran its backward for the inputs", mb->mb);
   return do_backward(stage, params, mb, static_cast<hipStream_t>(stream));
+}
+
+lc_status chunk_backward_input(lc_stage *stage, const lc_param_bufs *params,
+                               const lc_microbatch_desc *mb, void *stream) {
+  LC_TRY(check_params(stage, params, false));
+  LC_TRY(check_mb(mb, false));
+  if (stage->d.n_experts > 0)
+    return fail(LC_ERR_UNSUPPORTED, "split backward of mixture-of-experts stages");
+  if (mb->mb < 0 || find_slot(stage, mb->mb) < 0)
+    return fail(LC_ERR_STATE, "microbatch %d has no stashed forward", mb->mb);
+  if (find_wslot(stage, mb->mb) >= 0)
+    return fail(LC_ERR_STATE, "microbatch %d already ran its backward for the inputs", mb->mb);
+  if (find_wslot(stage, -1) < 0)
+    return fail(LC_ERR_STASH_FULL, "all %d weight-pass slots are in use",
+                (int)stage->wowner.size());
+  return do_backward_input(stage, params, mb, static_cast<hipStream_t>(stream));
+}
+
+lc_status chunk_backward_weight(lc_stage *stage, const lc_param_bufs *params,
+                                const lc_microbatch_desc *mb, void *stream) {
+  LC_TRY(check_params(stage, params, true));
+  if (!mb) return fail(LC_ERR_INVALID_ARG, "null microbatch descriptor");
+  if (mb->mb < 0 || find_wslot(stage, mb->mb) < 0)
+    return fail(LC_ERR_STATE, "microbatch %d has no pending weight pass", mb->mb);
+  return do_backward_weight(stage, params, mb->mb, static_cast<hipStream_t>(stream));
 }
 
 lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32_t *sel_out,
@@ -540,7 +703,8 @@ lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32
 lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
                        const lc_microbatch_desc *mbs, void *stream) {
   LC_TRY(check_params(stage, params, true));
-  LC_TRY(lc_order_validate(order, stage->slots, nullptr));
+  LC_TRY(lc_order_validate_split(order, stage->slots, (int32_t)stage->wowner.size(), nullptr,
+                                 nullptr));
   if (!mbs) return fail(LC_ERR_INVALID_ARG, "null microbatch array");
   for (int i = 0; i < order->num_microbatches; ++i) {
     if (mbs[i].mb != i) return fail(LC_ERR_INVALID_ARG, "mbs[%d].mb = %d, expected %d", i, mbs[i].mb, i);
@@ -551,12 +715,21 @@ lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_or
     if (stage->owner[i] != -1)
       return fail(LC_ERR_STATE, "lc_run_order needs an empty stash (microbatch %d is stashed)",
                   stage->owner[i]);
+  bool split = false;
+  for (int i = 0; i < order->n_entries; ++i) split |= order->entries[i].pass == LC_PASS_BI;
+  if (split && stage->d.n_experts > 0)
+    return fail(LC_ERR_UNSUPPORTED, "split backward of mixture-of-experts stages");
   hipStream_t s = static_cast<hipStream_t>(stream);
   for (int i = 0; i < order->n_entries; ++i) {
     const lc_order_entry e = order->entries[i];
     const lc_microbatch_desc *mb = &mbs[e.mb];
-    lc_status r = e.pass == LC_PASS_F ? do_forward(stage, params, mb, s)
-                                      : do_backward(stage, params, mb, s);
+    lc_status r;
+    switch (e.pass) {
+      case LC_PASS_F: r = do_forward(stage, params, mb, s); break;
+      case LC_PASS_B: r = do_backward(stage, params, mb, s); break;
+      case LC_PASS_BI: r = do_backward_input(stage, params, mb, s); break;
+      default: r = do_backward_weight(stage, params, e.mb, s); break;
+    }
     if (r != LC_OK) return r;
   }
   return LC_OK;

@@ -31,7 +31,7 @@ STATUS_NAMES = {0: "OK", -1: "INVALID_ARG", -2: "UNSUPPORTED", -3: "BAD_ORDER",
                 -4: "STASH_FULL", -5: "STATE", -6: "WORKSPACE", -7: "HIP"}
 
 LC_FP32, LC_BF16, LC_FP16 = 0, 1, 2
-LC_PASS_F, LC_PASS_B = 0, 1
+LC_PASS_F, LC_PASS_B, LC_PASS_BI, LC_PASS_BW = 0, 1, 2, 3
 (LC_T_WQ, LC_T_WK, LC_T_WV, LC_T_WO, LC_T_G1, LC_T_W1, LC_T_W3, LC_T_W2, LC_T_G2,
  LC_T_WR) = range(10)
 (LC_EPI_STORE, LC_EPI_STORE_F32, LC_EPI_ACCUM_F32, LC_EPI_RESIDUAL, LC_EPI_ROPE,
@@ -131,15 +131,29 @@ _SIGS = {
                                   C.POINTER(C.c_size_t), C.POINTER(C.c_int64)]),
     "lc_order_1f1b": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.POINTER(lc_order_entry),
                                 C.c_int32, C.POINTER(C.c_int32)]),
+    "lc_order_1f1b_split": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                      C.POINTER(lc_order_entry), C.c_int32,
+                                      C.POINTER(C.c_int32)]),
     "lc_order_validate": (C.c_int, [C.POINTER(lc_order), C.c_int32, C.POINTER(C.c_int32)]),
+    "lc_order_validate_split": (C.c_int, [C.POINTER(lc_order), C.c_int32, C.c_int32,
+                                          C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
     "lc_workspace_bytes": (C.c_int, [C.POINTER(lc_stage_desc), C.c_int32, C.POINTER(C.c_size_t)]),
+    "lc_workspace_bytes_split": (C.c_int, [C.POINTER(lc_stage_desc), C.c_int32, C.c_int32,
+                                           C.POINTER(C.c_size_t)]),
     "lc_stage_create": (C.c_int, [C.POINTER(lc_stage_desc), C.c_void_p, C.c_size_t, C.c_int32,
                                   C.c_void_p, C.POINTER(C.c_void_p)]),
+    "lc_stage_create_split": (C.c_int, [C.POINTER(lc_stage_desc), C.c_void_p, C.c_size_t,
+                                        C.c_int32, C.c_int32, C.c_void_p,
+                                        C.POINTER(C.c_void_p)]),
     "lc_stage_destroy": (C.c_int, [C.c_void_p]),
     "chunk_forward": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
                                 C.POINTER(lc_microbatch_desc), C.c_void_p]),
     "chunk_backward": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
                                  C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "chunk_backward_input": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
+                                       C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "chunk_backward_weight": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
+                                        C.POINTER(lc_microbatch_desc), C.c_void_p]),
     "lc_run_order": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs), C.POINTER(lc_order),
                                C.POINTER(lc_microbatch_desc), C.c_void_p]),
     "chunk_accumulate_grad": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_size_t,
@@ -238,6 +252,13 @@ def lc_order_1f1b(M, P, s) -> List[Tuple[int, int]]:
     return [(buf[i].mb, buf[i].pass_) for i in range(n.value)]
 
 
+def lc_order_1f1b_split(M, P, s, w_delay) -> List[Tuple[int, int]]:
+    buf = (lc_order_entry * max(1, 3 * M))()
+    n = C.c_int32()
+    _check(lib().lc_order_1f1b_split(M, P, s, w_delay, buf, 3 * M, C.byref(n)))
+    return [(buf[i].mb, buf[i].pass_) for i in range(n.value)]
+
+
 def make_order(entries: Sequence[Tuple[int, int]], M: int):
     arr = (lc_order_entry * max(1, len(entries)))(*[lc_order_entry(m, p) for m, p in entries])
     o = lc_order(M, len(entries), C.cast(arr, C.POINTER(lc_order_entry)))
@@ -255,9 +276,21 @@ def lc_order_validate(entries, M, max_in_flight) -> Tuple[int, int]:
     return st, pk.value
 
 
-def lc_workspace_bytes(desc, max_in_flight) -> int:
+def lc_order_validate_split(entries, M, max_in_flight, max_w_pending) -> Tuple[int, int, int]:
+    """Returns (status, peak, peak_w) without raising for Order errors."""
+    o = make_order(entries, M)
+    pk, pkw = C.c_int32(), C.c_int32()
+    st = lib().lc_order_validate_split(C.byref(o), max_in_flight, max_w_pending, C.byref(pk),
+                                       C.byref(pkw))
+    if st not in (LC_OK, LC_ERR_BAD_ORDER, LC_ERR_STASH_FULL):
+        _check(st)
+    return st, pk.value, pkw.value
+
+
+def lc_workspace_bytes(desc, max_in_flight, max_w_pending=0) -> int:
     n = C.c_size_t()
-    _check(lib().lc_workspace_bytes(C.byref(desc), max_in_flight, C.byref(n)))
+    _check(lib().lc_workspace_bytes_split(C.byref(desc), max_in_flight, max_w_pending,
+                                          C.byref(n)))
     return n.value
 
 
@@ -274,10 +307,11 @@ def lc_attention_scratch_bytes(B, S, H) -> int:
 class Stage:
     """Owns an lc_stage handle (host memory); the workspace belongs to the caller."""
 
-    def __init__(self, desc, workspace, ws_bytes, max_in_flight, stream=None):
+    def __init__(self, desc, workspace, ws_bytes, max_in_flight, stream=None, max_w_pending=0):
         h = C.c_void_p()
-        _check(lib().lc_stage_create(C.byref(desc), _vp(workspace), ws_bytes, max_in_flight,
-                                     C.c_void_p(stream_ptr(stream) or None), C.byref(h)))
+        _check(lib().lc_stage_create_split(C.byref(desc), _vp(workspace), ws_bytes,
+                                           max_in_flight, max_w_pending,
+                                           C.c_void_p(stream_ptr(stream) or None), C.byref(h)))
         self.handle = h
         self.desc = desc
 
@@ -293,8 +327,9 @@ class Stage:
             pass
 
 
-def lc_stage_create(desc, workspace, ws_bytes, max_in_flight, stream=None) -> Stage:
-    return Stage(desc, workspace, ws_bytes, max_in_flight, stream)
+def lc_stage_create(desc, workspace, ws_bytes, max_in_flight, stream=None,
+                    max_w_pending=0) -> Stage:
+    return Stage(desc, workspace, ws_bytes, max_in_flight, stream, max_w_pending)
 
 
 def _mb(mb, x=None, y=None, dy=None, dx=None):
@@ -313,6 +348,20 @@ def chunk_backward(stage: Stage, w, grad, mb, dy, dx, stream=None):
     d = _mb(mb, dy=dy, dx=dx)
     return _check(lib().chunk_backward(stage.handle, C.byref(pb), C.byref(d),
                                        C.c_void_p(stream_ptr(stream) or None)))
+
+
+def chunk_backward_input(stage: Stage, w, mb, dy, dx, stream=None):
+    pb = lc_param_bufs(_vp(w), _vp(None))
+    d = _mb(mb, dy=dy, dx=dx)
+    return _check(lib().chunk_backward_input(stage.handle, C.byref(pb), C.byref(d),
+                                             C.c_void_p(stream_ptr(stream) or None)))
+
+
+def chunk_backward_weight(stage: Stage, w, grad, mb, stream=None):
+    pb = lc_param_bufs(_vp(w), _vp(grad))
+    d = _mb(mb)
+    return _check(lib().chunk_backward_weight(stage.handle, C.byref(pb), C.byref(d),
+                                              C.c_void_p(stream_ptr(stream) or None)))
 
 
 def lc_run_order(stage: Stage, w, grad, entries, xs, ys, dys, dxs, stream=None):

@@ -32,7 +32,8 @@ class StageRunner:
     """One stage on one GPU: weights, gradient bucket, workspace, microbatches."""
 
     def __init__(self, desc: lc.lc_stage_desc, flat_params: np.ndarray, max_in_flight: int,
-                 device="cuda", stream: Optional[torch.cuda.Stream] = None):
+                 device="cuda", stream: Optional[torch.cuda.Stream] = None,
+                 max_w_pending: int = 0):
         require_gpu()
         self.desc = desc
         self.bf16 = desc.compute_dtype == lc.LC_BF16
@@ -43,13 +44,13 @@ class StageRunner:
         assert flat_params.size == self.n_params
         self.w = to_device(flat_params, self.bf16, device)
         self.grad = torch.zeros(self.n_params, dtype=torch.float32, device=device)
-        self.ws_bytes = lc.lc_workspace_bytes(desc, max_in_flight)
+        self.ws_bytes = lc.lc_workspace_bytes(desc, max_in_flight, max_w_pending)
         self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
         base = self.ws.data_ptr()
         self.ws_ptr = (base + 255) // 256 * 256
         self.max_in_flight = max_in_flight
         self.stage = lc.lc_stage_create(desc, self.ws_ptr, self.ws_bytes, max_in_flight,
-                                        self.stream)
+                                        self.stream, max_w_pending)
         self.T = desc.micro_batch * desc.seq_len
         self.master = None
 
@@ -78,6 +79,12 @@ class StageRunner:
     def backward(self, mb: int):
         lc.chunk_backward(self.stage, self.w, self.grad, mb, self.dY[mb], self.dX[mb],
                           self.stream)
+
+    def backward_input(self, mb: int):
+        lc.chunk_backward_input(self.stage, self.w, mb, self.dY[mb], self.dX[mb], self.stream)
+
+    def backward_weight(self, mb: int):
+        lc.chunk_backward_weight(self.stage, self.w, self.grad, mb, self.stream)
 
     def moe_routing(self, mb: int, layer: int) -> np.ndarray:
         """The experts chosen for each token of a stashed microbatch's layer, [T, 2]."""
@@ -121,7 +128,7 @@ class StageRunner:
 
 
 def random_stage(desc: lc.lc_stage_desc, max_in_flight: int, seed: int = 0, device="cuda",
-                 stream=None) -> StageRunner:
+                 stream=None, max_w_pending: int = 0) -> StageRunner:
     """A StageRunner with weights drawn on the device: matrices ~ N(0, 0.02)
     in the compute dtype, RMSNorm gains = 1 (benchmark inputs)."""
     require_gpu()
@@ -146,10 +153,11 @@ def random_stage(desc: lc.lc_stage_desc, max_in_flight: int, seed: int = 0, devi
     r.v = torch.zeros_like(master)
     r.step_count = 0
     r.grad = torch.zeros(r.n_params, dtype=torch.float32, device=device)
-    r.ws_bytes = lc.lc_workspace_bytes(desc, max_in_flight)
+    r.ws_bytes = lc.lc_workspace_bytes(desc, max_in_flight, max_w_pending)
     r.ws = torch.empty(r.ws_bytes + 256, dtype=torch.uint8, device=device)
     r.ws_ptr = (r.ws.data_ptr() + 255) // 256 * 256
     r.max_in_flight = max_in_flight
-    r.stage = lc.lc_stage_create(desc, r.ws_ptr, r.ws_bytes, max_in_flight, r.stream)
+    r.stage = lc.lc_stage_create(desc, r.ws_ptr, r.ws_bytes, max_in_flight, r.stream,
+                                 max_w_pending)
     r.T = desc.micro_batch * desc.seq_len
     return r

@@ -41,8 +41,11 @@ def desc_of(cfg):
                         rope_base=cfg.rope_base)
 
 
+PASS = {"F": lc.LC_PASS_F, "B": lc.LC_PASS_B, "Bi": lc.LC_PASS_BI, "Bw": lc.LC_PASS_BW}
+
+
 def to_c(entries):
-    return [(mb, lc.LC_PASS_F if ps == "F" else lc.LC_PASS_B) for mb, ps in entries]
+    return [(mb, PASS[ps]) for mb, ps in entries]
 
 
 def inputs(cfg, seed=0):
@@ -53,8 +56,9 @@ def inputs(cfg, seed=0):
     return flat, Xs, dYs
 
 
-def gpu_run(cfg, order, flat, Xs, dYs, max_in_flight=None):
-    r = StageRunner(desc_of(cfg), flat, max_in_flight or cfg.num_microbatches)
+def gpu_run(cfg, order, flat, Xs, dYs, max_in_flight=None, max_w_pending=0):
+    r = StageRunner(desc_of(cfg), flat, max_in_flight or cfg.num_microbatches,
+                    max_w_pending=max_w_pending)
     r.alloc_microbatches(Xs, dYs)
     r.run_order(to_c(order))
     torch.cuda.synchronize()
@@ -169,6 +173,84 @@ def test_stage_error_paths_have_no_side_effects():
     r.close()
 
 
+@pytest.mark.parametrize("cfg,tol", [(synth.TINY_FP32, 1e-4), (SMALL_BF16, 2e-2)],
+                         ids=["tiny_fp32", "small_bf16"])
+def test_split_backward_matches_full_backward_and_oracle(cfg, tol):
+    """Bi + Bw (PASS values of Section 4.1): with the Bw entries in
+    microbatch order, adjacent or deferred, every output and the gradient are
+    bit-identical to the plain Order's; Bw in another order changes the
+    gradient by rounding only (checked against the oracle)."""
+    banner(f"split backward {cfg.name}")
+    flat, Xs, dYs = inputs(cfg, seed=6)
+    M, P, s = cfg.num_microbatches, cfg.pp_size, cfg.pp_rank
+    ref = gpu_run(cfg, OO.one_f_one_b(M, P, s), flat, Xs, dYs)
+    for wd in (0, 1, M):
+        order = OO.one_f_one_b_split(M, P, s, wd)
+        r = gpu_run(cfg, order, flat, Xs, dYs, max_w_pending=min(wd + 1, M))
+        print(f"w_delay {wd}: {' '.join(f'{p}{m}' for m, p in order)}", flush=True)
+        assert torch.equal(r.grad, ref.grad), f"w_delay {wd}"
+        for mb in range(M):
+            assert torch.equal(r.Y[mb], ref.Y[mb]) and torch.equal(r.dX[mb], ref.dX[mb])
+        r.close()
+    rev = [(m, "F") for m in range(M)] + [(m, "Bi") for m in range(M)] + \
+          [(m, "Bw") for m in reversed(range(M))]
+    r = gpu_run(cfg, rev, flat, Xs, dYs, max_w_pending=M)
+    _, dXs, G = OS.run_order(cfg, flat, Xs, dYs, rev)
+    errs = per_tensor_errors(cfg, host(r.grad), G)
+    report(errs)
+    assert max(errs.values()) <= tol
+    for mb in range(M):
+        assert torch.equal(r.dX[mb], ref.dX[mb])
+        assert rel_err(host(r.dX[mb]), dXs[mb]) <= tol
+    r.close()
+    ref.close()
+
+
+def test_split_backward_error_paths():
+    cfg = SMALL_BF16
+    banner("split backward error paths")
+    flat, Xs, dYs = inputs(cfg, seed=7)
+    r = StageRunner(desc_of(cfg), flat, 2)  # no weight-pass slots
+    r.alloc_microbatches(Xs, dYs)
+    r.forward(0)
+    with pytest.raises(lc.LibchunkError) as e:
+        r.backward_input(0)
+    assert e.value.status == lc.LC_ERR_STASH_FULL
+    with pytest.raises(lc.LibchunkError) as e:
+        r.run_order(to_c(OO.parse("F0 Bi0 Bw0 F1 B1 F2 B2")))
+    assert e.value.status == lc.LC_ERR_STASH_FULL  # rejected before any launch
+    r.backward(0)
+    r.close()
+    r = StageRunner(desc_of(cfg), flat, 2, max_w_pending=1)
+    r.alloc_microbatches(Xs, dYs)
+    with pytest.raises(lc.LibchunkError) as e:
+        r.backward_input(0)
+    assert e.value.status == lc.LC_ERR_STATE
+    r.forward(0)
+    r.forward(1)
+    with pytest.raises(lc.LibchunkError) as e:
+        r.backward_weight(0)
+    assert e.value.status == lc.LC_ERR_STATE
+    r.backward_input(0)
+    for call in (lambda: r.backward_input(0), lambda: r.backward(0)):
+        with pytest.raises(lc.LibchunkError) as e:
+            call()
+        assert e.value.status == lc.LC_ERR_STATE
+    with pytest.raises(lc.LibchunkError) as e:
+        r.backward_input(1)
+    assert e.value.status == lc.LC_ERR_STASH_FULL  # the one weight slot is taken
+    with pytest.raises(lc.LibchunkError) as e:
+        r.forward(2)
+    assert e.value.status == lc.LC_ERR_STASH_FULL  # microbatch 0 still holds its stash
+    r.backward_weight(0)
+    r.backward(1)
+    with pytest.raises(lc.LibchunkError) as e:
+        r.backward_weight(0)
+    assert e.value.status == lc.LC_ERR_STATE
+    torch.cuda.synchronize()
+    r.close()
+
+
 @pytest.mark.parametrize("cfg,tol", [(synth.STAGE_7B, 2e-2),
                                      (synth.scaled(synth.STAGE_7B, bf16=False), 1e-4)],
                          ids=["stage7b_bf16", "stage7b_fp32"])
@@ -201,3 +283,27 @@ def test_full_size_stage_on_a_prefix(cfg, tol):
     report(errs, 12)
     worst = max(errs, key=errs.get)
     assert errs[worst] <= tol, (worst, errs[worst])
+
+
+def test_full_size_split_backward_is_bit_identical():
+    """The 7B-shaped stage, two microbatches: the split Order (Bi0 Bi1 Bw0
+    Bw1, two weight passes pending) gives the plain Order's dX and gradient
+    bit for bit."""
+    from paper_2606_11169_amd.runner import random_stage
+    cfg = synth.STAGE_7B
+    banner("full-size split backward")
+    got = []
+    for order, wp in ((OO.one_f_one_b(2, 8, 0), 0), (OO.one_f_one_b_split(2, 8, 0, 1), 2)):
+        r = random_stage(desc_of(cfg), 2, seed=1, max_w_pending=wp)
+        r.alloc_random_microbatches(2, seed=2)
+        r.run_order(to_c(order))
+        torch.cuda.synchronize()
+        got.append((r.grad.clone(), [t.clone() for t in r.dX], [t.clone() for t in r.Y]))
+        r.close()
+        del r
+        torch.cuda.empty_cache()
+    (ga, dxa, ya), (gb, dxb, yb) = got
+    assert torch.isfinite(ga).all() and ga.abs().max() > 0
+    assert torch.equal(ga, gb)
+    for mb in range(2):
+        assert torch.equal(dxa[mb], dxb[mb]) and torch.equal(ya[mb], yb[mb])

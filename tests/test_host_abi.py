@@ -80,8 +80,11 @@ def test_1f1b_matches_oracle(M, P, s):
     assert got == want
 
 
+PASS = {"F": lc.LC_PASS_F, "B": lc.LC_PASS_B, "Bi": lc.LC_PASS_BI, "Bw": lc.LC_PASS_BW}
+
+
 def to_c(entries):
-    return [(mb, lc.LC_PASS_F if ps == "F" else lc.LC_PASS_B) for mb, ps in entries]
+    return [(mb, PASS[ps]) for mb, ps in entries]
 
 
 STATUS = {"OK": lc.LC_OK, "BAD_ORDER": lc.LC_ERR_BAD_ORDER, "STASH_FULL": lc.LC_ERR_STASH_FULL}
@@ -114,6 +117,71 @@ def test_validate_matches_oracle_on_fixture_and_random_orders():
         assert st_c == STATUS[st_o], (seq, cap)
         if st_o == "OK":
             assert pk_c == pk_o
+
+
+@pytest.mark.parametrize("M,P,s,wd", [(4, 2, 0, 0), (4, 2, 0, 1), (3, 5, 1, 5), (3, 1, 0, 1),
+                                      (16, 8, 0, 7), (16, 8, 7, 0), (5, 8, 2, 2), (1, 1, 0, 3)])
+def test_1f1b_split_matches_oracle(M, P, s, wd):
+    assert lc.lc_order_1f1b_split(M, P, s, wd) == to_c(OO.one_f_one_b_split(M, P, s, wd))
+
+
+def test_validate_split_matches_oracle_on_rules_and_random_orders():
+    from tests.test_oracle_order import SPLIT_RULES
+    for M, body, status, peak in SPLIT_RULES:
+        st, pk, _ = lc.lc_order_validate_split(to_c(OO.parse(body)), M, M, M)
+        assert st == STATUS[status], body
+        if status == "OK":
+            assert pk == peak
+    rng = np.random.default_rng(1)
+    names = ["F", "B", "Bi", "Bw"]
+    for trial in range(4000):
+        M = int(rng.integers(1, 5))
+        kind = trial % 4
+        if kind == 0:  # a random split choice per microbatch, then shuffled
+            base = []
+            for i in range(M):
+                base += [(i, "F")] + ([(i, "B")] if rng.random() < 0.4 else [(i, "Bi"), (i, "Bw")])
+            seq = [base[i] for i in rng.permutation(len(base))]
+        elif kind == 1:
+            seq = OO.one_f_one_b_split(M, int(rng.integers(1, 6)), 0, int(rng.integers(0, 4)))
+        elif kind == 2:  # a valid Order with one entry's pass or mb changed
+            seq = OO.one_f_one_b_split(M, int(rng.integers(1, 6)), 0, int(rng.integers(0, 4)))
+            i = int(rng.integers(0, len(seq)))
+            if rng.random() < 0.5:
+                seq[i] = (seq[i][0], names[int(rng.integers(0, 4))])
+            else:
+                seq[i] = (int(rng.integers(0, M)), seq[i][1])
+        else:  # random entries
+            n = int(rng.integers(2 * M, 3 * M + 1))
+            seq = [(int(rng.integers(0, M)), names[int(rng.integers(0, 4))]) for _ in range(n)]
+        cap = int(rng.integers(1, M + 2))
+        wcap = int(rng.integers(0, cap + 1))
+        st_o, pk_o = OO.validate(seq, M, cap, max_w_pending=wcap)
+        st_c, pk_c, _ = lc.lc_order_validate_split(to_c(seq), M, cap, wcap)
+        assert st_c == STATUS[st_o], (seq, cap, wcap)
+        if st_o == "OK":
+            assert pk_c == pk_o
+        # the plain validator bounds pending weight passes by the stash only
+        st_p, _ = lc.lc_order_validate(to_c(seq), M, cap)
+        assert st_p == STATUS[OO.validate(seq, M, cap, max_w_pending=cap)[0]]
+
+
+def test_weight_pass_slots_in_the_workspace():
+    d = desc_of(synth.STAGE_7B)
+    w0 = lc.lc_workspace_bytes(d, 8)
+    w2 = lc.lc_workspace_bytes(d, 8, 2)
+    T, D, F, L = 4096, 4096, 11008, 4
+    # per layer: dy, dh [T,d], dgate|dup [T,2f], dq|dk|dv [T,3d] (bf16), two
+    # norm partial-sum blocks (T/16 rows of d fp32)
+    per = L * (2 * (T * D * 2) + T * 2 * F * 2 + T * 3 * D * 2 + 2 * (T // 16) * D * 4)
+    assert 2 * per <= w2 - w0 <= 2 * (per + L * 6 * 256)
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.lc_workspace_bytes(d, 2, 3)
+    assert e.value.status == lc.LC_ERR_INVALID_ARG
+    with pytest.raises(lc.LibchunkError) as e:
+        lc.lc_workspace_bytes(desc_of(synth.MOE_2K), 2, 1)
+    assert e.value.status == lc.LC_ERR_UNSUPPORTED
+    assert lc.lc_workspace_bytes(desc_of(synth.MOE_2K), 2, 0) > 0
 
 
 def test_workspace_grows_with_stash_slots():

@@ -56,3 +56,69 @@ def test_stash_limit():
     assert OO.validate(seq, 16, 7)[0] == "STASH_FULL"
     assert OO.validate(OO.gpipe(4), 4, 3)[0] == "STASH_FULL"
     assert OO.validate(OO.gpipe(4), 4, 4) == ("OK", 4)
+
+
+# Split backwards (PASS values Bi, Bw): 1F1B with every B split, Bw(j) right
+# after Bi(j + w_delay), listed by hand.
+SPLIT_HAND = {
+    (4, 2, 0, 0): "F0 F1 Bi0 Bw0 F2 Bi1 Bw1 F3 Bi2 Bw2 Bi3 Bw3",
+    (4, 2, 0, 1): "F0 F1 Bi0 F2 Bi1 Bw0 F3 Bi2 Bw1 Bi3 Bw2 Bw3",
+    (3, 5, 1, 5): "F0 F1 F2 Bi0 Bi1 Bi2 Bw0 Bw1 Bw2",
+    (3, 1, 0, 1): "F0 Bi0 F1 Bi1 Bw0 F2 Bi2 Bw1 Bw2",
+}
+
+
+@pytest.mark.parametrize("key", sorted(SPLIT_HAND))
+def test_1f1b_split_hand_listed(key):
+    M, P, s, wd = key
+    seq = OO.one_f_one_b_split(M, P, s, wd)
+    assert seq == OO.parse(SPLIT_HAND[key])
+    # removing the Bw entries and renaming Bi to B gives plain 1F1B
+    plain = [(mb, "B" if ps == "Bi" else ps) for mb, ps in seq if ps != "Bw"]
+    assert plain == OO.one_f_one_b(M, P, s)
+    st, pk = OO.validate(seq, M, max_in_flight=M)
+    assert st == "OK"
+    need_w = min(wd + 1, M)
+    assert OO.validate(seq, M, M, max_w_pending=need_w)[0] == "OK"
+    assert OO.validate(seq, M, M, max_w_pending=need_w - 1)[0] == "STASH_FULL"
+
+
+# (M, Order, status, peak in flight when OK), from the rules: one B or one
+# Bi + Bw per microbatch, Bi before Bw, F in order, B and Bi together in
+# order, Bw in any order; a microbatch holds its stash until B or Bw.
+SPLIT_RULES = [
+    (1, "F0 Bi0 Bw0", "OK", 1),
+    (1, "F0 Bw0", "BAD_ORDER", 0),
+    (1, "F0 Bi0", "BAD_ORDER", 0),
+    (1, "F0 Bi0 B0", "BAD_ORDER", 0),
+    (1, "F0 Bw0 Bi0", "BAD_ORDER", 0),
+    (1, "Bi0 F0 Bw0", "BAD_ORDER", 0),
+    (2, "F0 F1 Bi1 Bi0 Bw0 Bw1", "BAD_ORDER", 0),
+    (2, "F0 F1 Bi1 B0 Bw1", "BAD_ORDER", 0),
+    (2, "F0 F1 B0 Bi1 Bw1", "OK", 2),
+    (2, "F0 F1 Bi0 B1 Bw0", "OK", 2),
+    (2, "F0 F1 Bi0 Bi1 Bw1 Bw0", "OK", 2),
+    (2, "F0 Bi0 F1 Bw0 Bi1 Bw1", "OK", 2),
+    (2, "F0 Bi0 Bw0 F1 Bi1 Bw1", "OK", 1),
+    (2, "F0 Bi0 Bi0 F1 Bi1 Bw1", "BAD_ORDER", 0),
+    (2, "F0 F1 Bi0 Bw0 Bw0 B1", "BAD_ORDER", 0),
+]
+
+
+@pytest.mark.parametrize("M,body,status,peak", SPLIT_RULES)
+def test_split_order_rules(M, body, status, peak):
+    st, pk = OO.validate(OO.parse(body), M, max_in_flight=M)
+    assert st == status
+    if status == "OK":
+        assert pk == peak
+
+
+def test_split_pending_weight_passes_hold_the_stash():
+    # Bw(0) after F(1): microbatch 0 still holds its stash, so two slots
+    seq = OO.parse("F0 Bi0 F1 Bw0 Bi1 Bw1")
+    assert OO.validate(seq, 2, 1)[0] == "STASH_FULL"
+    assert OO.validate(OO.parse("F0 Bi0 Bw0 F1 Bi1 Bw1"), 2, 1) == ("OK", 1)
+    # two pending weight passes need two weight slots
+    seq = OO.parse("F0 F1 Bi0 Bi1 Bw0 Bw1")
+    assert OO.validate(seq, 2, 2, max_w_pending=1)[0] == "STASH_FULL"
+    assert OO.validate(seq, 2, 2, max_w_pending=2) == ("OK", 2)

@@ -352,3 +352,31 @@ def test_moe_dispatch_matches_forward_row_order():
         rows, slot = np.nonzero(sel == e)
         assert np.array_equal(perm[off[e]:off[e + 1]], rows)
         assert np.array_equal(rowpos[rows, slot], np.arange(off[e], off[e + 1]))
+
+
+def test_split_backward_gives_the_full_backward():
+    """Bi + Bw computes what B computes (Section 4.1, PASS values Bi, Bw):
+    same dX, and G receives the same per-microbatch gradients; deferring Bw
+    but keeping microbatch order keeps G bit-identical, and any Bw order
+    changes G by rounding only."""
+    cfg = tiny_cfg(micro_batch=1, num_microbatches=4)
+    flat, _, _ = random_inputs(cfg, 4)
+    rng = np.random.default_rng(5)
+    Xs = [rng.standard_normal((1, cfg.seq_len, cfg.d_model)) for _ in range(4)]
+    dYs = [rng.standard_normal((1, cfg.seq_len, cfg.d_model)) for _ in range(4)]
+    full = O.run_order(cfg, flat, Xs, dYs, OO.one_f_one_b(4, 3, 0))
+    for wd in (0, 1, 3):
+        got = O.run_order(cfg, flat, Xs, dYs, OO.one_f_one_b_split(4, 3, 0, wd))
+        assert np.array_equal(got[2], full[2])
+        for i in range(4):
+            assert np.array_equal(got[0][i], full[0][i]) and np.array_equal(got[1][i], full[1][i])
+    rev = OO.parse("F0 F1 F2 F3 Bi0 Bi1 Bi2 Bi3 Bw3 Bw1 Bw2 Bw0")
+    assert OO.validate(rev, 4, 4)[0] == "OK"
+    got = O.run_order(cfg, flat, Xs, dYs, rev)
+    assert np.max(np.abs(got[2] - full[2])) <= 1e-12 * np.max(np.abs(full[2]))
+    mixed = OO.parse("F0 F1 Bi0 B1 F2 F3 Bi2 Bw0 Bi3 Bw3 Bw2")
+    assert OO.validate(mixed, 4, 4)[0] == "OK"
+    got = O.run_order(cfg, flat, Xs, dYs, mixed)
+    assert np.max(np.abs(got[2] - full[2])) <= 1e-12 * np.max(np.abs(full[2]))
+    for i in range(4):
+        assert np.array_equal(got[1][i], full[1][i])

@@ -59,13 +59,20 @@ def desc_of(cfg, lc):
                         rope_base=cfg.rope_base)
 
 
-def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None):
+def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None, overlap=False):
     """Time steps of (zero G, the Order, AdamW over the bucket) on `cfg`;
     returns (ms per step, TFLOP/s, outputs finite). With w_delay set the
-    Order is 1F1B with split backwards (Bi, then Bw w_delay backwards later)."""
+    Order is 1F1B with split backwards (Bi, then Bw w_delay backwards later);
+    with overlap, 1F1B with its steady-state (F, B) pairs nested and run on
+    two streams."""
     from paper_2606_11169_amd.runner import random_stage
     M = cfg.num_microbatches
-    if w_delay is None:
+    aux = None
+    if overlap:
+        order = lc.lc_order_1f1b_overlap(M, cfg.pp_size, cfg.pp_rank)
+        wp = 0
+        aux = torch.cuda.Stream()
+    elif w_delay is None:
         order = lc.lc_order_1f1b(M, cfg.pp_size, cfg.pp_rank)
         wp = 0
     else:
@@ -74,7 +81,8 @@ def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None):
     st, peak, peak_w = lc.lc_order_validate_split(order, M, M, M)
     assert st == lc.LC_OK
     log(f"[bench] {cfg.name}: {M} microbatches, 1F1B(P={cfg.pp_size}, s={cfg.pp_rank})"
-        f"{'' if w_delay is None else f' split, w_delay {w_delay}'}, {peak} in flight, "
+        f"{'' if w_delay is None else f' split, w_delay {w_delay}'}"
+        f"{' with overlapped pairs on two streams' if overlap else ''}, {peak} in flight, "
         f"{peak_w} weight passes pending")
     r = random_stage(desc_of(cfg, lc), peak, seed=0, stream=stream, max_w_pending=wp)
     r.alloc_random_microbatches(M, seed=1)
@@ -82,7 +90,7 @@ def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None):
 
     def step():
         r.zero_grad()
-        r.run_order(order)
+        r.run_order(order, aux)
         r.adam_step(cfg.lr, cfg.beta1, cfg.beta2, cfg.adam_eps, cfg.weight_decay)
 
     for i in range(warmup):
@@ -278,6 +286,9 @@ def main():
     ap.add_argument("--split-only", type=int, default=None, metavar="W_DELAY",
                     help="only the 7B-shaped stage with split backwards (Bw W_DELAY "
                          "backwards after its Bi)")
+    ap.add_argument("--overlap-only", action="store_true",
+                    help="only the 7B-shaped and MoE stages with overlapped (F, B) pairs on "
+                         "two streams")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -308,6 +319,15 @@ def main():
                                           "value": round(stf, 2), "unit": "TFLOP/s",
                                           "ms_per_step": round(sms, 2),
                                           "outputs_finite": sfin}}))
+        return
+    if args.overlap_only:
+        res = {}
+        for c in (cfg, synth.MOE_2K):
+            oms, otf, ofin = time_stage(torch, lc, c, stream, args.steps, args.warmup,
+                                        "overlap", overlap=True)
+            res[c.name] = {"value": round(otf, 2), "unit": "TFLOP/s",
+                           "ms_per_step": round(oms, 2), "outputs_finite": ofin}
+        print(json.dumps({"overlap_stage": res}))
         return
     if args.roofline_only:
         calibration_copy(torch, lc, stream)

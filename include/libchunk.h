@@ -112,7 +112,13 @@ typedef enum lc_tensor_id {
   LC_T_W1 = 5, LC_T_W3 = 6, LC_T_W2 = 7, LC_T_G2 = 8, LC_T_WR = 9
 } lc_tensor_id;
 
-/* One Order entry: run pass `pass` (lc_pass) of microbatch `mb`. */
+/* Flag or-ed into an entry's pass: this entry and the next one form an
+ * overlapped pair (a nested list of two filters in Piper's Order directive,
+ * Section 4.1), which lc_run_order_overlap runs on two streams. */
+enum { LC_ORDER_WITH_NEXT = 0x100 };
+
+/* One Order entry: run pass `pass` (lc_pass, optionally | LC_ORDER_WITH_NEXT)
+ * of microbatch `mb`. */
 typedef struct lc_order_entry {
   int32_t mb;
   int32_t pass;
@@ -131,7 +137,12 @@ typedef struct lc_order_entry {
  *     local gradient accumulator and may come in any order;
  *   - at most max_in_flight microbatches sit between their F and their B
  *     or BW, and at most max_w_pending between their BI and BW (else
- *     LC_ERR_STASH_FULL). */
+ *     LC_ERR_STASH_FULL);
+ *   - an overlapped pair (first entry flagged LC_ORDER_WITH_NEXT) holds two
+ *     entries of different microbatches: F with B, BI or BW, or BI with BW
+ *     (at most one of the two uses the backward's working buffers, at most
+ *     one adds into the gradient). Both may run at once, so the rules above
+ *     are checked with the pair's F (or its BI, beside a BW) first. */
 typedef struct lc_order {
   int32_t num_microbatches;
   int32_t n_entries;
@@ -193,6 +204,12 @@ lc_status lc_param_offset(const lc_stage_desc *desc, int32_t layer, int32_t tens
  * backwards. `out` holds `capacity` entries (needs 2M); *n receives 2M. */
 lc_status lc_order_1f1b(int32_t M, int32_t P, int32_t s, lc_order_entry *out,
                         int32_t capacity, int32_t *n);
+
+/* The 1F1B Order above with every steady-state (F, B) pair flagged as an
+ * overlapped pair (none when W = 0: each pair would be one microbatch's F
+ * and B). Needs 2M entries. */
+lc_status lc_order_1f1b_overlap(int32_t M, int32_t P, int32_t s, lc_order_entry *out,
+                                int32_t capacity, int32_t *n);
 
 /* The 1F1B Order above with every B split into BI then BW: BW(j) is placed
  * right after BI(j + w_delay) (after the last BI when there is none), and
@@ -283,6 +300,24 @@ lc_status chunk_backward_weight(lc_stage *stage, const lc_param_bufs *params,
  * (num_microbatches entries). */
 lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
                        const lc_microbatch_desc *mbs, void *stream);
+
+/* lc_run_order on two streams (Piper Section 4.3.2, worker scheduling loop
+ * and stream management; the overlap of Section 4.1's nested Order): entries
+ * outside pairs and the backward of each overlapped pair (B, or BI beside a
+ * BW) run on `stream`, the pair's other entry on `aux_stream`. Within a pair
+ * the entry with more downstream dependants in the Order is enqueued first
+ * (F before B; BI before BW). A stream waits on the other's hipEvent only
+ * where an entry depends on work last enqueued there: the same microbatch's
+ * earlier pass, the stash or weight-pass slot it takes, the backward's
+ * working buffers, or the gradient bucket. aux_stream first waits for all
+ * work already enqueued on `stream`, and `stream` finally waits for
+ * aux_stream, so the call behaves like one enqueue on `stream`. Outputs and
+ * gradients are identical to lc_run_order's. aux_stream may equal stream
+ * (pairs then run one after the other). The events are host resources of
+ * the stage (created on first use, destroyed by lc_stage_destroy). */
+lc_status lc_run_order_overlap(lc_stage *stage, const lc_param_bufs *params,
+                               const lc_order *order, const lc_microbatch_desc *mbs,
+                               void *stream, void *aux_stream);
 
 /* Routing of a mixture-of-experts stage: copies the two experts chosen for
  * every token of layer `layer` of microbatch `mb` (int32 [micro_batch *

@@ -19,11 +19,22 @@ entries may come in any order (the accumulator receives them in that
 order). A microbatch keeps its stashed activations from F until its B or
 Bw, and its saved output gradients from Bi until its Bw.
 
+An Order may also nest two entries to mark them overlappable (Section 4.1,
+Order: a nested list of filters; the runtime interleaves the two sub-DAGs,
+Section 4.3.1). Reading for one stage: a nested pair holds two entries of
+different microbatches, at most one of which uses the backward's working
+buffers (B, Bi) and at most one of which adds into the gradient accumulator
+(B, Bw): {F, B}, {F, Bi}, {F, Bw} or {Bi, Bw}. As both may run at once, the
+pair takes its stash and weight-pass slots before it frees any: the rules
+are checked on the pair with its acquiring entry (F, Bi) first.
+
 Status values mirror the C library: OK, BAD_ORDER, STASH_FULL.
 """
 from __future__ import annotations
 
-from typing import List, Sequence, Tuple
+from typing import List, Sequence, Tuple, Union
+
+Entry = Tuple[int, str]
 
 OK, BAD_ORDER, STASH_FULL = "OK", "BAD_ORDER", "STASH_FULL"
 
@@ -67,8 +78,47 @@ def one_f_one_b_split(M: int, P: int, s: int, w_delay: int) -> List[Tuple[int, s
     return out
 
 
-def validate(entries: Sequence[Tuple[int, str]], M: int, max_in_flight: int,
-             max_w_pending: int = 1 << 30):
+def one_f_one_b_overlap(M: int, P: int, s: int) -> list:
+    """1F1B with every steady-state (forward of the next microbatch, backward
+    of the oldest) pair nested as an overlapped pair; with no warm-up (W = 0)
+    each such pair is one microbatch's F and B, which cannot overlap, and the
+    Order stays flat."""
+    W = min(P - s - 1, M)
+    out: list = [(i, "F") for i in range(W)]
+    for i in range(M - W):
+        pair = [(W + i, "F"), (i, "B")]
+        if W > 0:
+            out.append(pair)
+        else:
+            out.extend(pair)
+    out.extend((i, "B") for i in range(M - W, M))
+    return out
+
+
+_PAIRS = ({"F", "B"}, {"F", "Bi"}, {"F", "Bw"}, {"Bi", "Bw"})
+
+
+def pair_ok(pair) -> bool:
+    """A nested pair: two entries, different microbatches, an allowed kind."""
+    if len(pair) != 2:
+        return False
+    (m0, p0), (m1, p1) = pair
+    return m0 != m1 and {p0, p1} in _PAIRS
+
+
+def flatten(entries) -> List[Entry]:
+    """The Order as a flat sequence, each nested pair with its acquiring
+    entry (F, Bi) first."""
+    out: List[Entry] = []
+    for e in entries:
+        if isinstance(e, list):
+            out.extend(sorted(e, key=lambda x: 0 if x[1] in ("F", "Bi") else 1))
+        else:
+            out.append(e)
+    return out
+
+
+def validate(entries, M: int, max_in_flight: int, max_w_pending: int = 1 << 30):
     """Check an Order. Returns (status, peak number of stashed microbatches).
 
     Rules: for every 0 <= mb < M, (mb, F) appears once and either (mb, B)
@@ -76,8 +126,13 @@ def validate(entries: Sequence[Tuple[int, str]], M: int, max_in_flight: int,
     and Bi(mb) precedes Bw(mb); F entries are in increasing mb order, and so
     are the B and Bi entries taken together; the number of microbatches
     between their F and their B or Bw never exceeds max_in_flight, nor the
-    number between their Bi and Bw max_w_pending (else STASH_FULL).
+    number between their Bi and Bw max_w_pending (else STASH_FULL). Nested
+    pairs must satisfy pair_ok and are checked in their flatten() order.
     """
+    for e in entries:
+        if isinstance(e, list) and not pair_ok(e):
+            return BAD_ORDER, 0
+    entries = flatten(entries)
     if M <= 0 or not (2 * M <= len(entries) <= 3 * M):
         return BAD_ORDER, 0
     seen = {k: set() for k in ("F", "B", "Bi", "Bw")}
@@ -118,10 +173,20 @@ def validate(entries: Sequence[Tuple[int, str]], M: int, max_in_flight: int,
     return OK, peak
 
 
-def parse(text: str) -> List[Tuple[int, str]]:
-    """'F0 F1 B0 Bi1 Bw1' -> [(0,'F'), (1,'F'), (0,'B'), (1,'Bi'), (1,'Bw')]."""
-    out = []
-    for tok in text.split():
+def parse(text: str) -> list:
+    """'F0 F1 B0 Bi1 Bw1' -> [(0,'F'), (1,'F'), (0,'B'), (1,'Bi'), (1,'Bw')];
+    a bracketed group '[F1 B0]' becomes a nested list [(1,'F'), (0,'B')]."""
+    out: list = []
+    group = None
+    for tok in text.replace("[", " [ ").replace("]", " ] ").split():
+        if tok == "[":
+            group = []
+            continue
+        if tok == "]":
+            out.append(group)
+            group = None
+            continue
         k = 2 if tok[:2] in ("Bi", "Bw") else 1
-        out.append((int(tok[k:]), tok[:k]))
+        e = (int(tok[k:]), tok[:k])
+        (out if group is None else group).append(e)
     return out

@@ -30,6 +30,8 @@ import numpy as np
 
 import synth
 
+from . import order as orders
+
 F64 = np.float64
 
 
@@ -423,7 +425,7 @@ def run_order(cfg, flat_params, Xs: Sequence[np.ndarray], dYs: Sequence[np.ndarr
     stash = {}
     held = {}  # microbatch -> gradient computed by Bi, added by Bw
     G = np.zeros(synth.param_count(cfg), F64)
-    for mb, ps in order:
+    for mb, ps in orders.flatten(order):
         if ps == "F":
             Ys[mb], stash[mb] = stage_forward(cfg, layers, Xs[mb])
         elif ps == "B":

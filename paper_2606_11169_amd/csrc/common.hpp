@@ -21,12 +21,6 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 inline size_t dtype_size(int dt) { return dt == LC_FP32 ? 4 : 2; }
 inline bool valid_dtype(int dt) { return dt == LC_FP32 || dt == LC_BF16 || dt == LC_FP16; }
 
-#define LC_TRY(expr)                 \
-  do {                               \
-    lc_status _st = (expr);          \
-    if (_st != LC_OK) return _st;    \
-  } while (0)
-
 // ------------------------------------------------------------------ types
 typedef uint16_t bf16_t;  // storage of a bfloat16 value (bit-exact paths)
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;     // MFMA operand

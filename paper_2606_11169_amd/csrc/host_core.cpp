@@ -217,6 +217,41 @@ size_t attn_scratch_size(int64_t B, int64_t S, int64_t H) {
   return dbytes + (size_t)(B * S) * 4 * (size_t)H * 128 * 2;
 }
 
+lc_status flatten_order(const lc_order &order, std::vector<lc_order_entry> *flat) {
+  flat->clear();
+  flat->reserve((size_t)order.n_entries);
+  for (int32_t i = 0; i < order.n_entries; ++i) {
+    lc_order_entry e = order.entries[i];
+    if (!(e.pass & LC_ORDER_WITH_NEXT)) {
+      flat->push_back(e);
+      continue;
+    }
+    if (i + 1 >= order.n_entries)
+      return fail(LC_ERR_BAD_ORDER, "entry %d: overlapped with a next entry that does not exist", i);
+    lc_order_entry f = order.entries[i + 1];
+    if (f.pass & LC_ORDER_WITH_NEXT)
+      return fail(LC_ERR_BAD_ORDER, "entries %d-%d: an overlapped group holds two entries", i,
+                  i + 2);
+    e.pass &= ~LC_ORDER_WITH_NEXT;
+    const int a = e.pass, b = f.pass;
+    const bool kinds =
+        (a == LC_PASS_F && (b == LC_PASS_B || b == LC_PASS_BI || b == LC_PASS_BW)) ||
+        (b == LC_PASS_F && (a == LC_PASS_B || a == LC_PASS_BI || a == LC_PASS_BW)) ||
+        (a == LC_PASS_BI && b == LC_PASS_BW) || (a == LC_PASS_BW && b == LC_PASS_BI);
+    if (!kinds || e.mb == f.mb)
+      return fail(LC_ERR_BAD_ORDER,
+                  "entries %d, %d: an overlapped pair is F with B, Bi or Bw, or Bi with Bw, of "
+                  "two different microbatches",
+                  i, i + 1);
+    // the acquiring entry (F, Bi) first
+    if (b == LC_PASS_F || (b == LC_PASS_BI && a == LC_PASS_BW)) std::swap(e, f);
+    flat->push_back(e);
+    flat->push_back(f);
+    ++i;
+  }
+  return LC_OK;
+}
+
 }  // namespace lc
 
 using namespace lc;
@@ -300,6 +335,16 @@ lc_status lc_order_1f1b(int32_t M, int32_t P, int32_t s, lc_order_entry *out, in
   return LC_OK;
 }
 
+lc_status lc_order_1f1b_overlap(int32_t M, int32_t P, int32_t s, lc_order_entry *out,
+                                int32_t capacity, int32_t *n) {
+  LC_TRY(lc_order_1f1b(M, P, s, out, capacity, n));
+  // the steady state: entries W + 2i, W + 2i + 1 for i < M - W
+  const int32_t W = (P - s - 1) < M ? (P - s - 1) : M;
+  // (none without warm-up: each pair would be one microbatch's F and B)
+  for (int32_t i = 0; W > 0 && i < M - W; ++i) out[W + 2 * i].pass |= LC_ORDER_WITH_NEXT;
+  return LC_OK;
+}
+
 lc_status lc_order_1f1b_split(int32_t M, int32_t P, int32_t s, int32_t w_delay,
                               lc_order_entry *out, int32_t capacity, int32_t *n) {
   if (w_delay < 0) return fail(LC_ERR_INVALID_ARG, "w_delay must be >= 0");
@@ -338,13 +383,15 @@ lc_status lc_order_validate_split(const lc_order *order, int32_t max_in_flight,
     return fail(LC_ERR_BAD_ORDER, "an Order over %d microbatches has %d entries, not 2M to 3M", M,
                 order->n_entries);
   if (!order->entries) return fail(LC_ERR_INVALID_ARG, "null entries");
+  std::vector<lc_order_entry> flat;
+  LC_TRY(flatten_order(*order, &flat));
   // seen[mb] bit p: pass p of mb has appeared
   std::vector<uint8_t> seen((size_t)M, 0);
   static const char *const kName[4] = {"F", "B", "Bi", "Bw"};
   int32_t last_f = -1, last_b = -1, live = 0, pk = 0, wlive = 0, pkw = 0;
   lc_status res = LC_OK;
   for (int32_t i = 0; i < order->n_entries && res == LC_OK; ++i) {
-    const lc_order_entry e = order->entries[i];
+    const lc_order_entry e = flat[(size_t)i];
     if (e.mb < 0 || e.mb >= M) {
       res = fail(LC_ERR_BAD_ORDER, "entry %d: microbatch %d out of range", i, e.mb);
       break;

@@ -6,7 +6,15 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "libchunk.h"
+
+#define LC_TRY(expr)                 \
+  do {                               \
+    lc_status _st = (expr);          \
+    if (_st != LC_OK) return _st;    \
+  } while (0)
 
 namespace lc {
 
@@ -19,6 +27,11 @@ size_t attn_scratch_size(int64_t B, int64_t S, int64_t H);
 // Tokens per block of the MoE router weight gradient's partial sums.
 constexpr int kRouterTokensPerBlock = 128;
 size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E);
+
+// An Order's entries as one sequence: the LC_ORDER_WITH_NEXT flag removed
+// and every overlapped pair checked (LC_ERR_BAD_ORDER) and put with its
+// acquiring entry (F, or Bi beside Bw) first.
+lc_status flatten_order(const lc_order &order, std::vector<lc_order_entry> *flat);
 
 // Validates a stage descriptor (shapes, dtype, limits of this build).
 lc_status validate_desc(const lc_stage_desc *d);

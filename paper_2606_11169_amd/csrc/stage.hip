@@ -44,6 +44,7 @@ struct lc_stage {
   std::vector<int32_t> owner;      // microbatch stashed in each slot, -1 if free
   std::vector<const void *> xin0;  // the caller's X of that microbatch
   std::vector<int32_t> wowner;     // microbatch whose weight pass is pending, per weight-pass slot
+  std::vector<hipEvent_t> events;  // cross-stream synchronisation of lc_run_order_overlap
   std::vector<float> rope_host;    // cos table then sin table (fp32)
 };
 
@@ -634,6 +635,8 @@ lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_
 }
 
 lc_status lc_stage_destroy(lc_stage *stage) {
+  if (stage)
+    for (hipEvent_t e : stage->events) hipEventDestroy(e);
   delete stage;
   return LC_OK;
 }
@@ -700,8 +703,141 @@ lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32
   return e == hipSuccess ? LC_OK : hip_fail(e, "copying the routing");
 }
 
-lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
-                       const lc_microbatch_desc *mbs, void *stream) {
+}  // extern "C"
+
+namespace lc {
+namespace {
+
+// Last enqueue that touched a resource: stream index (0 = main, 1 = aux) and
+// the event recorded after it (-1: nothing recorded in this call, i.e.
+// ordered before the call on the main stream).
+struct LastUse {
+  int stream = 0;
+  int ev = -1;
+};
+
+lc_status ensure_events(lc_stage *st, size_t n) {
+  while (st->events.size() < n) {
+    hipEvent_t e;
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+    if (r != hipSuccess) return hip_fail(r, "creating an event");
+    st->events.push_back(e);
+  }
+  return LC_OK;
+}
+
+bool uses_scratch(int pass) { return pass == LC_PASS_B || pass == LC_PASS_BI; }
+bool writes_grad(int pass) { return pass == LC_PASS_B || pass == LC_PASS_BW; }
+
+// Number of later entries of the Order that depend on entry i (the later
+// passes of the same microbatch): the dispatch priority within a pair.
+int downstream(const std::vector<lc_order_entry> &flat, size_t i) {
+  int n = 0;
+  for (size_t j = i + 1; j < flat.size(); ++j) n += flat[j].mb == flat[i].mb;
+  return n;
+}
+
+lc_status run_entries(lc_stage *st, const lc_param_bufs *pb, const lc_order &order,
+                      const lc_microbatch_desc *mbs, hipStream_t s_main, hipStream_t s_aux) {
+  std::vector<lc_order_entry> flat;
+  LC_TRY(flatten_order(order, &flat));
+  const bool two = s_aux != s_main;
+  const hipStream_t strm[2] = {s_main, s_aux};
+  std::vector<LastUse> mb_use((size_t)order.num_microbatches), slot_use((size_t)st->slots),
+      wslot_use(st->wowner.size());
+  LastUse scratch_use, grad_use;
+  int nev = 0;
+  if (two) {
+    LC_TRY(ensure_events(st, flat.size() + 2));
+    // aux starts after everything already enqueued on main (the RoPE upload,
+    // the caller's zeroing of the gradient, ...)
+    hipError_t r = hipEventRecord(st->events[(size_t)nev], s_main);
+    if (r == hipSuccess) r = hipStreamWaitEvent(s_aux, st->events[(size_t)nev], 0);
+    if (r != hipSuccess) return hip_fail(r, "joining the auxiliary stream");
+    ++nev;
+  }
+  // flat keeps each pair's two entries adjacent; walk the original entries to
+  // know which ones are paired
+  size_t fi = 0;
+  for (int32_t i = 0; i < order.n_entries; ++i) {
+    const bool pair = (order.entries[i].pass & LC_ORDER_WITH_NEXT) != 0;
+    size_t idx[2] = {fi, fi + 1};
+    const int n = pair ? 2 : 1;
+    int on[2] = {0, 0};
+    if (pair) {
+      // the backward that uses the working buffers (B, Bi) or, for {Bi, Bw},
+      // the Bi stays on the main stream; the other entry goes to aux
+      const int p0 = flat[fi].pass, p1 = flat[fi + 1].pass;
+      const bool first_main = uses_scratch(p0) || (p0 != LC_PASS_F && p1 == LC_PASS_F);
+      on[0] = first_main ? 0 : 1;
+      on[1] = 1 - on[0];
+      if (downstream(flat, fi + 1) > downstream(flat, fi)) {
+        std::swap(idx[0], idx[1]);
+        std::swap(on[0], on[1]);
+      }
+      ++i;
+    }
+    for (int k = 0; k < n; ++k) {
+      const lc_order_entry e = flat[idx[k]];
+      const int si = two ? on[k] : 0;
+      const lc_microbatch_desc *mb = &mbs[e.mb];
+      int slot = -1, wslot = -1;
+      switch (e.pass) {
+        case LC_PASS_F: slot = find_slot(st, -1); break;
+        case LC_PASS_BI: slot = find_slot(st, e.mb); wslot = find_wslot(st, -1); break;
+        case LC_PASS_BW: slot = find_slot(st, e.mb); wslot = find_wslot(st, e.mb); break;
+        default: slot = find_slot(st, e.mb); break;
+      }
+      if (slot < 0 || (e.pass == LC_PASS_BI || e.pass == LC_PASS_BW) == (wslot < 0))
+        return fail(LC_ERR_STATE, "internal: no slot for entry of microbatch %d", e.mb);
+      if (two) {
+        LastUse *deps[5] = {&mb_use[(size_t)e.mb], &slot_use[(size_t)slot],
+                            wslot >= 0 ? &wslot_use[(size_t)wslot] : nullptr,
+                            uses_scratch(e.pass) ? &scratch_use : nullptr,
+                            writes_grad(e.pass) ? &grad_use : nullptr};
+        int waited[5], nw = 0;
+        for (LastUse *d : deps) {
+          if (!d || d->ev < 0 || d->stream == si) continue;
+          bool dup = false;
+          for (int w = 0; w < nw; ++w) dup |= waited[w] == d->ev;
+          if (dup) continue;
+          hipError_t r = hipStreamWaitEvent(strm[si], st->events[(size_t)d->ev], 0);
+          if (r != hipSuccess) return hip_fail(r, "waiting on the other stream");
+          waited[nw++] = d->ev;
+        }
+      }
+      lc_status r;
+      switch (e.pass) {
+        case LC_PASS_F: r = do_forward(st, pb, mb, strm[si]); break;
+        case LC_PASS_B: r = do_backward(st, pb, mb, strm[si]); break;
+        case LC_PASS_BI: r = do_backward_input(st, pb, mb, strm[si]); break;
+        default: r = do_backward_weight(st, pb, e.mb, strm[si]); break;
+      }
+      if (r != LC_OK) return r;
+      if (two) {
+        hipError_t er = hipEventRecord(st->events[(size_t)nev], strm[si]);
+        if (er != hipSuccess) return hip_fail(er, "recording an event");
+        const LastUse u{si, nev++};
+        mb_use[(size_t)e.mb] = u;
+        slot_use[(size_t)slot] = u;
+        if (wslot >= 0) wslot_use[(size_t)wslot] = u;
+        if (uses_scratch(e.pass)) scratch_use = u;
+        if (writes_grad(e.pass)) grad_use = u;
+      }
+    }
+    fi += (size_t)n;
+  }
+  if (two) {
+    // main continues after everything enqueued on aux
+    hipError_t r = hipEventRecord(st->events[(size_t)nev], s_aux);
+    if (r == hipSuccess) r = hipStreamWaitEvent(s_main, st->events[(size_t)nev], 0);
+    if (r != hipSuccess) return hip_fail(r, "joining the main stream");
+  }
+  return LC_OK;
+}
+
+lc_status check_run(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
+                    const lc_microbatch_desc *mbs) {
   LC_TRY(check_params(stage, params, true));
   LC_TRY(lc_order_validate_split(order, stage->slots, (int32_t)stage->wowner.size(), nullptr,
                                  nullptr));
@@ -715,24 +851,36 @@ lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_or
     if (stage->owner[i] != -1)
       return fail(LC_ERR_STATE, "lc_run_order needs an empty stash (microbatch %d is stashed)",
                   stage->owner[i]);
+  for (size_t i = 0; i < stage->wowner.size(); ++i)
+    if (stage->wowner[i] != -1)
+      return fail(LC_ERR_STATE, "lc_run_order needs no pending weight pass (microbatch %d)",
+                  stage->wowner[i]);
   bool split = false;
-  for (int i = 0; i < order->n_entries; ++i) split |= order->entries[i].pass == LC_PASS_BI;
+  for (int i = 0; i < order->n_entries; ++i)
+    split |= (order->entries[i].pass & ~LC_ORDER_WITH_NEXT) == LC_PASS_BI;
   if (split && stage->d.n_experts > 0)
     return fail(LC_ERR_UNSUPPORTED, "split backward of mixture-of-experts stages");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  for (int i = 0; i < order->n_entries; ++i) {
-    const lc_order_entry e = order->entries[i];
-    const lc_microbatch_desc *mb = &mbs[e.mb];
-    lc_status r;
-    switch (e.pass) {
-      case LC_PASS_F: r = do_forward(stage, params, mb, s); break;
-      case LC_PASS_B: r = do_backward(stage, params, mb, s); break;
-      case LC_PASS_BI: r = do_backward_input(stage, params, mb, s); break;
-      default: r = do_backward_weight(stage, params, e.mb, s); break;
-    }
-    if (r != LC_OK) return r;
-  }
   return LC_OK;
+}
+
+}  // namespace
+}  // namespace lc
+
+extern "C" {
+
+lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
+                       const lc_microbatch_desc *mbs, void *stream) {
+  LC_TRY(check_run(stage, params, order, mbs));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return run_entries(stage, params, *order, mbs, s, s);
+}
+
+lc_status lc_run_order_overlap(lc_stage *stage, const lc_param_bufs *params,
+                               const lc_order *order, const lc_microbatch_desc *mbs,
+                               void *stream, void *aux_stream) {
+  LC_TRY(check_run(stage, params, order, mbs));
+  return run_entries(stage, params, *order, mbs, static_cast<hipStream_t>(stream),
+                     static_cast<hipStream_t>(aux_stream));
 }
 
 }  // extern "C"

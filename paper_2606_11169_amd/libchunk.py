@@ -32,6 +32,7 @@ STATUS_NAMES = {0: "OK", -1: "INVALID_ARG", -2: "UNSUPPORTED", -3: "BAD_ORDER",
 
 LC_FP32, LC_BF16, LC_FP16 = 0, 1, 2
 LC_PASS_F, LC_PASS_B, LC_PASS_BI, LC_PASS_BW = 0, 1, 2, 3
+LC_ORDER_WITH_NEXT = 0x100
 (LC_T_WQ, LC_T_WK, LC_T_WV, LC_T_WO, LC_T_G1, LC_T_W1, LC_T_W3, LC_T_W2, LC_T_G2,
  LC_T_WR) = range(10)
 (LC_EPI_STORE, LC_EPI_STORE_F32, LC_EPI_ACCUM_F32, LC_EPI_RESIDUAL, LC_EPI_ROPE,
@@ -131,6 +132,9 @@ _SIGS = {
                                   C.POINTER(C.c_size_t), C.POINTER(C.c_int64)]),
     "lc_order_1f1b": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.POINTER(lc_order_entry),
                                 C.c_int32, C.POINTER(C.c_int32)]),
+    "lc_order_1f1b_overlap": (C.c_int, [C.c_int32, C.c_int32, C.c_int32,
+                                        C.POINTER(lc_order_entry), C.c_int32,
+                                        C.POINTER(C.c_int32)]),
     "lc_order_1f1b_split": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                       C.POINTER(lc_order_entry), C.c_int32,
                                       C.POINTER(C.c_int32)]),
@@ -156,6 +160,9 @@ _SIGS = {
                                         C.POINTER(lc_microbatch_desc), C.c_void_p]),
     "lc_run_order": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs), C.POINTER(lc_order),
                                C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "lc_run_order_overlap": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
+                                       C.POINTER(lc_order), C.POINTER(lc_microbatch_desc),
+                                       C.c_void_p, C.c_void_p]),
     "chunk_accumulate_grad": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_size_t,
                                         C.c_void_p]),
     "shard_adam_step": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
@@ -249,6 +256,13 @@ def lc_order_1f1b(M, P, s) -> List[Tuple[int, int]]:
     buf = (lc_order_entry * max(1, 2 * M))()
     n = C.c_int32()
     _check(lib().lc_order_1f1b(M, P, s, buf, 2 * M, C.byref(n)))
+    return [(buf[i].mb, buf[i].pass_) for i in range(n.value)]
+
+
+def lc_order_1f1b_overlap(M, P, s) -> List[Tuple[int, int]]:
+    buf = (lc_order_entry * max(1, 2 * M))()
+    n = C.c_int32()
+    _check(lib().lc_order_1f1b_overlap(M, P, s, buf, 2 * M, C.byref(n)))
     return [(buf[i].mb, buf[i].pass_) for i in range(n.value)]
 
 
@@ -364,13 +378,18 @@ def chunk_backward_weight(stage: Stage, w, grad, mb, stream=None):
                                               C.c_void_p(stream_ptr(stream) or None)))
 
 
-def lc_run_order(stage: Stage, w, grad, entries, xs, ys, dys, dxs, stream=None):
+def lc_run_order(stage: Stage, w, grad, entries, xs, ys, dys, dxs, stream=None,
+                 aux_stream=None):
+    """Runs an Order; with aux_stream given, through lc_run_order_overlap."""
     M = len(xs)
     o = make_order(entries, M)
     arr = (lc_microbatch_desc * M)(*[_mb(i, xs[i], ys[i], dys[i], dxs[i]) for i in range(M)])
     pb = lc_param_bufs(_vp(w), _vp(grad))
-    return _check(lib().lc_run_order(stage.handle, C.byref(pb), C.byref(o), arr,
-                                     C.c_void_p(stream_ptr(stream) or None)))
+    s0 = C.c_void_p(stream_ptr(stream) or None)
+    if aux_stream is None:
+        return _check(lib().lc_run_order(stage.handle, C.byref(pb), C.byref(o), arr, s0))
+    return _check(lib().lc_run_order_overlap(stage.handle, C.byref(pb), C.byref(o), arr, s0,
+                                             C.c_void_p(stream_ptr(aux_stream) or None)))
 
 
 # ------------------------------------------------------------------ buffers

@@ -93,9 +93,11 @@ class StageRunner:
         torch.cuda.synchronize()
         return out.cpu().numpy()
 
-    def run_order(self, entries: Sequence[Tuple[int, int]]):
+    def run_order(self, entries: Sequence[Tuple[int, int]], aux_stream=None):
+        """Enqueues an Order on self.stream; overlapped pairs use aux_stream
+        when one is given."""
         lc.lc_run_order(self.stage, self.w, self.grad, entries, self.X, self.Y, self.dY, self.dX,
-                        self.stream)
+                        self.stream, aux_stream)
 
     # -------------------------------------------------------------- optimizer
     def init_optimizer(self, flat_params: np.ndarray):

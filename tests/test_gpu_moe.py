@@ -271,6 +271,33 @@ def test_moe_stage_matches_oracle_with_gpu_routing():
     r.close()
 
 
+def test_moe_overlapped_pair_on_two_streams_is_bit_identical():
+    """A mixture-of-experts stage with its (F1, B0) pair nested and run on two
+    streams gives the flat Order's outputs and gradient bit for bit."""
+    cfg = SMALL_MOE
+    banner(f"moe overlapped pair {cfg.name}")
+    M = cfg.num_microbatches
+    flat = synth.stage_params(cfg, 1)
+    Xs = [synth.activation(cfg, 1, mb, "x") for mb in range(M)]
+    dYs = [synth.activation(cfg, 1, mb, "dy") for mb in range(M)]
+    F, B, NX = lc.LC_PASS_F, lc.LC_PASS_B, lc.LC_ORDER_WITH_NEXT
+    aux = torch.cuda.Stream()
+    runs = []
+    for order, stream in (([(0, F), (1, F), (0, B), (1, B)], None),
+                          ([(0, F), (1, F | NX), (0, B), (1, B)], aux)):
+        r = StageRunner(desc_of(cfg), flat, M)
+        r.alloc_microbatches(Xs, dYs)
+        r.run_order(order, stream)
+        torch.cuda.synchronize()
+        runs.append(r)
+    a, b = runs
+    assert torch.equal(a.grad, b.grad)
+    for mb in range(M):
+        assert torch.equal(a.Y[mb], b.Y[mb]) and torch.equal(a.dX[mb], b.dX[mb])
+    for r in runs:
+        r.close()
+
+
 def test_full_size_moe_stage_on_a_prefix():
     """The MoE workload at full size (4 layers, d 2048, 8 experts x 1408,
     2 x 2048 tokens): outputs and gradients on a 128-token prefix of each

@@ -45,7 +45,16 @@ PASS = {"F": lc.LC_PASS_F, "B": lc.LC_PASS_B, "Bi": lc.LC_PASS_BI, "Bw": lc.LC_P
 
 
 def to_c(entries):
-    return [(mb, PASS[ps]) for mb, ps in entries]
+    """Oracle Order -> C entries; a nested pair's first entry carries
+    LC_ORDER_WITH_NEXT."""
+    out = []
+    for e in entries:
+        if isinstance(e, list):
+            for k, (mb, ps) in enumerate(e):
+                out.append((mb, PASS[ps] | (lc.LC_ORDER_WITH_NEXT if k < len(e) - 1 else 0)))
+        else:
+            out.append((e[0], PASS[e[1]]))
+    return out
 
 
 def inputs(cfg, seed=0):
@@ -56,11 +65,11 @@ def inputs(cfg, seed=0):
     return flat, Xs, dYs
 
 
-def gpu_run(cfg, order, flat, Xs, dYs, max_in_flight=None, max_w_pending=0):
+def gpu_run(cfg, order, flat, Xs, dYs, max_in_flight=None, max_w_pending=0, aux_stream=None):
     r = StageRunner(desc_of(cfg), flat, max_in_flight or cfg.num_microbatches,
                     max_w_pending=max_w_pending)
     r.alloc_microbatches(Xs, dYs)
-    r.run_order(to_c(order))
+    r.run_order(to_c(order), aux_stream)
     torch.cuda.synchronize()
     return r
 
@@ -206,6 +215,39 @@ def test_split_backward_matches_full_backward_and_oracle(cfg, tol):
     ref.close()
 
 
+SPLIT_PAIRS = {
+    3: "F0 [F1 Bi0] [F2 Bw0] Bi1 [Bi2 Bw1] Bw2",
+    4: "F0 [F1 Bi0] [F2 Bw0] [F3 Bi1] [Bi2 Bw1] [Bi3 Bw2] Bw3",
+}
+
+
+@pytest.mark.parametrize("cfg", [synth.TINY_FP32, SMALL_BF16], ids=["tiny_fp32", "small_bf16"])
+def test_overlapped_pairs_on_two_streams_are_bit_identical(cfg):
+    """Nested pairs of the Order (Section 4.1) run on two streams with event
+    waits on cross-stream edges only: 1F1B with its steady-state (F, B)
+    pairs nested, and a split Order with (F, Bi), (F, Bw) and (Bi, Bw)
+    pairs, give the flat 1F1B Order's outputs and gradient bit for bit, on
+    two streams and with both streams the same."""
+    banner(f"overlapped pairs {cfg.name}")
+    flat, Xs, dYs = inputs(cfg, seed=8)
+    M, P, s = cfg.num_microbatches, cfg.pp_size, cfg.pp_rank
+    ref = gpu_run(cfg, OO.one_f_one_b(M, P, s), flat, Xs, dYs)
+    aux = torch.cuda.Stream()
+    cases = [(OO.one_f_one_b_overlap(M, P, s), 0), (OO.parse(SPLIT_PAIRS[M]), 2)]
+    for order, wp in cases:
+        assert OO.validate(order, M, M, max_w_pending=wp or M)[0] == "OK"
+        assert any(isinstance(e, list) for e in order)
+        for stream in (aux, None):
+            r = gpu_run(cfg, order, flat, Xs, dYs, max_w_pending=wp,
+                        aux_stream=stream if stream is not None else torch.cuda.current_stream())
+            torch.cuda.synchronize()
+            assert torch.equal(r.grad, ref.grad), (order, stream)
+            for mb in range(M):
+                assert torch.equal(r.Y[mb], ref.Y[mb]) and torch.equal(r.dX[mb], ref.dX[mb])
+            r.close()
+    ref.close()
+
+
 def test_split_backward_error_paths():
     cfg = SMALL_BF16
     banner("split backward error paths")
@@ -297,6 +339,30 @@ def test_full_size_split_backward_is_bit_identical():
         r = random_stage(desc_of(cfg), 2, seed=1, max_w_pending=wp)
         r.alloc_random_microbatches(2, seed=2)
         r.run_order(to_c(order))
+        torch.cuda.synchronize()
+        got.append((r.grad.clone(), [t.clone() for t in r.dX], [t.clone() for t in r.Y]))
+        r.close()
+        del r
+        torch.cuda.empty_cache()
+    (ga, dxa, ya), (gb, dxb, yb) = got
+    assert torch.isfinite(ga).all() and ga.abs().max() > 0
+    assert torch.equal(ga, gb)
+    for mb in range(2):
+        assert torch.equal(dxa[mb], dxb[mb]) and torch.equal(ya[mb], yb[mb])
+
+
+def test_full_size_overlapped_pair_is_bit_identical():
+    """The 7B-shaped stage: F0 [F1 B0] B1 with the pair on two streams gives
+    the flat Order's dX, Y and gradient bit for bit."""
+    from paper_2606_11169_amd.runner import random_stage
+    cfg = synth.STAGE_7B
+    banner("full-size overlapped pair")
+    got = []
+    aux = torch.cuda.Stream()
+    for order, stream in ((OO.parse("F0 F1 B0 B1"), None), (OO.parse("F0 [F1 B0] B1"), aux)):
+        r = random_stage(desc_of(cfg), 2, seed=1)
+        r.alloc_random_microbatches(2, seed=2)
+        r.run_order(to_c(order), stream)
         torch.cuda.synchronize()
         got.append((r.grad.clone(), [t.clone() for t in r.dX], [t.clone() for t in r.Y]))
         r.close()

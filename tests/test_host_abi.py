@@ -84,7 +84,16 @@ PASS = {"F": lc.LC_PASS_F, "B": lc.LC_PASS_B, "Bi": lc.LC_PASS_BI, "Bw": lc.LC_P
 
 
 def to_c(entries):
-    return [(mb, PASS[ps]) for mb, ps in entries]
+    """Oracle Order -> C entries; a nested pair's first entry carries
+    LC_ORDER_WITH_NEXT."""
+    out = []
+    for e in entries:
+        if isinstance(e, list):
+            for k, (mb, ps) in enumerate(e):
+                out.append((mb, PASS[ps] | (lc.LC_ORDER_WITH_NEXT if k < len(e) - 1 else 0)))
+        else:
+            out.append((e[0], PASS[e[1]]))
+    return out
 
 
 STATUS = {"OK": lc.LC_OK, "BAD_ORDER": lc.LC_ERR_BAD_ORDER, "STASH_FULL": lc.LC_ERR_STASH_FULL}
@@ -164,6 +173,54 @@ def test_validate_split_matches_oracle_on_rules_and_random_orders():
         # the plain validator bounds pending weight passes by the stash only
         st_p, _ = lc.lc_order_validate(to_c(seq), M, cap)
         assert st_p == STATUS[OO.validate(seq, M, cap, max_w_pending=cap)[0]]
+
+
+@pytest.mark.parametrize("M,P,s", [(4, 2, 0), (16, 8, 0), (3, 5, 1), (2, 2, 0), (5, 1, 0),
+                                   (1, 1, 0)])
+def test_1f1b_overlap_matches_oracle(M, P, s):
+    assert lc.lc_order_1f1b_overlap(M, P, s) == to_c(OO.one_f_one_b_overlap(M, P, s))
+
+
+def test_overlapped_pairs_match_oracle():
+    from tests.test_oracle_order import PAIR_RULES
+    for M, body, status, peak in PAIR_RULES:
+        st, pk = lc.lc_order_validate(to_c(OO.parse(body)), M, M)
+        assert st == STATUS[status], body
+        if status == "OK":
+            assert pk == peak
+    # a flagged last entry has no partner
+    F, B, NX = lc.LC_PASS_F, lc.LC_PASS_B, lc.LC_ORDER_WITH_NEXT
+    assert lc.lc_order_validate([(0, F), (0, B | NX)], 1, 1)[0] == lc.LC_ERR_BAD_ORDER
+    assert lc.lc_order_validate([(0, F | 0x200), (0, B)], 1, 1)[0] == lc.LC_ERR_BAD_ORDER
+    rng = np.random.default_rng(2)
+    names = ["F", "B", "Bi", "Bw"]
+    for trial in range(3000):
+        M = int(rng.integers(1, 5))
+        if trial % 2:
+            flat = OO.one_f_one_b_split(M, int(rng.integers(1, 6)), 0, int(rng.integers(0, 4)))
+        else:
+            flat = OO.one_f_one_b(M, int(rng.integers(1, 6)), 0)
+        if trial % 5 == 0 and flat:
+            i = int(rng.integers(0, len(flat)))
+            flat[i] = (int(rng.integers(0, M)), names[int(rng.integers(0, 4))])
+        seq, i = [], 0
+        while i < len(flat):  # nest random adjacent pairs, sometimes swapped
+            if i + 1 < len(flat) and rng.random() < 0.4:
+                pair = [flat[i], flat[i + 1]]
+                if rng.random() < 0.5:
+                    pair.reverse()
+                seq.append(pair)
+                i += 2
+            else:
+                seq.append(flat[i])
+                i += 1
+        cap = int(rng.integers(1, M + 2))
+        wcap = int(rng.integers(0, cap + 1))
+        st_o, pk_o = OO.validate(seq, M, cap, max_w_pending=wcap)
+        st_c, pk_c, _ = lc.lc_order_validate_split(to_c(seq), M, cap, wcap)
+        assert st_c == STATUS[st_o], (seq, cap, wcap)
+        if st_o == "OK":
+            assert pk_c == pk_o
 
 
 def test_weight_pass_slots_in_the_workspace():

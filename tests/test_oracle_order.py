@@ -122,3 +122,49 @@ def test_split_pending_weight_passes_hold_the_stash():
     seq = OO.parse("F0 F1 Bi0 Bi1 Bw0 Bw1")
     assert OO.validate(seq, 2, 2, max_w_pending=1)[0] == "STASH_FULL"
     assert OO.validate(seq, 2, 2, max_w_pending=2) == ("OK", 2)
+
+
+# Overlapped pairs (nested lists in the Order): two entries of different
+# microbatches, F with B/Bi/Bw or Bi with Bw; slots are taken before freed.
+PAIR_RULES = [
+    (2, "F0 [F1 B0] B1", "OK", 2),
+    (2, "F0 [B0 F1] B1", "OK", 2),
+    (2, "[F0 F1] B0 B1", "BAD_ORDER", 0),
+    (2, "F0 F1 [B0 B1]", "BAD_ORDER", 0),
+    (2, "F0 [F1 B1] B0", "BAD_ORDER", 0),
+    (2, "[F0 B0] F1 B1", "BAD_ORDER", 0),
+    (3, "F0 [F1 Bi0] [F2 Bw0] Bi1 Bi2 Bw1 Bw2", "OK", 3),
+    (2, "F0 F1 Bi0 [Bi1 Bw0] Bw1", "OK", 2),
+    (2, "F0 F1 [Bi0 Bw1] Bi1 Bw0", "BAD_ORDER", 0),
+    (2, "F0 F1 [Bi0 Bi1] Bw0 Bw1", "BAD_ORDER", 0),
+    (2, "F0 F1 [B0 Bw1] B1", "BAD_ORDER", 0),
+    (3, "F0 [F1 B0] [F2 B1] B2", "OK", 2),
+    (2, "F0 [F1 B0 B1]", "BAD_ORDER", 0),
+]
+
+
+@pytest.mark.parametrize("M,body,status,peak", PAIR_RULES)
+def test_overlapped_pair_rules(M, body, status, peak):
+    st, pk = OO.validate(OO.parse(body), M, max_in_flight=M)
+    assert st == status
+    if status == "OK":
+        assert pk == peak
+
+
+def test_overlapped_pairs_take_slots_before_freeing():
+    assert OO.validate(OO.parse("F0 B0 F1 B1"), 2, 1) == ("OK", 1)
+    assert OO.validate(OO.parse("F0 [F1 B0] B1"), 2, 1)[0] == "STASH_FULL"
+    seq = OO.parse("F0 F1 Bi0 [Bi1 Bw0] Bw1")
+    assert OO.validate(seq, 2, 2, max_w_pending=1)[0] == "STASH_FULL"
+    assert OO.validate(OO.parse("F0 F1 Bi0 Bw0 Bi1 Bw1"), 2, 2, max_w_pending=1)[0] == "OK"
+
+
+@pytest.mark.parametrize("M,P,s", [(4, 2, 0), (16, 8, 0), (3, 5, 1), (2, 2, 0), (5, 1, 0)])
+def test_1f1b_overlap_nests_the_steady_state(M, P, s):
+    seq = OO.one_f_one_b_overlap(M, P, s)
+    assert OO.flatten(seq) == OO.one_f_one_b(M, P, s)
+    W = min(P - s - 1, M)
+    pairs = [e for e in seq if isinstance(e, list)]
+    assert pairs == ([[(W + i, "F"), (i, "B")] for i in range(M - W)] if W else [])
+    st, pk = OO.validate(seq, M, M)
+    assert st == "OK" and pk == min(P - s, M)

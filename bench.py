@@ -114,6 +114,62 @@ def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None, overlap
     return ms, tflops, finite
 
 
+def time_zero(torch, lc, cfg, stream, steps, warmup, level, ranks=8):
+    """One data-parallel rank's step of the stage under ZeRO-2 or ZeRO-3 on one
+    GPU (rank 0 of `ranks`, collectives left out): zero the gradient shard,
+    the 1F1B Order through lc_run_order_zero (each backward into a temporary
+    full gradient, then its slice added into the shard; at level 3 the bf16
+    weights gathered from `ranks` shards before every entry), AdamW over the
+    shard. Returns (ms per step, TFLOP/s, bytes of persistent gradient +
+    optimizer state on this rank, bytes of the temporary buffers)."""
+    from paper_2606_11169_amd.runner import random_stage
+    M = cfg.num_microbatches
+    order = lc.lc_order_1f1b(M, cfg.pp_size, cfg.pp_rank)
+    r = random_stage(desc_of(cfg, lc), min(cfg.pp_size - cfg.pp_rank, M), seed=0, stream=stream)
+    r.alloc_random_microbatches(M, seed=1)
+    n = r.n_params
+    bounds = [min(n, (n * i // ranks) // 4 * 4) for i in range(ranks)] + [n]
+    off, end = bounds[0], bounds[1]
+    shard = torch.zeros(end - off, dtype=torch.float32, device=r.device)
+    full = torch.empty(n, dtype=torch.float32, device=r.device)
+    master = r.master[off:end].clone()
+    m = torch.zeros_like(master)
+    v = torch.zeros_like(master)
+    w_shards, w_full = (), None
+    if level == 3:
+        w_shards = [r.w[bounds[i]:bounds[i + 1]].clone() for i in range(ranks)]
+        w_full = torch.empty_like(r.w)
+    out = w_shards[0] if level == 3 else r.w[off:end]
+    log(f"[bench] {cfg.name}: ZeRO-{level}, rank 0 of {ranks}: shard of {end - off} elements")
+
+    def step(t):
+        with torch.cuda.stream(stream):
+            shard.zero_()
+        r.run_order_zero(order, level, shard, off, full, w_shards, w_full)
+        lc.shard_adam_step(master, m, v, shard, lc.LC_FP32, out, end - off, cfg.lr, cfg.beta1,
+                           cfg.beta2, cfg.adam_eps, cfg.weight_decay, t, stream)
+
+    for i in range(warmup):
+        step(i + 1)
+        torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(steps):
+        step(warmup + i + 1)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    tflops = stage_flops_per_mb(cfg) * M / (ms * 1e-3) / 1e12
+    persistent = (end - off) * 4 * 4 + (sum(x.numel() for x in w_shards[:1]) * 2 if level == 3
+                                        else n * 2)
+    temporary = n * 4 + (n * 2 if level == 3 else 0)
+    r.close()
+    del r
+    torch.cuda.empty_cache()
+    return ms, tflops, persistent, temporary
+
+
 def time_launches(torch, stream, fns, reps):
     """Per-launch HIP event timing; returns (total ms, launches)."""
     total, count = 0.0, 0
@@ -286,6 +342,8 @@ def main():
     ap.add_argument("--split-only", type=int, default=None, metavar="W_DELAY",
                     help="only the 7B-shaped stage with split backwards (Bw W_DELAY "
                          "backwards after its Bi)")
+    ap.add_argument("--zero-only", action="store_true",
+                    help="only the 7B-shaped stage as rank 0 of 8 under ZeRO-2 and ZeRO-3")
     ap.add_argument("--overlap-only", action="store_true",
                     help="only the 7B-shaped and MoE stages with overlapped (F, B) pairs on "
                          "two streams")
@@ -319,6 +377,17 @@ def main():
                                           "value": round(stf, 2), "unit": "TFLOP/s",
                                           "ms_per_step": round(sms, 2),
                                           "outputs_finite": sfin}}))
+        return
+    if args.zero_only:
+        res = {}
+        for level in (2, 3):
+            zms, ztf, pers, tmp = time_zero(torch, lc, cfg, stream, args.steps, args.warmup,
+                                            level)
+            res[f"zero{level}"] = {"value": round(ztf, 2), "unit": "TFLOP/s",
+                                   "ms_per_step": round(zms, 2),
+                                   "persistent_gib": round(pers / 2**30, 3),
+                                   "temporary_gib": round(tmp / 2**30, 3)}
+        print(json.dumps({"zero_stage": {"workload": cfg.name, "rank": "0 of 8", **res}}))
         return
     if args.overlap_only:
         res = {}

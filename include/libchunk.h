@@ -319,6 +319,43 @@ lc_status lc_run_order_overlap(lc_stage *stage, const lc_param_bufs *params,
                                const lc_order *order, const lc_microbatch_desc *mbs,
                                void *stream, void *aux_stream);
 
+/* ZeRO-2/3 buffers of one data-parallel rank, for lc_run_order_zero (Piper
+ * Section 4.3.2 "Memory management": persistent shard buffers, temporary full
+ * buffers for rematerialised state, a full gradient buffer per backward;
+ * ZeRO-2 and ZeRO-3 of Section 6.2). One GPU has no collectives: the
+ * reduce-scatter after each backward is this rank's share of it (its slice
+ * of the full gradient added into its shard), and the all-gather before
+ * each chunk concatenates weight shards that are all resident here. */
+typedef struct lc_zero_bufs {
+  int32_t level;        /* 2: gradients sharded; 3: gradients and weights */
+  int32_t n_w_shards;   /* level 3: number of weight shards, 1..1024 */
+  float *grad_shard;    /* persistent fp32 gradient shard: bucket elements
+                           [shard_offset, shard_offset + shard_len) */
+  size_t shard_offset;  /* multiple of 4 */
+  size_t shard_len;
+  float *grad_full;     /* temporary fp32 [n_params]: each B / BW's full
+                           gradient, zeroed at its start, reduced at its end */
+  const void *const *w_shards;  /* level 3: host array of n_w_shards device
+                                   pointers (compute dtype), bucket order */
+  const size_t *w_shard_lens;   /* level 3: host array, elements, summing to
+                                   the bucket size */
+  void *w_full;         /* level 3: temporary full weights (compute dtype),
+                           rebuilt from the shards before every entry */
+} lc_zero_bufs;
+
+/* Runs an Order on one stream like lc_run_order, with ZeRO buffers: before
+ * every entry (level 3) the weight shards are gathered into w_full and the
+ * entry reads its weights there (else params->w); every B and BW zeroes
+ * grad_full, adds its gradient there, then adds grad_full's slice
+ * [shard_offset, shard_offset + shard_len) into grad_shard. params->grad is
+ * ignored. grad_shard then holds, bit for bit, that slice of the gradient
+ * lc_run_order accumulates (every addition into +0 is exact). Overlapped
+ * pairs run one after the other. Device buffers 16-byte aligned;
+ * LC_ERR_INVALID_ARG for a bad layout (a slice out of range, shard lengths
+ * that do not sum to the bucket). */
+lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const lc_zero_bufs *zero,
+                            const lc_order *order, const lc_microbatch_desc *mbs, void *stream);
+
 /* Routing of a mixture-of-experts stage: copies the two experts chosen for
  * every token of layer `layer` of microbatch `mb` (int32 [micro_batch *
  * seq_len, 2], the order of lc_moe_route's sel) into the caller's device
@@ -335,6 +372,10 @@ lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32
  * element is read and written exactly once. accum and g must not overlap. */
 lc_status chunk_accumulate_grad(float *accum, const void *g, int32_t g_dtype, size_t n,
                                 void *stream);
+
+/* buf[i] = +0.0f for i < n (a kernel, so that it can be captured in a
+ * graph). buf 16-byte aligned. */
+lc_status lc_zero_fill_f32(float *buf, size_t n, void *stream);
 
 /* AdamW over a flat shard of n elements (decoupled weight decay, bias
  * correction). With host scalars c_wd = 1 - lr*wd, step_size =

@@ -109,15 +109,16 @@ inline unsigned ceil_div(size_t a, size_t b) { return unsigned((a + b - 1) / b);
 // ------------------------------------------------------------------ internal launchers
 // Defined in the kernel translation units; used by the stage composer.
 lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s);
+lc_status zero_fill_launch(float *buf, size_t n, hipStream_t s);
 lc_status rmsnorm_fwd_launch(const lc_norm_args &a, hipStream_t s);
 lc_status rmsnorm_bwd_launch(const lc_norm_args &a, hipStream_t s);
 // The backward's row pass only: dx (and dx_copy) and the gain-gradient
 // partial sums in a.scratch (a.dg_accum is ignored) ...
 lc_status rmsnorm_bwd_partials_launch(const lc_norm_args &a, hipStream_t s);
 // ... and, later, dg[k] += the sum of those partials in the order
-// rmsnorm_bwd_launch uses, for the same T and d.
+// rmsnorm_bwd_launch uses, for the same T and d (dg[k] = the sum if store).
 lc_status rmsnorm_dg_final_launch(const float *partial, float *dg, int64_t T, int64_t d,
-                                  hipStream_t s);
+                                  hipStream_t s, bool store = false);
 lc_status attn_fwd_launch(const lc_attn_args &a, hipStream_t s);
 lc_status attn_bwd_launch(const lc_attn_args &a, hipStream_t s);
 lc_status accumulate_launch(float *acc, const void *g, int g_dtype, size_t n, hipStream_t s);

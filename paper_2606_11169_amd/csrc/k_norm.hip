@@ -29,7 +29,8 @@ struct NormP {
   void *n, *dx, *dx_copy;
   float *rstd;
   float *partial, *dg;
-  int part;  // write the gain-gradient partial sums
+  int part;      // write the gain-gradient partial sums
+  int dg_store;  // the final sum overwrites dg instead of adding into it
   int64_t rows;
   int d;
   float eps;
@@ -250,7 +251,7 @@ __global__ __launch_bounds__(1024) void rmsnorm_dg_final_kernel(NormP p) {
     float tot = sl[0][kc];
 #pragma unroll
     for (int i = 1; i < DG_SLICES; ++i) tot += sl[i][kc];
-    p.dg[k] = p.dg[k] + tot;
+    p.dg[k] = p.dg_store ? tot : p.dg[k] + tot;
   }
 }
 
@@ -350,7 +351,7 @@ lc_status rmsnorm_bwd_partials_launch(const lc_norm_args &a, hipStream_t s) {
 }
 
 lc_status rmsnorm_dg_final_launch(const float *partial, float *dg, int64_t T, int64_t d,
-                                  hipStream_t s) {
+                                  hipStream_t s, bool store) {
   if (!partial || !dg || T <= 0 || d <= 0 || d > INT32_MAX)
     return fail(LC_ERR_INVALID_ARG, "rmsnorm: bad gain-gradient sum arguments");
   NormP p{};
@@ -359,6 +360,7 @@ lc_status rmsnorm_dg_final_launch(const float *partial, float *dg, int64_t T, in
   p.rows = T;
   p.d = (int)d;
   p.nblk = (int)((T + kNormRowsPerBlock - 1) / kNormRowsPerBlock);
+  p.dg_store = store;
   return dg_final(p, s);
 }
 

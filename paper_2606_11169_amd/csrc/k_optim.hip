@@ -70,6 +70,16 @@ __global__ __launch_bounds__(NTH) void accumulate_kernel(float *__restrict__ acc
   }
 }
 
+__global__ __launch_bounds__(NTH) void fill_zero_kernel(float *__restrict__ p, size_t n) {
+  const size_t nv = n / VEC;
+  const size_t i = (size_t)blockIdx.x * NTH + threadIdx.x;
+  if (i < nv) {
+    const float z[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    store8(p + i * VEC, z);
+  }
+  if (blockIdx.x == 0 && threadIdx.x < n - nv * VEC) p[nv * VEC + threadIdx.x] = 0.0f;
+}
+
 struct AdamS {
   float c_wd, b1, b2, omb1, omb2, step_size, bc2s, eps;
 };
@@ -191,6 +201,14 @@ lc_status accumulate_launch(float *acc, const void *g, int g_dtype, size_t n, hi
   return check_launch("accumulate_kernel");
 }
 
+lc_status zero_fill_launch(float *buf, size_t n, hipStream_t s) {
+  if (n == 0) return LC_OK;
+  if (!buf || !aligned16(buf)) return fail(LC_ERR_INVALID_ARG, "zero fill: null or unaligned buffer");
+  LC_TRY(check_n(n, "zero fill"));
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(stream_grid(n)), dim3(NTH), 0, s, buf, n);
+  return check_launch("fill_zero_kernel");
+}
+
 lc_status adam_launch(float *p, float *m, float *v, const void *g, int g_dtype, uint16_t *out,
                       size_t n, const lc_adam_hparams &hp, hipStream_t s) {
   if (n == 0) return LC_OK;
@@ -242,6 +260,10 @@ extern "C" {
 lc_status chunk_accumulate_grad(float *accum, const void *g, int32_t g_dtype, size_t n,
                                 void *stream) {
   return lc::accumulate_launch(accum, g, g_dtype, n, static_cast<hipStream_t>(stream));
+}
+
+lc_status lc_zero_fill_f32(float *buf, size_t n, void *stream) {
+  return lc::zero_fill_launch(buf, n, static_cast<hipStream_t>(stream));
 }
 
 lc_status shard_adam_step(float *master, float *m, float *v, const void *grad, int32_t grad_dtype,

@@ -45,6 +45,7 @@ struct lc_stage {
   std::vector<const void *> xin0;  // the caller's X of that microbatch
   std::vector<int32_t> wowner;     // microbatch whose weight pass is pending, per weight-pass slot
   std::vector<hipEvent_t> events;  // cross-stream synchronisation of lc_run_order_overlap
+  bool grad_store = false;         // backwards overwrite the gradient buffer (ZeRO runs, dense)
   std::vector<float> rope_host;    // cos table then sin table (fp32)
 };
 
@@ -299,6 +300,17 @@ static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const voi
 // Chunk B (wslot < 0), or the backward for the inputs (wslot >= 0: weight
 // products skipped, their operands and the gain partial sums left in weight-
 // pass slot wslot).
+// RMSNorm backward of Chunk B with its gain gradient added into (or, for a
+// stage writing fresh gradients, stored to) dg.
+static lc_status norm_bwd_full(const lc_stage *st, lc_norm_args nb, float *dg, hipStream_t s) {
+  if (!st->grad_store) {
+    nb.dg_accum = dg;
+    return rmsnorm_bwd_launch(nb, s);
+  }
+  LC_TRY(rmsnorm_bwd_partials_launch(nb, s));
+  return rmsnorm_dg_final_launch(static_cast<const float *>(nb.scratch), dg, nb.T, nb.d, s, true);
+}
+
 static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const void *x0,
                                  const void *dy_in, void *dx_out, int slot, int wslot,
                                  hipStream_t s) {
@@ -309,6 +321,8 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
   const StageTypes ty = P.ty;
   const bool copies = ty.op != ty.res;  // bf16 operand copies of fp32 gradients
   const bool split = wslot >= 0;
+  // the weight products overwrite their gradient instead of adding into it
+  const int gepi = st->grad_store ? LC_EPI_STORE_F32 : LC_EPI_ACCUM_F32;
   const int64_t T = P.T, D = d.d_model, F = d.d_ff;
   const size_t ea = dtype_size(ty.att), es = P.elem;
   const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
@@ -358,7 +372,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     LC_TRY(gemm_launch(a, s));
     // G[W2] += dy^T act
     if (!split) {
-      a = gemm_base(dt, LC_EPI_ACCUM_F32, D, F, T);
+      a = gemm_base(dt, gepi, D, F, T);
       a.A = dy_op; a.lda = D; a.a_kmajor = 0;
       a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
       a.C = w.gp(pp.w2); a.ldc = F;
@@ -372,7 +386,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     LC_TRY(gemm_launch(a, s));
     // G[W1; W3] += [dgate | dup]^T n2
     if (!split) {
-      a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * F, D, T);
+      a = gemm_base(dt, gepi, 2 * F, D, T);
       a.A = da; a.lda = 2 * F; a.a_kmajor = 0;
       a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
       a.C = w.gp(pp.w1); a.ldc = D;
@@ -392,9 +406,8 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
       nb.scratch = WL.at(P.w_p2); nb.scratch_bytes = rmsnorm_scratch_size(T, D);
       LC_TRY(rmsnorm_bwd_partials_launch(nb, s));
     } else {
-      nb.dg_accum = w.gp(pp.g2);
       nb.scratch = ws + P.s_norm; nb.scratch_bytes = P.s_norm_bytes;
-      LC_TRY(rmsnorm_bwd_launch(nb, s));
+      LC_TRY(norm_bwd_full(st, nb, w.gp(pp.g2), s));
     }
     // do = dh Wo
     a = gemm_base(dt, LC_EPI_STORE, T, D, D);
@@ -404,7 +417,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     LC_TRY(gemm_launch(a, s));
     // G[Wo] += dh^T o
     if (!split) {
-      a = gemm_base(dt, LC_EPI_ACCUM_F32, D, D, T);
+      a = gemm_base(dt, gepi, D, D, T);
       a.A = dh_op; a.lda = D; a.a_kmajor = 0;
       a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
       a.C = w.gp(pp.wo); a.ldc = D;
@@ -431,7 +444,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     LC_TRY(gemm_launch(a, s));
     // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
     if (!split) {
-      a = gemm_base(dt, LC_EPI_ACCUM_F32, 3 * D, D, T);
+      a = gemm_base(dt, gepi, 3 * D, D, T);
       a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 0;
       a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
       a.C = w.gp(pp.wq); a.ldc = D;
@@ -449,8 +462,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
       nb.scratch = WL.at(P.w_p1); nb.scratch_bytes = rmsnorm_scratch_size(T, D);
       LC_TRY(rmsnorm_bwd_partials_launch(nb, s));
     } else {
-      nb.dg_accum = w.gp(pp.g1);
-      LC_TRY(rmsnorm_bwd_launch(nb, s));
+      LC_TRY(norm_bwd_full(st, nb, w.gp(pp.g1), s));
     }
     dy_res = dx;
     dy_op = copies ? dy_next_op : dx;
@@ -469,37 +481,40 @@ static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, 
   const ParamPlan &pp = st->pp;
   const int dt = d.compute_dtype;
   const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const int gepi = st->grad_store ? LC_EPI_STORE_F32 : LC_EPI_ACCUM_F32;
   for (int l = d.n_layers - 1; l >= 0; --l) {
     const LayerBufs L = layer_bufs(st, slot, l);
     const LayerBufs WL = wlayer_bufs(st, wslot, l);
     const size_t lw = (size_t)l * pp.per_layer;
     const W w{static_cast<const char *>(pb->w) + lw * P.elem, pb->grad + lw, P.elem};
     // G[W2] += dy^T act
-    lc_gemm_args a = gemm_base(dt, LC_EPI_ACCUM_F32, D, F, T);
+    lc_gemm_args a = gemm_base(dt, gepi, D, F, T);
     a.A = WL.at(P.w_dy); a.lda = D; a.a_kmajor = 0;
     a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
     a.C = w.gp(pp.w2); a.ldc = F;
     LC_TRY(gemm_launch(a, s));
     // G[W1; W3] += [dgate | dup]^T n2
-    a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * F, D, T);
+    a = gemm_base(dt, gepi, 2 * F, D, T);
     a.A = WL.at(P.w_da); a.lda = 2 * F; a.a_kmajor = 0;
     a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.w1); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
-    LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p2)), w.gp(pp.g2), T, D, s));
+    LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p2)), w.gp(pp.g2), T, D, s,
+                                   st->grad_store));
     // G[Wo] += dh^T o
-    a = gemm_base(dt, LC_EPI_ACCUM_F32, D, D, T);
+    a = gemm_base(dt, gepi, D, D, T);
     a.A = WL.at(P.w_dh); a.lda = D; a.a_kmajor = 0;
     a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.wo); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
     // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
-    a = gemm_base(dt, LC_EPI_ACCUM_F32, 3 * D, D, T);
+    a = gemm_base(dt, gepi, 3 * D, D, T);
     a.A = WL.at(P.w_dqkv); a.lda = 3 * D; a.a_kmajor = 0;
     a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.wq); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
-    LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p1)), w.gp(pp.g1), T, D, s));
+    LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p1)), w.gp(pp.g1), T, D, s,
+                                   st->grad_store));
   }
   return LC_OK;
 }
@@ -737,8 +752,29 @@ int downstream(const std::vector<lc_order_entry> &flat, size_t i) {
   return n;
 }
 
-lc_status run_entries(lc_stage *st, const lc_param_bufs *pb, const lc_order &order,
-                      const lc_microbatch_desc *mbs, hipStream_t s_main, hipStream_t s_aux) {
+// ZeRO-3: the weight shards concatenated into the temporary full buffer.
+lc_status gather_weights(const lc_stage *st, const lc_zero_bufs &z, hipStream_t s) {
+  char *dst = static_cast<char *>(z.w_full);
+  for (int i = 0; i < z.n_w_shards; ++i) {
+    const size_t bytes = z.w_shard_lens[i] * st->plan.elem;
+    if (bytes) {
+      hipError_t e = hipMemcpyAsync(dst, z.w_shards[i], bytes, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return hip_fail(e, "gathering the weight shards");
+    }
+    dst += bytes;
+  }
+  return LC_OK;
+}
+
+lc_status run_entries(lc_stage *st, const lc_param_bufs *pb_in, const lc_order &order,
+                      const lc_microbatch_desc *mbs, hipStream_t s_main, hipStream_t s_aux,
+                      const lc_zero_bufs *z = nullptr) {
+  lc_param_bufs zb = *pb_in;
+  if (z) {
+    zb.grad = z->grad_full;
+    if (z->level == 3) zb.w = z->w_full;
+  }
+  const lc_param_bufs *pb = &zb;
   std::vector<lc_order_entry> flat;
   LC_TRY(flatten_order(order, &flat));
   const bool two = s_aux != s_main;
@@ -806,6 +842,13 @@ lc_status run_entries(lc_stage *st, const lc_param_bufs *pb, const lc_order &ord
           waited[nw++] = d->ev;
         }
       }
+      if (z && z->level == 3) LC_TRY(gather_weights(st, *z, strm[si]));
+      // a dense stage's backward writes every gradient element once, so it
+      // stores into the temporary gradient; a mixture-of-experts stage adds
+      // into a zeroed one (an expert may receive no rows)
+      if (z && writes_grad(e.pass) && st->d.n_experts > 0)
+        LC_TRY(zero_fill_launch(z->grad_full, st->pp.total, strm[si]));
+      st->grad_store = z && st->d.n_experts == 0;
       lc_status r;
       switch (e.pass) {
         case LC_PASS_F: r = do_forward(st, pb, mb, strm[si]); break;
@@ -813,7 +856,12 @@ lc_status run_entries(lc_stage *st, const lc_param_bufs *pb, const lc_order &ord
         case LC_PASS_BI: r = do_backward_input(st, pb, mb, strm[si]); break;
         default: r = do_backward_weight(st, pb, e.mb, strm[si]); break;
       }
+      st->grad_store = false;
       if (r != LC_OK) return r;
+      // this rank's share of the reduce-scatter
+      if (z && writes_grad(e.pass))
+        LC_TRY(accumulate_launch(z->grad_shard, z->grad_full + z->shard_offset, LC_FP32,
+                                 z->shard_len, strm[si]));
       if (two) {
         hipError_t er = hipEventRecord(st->events[(size_t)nev], strm[si]);
         if (er != hipSuccess) return hip_fail(er, "recording an event");
@@ -873,6 +921,41 @@ lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_or
   LC_TRY(check_run(stage, params, order, mbs));
   hipStream_t s = static_cast<hipStream_t>(stream);
   return run_entries(stage, params, *order, mbs, s, s);
+}
+
+lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const lc_zero_bufs *zero,
+                            const lc_order *order, const lc_microbatch_desc *mbs, void *stream) {
+  if (!zero) return fail(LC_ERR_INVALID_ARG, "null ZeRO buffers");
+  if (!params) return fail(LC_ERR_INVALID_ARG, "null parameter buffers");
+  const lc_zero_bufs &z = *zero;
+  if (z.level != 2 && z.level != 3) return fail(LC_ERR_INVALID_ARG, "ZeRO level must be 2 or 3");
+  if (!stage) return fail(LC_ERR_INVALID_ARG, "null stage");
+  const size_t n = stage->pp.total;
+  if (!z.grad_shard || !z.grad_full || !aligned16(z.grad_shard) || !aligned16(z.grad_full))
+    return fail(LC_ERR_INVALID_ARG, "ZeRO gradient buffers must be non-null and 16-byte aligned");
+  if (z.shard_offset % 4 || z.shard_offset > n || z.shard_len > n - z.shard_offset)
+    return fail(LC_ERR_INVALID_ARG, "gradient shard [%zu, +%zu) is not a 4-aligned slice of %zu",
+                z.shard_offset, z.shard_len, n);
+  lc_param_bufs pb = *params;
+  pb.grad = z.grad_full;
+  if (z.level == 3) {
+    if (z.n_w_shards < 1 || z.n_w_shards > 1024 || !z.w_shards || !z.w_shard_lens)
+      return fail(LC_ERR_INVALID_ARG, "ZeRO-3 needs 1..1024 weight shards");
+    if (!z.w_full || !aligned16(z.w_full))
+      return fail(LC_ERR_INVALID_ARG, "ZeRO-3 temporary weights must be non-null and 16-byte aligned");
+    size_t tot = 0;
+    for (int i = 0; i < z.n_w_shards; ++i) {
+      if (!z.w_shards[i] && z.w_shard_lens[i])
+        return fail(LC_ERR_INVALID_ARG, "weight shard %d is null", i);
+      tot += z.w_shard_lens[i];
+    }
+    if (tot != n)
+      return fail(LC_ERR_INVALID_ARG, "weight shards hold %zu elements, the bucket %zu", tot, n);
+    pb.w = z.w_full;
+  }
+  LC_TRY(check_run(stage, &pb, order, mbs));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return run_entries(stage, params, *order, mbs, s, s, zero);
 }
 
 lc_status lc_run_order_overlap(lc_stage *stage, const lc_param_bufs *params,

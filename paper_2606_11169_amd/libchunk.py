@@ -72,6 +72,13 @@ class lc_param_bufs(C.Structure):
     _fields_ = [("w", C.c_void_p), ("grad", C.c_void_p)]
 
 
+class lc_zero_bufs(C.Structure):
+    _fields_ = [("level", C.c_int32), ("n_w_shards", C.c_int32), ("grad_shard", C.c_void_p),
+                ("shard_offset", C.c_size_t), ("shard_len", C.c_size_t),
+                ("grad_full", C.c_void_p), ("w_shards", C.POINTER(C.c_void_p)),
+                ("w_shard_lens", C.POINTER(C.c_size_t)), ("w_full", C.c_void_p)]
+
+
 class lc_adam_hparams(C.Structure):
     _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float),
                 ("eps", C.c_float), ("weight_decay", C.c_float), ("reserved", C.c_int32),
@@ -160,6 +167,10 @@ _SIGS = {
                                         C.POINTER(lc_microbatch_desc), C.c_void_p]),
     "lc_run_order": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs), C.POINTER(lc_order),
                                C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "lc_run_order_zero": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
+                                    C.POINTER(lc_zero_bufs), C.POINTER(lc_order),
+                                    C.POINTER(lc_microbatch_desc), C.c_void_p]),
+    "lc_zero_fill_f32": (C.c_int, [C.c_void_p, C.c_size_t, C.c_void_p]),
     "lc_run_order_overlap": (C.c_int, [C.c_void_p, C.POINTER(lc_param_bufs),
                                        C.POINTER(lc_order), C.POINTER(lc_microbatch_desc),
                                        C.c_void_p, C.c_void_p]),
@@ -390,6 +401,36 @@ def lc_run_order(stage: Stage, w, grad, entries, xs, ys, dys, dxs, stream=None,
         return _check(lib().lc_run_order(stage.handle, C.byref(pb), C.byref(o), arr, s0))
     return _check(lib().lc_run_order_overlap(stage.handle, C.byref(pb), C.byref(o), arr, s0,
                                              C.c_void_p(stream_ptr(aux_stream) or None)))
+
+
+def lc_run_order_zero(stage: Stage, w, level, grad_shard, shard_offset, shard_len, grad_full,
+                      entries, xs, ys, dys, dxs, w_shards=(), w_full=None, stream=None):
+    """lc_run_order with ZeRO-2/3 buffers (w_shards: device tensors or
+    addresses, in bucket order, with their element counts taken from
+    .numel() for tensors, or (address, count) pairs)."""
+    M = len(xs)
+    o = make_order(entries, M)
+    arr = (lc_microbatch_desc * M)(*[_mb(i, xs[i], ys[i], dys[i], dxs[i]) for i in range(M)])
+    pb = lc_param_bufs(_vp(w), None)
+    ptrs, lens = [], []
+    for sh in w_shards:
+        if isinstance(sh, tuple):
+            ptrs.append(ptr(sh[0]))
+            lens.append(int(sh[1]))
+        else:
+            ptrs.append(ptr(sh))
+            lens.append(int(sh.numel()))
+    pa = (C.c_void_p * max(1, len(ptrs)))(*[p or None for p in ptrs])
+    la = (C.c_size_t * max(1, len(lens)))(*lens)
+    z = lc_zero_bufs(level, len(ptrs), _vp(grad_shard), shard_offset, shard_len, _vp(grad_full),
+                     C.cast(pa, C.POINTER(C.c_void_p)), C.cast(la, C.POINTER(C.c_size_t)),
+                     _vp(w_full))
+    return _check(lib().lc_run_order_zero(stage.handle, C.byref(pb), C.byref(z), C.byref(o), arr,
+                                          C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_zero_fill_f32(buf, n, stream=None):
+    return _check(lib().lc_zero_fill_f32(_vp(buf), n, C.c_void_p(stream_ptr(stream) or None)))
 
 
 # ------------------------------------------------------------------ buffers

@@ -99,6 +99,17 @@ class StageRunner:
         lc.lc_run_order(self.stage, self.w, self.grad, entries, self.X, self.Y, self.dY, self.dX,
                         self.stream, aux_stream)
 
+    def run_order_zero(self, entries, level, grad_shard, shard_offset, grad_full,
+                       w_shards=(), w_full=None):
+        """Enqueues an Order with ZeRO-2 (level 2) or ZeRO-3 (level 3)
+        buffers: each backward's full gradient goes to grad_full and its
+        slice [shard_offset, shard_offset + grad_shard.numel()) is added into
+        grad_shard; at level 3 the weights are gathered from w_shards into
+        w_full before every entry."""
+        lc.lc_run_order_zero(self.stage, self.w, level, grad_shard, shard_offset,
+                             grad_shard.numel(), grad_full, entries, self.X, self.Y, self.dY,
+                             self.dX, w_shards, w_full, self.stream)
+
     # -------------------------------------------------------------- optimizer
     def init_optimizer(self, flat_params: np.ndarray):
         """fp32 master weights and zero Adam moments. An fp32 stage's compute

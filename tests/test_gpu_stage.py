@@ -248,6 +248,59 @@ def test_overlapped_pairs_on_two_streams_are_bit_identical(cfg):
     ref.close()
 
 
+@pytest.mark.parametrize("cfg", [synth.TINY_FP32, SMALL_BF16], ids=["tiny_fp32", "small_bf16"])
+def test_zero_paths_give_the_accumulated_gradient_slices(cfg):
+    """ZeRO-2/3 on one GPU (each backward into a temporary full gradient,
+    then this rank's slice added into its persistent shard; at level 3 the
+    weights gathered from shards before every entry): for each of three
+    ranks' shards, the shard equals its slice of the plain Order's gradient
+    bit for bit, and Y, dX are unchanged; also with split backwards."""
+    banner(f"zero paths {cfg.name}")
+    flat, Xs, dYs = inputs(cfg, seed=9)
+    M, P, s = cfg.num_microbatches, cfg.pp_size, cfg.pp_rank
+    ref = gpu_run(cfg, OO.one_f_one_b(M, P, s), flat, Xs, dYs)
+    n = ref.n_params
+    bounds = [0, (n // 3) // 4 * 4, (2 * n // 3) // 4 * 4 + 4, n]
+    orders = [(OO.one_f_one_b(M, P, s), 0), (OO.one_f_one_b_split(M, P, s, 1), 2)]
+    for level in (2, 3):
+        for order, wp in orders:
+            for rank in range(3):
+                off, end = bounds[rank], bounds[rank + 1]
+                r = StageRunner(desc_of(cfg), flat, M, max_w_pending=wp)
+                r.alloc_microbatches(Xs, dYs)
+                shard = torch.zeros(end - off, dtype=torch.float32, device="cuda")
+                full = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+                w_shards, w_full = (), None
+                if level == 3:
+                    w_shards = [r.w[bounds[i]:bounds[i + 1]].clone() for i in range(3)]
+                    w_full = torch.full_like(r.w, float("nan"))
+                    r.w.fill_(float("nan"))  # ignored at level 3
+                r.run_order_zero(to_c(order), level, shard, off, full, w_shards, w_full)
+                torch.cuda.synchronize()
+                assert torch.equal(shard, ref.grad[off:end]), (level, rank, wp)
+                assert torch.all(r.grad == 0)  # params->grad is not touched
+                for mb in range(M):
+                    assert torch.equal(r.Y[mb], ref.Y[mb]) and torch.equal(r.dX[mb], ref.dX[mb])
+                r.close()
+    # bad layouts are rejected before anything is enqueued
+    r = StageRunner(desc_of(cfg), flat, M)
+    r.alloc_microbatches(Xs, dYs)
+    shard = torch.zeros(8, dtype=torch.float32, device="cuda")
+    full = torch.zeros(n, dtype=torch.float32, device="cuda")
+    order = to_c(OO.one_f_one_b(M, P, s))
+    for bad in (dict(level=2, grad_shard=shard, shard_offset=2),
+                dict(level=2, grad_shard=shard, shard_offset=n - 4),
+                dict(level=4, grad_shard=shard, shard_offset=0),
+                dict(level=3, grad_shard=shard, shard_offset=0,
+                     w_shards=[r.w[:n // 2]], w_full=torch.empty_like(r.w))):
+        with pytest.raises(lc.LibchunkError) as e:
+            r.run_order_zero(order, bad["level"], bad["grad_shard"], bad["shard_offset"], full,
+                             bad.get("w_shards", ()), bad.get("w_full"))
+        assert e.value.status == lc.LC_ERR_INVALID_ARG
+    r.close()
+    ref.close()
+
+
 def test_split_backward_error_paths():
     cfg = SMALL_BF16
     banner("split backward error paths")

@@ -69,6 +69,11 @@ typedef enum lc_pass { LC_PASS_F = 0, LC_PASS_B = 1, LC_PASS_BI = 2, LC_PASS_BW 
  *   on q and k (positions 0..seq_len-1 per sequence, angle p*base^(-2i/hd));
  *   o = causal softmax(q k^T / sqrt(hd)) v per head; h = x + o Wo^T;
  *   n2 = RMSNorm(h; g2); y = h + FFN(n2)
+ * Qwen3-style variant: with qk_norm, q and k are RMS-normalised over each
+ * head's head_dim values (gains qn, kn [head_dim], epsilon rms_eps) before
+ * RoPE; with 0 < n_kv_heads < n_heads (grouped-query attention) k and v
+ * have n_kv_heads heads (Wk, Wv are [n_kv_heads*head_dim, d]) and query
+ * head h uses key/value head h / (n_heads / n_kv_heads).
  * with FFN the SwiGLU (silu(n2 W1^T) * (n2 W3^T)) W2^T when n_experts == 0,
  * else a top-k (k = 2) softmax-routed mixture of SwiGLU experts whose gate
  * weights are renormalised over the selected experts (ties pick the lower
@@ -100,16 +105,20 @@ typedef struct lc_stage_desc {
   int32_t causal;        /* must be 1 */
   int32_t compute_dtype; /* lc_dtype of weights and activations; gradients
                             are always accumulated in fp32 */
+  int32_t n_kv_heads;    /* key/value heads; 0 = n_heads; divides n_heads */
+  int32_t qk_norm;       /* 1: per-head RMSNorm of q and k before RoPE */
 } lc_stage_desc;
 
 /* Tensor ids of the canonical flat layout (one bucket per stage). Per layer,
- * in this order: WQ, WK, WV, WO [d,d]; G1 [d]; dense: W1 (gate) [f,d],
+ * in this order: WQ [d,d], WK, WV [n_kv_heads*head_dim, d], WO [d,d]; G1
+ * [d]; with qk_norm QN, KN [head_dim]; dense: W1 (gate) [f,d],
  * W3 (up) [f,d], W2 (down) [d,f]; MoE: WR (router) [E,d], then for each
  * expert e: W1 [fe,d], W3 [fe,d], W2 [d,fe]; finally G2 [d]. The gradient,
  * master, m and v buffers use the same layout. */
 typedef enum lc_tensor_id {
   LC_T_WQ = 0, LC_T_WK = 1, LC_T_WV = 2, LC_T_WO = 3, LC_T_G1 = 4,
-  LC_T_W1 = 5, LC_T_W3 = 6, LC_T_W2 = 7, LC_T_G2 = 8, LC_T_WR = 9
+  LC_T_W1 = 5, LC_T_W3 = 6, LC_T_W2 = 7, LC_T_G2 = 8, LC_T_WR = 9,
+  LC_T_QN = 10, LC_T_KN = 11
 } lc_tensor_id;
 
 /* Flag or-ed into an entry's pass: this entry and the next one form an

@@ -146,7 +146,10 @@ size_t lc_rmsnorm_scratch_bytes(int64_t T, int64_t d);
  * lse[b,h,i] = log sum_{j<=i} exp(q_i.k_j / sqrt(hd)) (fp32 [B, H, S]).
  * q, k, v, o are [B, S, H*hd] row blocks: element (b, s, h, e) of q sits at
  * q[(b*S + s)*ld_qkv + h*hd + e] (likewise k, v with ld_qkv, o and dout
- * with ld_o, dq, dk, dv with ld_dqkv).
+ * with ld_o, dq, dk, dv with ld_dqkv). Grouped-query attention: with
+ * 0 < Hkv < H, k, v, dk, dv have Hkv heads and query head h uses key/value
+ * head h / (H / Hkv); dk and dv sum over the query heads of their group
+ * (in head order). Hkv = 0 means H.
  * Backward, given dout and P recomputed from lse:
  *   D_i = sum_e dout_ie o_ie, dv_j = sum_i P_ij dout_i,
  *   dS_ij = P_ij (dout_i.v_j - D_i), dq_i = sum_j dS_ij k_j / sqrt(hd),
@@ -170,11 +173,52 @@ typedef struct lc_attn_args {
   const void *dout; void *dq; void *dk; void *dv; int64_t ld_dqkv;
   const float *rope_cos; const float *rope_sin;
   void *scratch; size_t scratch_bytes;
+  int32_t Hkv;         /* key/value heads (0 = H); divides H */
+  int32_t reserved;
 } lc_attn_args;
 
 lc_status lc_attention_forward(const lc_attn_args *args, void *stream);
 lc_status lc_attention_backward(const lc_attn_args *args, void *stream);
 size_t lc_attention_scratch_bytes(int32_t B, int32_t S, int32_t H);
+/* The backward's scratch with Hkv key/value heads (grouped-query attention). */
+size_t lc_attention_scratch_bytes_kv(int32_t B, int32_t S, int32_t H, int32_t Hkv);
+
+/* ------------------------------------------------------------------ q/k norm
+ * Qwen3-style per-head RMSNorm of q and k fused with RoPE, over T tokens of
+ * a packed row qk[t] = [q heads 0..H-1 | k heads 0..Hkv-1] (hd values each,
+ * row stride ld): for every head row x (hd values),
+ *   r = 1/sqrt(mean(x^2) + eps), y = x * r * g   (g = gq for q, gk for k),
+ * then rotate-half RoPE on y at position t % seq_len (angles as in the
+ * stage: the fp32 tables cos, sin [seq_len, hd/2]).
+ * Forward: reads raw x from qk (dtype x_dtype: LC_FP16 or LC_FP32), writes
+ * the rotated y back in place, a copy of the raw rows to raw ([T, (H+Hkv)*hd],
+ * same dtype) and r to rstd ([T, H+Hkv] fp32).
+ * Backward: dqk holds the gradient with respect to y (attention's backward
+ * has already undone the rotation) (dtype d_dtype:
+ * LC_BF16 or LC_FP32, row stride ld_d); overwrites it in place with the
+ * gradient with respect to x (xh = x*r, dxh = dy*g:
+ * dx = r*(dxh - xh*mean(dxh*xh))), and adds sum over rows of dy*xh into
+ * dgq / dgk (fp32 [hd]; stored instead when store_dg is 1). The gain sums
+ * are deterministic: per-block partials in scratch
+ * (lc_qk_norm_scratch_bytes), then one ordered sum. hd in {16, 32, 64,
+ * 128}; g in w_dtype. */
+typedef struct lc_qknorm_args {
+  int64_t T;
+  int32_t H, Hkv, hd, seq_len;
+  float eps;
+  int32_t x_dtype, w_dtype, d_dtype;
+  void *qk; int64_t ld;
+  void *raw; float *rstd;
+  const void *gq; const void *gk;
+  const float *rope_cos; const float *rope_sin;
+  void *dqk; int64_t ld_d;
+  float *dgq; float *dgk; int32_t store_dg; int32_t reserved;
+  void *scratch; size_t scratch_bytes;
+} lc_qknorm_args;
+
+lc_status lc_qk_norm_rope_forward(const lc_qknorm_args *args, void *stream);
+lc_status lc_qk_norm_rope_backward(const lc_qknorm_args *args, void *stream);
+size_t lc_qk_norm_scratch_bytes(int64_t T, int32_t hd);
 
 /* ------------------------------------------------------------------ MoE routing
  * Router and dispatch of a top-2 mixture-of-experts FFN over T tokens of d

@@ -8,8 +8,11 @@ standard pre-norm decoder block, written from the textbook definitions:
 
   n1 = RMSNorm(x; g1)                      rstd = 1/sqrt(mean(x^2) + eps)
   q, k, v = n1 Wq^T, n1 Wk^T, n1 Wv^T      heads use contiguous column blocks
+  [Qwen3 variant: q, k <- RMSNorm over each head's hd values, gains qn, kn]
   q, k <- RoPE(q), RoPE(k)                 rotate-half pairs (i, i + hd/2)
-  o = softmax(q k^T / sqrt(hd) + causal) v per (batch row, head)
+  o = softmax(q k^T / sqrt(hd) + causal) v per (batch row, head); with
+      grouped-query attention k, v have kv_heads heads and query head h
+      uses key/value head h // (heads / kv_heads)
   h = x + o Wo^T
   n2 = RMSNorm(h; g2)
   dense: y = h + (silu(n2 W1^T) * (n2 W3^T)) W2^T
@@ -300,22 +303,40 @@ def moe_backward(dy, n2, p, cfg, mcache):
 # One decoder layer
 # ---------------------------------------------------------------------------
 
+def repeat_kv(t, groups: int):
+    """[b, S, kv, hd] -> [b, S, kv * groups, hd]: head h reads kv head h // groups."""
+    return np.repeat(t, groups, axis=2)
+
+
+def sum_groups(t, groups: int):
+    """VJP of repeat_kv: the gradients of a kv head's query heads summed."""
+    b, S, h, hd = t.shape
+    return t.reshape(b, S, h // groups, groups, hd).sum(axis=3)
+
+
 def layer_forward(p: Dict[str, np.ndarray], x, cfg, tabs, route_override=None):
     """One pre-norm decoder layer; x is [b, S, d]. Returns (y, cache)."""
     b, S, d = x.shape
-    h, hd = cfg.n_heads, cfg.head_dim
+    h, hd, hkv = cfg.n_heads, cfg.head_dim, cfg.kv_heads
     cos, sin = tabs
     n1, rstd1 = rmsnorm_forward(x, p["g1"], cfg.rms_eps)
     q = (n1 @ p["wq"].T).reshape(b, S, h, hd)
-    k = (n1 @ p["wk"].T).reshape(b, S, h, hd)
-    v = (n1 @ p["wv"].T).reshape(b, S, h, hd)
-    qr = rope_apply(q, cos, sin)
-    kr = rope_apply(k, cos, sin)
-    o = attention_forward(qr, kr, v).reshape(b, S, d)
+    k = (n1 @ p["wk"].T).reshape(b, S, hkv, hd)
+    v = (n1 @ p["wv"].T).reshape(b, S, hkv, hd)
+    cache = dict(x=x, n1=n1, rstd1=rstd1, v=v)
+    if cfg.qk_norm:
+        qh, rq = rmsnorm_forward(q, p["qn"], cfg.rms_eps)
+        kh, rk = rmsnorm_forward(k, p["kn"], cfg.rms_eps)
+        cache.update(q=q, k=k, rq=rq, rk=rk)
+    else:
+        qh, kh = q, k
+    qr = rope_apply(qh, cos, sin)
+    kr = rope_apply(kh, cos, sin)
+    G = h // hkv
+    o = attention_forward(qr, repeat_kv(kr, G), repeat_kv(v, G)).reshape(b, S, d)
     hres = x + o @ p["wo"].T
     n2, rstd2 = rmsnorm_forward(hres, p["g2"], cfg.rms_eps)
-    cache = dict(x=x, n1=n1, rstd1=rstd1, qr=qr, kr=kr, v=v, o=o, h=hres,
-                 n2=n2, rstd2=rstd2)
+    cache.update(qr=qr, kr=kr, o=o, h=hres, n2=n2, rstd2=rstd2)
     if cfg.moe:
         ff, mc = moe_forward(n2.reshape(b * S, d), p, cfg, route_override)
         y = hres + ff.reshape(b, S, d)
@@ -331,7 +352,8 @@ def layer_backward(p, cache, dy, cfg, tabs):
     """VJP of layer_forward. Returns (dx, grads) with grads keyed like p."""
     x = cache["x"]
     b, S, d = x.shape
-    h, hd = cfg.n_heads, cfg.head_dim
+    h, hd, hkv = cfg.n_heads, cfg.head_dim, cfg.kv_heads
+    G = h // hkv
     cos, sin = tabs
     g = {}
     # FFN (the residual passes dy straight to h)
@@ -350,11 +372,16 @@ def layer_backward(p, cache, dy, cfg, tabs):
     dh2 = dh.reshape(-1, d)
     do = (dh2 @ p["wo"]).reshape(b, S, h, hd)
     g["wo"] = dh2.T @ cache["o"].reshape(-1, d)
-    # attention, then undo the rotation
-    dqr, dkr, dv = attention_backward(do, cache["qr"], cache["kr"], cache["v"])
-    dq = rope_apply(dqr, cos, sin, inverse=True).reshape(-1, d)
-    dk = rope_apply(dkr, cos, sin, inverse=True).reshape(-1, d)
-    dv = dv.reshape(-1, d)
+    # attention over the repeated key/value heads, then undo the rotation
+    dqr, dkr, dv = attention_backward(do, cache["qr"], repeat_kv(cache["kr"], G),
+                                      repeat_kv(cache["v"], G))
+    dkr, dv = sum_groups(dkr, G), sum_groups(dv, G)
+    dq = rope_apply(dqr, cos, sin, inverse=True)
+    dk = rope_apply(dkr, cos, sin, inverse=True)
+    if cfg.qk_norm:
+        dq, g["qn"] = rmsnorm_backward(dq, cache["q"], cache["rq"], p["qn"])
+        dk, g["kn"] = rmsnorm_backward(dk, cache["k"], cache["rk"], p["kn"])
+    dq, dk, dv = dq.reshape(-1, d), dk.reshape(-1, hkv * hd), dv.reshape(-1, hkv * hd)
     n1 = cache["n1"].reshape(-1, d)
     dn1 = (dq @ p["wq"] + dk @ p["wk"] + dv @ p["wv"]).reshape(b, S, d)
     g["wq"], g["wk"], g["wv"] = dq.T @ n1, dk.T @ n1, dv.T @ n1

@@ -119,6 +119,12 @@ lc_status rmsnorm_bwd_partials_launch(const lc_norm_args &a, hipStream_t s);
 // rmsnorm_bwd_launch uses, for the same T and d (dg[k] = the sum if store).
 lc_status rmsnorm_dg_final_launch(const float *partial, float *dg, int64_t T, int64_t d,
                                   hipStream_t s, bool store = false);
+lc_status qknorm_fwd_launch(const lc_qknorm_args &a, hipStream_t s);
+// the backward's rows and gain partial sums (a.dgq, a.dgk unused) ...
+lc_status qknorm_bwd_partials_launch(const lc_qknorm_args &a, hipStream_t s);
+// ... and the ordered sum of those partials into (or, with store, onto) dgq, dgk
+lc_status qknorm_dg_final_launch(const float *partial, float *dgq, float *dgk, int64_t T, int hd,
+                                 bool store, hipStream_t s);
 lc_status attn_fwd_launch(const lc_attn_args &a, hipStream_t s);
 lc_status attn_bwd_launch(const lc_attn_args &a, hipStream_t s);
 lc_status accumulate_launch(float *acc, const void *g, int g_dtype, size_t n, hipStream_t s);

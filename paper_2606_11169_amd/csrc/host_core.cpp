@@ -27,6 +27,12 @@ lc_status validate_desc(const lc_stage_desc *d) {
   if (d->n_layers <= 0 || d->d_model <= 0 || d->n_heads <= 0 || d->head_dim <= 0 ||
       d->seq_len <= 0 || d->micro_batch <= 0)
     return fail(LC_ERR_INVALID_ARG, "stage dimensions must be positive");
+  if (d->n_kv_heads < 0 || (d->n_kv_heads > 0 && d->n_heads % d->n_kv_heads != 0))
+    return fail(LC_ERR_INVALID_ARG, "n_kv_heads (%d) must be 0 or divide n_heads (%d)",
+                d->n_kv_heads, d->n_heads);
+  if (d->qk_norm != 0 && d->qk_norm != 1) return fail(LC_ERR_INVALID_ARG, "qk_norm must be 0 or 1");
+  if (d->qk_norm && (d->head_dim < 16 || d->head_dim > 128 || (d->head_dim & (d->head_dim - 1))))
+    return fail(LC_ERR_UNSUPPORTED, "the q/k norm kernels need head_dim in {16, 32, 64, 128}");
   if ((int64_t)d->n_heads * d->head_dim != d->d_model)
     return fail(LC_ERR_INVALID_ARG, "d_model (%d) != n_heads (%d) * head_dim (%d)", d->d_model,
                 d->n_heads, d->head_dim);
@@ -66,11 +72,16 @@ ParamPlan param_plan(const lc_stage_desc &d) {
   ParamPlan p{};
   const size_t D = (size_t)d.d_model;
   size_t off = 0;
+  const size_t Dkv = (size_t)kv_heads(d) * (size_t)d.head_dim;
   p.wq = off; off += D * D;
-  p.wk = off; off += D * D;
-  p.wv = off; off += D * D;
+  p.wk = off; off += Dkv * D;
+  p.wv = off; off += Dkv * D;
   p.wo = off; off += D * D;
   p.g1 = off; off += D;
+  if (d.qk_norm) {
+    p.qn = off; off += (size_t)d.head_dim;
+    p.kn = off; off += (size_t)d.head_dim;
+  }
   if (d.n_experts == 0) {
     const size_t F = (size_t)d.d_ff;
     p.w1 = off; off += F * D;
@@ -122,6 +133,10 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_
   const size_t R = moe ? 2 * (size_t)T : (size_t)T;  // FFN rows (routed rows for MoE)
   p.elem = es;
   p.T = T;
+  const size_t Hkv = (size_t)kv_heads(d);
+  p.dkv = (int64_t)(Hkv * (size_t)d.head_dim);
+  p.qkv_cols = (int64_t)D + 2 * p.dkv;
+  const size_t QC = (size_t)p.qkv_cols;
   size_t off = 0;
   const size_t half = (size_t)d.head_dim / 2;
   p.rope_cos = off; off = align256(off + (size_t)d.seq_len * half * 4);
@@ -133,7 +148,11 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_
   p.xin = take((size_t)T * D * er);
   p.rstd1 = take((size_t)T * 4);
   p.n1 = take((size_t)T * D * es);
-  p.qkv = take((size_t)T * 3 * D * ea);
+  p.qkv = take((size_t)T * QC * ea);
+  if (d.qk_norm) {
+    p.qkraw = take((size_t)T * (D + (size_t)p.dkv) * ea);
+    p.rstdqk = take((size_t)T * (H + Hkv) * 4);
+  }
   p.o = take((size_t)T * D * es);
   p.lse = take((size_t)T * H * 4);
   p.h = take((size_t)T * D * er);
@@ -164,9 +183,10 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_
   p.w_dy = wtake((size_t)T * D * es);
   p.w_da = wtake(R * 2 * F * es);
   p.w_dh = wtake((size_t)T * D * es);
-  p.w_dqkv = wtake((size_t)T * 3 * D * es);
+  p.w_dqkv = wtake((size_t)T * QC * es);
   p.w_p2 = wtake(rmsnorm_scratch_size(T, d.d_model));
   p.w_p1 = wtake(rmsnorm_scratch_size(T, d.d_model));
+  p.w_pqk = d.qk_norm ? wtake(qknorm_scratch_size(T, d.head_dim)) : 0;
   p.wlayer_bytes = wo;
   p.wslot_bytes = wo * (size_t)d.n_layers;
   p.w_slots = max_w_pending;
@@ -180,13 +200,17 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_
   p.s_da = stake(R * 2 * F * es);
   p.s_dn = stake((size_t)T * D * er);
   p.s_do = stake((size_t)T * D * es);
-  p.s_dqkv = stake((size_t)T * 3 * D * es);
+  p.s_dqkv = stake((size_t)T * QC * es);
   p.s_dh = stake((size_t)T * D * er);
   p.s_dh16 = stake((size_t)T * D * es);
-  p.s_attn_bytes = attn_scratch_size(d.micro_batch, d.seq_len, d.n_heads);
+  p.s_attn_bytes = attn_scratch_size(d.micro_batch, d.seq_len, d.n_heads, (int64_t)Hkv);
   p.s_attn = stake(p.s_attn_bytes);
   p.s_norm_bytes = rmsnorm_scratch_size(T, d.d_model);
   p.s_norm = stake(p.s_norm_bytes);
+  if (d.qk_norm) {
+    p.s_qkn_bytes = qknorm_scratch_size(T, d.head_dim);
+    p.s_qkn = stake(p.s_qkn_bytes);
+  }
   if (moe) {
     p.s_moe_dys = stake(R * D * es);
     p.s_moe_dns = stake(R * D * 4);
@@ -210,11 +234,24 @@ size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E) {
   return (size_t)(nblk * E * d) * sizeof(float);
 }
 
-size_t attn_scratch_size(int64_t B, int64_t S, int64_t H) {
+size_t attn_share_offset(int64_t B, int64_t S, int64_t H, int64_t Hkv) {
   // D (fp32 [B, H, S]), then for the matrix-core backward bf16 rows of v
-  // ([B*S, H*128]) and bf16 transposes of q, k, dO ([B][H][128][S] each)
+  // ([B*S, Hkv*128]), bf16 transposes of q and dO ([B][H][128][S] each) and
+  // of k ([B][Hkv][128][S])
   const size_t dbytes = ((size_t)(B * S * H) * sizeof(float) + 255) / 256 * 256;
-  return dbytes + (size_t)(B * S) * 4 * (size_t)H * 128 * 2;
+  return align256(dbytes + (size_t)(B * S) * (size_t)(2 * H + 2 * Hkv) * 128 * 2);
+}
+
+size_t attn_scratch_size(int64_t B, int64_t S, int64_t H, int64_t Hkv) {
+  // with grouped-query attention, then each query head's fp32 share of dk
+  // and dv ([B*S, H*128] each)
+  const size_t shares = Hkv < H ? (size_t)(B * S) * (size_t)H * 128 * 4 * 2 : 0;
+  return attn_share_offset(B, S, H, Hkv) + shares;
+}
+
+size_t qknorm_scratch_size(int64_t T, int64_t hd) {
+  const int64_t nblk = (T + kQkTokensPerBlock - 1) / kQkTokensPerBlock;
+  return (size_t)(nblk * 2 * hd) * sizeof(float);
 }
 
 lc_status flatten_order(const lc_order &order, std::vector<lc_order_entry> *flat) {
@@ -283,8 +320,11 @@ lc_status lc_param_offset(const lc_stage_desc *desc, int32_t layer, int32_t tens
     return fail(LC_ERR_INVALID_ARG, "expert index only applies to W1/W3/W2");
   switch (tensor_id) {
     case LC_T_WQ: o = p.wq; r = D; c = D; break;
-    case LC_T_WK: o = p.wk; r = D; c = D; break;
-    case LC_T_WV: o = p.wv; r = D; c = D; break;
+    case LC_T_WK: o = p.wk; r = (int64_t)kv_heads(*desc) * desc->head_dim; c = D; break;
+    case LC_T_WV: o = p.wv; r = (int64_t)kv_heads(*desc) * desc->head_dim; c = D; break;
+    case LC_T_QN: case LC_T_KN:
+      if (!desc->qk_norm) return fail(LC_ERR_INVALID_ARG, "stage has no q/k norm gains");
+      o = tensor_id == LC_T_QN ? p.qn : p.kn; r = desc->head_dim; break;
     case LC_T_WO: o = p.wo; r = D; c = D; break;
     case LC_T_G1: o = p.g1; r = D; break;
     case LC_T_G2: o = p.g2; r = D; break;
@@ -487,7 +527,11 @@ lc_status lc_workspace_bytes(const lc_stage_desc *desc, int32_t max_in_flight, s
 
 size_t lc_rmsnorm_scratch_bytes(int64_t T, int64_t d) { return rmsnorm_scratch_size(T, d); }
 size_t lc_attention_scratch_bytes(int32_t B, int32_t S, int32_t H) {
-  return attn_scratch_size(B, S, H);
+  return attn_scratch_size(B, S, H, H);
 }
+size_t lc_attention_scratch_bytes_kv(int32_t B, int32_t S, int32_t H, int32_t Hkv) {
+  return attn_scratch_size(B, S, H, Hkv > 0 ? Hkv : H);
+}
+size_t lc_qk_norm_scratch_bytes(int64_t T, int32_t hd) { return qknorm_scratch_size(T, hd); }
 
 }  // extern "C"

@@ -23,7 +23,14 @@ lc_status fail(lc_status st, const char *fmt, ...) __attribute__((format(printf,
 // Rows per block of the RMSNorm backward's gain-gradient partial sums.
 constexpr int kNormRowsPerBlock = 16;
 size_t rmsnorm_scratch_size(int64_t T, int64_t d);
-size_t attn_scratch_size(int64_t B, int64_t S, int64_t H);
+size_t attn_scratch_size(int64_t B, int64_t S, int64_t H, int64_t Hkv);
+// byte offset of grouped-query attention's dk/dv shares in that scratch
+size_t attn_share_offset(int64_t B, int64_t S, int64_t H, int64_t Hkv);
+// Tokens per block of the per-head q/k RMSNorm's gain-gradient partial sums
+// (each block writes 2 * head_dim floats: q gains, then k gains).
+constexpr int kQkTokensPerBlock = 4;
+size_t qknorm_scratch_size(int64_t T, int64_t hd);
+inline int kv_heads(const lc_stage_desc &d) { return d.n_kv_heads > 0 ? d.n_kv_heads : d.n_heads; }
 // Tokens per block of the MoE router weight gradient's partial sums.
 constexpr int kRouterTokensPerBlock = 128;
 size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E);
@@ -40,6 +47,7 @@ lc_status validate_desc(const lc_stage_desc *d);
 struct ParamPlan {
   size_t per_layer;                 // elements per layer
   size_t wq, wk, wv, wo, g1;        // offsets inside a layer
+  size_t qn, kn;                    // per-head q/k norm gains (qk_norm)
   size_t w1, w3, w2;                // dense FFN
   size_t wr, expert0, expert_stride;  // MoE: router, first expert's W1, stride per expert
   size_t g2;
@@ -63,12 +71,17 @@ struct StagePlan {
   size_t elem;          // bytes per GEMM-operand element (2 or 4)
   StageTypes ty;
   int64_t T;            // tokens per microbatch
+  int64_t dkv;          // key/value width n_kv_heads * head_dim
+  int64_t qkv_cols;     // d + 2 dkv: columns of the packed q|k|v
   // RoPE table: cos then sin, fp32 [seq_len, head_dim/2]
   size_t rope_cos, rope_sin;
   // stash: max_in_flight slots of n_layers layer blocks
   size_t slot0, slot_bytes, layer_bytes;
   // offsets inside one layer block
   size_t xin, rstd1, n1, qkv, o, lse, h, rstd2, n2, gate, up, act;
+  // qk_norm: the projection's raw q|k [T, d + dkv] (att type) and the
+  // per-head reciprocal RMS [T, n_heads + n_kv_heads] (fp32)
+  size_t qkraw, rstdqk;
   // weight-pass slots (split backward): max_w_pending slots of n_layers
   // blocks, each holding the gradient operands a backward-for-inputs pass
   // leaves for the backward-for-weights pass of the same microbatch: the
@@ -77,7 +90,7 @@ struct StagePlan {
   // both norms (rmsnorm_scratch_size each)
   int32_t w_slots;
   size_t wslot0, wslot_bytes, wlayer_bytes;
-  size_t w_dy, w_da, w_dh, w_dqkv, w_p2, w_p1;
+  size_t w_dy, w_da, w_dh, w_dqkv, w_p2, w_p1, w_pqk;
   // MoE per-layer extras (0 when dense): routing (sel, w [T, 2]), dispatch
   // (perm, wrow [2T], rowpos [T, 2], expert offsets [E + 1]), the gathered
   // expert inputs xp [2T, d] (op type) and expert outputs eo [2T, d] (fp32)
@@ -93,6 +106,7 @@ struct StagePlan {
   size_t s_dh16;        // operand copy of dh [T, d] (op type)
   size_t s_attn, s_attn_bytes;  // attention backward scratch
   size_t s_norm, s_norm_bytes;  // RMSNorm backward scratch
+  size_t s_qkn, s_qkn_bytes;    // q/k norm gain partial sums (qk_norm)
   // MoE backward: weighted expert-output gradients dys [2T, d] (op type),
   // expert-input gradients dns [2T, d] (fp32), gate-weight gradients dw [2T],
   // router-logit gradients dl [T, 2], router weight-gradient partial sums

@@ -213,13 +213,17 @@ struct AttnP {
   __bf16 *dq, *dk, *dv;
   float *D;
   // backward: bf16 rows of v (p.v itself for bf16 inputs), and bf16 transposes
-  // [B][H][128][S] of q, k and dO (positions permuted within 16-groups)
+  // of q and dO ([B][H][128][S]) and of k ([B][Hkv][128][S]) (positions
+  // permuted within 16-groups)
   const __bf16 *vb;
   __bf16 *vb_w, *qt, *kt, *dot;
+  // grouped-query attention: fp32 partial dk, dv per query head [B*S, H*128]
+  float *dkp, *dvp;
   const float *rcos, *rsin;
   int64_t ld_qkv, ld_o, ld_d, ld_vb;
-  uint32_t qkv_bytes, o_bytes, vb_bytes, t_bytes, lse_bytes;  // buffer extents (q/k/v from p.q)
+  uint32_t qkv_bytes, o_bytes, vb_bytes, t_bytes, kt_bytes, lse_bytes;  // buffer extents (q/k/v from p.q)
   int S, H, B;
+  int Hkv, G;   // key/value heads; query heads per key/value head
   float scale;  // 1/sqrt(hd)
 };
 
@@ -241,6 +245,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
   const int myq = q0 + l32;
   const float sc = p.scale * LOG2E;
   const QE *Q = static_cast<const QE *>(p.q) + h * HD;
+  const int kvh = h / p.G;
 
   QV qf[8];
 #pragma unroll
@@ -260,7 +265,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
 #pragma unroll
     for (int t = 0; t < 4; ++t)
       tile_run(rs, st + (isK ? 0 : TILE), 4 * (w & 3) + t, row0 + (int64_t)kb * KB, p.ld_qkv,
-               h * HD, lane);
+               kvh * HD, lane);
   };
   const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
   load(0, L);
@@ -339,9 +344,11 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
 
 // ---------------------------------------------------------------- backward
 // One workgroup per (64-position block, head, batch row): D[b,h,i] =
-// sum_e dO[i,e] O[i,e]; the block's columns of dO, q and k transposed into
+// sum_e dO[i,e] O[i,e]; the block's columns of dO and q transposed into
 // [B][H][128][S] bf16 (positions of each 16-group in the order 0-3, 8-11,
-// 4-7, 12-15) through an LDS tile; for fp16 q/k/v, the bf16 rows of v.
+// 4-7, 12-15) through an LDS tile; the first query head of each key/value
+// head also transposes k into [B][Hkv][128][S] and, for fp16 q/k/v, writes
+// the bf16 rows of v.
 template <typename QE>
 __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p) {
   constexpr int W = 130;  // tile row stride (65 words): conflict-free fills and gathers
@@ -352,6 +359,10 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p) {
   const int64_t grow = (int64_t)b * p.S + pos0 + r;
   const int col = h * HD + qtr * 32;
   const int64_t hbase = ((int64_t)b * p.H + h) * HD * p.S;
+  const int kvh = h / p.G;
+  const bool lead = h % p.G == 0;  // workgroup-uniform
+  const int kcol = kvh * HD + qtr * 32;
+  const int64_t kbase = ((int64_t)b * p.Hkv + kvh) * HD * p.S;
 
   auto put = [&](int u, bf16x8_v v) {  // columns 32 qtr + 8u .. +7 of row r
     uint32_t *w = reinterpret_cast<uint32_t *>(tile + r * W + qtr * 32 + 8 * u);
@@ -361,7 +372,7 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p) {
     w[2] = x.z;
     w[3] = x.w;
   };
-  auto write_t = [&](__bf16 *dst) {  // 1024 chunks of 8 stored positions
+  auto write_t = [&](__bf16 *dst, int64_t base) {  // 1024 chunks of 8 stored positions
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
       const int idx = t + 256 * it, c = idx & 7, n = idx >> 3;
@@ -369,7 +380,7 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p) {
       bf16x8_v v;
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = tile[(rb + (e & 3) + 8 * (e >> 2)) * W + n];
-      *reinterpret_cast<bf16x8_v *>(dst + hbase + (int64_t)n * p.S + pos0 + 8 * c) = v;
+      *reinterpret_cast<bf16x8_v *>(dst + base + (int64_t)n * p.S + pos0 + 8 * c) = v;
     }
   };
 
@@ -386,23 +397,27 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p) {
   acc += __shfl_xor(acc, 2, 64);
   if (qtr == 0) p.D[((int64_t)b * p.H + h) * p.S + pos0 + r] = acc;
   __syncthreads();
-  write_t(p.dot);
+  write_t(p.dot, hbase);
 #pragma unroll
   for (int src = 0; src < 2; ++src) {
+    if (src == 1 && !lead) break;
     __syncthreads();
     const QE *X = static_cast<const QE *>(src == 0 ? p.q : p.k);
+    const int c0 = src == 0 ? col : kcol;
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      put(u, to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(X + grow * p.ld_qkv + col + 8 * u)));
+      put(u, to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(X + grow * p.ld_qkv + c0 + 8 * u)));
     __syncthreads();
-    write_t(src == 0 ? p.qt : p.kt);
+    write_t(src == 0 ? p.qt : p.kt, src == 0 ? hbase : kbase);
   }
   if constexpr (!std::is_same<QE, __bf16>::value) {
-    const QE *V = static_cast<const QE *>(p.v);
+    if (lead) {
+      const QE *V = static_cast<const QE *>(p.v);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      *reinterpret_cast<bf16x8_v *>(p.vb_w + grow * p.ld_vb + col + 8 * u) =
-          to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(V + grow * p.ld_qkv + col + 8 * u));
+      for (int u = 0; u < 4; ++u)
+        *reinterpret_cast<bf16x8_v *>(p.vb_w + grow * p.ld_vb + kcol + 8 * u) =
+            to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(V + grow * p.ld_qkv + kcol + 8 * u));
+    }
   }
 }
 
@@ -418,6 +433,16 @@ __device__ __forceinline__ void rope_inverse_pairs(f32x16_v (&acc)[4], const flo
       acc[i][r] = a * c + bb * sn;
       acc[i + 2][r] = bb * c - a * sn;
     }
+}
+
+// lane holds acc^T[e][token] for its own token; store that token's row (fp32)
+__device__ __forceinline__ void store_row_f32(float *row, const f32x16_v (&acc)[4], int hf) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4 *>(row + i * 32 + 8 * g + 4 * hf) =
+          make_float4(acc[i][4 * g], acc[i][4 * g + 1], acc[i][4 * g + 2], acc[i][4 * g + 3]);
 }
 
 // lane holds acc^T[e][token] for its own token; store that token's row (bf16)
@@ -449,7 +474,8 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   const bool active = q0 < p.S;
   const int myq = q0 + l32;
   const float sc = p.scale * LOG2E;
-  const int64_t hbase = ((int64_t)b * p.H + h) * HD * p.S;
+  const int kvh = h / p.G;
+  const int64_t kbase = ((int64_t)b * p.Hkv + kvh) * HD * p.S;
 
   QV qf[8];
   bf16x8_v df[8];
@@ -475,15 +501,15 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   // 48 runs per block: K (QE) runs 0-15, V (bf16) 16-31, K^T (bf16) 32-47; 6 per wave
   const i32x4_v rk = make_rsrc(p.k, p.qkv_bytes);
   const i32x4_v rvb = make_rsrc(p.vb, p.vb_bytes);
-  const i32x4_v rkt = make_rsrc(p.kt, p.t_bytes);
+  const i32x4_v rkt = make_rsrc(p.kt, p.kt_bytes);
   auto load = [&](int kb, lds_t *st) {
     const int64_t g0 = row0 + (int64_t)kb * KB;
 #pragma unroll
     for (int t = 0; t < 6; ++t) {
       const int run = 6 * w + t, which = run >> 4;
-      if (which == 0) tile_run(rk, st, run & 15, g0, p.ld_qkv, h * HD, lane);
-      else if (which == 1) tile_run(rvb, st + TILE, run & 15, g0, p.ld_vb, h * HD, lane);
-      else tt_run(rkt, st + 2 * TILE, run & 15, hbase, p.S, kb * KB, lane);
+      if (which == 0) tile_run(rk, st, run & 15, g0, p.ld_qkv, kvh * HD, lane);
+      else if (which == 1) tile_run(rvb, st + TILE, run & 15, g0, p.ld_vb, kvh * HD, lane);
+      else tt_run(rkt, st + 2 * TILE, run & 15, kbase, p.S, kb * KB, lane);
     }
   };
   const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
@@ -539,12 +565,14 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   store_row_t(p.dq + h * HD + (row0 + myq) * p.ld_d, acc, 1.0f, hf);
 }
 
-// dK, dV: one workgroup of 8 waves per 128 keys. Waves w and w + 4 own the
-// same 32 keys (their K and V fragments stay in registers) and take the first
-// and the second 32 queries of every 64-query block at or after the diagonal;
-// at the end wave w + 4 hands its partial dK, dV to wave w through LDS, which
-// adds them (fixed order: deterministic). LDS stage (two of them) =
-// Q (QE) | dO | Q^T | dO^T | lse | D of one 64-query block.
+// dK, dV: one workgroup of 8 waves per 128 keys and query head. Waves w and
+// w + 4 own the same 32 keys (their K and V fragments stay in registers) and
+// take the first and the second 32 queries of every 64-query block at or
+// after the diagonal; at the end wave w + 4 hands its partial dK, dV to wave w
+// through LDS, which adds them (fixed order: deterministic). LDS stage (two
+// of them) = Q (QE) | dO | Q^T | dO^T | lse | D of one 64-query block. With
+// grouped-query attention the workgroup writes its query head's share of the
+// key/value head's dK, dV as fp32 rows; attn_gqa_sum_kernel adds the shares.
 constexpr int KV_ROWS = 128;
 template <typename QE>
 __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
@@ -553,6 +581,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
   __shared__ __align__(16) char smem[2 * STAGE];
   lds_t *const L = LDS_AS(char, smem);
   const int kblk = (int)blockIdx.x / p.H, h = (int)blockIdx.x % p.H;  // earliest (heaviest) keys first
+  const int kvh = h / p.G;
   const int b = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -568,7 +597,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
   bf16x8_v vf[8];
 #pragma unroll
   for (int es = 0; es < 8; ++es) {
-    const int64_t off = h * HD + (row0 + myk) * p.ld_qkv + es * 16 + hf * 8;
+    const int64_t off = kvh * HD + (row0 + myk) * p.ld_qkv + es * 16 + hf * 8;
     kf[es] = *reinterpret_cast<const QV *>(static_cast<const QE *>(p.k) + off);
     vf[es] = to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(static_cast<const QE *>(p.v) + off));
   }
@@ -686,8 +715,44 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
       dv[i][r] += red[(64 + i * 16 + r) * 64];
     }
   if (p.rcos) rope_inverse_pairs(dk, p.rcos, p.rsin, myk, hf);
-  store_row_t(p.dk + h * HD + (row0 + myk) * p.ld_d, dk, 1.0f, hf);
-  store_row_t(p.dv + h * HD + (row0 + myk) * p.ld_d, dv, 1.0f, hf);
+  if (p.G == 1) {
+    store_row_t(p.dk + h * HD + (row0 + myk) * p.ld_d, dk, 1.0f, hf);
+    store_row_t(p.dv + h * HD + (row0 + myk) * p.ld_d, dv, 1.0f, hf);
+  } else {
+    const int64_t prow = (row0 + myk) * (int64_t)p.H * HD + h * HD;
+    store_row_f32(p.dkp + prow, dk, hf);
+    store_row_f32(p.dvp + prow, dv, hf);
+  }
+}
+
+// Grouped-query attention: dk, dv of key/value head kvh = the sum, in head
+// order, of the fp32 shares of its G query heads (8 elements per thread)
+__global__ __launch_bounds__(256) void attn_gqa_sum_kernel(AttnP p) {
+  const int64_t n8 = (int64_t)p.B * p.S * p.Hkv * HD / 8;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  const int64_t e0 = 8 * i;
+  const int64_t row = e0 / ((int64_t)p.Hkv * HD);
+  const int c = (int)(e0 % ((int64_t)p.Hkv * HD));  // kvh * HD + e
+  const int kvh = c / HD, e = c % HD;
+#pragma unroll
+  for (int which = 0; which < 2; ++which) {
+    const float *src = (which == 0 ? p.dkp : p.dvp) + row * (int64_t)p.H * HD + (int64_t)kvh * p.G * HD + e;
+    float acc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] = 0.0f;
+    for (int g = 0; g < p.G; ++g) {
+      const float4 a = *reinterpret_cast<const float4 *>(src + g * HD);
+      const float4 b = *reinterpret_cast<const float4 *>(src + g * HD + 4);
+      acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
+      acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+    }
+    bf16x8_v v;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = (__bf16)acc[u];
+    __bf16 *dst = (which == 0 ? p.dk : p.dv) + row * p.ld_d + c;
+    *reinterpret_cast<bf16x8_v *>(dst) = v;
+  }
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -702,6 +767,7 @@ struct AttnF {
   const float *rcos, *rsin;
   int64_t ld_qkv, ld_o, ld_d;
   int B, S, H, hd;
+  int Hkv, G;  // key/value heads; query heads per key/value head
   float scale;
 };
 
@@ -713,18 +779,19 @@ __global__ void attn_fwd_f32_kernel(AttnF p) {
   const int i = (int)(id % p.S), h = (int)((id / p.S) % p.H), b = (int)(id / ((int64_t)p.S * p.H));
   const int64_t r0 = (int64_t)b * p.S;
   const float *qi = p.q + (r0 + i) * p.ld_qkv + h * p.hd;
+  const int kvh = h / p.G;
   float acc[MAXHD];
   for (int e = 0; e < p.hd; ++e) acc[e] = 0.0f;
   float m = -INFINITY, l = 0.0f;
   for (int j = 0; j <= i; ++j) {
-    const float *kj = p.k + (r0 + j) * p.ld_qkv + h * p.hd;
+    const float *kj = p.k + (r0 + j) * p.ld_qkv + kvh * p.hd;
     float s = 0.0f;
     for (int e = 0; e < p.hd; ++e) s += qi[e] * kj[e];
     s *= p.scale;
     const float mn = fmaxf(m, s);
     const float a = expf(m - mn), w = expf(s - mn);
     l = l * a + w;
-    const float *vj = p.v + (r0 + j) * p.ld_qkv + h * p.hd;
+    const float *vj = p.v + (r0 + j) * p.ld_qkv + kvh * p.hd;
     for (int e = 0; e < p.hd; ++e) acc[e] = acc[e] * a + w * vj[e];
     m = mn;
   }
@@ -757,11 +824,12 @@ __global__ void attn_bwd_q_f32_kernel(AttnF p) {
   const int64_t si = ((int64_t)b * p.H + h) * p.S + i;
   p.D[si] = Di;
   const float L = p.lse[si];
+  const int kvh = h / p.G;
   float acc[MAXHD];
   for (int e = 0; e < p.hd; ++e) acc[e] = 0.0f;
   for (int j = 0; j <= i; ++j) {
-    const float *kj = p.k + (r0 + j) * p.ld_qkv + h * p.hd;
-    const float *vj = p.v + (r0 + j) * p.ld_qkv + h * p.hd;
+    const float *kj = p.k + (r0 + j) * p.ld_qkv + kvh * p.hd;
+    const float *vj = p.v + (r0 + j) * p.ld_qkv + kvh * p.hd;
     float s = 0.0f, dp = 0.0f;
     for (int e = 0; e < p.hd; ++e) {
       s += qi[e] * kj[e];
@@ -777,16 +845,19 @@ __global__ void attn_bwd_q_f32_kernel(AttnF p) {
   for (int e = 0; e < p.hd; ++e) dqi[e] = acc[e];
 }
 
-// per key: dk_j and dv_j (needs D from the kernel above)
+// per key and key/value head: dk_j and dv_j summed over the head's query
+// heads in order (needs D from the kernel above)
 __global__ void attn_bwd_kv_f32_kernel(AttnF p) {
   const int64_t id = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (id >= (int64_t)p.B * p.H * p.S) return;
-  const int j = (int)(id % p.S), h = (int)((id / p.S) % p.H), b = (int)(id / ((int64_t)p.S * p.H));
+  if (id >= (int64_t)p.B * p.Hkv * p.S) return;
+  const int j = (int)(id % p.S), kvh = (int)((id / p.S) % p.Hkv);
+  const int b = (int)(id / ((int64_t)p.S * p.Hkv));
   const int64_t r0 = (int64_t)b * p.S;
-  const float *kj = p.k + (r0 + j) * p.ld_qkv + h * p.hd;
-  const float *vj = p.v + (r0 + j) * p.ld_qkv + h * p.hd;
+  const float *kj = p.k + (r0 + j) * p.ld_qkv + kvh * p.hd;
+  const float *vj = p.v + (r0 + j) * p.ld_qkv + kvh * p.hd;
   float ak[MAXHD], av[MAXHD];
   for (int e = 0; e < p.hd; ++e) ak[e] = av[e] = 0.0f;
+  for (int h = kvh * p.G; h < (kvh + 1) * p.G; ++h)
   for (int i = j; i < p.S; ++i) {
     const float *qi = p.q + (r0 + i) * p.ld_qkv + h * p.hd;
     const float *doi = p.dout + (r0 + i) * p.ld_o + h * p.hd;
@@ -805,17 +876,24 @@ __global__ void attn_bwd_kv_f32_kernel(AttnF p) {
   }
   for (int e = 0; e < p.hd; ++e) ak[e] *= p.scale;
   if (p.rcos) rope_inv_vec(ak, p.hd, j, p.rcos, p.rsin);
-  float *dkj = p.dk + (r0 + j) * p.ld_d + h * p.hd;
-  float *dvj = p.dv + (r0 + j) * p.ld_d + h * p.hd;
+  float *dkj = p.dk + (r0 + j) * p.ld_d + kvh * p.hd;
+  float *dvj = p.dv + (r0 + j) * p.ld_d + kvh * p.hd;
   for (int e = 0; e < p.hd; ++e) {
     dkj[e] = ak[e];
     dvj[e] = av[e];
   }
 }
 
+int kv_of(const lc_attn_args &a) { return a.Hkv > 0 ? a.Hkv : a.H; }
+size_t attn_scratch_bytes_of(const lc_attn_args &a) {
+  return attn_scratch_size(a.B, a.S, a.H, kv_of(a));
+}
+
 lc_status check_common(const lc_attn_args &a, bool bwd) {
   if (a.B <= 0 || a.S <= 0 || a.H <= 0 || a.hd <= 0)
     return fail(LC_ERR_INVALID_ARG, "attention: dimensions must be positive");
+  if (a.Hkv < 0 || a.H % kv_of(a) != 0)
+    return fail(LC_ERR_INVALID_ARG, "attention: Hkv (%d) must be 0 or divide H (%d)", a.Hkv, a.H);
   if (a.ld_qkv < (int64_t)a.H * a.hd || a.ld_o < (int64_t)a.H * a.hd)
     return fail(LC_ERR_INVALID_ARG, "attention: leading dimension smaller than H*hd");
   if (!a.q || !a.k || !a.v || !a.o || !a.lse) return fail(LC_ERR_INVALID_ARG, "attention: null pointer");
@@ -828,7 +906,7 @@ lc_status check_common(const lc_attn_args &a, bool bwd) {
     if (a.ld_dqkv < (int64_t)a.H * a.hd) return fail(LC_ERR_INVALID_ARG, "attention: ld_dqkv too small");
     if ((a.rope_cos == nullptr) != (a.rope_sin == nullptr))
       return fail(LC_ERR_INVALID_ARG, "attention: give both RoPE tables or neither");
-    if (!a.scratch || a.scratch_bytes < attn_scratch_size(a.B, a.S, a.H))
+    if (!a.scratch || a.scratch_bytes < attn_scratch_bytes_of(a))
       return fail(LC_ERR_WORKSPACE, "attention backward: scratch too small");
   }
   if (a.dtype == LC_BF16 || a.dtype == LC_FP16) {
@@ -848,6 +926,7 @@ lc_status check_common(const lc_attn_args &a, bool bwd) {
   return LC_OK;
 }
 
+
 AttnP mc_params(const lc_attn_args &a) {
   AttnP p{};
   p.q = a.q;
@@ -861,17 +940,25 @@ AttnP mc_params(const lc_attn_args &a) {
   p.dv = static_cast<__bf16 *>(a.dv);
   p.D = static_cast<float *>(a.scratch);
   const int64_t rows = (int64_t)a.B * a.S, d = (int64_t)a.H * HD;
-  // scratch: D (fp32 [B, H, S], 256-byte aligned), v rows (bf16), then the
-  // transposes of q, k, dO (bf16 [B][H][128][S] each)
+  const int Hkv = kv_of(a);
+  const int64_t dkv = (int64_t)Hkv * HD;
+  // scratch: D (fp32 [B, H, S], 256-byte aligned), v rows (bf16 [rows, dkv]),
+  // the transposes of q ([B][H][128][S]), k ([B][Hkv][128][S]) and dO
+  // ([B][H][128][S]), then (grouped-query attention) the fp32 dk, dv shares
   const size_t dbytes = ((size_t)rows * a.H * sizeof(float) + 255) / 256 * 256;
   __bf16 *const cp = a.scratch ? reinterpret_cast<__bf16 *>(static_cast<char *>(a.scratch) + dbytes) : nullptr;
   const bool bf = a.dtype == LC_BF16;
   p.vb_w = cp;
   p.vb = bf ? static_cast<const __bf16 *>(a.v) : cp;
-  p.ld_vb = bf ? a.ld_qkv : d;
-  p.qt = cp ? cp + rows * d : nullptr;
-  p.kt = cp ? cp + 2 * rows * d : nullptr;
-  p.dot = cp ? cp + 3 * rows * d : nullptr;
+  p.ld_vb = bf ? a.ld_qkv : dkv;
+  p.qt = cp ? cp + rows * dkv : nullptr;
+  p.kt = cp ? cp + rows * (dkv + d) : nullptr;
+  p.dot = cp ? cp + rows * (2 * dkv + d) : nullptr;
+  if (a.scratch && Hkv < a.H) {
+    char *sh = static_cast<char *>(a.scratch) + attn_share_offset(a.B, a.S, a.H, Hkv);
+    p.dkp = reinterpret_cast<float *>(sh);
+    p.dvp = p.dkp + rows * d;
+  }
   p.rcos = a.rope_cos;
   p.rsin = a.rope_sin;
   p.ld_qkv = a.ld_qkv;
@@ -879,12 +966,15 @@ AttnP mc_params(const lc_attn_args &a) {
   p.ld_d = a.ld_dqkv;
   p.qkv_bytes = (uint32_t)(((rows - 1) * a.ld_qkv + d) * 2);
   p.o_bytes = (uint32_t)(((rows - 1) * a.ld_o + d) * 2);
-  p.vb_bytes = (uint32_t)(((rows - 1) * p.ld_vb + d) * 2);
+  p.vb_bytes = (uint32_t)(((rows - 1) * p.ld_vb + dkv) * 2);
   p.t_bytes = (uint32_t)(rows * d * 2);
+  p.kt_bytes = (uint32_t)(rows * dkv * 2);
   p.lse_bytes = (uint32_t)(rows * a.H * sizeof(float));
   p.S = a.S;
   p.H = a.H;
   p.B = a.B;
+  p.Hkv = Hkv;
+  p.G = a.H / Hkv;
   p.scale = 1.0f / sqrtf((float)a.hd);
   return p;
 }
@@ -917,6 +1007,8 @@ AttnF f32_params(const lc_attn_args &a) {
   p.ld_o = a.ld_o;
   p.ld_d = a.ld_dqkv;
   p.B = a.B; p.S = a.S; p.H = a.H; p.hd = a.hd;
+  p.Hkv = kv_of(a);
+  p.G = a.H / p.Hkv;
   p.scale = 1.0f / sqrtf((float)a.hd);
   return p;
 }
@@ -940,6 +1032,11 @@ lc_status bwd_mc(const lc_attn_args &a, hipStream_t s) {
   hipLaunchKernelGGL(attn_bwd_dkdv_kernel<QE>, dim3((unsigned)(a.S / KV_ROWS * a.H), a.B), dim3(NT), 0,
                      s, p);
   LC_TRY(check_launch("attn_bwd_dkdv_kernel"));
+  if (p.G > 1) {
+    const int64_t n8 = (int64_t)a.B * a.S * p.Hkv * HD / 8;
+    hipLaunchKernelGGL(attn_gqa_sum_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s, p);
+    LC_TRY(check_launch("attn_gqa_sum_kernel"));
+  }
   hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(nb, a.H, a.B), dim3(NT), 0, s, p);
   return check_launch("attn_bwd_dq_kernel");
 }
@@ -965,7 +1062,8 @@ lc_status attn_bwd_launch(const lc_attn_args &a, hipStream_t s) {
   const dim3 grid((unsigned)((n + 127) / 128));
   hipLaunchKernelGGL(attn_bwd_q_f32_kernel, grid, dim3(128), 0, s, p);
   LC_TRY(check_launch("attn_bwd_q_f32_kernel"));
-  hipLaunchKernelGGL(attn_bwd_kv_f32_kernel, grid, dim3(128), 0, s, p);
+  const int64_t nkv = (int64_t)a.B * p.Hkv * a.S;
+  hipLaunchKernelGGL(attn_bwd_kv_f32_kernel, dim3((unsigned)((nkv + 127) / 128)), dim3(128), 0, s, p);
   return check_launch("attn_bwd_kv_f32_kernel");
 }
 

@@ -220,6 +220,22 @@ static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, cons
                                 w.gp(pp.wr), T, (int)D, E, s);
 }
 
+// The per-head q/k norm arguments of one layer (q|k of the packed qkv rows).
+static lc_qknorm_args qknorm_base(lc_stage *st, const W &w, const LayerBufs &L) {
+  const lc_stage_desc &d = st->d;
+  const StagePlan &P = st->plan;
+  lc_qknorm_args q;
+  memset(&q, 0, sizeof q);
+  q.T = P.T;
+  q.H = d.n_heads; q.Hkv = kv_heads(d); q.hd = d.head_dim; q.seq_len = d.seq_len;
+  q.eps = d.rms_eps;
+  q.x_dtype = P.ty.att; q.w_dtype = d.compute_dtype; q.d_dtype = P.ty.op;
+  q.qk = L.at(P.qkv); q.ld = P.qkv_cols;
+  q.raw = L.at(P.qkraw); q.rstd = static_cast<float *>(L.at(P.rstdqk));
+  q.gq = w.wp(st->pp.qn); q.gk = w.wp(st->pp.kn);
+  return q;
+}
+
 static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const void *x, void *y,
                                 int slot, hipStream_t s) {
   const lc_stage_desc &d = st->d;
@@ -227,7 +243,7 @@ static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const voi
   const ParamPlan &pp = st->pp;
   const int dt = d.compute_dtype;
   const StageTypes ty = P.ty;
-  const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const int64_t T = P.T, D = d.d_model, F = d.d_ff, Dkv = P.dkv, QC = P.qkv_cols;
   const size_t ea = dtype_size(ty.att);
   const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
   const float *rs = reinterpret_cast<const float *>(st->ws + P.rope_sin);
@@ -245,21 +261,29 @@ static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const voi
     na.n = L.at(P.n1); na.out_dtype = ty.op;
     na.rstd = static_cast<float *>(L.at(P.rstd1));
     LC_TRY(rmsnorm_fwd_launch(na, s));
-    // [q|k|v] = n1 [Wq;Wk;Wv]^T, RoPE on q and k
-    lc_gemm_args a = gemm_base(dt, LC_EPI_ROPE, T, 3 * D, D);
+    // [q|k|v] = n1 [Wq;Wk;Wv]^T, RoPE on q and k (after their per-head norm)
+    lc_gemm_args a = gemm_base(dt, d.qk_norm ? LC_EPI_STORE : LC_EPI_ROPE, T, QC, D);
     a.A = L.at(P.n1); a.lda = D; a.a_kmajor = 1;
     a.B = w.wp(pp.wq); a.ldb = D; a.b_kmajor = 1;
-    a.C = L.at(P.qkv); a.ldc = 3 * D; a.c_dtype = ty.att;
-    a.rope_cos = rc; a.rope_sin = rs; a.rope_seq = d.seq_len; a.rope_cols = (int)(2 * D);
-    a.head_dim = d.head_dim;
+    a.C = L.at(P.qkv); a.ldc = QC; a.c_dtype = ty.att;
+    if (!d.qk_norm) {
+      a.rope_cos = rc; a.rope_sin = rs; a.rope_seq = d.seq_len; a.rope_cols = (int)(D + Dkv);
+      a.head_dim = d.head_dim;
+    }
     LC_TRY(gemm_launch(a, s));
+    if (d.qk_norm) {
+      lc_qknorm_args qa = qknorm_base(st, w, L);
+      qa.rope_cos = rc; qa.rope_sin = rs;
+      LC_TRY(qknorm_fwd_launch(qa, s));
+    }
     // o = causal attention
     char *qkv = static_cast<char *>(L.at(P.qkv));
     lc_attn_args at;
     memset(&at, 0, sizeof at);
     at.dtype = ty.att; at.o_dtype = ty.op;
     at.B = d.micro_batch; at.S = d.seq_len; at.H = d.n_heads; at.hd = d.head_dim;
-    at.q = qkv; at.k = qkv + D * ea; at.v = qkv + 2 * D * ea; at.ld_qkv = 3 * D;
+    at.Hkv = kv_heads(d);
+    at.q = qkv; at.k = qkv + D * ea; at.v = qkv + (D + Dkv) * ea; at.ld_qkv = QC;
     at.o = L.at(P.o); at.ld_o = D; at.lse = static_cast<float *>(L.at(P.lse));
     LC_TRY(attn_fwd_launch(at, s));
     // h = x + o Wo^T
@@ -323,7 +347,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
   const bool split = wslot >= 0;
   // the weight products overwrite their gradient instead of adding into it
   const int gepi = st->grad_store ? LC_EPI_STORE_F32 : LC_EPI_ACCUM_F32;
-  const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const int64_t T = P.T, D = d.d_model, F = d.d_ff, Dkv = P.dkv, QC = P.qkv_cols;
   const size_t ea = dtype_size(ty.att), es = P.elem;
   const float *rc = reinterpret_cast<const float *>(st->ws + P.rope_cos);
   const float *rs = reinterpret_cast<const float *>(st->ws + P.rope_sin);
@@ -429,23 +453,38 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     memset(&at, 0, sizeof at);
     at.dtype = ty.att; at.o_dtype = ty.op;
     at.B = d.micro_batch; at.S = d.seq_len; at.H = d.n_heads; at.hd = d.head_dim;
-    at.q = qkv; at.k = qkv + D * ea; at.v = qkv + 2 * D * ea; at.ld_qkv = 3 * D;
+    at.Hkv = kv_heads(d);
+    at.q = qkv; at.k = qkv + D * ea; at.v = qkv + (D + Dkv) * ea; at.ld_qkv = QC;
     at.o = L.at(P.o); at.ld_o = D; at.lse = static_cast<float *>(L.at(P.lse));
     at.dout = dO;
-    at.dq = dqkv; at.dk = dqkv + D * es; at.dv = dqkv + 2 * D * es; at.ld_dqkv = 3 * D;
+    at.dq = dqkv; at.dk = dqkv + D * es; at.dv = dqkv + (D + Dkv) * es; at.ld_dqkv = QC;
     at.rope_cos = rc; at.rope_sin = rs;
     at.scratch = ws + P.s_attn; at.scratch_bytes = P.s_attn_bytes;
     LC_TRY(attn_bwd_launch(at, s));
+    // dq, dk through the per-head norms (in place); G[qn], G[kn] += ...
+    if (d.qk_norm) {
+      lc_qknorm_args qa = qknorm_base(st, w, L);
+      qa.dqk = dqkv; qa.ld_d = QC;
+      if (split) {
+        qa.scratch = WL.at(P.w_pqk); qa.scratch_bytes = qknorm_scratch_size(T, d.head_dim);
+        LC_TRY(qknorm_bwd_partials_launch(qa, s));
+      } else {
+        qa.scratch = ws + P.s_qkn; qa.scratch_bytes = P.s_qkn_bytes;
+        LC_TRY(qknorm_bwd_partials_launch(qa, s));
+        LC_TRY(qknorm_dg_final_launch(static_cast<const float *>(qa.scratch), w.gp(pp.qn),
+                                      w.gp(pp.kn), T, d.head_dim, st->grad_store, s));
+      }
+    }
     // dn1 = [dq|dk|dv] [Wq;Wk;Wv]
-    a = gemm_base(dt, LC_EPI_STORE, T, D, 3 * D);
-    a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 1;
+    a = gemm_base(dt, LC_EPI_STORE, T, D, QC);
+    a.A = dqkv; a.lda = QC; a.a_kmajor = 1;
     a.B = w.wp(pp.wq); a.ldb = D; a.b_kmajor = 0;
     a.C = dn; a.ldc = D; a.c_dtype = ty.res;
     LC_TRY(gemm_launch(a, s));
     // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
     if (!split) {
-      a = gemm_base(dt, gepi, 3 * D, D, T);
-      a.A = dqkv; a.lda = 3 * D; a.a_kmajor = 0;
+      a = gemm_base(dt, gepi, QC, D, T);
+      a.A = dqkv; a.lda = QC; a.a_kmajor = 0;
       a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
       a.C = w.gp(pp.wq); a.ldc = D;
       LC_TRY(gemm_launch(a, s));
@@ -480,7 +519,7 @@ static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, 
   const StagePlan &P = st->plan;
   const ParamPlan &pp = st->pp;
   const int dt = d.compute_dtype;
-  const int64_t T = P.T, D = d.d_model, F = d.d_ff;
+  const int64_t T = P.T, D = d.d_model, F = d.d_ff, QC = P.qkv_cols;
   const int gepi = st->grad_store ? LC_EPI_STORE_F32 : LC_EPI_ACCUM_F32;
   for (int l = d.n_layers - 1; l >= 0; --l) {
     const LayerBufs L = layer_bufs(st, slot, l);
@@ -508,13 +547,16 @@ static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, 
     a.C = w.gp(pp.wo); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
     // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
-    a = gemm_base(dt, gepi, 3 * D, D, T);
-    a.A = WL.at(P.w_dqkv); a.lda = 3 * D; a.a_kmajor = 0;
+    a = gemm_base(dt, gepi, QC, D, T);
+    a.A = WL.at(P.w_dqkv); a.lda = QC; a.a_kmajor = 0;
     a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.wq); a.ldc = D;
     LC_TRY(gemm_launch(a, s));
     LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p1)), w.gp(pp.g1), T, D, s,
                                    st->grad_store));
+    if (d.qk_norm)
+      LC_TRY(qknorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_pqk)), w.gp(pp.qn),
+                                    w.gp(pp.kn), T, d.head_dim, st->grad_store, s));
   }
   return LC_OK;
 }

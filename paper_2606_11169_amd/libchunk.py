@@ -34,7 +34,7 @@ LC_FP32, LC_BF16, LC_FP16 = 0, 1, 2
 LC_PASS_F, LC_PASS_B, LC_PASS_BI, LC_PASS_BW = 0, 1, 2, 3
 LC_ORDER_WITH_NEXT = 0x100
 (LC_T_WQ, LC_T_WK, LC_T_WV, LC_T_WO, LC_T_G1, LC_T_W1, LC_T_W3, LC_T_W2, LC_T_G2,
- LC_T_WR) = range(10)
+ LC_T_WR, LC_T_QN, LC_T_KN) = range(12)
 (LC_EPI_STORE, LC_EPI_STORE_F32, LC_EPI_ACCUM_F32, LC_EPI_RESIDUAL, LC_EPI_ROPE,
  LC_EPI_SWIGLU, LC_EPI_SWIGLU_BWD) = range(7)
 LC_GROUP_NONE, LC_GROUP_ROWS, LC_GROUP_K = 0, 1, 2
@@ -51,7 +51,8 @@ class lc_stage_desc(C.Structure):
                 ("head_dim", C.c_int32), ("d_ff", C.c_int32), ("n_experts", C.c_int32),
                 ("top_k", C.c_int32), ("d_ff_expert", C.c_int32), ("seq_len", C.c_int32),
                 ("micro_batch", C.c_int32), ("rms_eps", C.c_float), ("rope_base", C.c_float),
-                ("causal", C.c_int32), ("compute_dtype", C.c_int32)]
+                ("causal", C.c_int32), ("compute_dtype", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("qk_norm", C.c_int32)]
 
 
 class lc_order_entry(C.Structure):
@@ -128,7 +129,19 @@ class lc_attn_args(C.Structure):
                 ("o", C.c_void_p), ("ld_o", C.c_int64), ("lse", C.c_void_p),
                 ("dout", C.c_void_p), ("dq", C.c_void_p), ("dk", C.c_void_p), ("dv", C.c_void_p),
                 ("ld_dqkv", C.c_int64), ("rope_cos", C.c_void_p), ("rope_sin", C.c_void_p),
-                ("scratch", C.c_void_p), ("scratch_bytes", C.c_size_t)]
+                ("scratch", C.c_void_p), ("scratch_bytes", C.c_size_t),
+                ("Hkv", C.c_int32), ("reserved", C.c_int32)]
+
+
+class lc_qknorm_args(C.Structure):
+    _fields_ = [("T", C.c_int64), ("H", C.c_int32), ("Hkv", C.c_int32), ("hd", C.c_int32),
+                ("seq_len", C.c_int32), ("eps", C.c_float), ("x_dtype", C.c_int32),
+                ("w_dtype", C.c_int32), ("d_dtype", C.c_int32), ("qk", C.c_void_p),
+                ("ld", C.c_int64), ("raw", C.c_void_p), ("rstd", C.c_void_p),
+                ("gq", C.c_void_p), ("gk", C.c_void_p), ("rope_cos", C.c_void_p),
+                ("rope_sin", C.c_void_p), ("dqk", C.c_void_p), ("ld_d", C.c_int64),
+                ("dgq", C.c_void_p), ("dgk", C.c_void_p), ("store_dg", C.c_int32),
+                ("reserved", C.c_int32), ("scratch", C.c_void_p), ("scratch_bytes", C.c_size_t)]
 
 
 # name -> (restype, argtypes)
@@ -186,6 +199,10 @@ _SIGS = {
     "lc_attention_forward": (C.c_int, [C.POINTER(lc_attn_args), C.c_void_p]),
     "lc_attention_backward": (C.c_int, [C.POINTER(lc_attn_args), C.c_void_p]),
     "lc_attention_scratch_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32]),
+    "lc_attention_scratch_bytes_kv": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
+    "lc_qk_norm_rope_forward": (C.c_int, [C.POINTER(lc_qknorm_args), C.c_void_p]),
+    "lc_qk_norm_rope_backward": (C.c_int, [C.POINTER(lc_qknorm_args), C.c_void_p]),
+    "lc_qk_norm_scratch_bytes": (C.c_size_t, [C.c_int64, C.c_int32]),
     "lc_cast_bf16": (C.c_int, [C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "lc_moe_route": (C.c_int, [C.POINTER(lc_moe_args), C.c_void_p]),
     "lc_moe_dispatch": (C.c_int, [C.POINTER(lc_moe_args), C.c_void_p]),
@@ -244,10 +261,18 @@ def _vp(x):
 
 def make_desc(n_layers, d_model, n_heads, head_dim, d_ff, seq_len, micro_batch, bf16,
               n_experts=0, top_k=0, d_ff_expert=0, rms_eps=1e-5, rope_base=10000.0,
-              causal=1) -> lc_stage_desc:
+              causal=1, n_kv_heads=0, qk_norm=False) -> lc_stage_desc:
     return lc_stage_desc(n_layers, d_model, n_heads, head_dim, d_ff, n_experts, top_k,
                          d_ff_expert, seq_len, micro_batch, rms_eps, rope_base, causal,
-                         LC_BF16 if bf16 else LC_FP32)
+                         LC_BF16 if bf16 else LC_FP32, n_kv_heads, 1 if qk_norm else 0)
+
+
+def desc_of_config(cfg) -> lc_stage_desc:
+    """The descriptor of a synth.StageConfig."""
+    return make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
+                     cfg.seq_len, cfg.micro_batch, cfg.bf16, n_experts=cfg.n_experts,
+                     top_k=cfg.top_k, d_ff_expert=cfg.d_ff_expert, rms_eps=cfg.rms_eps,
+                     rope_base=cfg.rope_base, n_kv_heads=cfg.n_kv_heads, qk_norm=cfg.qk_norm)
 
 
 def lc_param_count(desc: lc_stage_desc) -> int:
@@ -323,8 +348,14 @@ def lc_rmsnorm_scratch_bytes(T, d) -> int:
     return int(lib().lc_rmsnorm_scratch_bytes(T, d))
 
 
-def lc_attention_scratch_bytes(B, S, H) -> int:
+def lc_attention_scratch_bytes(B, S, H, Hkv=0) -> int:
+    if Hkv:
+        return int(lib().lc_attention_scratch_bytes_kv(B, S, H, Hkv))
     return int(lib().lc_attention_scratch_bytes(B, S, H))
+
+
+def lc_qk_norm_scratch_bytes(T, hd) -> int:
+    return int(lib().lc_qk_norm_scratch_bytes(T, hd))
 
 
 # ------------------------------------------------------------------ stage
@@ -489,7 +520,8 @@ def _fill(struct, **kw):
 
 
 _PTR_FIELDS = {"x", "g", "n", "rstd", "dn", "dres", "dx", "dx_copy", "dg_accum", "scratch", "q",
-               "k", "v", "o", "lse", "dout", "dq", "dk", "dv", "rope_cos", "rope_sin"}
+               "k", "v", "o", "lse", "dout", "dq", "dk", "dv", "rope_cos", "rope_sin", "qk",
+               "raw", "gq", "gk", "dqk", "dgq", "dgk"}
 
 
 def lc_rmsnorm_forward(T, d, x, g, eps, n, rstd, x_dtype, w_dtype, out_dtype, stream=None):
@@ -508,20 +540,41 @@ def lc_rmsnorm_backward(T, d, dn, x, rstd, g, dres, dx, dg_accum, scratch, scrat
     return _check(lib().lc_rmsnorm_backward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
 
 
-def lc_attention_forward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, ld_o, lse, stream=None):
+def lc_attention_forward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, ld_o, lse, stream=None,
+                         Hkv=0):
     a = _fill(lc_attn_args(), dtype=dtype, o_dtype=o_dtype, B=B, S=S, H=H, hd=hd, q=q, k=k, v=v,
-              ld_qkv=ld_qkv, o=o, ld_o=ld_o, lse=lse)
+              ld_qkv=ld_qkv, o=o, ld_o=ld_o, lse=lse, Hkv=Hkv)
     return _check(lib().lc_attention_forward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
 
 
 def lc_attention_backward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, dout, ld_o, lse, dq,
                           dk, dv, ld_dqkv, rope_cos, rope_sin, scratch, scratch_bytes,
-                          stream=None):
+                          stream=None, Hkv=0):
     a = _fill(lc_attn_args(), dtype=dtype, o_dtype=o_dtype, B=B, S=S, H=H, hd=hd, q=q, k=k, v=v,
               ld_qkv=ld_qkv, o=o, ld_o=ld_o, lse=lse, dout=dout, dq=dq, dk=dk, dv=dv,
               ld_dqkv=ld_dqkv, rope_cos=rope_cos, rope_sin=rope_sin, scratch=scratch,
-              scratch_bytes=scratch_bytes)
+              scratch_bytes=scratch_bytes, Hkv=Hkv)
     return _check(lib().lc_attention_backward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_qk_norm_rope_forward(T, H, Hkv, hd, seq_len, eps, qk, ld, raw, rstd, gq, gk, x_dtype,
+                            w_dtype, rope_cos, rope_sin, stream=None):
+    a = _fill(lc_qknorm_args(), T=T, H=H, Hkv=Hkv, hd=hd, seq_len=seq_len, eps=eps, qk=qk, ld=ld,
+              raw=raw, rstd=rstd, gq=gq, gk=gk, x_dtype=x_dtype, w_dtype=w_dtype,
+              rope_cos=rope_cos, rope_sin=rope_sin)
+    return _check(lib().lc_qk_norm_rope_forward(C.byref(a),
+                                                C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_qk_norm_rope_backward(T, H, Hkv, hd, seq_len, eps, raw, rstd, gq, gk, x_dtype, w_dtype,
+                             dqk, ld_d, d_dtype, dgq, dgk, scratch, scratch_bytes, store_dg=0,
+                             stream=None):
+    a = _fill(lc_qknorm_args(), T=T, H=H, Hkv=Hkv, hd=hd, seq_len=seq_len, eps=eps, raw=raw,
+              rstd=rstd, gq=gq, gk=gk, x_dtype=x_dtype, w_dtype=w_dtype, dqk=dqk, ld_d=ld_d,
+              d_dtype=d_dtype, dgq=dgq, dgk=dgk, scratch=scratch, scratch_bytes=scratch_bytes,
+              store_dg=store_dg)
+    return _check(lib().lc_qk_norm_rope_backward(C.byref(a),
+                                                 C.c_void_p(stream_ptr(stream) or None)))
 
 
 def lc_moe_route(T, d, E, n, wr, sel, w, n_dtype, w_dtype, stream=None):

@@ -143,7 +143,8 @@ class StageRunner:
 def random_stage(desc: lc.lc_stage_desc, max_in_flight: int, seed: int = 0, device="cuda",
                  stream=None, max_w_pending: int = 0) -> StageRunner:
     """A StageRunner with weights drawn on the device: matrices ~ N(0, 0.02)
-    in the compute dtype, RMSNorm gains = 1 (benchmark inputs)."""
+    in the compute dtype, RMSNorm gains (and q/k norm gains) = 1 (benchmark
+    inputs)."""
     require_gpu()
     r = StageRunner.__new__(StageRunner)
     r.desc = desc
@@ -156,8 +157,9 @@ def random_stage(desc: lc.lc_stage_desc, max_in_flight: int, seed: int = 0, devi
     g.manual_seed(seed)
     master = torch.randn(r.n_params, generator=g, device=device, dtype=torch.float32)
     master.mul_(0.02)
+    gains = (lc.LC_T_G1, lc.LC_T_G2) + ((lc.LC_T_QN, lc.LC_T_KN) if desc.qk_norm else ())
     for l in range(desc.n_layers):
-        for t in (lc.LC_T_G1, lc.LC_T_G2):
+        for t in gains:
             off, (n, _) = lc.lc_param_offset(desc, l, t)
             master[off:off + n] = 1.0
     r.w = master.to(r.dtype) if r.bf16 else master

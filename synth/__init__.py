@@ -46,6 +46,8 @@ class StageConfig:
     d_ff_expert: int = 0
     rms_eps: float = 1e-5
     rope_base: float = 10000.0
+    n_kv_heads: int = 0    # key/value heads (grouped-query attention); 0 = n_heads
+    qk_norm: bool = False  # per-head RMSNorm of q and k before RoPE (Qwen3)
     pp_size: int = 2       # pipeline depth used to build the 1F1B Order
     pp_rank: int = 0       # this stage's index in the pipeline
     # AdamW hyper-parameters applied after the last backward of a step
@@ -62,6 +64,10 @@ class StageConfig:
     @property
     def moe(self) -> bool:
         return self.n_experts > 0
+
+    @property
+    def kv_heads(self) -> int:
+        return self.n_kv_heads or self.n_heads
 
 
 @dataclasses.dataclass(frozen=True)
@@ -103,7 +109,16 @@ ADAM_1P6B = AdamShardConfig(
     name="adam_shard_1p6e9", n=1_600_000_000, lr=3e-4, beta1=0.9, beta2=0.95,
     eps=1e-8, weight_decay=0.1, p_std=0.02, g_std=1e-3)
 
-STAGES = {c.name: c for c in (TINY_FP32, LLAMA_2K, STAGE_7B, MOE_2K)}
+# Qwen3-8B-shaped stage: 4 layers of d 4096, 32 query heads and 8 key/value
+# heads of 128, per-head q/k RMSNorm, SwiGLU 12288
+QWEN3_STAGE = StageConfig(
+    name="qwen3_4L_d4096_kv8_s4096", n_layers=4, d_model=4096, n_heads=32,
+    head_dim=128, d_ff=12288, seq_len=4096, micro_batch=1, num_microbatches=16,
+    bf16=True, n_kv_heads=8, qk_norm=True, rms_eps=1e-6, rope_base=1000000.0,
+    pp_size=8, pp_rank=0, lr=3e-4, beta1=0.9, beta2=0.95, adam_eps=1e-8,
+    weight_decay=0.1)
+
+STAGES = {c.name: c for c in (TINY_FP32, LLAMA_2K, STAGE_7B, MOE_2K, QWEN3_STAGE)}
 
 
 def scaled(cfg: StageConfig, **kw) -> StageConfig:
@@ -122,12 +137,14 @@ DENSE_TENSORS = ("wq", "wk", "wv", "wo", "g1", "w1", "w3", "w2", "g2")
 def layout(cfg: StageConfig) -> List[Tuple[str, int, Tuple[int, ...]]]:
     """[(name, offset, shape)] of every parameter tensor in the flat bucket.
 
-    Per layer l: Wq, Wk, Wv, Wo [d, d]; g1 [d]; then either the dense FFN
+    Per layer l: Wq [d, d], Wk, Wv [kv_heads * hd, d], Wo [d, d]; g1 [d];
+    with qk_norm the q and k gains qn, kn [hd]; then either the dense FFN
     W1 (gate) [f, d], W3 (up) [f, d], W2 (down) [d, f], or the MoE block
     Wr [E, d] followed by W1_e, W3_e [fe, d], W2_e [d, fe] per expert e;
     then g2 [d]. Weights are [out, in] row-major.
     """
     d, f = cfg.d_model, cfg.d_ff
+    dkv = cfg.kv_heads * cfg.head_dim
     out = []
     off = 0
 
@@ -137,9 +154,14 @@ def layout(cfg: StageConfig) -> List[Tuple[str, int, Tuple[int, ...]]]:
         off += int(np.prod(shape))
 
     for l in range(cfg.n_layers):
-        for t in ("wq", "wk", "wv", "wo"):
-            add(f"L{l}.{t}", (d, d))
+        add(f"L{l}.wq", (d, d))
+        add(f"L{l}.wk", (dkv, d))
+        add(f"L{l}.wv", (dkv, d))
+        add(f"L{l}.wo", (d, d))
         add(f"L{l}.g1", (d,))
+        if cfg.qk_norm:
+            add(f"L{l}.qn", (cfg.head_dim,))
+            add(f"L{l}.kn", (cfg.head_dim,))
         if cfg.moe:
             fe = cfg.d_ff_expert
             add(f"L{l}.wr", (cfg.n_experts, d))
@@ -206,7 +228,7 @@ def stage_params(cfg: StageConfig, seed: int = 0,
     w = np.empty(n, dtype=np.float32)
     for tid, (name, off, shape) in enumerate(layout(cfg)):
         sz = int(np.prod(shape))
-        if name.endswith(".g1") or name.endswith(".g2"):
+        if name.endswith((".g1", ".g2", ".qn", ".kn")):
             if random_gains:
                 w[off:off + sz] = 1.0 + normal(seed, tid, sz, 0.1)
             else:

@@ -434,3 +434,140 @@ def test_attention_identical_keys_prefix_mean(dt):
     v = qkv[:, :, 2].astype(np.float64)
     prefix_mean = np.cumsum(v, axis=1) / np.arange(1, S + 1)[None, :, None, None]
     assert rel_err(host(o).reshape(B, S, H, hd), prefix_mean) <= 1e-2
+
+
+# ---------------------------------------------------------------- grouped-query attention
+
+def gqa_case(B, S, H, Hkv, hd, dt, seed, rope):
+    """Packed rows [q (H heads) | k (Hkv) | v (Hkv)] against the oracle's
+    attention over key/value heads repeated per group (query head h reads
+    key/value head h // (H / Hkv)); dk, dv sum over each group."""
+    banner(f"gqa attention B={B} S={S} H={H} Hkv={Hkv} hd={hd} dtype={dt} rope={rope}")
+    rng = np.random.default_rng(seed)
+    d, dkv = H * hd, Hkv * hd
+    G = H // Hkv
+    ld = d + 2 * dkv
+    mc = dt != lc.LC_FP32
+    o_dt = lc.LC_BF16 if mc else lc.LC_FP32
+    esz = 2 if mc else 4
+    qkv, qkvd = typed(rng.standard_normal((B * S, ld)), dt)
+    q = qkv[:, :d].reshape(B, S, H, hd).astype(np.float64)
+    k = qkv[:, d:d + dkv].reshape(B, S, Hkv, hd).astype(np.float64)
+    v = qkv[:, d + dkv:].reshape(B, S, Hkv, hd).astype(np.float64)
+    base = qkvd.data_ptr()
+    o = torch.empty((B * S, d), dtype=TORCH_DT[o_dt], device=DEV)
+    lse = torch.empty(B * H * S, dtype=torch.float32, device=DEV)
+    lc.lc_attention_forward(dt, o_dt, B, S, H, hd, base, base + d * esz, base + (d + dkv) * esz,
+                            ld, o, d, lse, Hkv=Hkv)
+    o_ref = OS.attention_forward(q, OS.repeat_kv(k, G), OS.repeat_kv(v, G))
+    tol = 2e-2 if mc else 1e-4
+    torch.cuda.synchronize()
+    assert rel_err(host(o).reshape(B, S, H, hd), o_ref) <= tol / 2
+    do, dod = typed(rng.standard_normal((B * S, d)), o_dt)
+    dqkv = torch.full((B * S, ld), float("nan"), dtype=TORCH_DT[o_dt], device=DEV)
+    cos = sin = None
+    if rope:
+        cos, sin = OS.rope_tables(S, hd, 10000.0)
+    sb = lc.lc_attention_scratch_bytes(B, S, H, Hkv)
+    scratch = torch.empty(sb, dtype=torch.uint8, device=DEV)
+    g0 = dqkv.data_ptr()
+    lc.lc_attention_backward(dt, o_dt, B, S, H, hd, base, base + d * esz, base + (d + dkv) * esz,
+                             ld, o, dod, d, lse, g0, g0 + d * esz, g0 + (d + dkv) * esz, ld,
+                             None if cos is None else f32(cos), None if sin is None else f32(sin),
+                             scratch, sb, Hkv=Hkv)
+    dq, dke, dve = OS.attention_backward(do.reshape(B, S, H, hd).astype(np.float64), q,
+                                         OS.repeat_kv(k, G), OS.repeat_kv(v, G))
+    dk, dv = OS.sum_groups(dke, G), OS.sum_groups(dve, G)
+    if rope:
+        dq = OS.rope_apply(dq, cos, sin, inverse=True)
+        dk = OS.rope_apply(dk, cos, sin, inverse=True)
+    torch.cuda.synchronize()
+    got = host(dqkv)
+    errs = [rel_err(got[:, :d].reshape(B, S, H, hd), dq),
+            rel_err(got[:, d:d + dkv].reshape(B, S, Hkv, hd), dk),
+            rel_err(got[:, d + dkv:].reshape(B, S, Hkv, hd), dv)]
+    print(f"gqa errors: dq {errs[0]:.2e} dk {errs[1]:.2e} dv {errs[2]:.2e}", flush=True)
+    for i, e in enumerate(errs):
+        assert e <= tol, ("dq", "dk", "dv")[i]
+
+
+@pytest.mark.parametrize("dt", [lc.LC_FP16, lc.LC_BF16], ids=["fp16", "bf16"])
+@pytest.mark.parametrize("H,Hkv", [(4, 1), (4, 2), (2, 2)])
+def test_gqa_attention_matrix_cores(H, Hkv, dt):
+    gqa_case(2, 256, H, Hkv, 128, dt, 21, True)
+
+
+@pytest.mark.parametrize("H,Hkv", [(4, 2), (6, 3)])
+def test_gqa_attention_fp32(H, Hkv):
+    gqa_case(2, 64, H, Hkv, 32, lc.LC_FP32, 22, True)
+
+
+# ---------------------------------------------------------------- per-head q/k norm
+
+@pytest.mark.parametrize("x_dt,d_dt,w_dt,hd", [(lc.LC_FP16, lc.LC_BF16, lc.LC_BF16, 128),
+                                               (lc.LC_FP32, lc.LC_FP32, lc.LC_FP32, 32),
+                                               (lc.LC_FP32, lc.LC_FP32, lc.LC_FP32, 64)],
+                         ids=["bf16_stage", "fp32_hd32", "fp32_hd64"])
+def test_qk_norm_rope(x_dt, d_dt, w_dt, hd):
+    """RMSNorm over each q and k head row, gains qn / kn, then RoPE (forward);
+    the backward maps the gradient at the normalised rows to the raw rows and
+    sums the gain gradients, against the oracle's RMSNorm and RoPE."""
+    banner(f"q/k norm x={x_dt} d={d_dt} hd={hd}")
+    rng = np.random.default_rng(23)
+    B, S, H, Hkv = 2, 24, 4, 2
+    T = B * S
+    d, dkv = H * hd, Hkv * hd
+    ld = d + 2 * dkv + 8  # a padded row, v columns untouched
+    eps = 1e-6
+    x, xd = typed(rng.standard_normal((T, ld)) * 3.0, x_dt)
+    gq, gqd = typed(1.0 + 0.1 * rng.standard_normal(hd), w_dt)
+    gk, gkd = typed(1.0 + 0.1 * rng.standard_normal(hd), w_dt)
+    cos, sin = OS.rope_tables(S, hd, 10000.0)
+    raw = torch.empty((T, d + dkv), dtype=TORCH_DT[x_dt], device=DEV)
+    rstd = torch.empty(T * (H + Hkv), dtype=torch.float32, device=DEV)
+    lc.lc_qk_norm_rope_forward(T, H, Hkv, hd, S, eps, xd, ld, raw, rstd, gqd, gkd, x_dt, w_dt,
+                               f32(cos), f32(sin))
+    torch.cuda.synchronize()
+    xq = x[:, :d].reshape(B, S, H, hd).astype(np.float64)
+    xk = x[:, d:d + dkv].reshape(B, S, Hkv, hd).astype(np.float64)
+    yq, rq = OS.rmsnorm_forward(xq, gq.astype(np.float64), eps)
+    yk, rk = OS.rmsnorm_forward(xk, gk.astype(np.float64), eps)
+    zq, zk = OS.rope_apply(yq, cos, sin), OS.rope_apply(yk, cos, sin)
+    got = host(xd)
+    tol = ROUND_TOL[x_dt] + 1e-5
+    assert rel_err(got[:, :d].reshape(B, S, H, hd), zq) <= tol
+    assert rel_err(got[:, d:d + dkv].reshape(B, S, Hkv, hd), zk) <= tol
+    assert np.array_equal(got[:, d + dkv:], x[:, d + dkv:])  # v and padding untouched
+    assert np.array_equal(host(raw), x[:, :d + dkv])
+    r_ref = np.concatenate([rq.reshape(T, H), rk.reshape(T, Hkv)], axis=1)
+    assert rel_err(host(rstd).reshape(T, H + Hkv), r_ref) <= 1e-5
+    # backward: dy at the normalised (unrotated) rows, in place
+    dy, dyd = typed(rng.standard_normal((T, ld)), d_dt)
+    dg = torch.full((2 * hd,), 0.5, dtype=torch.float32, device=DEV)
+    sb = lc.lc_qk_norm_scratch_bytes(T, hd)
+    scratch = torch.empty(sb, dtype=torch.uint8, device=DEV)
+    lc.lc_qk_norm_rope_backward(T, H, Hkv, hd, S, eps, raw, rstd, gqd, gkd, x_dt, w_dt, dyd, ld,
+                                d_dt, dg[:hd], dg[hd:], scratch, sb)
+    torch.cuda.synchronize()
+    xr = host(raw)  # the kernel's own raw rows and rstd: the reference uses them too
+    rr = host(rstd).reshape(T, H + Hkv)
+    dxq, dgq = OS.rmsnorm_backward(dy[:, :d].reshape(T, H, hd).astype(np.float64),
+                                   xr[:, :d].reshape(T, H, hd), rr[:, :H, None],
+                                   gq.astype(np.float64))
+    dxk, dgk = OS.rmsnorm_backward(dy[:, d:d + dkv].reshape(T, Hkv, hd).astype(np.float64),
+                                   xr[:, d:].reshape(T, Hkv, hd), rr[:, H:, None],
+                                   gk.astype(np.float64))
+    got = host(dyd)
+    tol = ROUND_TOL[d_dt] + 1e-5
+    assert rel_err(got[:, :d].reshape(T, H, hd), dxq) <= tol
+    assert rel_err(got[:, d:d + dkv].reshape(T, Hkv, hd), dxk) <= tol
+    assert np.array_equal(got[:, d + dkv:], dy[:, d + dkv:])
+    gg = host(dg)
+    assert rel_err(gg[:hd], 0.5 + dgq) <= 1e-5 and rel_err(gg[hd:], 0.5 + dgk) <= 1e-5
+    # the same call twice gives the same bits (fixed reduction order)
+    dyd2 = torch.from_numpy(dy).to(TORCH_DT[d_dt]).to(DEV)
+    dg2 = torch.full((2 * hd,), 0.5, dtype=torch.float32, device=DEV)
+    lc.lc_qk_norm_rope_backward(T, H, Hkv, hd, S, eps, raw, rstd, gqd, gkd, x_dt, w_dt, dyd2, ld,
+                                d_dt, dg2[:hd], dg2[hd:], scratch, sb)
+    torch.cuda.synchronize()
+    assert torch.equal(dyd2, dyd) and torch.equal(dg2, dg)

@@ -218,10 +218,7 @@ SMALL_MOE = synth.StageConfig(
 
 
 def desc_of(cfg):
-    return lc.make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
-                        cfg.seq_len, cfg.micro_batch, cfg.bf16, n_experts=cfg.n_experts,
-                        top_k=cfg.top_k, d_ff_expert=cfg.d_ff_expert, rms_eps=cfg.rms_eps,
-                        rope_base=cfg.rope_base)
+    return lc.desc_of_config(cfg)
 
 
 def test_moe_stage_matches_oracle_with_gpu_routing():

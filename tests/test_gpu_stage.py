@@ -35,10 +35,7 @@ def _gpu():
 
 
 def desc_of(cfg):
-    return lc.make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
-                        cfg.seq_len, cfg.micro_batch, cfg.bf16, n_experts=cfg.n_experts,
-                        top_k=cfg.top_k, d_ff_expert=cfg.d_ff_expert, rms_eps=cfg.rms_eps,
-                        rope_base=cfg.rope_base)
+    return lc.desc_of_config(cfg)
 
 
 PASS = {"F": lc.LC_PASS_F, "B": lc.LC_PASS_B, "Bi": lc.LC_PASS_BI, "Bw": lc.LC_PASS_BW}
@@ -90,10 +87,20 @@ def per_tensor_errors(cfg, got, ref):
 SMALL_BF16 = synth.StageConfig(
     name="small_bf16", n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ff=512, seq_len=256,
     micro_batch=2, num_microbatches=3, bf16=True, pp_size=3, pp_rank=0)
+# Qwen3-style variant (per-head q/k RMSNorm, grouped-query attention)
+QWEN_BF16 = synth.StageConfig(
+    name="qwen_bf16", n_layers=2, d_model=512, n_heads=4, head_dim=128, d_ff=512, seq_len=256,
+    micro_batch=2, num_microbatches=3, bf16=True, n_kv_heads=2, qk_norm=True, rms_eps=1e-6,
+    rope_base=1000000.0, pp_size=3, pp_rank=0)
+QWEN_FP32 = synth.StageConfig(
+    name="qwen_fp32", n_layers=2, d_model=128, n_heads=4, head_dim=32, d_ff=344, seq_len=64,
+    micro_batch=2, num_microbatches=4, bf16=False, n_kv_heads=2, qk_norm=True, rms_eps=1e-6,
+    pp_size=2, pp_rank=0)
 
 
-@pytest.mark.parametrize("cfg,tol", [(synth.TINY_FP32, 1e-4), (SMALL_BF16, 2e-2)],
-                         ids=["tiny_fp32", "small_bf16"])
+@pytest.mark.parametrize("cfg,tol", [(synth.TINY_FP32, 1e-4), (SMALL_BF16, 2e-2),
+                                     (QWEN_FP32, 1e-4), (QWEN_BF16, 2e-2)],
+                         ids=["tiny_fp32", "small_bf16", "qwen_fp32", "qwen_bf16"])
 def test_stage_matches_oracle(cfg, tol):
     banner(f"stage {cfg.name}")
     flat, Xs, dYs = inputs(cfg)
@@ -182,8 +189,9 @@ def test_stage_error_paths_have_no_side_effects():
     r.close()
 
 
-@pytest.mark.parametrize("cfg,tol", [(synth.TINY_FP32, 1e-4), (SMALL_BF16, 2e-2)],
-                         ids=["tiny_fp32", "small_bf16"])
+@pytest.mark.parametrize("cfg,tol", [(synth.TINY_FP32, 1e-4), (SMALL_BF16, 2e-2),
+                                     (QWEN_BF16, 2e-2)],
+                         ids=["tiny_fp32", "small_bf16", "qwen_bf16"])
 def test_split_backward_matches_full_backward_and_oracle(cfg, tol):
     """Bi + Bw (PASS values of Section 4.1): with the Bw entries in
     microbatch order, adjacent or deferred, every output and the gradient are
@@ -248,7 +256,8 @@ def test_overlapped_pairs_on_two_streams_are_bit_identical(cfg):
     ref.close()
 
 
-@pytest.mark.parametrize("cfg", [synth.TINY_FP32, SMALL_BF16], ids=["tiny_fp32", "small_bf16"])
+@pytest.mark.parametrize("cfg", [synth.TINY_FP32, SMALL_BF16, QWEN_BF16],
+                         ids=["tiny_fp32", "small_bf16", "qwen_bf16"])
 def test_zero_paths_give_the_accumulated_gradient_slices(cfg):
     """ZeRO-2/3 on one GPU (each backward into a temporary full gradient,
     then this rank's slice added into its persistent shard; at level 3 the
@@ -347,8 +356,9 @@ def test_split_backward_error_paths():
 
 
 @pytest.mark.parametrize("cfg,tol", [(synth.STAGE_7B, 2e-2),
-                                     (synth.scaled(synth.STAGE_7B, bf16=False), 1e-4)],
-                         ids=["stage7b_bf16", "stage7b_fp32"])
+                                     (synth.scaled(synth.STAGE_7B, bf16=False), 1e-4),
+                                     (synth.QWEN3_STAGE, 2e-2)],
+                         ids=["stage7b_bf16", "stage7b_fp32", "qwen3_bf16"])
 def test_full_size_stage_on_a_prefix(cfg, tol):
     P = 128
     banner(f"full-size {cfg.name} prefix {P}")

@@ -41,15 +41,12 @@ def test_library_exports_every_declared_function():
 
 
 def desc_of(cfg):
-    return lc.make_desc(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
-                        cfg.seq_len, cfg.micro_batch, cfg.bf16, n_experts=cfg.n_experts,
-                        top_k=cfg.top_k, d_ff_expert=cfg.d_ff_expert, rms_eps=cfg.rms_eps,
-                        rope_base=cfg.rope_base)
+    return lc.desc_of_config(cfg)
 
 
 TID = {"wq": lc.LC_T_WQ, "wk": lc.LC_T_WK, "wv": lc.LC_T_WV, "wo": lc.LC_T_WO,
        "g1": lc.LC_T_G1, "w1": lc.LC_T_W1, "w3": lc.LC_T_W3, "w2": lc.LC_T_W2,
-       "g2": lc.LC_T_G2, "wr": lc.LC_T_WR}
+       "g2": lc.LC_T_G2, "wr": lc.LC_T_WR, "qn": lc.LC_T_QN, "kn": lc.LC_T_KN}
 
 
 @pytest.mark.parametrize("cfg", list(synth.STAGES.values()), ids=list(synth.STAGES))

@@ -7,6 +7,10 @@ mathematics, independent of the oracle's own code:
 * causality of Y and of dX
 * accumulated microbatch gradients == full-batch gradient
 * closed forms of RMSNorm, RoPE, SwiGLU and the top-2 router
+* the Qwen3-style variant (per-head q/k RMSNorm, grouped-query attention):
+  finite differences, equality with multi-head attention whose key/value
+  heads are repeated per group, unit-RMS normalised heads and invariance
+  to a per-head scale of Wq, Wk
 """
 import numpy as np
 import pytest
@@ -64,7 +68,7 @@ def random_inputs(cfg, seed):
     # larger weights than the workload's 0.02 so every term matters
     flat = flat * 10.0
     for name, off, shape in synth.layout(cfg):
-        if name.endswith(".g1") or name.endswith(".g2"):
+        if name.endswith((".g1", ".g2", ".qn", ".kn")):
             flat[off:off + int(np.prod(shape))] /= 10.0
     X = rng.standard_normal((cfg.micro_batch, cfg.seq_len, cfg.d_model))
     dY = rng.standard_normal(X.shape)
@@ -380,3 +384,89 @@ def test_split_backward_gives_the_full_backward():
     assert np.max(np.abs(got[2] - full[2])) <= 1e-12 * np.max(np.abs(full[2]))
     for i in range(4):
         assert np.array_equal(got[1][i], full[1][i])
+
+
+# ---------------------------------------------------------------- Qwen3 variant
+
+def qwen_cfg(**kw):
+    base = dict(name="fdqwen", n_layers=2, d_model=32, n_heads=4, head_dim=8, d_ff=40,
+                seq_len=8, micro_batch=2, num_microbatches=2, bf16=False, n_kv_heads=2,
+                qk_norm=True)
+    base.update(kw)
+    return synth.StageConfig(**base)
+
+
+def test_fd_qwen3_variant_joint_and_per_tensor():
+    cfg = qwen_cfg()
+    flat, X, dY = random_inputs(cfg, 5)
+    rng = np.random.default_rng(13)
+    fd_check(cfg, flat, X, dY, rng.standard_normal(flat.shape), rng.standard_normal(X.shape))
+    cfg1 = qwen_cfg(n_layers=1)
+    flat, X, dY = random_inputs(cfg1, 6)
+    names = [n for n, _, _ in synth.layout(cfg1)]
+    assert "L0.qn" in names and "L0.kn" in names
+    for name, off, shape in synth.layout(cfg1):
+        u = np.zeros_like(flat)
+        sz = int(np.prod(shape))
+        u[off:off + sz] = rng.standard_normal(sz)
+        fd_check(cfg1, flat, X, dY, u, np.zeros_like(X))
+
+
+@pytest.mark.parametrize("qk_norm", [False, True])
+def test_gqa_equals_mha_with_repeated_kv_heads(qk_norm):
+    """Query head h of a grouped-query layer reads key/value head h // G: the
+    same layer with multi-head attention whose Wk, Wv row blocks are those of
+    head h // G gives the same Y and dX, and the grouped Wk, Wv gradients
+    are the sums of the repeated blocks' gradients."""
+    G = 2
+    gq = qwen_cfg(n_layers=1, qk_norm=qk_norm)
+    mh = qwen_cfg(n_layers=1, qk_norm=qk_norm, n_kv_heads=0)
+    flat, X, dY = random_inputs(gq, 8)
+    named = synth.unflatten(gq, flat)
+    hd, H = gq.head_dim, gq.n_heads
+    rep = {}
+    for name, off, shape in synth.layout(mh):
+        if name.endswith((".wk", ".wv")):
+            src = named[name].reshape(H // G, hd, -1)
+            rep[name] = np.repeat(src, G, axis=0).reshape(shape)
+        else:
+            rep[name] = named[name]
+    flat_mh = synth.flatten(mh, rep)
+    Yg, dXg, Gg = grads(gq, flat, X, dY)
+    Ym, dXm, Gm = grads(mh, flat_mh, X, dY)
+    assert np.allclose(Yg, Ym, rtol=0, atol=1e-12 * np.max(np.abs(Ym)))
+    assert np.allclose(dXg, dXm, rtol=0, atol=1e-12 * np.max(np.abs(dXm)))
+    gg, gm = synth.unflatten(gq, Gg), synth.unflatten(mh, Gm)
+    for name in gg:
+        if name.endswith((".wk", ".wv")):
+            want = gm[name].reshape(H // G, G, hd, -1).sum(axis=1).reshape(gg[name].shape)
+        else:
+            want = gm[name]
+        assert np.allclose(gg[name], want, rtol=0, atol=1e-11 * max(np.max(np.abs(want)), 1e-30)), name
+
+
+def test_qk_norm_unit_rms_and_scale_invariance():
+    """With gains 1 and eps 0 every rotated q and k head row has mean square
+    1 (RoPE keeps the norm, up to the fp32 rounding of its cos/sin table:
+    |cos^2 + sin^2 - 1| < 2^-22); scaling each head's rows of Wq and Wk by its
+    own positive constant leaves Y unchanged."""
+    cfg = qwen_cfg(n_layers=1, rms_eps=0.0)
+    flat = synth.stage_params(cfg, seed=9).astype(F64) * 10.0
+    named = synth.unflatten(cfg, flat)
+    for name in named:
+        if name.endswith((".g1", ".g2", ".qn", ".kn")):
+            named[name][:] = 1.0
+    flat = synth.flatten(cfg, named)
+    rng = np.random.default_rng(9)
+    X = rng.standard_normal((cfg.micro_batch, cfg.seq_len, cfg.d_model))
+    layers = O.layer_params(cfg, flat)
+    tabs = O.rope_tables(cfg.seq_len, cfg.head_dim, cfg.rope_base)
+    Y, c = O.layer_forward(layers[0], X, cfg, tabs)
+    for t in (c["qr"], c["kr"]):
+        assert np.allclose(np.mean(t * t, axis=-1), 1.0, rtol=0, atol=5e-7)
+    hd = cfg.head_dim
+    for name, nh in ((".wq", cfg.n_heads), (".wk", cfg.kv_heads)):
+        w = named["L0" + name].reshape(nh, hd, -1)
+        w *= rng.uniform(0.5, 3.0, size=(nh, 1, 1))
+    Y2, _ = O.layer_forward(O.layer_params(cfg, synth.flatten(cfg, named))[0], X, cfg, tabs)
+    assert np.max(np.abs(Y2 - Y)) <= 1e-12 * np.max(np.abs(Y))

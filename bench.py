@@ -47,7 +47,8 @@ def stage_flops_per_mb(cfg) -> float:
         ffn = 2.0 * (cfg.top_k * T) * d * (3 * cfg.d_ff_expert)
     else:
         ffn = 2.0 * T * d * (3 * f)
-    gemm = 2.0 * T * d * (3 * d + d) + ffn
+    dkv = cfg.kv_heads * hd  # grouped-query attention: narrower k, v projections
+    gemm = 2.0 * T * d * (d + 2 * dkv + d) + ffn
     attn = 4.0 * (S * (S + 1) / 2) * hd * H * b
     return 3.0 * cfg.n_layers * (gemm + attn)
 
@@ -339,6 +340,11 @@ def main():
     ap.add_argument("--split-only", type=int, default=None, metavar="W_DELAY",
                     help="only the 7B-shaped stage with split backwards (Bw W_DELAY "
                          "backwards after its Bi)")
+    ap.add_argument("--qwen3-only", action="store_true",
+                    help="only the Qwen3-8B-shaped stage (q/k norm, 8 key/value heads), flat "
+                         "and with overlapped pairs")
+    ap.add_argument("--flat", action="store_true",
+                    help="with --qwen3-only: the flat Order only (per-kernel profiles)")
     ap.add_argument("--zero-only", action="store_true",
                     help="only the 7B-shaped stage as rank 0 of 8 under ZeRO-2 and ZeRO-3")
     ap.add_argument("--overlap-only", action="store_true",
@@ -374,6 +380,20 @@ def main():
                                           "value": round(stf, 2), "unit": "TFLOP/s",
                                           "ms_per_step": round(sms, 2),
                                           "outputs_finite": sfin}}))
+        return
+    if args.qwen3_only:
+        qc = synth.QWEN3_STAGE
+        res = {}
+        for ov in ((False,) if args.flat else (False, True)):
+            qms, qtf, qfin = time_stage(torch, lc, qc, stream, args.steps, args.warmup, "qwen3",
+                                        overlap=ov)
+            res["overlap" if ov else "flat"] = {
+                "value": round(qtf, 2), "unit": "TFLOP/s", "ms_per_step": round(qms, 2),
+                "frac": round(qtf / BF16_PEAK_TFLOPS, 4), "outputs_finite": qfin}
+        print(json.dumps({"qwen3_stage": {
+            "workload": qc.name,
+            "algorithmic_tflop_per_step": round(stage_flops_per_mb(qc) * qc.num_microbatches / 1e12, 2),
+            **res}}))
         return
     if args.zero_only:
         res = {}

@@ -5,16 +5,19 @@
 //             dx_tk = dres_tk + rstd_t (dxh_tk - xh_tk * mean_k(dxh*xh)),
 //             dg_k += sum_t dn_tk xh_tk
 //
-// Row kernels: one wave per row, 8 elements per lane per step (16- or 32-byte
-// accesses). Rows of up to 4096 elements stay in registers between the
-// row's reduction and its write (one read); longer rows are read twice (the
-// second read hits L2). Every tensor's element type is a run-time value
-// (uniform branches). The gain gradient is a column reduction over rows:
-// each workgroup of the backward kernel handles kNormRowsPerBlock rows (wave
-// w: rows w, w + 4, ...) and writes the fp32 partial sums of its rows (each
-// wave's rows in order, then the waves in order), then the final kernel adds the partials of each column: sixteen
-// slices of consecutive blocks, each summed in block order, then the slices
-// in order — the same order on every run, no atomics.
+// Forward: one wave per row, 8 elements per lane per step (16- or 32-byte
+// accesses); rows of up to 4096 elements stay in registers between the row's
+// reduction and its write (one read), longer rows are read twice (the second
+// read hits L2). Backward: rows of up to 4096 elements are split over four
+// waves (so that a workgroup of 16 waves keeps four rows in registers at
+// once and the chip holds enough waves to cover memory latency); longer rows
+// go one per wave, read twice. Every tensor's element type is a run-time
+// value (uniform branches). The gain gradient is a column reduction over
+// rows: each backward workgroup handles kNormRowsPerBlock rows and writes
+// the fp32 partial sums of its rows in a fixed order, then the final kernel
+// adds the partials of each column: sixteen slices of consecutive blocks,
+// each summed in block order, then the slices in order — the same order on
+// every run, no atomics.
 #include "common.hpp"
 
 namespace lc {
@@ -90,52 +93,6 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(NormP p) {
   }
 }
 
-// dx for one row held by one wave (a: dn, b: x of the lane's chunks), and the
-// row's gain-gradient terms dn * x * rstd added into the lane's accumulators
-__device__ __forceinline__ void bwd_row_regs(const NormP &p, int64_t row, int lane,
-                                             float (&acc)[MAXU][8]) {
-  const int64_t base = row * p.d;
-  const float r = p.rstd[row];
-  float a[MAXU][8], b[MAXU][8];
-  float dot = 0.0f;  // sum_k dn*g*x
-#pragma unroll
-  for (int u = 0; u < MAXU; ++u) {
-    const int c = lane * 8 + 512 * u;
-    if (c < p.d) {
-      float gv[8];
-      load8_dt(p.dn, base + c, p.dn_dt, a[u]);
-      load8_dt(p.x, base + c, p.x_dt, b[u]);
-      load8_dt(p.g, c, p.w_dt, gv);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) dot += a[u][e] * gv[e] * b[u][e];
-    }
-  }
-  dot = wave_sum(dot);
-  const float mean = dot * r / (float)p.d;  // mean_k(dxh * xh)
-  const float r2m = r * mean;
-#pragma unroll
-  for (int u = 0; u < MAXU; ++u) {
-    const int c = lane * 8 + 512 * u;
-    if (c < p.d) {
-      float gv[8], o[8];
-      load8_dt(p.g, c, p.w_dt, gv);
-      if (p.dres) {
-        load8_dt(p.dres, base + c, p.dres_dt, o);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = 0.0f;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        o[e] += r * (a[u][e] * gv[e] - b[u][e] * r2m);
-        acc[u][e] += a[u][e] * (b[u][e] * r);
-      }
-      store8_dt(p.dx, base + c, p.out_dt, o);
-      if (p.dx_copy) store8_dt(p.dx_copy, base + c, LC_BF16, o);
-    }
-  }
-}
-
 // rows longer than MAXD: the row is read twice, the gain gradient is not formed here
 __device__ __forceinline__ void bwd_row_long(const NormP &p, int64_t row, int lane) {
   const int64_t base = row * p.d;
@@ -170,40 +127,104 @@ __device__ __forceinline__ void bwd_row_long(const NormP &p, int64_t row, int la
   }
 }
 
-// One workgroup per kNormRowsPerBlock rows (wave w: rows w, w + 4, ...); for
-// d <= MAXD it also writes partial[blk][k] = sum over the block's rows of
-// dn * x * rstd (each wave's rows in order, then wave 0's sum, wave 1's, ...).
-__global__ __launch_bounds__(256) void rmsnorm_bwd_rows_kernel(NormP p) {
+// Rows of up to MAXD values: one workgroup of 16 waves per kNormRowsPerBlock
+// rows, 4 waves per row (lane l of wave w of a row holds the 8-value chunks
+// starting at 8 (64 w + l) and 8 (64 w + l) + 2048), four rows at a time:
+// iteration i takes rows 4 i + s (s = wave / 4). A row's dot product is the
+// sum of its four waves' shares in wave order (through LDS); the gain
+// gradient's partial sums: each lane's rows in order, then the four row
+// slots in order, into partial[blk][k].
+constexpr int BW_THREADS = 1024;
+constexpr int BW_CHUNKS = MAXD / 2048;  // 8-value chunks per lane
+__global__ __launch_bounds__(BW_THREADS) void rmsnorm_bwd_rows_kernel(NormP p) {
   __shared__ float red[MAXD];
+  __shared__ float dots[2][4][4];  // [iteration parity][row slot][wave of the row]
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int slot = wv >> 2, wr = wv & 3;
+  const int rl = wr * 64 + lane;
   const int64_t r0 = (int64_t)blockIdx.x * kNormRowsPerBlock;
   const int64_t r1 = min(p.rows, r0 + kNormRowsPerBlock);
-  if (p.d > MAXD) {
-    for (int64_t row = r0 + wv; row < r1; row += 4) bwd_row_long(p, row, lane);
-    return;
-  }
-  float acc[MAXU][8];
+  float acc[BW_CHUNKS][8];
 #pragma unroll
-  for (int u = 0; u < MAXU; ++u)
+  for (int u = 0; u < BW_CHUNKS; ++u)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
-  for (int64_t row = r0 + wv; row < r1; row += 4) bwd_row_regs(p, row, lane, acc);
+#pragma unroll 1
+  for (int i = 0; i < kNormRowsPerBlock / 4; ++i) {
+    const int64_t row = r0 + 4 * i + slot;
+    const bool ok = row < r1;  // wave-uniform
+    const int64_t base = row * p.d;
+    float a[BW_CHUNKS][8], b[BW_CHUNKS][8];
+    float dot = 0.0f;  // this wave's share of sum_k dn*g*x
+    const float r = ok ? p.rstd[row] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < BW_CHUNKS; ++u) {
+      const int c = 8 * rl + 2048 * u;
+      if (ok && c < p.d) {
+        float gv[8];
+        load8_dt(p.dn, base + c, p.dn_dt, a[u]);
+        load8_dt(p.x, base + c, p.x_dt, b[u]);
+        load8_dt(p.g, c, p.w_dt, gv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dot += a[u][e] * gv[e] * b[u][e];
+      }
+    }
+    dot = wave_sum(dot);
+    if (lane == 0) dots[i & 1][slot][wr] = dot;
+    __syncthreads();
+    if (!ok) continue;
+    const float tot = dots[i & 1][slot][0] + dots[i & 1][slot][1] + dots[i & 1][slot][2] +
+                      dots[i & 1][slot][3];
+    const float mean = tot * r / (float)p.d;  // mean_k(dxh * xh)
+    const float r2m = r * mean;
+#pragma unroll
+    for (int u = 0; u < BW_CHUNKS; ++u) {
+      const int c = 8 * rl + 2048 * u;
+      if (c < p.d) {
+        float o[8], gv[8];
+        load8_dt(p.g, c, p.w_dt, gv);
+        if (p.dres) {
+          load8_dt(p.dres, base + c, p.dres_dt, o);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = 0.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          o[e] += r * (a[u][e] * gv[e] - b[u][e] * r2m);
+          acc[u][e] += a[u][e] * (b[u][e] * r);
+        }
+        store8_dt(p.dx, base + c, p.out_dt, o);
+        if (p.dx_copy) store8_dt(p.dx_copy, base + c, LC_BF16, o);
+      }
+    }
+  }
   if (!p.part) return;  // uniform: no gain gradient requested
 #pragma unroll 1
-  for (int w = 0; w < 4; ++w) {
-    if (wv == w) {
+  for (int s = 0; s < 4; ++s) {
+    if (slot == s) {
 #pragma unroll
-      for (int u = 0; u < MAXU; ++u) {
-        const int c = lane * 8 + 512 * u;
+      for (int u = 0; u < BW_CHUNKS; ++u) {
+        const int c = 8 * rl + 2048 * u;
         if (c < p.d) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) red[c + e] = (w == 0 ? 0.0f : red[c + e]) + acc[u][e];
+          for (int e = 0; e < 8; ++e) red[c + e] = (s == 0 ? 0.0f : red[c + e]) + acc[u][e];
         }
       }
     }
     __syncthreads();
   }
-  for (int k = threadIdx.x; k < p.d; k += 256) p.partial[(int64_t)blockIdx.x * p.d + k] = red[k];
+  for (int k = threadIdx.x; k < p.d; k += BW_THREADS) p.partial[(int64_t)blockIdx.x * p.d + k] = red[k];
+}
+
+// Rows longer than MAXD: one workgroup of 4 waves per kNormRowsPerBlock rows
+// (wave w: rows w, w + 4, ...), each row read twice; the gain gradient's
+// partial sums come from rmsnorm_dg_partial_kernel.
+__global__ __launch_bounds__(256) void rmsnorm_bwd_long_kernel(NormP p) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * kNormRowsPerBlock;
+  const int64_t r1 = min(p.rows, r0 + kNormRowsPerBlock);
+  for (int64_t row = r0 + wv; row < r1; row += 4) bwd_row_long(p, row, lane);
 }
 
 __device__ __forceinline__ float ld1_dt(const void *base, int64_t i, int dt) {
@@ -317,9 +338,13 @@ namespace {
 // Row kernel, plus the separate partial-sum kernel for rows longer than MAXD
 // when p.part is set.
 lc_status bwd_rows(const NormP &p, hipStream_t s) {
-  hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel, dim3((unsigned)p.nblk), dim3(256), 0, s, p);
-  LC_TRY(check_launch("rmsnorm_bwd_rows_kernel"));
-  if (!p.part || p.d <= MAXD) return LC_OK;
+  if (p.d <= MAXD) {
+    hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel, dim3((unsigned)p.nblk), dim3(BW_THREADS), 0, s, p);
+    return check_launch("rmsnorm_bwd_rows_kernel");
+  }
+  hipLaunchKernelGGL(rmsnorm_bwd_long_kernel, dim3((unsigned)p.nblk), dim3(256), 0, s, p);
+  LC_TRY(check_launch("rmsnorm_bwd_long_kernel"));
+  if (!p.part) return LC_OK;
   hipLaunchKernelGGL(rmsnorm_dg_partial_kernel, dim3((unsigned)((p.d + 255) / 256), (unsigned)p.nblk),
                      dim3(256), 0, s, p);
   return check_launch("rmsnorm_dg_partial_kernel");

@@ -571,3 +571,44 @@ def test_qk_norm_rope(x_dt, d_dt, w_dt, hd):
                                 d_dt, dg2[:hd], dg2[hd:], scratch, sb)
     torch.cuda.synchronize()
     assert torch.equal(dyd2, dyd) and torch.equal(dg2, dg)
+
+
+# ---------------------------------------------------------------- full-size AdamW shard
+
+def test_adam_full_size_shard_sampled_bit_exact():
+    """The 1.6e9-element shard in the benchmark's launch (two steps, bf16
+    gradient, bf16 cast): a sample of elements, including the first and the
+    last ones (the tail past the last 8-element block), taken before each
+    step and checked bit for bit against the oracle's AdamW on them."""
+    cfg = synth.ADAM_1P6B
+    n = cfg.n
+    banner(f"adam full-size shard n={n}")
+    g = torch.Generator(device=DEV)
+    g.manual_seed(11)
+    p = torch.randn(n, generator=g, device=DEV).mul_(cfg.p_std)
+    m = torch.zeros_like(p)
+    v = torch.zeros_like(p)
+    gr = torch.randn(n, generator=g, device=DEV).mul_(cfg.g_std).to(torch.bfloat16)
+    out = torch.empty(n, dtype=torch.bfloat16, device=DEV)
+    rng = np.random.default_rng(31)
+    idx = np.unique(np.concatenate([np.arange(16), np.arange(n - 16, n),
+                                    rng.integers(0, n, 200_000)]))
+    it = torch.from_numpy(idx).to(DEV)
+    for step in (1, 2):
+        p0, m0, v0 = (host32(t[it]) for t in (p, m, v))
+        g0 = gr[it].float().cpu().numpy()
+        lc.shard_adam_step(p, m, v, gr, lc.LC_BF16, out, n, cfg.lr, cfg.beta1, cfg.beta2,
+                           cfg.eps, cfg.weight_decay, step)
+        torch.cuda.synchronize()
+        pr, mr, vr = OP.adamw(p0, m0, v0, g0, cfg.lr, cfg.beta1, cfg.beta2, cfg.eps,
+                              cfg.weight_decay, step)
+        for got, ref, name in ((p, pr, "p"), (m, mr, "m"), (v, vr, "v")):
+            assert np.array_equal(host32(got[it]).view(np.uint32), ref.view(np.uint32)), name
+        assert np.array_equal(out[it].cpu().view(torch.int16).numpy().view(np.uint16),
+                              OP.bf16_rne_bits(pr)), "bf16 cast"
+    del p, m, v, gr, out
+    torch.cuda.empty_cache()
+
+
+def host32(t):
+    return t.detach().float().cpu().numpy().astype(np.float32)

@@ -7,10 +7,13 @@ chunk_backward / shard_adam_step) with the oracle.
 * Order invariance (1F1B vs GPipe: bitwise identical), run-to-run
   determinism, and the accumulated gradient equal, bit for bit, to the
   sequential fp32 sum of the per-microbatch gradients
-* the 7B-shaped stage at full size: outputs on a prefix of the sequence
-  against the oracle run on that prefix (causality makes the prefix
-  self-contained), with dY zero beyond the prefix so the full-size backward
-  (dX, every gradient) is checked too; dX beyond the prefix must be exactly 0
+* the 7B-shaped, Qwen3-8B-shaped and 8-layer d-2048 Llama-style stages at
+  full size: outputs on a prefix of the sequence against the oracle run on
+  that prefix (causality makes the prefix self-contained), with dY zero
+  beyond the prefix so the full-size backward (dX, every gradient) is
+  checked too; dX beyond the prefix must be exactly 0
+* split backwards (Bi/Bw), overlapped pairs on two streams and the ZeRO-2/3
+  paths: bit-identical to the plain Order, and against the oracle
 """
 import numpy as np
 import pytest
@@ -357,8 +360,8 @@ def test_split_backward_error_paths():
 
 @pytest.mark.parametrize("cfg,tol", [(synth.STAGE_7B, 2e-2),
                                      (synth.scaled(synth.STAGE_7B, bf16=False), 1e-4),
-                                     (synth.QWEN3_STAGE, 2e-2)],
-                         ids=["stage7b_bf16", "stage7b_fp32", "qwen3_bf16"])
+                                     (synth.QWEN3_STAGE, 2e-2), (synth.LLAMA_2K, 2e-2)],
+                         ids=["stage7b_bf16", "stage7b_fp32", "qwen3_bf16", "llama2k_bf16"])
 def test_full_size_stage_on_a_prefix(cfg, tol):
     P = 128
     banner(f"full-size {cfg.name} prefix {P}")

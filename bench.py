@@ -57,6 +57,9 @@ def desc_of(cfg, lc):
     return lc.desc_of_config(cfg)
 
 
+STEP_STATS = {}  # tag -> median and min of the timed steps
+
+
 def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None, overlap=False):
     """Time steps of (zero G, the Order, AdamW over the bucket) on `cfg`;
     returns (ms per step, TFLOP/s, outputs finite). With w_delay set the
@@ -96,14 +99,17 @@ def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None, overlap
         torch.cuda.synchronize()
         log(f"[bench] {tag} warmup {i + 1}/{warmup} done")
     torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
+    # an event before every step (and after the last) on the launch stream:
+    # per-step times without any host synchronisation inside the timed region
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record(stream)
     for i in range(steps):
         step()
-    t1.record(stream)
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms = t0.elapsed_time(t1) / steps
+    ms = ev[0].elapsed_time(ev[steps]) / steps
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+    STEP_STATS[tag] = {"median_ms": round(per[len(per) // 2], 2), "min_ms": round(per[0], 2)}
     tflops = stage_flops_per_mb(cfg) * M / (ms * 1e-3) / 1e12
     finite = bool(torch.isfinite(r.Y[M - 1].float()).all().item())
     r.close()
@@ -343,6 +349,11 @@ def main():
     ap.add_argument("--qwen3-only", action="store_true",
                     help="only the Qwen3-8B-shaped stage (q/k norm, 8 key/value heads), flat "
                          "and with overlapped pairs")
+    ap.add_argument("--overlap", action="store_true",
+                    help="7B-shaped stage: run the steady-state (F, B) pairs of the 1F1B Order "
+                         "overlapped on two streams (no gain measured there)")
+    ap.add_argument("--moe-flat", action="store_true",
+                    help="MoE stage: the flat 1F1B Order instead of overlapped (F, B) pairs")
     ap.add_argument("--flat", action="store_true",
                     help="with --qwen3-only: the flat Order only (per-kernel profiles)")
     ap.add_argument("--zero-only", action="store_true",
@@ -369,7 +380,8 @@ def main():
     stream = torch.cuda.current_stream()
     if args.moe_only:
         mcfg = synth.MOE_2K
-        mms, mtf, _ = time_stage(torch, lc, mcfg, stream, args.steps, args.warmup, "moe")
+        mms, mtf, _ = time_stage(torch, lc, mcfg, stream, args.steps, args.warmup, "moe",
+                                 overlap=not args.moe_flat)
         print(json.dumps({"moe_stage": {"workload": mcfg.name, "value": round(mtf, 2),
                                         "unit": "TFLOP/s", "ms_per_step": round(mms, 2)}}))
         return
@@ -419,7 +431,8 @@ def main():
         calibration_copy(torch, lc, stream)
         print(json.dumps({"roofline": wgrad_roofline(torch, lc, cfg, stream)}), flush=True)
         return
-    ms, tflops, finite = time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "7b")
+    ms, tflops, finite = time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "7b",
+                                    overlap=args.overlap)
     flops = stage_flops_per_mb(cfg) * M
     log(f"[bench] {ms:.1f} ms/step, {tflops:.1f} TFLOP/s ({100 * tflops / BF16_PEAK_TFLOPS:.1f}% of bf16 peak)")
 
@@ -428,9 +441,14 @@ def main():
     moe = None
     if not args.no_moe:
         mcfg = synth.MOE_2K
-        mms, mtf, mfin = time_stage(torch, lc, mcfg, stream, args.steps, args.warmup, "moe")
+        mover = not args.moe_flat
+        mms, mtf, mfin = time_stage(torch, lc, mcfg, stream, args.steps, args.warmup, "moe",
+                                    overlap=mover)
         moe = {"workload": mcfg.name, "value": round(mtf, 2), "unit": "TFLOP/s",
-               "ms_per_step": round(mms, 2), "frac": round(mtf / BF16_PEAK_TFLOPS, 4),
+               "order": f"1F1B(P={mcfg.pp_size},s={mcfg.pp_rank})"
+                        + (", (F, B) pairs overlapped on two streams" if mover else ""),
+               "ms_per_step": round(mms, 2), "step_ms": STEP_STATS.get("moe"),
+               "frac": round(mtf / BF16_PEAK_TFLOPS, 4),
                "algorithmic_tflop_per_step":
                    round(stage_flops_per_mb(mcfg) * mcfg.num_microbatches / 1e12, 3),
                "outputs_finite": mfin}
@@ -451,11 +469,14 @@ def main():
         "config": {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
                    "heads": cfg.n_heads, "head_dim": cfg.head_dim, "d_ff": cfg.d_ff,
                    "seq_len": cfg.seq_len, "micro_batch": cfg.micro_batch,
-                   "num_microbatches": M, "order": f"1F1B(P={cfg.pp_size},s={cfg.pp_rank})",
+                   "num_microbatches": M,
+                   "order": f"1F1B(P={cfg.pp_size},s={cfg.pp_rank})"
+                            + (", (F, B) pairs overlapped on two streams" if args.overlap else ""),
                    "optimizer": "AdamW over the stage bucket + bf16 cast",
                    "parallelism": "one GPU's share (no collectives)",
                    "algorithmic_tflop_per_step": round(flops / 1e12, 2)},
         "mfma_util": round(tflops / BF16_PEAK_TFLOPS, 4),
+        "step_ms": STEP_STATS.get("7b"),
         "roofline": roof,
         "adam_shard": adam,
         "moe_stage": moe,

@@ -268,6 +268,73 @@ def test_moe_stage_matches_oracle_with_gpu_routing():
     r.close()
 
 
+def test_moe_stage_with_an_expert_that_receives_no_tokens():
+    """Router rows u, -u, 0, 0 in every layer: each token picks the positive
+    one of experts 0 and 1, then expert 2 (experts 2 and 3 tie at logit 0,
+    the lower index wins), so expert 3 gets no rows. Its weight gradients and
+    its router row's gradient are exactly zero, and every output and gradient
+    matches the oracle given the GPU's routing (the oracle's own routing
+    agrees except where u.n2 is within rounding of 0)."""
+    cfg = SMALL_MOE
+    banner("moe stage with an unused expert")
+    M, E, d = cfg.num_microbatches, cfg.n_experts, cfg.d_model
+    flat = synth.stage_params(cfg, 2)
+    named = synth.unflatten(cfg, flat)
+    rng = np.random.default_rng(41)
+    for l in range(cfg.n_layers):
+        u = bf16_round(rng.standard_normal(d) / np.sqrt(d))
+        wr = named[f"L{l}.wr"]
+        wr[:] = 0.0
+        wr[0], wr[1] = u, -u
+    flat = synth.flatten(cfg, named, dtype=np.float32)
+    Xs = [synth.activation(cfg, 2, mb, "x") for mb in range(M)]
+    dYs = [synth.activation(cfg, 2, mb, "dy") for mb in range(M)]
+    r = StageRunner(desc_of(cfg), flat, M)
+    r.alloc_microbatches(Xs, dYs)
+    routes = []
+    for mb in range(M):
+        r.forward(mb)
+        routes.append([r.moe_routing(mb, l) for l in range(cfg.n_layers)])
+    for mb in range(M):
+        r.backward(mb)
+    torch.cuda.synchronize()
+    for mb in range(M):
+        for l in range(cfg.n_layers):
+            sel = routes[mb][l]
+            assert np.all(sel[:, 1] == 2) and np.all(np.isin(sel[:, 0], (0, 1))), (mb, l)
+    got = host(r.grad)
+    gg = synth.unflatten(cfg, got)
+    for l in range(cfg.n_layers):
+        for t in ("w1", "w3", "w2"):
+            assert np.all(gg[f"L{l}.e3.{t}"] == 0.0), (l, t)
+            assert np.any(gg[f"L{l}.e2.{t}"] != 0.0), (l, t)
+        assert np.all(gg[f"L{l}.wr"][3] == 0.0) and np.any(gg[f"L{l}.wr"][2] != 0.0)
+    layers = OS.layer_params(cfg, flat)
+    G = np.zeros(synth.param_count(cfg))
+    errs = {}
+    for mb in range(M):
+        Y, caches = OS.stage_forward(cfg, layers, Xs[mb], route_overrides=routes[mb])
+        for l in range(cfg.n_layers):
+            pi = caches[l]["moe"]["pi"]
+            own = np.argsort(-pi, axis=1, kind="stable")[:, :2]
+            for t in np.nonzero(~np.all(own == routes[mb][l], axis=1))[0]:
+                assert abs(pi[t, 0] - pi[t, 1]) < 1e-2, (mb, l, t)
+        dX, gmb = OS.stage_backward(cfg, layers, caches, dYs[mb])
+        G += gmb
+        errs[f"Y{mb}"] = rel_err(host(r.Y[mb]), Y)
+        errs[f"dX{mb}"] = rel_err(host(r.dX[mb]), dX)
+    for name, off, shape in synth.layout(cfg):
+        sz = int(np.prod(shape))
+        if np.any(G[off:off + sz] != 0.0):
+            errs[name] = rel_err(got[off:off + sz], G[off:off + sz])
+        else:
+            assert np.all(got[off:off + sz] == 0.0), name
+    top = sorted(errs.items(), key=lambda kv: -kv[1])[:6]
+    print("worst tensors: " + ", ".join(f"{n}={e:.2e}" for n, e in top), flush=True)
+    assert max(errs.values()) <= 2e-2
+    r.close()
+
+
 def test_moe_overlapped_pair_on_two_streams_is_bit_identical():
     """A mixture-of-experts stage with its (F1, B0) pair nested and run on two
     streams gives the flat Order's outputs and gradient bit for bit."""

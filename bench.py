@@ -58,14 +58,18 @@ def desc_of(cfg, lc):
 
 
 STEP_STATS = {}  # tag -> median and min of the timed steps
+WGRAD_TIMES = {}  # tag -> (durations in ms, FLOP) of the timed weight-gradient launches
 
 
-def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None, overlap=False):
+def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None, overlap=False,
+               time_wgrad=False):
     """Time steps of (zero G, the Order, AdamW over the bucket) on `cfg`;
     returns (ms per step, TFLOP/s, outputs finite). With w_delay set the
     Order is 1F1B with split backwards (Bi, then Bw w_delay backwards later);
     with overlap, 1F1B with its steady-state (F, B) pairs nested and run on
-    two streams."""
+    two streams. With time_wgrad, the library brackets every weight-gradient
+    product launch of the timed steps with HIP events on its stream
+    (lc_stage_timer_enable); the durations land in WGRAD_TIMES[tag]."""
     from paper_2606_11169_amd.runner import random_stage
     M = cfg.num_microbatches
     aux = None
@@ -102,11 +106,19 @@ def time_stage(torch, lc, cfg, stream, steps, warmup, tag, w_delay=None, overlap
     # an event before every step (and after the last) on the launch stream:
     # per-step times without any host synchronisation inside the timed region
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    cap = steps * cfg.n_layers * M * 4  # four dense weight-gradient products per layer and B
+    if time_wgrad:
+        lc.lc_stage_timer_enable(r.stage, cap)
     ev[0].record(stream)
     for i in range(steps):
         step()
         ev[i + 1].record(stream)
     torch.cuda.synchronize()
+    if time_wgrad:
+        wms, wfl, wn = lc.lc_stage_timer_read(r.stage, cap)
+        assert wn == cap == len(wms), (wn, cap)
+        WGRAD_TIMES[tag] = (wms, wfl)
+        lc.lc_stage_timer_enable(r.stage, 0)
     ms = ev[0].elapsed_time(ev[steps]) / steps
     per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
     STEP_STATS[tag] = {"median_ms": round(per[len(per) // 2], 2), "min_ms": round(per[0], 2)}
@@ -190,55 +202,23 @@ def time_launches(torch, stream, fns, reps):
     return total, count
 
 
-def wgrad_roofline(torch, lc, cfg, stream, reps=5):
-    """The weight-gradient GEMM (both operands token-major, fp32 accumulate
-    into the bucket): the kernel with the largest share of the step's time.
-    Its four per-layer launches are replayed with the stage's own operand
-    layouts (dW_qkv = dqkv^T n1, dW_o = dh^T o, dW_13 = [dg|du]^T n2,
-    dW_2 = dy^T act), `reps` rounds back to back, timed with HIP events on the
-    launch stream. Returns the roofline dict (achieved = algorithmic FLOP per
-    launch / average launch duration)."""
-    T, d, f = cfg.tokens, cfg.d_model, cfg.d_ff
-    dev = "cuda"
-    g = torch.Generator(device=dev)
-    g.manual_seed(7)
-
-    def rnd(cols):
-        return torch.randn((T, cols), generator=g, device=dev).to(torch.bfloat16)
-    dqkv, n1, dh, o, dgu, n2, dy, act = (rnd(3 * d), rnd(d), rnd(d), rnd(d), rnd(2 * f), rnd(d),
-                                         rnd(d), rnd(f))
-    G = torch.zeros((3 * d * d) + d * d + 2 * f * d + d * f, dtype=torch.float32, device=dev)
-    launches = [(3 * d, d, dqkv, 3 * d, n1, d), (d, d, dh, d, o, d),
-                (2 * f, d, dgu, 2 * f, n2, d), (d, f, dy, d, act, f)]
-    fns, flops, off = [], 0.0, 0
-    for (M, N, A, lda, B, ldb) in launches:
-        Cv = G[off:off + M * N]
-        off += M * N
-
-        def fn(M=M, N=N, A=A, lda=lda, B=B, ldb=ldb, Cv=Cv):
-            lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ACCUM_F32, M, N, T, A, lda, 0, B, ldb, 0, Cv, N,
-                       stream=stream)
-        fns.append(fn)
-        flops += 2.0 * M * N * T
-    for fn in fns:  # warm
-        fn()
-    torch.cuda.synchronize()
-    s = torch.cuda.Event(enable_timing=True)
-    e = torch.cuda.Event(enable_timing=True)
-    s.record(stream)
-    for _ in range(reps):
-        for fn in fns:
-            fn()
-    e.record(stream)
-    e.synchronize()
-    n = reps * len(fns)
-    avg_ms = s.elapsed_time(e) / n
-    avg_flops = flops / len(fns)
+def wgrad_roofline(times):
+    """Roofline entry of the weight-gradient GEMM (both operands token-major,
+    fp32 accumulate into the bucket; the kernel with the largest share of the
+    step's time), from its launches inside the timed steps: achieved =
+    average algorithmic FLOP per launch / average launch duration, both over
+    every timed launch (the four per-layer shapes dW_qkv = dqkv^T n1,
+    dW_o = dh^T o, dW_13 = [dg|du]^T n2, dW_2 = dy^T act, each B)."""
+    wms, wfl = times
+    n = len(wms)
+    avg_ms = sum(wms) / n
+    avg_flops = sum(wfl) / n
     achieved = avg_flops / (avg_ms * 1e-3) / 1e12
     return {"bound": "mfma", "kernel": "gemm_bf16_kernel<false,false,LC_EPI_ACCUM_F32>",
             "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(),
-            "avg_launch_ms": round(avg_ms, 4), "flop_per_launch": avg_flops}
+            "launches": n, "avg_launch_ms": round(avg_ms, 4), "flop_per_launch": avg_flops,
+            "timing": "HIP events around each launch inside the timed steps"}
 
 
 GEMM_SRC = os.path.join(ROOT, "paper_2606_11169_amd", "csrc", "k_gemm.hip")
@@ -342,7 +322,8 @@ def main():
     ap.add_argument("--moe-only", action="store_true",
                     help="only the MoE stage timing (kernel profiles of that workload)")
     ap.add_argument("--roofline-only", action="store_true",
-                    help="only the roofline kernel replay and the calibration copy (PMC runs)")
+                    help="only the calibration copy and the 7B-shaped stage with its weight-gradient "
+                         "launches timed (PMC runs)")
     ap.add_argument("--split-only", type=int, default=None, metavar="W_DELAY",
                     help="only the 7B-shaped stage with split backwards (Bw W_DELAY "
                          "backwards after its Bi)")
@@ -429,14 +410,15 @@ def main():
         return
     if args.roofline_only:
         calibration_copy(torch, lc, stream)
-        print(json.dumps({"roofline": wgrad_roofline(torch, lc, cfg, stream)}), flush=True)
+        time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "7b", time_wgrad=True)
+        print(json.dumps({"roofline": wgrad_roofline(WGRAD_TIMES["7b"])}), flush=True)
         return
     ms, tflops, finite = time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "7b",
-                                    overlap=args.overlap)
+                                    overlap=args.overlap, time_wgrad=True)
     flops = stage_flops_per_mb(cfg) * M
     log(f"[bench] {ms:.1f} ms/step, {tflops:.1f} TFLOP/s ({100 * tflops / BF16_PEAK_TFLOPS:.1f}% of bf16 peak)")
 
-    roof = wgrad_roofline(torch, lc, cfg, stream)
+    roof = wgrad_roofline(WGRAD_TIMES["7b"])
     log(f"[bench] roofline {roof}")
     moe = None
     if not args.no_moe:

@@ -375,6 +375,32 @@ lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const 
 lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32_t *sel_out,
                                void *stream);
 
+/* Timing of the weight-gradient products (measurement support, not needed to
+ * train). These are the products that form dW from the backward's output
+ * gradients and the stashed activations, in Chunk B or in its weight half
+ * (the BW pass of Section 4.1): G[W2], G[W1;W3], G[Wo], G[Wq;Wk;Wv]
+ * and, in mixture-of-experts layers, the grouped expert products.
+ *
+ * lc_stage_timer_enable(stage, max_launches): creates 2 * max_launches HIP
+ * events (host-side handles, no device buffers) and from then on brackets
+ * the next max_launches such launches, in launch order, with a pair of
+ * events recorded on the stream each is launched on; later launches run
+ * untimed. Any earlier events are destroyed and the count restarts.
+ * max_launches = 0 turns timing off. LC_ERR_INVALID_ARG for a null stage or
+ * max_launches outside [0, 2^20]; LC_ERR_HIP if event creation fails.
+ *
+ * lc_stage_timer_read(stage, ms, flop, cap, n): waits for the first
+ * min(cap, timed) stop events and writes, per timed launch i, its duration
+ * ms[i] (milliseconds between its two events) and its algorithmic FLOP
+ * flop[i] = 2 M N K; *n receives the number of launches timed since the last
+ * read (which may exceed cap) and the count restarts, so the events are
+ * reused. ms and flop are host arrays of cap entries. LC_ERR_INVALID_ARG for a
+ * null stage or n, negative cap, or null arrays with cap > 0. Events still
+ * pending in a stream must not be re-armed: read only after the launches
+ * timed so far were enqueued, and enable again only after a read. */
+lc_status lc_stage_timer_enable(lc_stage *stage, int32_t max_launches);
+lc_status lc_stage_timer_read(lc_stage *stage, float *ms, double *flop, int32_t cap, int32_t *n);
+
 /* ---------------------------------------------------------------- buffers */
 
 /* accum[i] += g[i] for i < n, in fp32 (g is fp32 or bf16 per g_dtype); each

@@ -46,6 +46,9 @@ struct lc_stage {
   std::vector<int32_t> wowner;     // microbatch whose weight pass is pending, per weight-pass slot
   std::vector<hipEvent_t> events;  // cross-stream synchronisation of lc_run_order_overlap
   bool grad_store = false;         // backwards overwrite the gradient buffer (ZeRO runs, dense)
+  std::vector<hipEvent_t> tev;     // weight-gradient product timing: start, stop per launch
+  std::vector<double> tflop;       // algorithmic FLOP of each timed launch (size = capacity)
+  int32_t tn = 0;                  // launches timed since the last read
   std::vector<float> rope_host;    // cos table then sin table (fp32)
 };
 
@@ -80,6 +83,26 @@ lc_gemm_args gemm_base(int dtype, int epi, int64_t M, int64_t N, int64_t K) {
   a.N = N;
   a.K = K;
   return a;
+}
+
+// A weight-gradient product (fp32 output into the gradient), bracketed by the
+// stage's timing events on its stream while lc_stage_timer_enable has left
+// capacity.
+lc_status wgrad_launch(lc_stage *st, const lc_gemm_args &a, hipStream_t s) {
+  const int32_t i = st->tn;
+  const bool timed = i < (int32_t)st->tflop.size();
+  if (timed) {
+    const hipError_t e = hipEventRecord(st->tev[2 * i], s);
+    if (e != hipSuccess) return hip_fail(e, "recording a timing event");
+  }
+  LC_TRY(gemm_launch(a, s));
+  if (timed) {
+    const hipError_t e = hipEventRecord(st->tev[2 * i + 1], s);
+    if (e != hipSuccess) return hip_fail(e, "recording a timing event");
+    st->tflop[i] = 2.0 * (double)a.M * (double)a.N * (double)a.K;
+    st->tn = i + 1;
+  }
+  return LC_OK;
 }
 
 lc_norm_args norm_base(int64_t T, int64_t d, float eps) {
@@ -193,7 +216,7 @@ static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, cons
   a.C = w.gp(pp.expert0 + 2 * FE * D); a.ldc = FE;
   a.group_mode = LC_GROUP_K; a.n_groups = E; a.group_offsets = off;
   a.group_stride_c = (int64_t)pp.expert_stride;
-  LC_TRY(gemm_launch(a, s));
+  LC_TRY(wgrad_launch(st, a, s));
   // dns = [dgate | dup] [W1_e; W3_e] per expert (fp32)
   a = gemm_base(dt, LC_EPI_STORE_F32, R, D, 2 * FE);
   a.A = da; a.lda = 2 * FE; a.a_kmajor = 1;
@@ -209,7 +232,7 @@ static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, cons
   a.C = w.gp(pp.expert0); a.ldc = D;
   a.group_mode = LC_GROUP_K; a.n_groups = E; a.group_offsets = off;
   a.group_stride_c = (int64_t)pp.expert_stride;
-  LC_TRY(gemm_launch(a, s));
+  LC_TRY(wgrad_launch(st, a, s));
   // dn = dns[rowpos0] + dns[rowpos1] + dl Wr; then G[Wr] += dl^T n2
   const int32_t *sel = static_cast<const int32_t *>(L.at(P.moe_sel));
   LC_TRY(moe_bwd_combine_launch(dns, dw, static_cast<const float *>(L.at(P.moe_w)), sel,
@@ -400,7 +423,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
       a.A = dy_op; a.lda = D; a.a_kmajor = 0;
       a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
       a.C = w.gp(pp.w2); a.ldc = F;
-      LC_TRY(gemm_launch(a, s));
+      LC_TRY(wgrad_launch(st, a, s));
     }
     // dn2 = [dgate | dup] [W1; W3]
     a = gemm_base(dt, LC_EPI_STORE, T, D, 2 * F);
@@ -414,7 +437,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
       a.A = da; a.lda = 2 * F; a.a_kmajor = 0;
       a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
       a.C = w.gp(pp.w1); a.ldc = D;
-      LC_TRY(gemm_launch(a, s));
+      LC_TRY(wgrad_launch(st, a, s));
     }
     }
     // dh = dy + RMSNorm2'(dn2); G[g2] += ... (or its partial sums)
@@ -445,7 +468,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
       a.A = dh_op; a.lda = D; a.a_kmajor = 0;
       a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
       a.C = w.gp(pp.wo); a.ldc = D;
-      LC_TRY(gemm_launch(a, s));
+      LC_TRY(wgrad_launch(st, a, s));
     }
     // dq, dk, dv (dq, dk rotated back)
     char *qkv = static_cast<char *>(L.at(P.qkv));
@@ -487,7 +510,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
       a.A = dqkv; a.lda = QC; a.a_kmajor = 0;
       a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
       a.C = w.gp(pp.wq); a.ldc = D;
-      LC_TRY(gemm_launch(a, s));
+      LC_TRY(wgrad_launch(st, a, s));
     }
     // dx = dh + RMSNorm1'(dn1); G[g1] += ... (or its partial sums)
     nb.dn = dn; nb.dn_dtype = ty.res;
@@ -531,13 +554,13 @@ static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, 
     a.A = WL.at(P.w_dy); a.lda = D; a.a_kmajor = 0;
     a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
     a.C = w.gp(pp.w2); a.ldc = F;
-    LC_TRY(gemm_launch(a, s));
+    LC_TRY(wgrad_launch(st, a, s));
     // G[W1; W3] += [dgate | dup]^T n2
     a = gemm_base(dt, gepi, 2 * F, D, T);
     a.A = WL.at(P.w_da); a.lda = 2 * F; a.a_kmajor = 0;
     a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.w1); a.ldc = D;
-    LC_TRY(gemm_launch(a, s));
+    LC_TRY(wgrad_launch(st, a, s));
     LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p2)), w.gp(pp.g2), T, D, s,
                                    st->grad_store));
     // G[Wo] += dh^T o
@@ -545,13 +568,13 @@ static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, 
     a.A = WL.at(P.w_dh); a.lda = D; a.a_kmajor = 0;
     a.B = L.at(P.o); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.wo); a.ldc = D;
-    LC_TRY(gemm_launch(a, s));
+    LC_TRY(wgrad_launch(st, a, s));
     // G[Wq;Wk;Wv] += [dq|dk|dv]^T n1
     a = gemm_base(dt, gepi, QC, D, T);
     a.A = WL.at(P.w_dqkv); a.lda = QC; a.a_kmajor = 0;
     a.B = L.at(P.n1); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.wq); a.ldc = D;
-    LC_TRY(gemm_launch(a, s));
+    LC_TRY(wgrad_launch(st, a, s));
     LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p1)), w.gp(pp.g1), T, D, s,
                                    st->grad_store));
     if (d.qk_norm)
@@ -692,8 +715,10 @@ lc_status lc_stage_create(const lc_stage_desc *desc, void *workspace, size_t ws_
 }
 
 lc_status lc_stage_destroy(lc_stage *stage) {
-  if (stage)
+  if (stage) {
     for (hipEvent_t e : stage->events) hipEventDestroy(e);
+    for (hipEvent_t e : stage->tev) hipEventDestroy(e);
+  }
   delete stage;
   return LC_OK;
 }
@@ -744,6 +769,42 @@ lc_status chunk_backward_weight(lc_stage *stage, const lc_param_bufs *params,
   if (mb->mb < 0 || find_wslot(stage, mb->mb) < 0)
     return fail(LC_ERR_STATE, "microbatch %d has no pending weight pass", mb->mb);
   return do_backward_weight(stage, params, mb->mb, static_cast<hipStream_t>(stream));
+}
+
+lc_status lc_stage_timer_enable(lc_stage *stage, int32_t max_launches) {
+  if (!stage || max_launches < 0 || max_launches > (1 << 20))
+    return fail(LC_ERR_INVALID_ARG, "null stage or launch capacity outside [0, 2^20]");
+  for (hipEvent_t e : stage->tev) hipEventDestroy(e);
+  stage->tev.clear();
+  stage->tflop.clear();
+  stage->tn = 0;
+  for (int64_t i = 0; i < 2 * (int64_t)max_launches; ++i) {
+    hipEvent_t e;
+    const hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      for (hipEvent_t x : stage->tev) hipEventDestroy(x);
+      stage->tev.clear();
+      return hip_fail(r, "creating timing events");
+    }
+    stage->tev.push_back(e);
+  }
+  stage->tflop.assign(max_launches, 0.0);
+  return LC_OK;
+}
+
+lc_status lc_stage_timer_read(lc_stage *stage, float *ms, double *flop, int32_t cap, int32_t *n) {
+  if (!stage || !n || cap < 0 || (cap > 0 && (!ms || !flop)))
+    return fail(LC_ERR_INVALID_ARG, "null stage, count or output arrays, or negative capacity");
+  const int32_t k = stage->tn < cap ? stage->tn : cap;
+  for (int32_t i = 0; i < k; ++i) {
+    hipError_t e = hipEventSynchronize(stage->tev[2 * i + 1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms[i], stage->tev[2 * i], stage->tev[2 * i + 1]);
+    if (e != hipSuccess) return hip_fail(e, "reading a timing event");
+    flop[i] = stage->tflop[i];
+  }
+  *n = stage->tn;
+  stage->tn = 0;
+  return LC_OK;
 }
 
 lc_status lc_stage_moe_routing(lc_stage *stage, int32_t mb, int32_t layer, int32_t *sel_out,

@@ -206,6 +206,9 @@ _SIGS = {
     "lc_cast_bf16": (C.c_int, [C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "lc_moe_route": (C.c_int, [C.POINTER(lc_moe_args), C.c_void_p]),
     "lc_moe_dispatch": (C.c_int, [C.POINTER(lc_moe_args), C.c_void_p]),
+    "lc_stage_timer_enable": (C.c_int, [C.c_void_p, C.c_int32]),
+    "lc_stage_timer_read": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                      C.c_void_p]),
     "lc_stage_moe_routing": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
                                        C.c_void_p]),
 }
@@ -591,6 +594,23 @@ def lc_moe_dispatch(T, E, sel, w, offsets, perm, wrow, rowpos, stream=None):
     a.offsets, a.perm = ptr(offsets) or None, ptr(perm) or None
     a.wrow, a.rowpos = ptr(wrow) or None, ptr(rowpos) or None
     return _check(lib().lc_moe_dispatch(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_stage_timer_enable(stage, max_launches):
+    """Brackets the stage's next `max_launches` weight-gradient product launches
+    with HIP events on their streams (0 turns timing off)."""
+    return _check(lib().lc_stage_timer_enable(stage.handle, C.c_int32(max_launches)))
+
+
+def lc_stage_timer_read(stage, cap):
+    """Waits for the timed launches and returns (durations in ms, FLOP per
+    launch, number timed since the last read); restarts the count."""
+    ms = (C.c_float * max(cap, 1))()
+    fl = (C.c_double * max(cap, 1))()
+    n = C.c_int32(0)
+    _check(lib().lc_stage_timer_read(stage.handle, ms, fl, C.c_int32(cap), C.byref(n)))
+    k = min(cap, n.value)
+    return list(ms[:k]), list(fl[:k]), n.value
 
 
 def lc_stage_moe_routing(stage, mb, layer, sel_out, stream=None):

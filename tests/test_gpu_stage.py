@@ -163,6 +163,44 @@ def test_order_invariance_determinism_and_exact_accumulation():
         r.close()
 
 
+def test_weight_gradient_timer_brackets_every_product():
+    """lc_stage_timer_enable/read: one event pair per weight-gradient product
+    in launch order (layers top down: W2, W1;W3, Wo, Wq;Wk;Wv), each with its
+    2 M N K; timing leaves the gradient bit-identical; the count restarts on
+    read and stops at the capacity."""
+    cfg = SMALL_BF16
+    banner("weight-gradient timer")
+    flat, Xs, dYs = inputs(cfg, seed=5)
+    M, nl = cfg.num_microbatches, cfg.n_layers
+    order = OO.one_f_one_b(M, 3, 0)
+    ref = gpu_run(cfg, order, flat, Xs, dYs)
+    r = StageRunner(desc_of(cfg), flat, M)
+    r.alloc_microbatches(Xs, dYs)
+    launches = 4 * nl * M
+    lc.lc_stage_timer_enable(r.stage, launches + 3)
+    r.run_order(to_c(order))
+    torch.cuda.synchronize()
+    ms, fl, n = lc.lc_stage_timer_read(r.stage, launches + 3)
+    assert n == launches and len(ms) == launches
+    assert torch.equal(ref.grad, r.grad)
+    T, D, F = cfg.tokens, cfg.d_model, cfg.d_ff
+    QC = D + 2 * cfg.head_dim * cfg.kv_heads
+    per_layer = [2.0 * D * F * T, 2.0 * 2 * F * D * T, 2.0 * D * D * T, 2.0 * QC * D * T]
+    assert fl == per_layer * (nl * M)
+    assert all(0.0 < t < 1e3 for t in ms)
+    assert lc.lc_stage_timer_read(r.stage, 4)[2] == 0
+    lc.lc_stage_timer_enable(r.stage, 5)
+    r.zero_grad()
+    r.run_order(to_c(order))
+    torch.cuda.synchronize()
+    ms, fl, n = lc.lc_stage_timer_read(r.stage, 2)
+    assert n == 5 and len(ms) == 2 and fl == per_layer[:2]
+    assert torch.equal(ref.grad, r.grad)
+    lc.lc_stage_timer_enable(r.stage, 0)
+    for x in (ref, r):
+        x.close()
+
+
 def test_stage_error_paths_have_no_side_effects():
     cfg = SMALL_BF16
     banner("stage error paths")

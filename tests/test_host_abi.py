@@ -310,3 +310,12 @@ def test_buffer_entry_points_reject_bad_arguments():
                    c_dtype=lc.LC_BF16)
     with pytest.raises(lc.LibchunkError):  # norm with an unknown dtype
         lc.lc_rmsnorm_forward(4, 8, 4096, 4096, 1e-5, 4096, 4096, 7, lc.LC_BF16, lc.LC_BF16)
+
+
+def test_timer_entry_points_reject_bad_arguments():
+    import ctypes
+    L = lc.lib()
+    assert L.lc_stage_timer_enable(None, 4) == lc.LC_ERR_INVALID_ARG
+    n = ctypes.c_int32(-1)
+    assert L.lc_stage_timer_read(None, None, None, 0, ctypes.byref(n)) == lc.LC_ERR_INVALID_ARG
+    assert n.value == -1

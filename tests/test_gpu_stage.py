@@ -14,6 +14,9 @@ chunk_backward / shard_adam_step) with the oracle.
   checked too; dX beyond the prefix must be exactly 0
 * split backwards (Bi/Bw), overlapped pairs on two streams and the ZeRO-2/3
   paths: bit-identical to the plain Order, and against the oracle
+* a NaN in one input token: propagated (causally) into Y, dX, the gradient and
+  the AdamW update, never skipped; everything it cannot reach bit-identical
+* the weight-gradient timing hook: one event pair per product, results unchanged
 """
 import numpy as np
 import pytest
@@ -197,6 +200,42 @@ def test_weight_gradient_timer_brackets_every_product():
     assert n == 5 and len(ms) == 2 and fl == per_layer[:2]
     assert torch.equal(ref.grad, r.grad)
     lc.lc_stage_timer_enable(r.stage, 0)
+    for x in (ref, r):
+        x.close()
+
+
+def test_non_finite_values_propagate_without_skipping():
+    """NaN is neither masked nor skipped: a NaN in one element of one token's
+    input makes every later position of that sequence NaN in Y (the token's
+    normalised row is all NaN and causal attention carries it forward), leaves
+    the positions before the token's 64-key block and the other sequence of the
+    microbatch bit-identical, leaves the other microbatches bit-identical, and
+    reaches the gradient; AdamW then turns exactly the parameters whose
+    gradient is NaN into NaN and updates the rest."""
+    cfg = SMALL_BF16
+    banner("NaN propagation")
+    flat, Xs, dYs = inputs(cfg, seed=6)
+    M = cfg.num_microbatches
+    order = OO.one_f_one_b(M, 3, 0)
+    ref = gpu_run(cfg, order, flat, Xs, dYs)
+    p = 150  # token of sequence 0; its 64-key block starts at 128
+    bad = [x.copy() for x in Xs]
+    bad[1][0, p, 7] = np.nan  # activations are [micro_batch, seq_len, d_model]
+    r = gpu_run(cfg, order, flat, bad, dYs)
+    assert torch.isnan(r.Y[1][0, p:].float()).all()
+    assert torch.equal(r.Y[1][0, :128], ref.Y[1][0, :128])
+    assert torch.equal(r.Y[1][1], ref.Y[1][1])  # the microbatch's other sequence
+    for mb in (0, 2):
+        assert torch.equal(r.Y[mb], ref.Y[mb]) and torch.equal(r.dX[mb], ref.dX[mb])
+    assert torch.isnan(r.dX[1][0, p].float()).all()
+    g_nan = torch.isnan(r.grad)
+    assert g_nan.any() and not torch.isnan(ref.grad).any()
+    r.init_optimizer(flat)
+    r.adam_step(1e-3, 0.9, 0.95, 1e-8, 0.1)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.isnan(r.master), g_nan)
+    assert torch.equal(torch.isnan(r.w.float()), g_nan)
+    assert torch.isfinite(r.master[~g_nan]).all()
     for x in (ref, r):
         x.close()
 

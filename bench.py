@@ -186,20 +186,18 @@ def time_zero(torch, lc, cfg, stream, steps, warmup, level, ranks=8):
     return ms, tflops, persistent, temporary
 
 
-def time_launches(torch, stream, fns, reps):
-    """Per-launch HIP event timing; returns (total ms, launches)."""
-    total, count = 0.0, 0
-    for _ in range(reps):
-        for fn in fns:
-            s = torch.cuda.Event(enable_timing=True)
-            e = torch.cuda.Event(enable_timing=True)
-            s.record(stream)
-            fn()
-            e.record(stream)
-            e.synchronize()
-            total += s.elapsed_time(e)
-            count += 1
-    return total, count
+def time_launches(torch, stream, fns):
+    """Per-launch HIP event timing on `stream`; returns the durations (ms)."""
+    out = []
+    for fn in fns:
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        fn()
+        e.record(stream)
+        e.synchronize()
+        out.append(s.elapsed_time(e))
+    return out
 
 
 def wgrad_roofline(times):
@@ -249,6 +247,39 @@ def measured_traffic():
     return float(vals["traffic_bytes_per_launch"]) if "traffic_bytes_per_launch" in vals else None
 
 
+MFMA_MD = os.path.join(ROOT, "profiles", "stage7b_mfma_busy.md")
+
+
+def csrc_hash() -> str:
+    """Digest of every HIP source of the library (the counters depend on all kernels)."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2606_11169_amd", "csrc")
+    for name in sorted(os.listdir(d)):
+        if name.endswith(".hip"):
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_mfma_busy():
+    """Matrix-core busy fraction of the 7B-shaped step from the committed PMC
+    summary (SQ_VALU_MFMA_BUSY_CYCLES over the SIMD-cycles its kernels had),
+    if it was taken on the current sources (else None)."""
+    try:
+        lines = open(MFMA_MD).read().splitlines()
+    except OSError:
+        return None
+    vals = {}
+    for ln in lines:
+        for key in ("mfma_busy_step:", "csrc_sha256_16:"):
+            if ln.startswith(key):
+                vals[key[:-1]] = ln.split(":", 1)[1].strip().split()[0]
+    if vals.get("csrc_sha256_16") != csrc_hash() or "mfma_busy_step" not in vals:
+        return None
+    return float(vals["mfma_busy_step"])
+
+
 def calibration_copy(torch, lc, stream):
     """A plain streaming kernel of known HBM traffic (for scaling PMC byte counters)."""
     a = torch.zeros(CAL_N, dtype=torch.float32, device="cuda")
@@ -259,7 +290,7 @@ def calibration_copy(torch, lc, stream):
     del a, g
 
 
-def adam_shard(torch, lc, shard, stream, reps=10):
+def adam_shard(torch, lc, shard, stream, reps=20):
     n = shard.n
     dev = "cuda"
     g = torch.Generator(device=dev)
@@ -276,13 +307,15 @@ def adam_shard(torch, lc, shard, stream, reps=10):
     step(1)
     step(2)
     torch.cuda.synchronize()
-    ms, cnt = time_launches(torch, stream, [lambda i=i: step(3 + i) for i in range(reps)], 1)
-    avg = ms / cnt
-    gbs = 28.0 * n / (avg * 1e-3) / 1e9
+    per = sorted(time_launches(torch, stream, [lambda i=i: step(3 + i) for i in range(reps)]))
+    med = per[len(per) // 2]
+    gbs = 28.0 * n / (med * 1e-3) / 1e9
     del p, m, v, gr, out
     torch.cuda.empty_cache()
-    return {"workload": shard.name, "n": n, "bytes_per_elem": 28, "ms": round(avg, 3),
-            "value": round(gbs, 1), "unit": "GB/s", "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+    return {"workload": shard.name, "n": n, "bytes_per_elem": 28, "launches": reps,
+            "ms": round(med, 3), "ms_min": round(per[0], 3),
+            "ms_mean": round(sum(per) / len(per), 3), "value": round(gbs, 1), "unit": "GB/s",
+            "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "timing": "median of per-launch HIP events"}
 
 
 def cpu_baseline(cfg, tokens: int):
@@ -458,6 +491,7 @@ def main():
                    "parallelism": "one GPU's share (no collectives)",
                    "algorithmic_tflop_per_step": round(flops / 1e12, 2)},
         "mfma_util": round(tflops / BF16_PEAK_TFLOPS, 4),
+        "mfma_busy_counters": measured_mfma_busy(),
         "step_ms": STEP_STATS.get("7b"),
         "roofline": roof,
         "adam_shard": adam,

@@ -379,7 +379,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share of the stage; --gpus {args.gpus} is not "
-              "supported (this build runs on a single GPU).", file=sys.stderr)
+              "supported (no collectives across GPUs are implemented).", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -45,7 +45,7 @@ extern "C" {
 typedef enum lc_status {
   LC_OK = 0,
   LC_ERR_INVALID_ARG = -1,  /* bad pointer, size, alignment or descriptor field */
-  LC_ERR_UNSUPPORTED = -2,  /* a valid shape this build does not implement      */
+  LC_ERR_UNSUPPORTED = -2,  /* a valid shape the library does not implement     */
   LC_ERR_BAD_ORDER = -3,    /* an Order that breaks the Order rules below        */
   LC_ERR_STASH_FULL = -4,   /* more microbatches in flight than stash slots      */
   LC_ERR_STATE = -5,        /* F twice for one microbatch, or B without its F    */

@@ -52,7 +52,7 @@ lc_status validate_desc(const lc_stage_desc *d) {
     if (d->compute_dtype != LC_BF16)
       return fail(LC_ERR_UNSUPPORTED, "MoE stages need compute_dtype LC_BF16 (grouped matrix-core products)");
   }
-  // limits of the kernels in this build
+  // limits of the kernels
   if (d->compute_dtype == LC_BF16) {
     if (d->head_dim != 128)
       return fail(LC_ERR_UNSUPPORTED, "bf16 attention kernels need head_dim == 128");

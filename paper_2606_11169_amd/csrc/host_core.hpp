@@ -40,7 +40,7 @@ size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E);
 // acquiring entry (F, or Bi beside Bw) first.
 lc_status flatten_order(const lc_order &order, std::vector<lc_order_entry> *flat);
 
-// Validates a stage descriptor (shapes, dtype, limits of this build).
+// Validates a stage descriptor (shapes, dtype, the kernels' limits).
 lc_status validate_desc(const lc_stage_desc *d);
 
 // Per-layer sizes of the canonical flat bucket.

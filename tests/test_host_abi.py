@@ -319,3 +319,28 @@ def test_timer_entry_points_reject_bad_arguments():
     n = ctypes.c_int32(-1)
     assert L.lc_stage_timer_read(None, None, None, 0, ctypes.byref(n)) == lc.LC_ERR_INVALID_ARG
     assert n.value == -1
+
+
+def test_missing_library_fails_loudly():
+    """No fallback: without the built HIP library every entry point raises."""
+    import subprocess
+    import sys
+    code = ("from paper_2606_11169_amd import libchunk as lc\n"
+            "lc.LIB_PATH = '/nonexistent/libchunk.so'\n"
+            "try:\n"
+            "    lc.lc_param_count(lc.desc_of_config(__import__('synth').TINY_FP32))\n"
+            "except RuntimeError as e:\n"
+            "    print('raised:', e)\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=str(__import__('pathlib').Path(__file__).resolve().parents[1]),
+                         timeout=120)
+    assert "raised:" in out.stdout and "is missing" in out.stdout, out.stdout + out.stderr
+
+
+def test_runner_refuses_to_run_without_a_gpu():
+    import torch
+    from paper_2606_11169_amd.runner import require_gpu
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(RuntimeError, match="needs a ROCm GPU"):
+        require_gpu()

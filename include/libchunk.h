@@ -241,12 +241,15 @@ lc_status lc_order_validate_split(const lc_order *order, int32_t max_in_flight,
 lc_status lc_order_validate(const lc_order *order, int32_t max_in_flight, int32_t *peak);
 
 /* Device workspace a stage needs for max_in_flight stashed microbatches and
- * max_w_pending weight-pass slots (0 <= max_w_pending <= max_in_flight; > 0
- * only for dense stages): activation stash, weight-pass slots, backward
- * scratch and RoPE table. A weight-pass slot holds, per layer, the gradient
- * operands of the weight products ([T, d], [T, 2 d_ff], [T, d], [T, 3d] in
- * the compute dtype, T = micro_batch * seq_len) and the two norms' fp32
- * gain-gradient partial sums. */
+ * max_w_pending weight-pass slots (0 <= max_w_pending <= max_in_flight):
+ * activation stash, weight-pass slots, backward scratch and RoPE table. A
+ * weight-pass slot holds, per layer, the gradient operands of the weight
+ * products ([T, d], [R, 2 f], [T, d], [T, d + 2 d_kv] in the compute dtype,
+ * T = micro_batch * seq_len; R = T and f = d_ff for a dense FFN, R = 2T
+ * routed rows and f = d_ff_expert for a mixture of experts, which also keeps
+ * its routed dy rows [2T, d], router logit gradients [T, 2] fp32 and the
+ * router gradient's fp32 partial sums) and the norms' fp32 gain-gradient
+ * partial sums. */
 lc_status lc_workspace_bytes_split(const lc_stage_desc *desc, int32_t max_in_flight,
                                    int32_t max_w_pending, size_t *bytes);
 
@@ -284,13 +287,12 @@ lc_status chunk_forward(lc_stage *stage, const lc_param_bufs *params,
 lc_status chunk_backward(lc_stage *stage, const lc_param_bufs *params,
                          const lc_microbatch_desc *mb, void *stream);
 
-/* Chunk BI of one microbatch (dense stages): dX = (dY/dX)^T dY exactly as
+/* Chunk BI of one microbatch: dX = (dY/dX)^T dY exactly as
  * chunk_backward computes it, without the parameter gradient. Reads dy now
  * (and x, for the first layer's norm); writes the weight products' gradient
  * operands and the norms' gain partial sums into a free weight-pass slot
  * (LC_ERR_STASH_FULL if none). The stash slot stays taken until BW.
- * LC_ERR_STATE if mb has no stashed forward or already ran BI;
- * LC_ERR_UNSUPPORTED for mixture-of-experts stages. */
+ * LC_ERR_STATE if mb has no stashed forward or already ran BI. */
 lc_status chunk_backward_input(lc_stage *stage, const lc_param_bufs *params,
                                const lc_microbatch_desc *mb, void *stream);
 

@@ -121,8 +121,6 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_
   if (max_in_flight <= 0) return fail(LC_ERR_INVALID_ARG, "max_in_flight must be positive");
   if (max_w_pending < 0 || max_w_pending > max_in_flight)
     return fail(LC_ERR_INVALID_ARG, "max_w_pending must be in [0, max_in_flight]");
-  if (max_w_pending > 0 && d.n_experts > 0)
-    return fail(LC_ERR_UNSUPPORTED, "split backward of mixture-of-experts stages");
   StagePlan p{};
   p.ty = stage_types(d);
   const size_t es = bytes_of(p.ty.op), ea = bytes_of(p.ty.att), er = bytes_of(p.ty.res);
@@ -187,6 +185,11 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_
   p.w_p2 = wtake(rmsnorm_scratch_size(T, d.d_model));
   p.w_p1 = wtake(rmsnorm_scratch_size(T, d.d_model));
   p.w_pqk = d.qk_norm ? wtake(qknorm_scratch_size(T, d.head_dim)) : 0;
+  if (moe) {
+    p.w_dys = wtake(R * D * es);
+    p.w_dl = wtake((size_t)T * 2 * 4);
+    p.w_rpart = wtake(moe_router_scratch_size(T, d.d_model, d.n_experts));
+  }
   p.wlayer_bytes = wo;
   p.wslot_bytes = wo * (size_t)d.n_layers;
   p.w_slots = max_w_pending;

@@ -91,6 +91,7 @@ struct StagePlan {
   int32_t w_slots;
   size_t wslot0, wslot_bytes, wlayer_bytes;
   size_t w_dy, w_da, w_dh, w_dqkv, w_p2, w_p1, w_pqk;
+  size_t w_dys, w_dl, w_rpart;  // MoE layers: routed dy rows, router logit gradients, dWr partials
   // MoE per-layer extras (0 when dense): routing (sel, w [T, 2]), dispatch
   // (perm, wrow [2T], rowpos [T, 2], expert offsets [E + 1]), the gathered
   // expert inputs xp [2T, d] (op type) and expert outputs eo [2T, d] (fp32)

@@ -176,11 +176,45 @@ static lc_status moe_forward(lc_stage *st, const W &w, const LayerBufs &L, void 
                             ma.rowpos, out, out_dt, T, (int)D, s);
 }
 
+// G[W2_e] += dys_e^T act_e over each expert's rows
+static lc_status moe_w2_grad(lc_stage *st, const W &w, const LayerBufs &L, const void *dys,
+                             hipStream_t s) {
+  const StagePlan &P = st->plan;
+  const ParamPlan &pp = st->pp;
+  const int64_t D = st->d.d_model, FE = st->d.d_ff_expert, R = 2 * P.T;
+  lc_gemm_args a = gemm_base(st->d.compute_dtype, LC_EPI_ACCUM_F32, D, FE, R);
+  a.A = dys; a.lda = D; a.a_kmajor = 0;
+  a.B = L.at(P.act); a.ldb = FE; a.b_kmajor = 0;
+  a.C = w.gp(pp.expert0 + 2 * FE * D); a.ldc = FE;
+  a.group_mode = LC_GROUP_K; a.n_groups = st->d.n_experts;
+  a.group_offsets = static_cast<const int32_t *>(L.at(P.moe_off));
+  a.group_stride_c = (int64_t)pp.expert_stride;
+  return wgrad_launch(st, a, s);
+}
+
+// G[W1_e; W3_e] += [dgate | dup]_e^T xp_e
+static lc_status moe_w13_grad(lc_stage *st, const W &w, const LayerBufs &L, const void *da,
+                              hipStream_t s) {
+  const StagePlan &P = st->plan;
+  const ParamPlan &pp = st->pp;
+  const int64_t D = st->d.d_model, FE = st->d.d_ff_expert, R = 2 * P.T;
+  lc_gemm_args a = gemm_base(st->d.compute_dtype, LC_EPI_ACCUM_F32, 2 * FE, D, R);
+  a.A = da; a.lda = 2 * FE; a.a_kmajor = 0;
+  a.B = L.at(P.moe_xp); a.ldb = D; a.b_kmajor = 0;
+  a.C = w.gp(pp.expert0); a.ldc = D;
+  a.group_mode = LC_GROUP_K; a.n_groups = st->d.n_experts;
+  a.group_offsets = static_cast<const int32_t *>(L.at(P.moe_off));
+  a.group_stride_c = (int64_t)pp.expert_stride;
+  return wgrad_launch(st, a, s);
+}
+
 // MoE FFN of one layer (Chunk B): given dy (the gradient at the layer output),
 // writes dn = dL/dn2 (fp32, P.s_dn) and adds the expert and router weight
-// gradients into the bucket.
+// gradients into the bucket. With a weight-pass layer block WL (the backward
+// for the inputs) the routed dy rows, [dgate | dup] and the router logit
+// gradients go there instead, and moe_weight adds the weight gradients.
 static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, const void *dy,
-                              int dy_dt, hipStream_t s) {
+                              int dy_dt, hipStream_t s, const LayerBufs *WL = nullptr) {
   const lc_stage_desc &d = st->d;
   const StagePlan &P = st->plan;
   const ParamPlan &pp = st->pp;
@@ -191,11 +225,11 @@ static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, cons
   char *ws = st->ws;
   const int32_t *off = static_cast<const int32_t *>(L.at(P.moe_off));
   const float *eo = static_cast<const float *>(L.at(P.moe_eo));
-  void *dys = ws + P.s_moe_dys;
+  void *dys = WL ? WL->at(P.w_dys) : ws + P.s_moe_dys;
   float *dns = reinterpret_cast<float *>(ws + P.s_moe_dns);
   float *dw = reinterpret_cast<float *>(ws + P.s_moe_dw);
-  float *dl = reinterpret_cast<float *>(ws + P.s_moe_dl);
-  void *da = ws + P.s_da;
+  float *dl = WL ? static_cast<float *>(WL->at(P.w_dl)) : reinterpret_cast<float *>(ws + P.s_moe_dl);
+  void *da = WL ? WL->at(P.w_da) : ws + P.s_da;
   // dys[r] = wrow[r] dy[perm[r]], dw[r] = dy[perm[r]] . eo[r]
   LC_TRY(moe_bwd_gather_launch(dy, dy_dt, eo, static_cast<const int32_t *>(L.at(P.moe_perm)),
                                static_cast<const float *>(L.at(P.moe_wrow)), dys, ty.op, dw, R,
@@ -209,14 +243,7 @@ static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, cons
   a.group_mode = LC_GROUP_ROWS; a.n_groups = E; a.group_offsets = off;
   a.group_stride_b = (int64_t)pp.expert_stride;
   LC_TRY(gemm_launch(a, s));
-  // G[W2_e] += dys_e^T act_e over each expert's rows
-  a = gemm_base(dt, LC_EPI_ACCUM_F32, D, FE, R);
-  a.A = dys; a.lda = D; a.a_kmajor = 0;
-  a.B = L.at(P.act); a.ldb = FE; a.b_kmajor = 0;
-  a.C = w.gp(pp.expert0 + 2 * FE * D); a.ldc = FE;
-  a.group_mode = LC_GROUP_K; a.n_groups = E; a.group_offsets = off;
-  a.group_stride_c = (int64_t)pp.expert_stride;
-  LC_TRY(wgrad_launch(st, a, s));
+  if (!WL) LC_TRY(moe_w2_grad(st, w, L, dys, s));
   // dns = [dgate | dup] [W1_e; W3_e] per expert (fp32)
   a = gemm_base(dt, LC_EPI_STORE_F32, R, D, 2 * FE);
   a.A = da; a.lda = 2 * FE; a.a_kmajor = 1;
@@ -225,22 +252,31 @@ static lc_status moe_backward(lc_stage *st, const W &w, const LayerBufs &L, cons
   a.group_mode = LC_GROUP_ROWS; a.n_groups = E; a.group_offsets = off;
   a.group_stride_b = (int64_t)pp.expert_stride;
   LC_TRY(gemm_launch(a, s));
-  // G[W1_e; W3_e] += [dgate | dup]_e^T xp_e
-  a = gemm_base(dt, LC_EPI_ACCUM_F32, 2 * FE, D, R);
-  a.A = da; a.lda = 2 * FE; a.a_kmajor = 0;
-  a.B = L.at(P.moe_xp); a.ldb = D; a.b_kmajor = 0;
-  a.C = w.gp(pp.expert0); a.ldc = D;
-  a.group_mode = LC_GROUP_K; a.n_groups = E; a.group_offsets = off;
-  a.group_stride_c = (int64_t)pp.expert_stride;
-  LC_TRY(wgrad_launch(st, a, s));
+  if (!WL) LC_TRY(moe_w13_grad(st, w, L, da, s));
   // dn = dns[rowpos0] + dns[rowpos1] + dl Wr; then G[Wr] += dl^T n2
   const int32_t *sel = static_cast<const int32_t *>(L.at(P.moe_sel));
   LC_TRY(moe_bwd_combine_launch(dns, dw, static_cast<const float *>(L.at(P.moe_w)), sel,
                                 static_cast<const int32_t *>(L.at(P.moe_rowpos)), w.wp(pp.wr), dt,
                                 dl, reinterpret_cast<float *>(ws + P.s_dn), T, (int)D, s));
+  if (WL) return LC_OK;
   return moe_router_grad_launch(L.at(P.n2), ty.op, sel, dl,
                                 reinterpret_cast<float *>(ws + P.s_moe_part), P.s_moe_part_bytes,
                                 w.gp(pp.wr), T, (int)D, E, s);
+}
+
+// The backward for the weights of a MoE FFN: the expert and router weight
+// gradients from the operands moe_backward left in the weight-pass layer
+// block WL (the router's partial sums go to WL too).
+static lc_status moe_weight(lc_stage *st, const W &w, const LayerBufs &L, const LayerBufs &WL,
+                            hipStream_t s) {
+  const StagePlan &P = st->plan;
+  LC_TRY(moe_w2_grad(st, w, L, WL.at(P.w_dys), s));
+  LC_TRY(moe_w13_grad(st, w, L, WL.at(P.w_da), s));
+  return moe_router_grad_launch(L.at(P.n2), P.ty.op, static_cast<const int32_t *>(L.at(P.moe_sel)),
+                                static_cast<const float *>(WL.at(P.w_dl)),
+                                static_cast<float *>(WL.at(P.w_rpart)),
+                                moe_router_scratch_size(P.T, st->d.d_model, st->d.n_experts),
+                                w.gp(st->pp.wr), P.T, st->d.d_model, st->d.n_experts, s);
 }
 
 // The per-head q/k norm arguments of one layer (q|k of the packed qkv rows).
@@ -408,7 +444,7 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     char *dqkv = split ? static_cast<char *>(WL.at(P.w_dqkv)) : ws + P.s_dqkv;
     lc_gemm_args a;
     if (d.n_experts > 0) {
-      LC_TRY(moe_backward(st, w, L, dy_res, dy_dt, s));
+      LC_TRY(moe_backward(st, w, L, dy_res, dy_dt, s, split ? &WL : nullptr));
     } else {
     // [dgate | dup] = SwiGLU'(dy W2)
     a = gemm_base(dt, LC_EPI_SWIGLU_BWD, T, F, D);
@@ -549,8 +585,12 @@ static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, 
     const LayerBufs WL = wlayer_bufs(st, wslot, l);
     const size_t lw = (size_t)l * pp.per_layer;
     const W w{static_cast<const char *>(pb->w) + lw * P.elem, pb->grad + lw, P.elem};
+    lc_gemm_args a;
+    if (d.n_experts > 0) {
+      LC_TRY(moe_weight(st, w, L, WL, s));
+    } else {
     // G[W2] += dy^T act
-    lc_gemm_args a = gemm_base(dt, gepi, D, F, T);
+    a = gemm_base(dt, gepi, D, F, T);
     a.A = WL.at(P.w_dy); a.lda = D; a.a_kmajor = 0;
     a.B = L.at(P.act); a.ldb = F; a.b_kmajor = 0;
     a.C = w.gp(pp.w2); a.ldc = F;
@@ -561,6 +601,7 @@ static lc_status weight_layers(lc_stage *st, const lc_param_bufs *pb, int slot, 
     a.B = L.at(P.n2); a.ldb = D; a.b_kmajor = 0;
     a.C = w.gp(pp.w1); a.ldc = D;
     LC_TRY(wgrad_launch(st, a, s));
+    }
     LC_TRY(rmsnorm_dg_final_launch(static_cast<const float *>(WL.at(P.w_p2)), w.gp(pp.g2), T, D, s,
                                    st->grad_store));
     // G[Wo] += dh^T o
@@ -750,8 +791,6 @@ lc_status chunk_backward_input(lc_stage *stage, const lc_param_bufs *params,
                                const lc_microbatch_desc *mb, void *stream) {
   LC_TRY(check_params(stage, params, false));
   LC_TRY(check_mb(mb, false));
-  if (stage->d.n_experts > 0)
-    return fail(LC_ERR_UNSUPPORTED, "split backward of mixture-of-experts stages");
   if (mb->mb < 0 || find_slot(stage, mb->mb) < 0)
     return fail(LC_ERR_STATE, "microbatch %d has no stashed forward", mb->mb);
   if (find_wslot(stage, mb->mb) >= 0)
@@ -1006,11 +1045,6 @@ lc_status check_run(lc_stage *stage, const lc_param_bufs *params, const lc_order
     if (stage->wowner[i] != -1)
       return fail(LC_ERR_STATE, "lc_run_order needs no pending weight pass (microbatch %d)",
                   stage->wowner[i]);
-  bool split = false;
-  for (int i = 0; i < order->n_entries; ++i)
-    split |= (order->entries[i].pass & ~LC_ORDER_WITH_NEXT) == LC_PASS_BI;
-  if (split && stage->d.n_experts > 0)
-    return fail(LC_ERR_UNSUPPORTED, "split backward of mixture-of-experts stages");
   return LC_OK;
 }
 

@@ -362,6 +362,59 @@ def test_moe_overlapped_pair_on_two_streams_is_bit_identical():
         r.close()
 
 
+@pytest.mark.parametrize("w_delay", [0, 1, 2])
+def test_moe_split_backward_is_bit_identical(w_delay):
+    """A mixture-of-experts stage under 1F1B with split backwards (Bi, then Bw
+    w_delay backwards later): the Bi passes leave the routed dy rows, the
+    experts' [dgate | dup] and the router logit gradients in weight-pass
+    slots, the Bw passes add the expert, router and attention weight
+    gradients; outputs and gradient equal the plain 1F1B Order's bit for
+    bit. The split pairs of the overlapped split Order on two streams give
+    the same bits too."""
+    cfg = SMALL_MOE
+    banner(f"moe split backward {cfg.name} w_delay {w_delay}")
+    M = cfg.num_microbatches
+    flat = synth.stage_params(cfg, 2)
+    Xs = [synth.activation(cfg, 2, mb, "x") for mb in range(M)]
+    dYs = [synth.activation(cfg, 2, mb, "dy") for mb in range(M)]
+    P, s = 3, 0
+    plain = lc.lc_order_1f1b(M, P, s)
+    split = lc.lc_order_1f1b_split(M, P, s, w_delay)
+    assert any(p & ~lc.LC_ORDER_WITH_NEXT == lc.LC_PASS_BW for _, p in split)
+    wp = min(w_delay + 1, M)
+    runs = []
+    for order, mwp in ((plain, 0), (split, wp)):
+        r = StageRunner(desc_of(cfg), flat, M, max_w_pending=mwp)
+        r.alloc_microbatches(Xs, dYs)
+        r.run_order(order)
+        torch.cuda.synchronize()
+        runs.append(r)
+    a, b = runs
+    assert torch.equal(a.grad, b.grad)
+    for mb in range(M):
+        assert torch.equal(a.Y[mb], b.Y[mb]) and torch.equal(a.dX[mb], b.dX[mb])
+    b.close()
+    # the split Order with its first adjacent (Bi, Bw) of two microbatches run
+    # as an overlapped pair (Bi first), with a weight-pass slot for each
+    BI, BW, NX = lc.LC_PASS_BI, lc.LC_PASS_BW, lc.LC_ORDER_WITH_NEXT
+    nested = list(split)
+    for i in range(len(nested) - 1):
+        (m1, p1), (m2, p2) = nested[i], nested[i + 1]
+        if {p1, p2} == {BI, BW} and m1 != m2:
+            bi, bw = ((m1, p1), (m2, p2)) if p1 == BI else ((m2, p2), (m1, p1))
+            nested[i:i + 2] = [(bi[0], BI | NX), bw]
+            break
+    else:
+        pytest.fail(f"no adjacent (Bi, Bw) pair in {split}")
+    c = StageRunner(desc_of(cfg), flat, M, max_w_pending=M)
+    c.alloc_microbatches(Xs, dYs)
+    c.run_order(nested, torch.cuda.Stream())
+    torch.cuda.synchronize()
+    assert torch.equal(a.grad, c.grad)
+    for r in (a, c):
+        r.close()
+
+
 def test_full_size_moe_stage_on_a_prefix():
     """The MoE workload at full size (4 layers, d 2048, 8 experts x 1408,
     2 x 2048 tokens): outputs and gradients on a 128-token prefix of each

@@ -336,8 +336,14 @@ def test_overlapped_pairs_on_two_streams_are_bit_identical(cfg):
     ref.close()
 
 
-@pytest.mark.parametrize("cfg", [synth.TINY_FP32, SMALL_BF16, QWEN_BF16],
-                         ids=["tiny_fp32", "small_bf16", "qwen_bf16"])
+SMALL_MOE_ZERO = synth.StageConfig(
+    name="small_moe_zero", n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ff=0,
+    seq_len=256, micro_batch=2, num_microbatches=3, bf16=True, n_experts=4, top_k=2,
+    d_ff_expert=128, pp_size=3, pp_rank=0)
+
+
+@pytest.mark.parametrize("cfg", [synth.TINY_FP32, SMALL_BF16, QWEN_BF16, SMALL_MOE_ZERO],
+                         ids=["tiny_fp32", "small_bf16", "qwen_bf16", "small_moe"])
 def test_zero_paths_give_the_accumulated_gradient_slices(cfg):
     """ZeRO-2/3 on one GPU (each backward into a temporary full gradient,
     then this rank's slice added into its persistent shard; at level 3 the

@@ -476,15 +476,16 @@ def test_full_size_stage_on_a_prefix(cfg, tol):
     assert errs[worst] <= tol, (worst, errs[worst])
 
 
-def test_full_size_split_backward_is_bit_identical():
-    """The 7B-shaped stage, two microbatches: the split Order (Bi0 Bi1 Bw0
-    Bw1, two weight passes pending) gives the plain Order's dX and gradient
-    bit for bit."""
+@pytest.mark.parametrize("cfg", [synth.STAGE_7B, synth.MOE_2K], ids=["7b", "moe"])
+def test_full_size_split_backward_is_bit_identical(cfg):
+    """The 7B-shaped and the mixture-of-experts stage at full size, two
+    microbatches: the split Order (Bi0 Bi1 Bw0 Bw1, two weight passes
+    pending) gives the plain Order's dX and gradient bit for bit."""
     from paper_2606_11169_amd.runner import random_stage
-    cfg = synth.STAGE_7B
-    banner("full-size split backward")
+    banner(f"full-size split backward {cfg.name}")
+    P = cfg.pp_size
     got = []
-    for order, wp in ((OO.one_f_one_b(2, 8, 0), 0), (OO.one_f_one_b_split(2, 8, 0, 1), 2)):
+    for order, wp in ((OO.one_f_one_b(2, P, 0), 0), (OO.one_f_one_b_split(2, P, 0, 1), 2)):
         r = random_stage(desc_of(cfg), 2, seed=1, max_w_pending=wp)
         r.alloc_random_microbatches(2, seed=2)
         r.run_order(to_c(order))

@@ -358,7 +358,7 @@ def main():
                     help="only the calibration copy and the 7B-shaped stage with its weight-gradient "
                          "launches timed (PMC runs)")
     ap.add_argument("--split-only", type=int, default=None, metavar="W_DELAY",
-                    help="only the 7B-shaped stage with split backwards (Bw W_DELAY "
+                    help="only the 7B-shaped and MoE stages with split backwards (Bw W_DELAY "
                          "backwards after its Bi)")
     ap.add_argument("--qwen3-only", action="store_true",
                     help="only the Qwen3-8B-shaped stage (q/k norm, 8 key/value heads), flat "
@@ -400,12 +400,14 @@ def main():
                                         "unit": "TFLOP/s", "ms_per_step": round(mms, 2)}}))
         return
     if args.split_only is not None:
-        sms, stf, sfin = time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "split",
-                                    w_delay=args.split_only)
-        print(json.dumps({"split_stage": {"workload": cfg.name, "w_delay": args.split_only,
-                                          "value": round(stf, 2), "unit": "TFLOP/s",
-                                          "ms_per_step": round(sms, 2),
-                                          "outputs_finite": sfin}}))
+        res = {}
+        for c in (cfg, synth.MOE_2K):
+            sms, stf, sfin = time_stage(torch, lc, c, stream, args.steps, args.warmup, "split",
+                                        w_delay=args.split_only)
+            res[c.name] = {"w_delay": args.split_only, "value": round(stf, 2),
+                           "unit": "TFLOP/s", "ms_per_step": round(sms, 2),
+                           "step_ms": STEP_STATS.get("split"), "outputs_finite": sfin}
+        print(json.dumps({"split_stage": res}))
         return
     if args.qwen3_only:
         qc = synth.QWEN3_STAGE

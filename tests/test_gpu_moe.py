@@ -274,7 +274,8 @@ def test_moe_stage_with_an_expert_that_receives_no_tokens():
     the lower index wins), so expert 3 gets no rows. Its weight gradients and
     its router row's gradient are exactly zero, and every output and gradient
     matches the oracle given the GPU's routing (the oracle's own routing
-    agrees except where u.n2 is within rounding of 0)."""
+    agrees except where u.n2 is within rounding of 0). Split backwards give
+    the same gradient and dX bit for bit."""
     cfg = SMALL_MOE
     banner("moe stage with an unused expert")
     M, E, d = cfg.num_microbatches, cfg.n_experts, cfg.d_model
@@ -302,6 +303,21 @@ def test_moe_stage_with_an_expert_that_receives_no_tokens():
         for l in range(cfg.n_layers):
             sel = routes[mb][l]
             assert np.all(sel[:, 1] == 2) and np.all(np.isin(sel[:, 0], (0, 1))), (mb, l)
+    # the same microbatches with split backwards (all Bi, then all Bw): the
+    # unused expert's grouped weight products run over empty groups there too
+    rs = StageRunner(desc_of(cfg), flat, M, max_w_pending=M)
+    rs.alloc_microbatches(Xs, dYs)
+    for mb in range(M):
+        rs.forward(mb)
+    for mb in range(M):
+        rs.backward_input(mb)
+    for mb in range(M):
+        rs.backward_weight(mb)
+    torch.cuda.synchronize()
+    assert torch.equal(rs.grad, r.grad)
+    for mb in range(M):
+        assert torch.equal(rs.dX[mb], r.dX[mb])
+    rs.close()
     got = host(r.grad)
     gg = synth.unflatten(cfg, got)
     for l in range(cfg.n_layers):

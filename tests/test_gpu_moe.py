@@ -221,8 +221,16 @@ def desc_of(cfg):
     return lc.desc_of_config(cfg)
 
 
-def test_moe_stage_matches_oracle_with_gpu_routing():
-    cfg = SMALL_MOE
+# Qwen3-MoE-style attention on a mixture-of-experts stage: grouped-query
+# attention (4 query heads over 2 key/value heads) with per-head q/k RMSNorm
+SMALL_MOE_QK = synth.StageConfig(
+    name="small_moe_qk", n_layers=2, d_model=512, n_heads=4, head_dim=128, d_ff=0, seq_len=256,
+    micro_batch=2, num_microbatches=2, bf16=True, n_experts=4, top_k=2, d_ff_expert=128,
+    n_kv_heads=2, qk_norm=True, rms_eps=1e-6, rope_base=1000000.0, pp_size=2, pp_rank=0)
+
+
+@pytest.mark.parametrize("cfg", [SMALL_MOE, SMALL_MOE_QK], ids=["mha", "gqa_qknorm"])
+def test_moe_stage_matches_oracle_with_gpu_routing(cfg):
     banner(f"moe stage {cfg.name}")
     M = cfg.num_microbatches
     flat = synth.stage_params(cfg, 0)

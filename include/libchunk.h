@@ -228,6 +228,14 @@ lc_status lc_order_1f1b_overlap(int32_t M, int32_t P, int32_t s, lc_order_entry 
 lc_status lc_order_1f1b_split(int32_t M, int32_t P, int32_t s, int32_t w_delay,
                               lc_order_entry *out, int32_t capacity, int32_t *n);
 
+/* lc_order_1f1b_split with every BI that is directly followed by the BW of
+ * another microbatch flagged LC_ORDER_WITH_NEXT: the two run as an
+ * overlapped pair (a weight pass beside the next microbatch's input pass,
+ * Section 4.1's nested Order), each entry in at most one pair. Same
+ * arguments and errors as lc_order_1f1b_split. */
+lc_status lc_order_1f1b_split_overlap(int32_t M, int32_t P, int32_t s, int32_t w_delay,
+                                      lc_order_entry *out, int32_t capacity, int32_t *n);
+
 /* Checks an Order against the rules above for at most max_in_flight
  * stashed microbatches and max_w_pending pending weight passes. *peak and
  * *peak_w (nullable) receive the largest numbers of each seen. Returns

@@ -95,6 +95,24 @@ def one_f_one_b_overlap(M: int, P: int, s: int) -> list:
     return out
 
 
+def one_f_one_b_split_overlap(M: int, P: int, s: int, w_delay: int) -> list:
+    """The split 1F1B Order with each Bi that another microbatch's Bw directly
+    follows nested with that Bw as an overlapped pair (the weight pass runs
+    beside the next input pass); an entry joins at most one pair."""
+    seq = one_f_one_b_split(M, P, s, w_delay)
+    out: list = []
+    i = 0
+    while i < len(seq):
+        nxt = seq[i + 1] if i + 1 < len(seq) else None
+        if seq[i][1] == "Bi" and nxt is not None and nxt[1] == "Bw" and nxt[0] != seq[i][0]:
+            out.append([seq[i], nxt])
+            i += 2
+        else:
+            out.append(seq[i])
+            i += 1
+    return out
+
+
 _PAIRS = ({"F", "B"}, {"F", "Bi"}, {"F", "Bw"}, {"Bi", "Bw"})
 
 

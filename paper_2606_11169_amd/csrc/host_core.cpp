@@ -413,6 +413,19 @@ lc_status lc_order_1f1b_split(int32_t M, int32_t P, int32_t s, int32_t w_delay,
   return LC_OK;
 }
 
+lc_status lc_order_1f1b_split_overlap(int32_t M, int32_t P, int32_t s, int32_t w_delay,
+                                      lc_order_entry *out, int32_t capacity, int32_t *n) {
+  LC_TRY(lc_order_1f1b_split(M, P, s, w_delay, out, capacity, n));
+  // each Bi with another microbatch's Bw right after it becomes a pair (an
+  // entry belongs to at most one pair)
+  for (int32_t i = 0; i + 1 < *n; ++i)
+    if (out[i].pass == LC_PASS_BI && out[i + 1].pass == LC_PASS_BW && out[i].mb != out[i + 1].mb) {
+      out[i].pass |= LC_ORDER_WITH_NEXT;
+      ++i;
+    }
+  return LC_OK;
+}
+
 lc_status lc_order_validate_split(const lc_order *order, int32_t max_in_flight,
                                   int32_t max_w_pending, int32_t *peak, int32_t *peak_w) {
   if (peak) *peak = 0;

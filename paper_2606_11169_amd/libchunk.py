@@ -158,6 +158,9 @@ _SIGS = {
     "lc_order_1f1b_split": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                       C.POINTER(lc_order_entry), C.c_int32,
                                       C.POINTER(C.c_int32)]),
+    "lc_order_1f1b_split_overlap": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                              C.POINTER(lc_order_entry), C.c_int32,
+                                              C.POINTER(C.c_int32)]),
     "lc_order_validate": (C.c_int, [C.POINTER(lc_order), C.c_int32, C.POINTER(C.c_int32)]),
     "lc_order_validate_split": (C.c_int, [C.POINTER(lc_order), C.c_int32, C.c_int32,
                                           C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
@@ -309,6 +312,13 @@ def lc_order_1f1b_split(M, P, s, w_delay) -> List[Tuple[int, int]]:
     buf = (lc_order_entry * max(1, 3 * M))()
     n = C.c_int32()
     _check(lib().lc_order_1f1b_split(M, P, s, w_delay, buf, 3 * M, C.byref(n)))
+    return [(buf[i].mb, buf[i].pass_) for i in range(n.value)]
+
+
+def lc_order_1f1b_split_overlap(M, P, s, w_delay) -> List[Tuple[int, int]]:
+    buf = (lc_order_entry * max(1, 3 * M))()
+    n = C.c_int32()
+    _check(lib().lc_order_1f1b_split_overlap(M, P, s, w_delay, buf, 3 * M, C.byref(n)))
     return [(buf[i].mb, buf[i].pass_) for i in range(n.value)]
 
 

@@ -430,13 +430,17 @@ def test_moe_split_backward_is_bit_identical(w_delay):
             break
     else:
         pytest.fail(f"no adjacent (Bi, Bw) pair in {split}")
-    c = StageRunner(desc_of(cfg), flat, M, max_w_pending=M)
-    c.alloc_microbatches(Xs, dYs)
-    c.run_order(nested, torch.cuda.Stream())
-    torch.cuda.synchronize()
-    assert torch.equal(a.grad, c.grad)
-    for r in (a, c):
-        r.close()
+    gen = lc.lc_order_1f1b_split_overlap(M, P, s, w_delay)  # the generator's nesting
+    for order in (nested, gen):
+        c = StageRunner(desc_of(cfg), flat, M, max_w_pending=M)
+        c.alloc_microbatches(Xs, dYs)
+        c.run_order(order, torch.cuda.Stream())
+        torch.cuda.synchronize()
+        assert torch.equal(a.grad, c.grad)
+        for mb in range(M):
+            assert torch.equal(a.dX[mb], c.dX[mb])
+        c.close()
+    a.close()
 
 
 def test_full_size_moe_stage_on_a_prefix():

@@ -178,6 +178,13 @@ def test_1f1b_overlap_matches_oracle(M, P, s):
     assert lc.lc_order_1f1b_overlap(M, P, s) == to_c(OO.one_f_one_b_overlap(M, P, s))
 
 
+@pytest.mark.parametrize("M,P,s,wd", [(8, 4, 0, 1), (8, 4, 0, 0), (16, 8, 0, 2), (3, 5, 1, 1),
+                                      (4, 1, 0, 1), (1, 1, 0, 0), (16, 8, 0, 7)])
+def test_1f1b_split_overlap_matches_oracle(M, P, s, wd):
+    assert lc.lc_order_1f1b_split_overlap(M, P, s, wd) == to_c(
+        OO.one_f_one_b_split_overlap(M, P, s, wd))
+
+
 def test_overlapped_pairs_match_oracle():
     from tests.test_oracle_order import PAIR_RULES
     for M, body, status, peak in PAIR_RULES:

@@ -168,3 +168,19 @@ def test_1f1b_overlap_nests_the_steady_state(M, P, s):
     assert pairs == ([[(W + i, "F"), (i, "B")] for i in range(M - W)] if W else [])
     st, pk = OO.validate(seq, M, M)
     assert st == "OK" and pk == min(P - s, M)
+
+
+@pytest.mark.parametrize("M,P,s,wd", [(8, 4, 0, 1), (8, 4, 0, 0), (16, 8, 0, 2), (3, 5, 1, 1),
+                                      (4, 1, 0, 1), (1, 1, 0, 0)])
+def test_split_overlap_nests_bi_with_the_next_bw(M, P, s, wd):
+    seq = OO.one_f_one_b_split_overlap(M, P, s, wd)
+    assert OO.flatten(seq) == OO.one_f_one_b_split(M, P, s, wd)
+    for e in seq:
+        if isinstance(e, list):
+            (m1, p1), (m2, p2) = e
+            assert (p1, p2) == ("Bi", "Bw") and m1 != m2
+    st, pk = OO.validate(seq, M, M, M)
+    assert st == "OK"
+    # w_delay 1 in the steady state: Bi(j) beside Bw(j - 1)
+    if wd == 1 and M - min(P - s - 1, M) > 1:
+        assert any(isinstance(e, list) for e in seq)

@@ -78,6 +78,7 @@ struct GemmP {
   uint32_t a_bytes, b_bytes;  // byte extent of each operand (< 2^31)
   int M, N, K;  // N: output columns (SwiGLU: gate/up width)
   int tiles_m, tiles_n;
+  int group;  // tile-rows per group of the tile walk
   int gmode, ngroups;
   const int32_t *goff;
   int64_t gstride_b, gstride_c;
@@ -234,8 +235,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   const int wm = w4, wn = grp;  // group g owns output columns [128 g, 128 g + 128)
 
   // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-  // contiguous run of tiles, then walk tiles in groups of 8 tile-rows so that
-  // neighbouring workgroups share A rows and B columns in the XCD's L2.
+  // contiguous run of tiles, then walk tiles in groups of p.group tile-rows
+  // (4 or 8, chosen by the host) so that neighbouring workgroups share A rows
+  // and B columns in the XCD's L2.
   int wg = blockIdx.x;
   const int nwg = gridDim.x;
   if ((nwg & 7) == 0) wg = (wg & 7) * (nwg >> 3) + (wg >> 3);
@@ -268,10 +270,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
       kend = min(max(p.goff[g + 1], kbeg), p.K);
       Cp = static_cast<char *>(p.C) + (int64_t)g * p.gstride_c * (p.c_dt == LC_FP32 ? 4 : 2);
     }
-    constexpr int GROUP = 8;
-    const int per_group = GROUP * p.tiles_n;
-    const int first_m = (t / per_group) * GROUP;
-    const int gsz = min(p.tiles_m - first_m, GROUP);
+    const int per_group = p.group * p.tiles_n;
+    const int first_m = (t / per_group) * p.group;
+    const int gsz = min(p.tiles_m - first_m, p.group);
     m0 = (first_m + (t % per_group) % gsz) * BM;
     tn = (t % per_group) / gsz;
   }
@@ -611,6 +612,9 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
   p.tiles_m = (int)((a.M + BM - 1) / BM);
   p.tiles_n = a.epilogue == LC_EPI_SWIGLU ? (int)((a.N + BN / 2 - 1) / (BN / 2))
                                           : (int)((a.N + BN - 1) / BN);
+  // 4 tile-rows per group when the grid is wide (32 or more tile-columns),
+  // else 8: the faster walk measured on the stage's shapes
+  p.group = p.tiles_n >= 32 ? 4 : 8;
   p.gmode = a.group_mode;
   p.ngroups = a.group_mode == LC_GROUP_NONE ? 1 : a.n_groups;
   p.goff = a.group_offsets;

@@ -357,3 +357,30 @@ def test_runner_refuses_to_run_without_a_gpu():
         pytest.skip("a GPU is present")
     with pytest.raises(RuntimeError, match="needs a ROCm GPU"):
         require_gpu()
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU's share: --gpus 2 exits with status 2 and a
+    message, before touching a GPU."""
+    import pathlib
+    import subprocess
+    import sys
+    root = pathlib.Path(__file__).resolve().parents[1]
+    out = subprocess.run([sys.executable, str(root / "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, cwd=str(root), timeout=120)
+    assert out.returncode == 2
+    assert "--gpus 2 is not supported" in out.stderr
+
+
+def test_bench_reads_the_committed_counter_summaries():
+    """The roofline traffic and matrix-core busy figures parse from profiles/
+    (a number while the sources match the recorded hashes, else None)."""
+    import importlib.util
+    import pathlib
+    root = pathlib.Path(__file__).resolve().parents[1]
+    spec = importlib.util.spec_from_file_location("bench_mod", root / "bench.py")
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    for v in (bench.measured_traffic(), bench.measured_mfma_busy()):
+        assert v is None or v > 0
+    assert len(bench.csrc_hash()) == 16 and len(bench.gemm_source_hash()) == 16

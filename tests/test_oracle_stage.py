@@ -470,3 +470,87 @@ def test_qk_norm_unit_rms_and_scale_invariance():
         w *= rng.uniform(0.5, 3.0, size=(nh, 1, 1))
     Y2, _ = O.layer_forward(O.layer_params(cfg, synth.flatten(cfg, named))[0], X, cfg, tabs)
     assert np.max(np.abs(Y2 - Y)) <= 1e-12 * np.max(np.abs(Y))
+
+
+# ---------------------------------------------------------------- readings
+# Closed forms that fix three readings of the layer which finite differences
+# cannot see (they only check the backward against the forward): the score
+# scale 1/sqrt(hd), the pre-norm residual composition and the roles of the
+# two FFN input matrices (W1 the silu gate, W3 the linear up branch).
+
+def test_attention_score_scale_is_inverse_sqrt_head_dim():
+    """One query over two keys, hd = 8. q.k0 = 0 and q.k1 = sqrt(8) ln 3, so
+    with scores q.k/sqrt(hd) the second query's weights are 1/4 and 3/4
+    exactly (e^0 : e^(ln 3) = 1 : 3) and its output is v0/4 + 3 v1/4; a
+    scale of 1/hd would give weights 1 : 3^(1/sqrt 8) instead."""
+    hd = 8
+    q = np.zeros((1, 2, 1, hd))
+    k = np.zeros((1, 2, 1, hd))
+    q[0, 1, 0, 0] = 1.0
+    k[0, 1, 0, 0] = np.sqrt(8.0) * np.log(3.0)
+    k[0, 0, 0, 1] = 5.0                       # orthogonal to q: score 0
+    rng = np.random.default_rng(21)
+    v = rng.standard_normal((1, 2, 1, hd))
+    o = O.attention_forward(q, k, v)
+    assert np.max(np.abs(o[0, 1, 0] - (0.25 * v[0, 0, 0] + 0.75 * v[0, 1, 0]))) <= 1e-15
+    assert np.array_equal(o[0, 0, 0], v[0, 0, 0])   # query 0 sees key 0 only
+    P = O.attention_probs(q[0, :, 0], k[0, :, 0])
+    assert abs(P[1, 0] - 0.25) <= 1e-16 and abs(P[1, 1] - 0.75) <= 1e-16
+
+
+def _zero_matrices(cfg, flat, names):
+    named = synth.unflatten(cfg, flat.copy())
+    for key in named:
+        if key.split(".", 1)[1] in names:
+            named[key][...] = 0.0
+    return synth.flatten(cfg, named)
+
+
+def test_residual_composition_zero_matrices_is_identity():
+    """Pre-norm residual layers: every projection matrix zero makes each
+    layer the identity, Y = X and dX = dY exactly, whatever the gains (a
+    post-norm layer would give RMSNorm(X), a dropped residual 0). With only
+    Wo and W2 zero the attention and FFN branches still run but add nothing,
+    so Y = X and dX = dY again."""
+    cfg = tiny_cfg()
+    flat, X, dY = random_inputs(cfg, 12)
+    allz = _zero_matrices(cfg, flat, {"wq", "wk", "wv", "wo", "w1", "w3", "w2"})
+    Y, dX, G = grads(cfg, allz, X, dY)
+    assert np.array_equal(Y, X) and np.array_equal(dX, dY)
+    outz = _zero_matrices(cfg, flat, {"wo", "w2"})
+    Y, dX, G = grads(cfg, outz, X, dY)
+    assert np.array_equal(Y, X) and np.array_equal(dX, dY)
+    # the branches did run: their output matrices receive nonzero gradients
+    gn = synth.unflatten(cfg, G)
+    assert np.any(gn["L0.wo"] != 0.0) and np.any(gn["L1.w2"] != 0.0)
+
+
+def test_swiglu_gate_is_w1_and_up_is_w3():
+    """A layer whose FFN sees n2 = 4 e0 on every token (attention zeroed,
+    X = 4 e0, eps 0, unit gains, d = 16): W3's column 0 is 1/4, so the up
+    branch is exactly 1, and W1's column 0 is z/4, so the gate is z. With W2
+    the identity (d_ff = d) the layer adds a = silu(z) * 1 to the residual:
+    Y - X = z / (1 + e^-z). Swapping the roles would add silu(1) z."""
+    cfg = tiny_cfg(n_layers=1, d_ff=16, rms_eps=0.0)
+    d = cfg.d_model
+    named = synth.unflatten(cfg, synth.stage_params(cfg, seed=3).astype(F64))
+    rng = np.random.default_rng(22)
+    z = rng.uniform(-4.0, 4.0, size=d)
+    for key in ("wq", "wk", "wv", "wo"):
+        named[f"L0.{key}"][...] = 0.0
+    named["L0.g1"][:] = 1.0
+    named["L0.g2"][:] = 1.0
+    named["L0.w1"][...] = rng.standard_normal((d, d))
+    named["L0.w1"][:, 0] = z / 4.0
+    named["L0.w3"][...] = rng.standard_normal((d, d))
+    named["L0.w3"][:, 0] = 0.25
+    named["L0.w2"][...] = np.eye(d)
+    flat = synth.flatten(cfg, named)
+    X = np.zeros((cfg.micro_batch, cfg.seq_len, d))
+    X[..., 0] = 4.0
+    Y, _, _ = grads(cfg, flat, X, np.zeros_like(X))
+    want = np.array([zi / (1.0 + np.exp(-zi)) for zi in z])
+    got = Y - X
+    assert np.max(np.abs(got - want[None, None, :])) <= 1e-14
+    swapped = 1.0 / (1.0 + np.exp(-1.0)) * z
+    assert np.max(np.abs(got - swapped[None, None, :])) > 0.1

@@ -199,12 +199,19 @@ typedef struct lc_stage lc_stage; /* opaque, host memory */
 /* ---------------------------------------------------------------- host-only
  * These make no HIP call and may be used without a GPU. */
 
-/* Number of elements of the stage's flat bucket. */
+/* Number of elements of the stage's flat bucket: the one flat parameter
+ * (and gradient) buffer per bucket that Piper's workers keep (Section 4.3.2,
+ * "Memory management"; Section 6.2 shards such buffers for ZeRO). Per
+ * layer, in order: Wq, Wk, Wv, Wo, g1, then W1 (gate), W3 (up), W2 (down)
+ * or, for a mixture of experts, Wr and each expert's W1, W3, W2, then g2
+ * (q/k gains after g1 when qk_norm is set). LC_ERR_INVALID_ARG for a bad
+ * descriptor. */
 lc_status lc_param_count(const lc_stage_desc *desc, size_t *n_elems);
 
 /* Offset (elements) and shape of tensor `tensor_id` of layer `layer`
- * (expert `expert` for MoE W1/W3/W2, else pass 0). shape[1] is 1 for
- * vectors. */
+ * (expert `expert` for MoE W1/W3/W2, else pass 0) in the flat bucket of
+ * lc_param_count (Section 4.3.2, "Memory management"). shape[1] is 1 for
+ * vectors. LC_ERR_INVALID_ARG for an index out of range. */
 lc_status lc_param_offset(const lc_stage_desc *desc, int32_t layer, int32_t tensor_id,
                           int32_t expert, size_t *offset, int64_t shape[2]);
 
@@ -249,7 +256,11 @@ lc_status lc_order_validate_split(const lc_order *order, int32_t max_in_flight,
 lc_status lc_order_validate(const lc_order *order, int32_t max_in_flight, int32_t *peak);
 
 /* Device workspace a stage needs for max_in_flight stashed microbatches and
- * max_w_pending weight-pass slots (0 <= max_w_pending <= max_in_flight):
+ * max_w_pending weight-pass slots (0 <= max_w_pending <= max_in_flight). The
+ * caller allocates it once; the stage carves it into the buffers that
+ * Piper's memory manager allocates per task and frees after their last
+ * consumer (Section 4.3.2, "Memory management"), reused here in stream
+ * order:
  * activation stash, weight-pass slots, backward scratch and RoPE table. A
  * weight-pass slot holds, per layer, the gradient operands of the weight
  * products ([T, d], [R, 2 f], [T, d], [T, d + 2 d_kv] in the compute dtype,
@@ -316,7 +327,10 @@ lc_status chunk_backward_weight(lc_stage *stage, const lc_param_bufs *params,
 /* Runs a whole Order: validates it (no side effects on failure), then
  * enqueues chunk_forward / chunk_backward / chunk_backward_input /
  * chunk_backward_weight in entry order. mbs[i] describes microbatch i
- * (num_microbatches entries). */
+ * (num_microbatches entries). Needs an empty stash (LC_ERR_STATE). If a
+ * launch fails after some entries were enqueued, the stash is emptied again
+ * before the error returns (the run's outputs are then undefined), so the
+ * stage stays usable. */
 lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_order *order,
                        const lc_microbatch_desc *mbs, void *stream);
 
@@ -370,8 +384,11 @@ typedef struct lc_zero_bufs {
  * ignored. grad_shard then holds, bit for bit, that slice of the gradient
  * lc_run_order accumulates (every addition into +0 is exact). Overlapped
  * pairs run one after the other. Device buffers 16-byte aligned;
- * LC_ERR_INVALID_ARG for a bad layout (a slice out of range, shard lengths
- * that do not sum to the bucket). */
+ * LC_ERR_INVALID_ARG for a bad layout, before anything is enqueued: a slice
+ * out of range, shard lengths that do not sum to the bucket, a grad_shard
+ * that overlaps grad_full, or a weight shard that overlaps w_full anywhere
+ * but at its own place there (a shard already at its place, an in-place
+ * gather, is not copied). */
 lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const lc_zero_bufs *zero,
                             const lc_order *order, const lc_microbatch_desc *mbs, void *stream);
 

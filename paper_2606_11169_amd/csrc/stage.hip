@@ -32,6 +32,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -899,7 +900,7 @@ lc_status gather_weights(const lc_stage *st, const lc_zero_bufs &z, hipStream_t 
   char *dst = static_cast<char *>(z.w_full);
   for (int i = 0; i < z.n_w_shards; ++i) {
     const size_t bytes = z.w_shard_lens[i] * st->plan.elem;
-    if (bytes) {
+    if (bytes && z.w_shards[i] != dst) {
       hipError_t e = hipMemcpyAsync(dst, z.w_shards[i], bytes, hipMemcpyDeviceToDevice, s);
       if (e != hipSuccess) return hip_fail(e, "gathering the weight shards");
     }
@@ -1048,6 +1049,25 @@ lc_status check_run(lc_stage *stage, const lc_param_bufs *params, const lc_order
   return LC_OK;
 }
 
+// The lc_run_order* calls start from an empty stash (check_run); if an entry
+// fails after others were enqueued, the stash returns to that empty state so
+// the stage stays usable (the outputs of the failed run are undefined).
+lc_status run_or_reset(lc_stage *st, const lc_param_bufs *pb, const lc_order &order,
+                       const lc_microbatch_desc *mbs, hipStream_t s_main, hipStream_t s_aux,
+                       const lc_zero_bufs *z = nullptr) {
+  const lc_status r = run_entries(st, pb, order, mbs, s_main, s_aux, z);
+  if (r != LC_OK) {
+    std::fill(st->owner.begin(), st->owner.end(), -1);
+    std::fill(st->wowner.begin(), st->wowner.end(), -1);
+  }
+  return r;
+}
+
+bool ranges_overlap(const void *a, size_t a_bytes, const void *b, size_t b_bytes) {
+  const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
+  return a_bytes && b_bytes && x < y + b_bytes && y < x + a_bytes;
+}
+
 }  // namespace
 }  // namespace lc
 
@@ -1057,7 +1077,7 @@ lc_status lc_run_order(lc_stage *stage, const lc_param_bufs *params, const lc_or
                        const lc_microbatch_desc *mbs, void *stream) {
   LC_TRY(check_run(stage, params, order, mbs));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return run_entries(stage, params, *order, mbs, s, s);
+  return run_or_reset(stage, params, *order, mbs, s, s);
 }
 
 lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const lc_zero_bufs *zero,
@@ -1073,6 +1093,8 @@ lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const 
   if (z.shard_offset % 4 || z.shard_offset > n || z.shard_len > n - z.shard_offset)
     return fail(LC_ERR_INVALID_ARG, "gradient shard [%zu, +%zu) is not a 4-aligned slice of %zu",
                 z.shard_offset, z.shard_len, n);
+  if (ranges_overlap(z.grad_shard, z.shard_len * 4, z.grad_full, n * 4))
+    return fail(LC_ERR_INVALID_ARG, "the gradient shard overlaps the temporary full gradient");
   lc_param_bufs pb = *params;
   pb.grad = z.grad_full;
   if (z.level == 3) {
@@ -1080,10 +1102,21 @@ lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const 
       return fail(LC_ERR_INVALID_ARG, "ZeRO-3 needs 1..1024 weight shards");
     if (!z.w_full || !aligned16(z.w_full))
       return fail(LC_ERR_INVALID_ARG, "ZeRO-3 temporary weights must be non-null and 16-byte aligned");
+    const size_t esz = stage->plan.elem;
     size_t tot = 0;
     for (int i = 0; i < z.n_w_shards; ++i) {
       if (!z.w_shards[i] && z.w_shard_lens[i])
         return fail(LC_ERR_INVALID_ARG, "weight shard %d is null", i);
+      if (z.w_shard_lens[i] > n - std::min(tot, n))
+        return fail(LC_ERR_INVALID_ARG, "weight shards hold more than the bucket's %zu elements", n);
+      // a shard may already sit at its own place in the temporary buffer (an
+      // in-place gather: its copy is skipped); any other overlap would let
+      // one shard's copy overwrite another before it is read
+      const char *own = static_cast<const char *>(z.w_full) + tot * esz;
+      if (z.w_shards[i] != own &&
+          ranges_overlap(z.w_shards[i], z.w_shard_lens[i] * esz, z.w_full, n * esz))
+        return fail(LC_ERR_INVALID_ARG, "weight shard %d overlaps the temporary full weights "
+                    "away from its own place", i);
       tot += z.w_shard_lens[i];
     }
     if (tot != n)
@@ -1092,15 +1125,15 @@ lc_status lc_run_order_zero(lc_stage *stage, const lc_param_bufs *params, const 
   }
   LC_TRY(check_run(stage, &pb, order, mbs));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return run_entries(stage, params, *order, mbs, s, s, zero);
+  return run_or_reset(stage, params, *order, mbs, s, s, zero);
 }
 
 lc_status lc_run_order_overlap(lc_stage *stage, const lc_param_bufs *params,
                                const lc_order *order, const lc_microbatch_desc *mbs,
                                void *stream, void *aux_stream) {
   LC_TRY(check_run(stage, params, order, mbs));
-  return run_entries(stage, params, *order, mbs, static_cast<hipStream_t>(stream),
-                     static_cast<hipStream_t>(aux_stream));
+  return run_or_reset(stage, params, *order, mbs, static_cast<hipStream_t>(stream),
+                      static_cast<hipStream_t>(aux_stream));
 }
 
 }  // extern "C"

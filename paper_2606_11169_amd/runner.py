@@ -133,8 +133,9 @@ class StageRunner:
                            self.stream)
 
     def zero_grad(self):
-        with torch.cuda.stream(self.stream):
-            self.grad.zero_()
+        """G = +0 before the first backward of a step (the library's fill
+        kernel, enqueued on the stage's stream)."""
+        lc.lc_zero_fill_f32(self.grad, self.n_params, self.stream)
 
     def close(self):
         self.stage.close()

@@ -413,6 +413,23 @@ def test_attention_longer_sequence():
     attn_case(1, 512, 1, 128, lc.LC_FP16, 12, True)
 
 
+@pytest.mark.parametrize("dt", [lc.LC_FP16, lc.LC_BF16], ids=["fp16", "bf16"])
+@pytest.mark.parametrize("rope", [False, True])
+def test_attention_half_full_last_block(rope, dt):
+    """S = 384: workgroups own 256 queries or keys, so the last block is half
+    full after a full one (partial-block masking in the forward, dK/dV and
+    dQ, and the heavy-first block order over unequal blocks)."""
+    attn_case(2, 384, 2, 128, dt, 15, rope)
+
+
+@pytest.mark.parametrize("dt", [lc.LC_FP16, lc.LC_BF16], ids=["fp16", "bf16"])
+@pytest.mark.parametrize("S", [2048, 4096])
+def test_attention_full_length(S, dt):
+    """The benchmark stages' sequence lengths, every position compared: the
+    long off-diagonal key loops of the forward and both backward kernels."""
+    attn_case(1, S, 2, 128, dt, 16 + S, True)
+
+
 @pytest.mark.parametrize("hd", [32, 8])
 def test_attention_fp32(hd):
     attn_case(2, 64, 4, hd, lc.LC_FP32, 13, True)
@@ -495,6 +512,11 @@ def gqa_case(B, S, H, Hkv, hd, dt, seed, rope):
 @pytest.mark.parametrize("H,Hkv", [(4, 1), (4, 2), (2, 2)])
 def test_gqa_attention_matrix_cores(H, Hkv, dt):
     gqa_case(2, 256, H, Hkv, 128, dt, 21, True)
+
+
+@pytest.mark.parametrize("rope", [False, True])
+def test_gqa_attention_half_full_last_block(rope):
+    gqa_case(1, 384, 4, 2, 128, lc.LC_FP16, 24, rope)
 
 
 @pytest.mark.parametrize("H,Hkv", [(4, 2), (6, 3)])
@@ -612,3 +634,130 @@ def test_adam_full_size_shard_sampled_bit_exact():
 
 def host32(t):
     return t.detach().float().cpu().numpy().astype(np.float32)
+
+
+# ---------------------------------------------------------------- 64-bit coverage
+
+N64 = (1 << 31) + 17   # element indices and byte offsets past 2^31 and 2^32
+PAD = 64               # canary words after each buffer
+
+
+def _index_field(n, shift, bits, dtype, chunk=1 << 28):
+    """t[i] = (i >> shift) & (2^bits - 1) as `dtype` (exact), built in chunks."""
+    out = torch.empty(n + PAD, dtype=dtype, device=DEV)
+    for a in range(0, n, chunk):
+        b = min(n, a + chunk)
+        i = torch.arange(a, b, dtype=torch.int64, device=DEV)
+        out[a:b] = ((i >> shift) & ((1 << bits) - 1)).to(dtype)
+    return out
+
+
+def _all_equal_field(t, n, shift, bits, chunk=1 << 28):
+    for a in range(0, n, chunk):
+        b = min(n, a + chunk)
+        i = torch.arange(a, b, dtype=torch.int64, device=DEV)
+        want = ((i >> shift) & ((1 << bits) - 1)).to(torch.float32)
+        if not torch.equal(t[a:b], want):
+            bad = torch.nonzero(t[a:b] != want)[0].item() + a
+            return bad
+    return -1
+
+
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
+def test_accumulate_coverage_past_2_pow_31(gdt):
+    """n = 2^31 + 17: the bucket zeroed by the fill kernel, then one
+    accumulate of g[i] = a bit field of i, for fields that together name
+    every index (fp32: 20 + 12 bits; bf16, exact up to 256: four bytes).
+    Every element must equal its own index's field (each updated exactly
+    once, from its own g) and the canary words after G stay untouched."""
+    n = N64
+    fields = [(0, 20), (20, 12)] if gdt == "f32" else [(0, 8), (8, 8), (16, 8), (24, 8)]
+    tdt = torch.float32 if gdt == "f32" else torch.bfloat16
+    G = torch.full((n + PAD,), 7.0, dtype=torch.float32, device=DEV)
+    for shift, bits in fields:
+        banner(f"accumulate n=2^31+17 g={gdt} field {shift}:{bits}")
+        g = _index_field(n, shift, bits, tdt)
+        g[n:] = 3.0
+        lc.lc_zero_fill_f32(G, n)
+        lc.chunk_accumulate_grad(G, g, lc.LC_BF16 if gdt == "bf16" else lc.LC_FP32, n)
+        torch.cuda.synchronize()
+        bad = _all_equal_field(G, n, shift, bits)
+        assert bad < 0, f"element {bad} holds {G[bad].item()}"
+        assert torch.all(G[n:] == 7.0)
+        del g
+    del G
+    torch.cuda.empty_cache()
+
+
+def test_adam_coverage_past_2_pow_31():
+    """n = 2^31 + 17, bf16 gradient and bf16 cast. (1) Coverage: g = m = v = 0
+    and weight decay 0.1 make the step p' = fl(p * c_wd) exactly (m' = v' = 0,
+    the update term 0), so with p[i] a bit field of i every element of p and
+    of the cast must hold its own index's value; two fields name every index.
+    (2) Random p, m, v, g: elements at the head, the tail and around 2^31,
+    plus a random sample, bit for bit against the oracle's AdamW. Canary
+    words after every buffer stay untouched."""
+    n = N64
+    lr, b1, b2, eps, wd = 3e-4, 0.9, 0.95, 1e-8, 0.1
+    c_wd = torch.tensor(np.float32(1.0 - lr * wd), device=DEV)
+    m = torch.zeros(n + PAD, dtype=torch.float32, device=DEV)
+    v = torch.zeros(n + PAD, dtype=torch.float32, device=DEV)
+    g = torch.zeros(n + PAD, dtype=torch.bfloat16, device=DEV)
+    out = torch.full((n + PAD,), 5.0, dtype=torch.bfloat16, device=DEV)
+    for shift, bits in ((0, 20), (20, 12)):
+        banner(f"adam n=2^31+17 coverage field {shift}:{bits}")
+        p = _index_field(n, shift, bits, torch.float32)
+        p[n:] = 9.0
+        m.zero_(), v.zero_(), g.zero_()
+        lc.shard_adam_step(p, m, v, g, lc.LC_BF16, out, n, lr, b1, b2, eps, wd, 1)
+        torch.cuda.synchronize()
+        for a in range(0, n, 1 << 28):
+            b = min(n, a + (1 << 28))
+            i = torch.arange(a, b, dtype=torch.int64, device=DEV)
+            want = ((i >> shift) & ((1 << bits) - 1)).to(torch.float32) * c_wd
+            assert torch.equal(p[a:b], want), (shift, a)
+            assert torch.equal(out[a:b], want.to(torch.bfloat16)), (shift, a)
+        assert torch.all(m[:n] == 0) and torch.all(v[:n] == 0)
+        for t, c in ((p, 9.0), (m, 0.0), (v, 0.0), (out, 5.0)):
+            assert torch.all(t[n:] == c)
+        del p
+    banner("adam n=2^31+17 sampled bit-exact")
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(12)
+    p = torch.randn(n + PAD, generator=gen, device=DEV).mul_(0.02)
+    m.normal_(0.0, 1e-3, generator=gen)
+    v.normal_(0.0, 1e-3, generator=gen).square_()
+    g.copy_(torch.randn(n + PAD, generator=gen, device=DEV).mul_(1e-3).to(torch.bfloat16))
+    canary = [t[n:].clone() for t in (p, m, v, g, out)]
+    # contiguous windows inside [0, n) read by plain slicing: the head, the
+    # tail (which crosses 2^31: n - 64 = 2^31 - 47), just below 2^31, and
+    # random places
+    rng = np.random.default_rng(32)
+    W = 64
+    starts = sorted({0, n - W, (1 << 31) - 2 * W} |
+                    {int(a) for a in rng.integers(0, n - W + 1, 400)})
+    assert all(0 <= a and a + W <= n for a in starts)
+
+    def windows(t):
+        return np.concatenate([t[a:a + W].float().cpu().numpy() for a in starts])
+
+    p0, m0, v0, g0 = (windows(t) for t in (p, m, v, g))
+    for name, a in (("p", p0), ("m", m0), ("v", v0), ("g", g0)):
+        assert np.all(np.isfinite(a)), f"non-finite {name} input at {np.nonzero(~np.isfinite(a))[0][:8]}"
+    lc.shard_adam_step(p, m, v, g, lc.LC_BF16, out, n, lr, b1, b2, eps, wd, 7)
+    torch.cuda.synchronize()
+    pr, mr, vr = OP.adamw(p0, m0, v0, g0, lr, b1, b2, eps, wd, 7)
+    pos = np.concatenate([np.arange(a, a + W) for a in starts])
+    bad = {}
+    for got, ref, name in ((p, pr, "p"), (m, mr, "m"), (v, vr, "v")):
+        diff = windows(got).astype(np.float32).view(np.uint32) != ref.view(np.uint32)
+        bad[name] = (int(diff[pos < (1 << 31)].sum()), int(diff[pos >= (1 << 31)].sum()))
+    ob = np.concatenate([out[a:a + W].cpu().view(torch.int16).numpy().view(np.uint16)
+                         for a in starts])
+    bad["out"] = int((ob != OP.bf16_rne_bits(pr)).sum())
+    print(f"mismatches (below 2^31, from 2^31) over {pos.size} elements: {bad}", flush=True)
+    assert all(b == (0, 0) for k, b in bad.items() if k != "out") and bad["out"] == 0, bad
+    for t, c in zip((p, m, v, g, out), canary):
+        assert torch.equal(t[n:], c)
+    del p, m, v, g, out
+    torch.cuda.empty_cache()

@@ -24,7 +24,8 @@ import synth
 from oracle import stage as OS
 from paper_2606_11169_amd import libchunk as lc
 from paper_2606_11169_amd.runner import StageRunner, require_gpu
-from tests.gpu_util import DEV, banner, bf16, f32, host, rel_err
+from tests.gpu_util import (DEV, banner, bf16, check_routing_near_ties, f32, gpu_routes, host,
+                            oracle_order_with_routes, rel_err)
 
 pytestmark = pytest.mark.gpu
 
@@ -382,8 +383,32 @@ def test_moe_overlapped_pair_on_two_streams_is_bit_identical():
     assert torch.equal(a.grad, b.grad)
     for mb in range(M):
         assert torch.equal(a.Y[mb], b.Y[mb]) and torch.equal(a.dX[mb], b.dX[mb])
+    # and against the oracle running the same nested Order, given the GPU's
+    # routing (a forward per microbatch on a fresh stage reads it back)
+    oracle_order = [(0, "F"), [(1, "F"), (0, "B")], (1, "B")]
+    check_order_against_oracle(cfg, flat, Xs, dYs, oracle_order, b)
     for r in runs:
         r.close()
+
+
+def check_order_against_oracle(cfg, flat, Xs, dYs, order, run, tol=2e-2):
+    """Y, dX and every gradient tensor of a GPU run of `order` against the
+    oracle executing the same Order (its nested pairs in sequence; Bw adds
+    the gradient Bi computed), with the GPU's routing as the override."""
+    routes = gpu_routes(cfg, flat, Xs, dYs)
+    Ys, dXs, G = oracle_order_with_routes(cfg, flat, Xs, dYs, order, routes)
+    M = len(Xs)
+    errs = {}
+    got = host(run.grad)
+    for name, off, shape in synth.layout(cfg):
+        sz = int(np.prod(shape))
+        errs[name] = rel_err(got[off:off + sz], G[off:off + sz])
+    for mb in range(M):
+        errs[f"Y{mb}"] = rel_err(host(run.Y[mb]), Ys[mb])
+        errs[f"dX{mb}"] = rel_err(host(run.dX[mb]), dXs[mb])
+    top = sorted(errs.items(), key=lambda kv: -kv[1])[:4]
+    print("vs oracle, worst: " + ", ".join(f"{n}={e:.2e}" for n, e in top), flush=True)
+    assert max(errs.values()) <= tol, max(errs, key=errs.get)
 
 
 @pytest.mark.parametrize("w_delay", [0, 1, 2])
@@ -431,7 +456,7 @@ def test_moe_split_backward_is_bit_identical(w_delay):
     else:
         pytest.fail(f"no adjacent (Bi, Bw) pair in {split}")
     gen = lc.lc_order_1f1b_split_overlap(M, P, s, w_delay)  # the generator's nesting
-    for order in (nested, gen):
+    for k, order in enumerate((nested, gen)):
         c = StageRunner(desc_of(cfg), flat, M, max_w_pending=M)
         c.alloc_microbatches(Xs, dYs)
         c.run_order(order, torch.cuda.Stream())
@@ -439,8 +464,62 @@ def test_moe_split_backward_is_bit_identical(w_delay):
         assert torch.equal(a.grad, c.grad)
         for mb in range(M):
             assert torch.equal(a.dX[mb], c.dX[mb])
+        if k == 1:
+            check_order_against_oracle(cfg, flat, Xs, dYs, c_to_oracle(order), c)
         c.close()
     a.close()
+
+
+def c_to_oracle(entries):
+    """C Order entries -> the oracle's Order (a flagged entry and the next
+    one form a nested pair)."""
+    names = {lc.LC_PASS_F: "F", lc.LC_PASS_B: "B", lc.LC_PASS_BI: "Bi", lc.LC_PASS_BW: "Bw"}
+    out, i = [], 0
+    while i < len(entries):
+        mb, p = entries[i]
+        if p & lc.LC_ORDER_WITH_NEXT:
+            mb2, p2 = entries[i + 1]
+            out.append([(mb, names[p & ~lc.LC_ORDER_WITH_NEXT]), (mb2, names[p2])])
+            i += 2
+        else:
+            out.append((mb, names[p]))
+            i += 1
+    return out
+
+
+def test_full_length_moe_layer():
+    """One layer of the mixture-of-experts workload (d 2048, 8 experts x
+    1408, 2 x 2048 tokens) over whole sequences with dY nonzero everywhere:
+    the GPU's routing agrees with the oracle's own top-2 except at near-ties,
+    and Y, dX and every gradient tensor match the oracle run with the GPU's
+    routing at every position."""
+    cfg = synth.scaled(synth.MOE_2K, name="moe_1L_s2048", n_layers=1, num_microbatches=1)
+    banner(f"full-length {cfg.name}")
+    flat = synth.stage_params(cfg, 0)
+    X = synth.activation(cfg, 0, 0, "x")
+    dY = synth.activation(cfg, 0, 0, "dy")
+    r = StageRunner(desc_of(cfg), flat, 1)
+    r.alloc_microbatches([X], [dY])
+    r.forward(0)
+    route = [r.moe_routing(0, l) for l in range(cfg.n_layers)]
+    r.backward(0)
+    torch.cuda.synchronize()
+    Yg, dXg, Gg = host(r.Y[0]), host(r.dX[0]), host(r.grad)
+    r.close()
+    del r
+    torch.cuda.empty_cache()
+    layers = OS.layer_params(cfg, flat)
+    Yr, caches = OS.stage_forward(cfg, layers, X, route_overrides=route)
+    mism = check_routing_near_ties(caches, route)
+    dXr, Gr = OS.stage_backward(cfg, layers, caches, dY)
+    errs = {"Y": rel_err(Yg, Yr), "dX": rel_err(dXg, dXr)}
+    for name, off, shape in synth.layout(cfg):
+        sz = int(np.prod(shape))
+        errs[name] = rel_err(Gg[off:off + sz], Gr[off:off + sz])
+    top = sorted(errs.items(), key=lambda kv: -kv[1])[:8]
+    print("worst tensors: " + ", ".join(f"{n}={e:.2e}" for n, e in top)
+          + f"; {mism} near-tie routing differences", flush=True)
+    assert max(errs.values()) <= 2e-2
 
 
 def test_full_size_moe_stage_on_a_prefix():
@@ -471,6 +550,8 @@ def test_full_size_moe_stage_on_a_prefix():
     override = [rt[rows] for rt in route]
     layers = OS.layer_params(cfg, flat)
     Yp, caches = OS.stage_forward(cfg, layers, X[:, :P], route_overrides=override)
+    mism = check_routing_near_ties(caches, override)
+    print(f"routing differs from the oracle's own top-2 at {mism} near-ties", flush=True)
     dXp, Gp = OS.stage_backward(cfg, layers, caches, dY[:, :P])
     errs = {"Y": rel_err(Yg[:, :P], Yp), "dX": rel_err(dXg[:, :P], dXp)}
     assert np.all(dXg[:, P:] == 0.0)

@@ -28,7 +28,7 @@ from oracle import order as OO
 from oracle import stage as OS
 from paper_2606_11169_amd import libchunk as lc
 from paper_2606_11169_amd.runner import StageRunner, require_gpu
-from tests.gpu_util import banner, host, rel_err
+from tests.gpu_util import banner, gpu_routes, host, oracle_order_with_routes, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -104,9 +104,17 @@ QWEN_FP32 = synth.StageConfig(
     pp_size=2, pp_rank=0)
 
 
+# 384 tokens: a half-full last 256-row block of the attention kernels after a
+# full one (forward, dK/dV and dQ partial-block masking)
+SMALL_BF16_S384 = synth.scaled(SMALL_BF16, name="small_bf16_s384", seq_len=384,
+                               num_microbatches=2, pp_size=2)
+
+
 @pytest.mark.parametrize("cfg,tol", [(synth.TINY_FP32, 1e-4), (SMALL_BF16, 2e-2),
-                                     (QWEN_FP32, 1e-4), (QWEN_BF16, 2e-2)],
-                         ids=["tiny_fp32", "small_bf16", "qwen_fp32", "qwen_bf16"])
+                                     (QWEN_FP32, 1e-4), (QWEN_BF16, 2e-2),
+                                     (SMALL_BF16_S384, 2e-2)],
+                         ids=["tiny_fp32", "small_bf16", "qwen_fp32", "qwen_bf16",
+                              "small_bf16_s384"])
 def test_stage_matches_oracle(cfg, tol):
     banner(f"stage {cfg.name}")
     flat, Xs, dYs = inputs(cfg)
@@ -133,14 +141,28 @@ def test_stage_matches_oracle(cfg, tol):
                                    cfg.adam_eps, cfg.weight_decay, 1)
     assert rel_err(host(r.m), m_ref) <= tol
     assert rel_err(host(r.v), v_ref) <= 2 * tol
-    # at t = 1 the update is ~ -lr*sign(g): an element whose gradient sign
-    # differs between the two sides (|g| within the tolerated error of 0)
-    # moves the other way; compare the elements whose signs agree
-    keep = np.sign(Gg.astype(np.float32)) == np.sign(g_ref)
-    print(f"adam: {int((~keep).sum())} of {keep.size} elements with opposite gradient signs")
-    assert keep.mean() > 0.9
+    # at t = 1 the update is ~ -lr*sign(g), so an element whose gradient is
+    # within the tolerated error of 0 may move either way. Such elements are
+    # the ones with |g_ref| <= tol * max|g_ref| over their tensor: p is
+    # compared on all others, and every sign disagreement must lie among them
+    keep = adam_comparable(cfg, G, tol)
+    flips = np.sign(Gg.astype(np.float32)) != np.sign(g_ref)
+    print(f"adam: {int((~keep).sum())} of {keep.size} elements near zero gradient excluded, "
+          f"{int(flips.sum())} sign disagreements")
+    assert not np.any(flips & keep), "a gradient sign differs where |g_ref| is not near 0"
     assert rel_err(host(r.master)[keep], p_ref[keep]) <= tol
     r.close()
+
+
+def adam_comparable(cfg, G, tol):
+    """Elements whose reference gradient is not within tol * max|G| of its
+    tensor from zero: there the first AdamW step's direction is fixed."""
+    keep = np.ones(G.size, bool)
+    for name, off, shape in synth.layout(cfg):
+        sz = int(np.prod(shape))
+        g = np.abs(G[off:off + sz])
+        keep[off:off + sz] = g > tol * np.max(g)
+    return keep
 
 
 def test_order_invariance_determinism_and_exact_accumulation():
@@ -319,12 +341,23 @@ def test_overlapped_pairs_on_two_streams_are_bit_identical(cfg):
     banner(f"overlapped pairs {cfg.name}")
     flat, Xs, dYs = inputs(cfg, seed=8)
     M, P, s = cfg.num_microbatches, cfg.pp_size, cfg.pp_rank
+    tol = 2e-2 if cfg.bf16 else 1e-4
     ref = gpu_run(cfg, OO.one_f_one_b(M, P, s), flat, Xs, dYs)
     aux = torch.cuda.Stream()
     cases = [(OO.one_f_one_b_overlap(M, P, s), 0), (OO.parse(SPLIT_PAIRS[M]), 2)]
     for order, wp in cases:
         assert OO.validate(order, M, M, max_w_pending=wp or M)[0] == "OK"
         assert any(isinstance(e, list) for e in order)
+        # the oracle runs the same nested Order (its pairs in sequence)
+        r = gpu_run(cfg, order, flat, Xs, dYs, max_w_pending=wp, aux_stream=aux)
+        Ys, dXs, G = OS.run_order(cfg, flat, Xs, dYs, order)
+        errs = per_tensor_errors(cfg, host(r.grad), G)
+        for mb in range(M):
+            errs[f"Y{mb}"] = rel_err(host(r.Y[mb]), Ys[mb])
+            errs[f"dX{mb}"] = rel_err(host(r.dX[mb]), dXs[mb])
+        report(errs)
+        assert max(errs.values()) <= tol, (order, max(errs, key=errs.get))
+        r.close()
         for stream in (aux, None):
             r = gpu_run(cfg, order, flat, Xs, dYs, max_w_pending=wp,
                         aux_stream=stream if stream is not None else torch.cuda.current_stream())
@@ -353,12 +386,22 @@ def test_zero_paths_give_the_accumulated_gradient_slices(cfg):
     banner(f"zero paths {cfg.name}")
     flat, Xs, dYs = inputs(cfg, seed=9)
     M, P, s = cfg.num_microbatches, cfg.pp_size, cfg.pp_rank
+    tol = 2e-2 if cfg.bf16 else 1e-4
     ref = gpu_run(cfg, OO.one_f_one_b(M, P, s), flat, Xs, dYs)
     n = ref.n_params
     bounds = [0, (n // 3) // 4 * 4, (2 * n // 3) // 4 * 4 + 4, n]
     orders = [(OO.one_f_one_b(M, P, s), 0), (OO.one_f_one_b_split(M, P, s, 1), 2)]
+    # the oracle's gradient: the three ranks' shards together must be it (a
+    # mixture-of-experts stage's oracle takes the GPU's routing, as near-ties
+    # may route either way)
+    if cfg.moe:
+        routes = gpu_routes(cfg, flat, Xs, dYs)
+        _, _, G_ref = oracle_order_with_routes(cfg, flat, Xs, dYs, orders[0][0], routes)
+    else:
+        _, _, G_ref = OS.run_order(cfg, flat, Xs, dYs, orders[0][0])
     for level in (2, 3):
         for order, wp in orders:
+            shards = []
             for rank in range(3):
                 off, end = bounds[rank], bounds[rank + 1]
                 r = StageRunner(desc_of(cfg), flat, M, max_w_pending=wp)
@@ -376,22 +419,55 @@ def test_zero_paths_give_the_accumulated_gradient_slices(cfg):
                 assert torch.all(r.grad == 0)  # params->grad is not touched
                 for mb in range(M):
                     assert torch.equal(r.Y[mb], ref.Y[mb]) and torch.equal(r.dX[mb], ref.dX[mb])
+                shards.append(host(shard))
                 r.close()
-    # bad layouts are rejected before anything is enqueued
+            errs = per_tensor_errors(cfg, np.concatenate(shards), G_ref)
+            report(errs, 3)
+            assert max(errs.values()) <= tol, (level, wp, max(errs, key=errs.get))
+    # ZeRO-3 with every weight shard already at its place in w_full (an
+    # in-place gather): the same shard as the plain Order's slice
+    r = StageRunner(desc_of(cfg), flat, M)
+    r.alloc_microbatches(Xs, dYs)
+    w_full = r.w.clone()
+    r.w.fill_(float("nan"))
+    shard = torch.zeros(bounds[2] - bounds[1], dtype=torch.float32, device="cuda")
+    full = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+    r.run_order_zero(to_c(orders[0][0]), 3, shard, bounds[1], full,
+                     [w_full[bounds[i]:bounds[i + 1]] for i in range(3)], w_full)
+    torch.cuda.synchronize()
+    assert torch.equal(shard, ref.grad[bounds[1]:bounds[2]])
+    r.close()
+    # bad layouts are rejected before anything is enqueued, and the stage
+    # still runs an Order afterwards
     r = StageRunner(desc_of(cfg), flat, M)
     r.alloc_microbatches(Xs, dYs)
     shard = torch.zeros(8, dtype=torch.float32, device="cuda")
-    full = torch.zeros(n, dtype=torch.float32, device="cuda")
+    full = torch.zeros(n + 64, dtype=torch.float32, device="cuda")
+    wbuf = torch.empty(n + 64, dtype=r.w.dtype, device="cuda")
     order = to_c(OO.one_f_one_b(M, P, s))
     for bad in (dict(level=2, grad_shard=shard, shard_offset=2),
                 dict(level=2, grad_shard=shard, shard_offset=n - 4),
                 dict(level=4, grad_shard=shard, shard_offset=0),
                 dict(level=3, grad_shard=shard, shard_offset=0,
-                     w_shards=[r.w[:n // 2]], w_full=torch.empty_like(r.w))):
+                     w_shards=[r.w[:n // 2]], w_full=torch.empty_like(r.w)),
+                # the shard is a view into the temporary full gradient
+                dict(level=2, grad_shard=full[16:24], shard_offset=0, msg="overlap"),
+                dict(level=2, grad_shard=full[n:n + 8], shard_offset=0, full=full[4:n + 4],
+                     msg="overlap"),
+                # a weight shard inside w_full, away from its own place
+                dict(level=3, grad_shard=shard, shard_offset=0, w_full=wbuf[:n],
+                     w_shards=[wbuf[8:8 + n // 2], r.w[n // 2:]], msg="overlap"),
+                dict(level=3, grad_shard=shard, shard_offset=0, w_full=wbuf[:n],
+                     w_shards=[r.w[:n // 2], wbuf[n // 2 + 8:n + 8]], msg="overlap")):
         with pytest.raises(lc.LibchunkError) as e:
-            r.run_order_zero(order, bad["level"], bad["grad_shard"], bad["shard_offset"], full,
-                             bad.get("w_shards", ()), bad.get("w_full"))
+            r.run_order_zero(order, bad["level"], bad["grad_shard"], bad["shard_offset"],
+                             bad.get("full", full[:n]), bad.get("w_shards", ()), bad.get("w_full"))
         assert e.value.status == lc.LC_ERR_INVALID_ARG
+        assert bad.get("msg", "") in str(e.value), str(e.value)
+    torch.cuda.synchronize()
+    r.run_order(order)
+    torch.cuda.synchronize()
+    assert torch.equal(r.grad, ref.grad)
     r.close()
     ref.close()
 
@@ -473,6 +549,48 @@ def test_full_size_stage_on_a_prefix(cfg, tol):
     errs = per_tensor_errors(cfg, Gg, Gp)
     report(errs, 12)
     worst = max(errs, key=errs.get)
+    assert errs[worst] <= tol, (worst, errs[worst])
+
+
+FULL_LENGTH = [
+    synth.scaled(synth.STAGE_7B, name="stage7b_1L_s4096", n_layers=1, num_microbatches=1),
+    synth.scaled(synth.QWEN3_STAGE, name="qwen3_1L_s4096", n_layers=1, num_microbatches=1),
+    synth.scaled(synth.LLAMA_2K, name="llama_2L_s2048", n_layers=2, num_microbatches=1),
+]
+
+
+@pytest.mark.parametrize("cfg", FULL_LENGTH, ids=["stage7b_1L", "qwen3_1L", "llama2k_2L"])
+def test_full_length_layers(cfg):
+    """Layers of the benchmark shapes over whole sequences (4096 tokens for
+    the 7B- and Qwen3-shaped layers, 2048 for the Llama-style ones) with dY
+    nonzero everywhere: Y, dX and every gradient tensor against the oracle
+    at every position, so the long key loops of attention, its heavy-first
+    block order and the long-context terms of every weight gradient are all
+    compared. The margin to the 2e-2 tolerance is printed."""
+    tol = 2e-2
+    banner(f"full-length {cfg.name}")
+    flat = synth.stage_params(cfg, 0)
+    X = synth.activation(cfg, 0, 0, "x")
+    dY = synth.activation(cfg, 0, 0, "dy")
+    r = StageRunner(desc_of(cfg), flat, 1)
+    r.alloc_microbatches([X], [dY])
+    r.forward(0)
+    r.backward(0)
+    torch.cuda.synchronize()
+    Yg, dXg, Gg = host(r.Y[0]), host(r.dX[0]), host(r.grad)
+    r.close()
+    del r
+    torch.cuda.empty_cache()
+    banner(f"full-length {cfg.name}: oracle")
+    layers = OS.layer_params(cfg, flat)
+    Yr, caches = OS.stage_forward(cfg, layers, X)
+    dXr, Gr = OS.stage_backward(cfg, layers, caches, dY)
+    errs = per_tensor_errors(cfg, Gg, Gr)
+    errs["Y"] = rel_err(Yg, Yr)
+    errs["dX"] = rel_err(dXg, dXr)
+    report(errs, 12)
+    worst = max(errs, key=errs.get)
+    print(f"margin: worst {worst} {errs[worst]:.2e} = {errs[worst] / tol:.0%} of {tol}", flush=True)
     assert errs[worst] <= tol, (worst, errs[worst])
 
 

@@ -140,6 +140,24 @@ lc_status lc_rmsnorm_forward(const lc_norm_args *args, void *stream);
 lc_status lc_rmsnorm_backward(const lc_norm_args *args, void *stream);
 size_t lc_rmsnorm_scratch_bytes(int64_t T, int64_t d);
 
+/* lc_rmsnorm_backward for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results, bit for bit, but the gain
+ * gradient's partial sums go to a fixed device array of
+ * LC_RMSNORM_NOALLOC_SCRATCH_BYTES inside the library instead of
+ * args->scratch (ignored; may be NULL). The call allocates nothing: on the
+ * first call on a device it looks up that device's copy of the array
+ * (hipGetSymbolAddress, with that device current) and keeps the address.
+ * The caller still passes every input and output. Each partial sum is
+ * written before it is read, so nothing needs clearing between calls. All
+ * calls on one GPU share its array: calls that may overlap on one GPU
+ * (different streams without ordering, or host threads) race and must be
+ * serialised by the caller. Limit: ceil(T / 16) * d <= 4,194,304 partial
+ * sums (for example T <= 16384 at d = 4096), else LC_ERR_WORKSPACE before
+ * anything is enqueued. Without dg_accum no scratch is used. */
+#define LC_RMSNORM_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+lc_status lc_rmsnorm_backward_noalloc(const lc_norm_args *args, void *stream);
+
 /* ------------------------------------------------------------------ attention
  * Causal softmax attention per (batch row b, head h): for query i,
  *   o_i = sum_{j<=i} softmax_j(q_i.k_j / sqrt(hd)) v_j,

@@ -20,6 +20,8 @@
 // every run, no atomics.
 #include "common.hpp"
 
+#include <mutex>
+
 namespace lc {
 namespace {
 
@@ -389,9 +391,73 @@ lc_status rmsnorm_dg_final_launch(const float *partial, float *dg, int64_t T, in
   return dg_final(p, s);
 }
 
+// ---------------------------------------------------------------- no allocation
+// lc_rmsnorm_backward_noalloc keeps the gain gradient's partial sums in this
+// fixed device array instead of a caller's scratch. Each GPU the library runs
+// on holds its own copy (module memory, until the process ends). The array's
+// name is a host-side stand-in: host code uses only the address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) float scratch[LC_RMSNORM_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, looked up on
+// the first call on that device (with it current) and kept.
+lc_status noalloc_scratch(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "rmsnorm (no allocation): hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(LC_ERR_UNSUPPORTED, "rmsnorm (no allocation): device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "rmsnorm (no allocation): hipGetSymbolAddress");
+    if (!p) return fail(LC_ERR_HIP, "rmsnorm (no allocation): null scratch address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LC_OK;
+}
+
+}  // namespace
+
+lc_status rmsnorm_bwd_noalloc_launch(const lc_norm_args &in, hipStream_t s) {
+  lc_norm_args a = in;
+  a.scratch = nullptr;
+  a.scratch_bytes = 0;
+  if (a.dg_accum) {
+    if (a.T <= 0 || a.d <= 0 || a.d > INT32_MAX)
+      return fail(LC_ERR_INVALID_ARG, "rmsnorm: T and d must be positive (d < 2^31)");
+    // ceil(T / 16) * d * 4 bytes of partial sums, compared without overflow
+    const uint64_t blocks = ((uint64_t)a.T + kNormRowsPerBlock - 1) / kNormRowsPerBlock;
+    const uint64_t cap = LC_RMSNORM_NOALLOC_SCRATCH_BYTES / sizeof(float);
+    if (blocks > cap / (uint64_t)a.d)
+      return fail(LC_ERR_WORKSPACE,
+                  "rmsnorm (no allocation): T = %lld, d = %lld need %llu bytes of partial sums, "
+                  "more than the fixed %zu (ceil(T / 16) * d * 4 must fit)",
+                  (long long)a.T, (long long)a.d,
+                  (unsigned long long)(blocks * (uint64_t)a.d * sizeof(float)),
+                  (size_t)LC_RMSNORM_NOALLOC_SCRATCH_BYTES);
+    LC_TRY(noalloc_scratch(&a.scratch));
+    a.scratch_bytes = LC_RMSNORM_NOALLOC_SCRATCH_BYTES;
+  }
+  return rmsnorm_bwd_launch(a, s);
+}
+
 }  // namespace lc
 
 extern "C" {
+
+lc_status lc_rmsnorm_backward_noalloc(const lc_norm_args *args, void *stream) {
+  if (!args) return lc::fail(LC_ERR_INVALID_ARG, "rmsnorm: null args");
+  return lc::rmsnorm_bwd_noalloc_launch(*args, static_cast<hipStream_t>(stream));
+}
 
 lc_status lc_rmsnorm_forward(const lc_norm_args *args, void *stream) {
   if (!args) return lc::fail(LC_ERR_INVALID_ARG, "rmsnorm: null args");

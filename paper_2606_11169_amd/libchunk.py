@@ -199,6 +199,7 @@ _SIGS = {
     "lc_rmsnorm_forward": (C.c_int, [C.POINTER(lc_norm_args), C.c_void_p]),
     "lc_rmsnorm_backward": (C.c_int, [C.POINTER(lc_norm_args), C.c_void_p]),
     "lc_rmsnorm_scratch_bytes": (C.c_size_t, [C.c_int64, C.c_int64]),
+    "lc_rmsnorm_backward_noalloc": (C.c_int, [C.POINTER(lc_norm_args), C.c_void_p]),
     "lc_attention_forward": (C.c_int, [C.POINTER(lc_attn_args), C.c_void_p]),
     "lc_attention_backward": (C.c_int, [C.POINTER(lc_attn_args), C.c_void_p]),
     "lc_attention_scratch_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32]),
@@ -551,6 +552,17 @@ def lc_rmsnorm_backward(T, d, dn, x, rstd, g, dres, dx, dg_accum, scratch, scrat
               dn_dtype=dn_dtype, x_dtype=x_dtype, w_dtype=w_dtype, dres_dtype=dres_dtype,
               out_dtype=out_dtype)
     return _check(lib().lc_rmsnorm_backward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
+
+
+def lc_rmsnorm_backward_noalloc(T, d, dn, x, rstd, g, dres, dx, dg_accum, dn_dtype, x_dtype,
+                                w_dtype, dres_dtype, out_dtype, dx_copy=None, stream=None):
+    """lc_rmsnorm_backward with the library's fixed scratch array (no scratch
+    argument, nothing allocated)."""
+    a = _fill(lc_norm_args(), T=T, d=d, dn=dn, x=x, rstd=rstd, g=g, dres=dres, dx=dx,
+              dx_copy=dx_copy, dg_accum=dg_accum, dn_dtype=dn_dtype, x_dtype=x_dtype,
+              w_dtype=w_dtype, dres_dtype=dres_dtype, out_dtype=out_dtype)
+    return _check(lib().lc_rmsnorm_backward_noalloc(C.byref(a),
+                                                    C.c_void_p(stream_ptr(stream) or None)))
 
 
 def lc_attention_forward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, ld_o, lse, stream=None,

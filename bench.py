@@ -165,8 +165,7 @@ def time_zero(torch, lc, cfg, stream, steps, warmup, level, ranks=8):
     log(f"[bench] {cfg.name}: ZeRO-{level}, rank 0 of {ranks}: shard of {end - off} elements")
 
     def step(t):
-        with torch.cuda.stream(stream):
-            shard.zero_()
+        lc.lc_zero_fill_f32(shard, shard.numel(), stream)
         r.run_order_zero(order, level, shard, off, full, w_shards, w_full)
         lc.shard_adam_step(master, m, v, shard, lc.LC_FP32, out, end - off, cfg.lr, cfg.beta1,
                            cfg.beta2, cfg.adam_eps, cfg.weight_decay, t, stream)
@@ -270,8 +269,10 @@ def csrc_hash() -> str:
 
 def measured_mfma_busy():
     """Matrix-core busy fraction of the 7B-shaped step from the committed PMC
-    summary (SQ_VALU_MFMA_BUSY_CYCLES over the SIMD-cycles its kernels had),
-    if it was taken on the current sources (else None)."""
+    summary (SQ_VALU_MFMA_BUSY_CYCLES over the SIMD-cycles its kernels had).
+    Not measured by this run: reported with its source file and the source
+    digest it was taken on, and only while that digest matches the current
+    sources (else None)."""
     try:
         lines = open(MFMA_MD).read().splitlines()
     except OSError:
@@ -283,7 +284,10 @@ def measured_mfma_busy():
                 vals[key[:-1]] = ln.split(":", 1)[1].strip().split()[0]
     if vals.get("csrc_sha256_16") != csrc_hash() or "mfma_busy_step" not in vals:
         return None
-    return float(vals["mfma_busy_step"])
+    return {"value": float(vals["mfma_busy_step"]),
+            "source": os.path.relpath(MFMA_MD, ROOT), "csrc_sha256_16": vals["csrc_sha256_16"],
+            "measured": "a separate rocprofv3 --pmc run of one 7B-shaped step (see the source "
+                        "file for its command), not this run"}
 
 
 def calibration_copy(torch, lc, stream):
@@ -294,6 +298,29 @@ def calibration_copy(torch, lc, stream):
         lc.chunk_accumulate_grad(a, g, lc.LC_FP32, CAL_N, stream=stream)
     torch.cuda.synchronize()
     del a, g
+
+
+ADAM_MD = os.path.join(ROOT, "profiles", "adam_shard_traffic.md")
+OPTIM_SRC = os.path.join(ROOT, "paper_2606_11169_amd", "csrc", "k_optim.hip")
+
+
+def adam_traffic():
+    """HBM bytes per AdamW launch from the committed PMC summary, if it was
+    taken on the current k_optim.hip (else None)."""
+    import hashlib
+    try:
+        lines = open(ADAM_MD).read().splitlines()
+        h = hashlib.sha256(open(OPTIM_SRC, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    vals = {}
+    for ln in lines:
+        for key in ("traffic_bytes_per_launch:", "k_optim_sha256_16:"):
+            if ln.startswith(key):
+                vals[key[:-1]] = ln.split(":", 1)[1].strip().split()[0]
+    if vals.get("k_optim_sha256_16") != h or "traffic_bytes_per_launch" not in vals:
+        return None
+    return float(vals["traffic_bytes_per_launch"])
 
 
 def adam_shard(torch, lc, shard, stream, reps=20):
@@ -321,16 +348,30 @@ def adam_shard(torch, lc, shard, stream, reps=20):
     return {"workload": shard.name, "n": n, "bytes_per_elem": 28, "launches": reps,
             "ms": round(med, 3), "ms_min": round(per[0], 3),
             "ms_mean": round(sum(per) / len(per), 3), "value": round(gbs, 1), "unit": "GB/s",
-            "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "timing": "median of per-launch HIP events"}
+            "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "timing": "median of per-launch HIP events",
+            "traffic": adam_traffic(), "algorithmic_bytes": 28 * n}
 
 
-def cpu_baseline(cfg, tokens: int):
+def cpu_model() -> str:
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, tokens: int, adam_sample: int = 20_000_000):
     """The oracle, as it stands, on one layer of the workload truncated to
-    `tokens` positions of one sequence: Chunk F then Chunk B."""
+    `tokens` positions of one sequence (Chunk F then Chunk B), and its AdamW
+    on a slice of the bucket; the full step's oracle time is extrapolated
+    from them (every layer and microbatch does the same work)."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     import synth
+    from oracle import optim as OP
     from oracle import stage as OS
     sample = synth.scaled(cfg, n_layers=1, seq_len=tokens, micro_batch=1, bf16=False)
     flat = synth.stage_params(sample, 0)
@@ -341,13 +382,99 @@ def cpu_baseline(cfg, tokens: int):
     Y, caches = OS.stage_forward(sample, layers, X)
     dX, G = OS.stage_backward(sample, layers, caches, dY)
     dt = time.perf_counter() - t0
+    del Y, caches, dX, G, layers, flat
+    p, m, v, g = synth.adam_inputs(adam_sample, seed=0)
+    t0 = time.perf_counter()
+    OP.adamw(p, m, v, g, cfg.lr, cfg.beta1, cfg.beta2, cfg.adam_eps, cfg.weight_decay, 1)
+    dta = time.perf_counter() - t0
+    n_params = synth.param_count(cfg)
     flops = stage_flops_per_mb(sample)
+    ratio = stage_flops_per_mb(cfg) * cfg.num_microbatches / flops
+    step_s = dt * ratio + dta * n_params / adam_sample
     threads = max([i.get("num_threads", 1) for i in threadpool_info()
                    if i.get("internal_api") == "openblas"] or [1])
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = os.cpu_count()
     return {"value": round(flops / dt / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle", "seconds": round(dt, 2),
             "sample": f"1 of {cfg.n_layers} layers, first {tokens} of {cfg.seq_len} tokens of one "
-                      f"microbatch, Chunk F + Chunk B in float64 numpy ({flops / 1e12:.3f} TFLOP)"}
+                      f"microbatch, Chunk F + Chunk B in float64 numpy ({flops / 1e12:.3f} TFLOP; "
+                      f"matrix products on {threads} BLAS threads, the rest on one), and AdamW "
+                      f"on {adam_sample} elements in {dta:.2f} s",
+            "nproc": os.cpu_count(), "affinity_cpus": affinity, "cpu_model": cpu_model(),
+            "extrapolated_step_seconds": round(step_s, 1),
+            "extrapolation": f"sample time x {ratio:g} (the step's algorithmic FLOP over the "
+                             f"sample's) + AdamW time scaled to the {n_params}-element bucket "
+                             "(not measured)"}
+
+
+def streaming_kernels(torch, lc, cfg, stream, reps=20):
+    """Achieved HBM GB/s of the stage's bandwidth-bound kernels, each timed
+    alone (median of per-launch HIP events) at the 7B-shaped stage's own shapes
+    and element types: RMSNorm forward (fp32 residual rows -> bf16 normalised
+    rows + fp32 rstd) and backward (fp32 dn, x, dres -> fp32 dx + its bf16
+    copy, gain partial sums) over T = 4096 rows of d = 4096, and gradient
+    accumulation of an fp32 gradient into the stage's 809.5 M-element fp32
+    bucket. Bytes are the algorithmic minimum (each operand read or written
+    once)."""
+    T, d = cfg.tokens, cfg.d_model
+    F32, BF16 = lc.LC_FP32, lc.LC_BF16
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    x = torch.randn((T, d), generator=g, device="cuda")
+    dn = torch.randn((T, d), generator=g, device="cuda")
+    dres = torch.randn((T, d), generator=g, device="cuda")
+    gain = torch.ones(d, dtype=torch.bfloat16, device="cuda")
+    n = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    rstd = torch.empty(T, dtype=torch.float32, device="cuda")
+    dx = torch.empty((T, d), dtype=torch.float32, device="cuda")
+    cp = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    dg = torch.zeros(d, dtype=torch.float32, device="cuda")
+    sb = lc.lc_rmsnorm_scratch_bytes(T, d)
+    scratch = torch.empty(sb, dtype=torch.uint8, device="cuda")
+
+    def fwd():
+        lc.lc_rmsnorm_forward(T, d, x, gain, cfg.rms_eps, n, rstd, F32, BF16, BF16, stream=stream)
+
+    def bwd():
+        lc.lc_rmsnorm_backward(T, d, dn, x, rstd, gain, dres, dx, dg, scratch, sb, F32, F32, BF16,
+                               F32, F32, dx_copy=cp, stream=stream)
+    out = {}
+    for name, fn, nbytes in (("rmsnorm_forward", fwd, T * d * (4 + 2) + T * 4),
+                             ("rmsnorm_backward", bwd, T * d * (4 * 4 + 2) + T * 4)):
+        fn()
+        torch.cuda.synchronize()
+        per = sorted(time_launches(torch, stream, [fn] * reps))
+        med = per[len(per) // 2]
+        out[name] = {"value": round(nbytes / (med * 1e-3) / 1e9, 1), "unit": "GB/s",
+                     "us": round(med * 1e3, 1), "bytes": nbytes,
+                     "frac_hbm": round(nbytes / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del x, dn, dres, n, dx, cp, scratch
+    nacc = synth_param_count(cfg)
+    acc = torch.zeros(nacc, dtype=torch.float32, device="cuda")
+    gr = torch.ones(nacc, dtype=torch.float32, device="cuda")
+
+    def accum():
+        lc.chunk_accumulate_grad(acc, gr, F32, nacc, stream=stream)
+    accum()
+    torch.cuda.synchronize()
+    per = sorted(time_launches(torch, stream, [accum] * reps))
+    med = per[len(per) // 2]
+    out["accumulate"] = {"value": round(12.0 * nacc / (med * 1e-3) / 1e9, 1), "unit": "GB/s",
+                         "us": round(med * 1e3, 1), "bytes": 12 * nacc, "n": nacc,
+                         "frac_hbm": round(12.0 * nacc / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del acc, gr
+    torch.cuda.empty_cache()
+    out["timing"] = ("each kernel alone at the 7B-shaped stage's shapes and types, median of "
+                     f"{reps} launches timed with HIP events on the launch stream")
+    return out
+
+
+def synth_param_count(cfg):
+    import synth
+    return synth.param_count(cfg)
 
 
 MOE_W_DELAY = 1
@@ -392,6 +519,10 @@ def main():
     ap.add_argument("--overlap-only", action="store_true",
                     help="only the 7B-shaped and MoE stages with overlapped (F, B) pairs on "
                          "two streams")
+    ap.add_argument("--adam-only", action="store_true",
+                    help="only the calibration copy and the AdamW shard (PMC runs)")
+    ap.add_argument("--no-streaming", action="store_true",
+                    help="skip the RMSNorm / accumulate bandwidth lines")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -460,6 +591,11 @@ def main():
                            "ms_per_step": round(oms, 2), "outputs_finite": ofin}
         print(json.dumps({"overlap_stage": res}))
         return
+    if args.adam_only:
+        calibration_copy(torch, lc, stream)
+        print(json.dumps({"adam_shard": adam_shard(torch, lc, synth.ADAM_1P6B, stream,
+                                                   reps=args.steps)}), flush=True)
+        return
     if args.roofline_only:
         calibration_copy(torch, lc, stream)
         time_stage(torch, lc, cfg, stream, args.steps, args.warmup, "7b", time_wgrad=True)
@@ -491,6 +627,9 @@ def main():
     adam = None if args.no_adam_shard else adam_shard(torch, lc, synth.ADAM_1P6B, stream)
     if adam:
         log(f"[bench] adam shard {adam}")
+    streaming = None if args.no_streaming else streaming_kernels(torch, lc, cfg, stream)
+    if streaming:
+        log(f"[bench] streaming kernels {streaming}")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, args.cpu_tokens)
@@ -515,6 +654,7 @@ def main():
         "step_ms": STEP_STATS.get("7b"),
         "roofline": roof,
         "adam_shard": adam,
+        "streaming": streaming,
         "moe_stage": moe,
         "cpu_baseline": cpu,
         "outputs_finite": finite,

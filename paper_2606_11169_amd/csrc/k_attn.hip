@@ -658,34 +658,56 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
     const int q0 = qbi * KB + 32 * hq;  // this wave's 32 queries
     if (q0 + 31 >= k0w) {
       f32x16_v s = zero16(), dp = zero16();
+      // fragment rows of this wave's 32 queries (frag_rows, written out): the
+      // lane's row start and its swizzle term, made opaque each block so that
+      // the eight per-k-step offsets are recomputed (two instructions each)
+      // instead of being held in registers across the loop
+      int rsw = ((32 * hq + l32) << 8) | ((hf ^ swz(l32)) << 4);
+      asm volatile("" : "+v"(rsw));
+      const lds_t *qrow = cur + (rsw & ~0xFF);
+      const int x4 = rsw & 0xF0;
 #pragma unroll
       for (int es = 0; es < 8; ++es) {
-        s = mfma(frag_rows<QV>(cur, 32 * hq, es, lane), kf[es], s);
-        dp = mfma(frag_rows<bf16x8_v>(cur + TILE, 32 * hq, es, lane), vf[es], dp);
-        // at most two k-steps of fragments in flight (registers are the limit)
-        if (es & 1) __builtin_amdgcn_sched_barrier(0);
+        const int off = (32 * es) ^ x4;  // ((2 es + hf) ^ swz) << 4
+        typedef __attribute__((address_space(3))) QV lds_q;
+        typedef __attribute__((address_space(3))) bf16x8_v lds_b;
+        s = mfma(*reinterpret_cast<const lds_q *>(qrow + off), kf[es], s);
+        dp = mfma(*reinterpret_cast<const lds_b *>(qrow + TILE + off), vf[es], dp);
+        // one k-step of fragments in flight: registers are the limit, and a
+        // spilled value reloaded here would wait for the stage's prefetch too
+        // (one counter covers both kinds of load)
+        __builtin_amdgcn_sched_barrier(0);
       }
       if (q0 < k0w + 31) {  // diagonal block (wave-uniform): P = 0 for queries before the key
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           if (q0 + out_row(r, hf) < myk) s[r] = -INFINITY;
       }
+      // four rows at a time (their lse and D are 4 consecutive floats each),
+      // so that only 8 of them are held at once
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qi = out_row(r, hf);
-        const float pv = ex2(__builtin_fmaf(s[r], sc, -sL[qi] * LOG2E));
-        s[r] = pv;
-        dp[r] = pv * (dp[r] - sL[64 + qi]);
+      for (int r4 = 0; r4 < 16; r4 += 4) {
+#pragma unroll
+        for (int r = r4; r < r4 + 4; ++r) {
+          const int qi = out_row(r, hf);
+          const float pv = ex2(__builtin_fmaf(s[r], sc, -sL[qi] * LOG2E));
+          s[r] = pv;
+          dp[r] = pv * (dp[r] - sL[64 + qi]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
+      // P and dS rounded to bf16 before the gradient products, so that the
+      // fp32 score registers are free while those run
+      const bf16x8_v pf[2] = {pack8<__bf16>(s, 0), pack8<__bf16>(s, 8)};
+      const bf16x8_v sf[2] = {pack8<__bf16>(dp, 0), pack8<__bf16>(dp, 8)};
+      __builtin_amdgcn_sched_barrier(0);
       const lds_t *qt = cur + 2 * TILE, *dot = cur + 3 * TILE;
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const bf16x8_v pf = pack8<__bf16>(s, 8 * t);
-        const bf16x8_v sf = pack8<__bf16>(dp, 8 * t);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          dv[i] = mfma(frag_t<bf16x8_v>(dot, i * 32, hq, t, lane), pf, dv[i]);
-          dk[i] = mfma(frag_t<bf16x8_v>(qt, i * 32, hq, t, lane), sf, dk[i]);
+          dv[i] = mfma(frag_t<bf16x8_v>(dot, i * 32, hq, t, lane), pf[t], dv[i]);
+          dk[i] = mfma(frag_t<bf16x8_v>(qt, i * 32, hq, t, lane), sf[t], dk[i]);
           if (i & 1) __builtin_amdgcn_sched_barrier(0);
         }
       }

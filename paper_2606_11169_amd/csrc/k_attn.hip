@@ -228,14 +228,27 @@ struct AttnP {
 };
 
 // ---------------------------------------------------------------- forward
+// Query block, head and batch row of this workgroup (forward and dQ grids):
+// the blocks in decreasing order of work (a causal block's work grows with its
+// index), the (batch row, head) pairs fastest. Workgroups are handed to the 8
+// XCDs round-robin, so each XCD receives blocks of every size; with the block
+// index fastest instead, one XCD would receive only the heaviest and the
+// middle blocks of every head (twice the mean work).
+__device__ __forceinline__ void query_block_of(const AttnP &p, int nqb, int &qb, int &h, int &b) {
+  const int nbh = p.H * p.B, i = (int)blockIdx.x;
+  qb = nqb - 1 - i / nbh;
+  h = (i % nbh) % p.H;
+  b = (i % nbh) / p.H;
+}
+
 template <typename QE>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
   __shared__ __align__(16) char smem[2 * 2 * TILE];  // stage s: K tile | V tile
   lds_t *const L = LDS_AS(char, smem);
   const int nqb = (p.S + ROWS - 1) / ROWS;
-  const int qb = nqb - 1 - (int)blockIdx.x;  // heaviest blocks first
-  const int h = blockIdx.y, b = blockIdx.z;
+  int qb, h, b;
+  query_block_of(p, nqb, qb, h, b);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hf = lane >> 5;
@@ -464,8 +477,8 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   __shared__ __align__(16) char smem[2 * 3 * TILE];
   lds_t *const L = LDS_AS(char, smem);
   const int nqb = (p.S + ROWS - 1) / ROWS;
-  const int qb = nqb - 1 - (int)blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  int qb, h, b;
+  query_block_of(p, nqb, qb, h, b);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hf = lane >> 5;
@@ -1039,7 +1052,8 @@ template <typename QE>
 lc_status fwd_mc(const lc_attn_args &a, hipStream_t s) {
   LC_TRY(check_extents(a));
   const unsigned nqb = (unsigned)((a.S + ROWS - 1) / ROWS);
-  hipLaunchKernelGGL(attn_fwd_kernel<QE>, dim3(nqb, a.H, a.B), dim3(NT), 0, s, mc_params(a));
+  hipLaunchKernelGGL(attn_fwd_kernel<QE>, dim3(nqb * (unsigned)(a.H * a.B)), dim3(NT), 0, s,
+                     mc_params(a));
   return check_launch("attn_fwd_kernel");
 }
 
@@ -1059,7 +1073,7 @@ lc_status bwd_mc(const lc_attn_args &a, hipStream_t s) {
     hipLaunchKernelGGL(attn_gqa_sum_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s, p);
     LC_TRY(check_launch("attn_gqa_sum_kernel"));
   }
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(nb, a.H, a.B), dim3(NT), 0, s, p);
+  hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(nb * (unsigned)(a.H * a.B)), dim3(NT), 0, s, p);
   return check_launch("attn_bwd_dq_kernel");
 }
 

@@ -10,8 +10,9 @@
 // instruction). The score block is computed transposed, S^T = K Q^T, so each
 // lane holds one query's scores: the row max and row sum need lane-local work
 // plus one swap with the partner lane (lane ^ 32). The output is accumulated
-// transposed, O^T += V^T P^T, so the rescale is a lane-local scalar (skipped
-// when no query's maximum moved), and the P^T accumulator registers feed the
+// transposed, O^T += V^T P^T, so the rescale is a lane-local scalar (done
+// only when some query's score exceeds its reference maximum by more than
+// 2^8), and the P^T accumulator registers feed the
 // MFMA directly: the keys a lane holds define the k slots, and the V^T
 // fragment is read in that key order with the transposing LDS load
 // ds_read_b64_tr_b16 from V's key-major rows. Forward products use the q/k/v
@@ -173,6 +174,19 @@ __device__ __forceinline__ VT frag_t(const lds_t *t, int row0, int j, int tt, in
                                                                          ((c ^ ((r >> 1) & 7)) << 4));
 }
 
+// max / sum of a lane's value and lane (l ^ 32)'s, in every lane
+// (v_permlane32_swap: the upper half of one register trades places with the
+// lower half of the other; with both registers holding x, the results hold the
+// lower and the upper half of x in both halves)
+__device__ __forceinline__ float max_with_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_with_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <typename E>
 __device__ __forceinline__ typename V8<E>::type pack8(const f32x16_v &a, int base) {
   typename V8<E>::type r;
@@ -290,10 +304,21 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
     const int k0 = kb * KB;
     if (active && k0 <= q0 + 31) {
       f32x16_v s[2] = {zero16(), zero16()};
+      // K fragments are read one k-step ahead of the products that use them
+      QV kf[2][2];
+      kf[0][0] = frag_rows<QV>(cur, 0, 0, lane);
+      kf[0][1] = frag_rows<QV>(cur, 32, 0, lane);
 #pragma unroll
-      for (int es = 0; es < 8; ++es)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), qf[es], s[j]);
+      for (int es = 0; es < 8; ++es) {
+        if (es + 1 < 8) {
+          kf[(es + 1) & 1][0] = frag_rows<QV>(cur, 0, es + 1, lane);
+          kf[(es + 1) & 1][1] = frag_rows<QV>(cur, 32, es + 1, lane);
+        }
+        __builtin_amdgcn_sched_barrier(0);  // (keeps the reads ahead of the products)
+        s[0] = mfma(kf[es & 1][0], qf[es], s[0]);
+        s[1] = mfma(kf[es & 1][1], qf[es], s[1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if (k0 + KB - 1 > q0) {  // diagonal block (wave-uniform): mask keys after the query
 #pragma unroll
         for (int j = 0; j < 2; ++j)
@@ -301,14 +326,19 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
           for (int r = 0; r < 16; ++r)
             if (k0 + j * 32 + out_row(r, hf) > myq) s[j][r] = -INFINITY;
       }
-      float mx = -INFINITY;
+      float mx0 = -INFINITY, mx1 = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[j][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m, mx * sc);
-      if (__any(mn > m)) {  // rescale only when some query's maximum moved
+      for (int r = 0; r < 16; ++r) {
+        mx0 = fmaxf(mx0, s[0][r]);
+        mx1 = fmaxf(mx1, s[1][r]);
+      }
+      const float mx = max_with_partner(fmaxf(mx0, mx1)) * sc;
+      // The reference maximum m only moves when a score exceeds it by more
+      // than 8 (base-2 exponent units): softmax weights stay <= 2^8, exact in
+      // the fp16/bf16 P and far from fp32 overflow, and most blocks skip the
+      // rescale of the output.
+      if (__any(mx > m + 8.0f)) {
+        const float mn = fmaxf(m, mx);
         const float alpha = mn > m ? ex2(m - mn) : 1.0f;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -317,16 +347,16 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
         l *= alpha;
         m = mn;
       }
-      float ls = 0.0f;
+      float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // four independent chains
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const float pv = ex2(__builtin_fmaf(s[j][r], sc, -m));
           s[j][r] = pv;
-          ls += pv;
+          ls[2 * j + (r & 1)] += pv;
         }
-      l += ls;
+      l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
       const lds_t *vt = cur + TILE;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
@@ -341,7 +371,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
     __syncthreads();
   }
   if (!active) return;
-  const float lt = l + __shfl_xor(l, 32, 64);
+  const float lt = sum_with_partner(l);
   const float inv = 1.0f / lt;
   __bf16 *orow = p.o + (row0 + myq) * p.ld_o + h * HD;
 #pragma unroll

@@ -565,13 +565,28 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
     const int k0 = kb * KB;
     if (active && k0 <= q0 + 31) {
       f32x16_v s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
+      // K fragments are read one k-step ahead of their products, V fragments
+      // two products ahead of theirs (registers allow no more)
+      QV kf[2][2];
 #pragma unroll
-      for (int es = 0; es < 8; ++es)
+      for (int j = 0; j < 2; ++j) kf[0][j] = frag_rows<QV>(cur, j * 32, 0, lane);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          s[j] = mfma(frag_rows<QV>(cur, j * 32, es, lane), qf[es], s[j]);
-          dp[j] = mfma(frag_rows<bf16x8_v>(cur + TILE, j * 32, es, lane), df[es], dp[j]);
+      for (int es = 0; es < 8; ++es) {
+        bf16x8_v vf[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) vf[j] = frag_rows<bf16x8_v>(cur + TILE, j * 32, es, lane);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) s[j] = mfma(kf[es & 1][j], qf[es], s[j]);
+        if (es + 1 < 8) {
+#pragma unroll
+          for (int j = 0; j < 2; ++j) kf[(es + 1) & 1][j] = frag_rows<QV>(cur, j * 32, es + 1, lane);
         }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) dp[j] = mfma(vf[j], df[es], dp[j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if (k0 + KB - 1 > q0) {  // diagonal block (wave-uniform): P = 0 for keys after the query
 #pragma unroll
         for (int j = 0; j < 2; ++j)

@@ -724,17 +724,25 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
       asm volatile("" : "+v"(rsw));
       const lds_t *qrow = cur + (rsw & ~0xFF);
       const int x4 = rsw & 0xF0;
+      typedef __attribute__((address_space(3))) QV lds_q;
+      typedef __attribute__((address_space(3))) bf16x8_v lds_b;
+      // each fragment is read one product ahead of the product that uses it
+      QV qa = *reinterpret_cast<const lds_q *>(qrow + x4);
+      bf16x8_v da = *reinterpret_cast<const lds_b *>(qrow + TILE + x4);
 #pragma unroll
       for (int es = 0; es < 8; ++es) {
-        const int off = (32 * es) ^ x4;  // ((2 es + hf) ^ swz) << 4
-        typedef __attribute__((address_space(3))) QV lds_q;
-        typedef __attribute__((address_space(3))) bf16x8_v lds_b;
-        s = mfma(*reinterpret_cast<const lds_q *>(qrow + off), kf[es], s);
-        dp = mfma(*reinterpret_cast<const lds_b *>(qrow + TILE + off), vf[es], dp);
-        // one k-step of fragments in flight: registers are the limit, and a
-        // spilled value reloaded here would wait for the stage's prefetch too
-        // (one counter covers both kinds of load)
+        const int offn = (32 * (es + 1)) ^ x4;  // ((2 (es + 1) + hf) ^ swz) << 4
+        QV qn{};
+        bf16x8_v dn{};
+        if (es + 1 < 8) qn = *reinterpret_cast<const lds_q *>(qrow + offn);
         __builtin_amdgcn_sched_barrier(0);
+        s = mfma(qa, kf[es], s);
+        if (es + 1 < 8) dn = *reinterpret_cast<const lds_b *>(qrow + TILE + offn);
+        __builtin_amdgcn_sched_barrier(0);
+        dp = mfma(da, vf[es], dp);
+        __builtin_amdgcn_sched_barrier(0);
+        qa = qn;
+        da = dn;
       }
       if (q0 < k0w + 31) {  // diagonal block (wave-uniform): P = 0 for queries before the key
 #pragma unroll

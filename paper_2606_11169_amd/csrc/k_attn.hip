@@ -102,6 +102,15 @@ __device__ __forceinline__ void dma16(i32x4_v rs, lds_t *lds, uint32_t off) {
                : "v"(off), "s"(rs), "s"(m0)
                : "memory", "m0");
 }
+// the same with a wave-uniform part of the offset in the instruction's scalar
+// offset (every access in range: the callers' tiles lie inside their buffers)
+__device__ __forceinline__ void dma16s(i32x4_v rs, lds_t *lds, uint32_t voff, uint32_t soff) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t) reinterpret_cast<uintptr_t>(lds));
+  asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voff), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(soff)), "s"(m0)
+               : "memory", "m0");
+}
 // 4 bytes per lane into lds + 4 * lane
 __device__ __forceinline__ void dma4(i32x4_v rs, lds_t *lds, uint32_t off) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t) reinterpret_cast<uintptr_t>(lds));
@@ -693,11 +702,16 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
     ublk = (uint32_t)(KB * 2);
   }
   u0 = urun * (uint32_t)(8 * (w & 1));
+  // per-lane part of the offsets; the run and block parts go in the scalar
+  // offset (four registers instead of eight held across the block loop)
+  uint32_t vo[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) vo[v] = lbase + lcol[v];
   auto load = [&](int qbi, lds_t *st) {
     lds_t *const tile = st + tl * TILE + (w & 1) * 8 * 1024;
     const uint32_t ub = ublk * (uint32_t)qbi + u0;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) dma16(rs, tile + t * 1024, ub + urun * t + lbase + lcol[t & 3]);
+    for (int t = 0; t < 8; ++t) dma16s(rs, tile + t * 1024, vo[t & 3], ub + urun * t);
     if (w == NT / 64 - 1) {
       const uint32_t off = (uint32_t)((sbase + (int64_t)qbi * KB + lane) * 4);
       dma4(rl, st + 4 * TILE, off);

@@ -763,18 +763,29 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
         for (int r = 0; r < 16; ++r)
           if (q0 + out_row(r, hf) < myk) s[r] = -INFINITY;
       }
-      // four rows at a time (their lse and D are 4 consecutive floats each),
-      // so that only 8 of them are held at once
+      // four rows at a time: their lse and D are 4 consecutive floats each
+      // (rows 8 g + 4 hf + [0, 4) of the half), read one group ahead
+      typedef __attribute__((ext_vector_type(4))) float f4_t;
+      const f4_t *const lseq = reinterpret_cast<const f4_t *>(sL + 4 * hf);
+      f4_t lc = lseq[0], dc = lseq[16];
 #pragma unroll
-      for (int r4 = 0; r4 < 16; r4 += 4) {
-#pragma unroll
-        for (int r = r4; r < r4 + 4; ++r) {
-          const int qi = out_row(r, hf);
-          const float pv = ex2(__builtin_fmaf(s[r], sc, -sL[qi] * LOG2E));
-          s[r] = pv;
-          dp[r] = pv * (dp[r] - sL[64 + qi]);
+      for (int g = 0; g < 4; ++g) {
+        f4_t ln{}, dn{};
+        if (g + 1 < 4) {
+          ln = lseq[2 * (g + 1)];
+          dn = lseq[16 + 2 * (g + 1)];
         }
         __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;  // out_row(r, hf) = 8 g + 4 hf + e
+          const float pv = ex2(__builtin_fmaf(s[r], sc, -lc[e] * LOG2E));
+          s[r] = pv;
+          dp[r] = pv * (dp[r] - dc[e]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        lc = ln;
+        dc = dn;
       }
       // P and dS rounded to bf16 before the gradient products, so that the
       // fp32 score registers are free while those run

@@ -793,14 +793,22 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
       const bf16x8_v sf[2] = {pack8<__bf16>(dp, 0), pack8<__bf16>(dp, 8)};
       __builtin_amdgcn_sched_barrier(0);
       const lds_t *qt = cur + 2 * TILE, *dot = cur + 3 * TILE;
+      // steps n = 4 t + i; the dO^T and Q^T fragments of step n + 1 are read
+      // while step n multiplies
+      bf16x8_v fo[2], fq[2];
+      fo[0] = frag_t<bf16x8_v>(dot, 0, hq, 0, lane);
+      fq[0] = frag_t<bf16x8_v>(qt, 0, hq, 0, lane);
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          dv[i] = mfma(frag_t<bf16x8_v>(dot, i * 32, hq, t, lane), pf[t], dv[i]);
-          dk[i] = mfma(frag_t<bf16x8_v>(qt, i * 32, hq, t, lane), sf[t], dk[i]);
-          if (i & 1) __builtin_amdgcn_sched_barrier(0);
+      for (int n = 0; n < 8; ++n) {
+        const int t = n >> 2, i = n & 3;
+        if (n + 1 < 8) {
+          fo[(n + 1) & 1] = frag_t<bf16x8_v>(dot, ((n + 1) & 3) * 32, hq, (n + 1) >> 2, lane);
+          fq[(n + 1) & 1] = frag_t<bf16x8_v>(qt, ((n + 1) & 3) * 32, hq, (n + 1) >> 2, lane);
         }
+        __builtin_amdgcn_sched_barrier(0);
+        dv[i] = mfma(fo[n & 1], pf[t], dv[i]);
+        dk[i] = mfma(fq[n & 1], sf[t], dk[i]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     wait_vm0();

@@ -323,6 +323,41 @@ def adam_traffic():
     return float(vals["traffic_bytes_per_launch"])
 
 
+def gemm_compare(torch, lc, stream, reps=20, n=4096):
+    """Diagnostic: the library's GEMM and hipBLASLt (torch.matmul; the library never calls
+    it) on one n^3 product C = A B^T of N(0, 1) bf16 operands, both k-major (the layout of
+    the stage's forward products), bf16 output; `reps` launches back to back between two
+    HIP events (per-launch events would add each call's host-side launch gap)."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    a = torch.randn(n, n, generator=g, device="cuda").to(torch.bfloat16)
+    b = torch.randn(n, n, generator=g, device="cuda").to(torch.bfloat16)
+    c = torch.empty(n, n, dtype=torch.bfloat16, device="cuda")
+
+    def lib():
+        lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE, n, n, n, a, n, 1, b, n, 1, c, n, stream=stream)
+
+    def blas():
+        torch.matmul(a, b.t(), out=c)
+
+    out = {"workload": f"gemm_nt_{n}^3_bf16", "flop": 2 * n ** 3}
+    with torch.cuda.stream(stream):
+        for name, fn in (("lc_gemm", lib), ("hipblaslt", blas)):
+            for _ in range(3):
+                fn()
+            stream.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            e1.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            out[name] = {"us": round(ms * 1e3, 1), "tflops": round(2 * n ** 3 / (ms * 1e-3) / 1e12, 1)}
+    return out
+
+
 def adam_shard(torch, lc, shard, stream, reps=20):
     n = shard.n
     dev = "cuda"
@@ -521,6 +556,9 @@ def main():
                          "two streams")
     ap.add_argument("--adam-only", action="store_true",
                     help="only the calibration copy and the AdamW shard (PMC runs)")
+    ap.add_argument("--gemm-compare", action="store_true",
+                    help="only the library's GEMM beside hipBLASLt on a 4096^3 NT product "
+                         "(a diagnostic for the matrix cores' sustained rate)")
     ap.add_argument("--no-streaming", action="store_true",
                     help="skip the RMSNorm / accumulate bandwidth lines")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
@@ -590,6 +628,10 @@ def main():
             res[c.name] = {"value": round(otf, 2), "unit": "TFLOP/s",
                            "ms_per_step": round(oms, 2), "outputs_finite": ofin}
         print(json.dumps({"overlap_stage": res}))
+        return
+    if args.gemm_compare:
+        print(json.dumps({"gemm_compare": gemm_compare(torch, lc, stream, reps=args.steps)}),
+              flush=True)
         return
     if args.adam_only:
         calibration_copy(torch, lc, stream)

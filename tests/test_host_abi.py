@@ -381,6 +381,9 @@ def test_bench_reads_the_committed_counter_summaries():
     spec = importlib.util.spec_from_file_location("bench_mod", root / "bench.py")
     bench = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(bench)
-    for v in (bench.measured_traffic(), bench.measured_mfma_busy()):
-        assert v is None or v > 0
+    t = bench.measured_traffic()
+    assert t is None or t > 0
+    b = bench.measured_mfma_busy()
+    assert b is None or (0 < b["value"] < 1 and b["source"] == "profiles/stage7b_mfma_busy.md"
+                         and b["csrc_sha256_16"] == bench.csrc_hash())
     assert len(bench.csrc_hash()) == 16 and len(bench.gemm_source_hash()) == 16

@@ -174,8 +174,8 @@ lc_status lc_rmsnorm_backward_noalloc(const lc_norm_args *args, void *stream);
  *   dk_j = sum_i dS_ij q_i / sqrt(hd);
  * if rope_cos/rope_sin are non-NULL, dq and dk are then rotated back by
  * -angle (the transpose of the forward rotation, positions 0..S-1).
- * Deterministic (no atomics); scratch (lc_attention_scratch_bytes) holds D,
- * a bf16 copy of v and bf16 transposes of q, k, dout that the backward's
+ * Deterministic (no atomics); scratch (lc_attention_scratch_bytes) holds D
+ * and, for fp16 q/k/v, the bf16 copies of q, k and v that the backward's
  * gradient products read.
  * Types: matrix-core path: q, k, v LC_FP16 or LC_BF16 (`dtype`; forward
  * products in that type), o, dout, dq, dk, dv LC_BF16 (gradient products in

@@ -18,27 +18,24 @@
 // ds_read_b64_tr_b16 from V's key-major rows. Forward products use the q/k/v
 // element type (P is rounded to it too).
 //
-// Backward (deterministic, no atomics): a prep pass computes D = rowsum(dO*O)
-// and writes bf16 transposes of q, k and dO (per head, [head dim][position])
-// plus, for fp16 inputs, a bf16 copy of v; then one kernel per 128 keys
-// accumulates dV^T = dO^T P and dK^T = Q^T dS over the query blocks at or
-// after the diagonal, and one kernel per 256 queries accumulates
-// dQ^T = K^T dS^T over the visible key blocks. Both recompute P from the
-// forward's log-sum-exp with the forward's q/k element type (so P matches the
-// forward) and take every gradient product in bf16. RoPE's inverse rotation
-// of dq/dk is applied in the epilogues.
+// Backward (deterministic, no atomics): one kernel per 256 queries forms
+// D = rowsum(dO*O) of its queries (written out for the next kernel) and
+// accumulates dQ^T = K^T dS^T over the visible key blocks; then one kernel per
+// 128 keys accumulates dV^T = dO^T P and dK^T = Q^T dS over the query blocks
+// at or after the diagonal. Both recompute P from the forward's log-sum-exp
+// with the forward's q/k element type (so P matches the forward) and take
+// every gradient product in bf16; for fp16 inputs a copy pass first writes
+// bf16 rows of q, k and v for those products. The gradient products read
+// their K^T, Q^T and dO^T operands from the same row tiles as the score
+// products, with transposing LDS reads in the accumulator's key (or query)
+// order, so no transposed copy is ever written. RoPE's inverse rotation of
+// dq/dk is applied in the epilogues.
 //
 // Row tiles are [64 rows][128 columns] of 2-byte elements (256-byte rows of 16
 // chunks); chunk c of row r sits at chunk c ^ f(r) with
 // f(r) = ((r & 3) << 2) | ((r >> 2) & 3). A 128-bit fragment read (16
 // consecutive rows, one chunk) and a transposing read (4 consecutive rows,
 // four chunks) both touch every bank once per phase.
-// Transposed tiles (backward) are [128 head-dim rows][64 positions] (128-byte
-// rows of 8 chunks, chunk c of row r at c ^ ((r >> 1) & 7)). The prep pass
-// stores the positions of every 16-group in the order 0-3, 8-11, 4-7, 12-15:
-// the order in which a 32 x 32 accumulator's registers 8t .. 8t+7 hold their
-// rows, so the k values of a gradient product's fragment are 16 contiguous
-// bytes (one ds_read_b128) instead of two transposing reads.
 #include "common.hpp"
 
 #include <math.h>
@@ -159,28 +156,24 @@ __device__ __forceinline__ VT frag_cols(const lds_t *t, int col0, int kbase, int
   return __builtin_bit_cast(VT, v);
 }
 
-// Run `run` (0..15) of a transposed [128][64] tile: head-dim rows 8 run ..
-// 8 run + 7, positions pos0 .. pos0 + 63 of the [128][S] matrix of one head
-// that starts at element `hbase` of its buffer.
-__device__ __forceinline__ void tt_run(i32x4_v rs, lds_t *tile, int run, int64_t hbase, int S,
-                                       int pos0, int lane) {
-  const int r = 8 * run + (lane >> 3);
-  const int c = (lane & 7) ^ ((r >> 1) & 7);
-  const uint32_t off = (uint32_t)((hbase + (int64_t)r * S + pos0 + 8 * c) * 2);
-  dma16(rs, tile + run * 1024, off);
+// frag_cols for col0 = 32 i and kbase a multiple of 16, from `a`: the LDS
+// byte address of a 256-byte-aligned tile plus cols_lane(lane). The lane term
+// holds (lane % 16) / 4 in address bits 6-7, which column block i flips by
+// XOR; rows c + 8 .. c + 11 differ from rows c .. c + 3 by 8 rows and by
+// chunk bit 1 (address bit 5). One XOR per address, the rest immediate.
+__device__ __forceinline__ uint32_t cols_lane(int lane) {
+  const int i16 = lane & 15, hf = lane >> 5, b4 = (lane >> 4) & 1;
+  return (uint32_t)((4 * hf + (i16 >> 2)) * 256 + 64 * (i16 >> 2) +
+                    16 * ((2 * b4 + ((i16 >> 1) & 1)) ^ hf) + 8 * (i16 & 1));
 }
-
-// MFMA operand of transposed-tile rows row0 .. row0+31 (lane l: row row0 + l % 32)
-// whose 8 k values are the stored positions 32 j + 16 t + 8 (lane / 32) + [0, 8):
-// in the prep pass's order these are the positions a 32 x 32 accumulator's
-// registers 8t .. 8t+7 hold (rows 16t + 4 hf + [0, 4) and 16t + 8 + 4 hf + [0, 4)
-// of block j).
 template <typename VT>
-__device__ __forceinline__ VT frag_t(const lds_t *t, int row0, int j, int tt, int lane) {
-  const int r = row0 + (lane & 31);
-  const int c = 4 * j + 2 * tt + (lane >> 5);
-  return *reinterpret_cast<const __attribute__((address_space(3))) VT *>(t + r * 128 +
-                                                                         ((c ^ ((r >> 1) & 7)) << 4));
+__device__ __forceinline__ VT frag_cols_x(uint32_t a, int i, int kbase) {
+  typedef __attribute__((address_space(3))) s16x4_v lds_v4;
+  const uint32_t lo = (a ^ (64u * i)) + 256u * kbase;
+  const uint32_t hi = (a ^ (64u * i) ^ 32u) + 256u * kbase + 2048u;
+  const s16x4_v v[2] = {__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(uintptr_t)lo),
+                        __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(uintptr_t)hi)};
+  return __builtin_bit_cast(VT, v);
 }
 
 // max / sum of a lane's value and lane (l ^ 32)'s, in every lane
@@ -235,16 +228,16 @@ struct AttnP {
   const __bf16 *dout;
   __bf16 *dq, *dk, *dv;
   float *D;
-  // backward: bf16 rows of v (p.v itself for bf16 inputs), and bf16 transposes
-  // of q and dO ([B][H][128][S]) and of k ([B][Hkv][128][S]) (positions
-  // permuted within 16-groups)
-  const __bf16 *vb;
-  __bf16 *vb_w, *qt, *kt, *dot;
+  // backward: bf16 rows of q, k and v for the gradient products (p.q, p.k,
+  // p.v themselves for bf16 inputs; for fp16 inputs copies in the scratch,
+  // written through the _w pointers)
+  const __bf16 *qb, *kb, *vb;
+  __bf16 *qb_w, *kb_w, *vb_w;
   // grouped-query attention: fp32 partial dk, dv per query head [B*S, H*128]
   float *dkp, *dvp;
   const float *rcos, *rsin;
-  int64_t ld_qkv, ld_o, ld_d, ld_vb;
-  uint32_t qkv_bytes, o_bytes, vb_bytes, t_bytes, kt_bytes, lse_bytes;  // buffer extents (q/k/v from p.q)
+  int64_t ld_qkv, ld_o, ld_d, ld_qb, ld_kb, ld_vb;
+  uint32_t qkv_bytes, o_bytes, qb_bytes, kb_bytes, vb_bytes, lse_bytes;  // buffer extents (q/k/v from p.q)
   int S, H, B;
   int Hkv, G;   // key/value heads; query heads per key/value head
   float scale;  // 1/sqrt(hd)
@@ -395,82 +388,27 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
 }
 
 // ---------------------------------------------------------------- backward
-// One workgroup per (64-position block, head, batch row): D[b,h,i] =
-// sum_e dO[i,e] O[i,e]; the block's columns of dO and q transposed into
-// [B][H][128][S] bf16 (positions of each 16-group in the order 0-3, 8-11,
-// 4-7, 12-15) through an LDS tile; the first query head of each key/value
-// head also transposes k into [B][Hkv][128][S] and, for fp16 q/k/v, writes
-// the bf16 rows of v.
-template <typename QE>
-__global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnP p) {
-  constexpr int W = 130;  // tile row stride (65 words): conflict-free fills and gathers
-  __shared__ __align__(16) __bf16 tile[64 * W];
-  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int t = threadIdx.x, r = t >> 2, qtr = t & 3;  // row, 32-column quarter
-  const int pos0 = blk * 64;
-  const int64_t grow = (int64_t)b * p.S + pos0 + r;
-  const int col = h * HD + qtr * 32;
-  const int64_t hbase = ((int64_t)b * p.H + h) * HD * p.S;
-  const int kvh = h / p.G;
-  const bool lead = h % p.G == 0;  // workgroup-uniform
-  const int kcol = kvh * HD + qtr * 32;
-  const int64_t kbase = ((int64_t)b * p.Hkv + kvh) * HD * p.S;
-
-  auto put = [&](int u, bf16x8_v v) {  // columns 32 qtr + 8u .. +7 of row r
-    uint32_t *w = reinterpret_cast<uint32_t *>(tile + r * W + qtr * 32 + 8 * u);
-    const uint4 x = __builtin_bit_cast(uint4, v);
-    w[0] = x.x;
-    w[1] = x.y;
-    w[2] = x.z;
-    w[3] = x.w;
-  };
-  auto write_t = [&](__bf16 *dst, int64_t base) {  // 1024 chunks of 8 stored positions
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int idx = t + 256 * it, c = idx & 7, n = idx >> 3;
-      const int rb = 16 * (c >> 1) + 4 * (c & 1);
-      bf16x8_v v;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = tile[(rb + (e & 3) + 8 * (e >> 2)) * W + n];
-      *reinterpret_cast<bf16x8_v *>(dst + base + (int64_t)n * p.S + pos0 + 8 * c) = v;
-    }
-  };
-
-  float acc = 0.0f;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const bf16x8_v a = *reinterpret_cast<const bf16x8_v *>(p.dout + grow * p.ld_o + col + 8 * u);
-    const bf16x8_v o = *reinterpret_cast<const bf16x8_v *>(p.o + grow * p.ld_o + col + 8 * u);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc += (float)a[i] * (float)o[i];
-    put(u, a);
+// fp16 inputs: bf16 rows of q, k and v for the gradient products, one
+// 16-byte chunk (8 elements) per thread, consecutive threads on consecutive
+// chunks of the [B*S, H*128] (q) and [B*S, Hkv*128] (k, v) matrices.
+__global__ __launch_bounds__(256) void attn_bwd_copy_kernel(AttnP p) {
+  const int64_t rows = (int64_t)p.B * p.S;
+  const int cq = p.H * HD / 8, ck = p.Hkv * HD / 8;  // chunks per row
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  int src = 0, cpr = cq;
+  if (i >= rows * cq) {
+    i -= rows * cq;
+    src = 1 + (int)(i / (rows * ck));
+    i -= (src - 1) * rows * ck;
+    cpr = ck;
   }
-  acc += __shfl_xor(acc, 1, 64);
-  acc += __shfl_xor(acc, 2, 64);
-  if (qtr == 0) p.D[((int64_t)b * p.H + h) * p.S + pos0 + r] = acc;
-  __syncthreads();
-  write_t(p.dot, hbase);
-#pragma unroll
-  for (int src = 0; src < 2; ++src) {
-    if (src == 1 && !lead) break;
-    __syncthreads();
-    const QE *X = static_cast<const QE *>(src == 0 ? p.q : p.k);
-    const int c0 = src == 0 ? col : kcol;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      put(u, to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(X + grow * p.ld_qkv + c0 + 8 * u)));
-    __syncthreads();
-    write_t(src == 0 ? p.qt : p.kt, src == 0 ? hbase : kbase);
-  }
-  if constexpr (!std::is_same<QE, __bf16>::value) {
-    if (lead) {
-      const QE *V = static_cast<const QE *>(p.v);
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        *reinterpret_cast<bf16x8_v *>(p.vb_w + grow * p.ld_vb + kcol + 8 * u) =
-            to_bf16x8<QE>(*reinterpret_cast<const uint4 *>(V + grow * p.ld_qkv + kcol + 8 * u));
-    }
-  }
+  if (src > 2) return;
+  const int64_t r = i / cpr, c = 8 * (i % cpr);
+  const _Float16 *const x = static_cast<const _Float16 *>(src == 0 ? p.q : src == 1 ? p.k : p.v);
+  __bf16 *const y = src == 0 ? p.qb_w : src == 1 ? p.kb_w : p.vb_w;
+  const int64_t ldy = src == 0 ? p.ld_qb : src == 1 ? p.ld_kb : p.ld_vb;
+  *reinterpret_cast<bf16x8_v *>(y + r * ldy + c) =
+      to_bf16x8<_Float16>(*reinterpret_cast<const uint4 *>(x + r * p.ld_qkv + c));
 }
 
 __device__ __forceinline__ void rope_inverse_pairs(f32x16_v (&acc)[4], const float *rcos,
@@ -509,11 +447,15 @@ __device__ __forceinline__ void store_row_t(__bf16 *row, const f32x16_v (&acc)[4
     }
 }
 
-// dQ: one workgroup per 256 queries; LDS stage = K (QE) | V (bf16) | K^T (bf16)
+// dQ: one workgroup per 256 queries; LDS stage = K (QE) | V (bf16), plus the
+// bf16 rows of K for fp16 inputs. Each query's D = dO.O is formed here from
+// the dO row the lane pair holds and written out for the dK/dV kernel.
 template <typename QE>
 __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
-  __shared__ __align__(16) char smem[2 * 3 * TILE];
+  constexpr bool SEP = !std::is_same<QE, __bf16>::value;  // separate bf16 K tile
+  constexpr int NTQ = SEP ? 3 : 2;                          // tiles per stage
+  __shared__ __align__(256) char smem[2 * NTQ * TILE];      // 256-byte aligned (frag_cols_x)
   lds_t *const L = LDS_AS(char, smem);
   const int nqb = (p.S + ROWS - 1) / ROWS;
   int qb, h, b;
@@ -527,7 +469,6 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   const int myq = q0 + l32;
   const float sc = p.scale * LOG2E;
   const int kvh = h / p.G;
-  const int64_t kbase = ((int64_t)b * p.Hkv + kvh) * HD * p.S;
 
   QV qf[8];
   bf16x8_v df[8];
@@ -545,32 +486,46 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   }
   const int64_t si = ((int64_t)b * p.H + h) * p.S + (active ? myq : 0);
   const float lse2 = p.lse[si] * LOG2E;
-  const float Dq = p.D[si];
   f32x16_v acc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc[i] = zero16();
 
-  // 48 runs per block: K (QE) runs 0-15, V (bf16) 16-31, K^T (bf16) 32-47; 6 per wave
+  // 16 NTQ runs per block: K (QE) runs 0-15, V (bf16) 16-31, bf16 K 32-47;
+  // 2 NTQ per wave
   const i32x4_v rk = make_rsrc(p.k, p.qkv_bytes);
   const i32x4_v rvb = make_rsrc(p.vb, p.vb_bytes);
-  const i32x4_v rkt = make_rsrc(p.kt, p.kt_bytes);
+  const i32x4_v rkb = make_rsrc(p.kb, p.kb_bytes);
   auto load = [&](int kb, lds_t *st) {
     const int64_t g0 = row0 + (int64_t)kb * KB;
 #pragma unroll
-    for (int t = 0; t < 6; ++t) {
-      const int run = 6 * w + t, which = run >> 4;
+    for (int t = 0; t < 2 * NTQ; ++t) {
+      const int run = 2 * NTQ * w + t, which = run >> 4;
       if (which == 0) tile_run(rk, st, run & 15, g0, p.ld_qkv, kvh * HD, lane);
       else if (which == 1) tile_run(rvb, st + TILE, run & 15, g0, p.ld_vb, kvh * HD, lane);
-      else tt_run(rkt, st + 2 * TILE, run & 15, kbase, p.S, kb * KB, lane);
+      else tile_run(rkb, st + 2 * TILE, run & 15, g0, p.ld_kb, kvh * HD, lane);
     }
   };
   const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
   load(0, L);
+  // D of this query (its O row read while the first block streams in): the
+  // lane's 64 products, then its partner's (lane ^ 32)
+  float Dq = 0.0f;
+  if (active) {
+#pragma unroll
+    for (int es = 0; es < 8; ++es) {
+      const bf16x8_v o8 = *reinterpret_cast<const bf16x8_v *>(p.o + h * HD + (row0 + myq) * p.ld_o +
+                                                              es * 16 + hf * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Dq += (float)df[es][e] * (float)o8[e];
+    }
+  }
+  Dq = sum_with_partner(Dq);
+  if (active && hf == 0) p.D[si] = Dq;
   wait_vm0();
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    const lds_t *cur = L + (kb & 1) * 3 * TILE;
-    if (kb + 1 < nkb) load(kb + 1, L + ((kb + 1) & 1) * 3 * TILE);
+    const lds_t *cur = L + (kb & 1) * NTQ * TILE;
+    if (kb + 1 < nkb) load(kb + 1, L + ((kb + 1) & 1) * NTQ * TILE);
     const int k0 = kb * KB;
     if (active && k0 <= q0 + 31) {
       f32x16_v s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
@@ -610,14 +565,18 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
           const float pv = ex2(__builtin_fmaf(s[j][r], sc, -lse2));
           dp[j][r] = pv * (dp[j][r] - Dq);
         }
-      const lds_t *kt = cur + 2 * TILE;
+      // K^T fragments: transposing reads of the bf16 K rows in dS's key order
+      uint32_t cl = cols_lane(lane);
+      asm volatile("" : "+v"(cl));  // recomputed each block, not held across the loop
+      const uint32_t ak = (uint32_t)(uintptr_t)cur + cl + (SEP ? 2 * TILE : 0);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const bf16x8_v sf = pack8<__bf16>(dp[j], 8 * t);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) acc[i] = mfma(frag_t<bf16x8_v>(kt, i * 32, j, t, lane), sf, acc[i]);
+          for (int i = 0; i < 4; ++i)
+            acc[i] = mfma(frag_cols_x<bf16x8_v>(ak, i, j * 32 + 16 * t), sf, acc[i]);
         }
     }
     wait_vm0();
@@ -637,15 +596,22 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
 // take the first and the second 32 queries of every 64-query block at or
 // after the diagonal; at the end wave w + 4 hands its partial dK, dV to wave w
 // through LDS, which adds them (fixed order: deterministic). LDS stage (two
-// of them) = Q (QE) | dO | Q^T | dO^T | lse | D of one 64-query block. With
+// of them) = Q (QE) | dO | (fp16 inputs: bf16 Q) | lse | D of one 64-query
+// block. With
 // grouped-query attention the workgroup writes its query head's share of the
 // key/value head's dK, dV as fp32 rows; attn_gqa_sum_kernel adds the shares.
 constexpr int KV_ROWS = 128;
 template <typename QE>
 __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
-  constexpr int STAGE = 4 * TILE + 512;
-  __shared__ __align__(16) char smem[2 * STAGE];
+  constexpr bool SEP = !std::is_same<QE, __bf16>::value;  // separate bf16 Q tile
+  constexpr int NTK = SEP ? 3 : 2;                          // row tiles per stage
+  constexpr int RPW = SEP ? 8 : 4;                          // tile runs per wave
+  constexpr int STAGE = NTK * TILE + 512;
+  // two stages (256-byte aligned for frag_cols_x), reused at the end for the
+  // partial dK, dV that waves 4-7 hand over (4 x 128 rows x 64 lanes fp32)
+  constexpr int HANDOFF = 4 * 128 * 64 * 4;
+  __shared__ __align__(256) char smem[2 * STAGE > HANDOFF ? 2 * STAGE : HANDOFF];
   lds_t *const L = LDS_AS(char, smem);
   const int kblk = (int)blockIdx.x / p.H, h = (int)blockIdx.x % p.H;  // earliest (heaviest) keys first
   const int kvh = h / p.G;
@@ -658,7 +624,6 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
   const int k0w = kblk * KV_ROWS + pw * 32;
   const int myk = k0w + l32;
   const float sc = p.scale * LOG2E;
-  const int64_t hbase = ((int64_t)b * p.H + h) * HD * p.S;
 
   QV kf[8];
   bf16x8_v vf[8];
@@ -672,50 +637,42 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) dk[i] = dv[i] = zero16();
 
-  // 64 runs per block: wave w brings runs 8 (w & 1) .. + 7 of tile w >> 1
-  // (Q (QE), dO, Q^T, dO^T); the last wave also brings lse and D (64 floats each)
-  const int tl = w >> 1;
+  // 16 NTK runs per block: wave w brings runs RPW sub .. + RPW - 1 of tile tl
+  // (Q (QE), dO, bf16 Q; with three tiles waves 6 and 7 bring none); the last
+  // wave also brings lse and D (64 floats each)
+  const int tl = SEP ? (w >> 1) : (w >> 2), sub = SEP ? (w & 1) : (w & 3);
+  const bool brings = tl < NTK;  // wave-uniform
   const i32x4_v rs = tl == 0 ? make_rsrc(p.q, p.qkv_bytes)
                    : tl == 1 ? make_rsrc(p.dout, p.o_bytes)
-                   : tl == 2 ? make_rsrc(p.qt, p.t_bytes)
-                             : make_rsrc(p.dot, p.t_bytes);
+                             : make_rsrc(p.qb, p.qb_bytes);
   const i32x4_v rl = make_rsrc(p.lse, p.lse_bytes);
   const i32x4_v rd = make_rsrc(p.D, p.lse_bytes);
   const int64_t sbase = ((int64_t)b * p.H + h) * p.S;
-  // Byte offset of run t (0..15) of block qbi = ublk * qbi + urun * t + lbase
-  // + lcol[t & 3]: the same element addresses as tile_run / tt_run, with one
-  // per-lane base and four per-lane column variants (row tiles: the swizzle of
-  // row 4t + lane/16 depends on t & 3; transposed tiles: on t & 1).
-  uint32_t lbase, lcol[4], urun, ublk, u0;
-  if (tl < 2) {
-    const int64_t ld = tl == 0 ? p.ld_qkv : p.ld_o;
-    lbase = (uint32_t)(((row0 + (lane >> 4)) * ld + h * HD) * 2);
-#pragma unroll
-    for (int v = 0; v < 4; ++v) lcol[v] = (uint32_t)(16 * ((lane & 15) ^ ((((lane >> 4) & 3) << 2) | v)));
-    urun = (uint32_t)(4 * ld * 2);
-    ublk = (uint32_t)(KB * ld * 2);
-  } else {
-    lbase = (uint32_t)((hbase + (int64_t)(lane >> 3) * p.S) * 2);
-#pragma unroll
-    for (int v = 0; v < 4; ++v) lcol[v] = (uint32_t)(16 * ((lane & 7) ^ ((4 * (v & 1) + (lane >> 4)) & 7)));
-    urun = (uint32_t)(8 * p.S * 2);
-    ublk = (uint32_t)(KB * 2);
-  }
-  u0 = urun * (uint32_t)(8 * (w & 1));
+  // Byte offset of run t of block qbi = ublk * qbi + urun * t + lbase +
+  // lcol[t & 3]: the same element addresses as tile_run, with one per-lane
+  // base and four per-lane column variants (the swizzle of row 4t + lane/16
+  // depends on t & 3; RPW sub is a multiple of 4)
+  const int64_t ld = tl == 0 ? p.ld_qkv : tl == 1 ? p.ld_o : p.ld_qb;
+  const uint32_t lbase = (uint32_t)(((row0 + (lane >> 4)) * ld + h * HD) * 2);
+  const uint32_t urun = (uint32_t)(4 * ld * 2), ublk = (uint32_t)(KB * ld * 2);
+  const uint32_t u0 = urun * (uint32_t)(RPW * sub);
   // per-lane part of the offsets; the run and block parts go in the scalar
   // offset (four registers instead of eight held across the block loop)
   uint32_t vo[4];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) vo[v] = lbase + lcol[v];
+  for (int v = 0; v < 4; ++v)
+    vo[v] = lbase + (uint32_t)(16 * ((lane & 15) ^ ((((lane >> 4) & 3) << 2) | v)));
   auto load = [&](int qbi, lds_t *st) {
-    lds_t *const tile = st + tl * TILE + (w & 1) * 8 * 1024;
+    lds_t *const tile = st + tl * TILE + sub * RPW * 1024;
     const uint32_t ub = ublk * (uint32_t)qbi + u0;
+    if (brings) {
 #pragma unroll
-    for (int t = 0; t < 8; ++t) dma16s(rs, tile + t * 1024, vo[t & 3], ub + urun * t);
+      for (int t = 0; t < RPW; ++t) dma16s(rs, tile + t * 1024, vo[t & 3], ub + urun * t);
+    }
     if (w == NT / 64 - 1) {
       const uint32_t off = (uint32_t)((sbase + (int64_t)qbi * KB + lane) * 4);
-      dma4(rl, st + 4 * TILE, off);
-      dma4(rd, st + 4 * TILE + 256, off);
+      dma4(rl, st + NTK * TILE, off);
+      dma4(rd, st + NTK * TILE + 256, off);
     }
   };
   const int qfirst = kblk * KV_ROWS / KB, nqblk = p.S / KB;
@@ -726,7 +683,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
     const int cur_i = (qbi - qfirst) & 1;
     const lds_t *cur = L + cur_i * STAGE;
     if (qbi + 1 < nqblk) load(qbi + 1, L + (cur_i ^ 1) * STAGE);
-    const float *sL = reinterpret_cast<const float *>(smem + cur_i * STAGE + 4 * TILE) + 32 * hq;
+    const float *sL = reinterpret_cast<const float *>(smem + cur_i * STAGE + NTK * TILE) + 32 * hq;
     const int q0 = qbi * KB + 32 * hq;  // this wave's 32 queries
     if (q0 + 31 >= k0w) {
       f32x16_v s = zero16(), dp = zero16();
@@ -792,18 +749,23 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
       const bf16x8_v pf[2] = {pack8<__bf16>(s, 0), pack8<__bf16>(s, 8)};
       const bf16x8_v sf[2] = {pack8<__bf16>(dp, 0), pack8<__bf16>(dp, 8)};
       __builtin_amdgcn_sched_barrier(0);
-      const lds_t *qt = cur + 2 * TILE, *dot = cur + 3 * TILE;
+      // dO^T and Q^T fragments: transposing reads of the dO and bf16 Q rows
+      // in P's query order (queries 32 hq + 16 t + 4 hf + [0, 4), + 8 + [0, 4))
+      uint32_t cl = cols_lane(lane);
+      asm volatile("" : "+v"(cl));  // recomputed each block, not held across the loop
+      const uint32_t aq = (uint32_t)(uintptr_t)cur + cl + (SEP ? 2 * TILE : 0), ao = aq + (SEP ? -TILE : TILE);
       // steps n = 4 t + i; the dO^T and Q^T fragments of step n + 1 are read
       // while step n multiplies
       bf16x8_v fo[2], fq[2];
-      fo[0] = frag_t<bf16x8_v>(dot, 0, hq, 0, lane);
-      fq[0] = frag_t<bf16x8_v>(qt, 0, hq, 0, lane);
+      fo[0] = frag_cols_x<bf16x8_v>(ao, 0, 32 * hq);
+      fq[0] = frag_cols_x<bf16x8_v>(aq, 0, 32 * hq);
 #pragma unroll
       for (int n = 0; n < 8; ++n) {
         const int t = n >> 2, i = n & 3;
         if (n + 1 < 8) {
-          fo[(n + 1) & 1] = frag_t<bf16x8_v>(dot, ((n + 1) & 3) * 32, hq, (n + 1) >> 2, lane);
-          fq[(n + 1) & 1] = frag_t<bf16x8_v>(qt, ((n + 1) & 3) * 32, hq, (n + 1) >> 2, lane);
+          const int i1 = (n + 1) & 3, k1 = 32 * hq + 16 * ((n + 1) >> 2);
+          fo[(n + 1) & 1] = frag_cols_x<bf16x8_v>(ao, i1, k1);
+          fq[(n + 1) & 1] = frag_cols_x<bf16x8_v>(aq, i1, k1);
         }
         __builtin_amdgcn_sched_barrier(0);
         dv[i] = mfma(fo[n & 1], pf[t], dv[i]);
@@ -1063,18 +1025,21 @@ AttnP mc_params(const lc_attn_args &a) {
   const int64_t rows = (int64_t)a.B * a.S, d = (int64_t)a.H * HD;
   const int Hkv = kv_of(a);
   const int64_t dkv = (int64_t)Hkv * HD;
-  // scratch: D (fp32 [B, H, S], 256-byte aligned), v rows (bf16 [rows, dkv]),
-  // the transposes of q ([B][H][128][S]), k ([B][Hkv][128][S]) and dO
-  // ([B][H][128][S]), then (grouped-query attention) the fp32 dk, dv shares
+  // scratch: D (fp32 [B, H, S], 256-byte aligned), then for fp16 inputs bf16
+  // rows of v ([rows, dkv]), q ([rows, d]) and k ([rows, dkv]), then
+  // (grouped-query attention) the fp32 dk, dv shares
   const size_t dbytes = ((size_t)rows * a.H * sizeof(float) + 255) / 256 * 256;
   __bf16 *const cp = a.scratch ? reinterpret_cast<__bf16 *>(static_cast<char *>(a.scratch) + dbytes) : nullptr;
   const bool bf = a.dtype == LC_BF16;
-  p.vb_w = cp;
-  p.vb = bf ? static_cast<const __bf16 *>(a.v) : cp;
+  p.vb_w = bf ? nullptr : cp;
+  p.qb_w = bf || !cp ? nullptr : cp + rows * dkv;
+  p.kb_w = bf || !cp ? nullptr : cp + rows * (dkv + d);
+  p.vb = bf ? static_cast<const __bf16 *>(a.v) : p.vb_w;
+  p.qb = bf ? static_cast<const __bf16 *>(a.q) : p.qb_w;
+  p.kb = bf ? static_cast<const __bf16 *>(a.k) : p.kb_w;
   p.ld_vb = bf ? a.ld_qkv : dkv;
-  p.qt = cp ? cp + rows * dkv : nullptr;
-  p.kt = cp ? cp + rows * (dkv + d) : nullptr;
-  p.dot = cp ? cp + rows * (2 * dkv + d) : nullptr;
+  p.ld_qb = bf ? a.ld_qkv : d;
+  p.ld_kb = bf ? a.ld_qkv : dkv;
   if (a.scratch && Hkv < a.H) {
     char *sh = static_cast<char *>(a.scratch) + attn_share_offset(a.B, a.S, a.H, Hkv);
     p.dkp = reinterpret_cast<float *>(sh);
@@ -1088,8 +1053,8 @@ AttnP mc_params(const lc_attn_args &a) {
   p.qkv_bytes = (uint32_t)(((rows - 1) * a.ld_qkv + d) * 2);
   p.o_bytes = (uint32_t)(((rows - 1) * a.ld_o + d) * 2);
   p.vb_bytes = (uint32_t)(((rows - 1) * p.ld_vb + dkv) * 2);
-  p.t_bytes = (uint32_t)(rows * d * 2);
-  p.kt_bytes = (uint32_t)(rows * dkv * 2);
+  p.qb_bytes = (uint32_t)(((rows - 1) * p.ld_qb + d) * 2);
+  p.kb_bytes = (uint32_t)(((rows - 1) * p.ld_kb + dkv) * 2);
   p.lse_bytes = (uint32_t)(rows * a.H * sizeof(float));
   p.S = a.S;
   p.H = a.H;
@@ -1147,10 +1112,15 @@ template <typename QE>
 lc_status bwd_mc(const lc_attn_args &a, hipStream_t s) {
   LC_TRY(check_extents(a));
   const AttnP p = mc_params(a);
-  hipLaunchKernelGGL(attn_bwd_prep_kernel<QE>, dim3((unsigned)(a.S / 64), a.H, a.B), dim3(256), 0,
-                     s, p);
-  LC_TRY(check_launch("attn_bwd_prep_kernel"));
+  if constexpr (!std::is_same<QE, __bf16>::value) {
+    const int64_t chunks = (int64_t)a.B * a.S * (a.H + 2 * p.Hkv) * HD / 8;
+    hipLaunchKernelGGL(attn_bwd_copy_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, p);
+    LC_TRY(check_launch("attn_bwd_copy_kernel"));
+  }
+  // dQ first: it writes D, which the dK/dV kernel reads
   const unsigned nb = (unsigned)((a.S + ROWS - 1) / ROWS);
+  hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(nb * (unsigned)(a.H * a.B)), dim3(NT), 0, s, p);
+  LC_TRY(check_launch("attn_bwd_dq_kernel"));
   hipLaunchKernelGGL(attn_bwd_dkdv_kernel<QE>, dim3((unsigned)(a.S / KV_ROWS * a.H), a.B), dim3(NT), 0,
                      s, p);
   LC_TRY(check_launch("attn_bwd_dkdv_kernel"));
@@ -1159,8 +1129,7 @@ lc_status bwd_mc(const lc_attn_args &a, hipStream_t s) {
     hipLaunchKernelGGL(attn_gqa_sum_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s, p);
     LC_TRY(check_launch("attn_gqa_sum_kernel"));
   }
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<QE>, dim3(nb * (unsigned)(a.H * a.B)), dim3(NT), 0, s, p);
-  return check_launch("attn_bwd_dq_kernel");
+  return LC_OK;
 }
 
 }  // namespace

@@ -16,18 +16,27 @@
 //
 // Operand tiles go from HBM straight into LDS (buffer_load_dwordx4 ... lds:
 // lane l of a wave's load fills bytes [16 l, 16 l + 16) of a 1 KiB LDS run),
-// so no register staging is needed; each lane picks the global 16 bytes that
-// belong at its LDS slot, which is how the tiles are swizzled. Buffer
+// so no register staging is needed; the lanes of a load read global memory in
+// address order, and padding between runs keeps fragment reads free of LDS
+// bank conflicts. Buffer
 // descriptors make out-of-range lanes (matrix edges, K tail) read zeros.
 //   k-major operand: LDS rows of 64 k (128 B, one full cache line of the
-//     operand row per load lane group); 16-byte chunk c of row r sits at
-//     chunk c ^ ((r >> 1) & 7). A fragment (32 rows at one k chunk, 16 bytes
-//     per lane) is one ds_read_b128, and every 16 lanes touch all 64 banks
-//     once. (Rows of 32 k, i.e. half cache lines per load, cost a third of
-//     the throughput of the global->LDS path.)
+//     operand row per 8-lane group, lanes in address order). Load run q
+//     (0..31) holds tile rows q, q + 32, ..., q + 224, and runs sit 1040 bytes
+//     apart, so tile row 32 p + q is at q * 1040 + 128 p. A fragment (32 rows
+//     at one k chunk, 16 bytes per lane) is one ds_read_b128 of 32 runs at one
+//     position, and the 16-byte run padding makes every 16 lanes touch all 64
+//     banks once. (An earlier layout kept runs of 8 consecutive rows and
+//     XOR-swizzled the 16-byte chunks of each cache line across the lanes of
+//     a load, and the m/n-major one below XOR-swizzled 64-byte blocks: both
+//     conflict-free too, but every product ran 3-6% slower with them. Rows of
+//     32 k, i.e. half cache lines per load, cost a third of the throughput of
+//     the global->LDS path.)
 //   m/n-major operand (a weight read as dX = dY W, both operands of a weight
-//     gradient dW = dY^T X): LDS rows of one k and 256 m (512 B), chunk c of
-//     row k at chunk c ^ (4 (k & 3)). The fragment is read with the CDNA4
+//     gradient dW = dY^T X): LDS rows of one k and 256 m (512 B, lanes in
+//     address order); run q holds k rows q and q + 32, runs sit 1088 bytes
+//     apart, so the four k rows one transposing read spans fall on different
+//     banks. The fragment is read with the CDNA4
 //     transposing load ds_read_b64_tr_b16: in each group of 16 lanes, lane j
 //     receives element j % 4 of the 8 bytes addressed by lane 4e + j / 4 as its
 //     element e, so lanes addressing four consecutive k rows at four 4-element
@@ -54,7 +63,11 @@ constexpr int KS = 64;             // k per stage
 constexpr int NT = 512;            // threads per workgroup (8 waves)
 constexpr int WM = 64, WN = 128;   // wave tile
 constexpr int FM = WM / 32, FN = WN / 32;
-constexpr int OPND_BYTES = BM * KS * 2;       // one operand's stage in LDS (32 KiB)
+// LDS-DMA runs: one 1 KiB load per wave instruction, with 16 bytes of padding
+// after each run of a k-major operand and 64 after each run of an m/n-major one.
+constexpr int RUN_K = 1024 + 16;
+constexpr int RUN_MN = 1024 + 64;
+constexpr int OPND_BYTES = 32 * RUN_MN;       // one operand's stage in LDS (32 runs)
 constexpr int STAGE_BYTES = 2 * OPND_BYTES;   // A | B
 constexpr uint32_t OOB = 0x80000000u;    // buffer offset beyond every operand: reads 0
 
@@ -114,20 +127,17 @@ __device__ __forceinline__ void dma16(i32x4_v rs, lds_t *lds, uint32_t off) {
 
 // One wave's share of an operand's loads: 8 of the 32 1-KiB LDS runs of a
 // 256 x 64 stage (the four waves of a group load one operand).
-//   k-major: run q = rows 8q .. 8q+7; lane l -> row 8q + l/8, LDS chunk l%8
-//     holding global k chunk (l%8) ^ ((row >> 1) & 7).
+//   k-major: run q = tile rows q + 32 p (p = 0..7); lane l -> position l/8,
+//     global k chunk l%8.
 //     ROWMAP 0: tile row r -> operand row base + r (valid below lim)
 //     ROWMAP 1 (SwiGLU B rows): tile row r -> gate row ob + (r>>7)*64 + (r&63)
 //       for (r&127) < 64, else up row lim + ob + (r>>7)*64 + (r&63); valid
 //       while the output column ob + (r>>7)*64 + (r&63) < lim.
-//   m/n-major: run q = k rows 2q, 2q+1; lane l -> k row 2q + l/32, LDS chunk
-//     l%32 holding global columns 8 ((l%32) ^ (4 (krow & 3))) .. +7.
-// Run t of wave w is q = 8w + t: consecutive runs are a fixed byte distance
-// apart in the operand, and the swizzle term of a run depends only on the
-// parity of t ((row >> 1) & 7 = (l >> 4) + 4 (t & 1) for k-major runs,
-// krow & 3 = (2t + l/32) & 3 for m/n-major ones). The per-lane state is a row
-// offset, the two parity variants of the in-row offset (and, k-major, of the
-// lane's k position), a validity mask and a k position; everything else is
+//   m/n-major: run q = k rows q and q + 32; lane l -> k row q + 32 (l/32),
+//     global columns 8 (l%32) .. +7.
+// Run t of wave w is q = 8w + t: consecutive runs are one row (k-major) or one
+// k row (m/n-major) apart in the operand. The per-lane state is a row offset,
+// an in-row offset, a validity mask and a k position; everything else is
 // wave-uniform.
 template <bool KMAJ, int ROWMAP>
 struct Stream {
@@ -136,44 +146,39 @@ struct Stream {
   uint32_t run;      // byte distance between consecutive runs
   uint32_t kb;       // bytes per unit of k
   uint32_t rows;     // bit t set when run t's row / columns are inside the operand
-  int kl[2];         // k-major: first k of this lane's chunk (even / odd runs);
-                     // m/n-major: k row of run 0 (both entries)
+  int kl[2];         // k-major: first k of this lane's chunk; m/n-major: k row
+                     // of run 0 (both entries equal)
 
   __device__ __forceinline__ void init(int64_t ld, int base_row, int lim, int wave, int lane) {
     if constexpr (KMAJ) {
-      const int sw = lane >> 4;  // (row >> 1) & 7 of even runs; odd runs add 4
-      kl[0] = 8 * ((lane & 7) ^ sw);
-      kl[1] = 8 * ((lane & 7) ^ (sw + 4));
+      const int pos = lane >> 3;  // the lane's row position inside each run
+      kl[0] = kl[1] = 8 * (lane & 7);
       int grow0, oc0;
       if constexpr (ROWMAP == 0) {
-        grow0 = base_row + 64 * wave + (lane >> 3);
+        grow0 = base_row + 8 * wave + 32 * pos;
         oc0 = grow0;
       } else {
-        // tile rows 64 w .. 64 w + 63: gate rows for even w, up rows for odd w
-        oc0 = base_row + (wave >> 1) * 64 + (lane >> 3);
-        grow0 = (wave & 1) ? lim + oc0 : oc0;
+        // tile row r = q + 32 pos: a gate row while (pos & 2) == 0, else an up
+        // row, of output column base_row + (pos >> 2) 64 + 32 (pos & 1) + q
+        oc0 = base_row + (pos >> 2) * 64 + 32 * (pos & 1) + 8 * wave;
+        grow0 = (pos & 2) ? lim + oc0 : oc0;
       }
       rows = 0;
 #pragma unroll
-      for (int t = 0; t < 8; ++t) rows |= (oc0 + 8 * t < lim ? 1u : 0u) << t;
+      for (int t = 0; t < 8; ++t) rows |= (oc0 + t < lim ? 1u : 0u) << t;
       base = rows ? (uint32_t)((int64_t)grow0 * ld * 2) : 0u;
-      col[0] = (uint32_t)(kl[0] * 2);
-      col[1] = (uint32_t)(kl[1] * 2);
-      run = (uint32_t)(8 * ld * 2);
+      col[0] = col[1] = (uint32_t)(kl[0] * 2);
+      run = (uint32_t)(ld * 2);
       kb = 2;
     } else {
       static_assert(ROWMAP == 0, "row remap needs a k-major operand");
-      const int kr0 = 16 * wave + (lane >> 5);        // k row of run 0; kr0 & 3 == lane >> 5
-      const int c0 = (lane & 31) ^ (4 * (lane >> 5));  // odd runs: c0 ^ 8
-      const int gm0 = base_row + 8 * c0, gm1 = base_row + 8 * (c0 ^ 8);
+      const int kr0 = 8 * wave + 32 * (lane >> 5);  // k row of run 0
+      const int gm = base_row + 8 * (lane & 31);    // first of the lane's 8 columns
       kl[0] = kl[1] = kr0;
-      rows = 0;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) rows |= (((t & 1) ? gm1 : gm0) < lim ? 1u : 0u) << t;
+      rows = gm < lim ? 0xFFu : 0u;
       base = (uint32_t)((int64_t)kr0 * ld * 2);
-      col[0] = gm0 < lim ? (uint32_t)(gm0 * 2) : 0u;
-      col[1] = gm1 < lim ? (uint32_t)(gm1 * 2) : 0u;
-      run = (uint32_t)(2 * ld * 2);
+      col[0] = col[1] = gm < lim ? (uint32_t)(gm * 2) : 0u;
+      run = (uint32_t)(ld * 2);
       kb = (uint32_t)(ld * 2);
     }
   }
@@ -184,9 +189,9 @@ struct Stream {
     for (int t = 0; t < 8; ++t) {
       bool ok = (rows >> t) & 1u;
       if constexpr (KMAJ) ok = ok && k0 + kl[t & 1] < K;
-      else ok = ok && k0 + kl[0] + 2 * t < K;
+      else ok = ok && k0 + kl[0] + t < K;
       const uint32_t off = ok ? base + t * run + col[t & 1] + (uint32_t)k0 * kb : OOB;
-      dma16(rs, lds + (8 * wave + t) * 1024, off);
+      dma16(rs, lds + (8 * wave + t) * (KMAJ ? RUN_K : RUN_MN), off);
     }
   }
 };
@@ -196,17 +201,17 @@ struct Stream {
 template <bool KMAJ>
 __device__ __forceinline__ bf16x8_v frag(const lds_t *t, int row0, int s, int lane) {
   if constexpr (KMAJ) {
-    const int row = row0 + (lane & 31);
+    // tile row row0 + i (row0 a multiple of 32) is position row0 / 32 of run i
     const int c = 2 * s + (lane >> 5);
-    return *reinterpret_cast<const lds_v8 *>(t + row * 128 + ((c ^ ((row >> 1) & 7)) << 4));
+    return *reinterpret_cast<const lds_v8 *>(t + (lane & 31) * RUN_K + (row0 >> 5) * 128 + c * 16);
   } else {
+    // k row k is position k / 32 of run k % 32
     const int i16 = lane & 15, g = lane >> 4;
     const int m = row0 + 16 * (g & 1) + 4 * (i16 & 3);
     const int k = 16 * s + 8 * (g >> 1) + (i16 >> 2);
-    const int cb = ((m >> 3) ^ (4 * (i16 >> 2))) << 4;  // k & 3 == i16 >> 2
-    const lds_t *p0 = t + k * 512 + cb + (m & 7) * 2;
+    const lds_t *p0 = t + (k & 31) * RUN_MN + (k >> 5) * 512 + m * 2;
     const s16x4_v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(p0));
-    const s16x4_v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(p0 + 4 * 512));
+    const s16x4_v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(p0 + 4 * RUN_MN));
     const s16x4_v v[2] = {lo, hi};
     return __builtin_bit_cast(bf16x8_v, v);
   }

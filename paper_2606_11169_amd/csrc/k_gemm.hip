@@ -125,6 +125,18 @@ __device__ __forceinline__ void dma16(i32x4_v rs, lds_t *lds, uint32_t off) {
                : "memory", "m0");
 }
 
+// The same with a wave-uniform part of the offset in the instruction's scalar
+// offset. The hardware checks only the per-lane offset against the buffer's
+// size, so callers use it where every lane's whole offset is inside the
+// operand or the lane's own offset is OOB.
+__device__ __forceinline__ void dma16s(i32x4_v rs, lds_t *lds, uint32_t voff, uint32_t soff) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t) reinterpret_cast<uintptr_t>(lds));
+  asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voff), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(soff)), "s"(m0)
+               : "memory", "m0");
+}
+
 // One wave's share of an operand's loads: 8 of the 32 1-KiB LDS runs of a
 // 256 x 64 stage (the four waves of a group load one operand).
 //   k-major: run q = tile rows q + 32 p (p = 0..7); lane l -> position l/8,
@@ -183,16 +195,25 @@ struct Stream {
     }
   }
 
-  // the wave's 8 runs of the stage starting at k0, into `lds` (the operand's stage)
+  // each run's per-lane byte offset at k = k0 (OOB for lanes outside the
+  // operand's rows or columns); valid for stages that end at or before K
+  __device__ __forceinline__ void offsets(uint32_t vo[8], int k0) const {
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      vo[t] = (rows >> t) & 1u ? base + t * run + col[t & 1] + (uint32_t)k0 * kb : OOB;
+  }
+  // run t of the wave's 8 runs of the stage starting at k0, into `lds` (the
+  // operand's stage), every lane checked against K
+  __device__ __forceinline__ void load1(i32x4_v rs, lds_t *lds, int wave, int k0, int K, int t) const {
+    bool ok = (rows >> t) & 1u;
+    if constexpr (KMAJ) ok = ok && k0 + kl[t & 1] < K;
+    else ok = ok && k0 + kl[0] + t < K;
+    const uint32_t off = ok ? base + t * run + col[t & 1] + (uint32_t)k0 * kb : OOB;
+    dma16(rs, lds + (8 * wave + t) * (KMAJ ? RUN_K : RUN_MN), off);
+  }
   __device__ __forceinline__ void load(i32x4_v rs, lds_t *lds, int wave, int k0, int K) const {
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      bool ok = (rows >> t) & 1u;
-      if constexpr (KMAJ) ok = ok && k0 + kl[t & 1] < K;
-      else ok = ok && k0 + kl[0] + t < K;
-      const uint32_t off = ok ? base + t * run + col[t & 1] + (uint32_t)k0 * kb : OOB;
-      dma16(rs, lds + (8 * wave + t) * (KMAJ ? RUN_K : RUN_MN), off);
-    }
+    for (int t = 0; t < 8; ++t) load1(rs, lds, wave, k0, K, t);
   }
 };
 
@@ -299,10 +320,28 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   Stream<B_K, SWI ? 1 : 0> sb_;
   if (grp == 0) sa_.init(p.lda, m0, m_lim, w4, lane);
   else sb_.init(p.ldb, n0, p.N, w4, lane);
+  // Full stages use offsets computed once: run t's per-lane offset at kbeg,
+  // plus the stage's k advance in the scalar offset (the same code for both
+  // groups). A last stage that ends past K takes the per-lane K check.
+  uint32_t vo[8];
+  if (grp == 0) sa_.offsets(vo, kbeg);
+  else sb_.offsets(vo, kbeg);
+  const bool gk = grp == 0 ? A_K : B_K;
+  const uint32_t kbw = gk ? 2u : (uint32_t)((grp == 0 ? p.lda : p.ldb) * 2);
+  const int runb = gk ? RUN_K : RUN_MN;
+  lds_t *const dst0 = R0 + grp * OPND_BYTES + 8 * w4 * runb;
+  const bool ragged = (kend - kbeg) % KS != 0;
   auto load = [&](int st) {  // this group's operand of stage st
-    lds_t *stage = R0 + (st & 1) * STAGE_BYTES;
-    if (grp == 0) sa_.load(rs, stage, w4, kbeg + st * KS, kend);
-    else sb_.load(rs, stage + OPND_BYTES, w4, kbeg + st * KS, kend);
+    if (ragged && st == ns - 1) {
+      lds_t *stage = R0 + (st & 1) * STAGE_BYTES;
+      if (grp == 0) sa_.load(rs, stage, w4, kbeg + st * KS, kend);
+      else sb_.load(rs, stage + OPND_BYTES, w4, kbeg + st * KS, kend);
+      return;
+    }
+    lds_t *d = dst0 + (st & 1) * STAGE_BYTES;
+    const uint32_t so = (uint32_t)(st * KS) * kbw;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) dma16s(rs, d + t * runb, vo[t], so);
   };
 
   typedef bf16x8_v FragA[FM];

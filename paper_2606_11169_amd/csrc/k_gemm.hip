@@ -412,9 +412,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   typedef __attribute__((ext_vector_type(4))) float f32x4_t;
   typedef __attribute__((address_space(3))) f32x4_t lds_f4;
   const int ncol0 = n0 + wn * WN;  // first of the wave's 128 accumulator columns (non-SwiGLU)
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int mrow0 = m0 + wm * WM + i * 32;
+  // 32-row block i of the wave's results into its LDS staging area
+  auto stage_block = [&](int i) {
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -423,111 +422,146 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
         const f32x4_t w = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
         *reinterpret_cast<lds_f4 *>(E + frow * 512 + ((c ^ (frow & 15)) << 4)) = w;
       }
-    auto chunk = [&](int r, int c) -> float4 {
-      const f32x4_t v = *reinterpret_cast<const lds_f4 *>(E + r * 512 + ((c ^ (r & 15)) << 4));
-      return make_float4(v[0], v[1], v[2], v[3]);
-    };
-    if constexpr (EPI == LC_EPI_ROPE || EPI == LC_EPI_SWIGLU) {
-      // lane: row 4 s + lane / 16, column quads q and q + 16 (columns 4q and 64 + 4q)
-      const int q = lane & 15;
+  };
+  auto chunk = [&](int r, int c) -> float4 {
+    const f32x4_t v = *reinterpret_cast<const lds_f4 *>(E + r * 512 + ((c ^ (r & 15)) << 4));
+    return make_float4(v[0], v[1], v[2], v[3]);
+  };
+  if constexpr (EPI == LC_EPI_ROPE || EPI == LC_EPI_SWIGLU) {
 #pragma unroll
-      for (int s0 = 0; s0 < 8; s0 += 4) {
-        float4 x1[4], x2[4], cs[4], sn[4];
+    for (int i = 0; i < FM; ++i) {
+      const int mrow0 = m0 + wm * WM + i * 32;
+      stage_block(i);
+      {
+        // lane: row 4 s + lane / 16, column quads q and q + 16 (columns 4q and 64 + 4q)
+        const int q = lane & 15;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int rl = 4 * (s0 + u) + (lane >> 4);
-          x1[u] = chunk(rl, q);
-          x2[u] = chunk(rl, q + 16);
-          if constexpr (EPI == LC_EPI_ROPE) {
-            const int m = min(mrow0 + rl, m_lim - 1);
-            const int pos = m % p.rope_seq;
-            cs[u] = *reinterpret_cast<const float4 *>(p.rcos + (int64_t)pos * 64 + 4 * q);
-            sn[u] = *reinterpret_cast<const float4 *>(p.rsin + (int64_t)pos * 64 + 4 * q);
-          }
-        }
+        for (int s0 = 0; s0 < 8; s0 += 4) {
+          float4 x1[4], x2[4], cs[4], sn[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int rl = 4 * (s0 + u) + (lane >> 4);
-          const int m = mrow0 + rl;
-          if (m >= m_lim) continue;
-          float a[4] = {x1[u].x, x1[u].y, x1[u].z, x1[u].w};
-          float b[4] = {x2[u].x, x2[u].y, x2[u].z, x2[u].w};
-          if constexpr (EPI == LC_EPI_ROPE) {
-            if (ncol0 >= p.N) continue;  // head past the output (uniform)
-            if (ncol0 < p.rope_cols) {
-              const float cv[4] = {cs[u].x, cs[u].y, cs[u].z, cs[u].w};
-              const float sv[4] = {sn[u].x, sn[u].y, sn[u].z, sn[u].w};
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const float x = a[e], y = b[e];
-                a[e] = x * cv[e] - y * sv[e];
-                b[e] = x * sv[e] + y * cv[e];
-              }
+          for (int u = 0; u < 4; ++u) {
+            const int rl = 4 * (s0 + u) + (lane >> 4);
+            x1[u] = chunk(rl, q);
+            x2[u] = chunk(rl, q + 16);
+            if constexpr (EPI == LC_EPI_ROPE) {
+              const int m = min(mrow0 + rl, m_lim - 1);
+              const int pos = m % p.rope_seq;
+              cs[u] = *reinterpret_cast<const float4 *>(p.rcos + (int64_t)pos * 64 + 4 * q);
+              sn[u] = *reinterpret_cast<const float4 *>(p.rsin + (int64_t)pos * 64 + 4 * q);
             }
-            const int64_t row = (int64_t)m * p.ldc + ncol0 + 4 * q;
-            store4_dt(Cp, row, p.c_dt, a[0], a[1], a[2], a[3]);
-            store4_dt(Cp, row + 64, p.c_dt, b[0], b[1], b[2], b[3]);
-          } else {
-            const int n = n0 + wn * 64 + 4 * q;  // output column of the gate/up pair
-            if (n >= p.N) continue;
-            float act[4];
+          }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) act[e] = a[e] * sigmoidf_(a[e]) * b[e];
-            const int64_t oa = (int64_t)m * p.ld_aux + n;
-            store4_dt(p.aux0, oa, p.aux_dt, a[0], a[1], a[2], a[3]);
-            store4_dt(p.aux1, oa, p.aux_dt, b[0], b[1], b[2], b[3]);
-            store4_dt(Cp, (int64_t)m * p.ldc + n, p.c_dt, act[0], act[1], act[2], act[3]);
+          for (int u = 0; u < 4; ++u) {
+            const int rl = 4 * (s0 + u) + (lane >> 4);
+            const int m = mrow0 + rl;
+            if (m >= m_lim) continue;
+            float a[4] = {x1[u].x, x1[u].y, x1[u].z, x1[u].w};
+            float b[4] = {x2[u].x, x2[u].y, x2[u].z, x2[u].w};
+            if constexpr (EPI == LC_EPI_ROPE) {
+              if (ncol0 >= p.N) continue;  // head past the output (uniform)
+              if (ncol0 < p.rope_cols) {
+                const float cv[4] = {cs[u].x, cs[u].y, cs[u].z, cs[u].w};
+                const float sv[4] = {sn[u].x, sn[u].y, sn[u].z, sn[u].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const float x = a[e], y = b[e];
+                  a[e] = x * cv[e] - y * sv[e];
+                  b[e] = x * sv[e] + y * cv[e];
+                }
+              }
+              const int64_t row = (int64_t)m * p.ldc + ncol0 + 4 * q;
+              store4_dt(Cp, row, p.c_dt, a[0], a[1], a[2], a[3]);
+              store4_dt(Cp, row + 64, p.c_dt, b[0], b[1], b[2], b[3]);
+            } else {
+              const int n = n0 + wn * 64 + 4 * q;  // output column of the gate/up pair
+              if (n >= p.N) continue;
+              float act[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) act[e] = a[e] * sigmoidf_(a[e]) * b[e];
+              const int64_t oa = (int64_t)m * p.ld_aux + n;
+              store4_dt(p.aux0, oa, p.aux_dt, a[0], a[1], a[2], a[3]);
+              store4_dt(p.aux1, oa, p.aux_dt, b[0], b[1], b[2], b[3]);
+              store4_dt(Cp, (int64_t)m * p.ldc + n, p.c_dt, act[0], act[1], act[2], act[3]);
+            }
           }
         }
       }
-    } else {
-      // lane: row 2 s + lane / 32, column quad lane % 32
-      const int q = lane & 31;
-      const int n = ncol0 + 4 * q;
-      const int ncl = n < p.N ? n : p.N - 4;  // loads of columns past N read valid data (unused)
+    }
+  } else {
+    // lane: row 2 s + lane / 32, column quad lane % 32. Pass t covers PU
+    // values of s (2 PU rows) of 32-row block t / PPB. Epilogues that read a
+    // tensor (residual, gradient bucket, gate/up) keep two passes of loads in
+    // flight and issue pass t + 2's loads before pass t's stores: a wave's
+    // loads and stores retire in issue order, so a wait for a load then never
+    // waits for an earlier store.
+    constexpr bool LD = EPI == LC_EPI_RESIDUAL || EPI == LC_EPI_ACCUM_F32 || EPI == LC_EPI_SWIGLU_BWD;
+    constexpr int PU = 4, PPB = 16 / PU, NP = FM * PPB;
+    const int q = lane & 31;
+    const int n = ncol0 + 4 * q;
+    const int ncl = n < p.N ? n : p.N - 4;  // loads of columns past N read valid data (unused)
+    auto row_of = [&](int t, int u) { return 2 * ((t % PPB) * PU + u) + (lane >> 5); };
+    float4 xa[2][PU], ya[2][PU];
+    auto issue = [&](int t, float4 (&x)[PU], float4 (&y)[PU]) {
+      const int mrow0 = m0 + wm * WM + (t / PPB) * 32;
 #pragma unroll
-      for (int s0 = 0; s0 < 16; s0 += 8) {
-        float4 v[8], x[8], y[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int rl = 2 * (s0 + u) + (lane >> 5);
-          const int mc = min(mrow0 + rl, m_lim - 1);
-          v[u] = chunk(rl, q);
-          if constexpr (EPI == LC_EPI_RESIDUAL) x[u] = load4_dt(p.R, (int64_t)mc * p.ldr + ncl, p.r_dt);
-          if constexpr (EPI == LC_EPI_ACCUM_F32)
-            x[u] = *reinterpret_cast<const float4 *>(static_cast<const float *>(Cp) + (int64_t)mc * p.ldc + ncl);
-          if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
-            x[u] = load4_dt(p.aux0, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
-            y[u] = load4_dt(p.aux1, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
-          }
+      for (int u = 0; u < PU; ++u) {
+        const int mc = min(mrow0 + row_of(t, u), m_lim - 1);
+        if constexpr (EPI == LC_EPI_RESIDUAL) x[u] = load4_dt(p.R, (int64_t)mc * p.ldr + ncl, p.r_dt);
+        if constexpr (EPI == LC_EPI_ACCUM_F32)
+          x[u] = *reinterpret_cast<const float4 *>(static_cast<const float *>(Cp) + (int64_t)mc * p.ldc + ncl);
+        if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
+          x[u] = load4_dt(p.aux0, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
+          y[u] = load4_dt(p.aux1, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
         }
+      }
+    };
+    stage_block(0);
+    if constexpr (LD) {
+      issue(0, xa[0], ya[0]);
+      issue(1, xa[1], ya[1]);
+    }
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int rl = 2 * (s0 + u) + (lane >> 5);
-          const int m = mrow0 + rl;
-          if (m >= m_lim || n >= p.N) continue;
-          const int64_t oc = (int64_t)m * p.ldc + n;
-          float o[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-          if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
-            const float gv[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-            const float uv[4] = {y[u].x, y[u].y, y[u].z, y[u].w};
-            float dg[4], du[4];
+    for (int t = 0; t < NP; ++t) {
+      if (t > 0 && t % PPB == 0) stage_block(t / PPB);  // after pass t - 1's LDS reads
+      const int mrow0 = m0 + wm * WM + (t / PPB) * 32;
+      float4 ra[PU], rb[PU];  // pass t's results (rb: SwiGLU backward's du)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float sg = sigmoidf_(gv[e]);
-              dg[e] = o[e] * uv[e] * sg * (1.0f + gv[e] * (1.0f - sg));
-              du[e] = o[e] * gv[e] * sg;
-            }
-            store4_dt(Cp, oc, p.c_dt, dg[0], dg[1], dg[2], dg[3]);
-            store4_dt(Cp, oc + p.N, p.c_dt, du[0], du[1], du[2], du[3]);
-          } else if constexpr (EPI == LC_EPI_ACCUM_F32) {
-            *reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc) =
-                make_float4(x[u].x + o[0], x[u].y + o[1], x[u].z + o[2], x[u].w + o[3]);
-          } else if constexpr (EPI == LC_EPI_RESIDUAL) {
-            store4_dt(Cp, oc, p.c_dt, x[u].x + o[0], x[u].y + o[1], x[u].z + o[2], x[u].w + o[3]);
-          } else {
-            store4_dt(Cp, oc, p.c_dt, o[0], o[1], o[2], o[3]);
+      for (int u = 0; u < PU; ++u) {
+        const float4 v = chunk(row_of(t, u), q);
+        const float4 x = xa[t & 1][u], y = ya[t & 1][u];
+        if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
+          const float o[4] = {v.x, v.y, v.z, v.w};
+          const float gv[4] = {x.x, x.y, x.z, x.w};
+          const float uv[4] = {y.x, y.y, y.z, y.w};
+          float dg[4], du[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float sg = sigmoidf_(gv[e]);
+            dg[e] = o[e] * uv[e] * sg * (1.0f + gv[e] * (1.0f - sg));
+            du[e] = o[e] * gv[e] * sg;
           }
+          ra[u] = make_float4(dg[0], dg[1], dg[2], dg[3]);
+          rb[u] = make_float4(du[0], du[1], du[2], du[3]);
+        } else if constexpr (LD) {
+          ra[u] = make_float4(x.x + v.x, x.y + v.y, x.z + v.z, x.w + v.w);
+        } else {
+          ra[u] = v;
+        }
+      }
+      if constexpr (LD) {
+        if (t + 2 < NP) issue(t + 2, xa[t & 1], ya[t & 1]);
+      }
+#pragma unroll
+      for (int u = 0; u < PU; ++u) {
+        const int m = mrow0 + row_of(t, u);
+        if (m >= m_lim || n >= p.N) continue;
+        const int64_t oc = (int64_t)m * p.ldc + n;
+        if constexpr (EPI == LC_EPI_ACCUM_F32) {
+          *reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc) = ra[u];
+        } else {
+          store4_dt(Cp, oc, p.c_dt, ra[u].x, ra[u].y, ra[u].z, ra[u].w);
+          if constexpr (EPI == LC_EPI_SWIGLU_BWD)
+            store4_dt(Cp, oc + p.N, p.c_dt, rb[u].x, rb[u].y, rb[u].z, rb[u].w);
         }
       }
     }

@@ -7,7 +7,7 @@
 // running row maximum and row sum (online softmax) and the output in
 // registers. K and V blocks stream from HBM straight into a two-stage LDS ring
 // (buffer_load_dwordx4 ... lds, one 1 KiB run of 4 rows per wave
-// instruction). The score block is computed transposed, S^T = K Q^T, so each
+// instruction, each row's 256 bytes read in address order). The score block is computed transposed, S^T = K Q^T, so each
 // lane holds one query's scores: the row max and row sum need lane-local work
 // plus one swap with the partner lane (lane ^ 32). The output is accumulated
 // transposed, O^T += V^T P^T, so the rescale is a lane-local scalar (done
@@ -32,10 +32,14 @@
 // dq/dk is applied in the epilogues.
 //
 // Row tiles are [64 rows][128 columns] of 2-byte elements (256-byte rows of 16
-// chunks); chunk c of row r sits at chunk c ^ f(r) with
-// f(r) = ((r & 3) << 2) | ((r >> 2) & 3). A 128-bit fragment read (16
-// consecutive rows, one chunk) and a transposing read (4 consecutive rows,
-// four chunks) both touch every bank once per phase.
+// chunks) in 16 load runs 1040 bytes apart: run q holds rows f(q) + 16 p
+// (p = 0..3) with f(r) = ((r & 3) << 2) | ((r >> 2) & 3), so row r sits at
+// f(r % 16) * 1040 + (r / 16) * 256. A 128-bit fragment read (16 consecutive
+// rows, one chunk) and a transposing read (4 consecutive rows, four chunks)
+// both touch every bank once per phase, and every fragment address is a
+// per-lane base plus an immediate offset (no per-read address arithmetic). An
+// earlier layout XOR-swizzled the chunks of each row across the lanes of a
+// load, which needed an XOR and an add per transposing read.
 #include "common.hpp"
 
 #include <math.h>
@@ -57,7 +61,9 @@ constexpr float LOG2E = 1.4426950408889634f;
 // rounded to 16 bits (where they are zero anyway); 2^-inf = 0.
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 constexpr float LN2 = 0.6931471805599453f;
-constexpr int TILE = KB * HD * 2;  // 16 KiB: one [64][128] tile of 2-byte elements
+// one [64][128] tile of 2-byte elements: 16 load runs of 1 KiB, 16 bytes apart
+constexpr int RUNB = 1024 + 16;
+constexpr int TILE = 16 * RUNB;
 
 typedef __attribute__((ext_vector_type(4))) int i32x4_v;
 typedef __attribute__((ext_vector_type(4))) short s16x4_v;
@@ -76,8 +82,9 @@ __device__ __forceinline__ f32x16_v mfma(f16x8_v a, f16x8_v b, f32x16_v c) {
 }
 
 // ---------------------------------------------------------------- tiles
+// load run of tile row r (an involution on 0..15: run q holds rows swz(q) + 16 p)
 __device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
-__device__ __forceinline__ int tile_off(int r, int c) { return r * 256 + ((c ^ swz(r)) << 4); }
+__device__ __forceinline__ int tile_off(int r, int c) { return swz(r & 15) * RUNB + (r >> 4) * 256 + c * 16; }
 
 __device__ __forceinline__ i32x4_v make_rsrc(const void *base, uint32_t bytes) {
   const uint64_t a = reinterpret_cast<uint64_t>(base);
@@ -117,63 +124,53 @@ __device__ __forceinline__ void dma4(i32x4_v rs, lds_t *lds, uint32_t off) {
                : "memory", "m0");
 }
 
-// Run `run` (0..15) of a [64][128] tile: rows 4 run .. 4 run + 3 of the block
-// whose row 0 is global row `grow0` of a matrix with `ld` elements per row,
-// columns col0 .. col0 + 127.
+// Run `run` (0..15) of a [64][128] tile: rows swz(run) + 16 p (p = 0..3) of
+// the block whose row 0 is global row `grow0` of a matrix with `ld` elements
+// per row, columns col0 .. col0 + 127; each 16-lane group reads one row's 256
+// bytes in address order.
 __device__ __forceinline__ void tile_run(i32x4_v rs, lds_t *tile, int run, int64_t grow0,
                                          int64_t ld, int col0, int lane) {
-  const int r = 4 * run + (lane >> 4);
-  const int c = (lane & 15) ^ swz(r);
-  const uint32_t off = (uint32_t)(((grow0 + r) * ld + col0 + 8 * c) * 2);
-  dma16(rs, tile + run * 1024, off);
+  const int r = swz(run) + 16 * (lane >> 4);
+  const uint32_t off = (uint32_t)(((grow0 + r) * ld + col0 + 8 * (lane & 15)) * 2);
+  dma16(rs, tile + run * RUNB, off);
 }
 
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // MFMA operand of 32 tile rows row0 .. row0+31 at columns 16 s + 8 (lane / 32) + [0, 8)
+// (row0 a multiple of 32): rows_lane(lane) plus an immediate offset
+__device__ __forceinline__ uint32_t rows_lane(int lane) {
+  return (uint32_t)(swz(lane & 15) * RUNB + ((lane >> 4) & 1) * 256 + (lane >> 5) * 16);
+}
 template <typename VT>
 __device__ __forceinline__ VT frag_rows(const lds_t *t, int row0, int s, int lane) {
-  const int r = row0 + (lane & 31);
   return *reinterpret_cast<const __attribute__((address_space(3))) VT *>(
-      t + tile_off(r, 2 * s + (lane >> 5)));
+      t + rows_lane(lane) + (row0 >> 4) * 256 + 32 * s);
 }
 
 // MFMA operand of 32 tile columns col0 .. col0+31 (lane l: column col0 + l % 32)
 // whose 8 k values are tile rows c .. c+3 and c+8 .. c+11, c = kbase + 4 (lane / 32):
 // the key (or query) order of a 32 x 32 accumulator's registers 8t .. 8t+7
 // (rows 16t + 4 hf + [0, 4) and 16t + 8 + 4 hf + [0, 4)), kbase = 32 j + 16 t.
-template <typename VT>
-__device__ __forceinline__ VT frag_cols(const lds_t *t, int col0, int kbase, int lane) {
-  const int i16 = lane & 15;
-  const int r = kbase + 4 * (lane >> 5) + (i16 >> 2);
-  const int col = col0 + 16 * ((lane >> 4) & 1) + 4 * (i16 & 3);
-  const lds_t *p0 = t + tile_off(r, col >> 3) + (col & 7) * 2;
-  const lds_t *p1 = t + tile_off(r + 8, col >> 3) + (col & 7) * 2;
-  typedef __attribute__((address_space(3))) s16x4_v lds_v4;
-  const s16x4_v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)p0);
-  const s16x4_v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)p1);
-  const s16x4_v v[2] = {lo, hi};
-  return __builtin_bit_cast(VT, v);
-}
-
-// frag_cols for col0 = 32 i and kbase a multiple of 16, from `a`: the LDS
-// byte address of a 256-byte-aligned tile plus cols_lane(lane). The lane term
-// holds (lane % 16) / 4 in address bits 6-7, which column block i flips by
-// XOR; rows c + 8 .. c + 11 differ from rows c .. c + 3 by 8 rows and by
-// chunk bit 1 (address bit 5). One XOR per address, the rest immediate.
+// Two transposing reads: rows c .. c+3 sit in runs swz(c % 16 ..), 64 bytes
+// apart in the banks, and rows c+8 .. c+11 two runs further (swz(x + 8) =
+// swz(x) + 2 for x < 8), so every address is cols_lane(lane) plus an immediate.
 __device__ __forceinline__ uint32_t cols_lane(int lane) {
   const int i16 = lane & 15, hf = lane >> 5, b4 = (lane >> 4) & 1;
-  return (uint32_t)((4 * hf + (i16 >> 2)) * 256 + 64 * (i16 >> 2) +
-                    16 * ((2 * b4 + ((i16 >> 1) & 1)) ^ hf) + 8 * (i16 & 1));
+  return (uint32_t)(swz(4 * hf + (i16 >> 2)) * RUNB + (16 * b4 + 4 * (i16 & 3)) * 2);
 }
 template <typename VT>
 __device__ __forceinline__ VT frag_cols_x(uint32_t a, int i, int kbase) {
   typedef __attribute__((address_space(3))) s16x4_v lds_v4;
-  const uint32_t lo = (a ^ (64u * i)) + 256u * kbase;
-  const uint32_t hi = (a ^ (64u * i) ^ 32u) + 256u * kbase + 2048u;
+  const uint32_t lo = a + 64u * i + 16u * kbase;
   const s16x4_v v[2] = {__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(uintptr_t)lo),
-                        __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(uintptr_t)hi)};
+                        __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4 *)(uintptr_t)(lo + 2 * RUNB))};
   return __builtin_bit_cast(VT, v);
+}
+// the same from a tile pointer (kbase a multiple of 16)
+template <typename VT>
+__device__ __forceinline__ VT frag_cols(const lds_t *t, int col0, int kbase, int lane) {
+  return frag_cols_x<VT>((uint32_t)(uintptr_t)t + cols_lane(lane), col0 >> 5, kbase);
 }
 
 // max / sum of a lane's value and lane (l ^ 32)'s, in every lane
@@ -359,15 +356,26 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
           ls[2 * j + (r & 1)] += pv;
         }
       l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
-      const lds_t *vt = cur + TILE;
+      // V^T fragments of step n = 2 j + t (keys 32 j + 16 t ..) read while
+      // step n - 1 multiplies
+      const uint32_t av = (uint32_t)(uintptr_t)(cur + TILE) + cols_lane(lane);
+      QV vfr[2][4];
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int i = 0; i < 4; ++i) vfr[0][i] = frag_cols_x<QV>(av, i, 0);
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const QV pf = pack8<QE>(s[j], 8 * t);
+      for (int n = 0; n < 4; ++n) {
+        const int j = n >> 1, t = n & 1;
+        if (n + 1 < 4) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o[i] = mfma(frag_cols<QV>(vt, i * 32, j * 32 + 16 * t, lane), pf, o[i]);
+          for (int i = 0; i < 4; ++i)
+            vfr[(n + 1) & 1][i] = frag_cols_x<QV>(av, i, 32 * ((n + 1) >> 1) + 16 * ((n + 1) & 1));
         }
+        const QV pf = pack8<QE>(s[j], 8 * t);
+        __builtin_amdgcn_sched_barrier(0);  // (keeps the reads ahead of the products)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = mfma(vfr[n & 1][i], pf, o[i]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     wait_vm0();
     __syncthreads();
@@ -455,7 +463,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   typedef typename V8<QE>::type QV;
   constexpr bool SEP = !std::is_same<QE, __bf16>::value;  // separate bf16 K tile
   constexpr int NTQ = SEP ? 3 : 2;                          // tiles per stage
-  __shared__ __align__(256) char smem[2 * NTQ * TILE];      // 256-byte aligned (frag_cols_x)
+  __shared__ __align__(16) char smem[2 * NTQ * TILE];
   lds_t *const L = LDS_AS(char, smem);
   const int nqb = (p.S + ROWS - 1) / ROWS;
   int qb, h, b;
@@ -648,26 +656,20 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
   const i32x4_v rl = make_rsrc(p.lse, p.lse_bytes);
   const i32x4_v rd = make_rsrc(p.D, p.lse_bytes);
   const int64_t sbase = ((int64_t)b * p.H + h) * p.S;
-  // Byte offset of run t of block qbi = ublk * qbi + urun * t + lbase +
-  // lcol[t & 3]: the same element addresses as tile_run, with one per-lane
-  // base and four per-lane column variants (the swizzle of row 4t + lane/16
-  // depends on t & 3; RPW sub is a multiple of 4)
+  // Byte offset of run q of block qbi: the lane's row 16 (lane / 16) and
+  // column chunk lane % 16 (one per-lane offset), plus the block's and the
+  // run's first row swz(q) in the instruction's scalar offset
   const int64_t ld = tl == 0 ? p.ld_qkv : tl == 1 ? p.ld_o : p.ld_qb;
-  const uint32_t lbase = (uint32_t)(((row0 + (lane >> 4)) * ld + h * HD) * 2);
-  const uint32_t urun = (uint32_t)(4 * ld * 2), ublk = (uint32_t)(KB * ld * 2);
-  const uint32_t u0 = urun * (uint32_t)(RPW * sub);
-  // per-lane part of the offsets; the run and block parts go in the scalar
-  // offset (four registers instead of eight held across the block loop)
-  uint32_t vo[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v)
-    vo[v] = lbase + (uint32_t)(16 * ((lane & 15) ^ ((((lane >> 4) & 3) << 2) | v)));
+  const uint32_t vo = (uint32_t)(((row0 + 16 * (lane >> 4)) * ld + h * HD + 8 * (lane & 15)) * 2);
+  const uint32_t urow = (uint32_t)(ld * 2), ublk = (uint32_t)(KB * ld * 2);
   auto load = [&](int qbi, lds_t *st) {
-    lds_t *const tile = st + tl * TILE + sub * RPW * 1024;
-    const uint32_t ub = ublk * (uint32_t)qbi + u0;
+    lds_t *const tile = st + tl * TILE;
     if (brings) {
 #pragma unroll
-      for (int t = 0; t < RPW; ++t) dma16s(rs, tile + t * 1024, vo[t & 3], ub + urun * t);
+      for (int t = 0; t < RPW; ++t) {
+        const int q = RPW * sub + t;
+        dma16s(rs, tile + q * RUNB, vo, ublk * (uint32_t)qbi + urow * (uint32_t)swz(q));
+      }
     }
     if (w == NT / 64 - 1) {
       const uint32_t off = (uint32_t)((sbase + (int64_t)qbi * KB + lane) * 4);
@@ -687,22 +689,19 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
     const int q0 = qbi * KB + 32 * hq;  // this wave's 32 queries
     if (q0 + 31 >= k0w) {
       f32x16_v s = zero16(), dp = zero16();
-      // fragment rows of this wave's 32 queries (frag_rows, written out): the
-      // lane's row start and its swizzle term, made opaque each block so that
-      // the eight per-k-step offsets are recomputed (two instructions each)
-      // instead of being held in registers across the loop
-      int rsw = ((32 * hq + l32) << 8) | ((hf ^ swz(l32)) << 4);
-      asm volatile("" : "+v"(rsw));
-      const lds_t *qrow = cur + (rsw & ~0xFF);
-      const int x4 = rsw & 0xF0;
+      // fragment rows of this wave's 32 queries: a per-lane base, made opaque
+      // each block (so that it is not held across the loop), plus immediates
+      uint32_t rl_ = rows_lane(lane) + 2 * hq * 256;
+      asm volatile("" : "+v"(rl_));
+      const lds_t *qrow = cur + rl_;
       typedef __attribute__((address_space(3))) QV lds_q;
       typedef __attribute__((address_space(3))) bf16x8_v lds_b;
       // each fragment is read one product ahead of the product that uses it
-      QV qa = *reinterpret_cast<const lds_q *>(qrow + x4);
-      bf16x8_v da = *reinterpret_cast<const lds_b *>(qrow + TILE + x4);
+      QV qa = *reinterpret_cast<const lds_q *>(qrow);
+      bf16x8_v da = *reinterpret_cast<const lds_b *>(qrow + TILE);
 #pragma unroll
       for (int es = 0; es < 8; ++es) {
-        const int offn = (32 * (es + 1)) ^ x4;  // ((2 (es + 1) + hf) ^ swz) << 4
+        const int offn = 32 * (es + 1);
         QV qn{};
         bf16x8_v dn{};
         if (es + 1 < 8) qn = *reinterpret_cast<const lds_q *>(qrow + offn);
@@ -753,17 +752,19 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
       // in P's query order (queries 32 hq + 16 t + 4 hf + [0, 4), + 8 + [0, 4))
       uint32_t cl = cols_lane(lane);
       asm volatile("" : "+v"(cl));  // recomputed each block, not held across the loop
-      const uint32_t aq = (uint32_t)(uintptr_t)cur + cl + (SEP ? 2 * TILE : 0), ao = aq + (SEP ? -TILE : TILE);
+      // (the wave's query half, rows 32 hq .., in the base: compile-time offsets)
+      const uint32_t aq = (uint32_t)(uintptr_t)cur + cl + 512 * hq + (SEP ? 2 * TILE : 0),
+                     ao = aq + (SEP ? -TILE : TILE);
       // steps n = 4 t + i; the dO^T and Q^T fragments of step n + 1 are read
       // while step n multiplies
       bf16x8_v fo[2], fq[2];
-      fo[0] = frag_cols_x<bf16x8_v>(ao, 0, 32 * hq);
-      fq[0] = frag_cols_x<bf16x8_v>(aq, 0, 32 * hq);
+      fo[0] = frag_cols_x<bf16x8_v>(ao, 0, 0);
+      fq[0] = frag_cols_x<bf16x8_v>(aq, 0, 0);
 #pragma unroll
       for (int n = 0; n < 8; ++n) {
         const int t = n >> 2, i = n & 3;
         if (n + 1 < 8) {
-          const int i1 = (n + 1) & 3, k1 = 32 * hq + 16 * ((n + 1) >> 2);
+          const int i1 = (n + 1) & 3, k1 = 16 * ((n + 1) >> 2);
           fo[(n + 1) & 1] = frag_cols_x<bf16x8_v>(ao, i1, k1);
           fq[(n + 1) & 1] = frag_cols_x<bf16x8_v>(aq, i1, k1);
         }

@@ -238,9 +238,10 @@ size_t moe_router_scratch_size(int64_t T, int64_t d, int64_t E) {
 }
 
 size_t attn_share_offset(int64_t B, int64_t S, int64_t H, int64_t Hkv) {
-  // D (fp32 [B, H, S]), then for the matrix-core backward of fp16 inputs
-  // bf16 rows of v ([B*S, Hkv*128]), q ([B*S, H*128]) and k ([B*S, Hkv*128])
-  const size_t dbytes = ((size_t)(B * S * H) * sizeof(float) + 255) / 256 * 256;
+  // D and -lse log2(e) (fp32 [B, H, S] each), then for the matrix-core
+  // backward of fp16 inputs bf16 rows of v ([B*S, Hkv*128]), q ([B*S, H*128])
+  // and k ([B*S, Hkv*128])
+  const size_t dbytes = ((size_t)(B * S * H) * 2 * sizeof(float) + 255) / 256 * 256;
   return align256(dbytes + (size_t)(B * S) * (size_t)(H + 2 * Hkv) * 128 * 2);
 }
 

@@ -124,15 +124,19 @@ __device__ __forceinline__ void dma4(i32x4_v rs, lds_t *lds, uint32_t off) {
                : "memory", "m0");
 }
 
-// Run `run` (0..15) of a [64][128] tile: rows swz(run) + 16 p (p = 0..3) of
-// the block whose row 0 is global row `grow0` of a matrix with `ld` elements
-// per row, columns col0 .. col0 + 127; each 16-lane group reads one row's 256
-// bytes in address order.
-__device__ __forceinline__ void tile_run(i32x4_v rs, lds_t *tile, int run, int64_t grow0,
-                                         int64_t ld, int col0, int lane) {
-  const int r = swz(run) + 16 * (lane >> 4);
-  const uint32_t off = (uint32_t)(((grow0 + r) * ld + col0 + 8 * (lane & 15)) * 2);
-  dma16(rs, tile + run * RUNB, off);
+// Run `run` (0..15) of a [64][128] tile: rows swz(run) + 16 p (p = 0..3) of a
+// block of 64 rows, each 16-lane group reading one row's 256 bytes in address
+// order. run_lane is the per-lane part of the byte offset (row 16 (lane / 16)
+// after row0, chunk lane % 16 after col0, with `ld` elements per row);
+// tile_run_s loads run `run` of block kb, the block's and the run's first row
+// in the instruction's scalar offset (every access in range: the callers'
+// tiles lie inside their buffers).
+__device__ __forceinline__ uint32_t run_lane(int64_t row0, int64_t ld, int col0, int lane) {
+  return (uint32_t)(((row0 + 16 * (lane >> 4)) * ld + col0 + 8 * (lane & 15)) * 2);
+}
+__device__ __forceinline__ void tile_run_s(i32x4_v rs, lds_t *tile, int run, int kb, uint32_t vo,
+                                           uint32_t row_bytes) {
+  dma16s(rs, tile + run * RUNB, vo, (uint32_t)(kb * KB + swz(run)) * row_bytes);
 }
 
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
@@ -225,6 +229,7 @@ struct AttnP {
   const __bf16 *dout;
   __bf16 *dq, *dk, *dv;
   float *D;
+  float *nl2;  // -lse log2(e) of every query, written by the dQ kernel for dK/dV
   // backward: bf16 rows of q, k and v for the gradient products (p.q, p.k,
   // p.v themselves for bf16 inputs; for fp16 inputs copies in the scratch,
   // written through the _w pointers)
@@ -287,11 +292,10 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnP p) {
   // waves 0-3 stream K (runs 4 (w & 3) .. + 3), waves 4-7 stream V
   const bool isK = w < 4;
   const i32x4_v rs = make_rsrc(isK ? p.k : p.v, p.qkv_bytes);
+  const uint32_t vo = run_lane(row0, p.ld_qkv, kvh * HD, lane), rowb = (uint32_t)(p.ld_qkv * 2);
   auto load = [&](int kb, lds_t *st) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
-      tile_run(rs, st + (isK ? 0 : TILE), 4 * (w & 3) + t, row0 + (int64_t)kb * KB, p.ld_qkv,
-               kvh * HD, lane);
+    for (int t = 0; t < 4; ++t) tile_run_s(rs, st + (isK ? 0 : TILE), 4 * (w & 3) + t, kb, vo, rowb);
   };
   const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
   load(0, L);
@@ -503,14 +507,16 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
   const i32x4_v rk = make_rsrc(p.k, p.qkv_bytes);
   const i32x4_v rvb = make_rsrc(p.vb, p.vb_bytes);
   const i32x4_v rkb = make_rsrc(p.kb, p.kb_bytes);
+  const uint32_t vok = run_lane(row0, p.ld_qkv, kvh * HD, lane), vov = run_lane(row0, p.ld_vb, kvh * HD, lane),
+                 vokb = run_lane(row0, p.ld_kb, kvh * HD, lane);
+  const uint32_t rbk = (uint32_t)(p.ld_qkv * 2), rbv = (uint32_t)(p.ld_vb * 2), rbkb = (uint32_t)(p.ld_kb * 2);
   auto load = [&](int kb, lds_t *st) {
-    const int64_t g0 = row0 + (int64_t)kb * KB;
 #pragma unroll
     for (int t = 0; t < 2 * NTQ; ++t) {
-      const int run = 2 * NTQ * w + t, which = run >> 4;
-      if (which == 0) tile_run(rk, st, run & 15, g0, p.ld_qkv, kvh * HD, lane);
-      else if (which == 1) tile_run(rvb, st + TILE, run & 15, g0, p.ld_vb, kvh * HD, lane);
-      else tile_run(rkb, st + 2 * TILE, run & 15, g0, p.ld_kb, kvh * HD, lane);
+      const int run = 2 * NTQ * w + t, which = run >> 4;  // (wave-uniform)
+      if (which == 0) tile_run_s(rk, st, run & 15, kb, vok, rbk);
+      else if (which == 1) tile_run_s(rvb, st + TILE, run & 15, kb, vov, rbv);
+      else tile_run_s(rkb, st + 2 * TILE, run & 15, kb, vokb, rbkb);
     }
   };
   const int nkb = min(p.S, (qb + 1) * ROWS) / KB;
@@ -528,7 +534,10 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
     }
   }
   Dq = sum_with_partner(Dq);
-  if (active && hf == 0) p.D[si] = Dq;
+  if (active && hf == 0) {
+    p.D[si] = Dq;
+    p.nl2[si] = -lse2;
+  }
   wait_vm0();
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
@@ -604,7 +613,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnP p) {
 // take the first and the second 32 queries of every 64-query block at or
 // after the diagonal; at the end wave w + 4 hands its partial dK, dV to wave w
 // through LDS, which adds them (fixed order: deterministic). LDS stage (two
-// of them) = Q (QE) | dO | (fp16 inputs: bf16 Q) | lse | D of one 64-query
+// of them) = Q (QE) | dO | (fp16 inputs: bf16 Q) | -lse log2(e) | D of one 64-query
 // block. With
 // grouped-query attention the workgroup writes its query head's share of the
 // key/value head's dK, dV as fp32 rows; attn_gqa_sum_kernel adds the shares.
@@ -647,13 +656,13 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
 
   // 16 NTK runs per block: wave w brings runs RPW sub .. + RPW - 1 of tile tl
   // (Q (QE), dO, bf16 Q; with three tiles waves 6 and 7 bring none); the last
-  // wave also brings lse and D (64 floats each)
+  // wave also brings -lse log2(e) and D (64 floats each)
   const int tl = SEP ? (w >> 1) : (w >> 2), sub = SEP ? (w & 1) : (w & 3);
   const bool brings = tl < NTK;  // wave-uniform
   const i32x4_v rs = tl == 0 ? make_rsrc(p.q, p.qkv_bytes)
                    : tl == 1 ? make_rsrc(p.dout, p.o_bytes)
                              : make_rsrc(p.qb, p.qb_bytes);
-  const i32x4_v rl = make_rsrc(p.lse, p.lse_bytes);
+  const i32x4_v rl = make_rsrc(p.nl2, p.lse_bytes);  // -lse log2(e), from the dQ kernel
   const i32x4_v rd = make_rsrc(p.D, p.lse_bytes);
   const int64_t sbase = ((int64_t)b * p.H + h) * p.S;
   // Byte offset of run q of block qbi: the lane's row 16 (lane / 16) and
@@ -719,7 +728,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
         for (int r = 0; r < 16; ++r)
           if (q0 + out_row(r, hf) < myk) s[r] = -INFINITY;
       }
-      // four rows at a time: their lse and D are 4 consecutive floats each
+      // four rows at a time: their -lse log2(e) and D are 4 consecutive floats each
       // (rows 8 g + 4 hf + [0, 4) of the half), read one group ahead
       typedef __attribute__((ext_vector_type(4))) float f4_t;
       const f4_t *const lseq = reinterpret_cast<const f4_t *>(sL + 4 * hf);
@@ -735,7 +744,7 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnP p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * g + e;  // out_row(r, hf) = 8 g + 4 hf + e
-          const float pv = ex2(__builtin_fmaf(s[r], sc, -lc[e] * LOG2E));
+          const float pv = ex2(__builtin_fmaf(s[r], sc, lc[e]));
           s[r] = pv;
           dp[r] = pv * (dp[r] - dc[e]);
         }
@@ -1026,10 +1035,11 @@ AttnP mc_params(const lc_attn_args &a) {
   const int64_t rows = (int64_t)a.B * a.S, d = (int64_t)a.H * HD;
   const int Hkv = kv_of(a);
   const int64_t dkv = (int64_t)Hkv * HD;
-  // scratch: D (fp32 [B, H, S], 256-byte aligned), then for fp16 inputs bf16
-  // rows of v ([rows, dkv]), q ([rows, d]) and k ([rows, dkv]), then
-  // (grouped-query attention) the fp32 dk, dv shares
-  const size_t dbytes = ((size_t)rows * a.H * sizeof(float) + 255) / 256 * 256;
+  // scratch: D, then -lse log2(e) (fp32 [B, H, S] each; 256-byte aligned
+  // together), then for fp16 inputs bf16 rows of v ([rows, dkv]), q ([rows, d])
+  // and k ([rows, dkv]), then (grouped-query attention) the fp32 dk, dv shares
+  if (p.D) p.nl2 = p.D + rows * a.H;
+  const size_t dbytes = ((size_t)rows * a.H * 2 * sizeof(float) + 255) / 256 * 256;
   __bf16 *const cp = a.scratch ? reinterpret_cast<__bf16 *>(static_cast<char *>(a.scratch) + dbytes) : nullptr;
   const bool bf = a.dtype == LC_BF16;
   p.vb_w = bf ? nullptr : cp;

@@ -43,7 +43,10 @@ extern "C" {
  *                     head of head_dim columns: pair (i, i+hd/2) at
  *                     position p = m mod rope_seq by angle table
  *                     cos/sin[p*hd/2 + i] (fp32 tables, [rope_seq, hd/2]);
- *                     C: c_dtype. head_dim must be 128 for bf16.
+ *                     C: c_dtype. head_dim must be 128 for bf16. With aux0
+ *                     non-NULL the same values are also written to aux0
+ *                     ([M, N], ld_aux, aux_dtype): a second copy in another
+ *                     type (the attention backward's bf16 q, k, v).
  *   LC_EPI_SWIGLU     gated FFN input projection: B holds W1 rows
  *                     [0, N) (gate) and W3 rows [N, 2N) (up) (B k-major,
  *                     2N rows); writes gate = acc_W1 to aux0 and
@@ -176,7 +179,13 @@ lc_status lc_rmsnorm_backward_noalloc(const lc_norm_args *args, void *stream);
  * -angle (the transpose of the forward rotation, positions 0..S-1).
  * Deterministic (no atomics); scratch (lc_attention_scratch_bytes) holds D
  * and, for fp16 q/k/v, the bf16 copies of q, k and v that the backward's
- * gradient products read.
+ * gradient products read. A caller that already holds those copies (the
+ * projection's epilogue can write them, lc_gemm LC_EPI_ROPE with aux0) passes
+ * them in qkv_bf16: bf16 [B*S, ...] rows of stride ld_qkv_bf16 with q at
+ * column 0, k at column H*hd and v at column (H + Hkv)*hd, holding q, k, v
+ * rounded to bf16 (from the fp16 values, or from the fp32 values those were
+ * rounded from); the backward then reads them instead of writing its own
+ * (NULL: it writes them into the scratch).
  * Types: matrix-core path: q, k, v LC_FP16 or LC_BF16 (`dtype`; forward
  * products in that type), o, dout, dq, dk, dv LC_BF16 (gradient products in
  * bf16), head_dim 128, S a multiple of 128. fp32 path: everything LC_FP32,
@@ -193,6 +202,7 @@ typedef struct lc_attn_args {
   void *scratch; size_t scratch_bytes;
   int32_t Hkv;         /* key/value heads (0 = H); divides H */
   int32_t reserved;
+  const void *qkv_bf16; int64_t ld_qkv_bf16;  /* optional bf16 q|k|v copies (backward, fp16 q/k/v) */
 } lc_attn_args;
 
 lc_status lc_attention_forward(const lc_attn_args *args, void *stream);

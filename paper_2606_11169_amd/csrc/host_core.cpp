@@ -147,6 +147,7 @@ lc_status stage_plan(const lc_stage_desc &d, int32_t max_in_flight, int32_t max_
   p.rstd1 = take((size_t)T * 4);
   p.n1 = take((size_t)T * D * es);
   p.qkv = take((size_t)T * QC * ea);
+  p.qkvb = (p.ty.att == LC_FP16 && !d.qk_norm) ? take((size_t)T * QC * 2) : 0;
   if (d.qk_norm) {
     p.qkraw = take((size_t)T * (D + (size_t)p.dkv) * ea);
     p.rstdqk = take((size_t)T * (H + Hkv) * 4);

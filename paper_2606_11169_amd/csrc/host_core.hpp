@@ -82,6 +82,9 @@ struct StagePlan {
   // qk_norm: the projection's raw q|k [T, d + dkv] (att type) and the
   // per-head reciprocal RMS [T, n_heads + n_kv_heads] (fp32)
   size_t qkraw, rstdqk;
+  // fp16 attention operands without qk_norm: the projection's bf16 copy of
+  // q|k|v [T, qkv_cols] for the attention backward's gradient products (0: none)
+  size_t qkvb;
   // weight-pass slots (split backward): max_w_pending slots of n_layers
   // blocks, each holding the gradient operands a backward-for-inputs pass
   // leaves for the backward-for-weights pass of the same microbatch: the

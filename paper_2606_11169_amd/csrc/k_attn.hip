@@ -1042,15 +1042,23 @@ AttnP mc_params(const lc_attn_args &a) {
   const size_t dbytes = ((size_t)rows * a.H * 2 * sizeof(float) + 255) / 256 * 256;
   __bf16 *const cp = a.scratch ? reinterpret_cast<__bf16 *>(static_cast<char *>(a.scratch) + dbytes) : nullptr;
   const bool bf = a.dtype == LC_BF16;
-  p.vb_w = bf ? nullptr : cp;
-  p.qb_w = bf || !cp ? nullptr : cp + rows * dkv;
-  p.kb_w = bf || !cp ? nullptr : cp + rows * (dkv + d);
-  p.vb = bf ? static_cast<const __bf16 *>(a.v) : p.vb_w;
-  p.qb = bf ? static_cast<const __bf16 *>(a.q) : p.qb_w;
-  p.kb = bf ? static_cast<const __bf16 *>(a.k) : p.kb_w;
-  p.ld_vb = bf ? a.ld_qkv : dkv;
-  p.ld_qb = bf ? a.ld_qkv : d;
-  p.ld_kb = bf ? a.ld_qkv : dkv;
+  if (!bf && a.qkv_bf16) {  // the caller's bf16 copies: no copy pass
+    const __bf16 *c = static_cast<const __bf16 *>(a.qkv_bf16);
+    p.qb = c;
+    p.kb = c + d;
+    p.vb = c + d + dkv;
+    p.ld_qb = p.ld_kb = p.ld_vb = a.ld_qkv_bf16;
+  } else {
+    p.vb_w = bf ? nullptr : cp;
+    p.qb_w = bf || !cp ? nullptr : cp + rows * dkv;
+    p.kb_w = bf || !cp ? nullptr : cp + rows * (dkv + d);
+    p.vb = bf ? static_cast<const __bf16 *>(a.v) : p.vb_w;
+    p.qb = bf ? static_cast<const __bf16 *>(a.q) : p.qb_w;
+    p.kb = bf ? static_cast<const __bf16 *>(a.k) : p.kb_w;
+    p.ld_vb = bf ? a.ld_qkv : dkv;
+    p.ld_qb = bf ? a.ld_qkv : d;
+    p.ld_kb = bf ? a.ld_qkv : dkv;
+  }
   if (a.scratch && Hkv < a.H) {
     char *sh = static_cast<char *>(a.scratch) + attn_share_offset(a.B, a.S, a.H, Hkv);
     p.dkp = reinterpret_cast<float *>(sh);
@@ -1083,6 +1091,14 @@ lc_status check_extents(const lc_attn_args &a) {
   if (((rows - 1) * a.ld_qkv + d) * 2 >= lim || ((rows - 1) * a.ld_o + d) * 2 >= lim ||
       rows * d * 2 >= lim)
     return fail(LC_ERR_UNSUPPORTED, "attention: a q/k/v/o matrix spans 2 GiB or more");
+  if (a.qkv_bf16 && a.dtype == LC_FP16) {
+    const int64_t cols = d + 2 * (int64_t)kv_of(a) * HD;
+    if (!aligned16(a.qkv_bf16) || a.ld_qkv_bf16 < cols || a.ld_qkv_bf16 % 8)
+      return fail(LC_ERR_INVALID_ARG, "attention: qkv_bf16 must be 16-byte aligned with ld_qkv_bf16 >= "
+                  "(H + 2 Hkv) * 128, a multiple of 8");
+    if (((rows - 1) * a.ld_qkv_bf16 + cols) * 2 >= lim)
+      return fail(LC_ERR_UNSUPPORTED, "attention: the bf16 q/k/v copies span 2 GiB or more");
+  }
   return LC_OK;
 }
 
@@ -1123,7 +1139,7 @@ template <typename QE>
 lc_status bwd_mc(const lc_attn_args &a, hipStream_t s) {
   LC_TRY(check_extents(a));
   const AttnP p = mc_params(a);
-  if constexpr (!std::is_same<QE, __bf16>::value) {
+  if (!std::is_same<QE, __bf16>::value && !a.qkv_bf16) {
     const int64_t chunks = (int64_t)a.B * a.S * (a.H + 2 * p.Hkv) * HD / 8;
     hipLaunchKernelGGL(attn_bwd_copy_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, p);
     LC_TRY(check_launch("attn_bwd_copy_kernel"));

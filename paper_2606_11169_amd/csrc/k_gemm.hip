@@ -472,6 +472,11 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
               const int64_t row = (int64_t)m * p.ldc + ncol0 + 4 * q;
               store4_dt(Cp, row, p.c_dt, a[0], a[1], a[2], a[3]);
               store4_dt(Cp, row + 64, p.c_dt, b[0], b[1], b[2], b[3]);
+              if (p.aux0) {  // a second copy in aux_dt
+                const int64_t ra = (int64_t)m * p.ld_aux + ncol0 + 4 * q;
+                store4_dt(p.aux0, ra, p.aux_dt, a[0], a[1], a[2], a[3]);
+                store4_dt(p.aux0, ra + 64, p.aux_dt, b[0], b[1], b[2], b[3]);
+              }
             } else {
               const int n = n0 + wn * 64 + 4 * q;  // output column of the gate/up pair
               if (n >= p.N) continue;
@@ -630,6 +635,10 @@ static lc_status check_gemm_args(const lc_gemm_args &a) {
       return fail(LC_ERR_INVALID_ARG, "gemm: negative group_stride_b");
     if (a.group_mode == LC_GROUP_K && (a.a_kmajor || a.b_kmajor || a.group_stride_c < 0))
       return fail(LC_ERR_UNSUPPORTED, "gemm: LC_GROUP_K needs m/n-major operands and group_stride_c >= 0");
+  }
+  if (a.epilogue == LC_EPI_ROPE && a.aux0) {
+    if (!aligned16(a.aux0) || (bf && a.ld_aux % 8) || a.ld_aux < a.N || !valid_dtype(a.aux_dtype))
+      return fail(LC_ERR_INVALID_ARG, "gemm: bad RoPE copy operand");
   }
   if (a.epilogue == LC_EPI_ROPE) {
     if (!a.rope_cos || !a.rope_sin || a.rope_seq <= 0 || a.rope_cols < 0 ||

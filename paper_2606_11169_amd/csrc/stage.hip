@@ -329,6 +329,9 @@ static lc_status forward_layers(lc_stage *st, const lc_param_bufs *pb, const voi
     if (!d.qk_norm) {
       a.rope_cos = rc; a.rope_sin = rs; a.rope_seq = d.seq_len; a.rope_cols = (int)(D + Dkv);
       a.head_dim = d.head_dim;
+      if (P.qkvb) {  // the bf16 copy the attention backward's gradient products read
+        a.aux0 = L.at(P.qkvb); a.ld_aux = QC; a.aux_dtype = LC_BF16;
+      }
     }
     LC_TRY(gemm_launch(a, s));
     if (d.qk_norm) {
@@ -520,6 +523,9 @@ static lc_status backward_layers(lc_stage *st, const lc_param_bufs *pb, const vo
     at.dq = dqkv; at.dk = dqkv + D * es; at.dv = dqkv + (D + Dkv) * es; at.ld_dqkv = QC;
     at.rope_cos = rc; at.rope_sin = rs;
     at.scratch = ws + P.s_attn; at.scratch_bytes = P.s_attn_bytes;
+    if (P.qkvb) {
+      at.qkv_bf16 = L.at(P.qkvb); at.ld_qkv_bf16 = QC;
+    }
     LC_TRY(attn_bwd_launch(at, s));
     // dq, dk through the per-head norms (in place); G[qn], G[kn] += ...
     if (d.qk_norm) {

@@ -130,7 +130,8 @@ class lc_attn_args(C.Structure):
                 ("dout", C.c_void_p), ("dq", C.c_void_p), ("dk", C.c_void_p), ("dv", C.c_void_p),
                 ("ld_dqkv", C.c_int64), ("rope_cos", C.c_void_p), ("rope_sin", C.c_void_p),
                 ("scratch", C.c_void_p), ("scratch_bytes", C.c_size_t),
-                ("Hkv", C.c_int32), ("reserved", C.c_int32)]
+                ("Hkv", C.c_int32), ("reserved", C.c_int32),
+                ("qkv_bf16", C.c_void_p), ("ld_qkv_bf16", C.c_int64)]
 
 
 class lc_qknorm_args(C.Structure):
@@ -534,6 +535,7 @@ def _fill(struct, **kw):
 
 
 _PTR_FIELDS = {"x", "g", "n", "rstd", "dn", "dres", "dx", "dx_copy", "dg_accum", "scratch", "q",
+               "qkv_bf16",
                "k", "v", "o", "lse", "dout", "dq", "dk", "dv", "rope_cos", "rope_sin", "qk",
                "raw", "gq", "gk", "dqk", "dgq", "dgk"}
 
@@ -574,11 +576,11 @@ def lc_attention_forward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, ld_o, 
 
 def lc_attention_backward(dtype, o_dtype, B, S, H, hd, q, k, v, ld_qkv, o, dout, ld_o, lse, dq,
                           dk, dv, ld_dqkv, rope_cos, rope_sin, scratch, scratch_bytes,
-                          stream=None, Hkv=0):
+                          stream=None, Hkv=0, qkv_bf16=None, ld_qkv_bf16=0):
     a = _fill(lc_attn_args(), dtype=dtype, o_dtype=o_dtype, B=B, S=S, H=H, hd=hd, q=q, k=k, v=v,
               ld_qkv=ld_qkv, o=o, ld_o=ld_o, lse=lse, dout=dout, dq=dq, dk=dk, dv=dv,
               ld_dqkv=ld_dqkv, rope_cos=rope_cos, rope_sin=rope_sin, scratch=scratch,
-              scratch_bytes=scratch_bytes, Hkv=Hkv)
+              scratch_bytes=scratch_bytes, Hkv=Hkv, qkv_bf16=qkv_bf16, ld_qkv_bf16=ld_qkv_bf16)
     return _check(lib().lc_attention_backward(C.byref(a), C.c_void_p(stream_ptr(stream) or None)))
 
 

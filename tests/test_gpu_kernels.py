@@ -430,6 +430,62 @@ def test_attention_full_length(S, dt):
     attn_case(1, S, 2, 128, dt, 16 + S, True)
 
 
+def test_attention_backward_with_caller_bf16_copies():
+    """fp16 q/k/v with the bf16 copies supplied by the caller (qkv_bf16): the
+    backward reads them instead of writing its own, bit for bit the same."""
+    banner("attention backward with caller bf16 copies")
+    rng = np.random.default_rng(31)
+    B, S, H, hd = 1, 384, 2, 128
+    d = H * hd
+    qkv, qkvd = packed_qkv(rng, B, S, H, hd, lc.LC_FP16)
+    base = qkvd.data_ptr()
+    o = torch.empty((B * S, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty(B * H * S, dtype=torch.float32, device=DEV)
+    lc.lc_attention_forward(lc.LC_FP16, lc.LC_BF16, B, S, H, hd, base, base + 2 * d, base + 4 * d,
+                            3 * d, o, d, lse)
+    _, dod = typed(rng.standard_normal((B * S, d)), lc.LC_BF16)
+    cos, sin = OS.rope_tables(S, hd, 10000.0)
+    copies = torch.zeros((B * S, 3 * d + 64), dtype=torch.bfloat16, device=DEV)  # padded rows
+    copies[:, :3 * d] = qkvd.to(torch.bfloat16)
+    outs = []
+    for caller in (False, True):
+        sb = lc.lc_attention_scratch_bytes(B, S, H)
+        scratch = torch.empty(sb, dtype=torch.uint8, device=DEV)
+        dqkv = torch.zeros((B * S, 3 * d), dtype=torch.bfloat16, device=DEV)
+        g0 = dqkv.data_ptr()
+        lc.lc_attention_backward(lc.LC_FP16, lc.LC_BF16, B, S, H, hd, base, base + 2 * d,
+                                 base + 4 * d, 3 * d, o, dod, d, lse, g0, g0 + 2 * d, g0 + 4 * d,
+                                 3 * d, f32(cos), f32(sin), scratch, sb,
+                                 qkv_bf16=copies if caller else None,
+                                 ld_qkv_bf16=3 * d + 64 if caller else 0)
+        torch.cuda.synchronize()
+        outs.append(bits16(dqkv))
+    assert np.array_equal(outs[0], outs[1])
+
+
+def test_gemm_rope_epilogue_second_copy():
+    """LC_EPI_ROPE with aux0: the rotated q|k|v in fp16 (C) and in bf16 (aux0)."""
+    banner("gemm rope second copy")
+    rng = np.random.default_rng(32)
+    H, hd, S = 2, 128, 256
+    d = H * hd
+    T, N, K = S, 3 * d, d
+    A, B, Ad, Bd, lda, ldb = operands(rng, T, N, K, True, True, False)
+    cos, sin = OS.rope_tables(S, hd, 10000.0)
+    C = torch.empty((T, N), dtype=torch.float16, device=DEV)
+    Cb = torch.empty((T, N + 8), dtype=torch.bfloat16, device=DEV)
+    lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_ROPE, T, N, K, Ad, lda, 1, Bd, ldb, 1, C, N,
+               rope_cos=f32(cos), rope_sin=f32(sin), rope_seq=S, rope_cols=2 * d, head_dim=hd,
+               c_dtype=lc.LC_FP16, aux0=Cb, ld_aux=N + 8, aux_dtype=lc.LC_BF16)
+    torch.cuda.synchronize()
+    prod = (A.astype(np.float64) @ B.astype(np.float64).T).reshape(1, S, 3, H, hd)
+    q = OS.rope_apply(prod[:, :, 0], cos, sin)
+    k = OS.rope_apply(prod[:, :, 1], cos, sin)
+    ref = np.stack([q, k, prod[:, :, 2]], axis=2).reshape(T, N)
+    assert rel_err(host(C), ref) <= ROUND_TOL[lc.LC_FP16]
+    assert rel_err(host(Cb)[:, :N], ref) <= ROUND_TOL[lc.LC_BF16]
+
+
 @pytest.mark.parametrize("hd", [32, 8])
 def test_attention_fp32(hd):
     attn_case(2, 64, 4, hd, lc.LC_FP32, 13, True)

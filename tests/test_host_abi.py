@@ -257,10 +257,11 @@ def test_workspace_grows_with_stash_slots():
     w8 = lc.lc_workspace_bytes(d, 8)
     slot = (w8 - w1) // 7
     T, D, F, L = 4096, 4096, 11008, 4
-    # per layer: x, h (fp32 [T,d]); n1, o, n2 (bf16 [T,d]); q, k, v (fp16 [T,d]);
-    # gate, up (fp32 [T,f]); act (bf16 [T,f]); rstd1, rstd2, lse (fp32 rows)
-    approx = L * (4 * T * D * 2 + 2 * T * D * 3 + 2 * T * D * 3 + 4 * T * F * 2 + 2 * T * F
-                  + 4 * T * (2 + 32))
+    # per layer: x, h (fp32 [T,d]); n1, o, n2 (bf16 [T,d]); q, k, v (fp16 [T,d])
+    # and their bf16 copy; gate, up (fp32 [T,f]); act (bf16 [T,f]); rstd1,
+    # rstd2, lse (fp32 rows)
+    approx = L * (4 * T * D * 2 + 2 * T * D * 3 + 2 * T * D * 3 + 2 * T * D * 3 + 4 * T * F * 2
+                  + 2 * T * F + 4 * T * (2 + 32))
     assert approx <= slot <= approx + L * 16 * 256
 
 

@@ -178,7 +178,8 @@ lc_status lc_rmsnorm_backward_noalloc(const lc_norm_args *args, void *stream);
  * if rope_cos/rope_sin are non-NULL, dq and dk are then rotated back by
  * -angle (the transpose of the forward rotation, positions 0..S-1).
  * Deterministic (no atomics); scratch (lc_attention_scratch_bytes) holds D
- * and, for fp16 q/k/v, the bf16 copies of q, k and v that the backward's
+ * and -lse log2(e) per query (fp32 [B, H, S] each) and, for fp16 q/k/v, the
+ * bf16 copies of q, k and v that the backward's
  * gradient products read. A caller that already holds those copies (the
  * projection's epilogue can write them, lc_gemm LC_EPI_ROPE with aux0) passes
  * them in qkv_bf16: bf16 [B*S, ...] rows of stride ld_qkv_bf16 with q at

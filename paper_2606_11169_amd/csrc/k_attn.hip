@@ -24,8 +24,9 @@
 // 128 keys accumulates dV^T = dO^T P and dK^T = Q^T dS over the query blocks
 // at or after the diagonal. Both recompute P from the forward's log-sum-exp
 // with the forward's q/k element type (so P matches the forward) and take
-// every gradient product in bf16; for fp16 inputs a copy pass first writes
-// bf16 rows of q, k and v for those products. The gradient products read
+// every gradient product in bf16; for fp16 inputs they read bf16 rows of q,
+// k and v that the caller passes (the QKV projection's epilogue writes them)
+// or that a copy pass writes first. The gradient products read
 // their K^T, Q^T and dO^T operands from the same row tiles as the score
 // products, with transposing LDS reads in the accumulator's key (or query)
 // order, so no transposed copy is ever written. RoPE's inverse rotation of

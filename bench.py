@@ -358,6 +358,66 @@ def gemm_compare(torch, lc, stream, reps=20, n=4096):
     return out
 
 
+def gemm_compare_shapes(torch, lc, cfg, stream, reps=10):
+    """Diagnostic: the library's GEMM main loop (plain bf16 store; the stage's fused
+    epilogues left out so both sides do the same work) and hipBLASLt (torch.matmul; the
+    library never calls it) at the stage's twelve product shapes and layouts, N(0, 1)
+    bf16 operands; `reps` launches back to back between two HIP events per side.
+    Layouts as C = A B^T: NT = both operands k-major (forward projections), NN = B
+    m/n-major (input gradients), TN = both m/n-major (weight gradients)."""
+    T, d, f = cfg.tokens, cfg.d_model, cfg.d_ff
+    q = cfg.n_heads * cfg.head_dim + 2 * cfg.kv_heads * cfg.head_dim
+    shapes = [("qkv", "NT", T, q, d), ("o", "NT", T, d, d), ("gate_up", "NT", T, 2 * f, d),
+              ("down", "NT", T, d, f), ("dn2", "NN", T, d, 2 * f), ("do", "NN", T, d, d),
+              ("dn1", "NN", T, d, q), ("dh", "NN", T, f, d), ("dW_qkv", "TN", q, d, T),
+              ("dW_o", "TN", d, d, T), ("dW_13", "TN", 2 * f, d, T), ("dW_2", "TN", d, f, T)]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    out = []
+    for name, lay, M, N, K in shapes:
+        if lay == "NT":
+            a = torch.randn(M, K, generator=g, device="cuda").to(torch.bfloat16)
+            b = torch.randn(N, K, generator=g, device="cuda").to(torch.bfloat16)
+            args, blas_ab = (a, K, 1, b, K, 1), (a, b.t())
+        elif lay == "NN":
+            a = torch.randn(M, K, generator=g, device="cuda").to(torch.bfloat16)
+            b = torch.randn(K, N, generator=g, device="cuda").to(torch.bfloat16)
+            args, blas_ab = (a, K, 1, b, N, 0), (a, b)
+        else:
+            a = torch.randn(K, M, generator=g, device="cuda").to(torch.bfloat16)
+            b = torch.randn(K, N, generator=g, device="cuda").to(torch.bfloat16)
+            args, blas_ab = (a, M, 0, b, N, 0), (a.t(), b)
+        c = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+
+        def lib():
+            lc.lc_gemm(lc.LC_BF16, lc.LC_EPI_STORE, M, N, K, *args, c, N, stream=stream)
+
+        def blas():
+            torch.matmul(*blas_ab, out=c)
+        row = {"product": name, "layout": lay, "M": M, "N": N, "K": K}
+        with torch.cuda.stream(stream):
+            for side, fn in (("lc_gemm", lib), ("hipblaslt", blas)):
+                for _ in range(3):
+                    fn()
+                stream.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(reps):
+                    fn()
+                e1.record(stream)
+                e1.synchronize()
+                ms = e0.elapsed_time(e1) / reps
+                row[side] = {"us": round(ms * 1e3, 1), "tflops": round(2 * M * N * K / (ms * 1e-3) / 1e12, 1)}
+        row["ratio"] = round(row["hipblaslt"]["us"] / row["lc_gemm"]["us"], 3)
+        print(f"[bench] {name} {lay} {M}x{N}x{K}: lc {row['lc_gemm']['us']} us, hipBLASLt "
+              f"{row['hipblaslt']['us']} us", file=sys.stderr, flush=True)
+        out.append(row)
+        del a, b, c
+    return {"workload": cfg.name, "timing": f"{reps} launches back to back between HIP events",
+            "shapes": out}
+
+
 def adam_shard(torch, lc, shard, stream, reps=20):
     n = shard.n
     dev = "cuda"
@@ -556,6 +616,8 @@ def main():
                          "two streams")
     ap.add_argument("--adam-only", action="store_true",
                     help="only the calibration copy and the AdamW shard (PMC runs)")
+    ap.add_argument("--gemm-shapes", action="store_true",
+                    help="diagnostic: the library's GEMM beside hipBLASLt at the 7B stage's twelve product shapes")
     ap.add_argument("--gemm-compare", action="store_true",
                     help="only the library's GEMM beside hipBLASLt on a 4096^3 NT product "
                          "(a diagnostic for the matrix cores' sustained rate)")
@@ -628,6 +690,10 @@ def main():
             res[c.name] = {"value": round(otf, 2), "unit": "TFLOP/s",
                            "ms_per_step": round(oms, 2), "outputs_finite": ofin}
         print(json.dumps({"overlap_stage": res}))
+        return
+    if args.gemm_shapes:
+        print(json.dumps({"gemm_shapes": gemm_compare_shapes(torch, lc, cfg, stream, reps=args.steps)}),
+              flush=True)
         return
     if args.gemm_compare:
         print(json.dumps({"gemm_compare": gemm_compare(torch, lc, stream, reps=args.steps)}),

@@ -463,6 +463,41 @@ def test_attention_backward_with_caller_bf16_copies():
     assert np.array_equal(outs[0], outs[1])
 
 
+def test_gqa_attention_backward_with_caller_bf16_copies():
+    """Grouped-query attention (4 query heads over 2 key/value heads), fp16 q/k/v:
+    caller-supplied bf16 copies (k at column H*hd, v at (H + Hkv)*hd of the copy
+    rows) give the gradients of the backward's own copy pass, bit for bit."""
+    banner("gqa attention backward with caller bf16 copies")
+    rng = np.random.default_rng(33)
+    B, S, H, Hkv, hd = 1, 256, 4, 2, 128
+    d, dkv = H * hd, Hkv * hd
+    ld = d + 2 * dkv
+    _, qkvd = typed(rng.standard_normal((B * S, ld)), lc.LC_FP16)
+    base = qkvd.data_ptr()
+    o = torch.empty((B * S, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty(B * H * S, dtype=torch.float32, device=DEV)
+    lc.lc_attention_forward(lc.LC_FP16, lc.LC_BF16, B, S, H, hd, base, base + 2 * d,
+                            base + 2 * (d + dkv), ld, o, d, lse, Hkv=Hkv)
+    _, dod = typed(rng.standard_normal((B * S, d)), lc.LC_BF16)
+    cos, sin = OS.rope_tables(S, hd, 10000.0)
+    copies = torch.zeros((B * S, ld + 32), dtype=torch.bfloat16, device=DEV)  # padded rows
+    copies[:, :ld] = qkvd.to(torch.bfloat16)
+    outs = []
+    for caller in (False, True):
+        sb = lc.lc_attention_scratch_bytes(B, S, H, Hkv)
+        scratch = torch.empty(sb, dtype=torch.uint8, device=DEV)
+        dqkv = torch.zeros((B * S, ld), dtype=torch.bfloat16, device=DEV)
+        g0 = dqkv.data_ptr()
+        lc.lc_attention_backward(lc.LC_FP16, lc.LC_BF16, B, S, H, hd, base, base + 2 * d,
+                                 base + 2 * (d + dkv), ld, o, dod, d, lse, g0, g0 + 2 * d,
+                                 g0 + 2 * (d + dkv), ld, f32(cos), f32(sin), scratch, sb, Hkv=Hkv,
+                                 qkv_bf16=copies if caller else None,
+                                 ld_qkv_bf16=ld + 32 if caller else 0)
+        torch.cuda.synchronize()
+        outs.append(bits16(dqkv))
+    assert np.array_equal(outs[0], outs[1])
+
+
 def test_gemm_rope_epilogue_second_copy():
     """LC_EPI_ROPE with aux0: the rotated q|k|v in fp16 (C) and in bf16 (aux0)."""
     banner("gemm rope second copy")

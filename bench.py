@@ -616,6 +616,8 @@ def main():
                          "two streams")
     ap.add_argument("--adam-only", action="store_true",
                     help="only the calibration copy and the AdamW shard (PMC runs)")
+    ap.add_argument("--streaming-only", action="store_true",
+                    help="only the calibration accumulate and the RMSNorm / accumulate kernels at the 7B shapes")
     ap.add_argument("--gemm-shapes", action="store_true",
                     help="diagnostic: the library's GEMM beside hipBLASLt at the 7B stage's twelve product shapes")
     ap.add_argument("--gemm-compare", action="store_true",
@@ -690,6 +692,11 @@ def main():
             res[c.name] = {"value": round(otf, 2), "unit": "TFLOP/s",
                            "ms_per_step": round(oms, 2), "outputs_finite": ofin}
         print(json.dumps({"overlap_stage": res}))
+        return
+    if args.streaming_only:
+        calibration_copy(torch, lc, stream)
+        print(json.dumps({"streaming": streaming_kernels(torch, lc, cfg, stream, reps=args.steps)}),
+              flush=True)
         return
     if args.gemm_shapes:
         print(json.dumps({"gemm_shapes": gemm_compare_shapes(torch, lc, cfg, stream, reps=args.steps)}),

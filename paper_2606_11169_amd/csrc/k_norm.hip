@@ -12,7 +12,9 @@
 // waves (so that a workgroup of 16 waves keeps four rows in registers at
 // once and the chip holds enough waves to cover memory latency); longer rows
 // go one per wave, read twice. Every tensor's element type is a run-time
-// value (uniform branches). The gain gradient is a column reduction over
+// value (uniform branches), except in the instantiations for the decoder
+// stage's own type mix, where the types are template arguments (straight-line
+// loads: 20-25% faster forward, 9% faster backward rows). The gain gradient is a column reduction over
 // rows: each backward workgroup handles kNormRowsPerBlock rows and writes
 // the fp32 partial sums of its rows in a fixed order, then the final kernel
 // adds the partials of each column: sixteen slices of consecutive blocks,
@@ -26,6 +28,19 @@ namespace lc {
 namespace {
 
 constexpr int ROWS_PER_BLOCK = 4;  // forward: one wave per row
+
+// 8 consecutive values of a tensor whose element type is the template
+// argument DT, or the run-time value rt when DT < 0 (the generic kernels):
+// with a compile-time type the loads are straight-line code, which lets the
+// compiler keep several rows' loads in flight without waiting at branches
+template <int DT>
+__device__ __forceinline__ void ld8(const void *base, int64_t idx, int rt, float (&x)[8]) {
+  load8_dt(base, idx, DT < 0 ? rt : DT, x);
+}
+template <int DT>
+__device__ __forceinline__ void st8(void *base, int64_t idx, int rt, const float (&x)[8]) {
+  store8_dt(base, idx, DT < 0 ? rt : DT, x);
+}
 constexpr int MAXU = 8;            // 8-element chunks per lane held in registers
 constexpr int MAXD = 64 * 8 * MAXU;
 
@@ -43,6 +58,7 @@ struct NormP {
   int nblk;
 };
 
+template <int XDT, int WDT, int ODT>
 __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(NormP p) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * ROWS_PER_BLOCK + (threadIdx.x >> 6);
@@ -55,7 +71,7 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(NormP p) {
     for (int u = 0; u < MAXU; ++u) {
       const int c = lane * 8 + 512 * u;
       if (c < p.d) {
-        load8_dt(p.x, base + c, p.x_dt, v[u]);
+        ld8<XDT>(p.x, base + c, p.x_dt, v[u]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) ss += v[u][e] * v[u][e];
       }
@@ -68,10 +84,10 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(NormP p) {
       const int c = lane * 8 + 512 * u;
       if (c < p.d) {
         float gv[8];
-        load8_dt(p.g, c, p.w_dt, gv);
+        ld8<WDT>(p.g, c, p.w_dt, gv);
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[u][e] = v[u][e] * r * gv[e];
-        store8_dt(p.n, base + c, p.out_dt, v[u]);
+        st8<ODT>(p.n, base + c, p.out_dt, v[u]);
       }
     }
     return;
@@ -138,6 +154,7 @@ __device__ __forceinline__ void bwd_row_long(const NormP &p, int64_t row, int la
 // slots in order, into partial[blk][k].
 constexpr int BW_THREADS = 1024;
 constexpr int BW_CHUNKS = MAXD / 2048;  // 8-value chunks per lane
+template <int DNDT, int XDT, int WDT, int RDT, int ODT>
 __global__ __launch_bounds__(BW_THREADS) void rmsnorm_bwd_rows_kernel(NormP p) {
   __shared__ float red[MAXD];
   __shared__ float dots[2][4][4];  // [iteration parity][row slot][wave of the row]
@@ -164,9 +181,9 @@ __global__ __launch_bounds__(BW_THREADS) void rmsnorm_bwd_rows_kernel(NormP p) {
       const int c = 8 * rl + 2048 * u;
       if (ok && c < p.d) {
         float gv[8];
-        load8_dt(p.dn, base + c, p.dn_dt, a[u]);
-        load8_dt(p.x, base + c, p.x_dt, b[u]);
-        load8_dt(p.g, c, p.w_dt, gv);
+        ld8<DNDT>(p.dn, base + c, p.dn_dt, a[u]);
+        ld8<XDT>(p.x, base + c, p.x_dt, b[u]);
+        ld8<WDT>(p.g, c, p.w_dt, gv);
 #pragma unroll
         for (int e = 0; e < 8; ++e) dot += a[u][e] * gv[e] * b[u][e];
       }
@@ -184,9 +201,9 @@ __global__ __launch_bounds__(BW_THREADS) void rmsnorm_bwd_rows_kernel(NormP p) {
       const int c = 8 * rl + 2048 * u;
       if (c < p.d) {
         float o[8], gv[8];
-        load8_dt(p.g, c, p.w_dt, gv);
+        ld8<WDT>(p.g, c, p.w_dt, gv);
         if (p.dres) {
-          load8_dt(p.dres, base + c, p.dres_dt, o);
+          ld8<RDT>(p.dres, base + c, p.dres_dt, o);
         } else {
 #pragma unroll
           for (int e = 0; e < 8; ++e) o[e] = 0.0f;
@@ -196,8 +213,8 @@ __global__ __launch_bounds__(BW_THREADS) void rmsnorm_bwd_rows_kernel(NormP p) {
           o[e] += r * (a[u][e] * gv[e] - b[u][e] * r2m);
           acc[u][e] += a[u][e] * (b[u][e] * r);
         }
-        store8_dt(p.dx, base + c, p.out_dt, o);
-        if (p.dx_copy) store8_dt(p.dx_copy, base + c, LC_BF16, o);
+        st8<ODT>(p.dx, base + c, p.out_dt, o);
+        if (p.dx_copy) st8<LC_BF16>(p.dx_copy, base + c, LC_BF16, o);
       }
     }
   }
@@ -330,8 +347,13 @@ NormP make_params(const lc_norm_args &a) {
 lc_status rmsnorm_fwd_launch(const lc_norm_args &a, hipStream_t s) {
   LC_TRY(check_common(a, false));
   const NormP p = make_params(a);
-  hipLaunchKernelGGL(rmsnorm_fwd_kernel, dim3((unsigned)((a.T + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK)),
-                     dim3(256), 0, s, p);
+  const dim3 grid((unsigned)((a.T + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK));
+  // the decoder stage's type mix (fp32 residual rows, bf16 gain and output)
+  // has its own instantiation; every other mix takes the generic kernel
+  if (p.x_dt == LC_FP32 && p.w_dt == LC_BF16 && p.out_dt == LC_BF16)
+    hipLaunchKernelGGL((rmsnorm_fwd_kernel<LC_FP32, LC_BF16, LC_BF16>), grid, dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL((rmsnorm_fwd_kernel<-1, -1, -1>), grid, dim3(256), 0, s, p);
   return check_launch("rmsnorm_fwd_kernel");
 }
 
@@ -341,7 +363,15 @@ namespace {
 // when p.part is set.
 lc_status bwd_rows(const NormP &p, hipStream_t s) {
   if (p.d <= MAXD) {
-    hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel, dim3((unsigned)p.nblk), dim3(BW_THREADS), 0, s, p);
+    // the decoder stage's type mix (fp32 dn, x, residual gradient and dx, bf16
+    // gain) has its own instantiation; every other mix takes the generic kernel
+    if (p.dn_dt == LC_FP32 && p.x_dt == LC_FP32 && p.w_dt == LC_BF16 && p.out_dt == LC_FP32 &&
+        (!p.dres || p.dres_dt == LC_FP32))
+      hipLaunchKernelGGL((rmsnorm_bwd_rows_kernel<LC_FP32, LC_FP32, LC_BF16, LC_FP32, LC_FP32>),
+                         dim3((unsigned)p.nblk), dim3(BW_THREADS), 0, s, p);
+    else
+      hipLaunchKernelGGL((rmsnorm_bwd_rows_kernel<-1, -1, -1, -1, -1>), dim3((unsigned)p.nblk),
+                         dim3(BW_THREADS), 0, s, p);
     return check_launch("rmsnorm_bwd_rows_kernel");
   }
   hipLaunchKernelGGL(rmsnorm_bwd_long_kernel, dim3((unsigned)p.nblk), dim3(256), 0, s, p);

@@ -250,7 +250,21 @@ __device__ __forceinline__ void interleave_steps() {
   }
 }
 
-template <bool A_K, bool B_K, int EPI>
+// Element types of an epilogue's tensors: TM = 0 takes them from the run-time
+// values in GemmP (uniform branches around every access); TM = 1 fixes them to
+// the decoder stage's own mix for EPI (the branch-free accesses let the
+// compiler keep the epilogue's loads in flight instead of waiting at each
+// branch): residual add fp32 R and C, SwiGLU and its backward fp32 gate/up and
+// bf16 C. The host takes TM = 1 when the call's types are exactly that mix.
+template <int EPI, int TM>
+struct EpiTypes {
+  static constexpr bool RES = EPI == LC_EPI_RESIDUAL, SWI = EPI == LC_EPI_SWIGLU || EPI == LC_EPI_SWIGLU_BWD;
+  static constexpr int C = TM == 0 ? -1 : RES ? LC_FP32 : SWI ? LC_BF16 : -1;
+  static constexpr int R = TM == 0 ? -1 : RES ? LC_FP32 : -1;
+  static constexpr int X = TM == 0 ? -1 : SWI ? LC_FP32 : -1;
+};
+
+template <bool A_K, bool B_K, int EPI, int TM>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   __shared__ __align__(16) char ring[2 * STAGE_BYTES];
 
@@ -409,6 +423,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
   __syncthreads();  // every wave's last fragment reads are done
   const int frow = lane & 31, fhalf = lane >> 5;
   lds_t *const E = R0 + wave * 16384;
+  typedef EpiTypes<EPI, TM> ET;
+  const int c_dt = ET::C >= 0 ? ET::C : p.c_dt, r_dt = ET::R >= 0 ? ET::R : p.r_dt,
+            aux_dt = ET::X >= 0 ? ET::X : p.aux_dt;
   typedef __attribute__((ext_vector_type(4))) float f32x4_t;
   typedef __attribute__((address_space(3))) f32x4_t lds_f4;
   const int ncol0 = n0 + wn * WN;  // first of the wave's 128 accumulator columns (non-SwiGLU)
@@ -470,12 +487,12 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
                 }
               }
               const int64_t row = (int64_t)m * p.ldc + ncol0 + 4 * q;
-              store4_dt(Cp, row, p.c_dt, a[0], a[1], a[2], a[3]);
-              store4_dt(Cp, row + 64, p.c_dt, b[0], b[1], b[2], b[3]);
+              store4_dt(Cp, row, c_dt, a[0], a[1], a[2], a[3]);
+              store4_dt(Cp, row + 64, c_dt, b[0], b[1], b[2], b[3]);
               if (p.aux0) {  // a second copy in aux_dt
                 const int64_t ra = (int64_t)m * p.ld_aux + ncol0 + 4 * q;
-                store4_dt(p.aux0, ra, p.aux_dt, a[0], a[1], a[2], a[3]);
-                store4_dt(p.aux0, ra + 64, p.aux_dt, b[0], b[1], b[2], b[3]);
+                store4_dt(p.aux0, ra, aux_dt, a[0], a[1], a[2], a[3]);
+                store4_dt(p.aux0, ra + 64, aux_dt, b[0], b[1], b[2], b[3]);
               }
             } else {
               const int n = n0 + wn * 64 + 4 * q;  // output column of the gate/up pair
@@ -484,9 +501,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
 #pragma unroll
               for (int e = 0; e < 4; ++e) act[e] = a[e] * sigmoidf_(a[e]) * b[e];
               const int64_t oa = (int64_t)m * p.ld_aux + n;
-              store4_dt(p.aux0, oa, p.aux_dt, a[0], a[1], a[2], a[3]);
-              store4_dt(p.aux1, oa, p.aux_dt, b[0], b[1], b[2], b[3]);
-              store4_dt(Cp, (int64_t)m * p.ldc + n, p.c_dt, act[0], act[1], act[2], act[3]);
+              store4_dt(p.aux0, oa, aux_dt, a[0], a[1], a[2], a[3]);
+              store4_dt(p.aux1, oa, aux_dt, b[0], b[1], b[2], b[3]);
+              store4_dt(Cp, (int64_t)m * p.ldc + n, c_dt, act[0], act[1], act[2], act[3]);
             }
           }
         }
@@ -511,12 +528,12 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
 #pragma unroll
       for (int u = 0; u < PU; ++u) {
         const int mc = min(mrow0 + row_of(t, u), m_lim - 1);
-        if constexpr (EPI == LC_EPI_RESIDUAL) x[u] = load4_dt(p.R, (int64_t)mc * p.ldr + ncl, p.r_dt);
+        if constexpr (EPI == LC_EPI_RESIDUAL) x[u] = load4_dt(p.R, (int64_t)mc * p.ldr + ncl, r_dt);
         if constexpr (EPI == LC_EPI_ACCUM_F32)
           x[u] = *reinterpret_cast<const float4 *>(static_cast<const float *>(Cp) + (int64_t)mc * p.ldc + ncl);
         if constexpr (EPI == LC_EPI_SWIGLU_BWD) {
-          x[u] = load4_dt(p.aux0, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
-          y[u] = load4_dt(p.aux1, (int64_t)mc * p.ld_aux + ncl, p.aux_dt);
+          x[u] = load4_dt(p.aux0, (int64_t)mc * p.ld_aux + ncl, aux_dt);
+          y[u] = load4_dt(p.aux1, (int64_t)mc * p.ld_aux + ncl, aux_dt);
         }
       }
     };
@@ -564,23 +581,23 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
         if constexpr (EPI == LC_EPI_ACCUM_F32) {
           *reinterpret_cast<float4 *>(static_cast<float *>(Cp) + oc) = ra[u];
         } else {
-          store4_dt(Cp, oc, p.c_dt, ra[u].x, ra[u].y, ra[u].z, ra[u].w);
+          store4_dt(Cp, oc, c_dt, ra[u].x, ra[u].y, ra[u].z, ra[u].w);
           if constexpr (EPI == LC_EPI_SWIGLU_BWD)
-            store4_dt(Cp, oc + p.N, p.c_dt, rb[u].x, rb[u].y, rb[u].z, rb[u].w);
+            store4_dt(Cp, oc + p.N, c_dt, rb[u].x, rb[u].y, rb[u].z, rb[u].w);
         }
       }
     }
   }
 }
 
-template <bool A_K, bool B_K, int EPI>
+template <bool A_K, bool B_K, int EPI, int TM = 0>
 lc_status launch_t(const GemmP &p, hipStream_t s) {
   // LC_GROUP_ROWS: an upper bound on the groups' row tiles (each group adds at
   // most one partial tile); LC_GROUP_K: every group has the full output grid
   unsigned grid = (unsigned)p.tiles_m * (unsigned)p.tiles_n;
   if (p.gmode == LC_GROUP_ROWS) grid = (unsigned)(p.tiles_m + p.ngroups) * (unsigned)p.tiles_n;
   if (p.gmode == LC_GROUP_K) grid *= (unsigned)p.ngroups;
-  hipLaunchKernelGGL((gemm_bf16_kernel<A_K, B_K, EPI>), dim3(grid), dim3(NT), 0, s, p);
+  hipLaunchKernelGGL((gemm_bf16_kernel<A_K, B_K, EPI, TM>), dim3(grid), dim3(NT), 0, s, p);
   return check_launch("gemm_bf16_kernel");
 }
 
@@ -726,15 +743,21 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
       if (!ak && !bk) return launch_t<false, false, LC_EPI_ACCUM_F32>(p, s);
       break;
     case LC_EPI_RESIDUAL:
+      if (ak && bk && p.c_dt == LC_FP32 && p.r_dt == LC_FP32)
+        return launch_t<true, true, LC_EPI_RESIDUAL, 1>(p, s);
       if (ak && bk) return launch_t<true, true, LC_EPI_RESIDUAL>(p, s);
       break;
     case LC_EPI_ROPE:
       if (ak && bk) return launch_t<true, true, LC_EPI_ROPE>(p, s);
       break;
     case LC_EPI_SWIGLU:
+      if (ak && bk && p.c_dt == LC_BF16 && p.aux_dt == LC_FP32)
+        return launch_t<true, true, LC_EPI_SWIGLU, 1>(p, s);
       if (ak && bk) return launch_t<true, true, LC_EPI_SWIGLU>(p, s);
       break;
     case LC_EPI_SWIGLU_BWD:
+      if (ak && !bk && p.c_dt == LC_BF16 && p.aux_dt == LC_FP32)
+        return launch_t<true, false, LC_EPI_SWIGLU_BWD, 1>(p, s);
       if (ak && !bk) return launch_t<true, false, LC_EPI_SWIGLU_BWD>(p, s);
       if (ak && bk) return launch_t<true, true, LC_EPI_SWIGLU_BWD>(p, s);
       break;

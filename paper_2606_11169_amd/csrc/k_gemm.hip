@@ -255,13 +255,15 @@ __device__ __forceinline__ void interleave_steps() {
 // the decoder stage's own mix for EPI (the branch-free accesses let the
 // compiler keep the epilogue's loads in flight instead of waiting at each
 // branch): residual add fp32 R and C, SwiGLU and its backward fp32 gate/up and
-// bf16 C. The host takes TM = 1 when the call's types are exactly that mix.
+// bf16 C, RoPE fp16 C and bf16 copy. The host takes TM = 1 when the call's
+// types are exactly that mix.
 template <int EPI, int TM>
 struct EpiTypes {
   static constexpr bool RES = EPI == LC_EPI_RESIDUAL, SWI = EPI == LC_EPI_SWIGLU || EPI == LC_EPI_SWIGLU_BWD;
-  static constexpr int C = TM == 0 ? -1 : RES ? LC_FP32 : SWI ? LC_BF16 : -1;
+  static constexpr bool ROPE = EPI == LC_EPI_ROPE;
+  static constexpr int C = TM == 0 ? -1 : RES ? LC_FP32 : SWI ? LC_BF16 : ROPE ? LC_FP16 : -1;
   static constexpr int R = TM == 0 ? -1 : RES ? LC_FP32 : -1;
-  static constexpr int X = TM == 0 ? -1 : SWI ? LC_FP32 : -1;
+  static constexpr int X = TM == 0 ? -1 : SWI ? LC_FP32 : ROPE ? LC_BF16 : -1;
 };
 
 template <bool A_K, bool B_K, int EPI, int TM>
@@ -748,6 +750,8 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
       if (ak && bk) return launch_t<true, true, LC_EPI_RESIDUAL>(p, s);
       break;
     case LC_EPI_ROPE:
+      if (ak && bk && p.c_dt == LC_FP16 && (!p.aux0 || p.aux_dt == LC_BF16))
+        return launch_t<true, true, LC_EPI_ROPE, 1>(p, s);
       if (ak && bk) return launch_t<true, true, LC_EPI_ROPE>(p, s);
       break;
     case LC_EPI_SWIGLU:

@@ -6,6 +6,8 @@
 #include <stddef.h>
 
 #include "libchunk.h"
+
+#include <type_traits>
 #include "libchunk_ops.h"
 #include "host_core.hpp"
 
@@ -89,6 +91,28 @@ __device__ __forceinline__ void load8_dt(const void *base, int64_t idx, int dt, 
 __device__ __forceinline__ void store8_dt(void *base, int64_t idx, int dt, const float (&x)[8]) {
   store4_dt(base, idx, dt, x[0], x[1], x[2], x[3]);
   store4_dt(base, idx + 4, dt, x[4], x[5], x[6], x[7]);
+}
+
+// 8 consecutive values of a tensor whose element type is the template
+// argument DT, or the run-time value rt when DT < 0: with a compile-time type
+// the accesses are straight-line code, which lets the compiler keep several
+// loads in flight instead of waiting at the type branches
+template <int DT>
+__device__ __forceinline__ void ld8(const void *base, int64_t idx, int rt, float (&x)[8]) {
+  load8_dt(base, idx, DT < 0 ? rt : DT, x);
+}
+template <int DT>
+__device__ __forceinline__ void st8(void *base, int64_t idx, int rt, const float (&x)[8]) {
+  store8_dt(base, idx, DT < 0 ? rt : DT, x);
+}
+
+// Calls f with the element type dt as a compile-time constant
+// (std::integral_constant<int, dt>); dt must be a valid lc_dtype.
+template <typename F>
+inline void with_dtype(int dt, F f) {
+  if (dt == LC_FP32) f(std::integral_constant<int, LC_FP32>{});
+  else if (dt == LC_BF16) f(std::integral_constant<int, LC_BF16>{});
+  else f(std::integral_constant<int, LC_FP16>{});
 }
 
 // logistic sigmoid with the hardware reciprocal (about 1 ulp); used in

@@ -39,6 +39,7 @@ struct RouteP {
 };
 
 // one wave per token, 4 tokens per workgroup
+template <int ND, int WD>  // element types of n and Wr (compile-time)
 __global__ __launch_bounds__(256) void moe_route_kernel(RouteP p) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -52,8 +53,8 @@ __global__ __launch_bounds__(256) void moe_route_kernel(RouteP p) {
     float s = 0.0f;
     for (int c = lane * 8; c < p.d; c += 64 * 8) {
       float a[8], b[8];
-      load8_dt(p.n, t * p.d + c, p.n_dt, a);
-      load8_dt(p.wr, (int64_t)e * p.d + c, p.w_dt, b);
+      ld8<ND>(p.n, t * p.d + c, p.n_dt, a);
+      ld8<WD>(p.wr, (int64_t)e * p.d + c, p.w_dt, b);
 #pragma unroll
       for (int i = 0; i < 8; ++i) s += a[i] * b[i];
     }
@@ -193,6 +194,7 @@ struct CombineP {
   int d, h_dt, out_dt;
 };
 
+template <int HD, int OD>  // element types of h and out
 __global__ __launch_bounds__(256) void moe_combine_kernel(CombineP p) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -203,12 +205,12 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(CombineP p) {
   const int64_t r0 = q0 >= 0 ? q0 : 0, r1 = q1 >= 0 ? q1 : 0;
   for (int c = lane * 8; c < p.d; c += 64 * 8) {
     float x[8], a[8], b[8];
-    load8_dt(p.h, t * p.d + c, p.h_dt, x);
-    load8_dt(p.eo, r0 * p.d + c, LC_FP32, a);
-    load8_dt(p.eo, r1 * p.d + c, LC_FP32, b);
+    ld8<HD>(p.h, t * p.d + c, p.h_dt, x);
+    ld8<LC_FP32>(p.eo, r0 * p.d + c, LC_FP32, a);
+    ld8<LC_FP32>(p.eo, r1 * p.d + c, LC_FP32, b);
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = (x[i] + w0 * a[i]) + w1 * b[i];
-    store8_dt(p.out, t * p.d + c, p.out_dt, x);
+    st8<OD>(p.out, t * p.d + c, p.out_dt, x);
   }
 }
 
@@ -224,6 +226,7 @@ struct BwdGatherP {
   int d, dy_dt, dys_dt;
 };
 
+template <int GD, int SD>  // element types of dy and dys
 __global__ __launch_bounds__(256) void moe_bwd_gather_kernel(BwdGatherP p) {
   const int lane = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -233,14 +236,14 @@ __global__ __launch_bounds__(256) void moe_bwd_gather_kernel(BwdGatherP p) {
   float dot = 0.0f;
   for (int c = lane * 8; c < p.d; c += 64 * 8) {
     float g[8], e[8];
-    load8_dt(p.dy, t * p.d + c, p.dy_dt, g);
-    load8_dt(p.eo, r * p.d + c, LC_FP32, e);
+    ld8<GD>(p.dy, t * p.d + c, p.dy_dt, g);
+    ld8<LC_FP32>(p.eo, r * p.d + c, LC_FP32, e);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       dot += g[i] * e[i];
       g[i] *= wr;
     }
-    store8_dt(p.dys, r * p.d + c, p.dys_dt, g);
+    st8<SD>(p.dys, r * p.d + c, p.dys_dt, g);
   }
   dot = wave_sum(dot);
   if (lane == 0) p.dw[r] = dot;
@@ -258,6 +261,7 @@ struct BwdCombineP {
   int d, w_dt;
 };
 
+template <int WD>  // element type of Wr
 __global__ __launch_bounds__(256) void moe_bwd_combine_kernel(BwdCombineP p) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -277,13 +281,13 @@ __global__ __launch_bounds__(256) void moe_bwd_combine_kernel(BwdCombineP p) {
   }
   for (int c = lane * 8; c < p.d; c += 64 * 8) {
     float a[8], b[8], g0[8], g1[8];
-    load8_dt(p.dns, r0 * p.d + c, LC_FP32, a);
-    load8_dt(p.dns, r1 * p.d + c, LC_FP32, b);
-    load8_dt(p.wr, (int64_t)e0 * p.d + c, p.w_dt, g0);
-    load8_dt(p.wr, (int64_t)e1 * p.d + c, p.w_dt, g1);
+    ld8<LC_FP32>(p.dns, r0 * p.d + c, LC_FP32, a);
+    ld8<LC_FP32>(p.dns, r1 * p.d + c, LC_FP32, b);
+    ld8<WD>(p.wr, (int64_t)e0 * p.d + c, p.w_dt, g0);
+    ld8<WD>(p.wr, (int64_t)e1 * p.d + c, p.w_dt, g1);
 #pragma unroll
     for (int i = 0; i < 8; ++i) a[i] = ((s0 * a[i] + s1 * b[i]) + dl0 * g0[i]) + dl1 * g1[i];
-    store8_dt(p.dn, t * p.d + c, LC_FP32, a);
+    st8<LC_FP32>(p.dn, t * p.d + c, LC_FP32, a);
   }
 }
 
@@ -298,6 +302,7 @@ struct RouterGradP {
 };
 
 // partial[blk][e][i] = sum over the block's tokens of dl(t, e) n[t, i]
+template <int ND>  // element type of n
 __global__ __launch_bounds__(256) void moe_router_partial_kernel(RouterGradP p) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   const int blk = blockIdx.y, e = blockIdx.z;
@@ -308,8 +313,9 @@ __global__ __launch_bounds__(256) void moe_router_partial_kernel(RouterGradP p) 
   for (int64_t t = t0; t < t1; ++t) {
     const float c = p.sel[2 * t] == e ? p.dl[2 * t] : (p.sel[2 * t + 1] == e ? p.dl[2 * t + 1] : 0.0f);
     float x;
-    if (p.n_dt == LC_FP32) x = static_cast<const float *>(p.n)[t * p.d + i];
-    else x = (float)static_cast<const __bf16 *>(p.n)[t * p.d + i];
+    if constexpr (ND == LC_FP32) x = static_cast<const float *>(p.n)[t * p.d + i];
+    else if constexpr (ND == LC_BF16) x = (float)static_cast<const __bf16 *>(p.n)[t * p.d + i];
+    else x = (float)static_cast<const _Float16 *>(p.n)[t * p.d + i];
     s += c * x;
   }
   p.partial[((int64_t)blk * p.E + e) * p.d + i] = s;
@@ -342,7 +348,12 @@ lc_status moe_route_launch(const lc_moe_args &a, hipStream_t s) {
   if (!valid_dtype(a.n_dtype) || !valid_dtype(a.w_dtype))
     return fail(LC_ERR_INVALID_ARG, "moe route: unknown dtype");
   RouteP p{a.n, a.wr, a.sel, a.w, a.T, a.d, a.E, a.n_dtype, a.w_dtype};
-  hipLaunchKernelGGL(moe_route_kernel, dim3(rows_grid(a.T)), dim3(256), 0, s, p);
+  with_dtype(a.n_dtype, [&](auto nd) {
+    with_dtype(a.w_dtype, [&](auto wd) {
+      hipLaunchKernelGGL((moe_route_kernel<decltype(nd)::value, decltype(wd)::value>),
+                         dim3(rows_grid(a.T)), dim3(256), 0, s, p);
+    });
+  });
   return check_launch("moe_route_kernel");
 }
 
@@ -369,7 +380,12 @@ lc_status moe_combine_launch(const void *h, int h_dt, const float *eo, const flo
                              const int32_t *rowpos, void *out, int out_dt, int64_t T, int d,
                              hipStream_t s) {
   CombineP p{h, eo, w, rowpos, out, T, d, h_dt, out_dt};
-  hipLaunchKernelGGL(moe_combine_kernel, dim3(rows_grid(T)), dim3(256), 0, s, p);
+  with_dtype(h_dt, [&](auto hd) {
+    with_dtype(out_dt, [&](auto od) {
+      hipLaunchKernelGGL((moe_combine_kernel<decltype(hd)::value, decltype(od)::value>),
+                         dim3(rows_grid(T)), dim3(256), 0, s, p);
+    });
+  });
   return check_launch("moe_combine_kernel");
 }
 
@@ -377,7 +393,12 @@ lc_status moe_bwd_gather_launch(const void *dy, int dy_dt, const float *eo, cons
                                 const float *wrow, void *dys, int dys_dt, float *dw,
                                 int64_t rows, int d, hipStream_t s) {
   BwdGatherP p{dy, eo, perm, wrow, dys, dw, rows, d, dy_dt, dys_dt};
-  hipLaunchKernelGGL(moe_bwd_gather_kernel, dim3(rows_grid(rows)), dim3(256), 0, s, p);
+  with_dtype(dy_dt, [&](auto gd) {
+    with_dtype(dys_dt, [&](auto sd) {
+      hipLaunchKernelGGL((moe_bwd_gather_kernel<decltype(gd)::value, decltype(sd)::value>),
+                         dim3(rows_grid(rows)), dim3(256), 0, s, p);
+    });
+  });
   return check_launch("moe_bwd_gather_kernel");
 }
 
@@ -386,7 +407,10 @@ lc_status moe_bwd_combine_launch(const float *dns, const float *dw, const float 
                                  int w_dt, float *dl, float *dn, int64_t T, int d,
                                  hipStream_t s) {
   BwdCombineP p{dns, dw, w, sel, rowpos, wr, dl, dn, T, d, w_dt};
-  hipLaunchKernelGGL(moe_bwd_combine_kernel, dim3(rows_grid(T)), dim3(256), 0, s, p);
+  with_dtype(w_dt, [&](auto wd) {
+    hipLaunchKernelGGL((moe_bwd_combine_kernel<decltype(wd)::value>), dim3(rows_grid(T)), dim3(256),
+                       0, s, p);
+  });
   return check_launch("moe_bwd_combine_kernel");
 }
 
@@ -397,8 +421,10 @@ lc_status moe_router_grad_launch(const void *n, int n_dt, const int32_t *sel, co
   if (scratch_bytes < moe_router_scratch_size(T, d, E))
     return fail(LC_ERR_WORKSPACE, "moe router gradient: scratch too small");
   RouterGradP p{n, sel, dl, scratch, g, T, d, E, n_dt, nblk};
-  hipLaunchKernelGGL(moe_router_partial_kernel, dim3((unsigned)((d + 255) / 256), (unsigned)nblk,
-                     (unsigned)E), dim3(256), 0, s, p);
+  with_dtype(n_dt, [&](auto nd) {
+    hipLaunchKernelGGL((moe_router_partial_kernel<decltype(nd)::value>),
+                       dim3((unsigned)((d + 255) / 256), (unsigned)nblk, (unsigned)E), dim3(256), 0, s, p);
+  });
   LC_TRY(check_launch("moe_router_partial_kernel"));
   hipLaunchKernelGGL(moe_router_final_kernel, dim3((unsigned)(((int64_t)E * d + 255) / 256)),
                      dim3(256), 0, s, p);

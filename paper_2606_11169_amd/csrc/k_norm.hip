@@ -28,19 +28,6 @@ namespace lc {
 namespace {
 
 constexpr int ROWS_PER_BLOCK = 4;  // forward: one wave per row
-
-// 8 consecutive values of a tensor whose element type is the template
-// argument DT, or the run-time value rt when DT < 0 (the generic kernels):
-// with a compile-time type the loads are straight-line code, which lets the
-// compiler keep several rows' loads in flight without waiting at branches
-template <int DT>
-__device__ __forceinline__ void ld8(const void *base, int64_t idx, int rt, float (&x)[8]) {
-  load8_dt(base, idx, DT < 0 ? rt : DT, x);
-}
-template <int DT>
-__device__ __forceinline__ void st8(void *base, int64_t idx, int rt, const float (&x)[8]) {
-  store8_dt(base, idx, DT < 0 ? rt : DT, x);
-}
 constexpr int MAXU = 8;            // 8-element chunks per lane held in registers
 constexpr int MAXD = 64 * 8 * MAXU;
 

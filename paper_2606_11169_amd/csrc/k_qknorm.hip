@@ -49,6 +49,7 @@ __device__ __forceinline__ float row_sum(float v, int lpr) {
   return v;
 }
 
+template <int XD, int WD>  // element types of q|k and the gains (compile-time)
 __global__ __launch_bounds__(NTH) void qk_norm_rope_fwd_kernel(QkP p) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int rpw = 64 / p.lpr, l = lane % p.lpr;
@@ -59,8 +60,8 @@ __global__ __launch_bounds__(NTH) void qk_norm_rope_fwd_kernel(QkP p) {
   const bool isq = j < p.H;
   const int64_t col = (int64_t)j * p.hd + 8 * l;  // q heads then k heads
   float x[8];
-  load8_dt(p.qk, t * p.ld + col, p.x_dt, x);
-  store8_dt(p.raw, row * p.hd + 8 * l, p.x_dt, x);
+  ld8<XD>(p.qk, t * p.ld + col, p.x_dt, x);
+  st8<XD>(p.raw, row * p.hd + 8 * l, p.x_dt, x);
   float ss = 0.0f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) ss += x[e] * x[e];
@@ -68,7 +69,7 @@ __global__ __launch_bounds__(NTH) void qk_norm_rope_fwd_kernel(QkP p) {
   const float r = 1.0f / sqrtf(ss / (float)p.hd + p.eps);
   if (l == 0) p.rstd[row] = r;
   float g[8];
-  load8_dt(isq ? p.gq : p.gk, 8 * l, p.w_dt, g);
+  ld8<WD>(isq ? p.gq : p.gk, 8 * l, p.w_dt, g);
   float y[8], z[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) y[e] = x[e] * r * g[e];
@@ -86,9 +87,10 @@ __global__ __launch_bounds__(NTH) void qk_norm_rope_fwd_kernel(QkP p) {
     // first half: a c - b s; second half: a s + b c (a = value i, b = value i + hd/2)
     z[e] = first ? y[e] * c - other * s : other * s + y[e] * c;
   }
-  store8_dt(p.qk, t * p.ld + col, p.x_dt, z);
+  st8<XD>(p.qk, t * p.ld + col, p.x_dt, z);
 }
 
+template <int XD, int WD, int DD>  // element types of raw q|k, the gains and the gradient
 __global__ __launch_bounds__(NTH) void qk_norm_bwd_kernel(QkP p) {
   __shared__ float red[2][128];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -98,8 +100,8 @@ __global__ __launch_bounds__(NTH) void qk_norm_bwd_kernel(QkP p) {
   float aq[8], ak[8], gq[8], gk[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) aq[e] = ak[e] = 0.0f;
-  load8_dt(p.gq, 8 * l, p.w_dt, gq);
-  load8_dt(p.gk, 8 * l, p.w_dt, gk);
+  ld8<WD>(p.gq, 8 * l, p.w_dt, gq);
+  ld8<WD>(p.gk, 8 * l, p.w_dt, gk);
   // iteration it: rows r0 + (4 it + wv) rpw + slot
   for (int64_t base = r0 + (int64_t)wv * rpw; base < r1; base += 4 * rpw) {
     const int64_t row = base + slot;
@@ -110,8 +112,8 @@ __global__ __launch_bounds__(NTH) void qk_norm_bwd_kernel(QkP p) {
     const bool isq = j < p.H;
     const int64_t col = (int64_t)j * p.hd + 8 * l;
     float a[8], b[8];
-    load8_dt(p.dqk, t * p.ld_d + col, p.d_dt, a);
-    load8_dt(p.raw, rr * p.hd + 8 * l, p.x_dt, b);
+    ld8<DD>(p.dqk, t * p.ld_d + col, p.d_dt, a);
+    ld8<XD>(p.raw, rr * p.hd + 8 * l, p.x_dt, b);
     const float r = p.rstd[rr];
     float dot = 0.0f;  // sum dy * g * x
 #pragma unroll
@@ -129,7 +131,7 @@ __global__ __launch_bounds__(NTH) void qk_norm_bwd_kernel(QkP p) {
       if (isq) aq[e] += term;
       else ak[e] += term;
     }
-    store8_dt(p.dqk, t * p.ld_d + col, p.d_dt, o);
+    st8<DD>(p.dqk, t * p.ld_d + col, p.d_dt, o);
   }
   // the wave's row slots: fixed shuffle tree (slot 0 ends with the sum)
   for (int o = p.lpr; o < 64; o <<= 1) {
@@ -240,15 +242,28 @@ lc_status qknorm_fwd_launch(const lc_qknorm_args &a, hipStream_t s) {
   LC_TRY(check(a, false));
   const QkP p = make(a);
   const int64_t rows = a.T * p.NH, per_block = 4 * (64 / p.lpr);
-  hipLaunchKernelGGL(qk_norm_rope_fwd_kernel, dim3((unsigned)((rows + per_block - 1) / per_block)),
-                     dim3(NTH), 0, s, p);
+  const dim3 grid((unsigned)((rows + per_block - 1) / per_block));
+  with_dtype(p.x_dt, [&](auto xd) {
+    with_dtype(p.w_dt, [&](auto wd) {
+      hipLaunchKernelGGL((qk_norm_rope_fwd_kernel<decltype(xd)::value, decltype(wd)::value>), grid,
+                         dim3(NTH), 0, s, p);
+    });
+  });
   return check_launch("qk_norm_rope_fwd_kernel");
 }
 
 lc_status qknorm_bwd_partials_launch(const lc_qknorm_args &a, hipStream_t s) {
   LC_TRY(check(a, true));
   const QkP p = make(a);
-  hipLaunchKernelGGL(qk_norm_bwd_kernel, dim3((unsigned)p.nblk), dim3(NTH), 0, s, p);
+  with_dtype(p.x_dt, [&](auto xd) {
+    with_dtype(p.w_dt, [&](auto wd) {
+      with_dtype(p.d_dt, [&](auto dd) {
+        hipLaunchKernelGGL((qk_norm_bwd_kernel<decltype(xd)::value, decltype(wd)::value,
+                                               decltype(dd)::value>),
+                           dim3((unsigned)p.nblk), dim3(NTH), 0, s, p);
+      });
+    });
+  });
   return check_launch("qk_norm_bwd_kernel");
 }
 

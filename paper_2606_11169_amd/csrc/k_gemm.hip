@@ -50,7 +50,8 @@
 // 16 contiguous bytes per lane, and the column pairs (c, c + 64) that RoPE and
 // SwiGLU combine sit in the same lane (blocks j and j + 2 of a 128-wide wave).
 // Output, residual and gate/up element types are run-time values (uniform
-// branches in the epilogue only).
+// branches in the epilogue only), except in the instantiations for the decoder
+// stage's own type mix (EpiTypes below), where they are compile-time constants.
 #include "common.hpp"
 
 #include <type_traits>

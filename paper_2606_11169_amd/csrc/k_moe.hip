@@ -301,24 +301,47 @@ struct RouterGradP {
   int d, E, n_dt, nblk;
 };
 
-// partial[blk][e][i] = sum over the block's tokens of dl(t, e) n[t, i]
+// partial[blk][e][i] = sum over the block's tokens of dl(t, e) n[t, i]. A
+// thread owns column i for a group of up to 8 experts (grid z), so each n
+// value is read once per group rather than once per expert; every sum runs
+// over the block's tokens in order.
+constexpr int kRouterExpertsPerPass = 8;
 template <int ND>  // element type of n
 __global__ __launch_bounds__(256) void moe_router_partial_kernel(RouterGradP p) {
   const int i = blockIdx.x * 256 + threadIdx.x;
-  const int blk = blockIdx.y, e = blockIdx.z;
-  if (i >= p.d) return;
+  const int blk = blockIdx.y, eg = blockIdx.z * kRouterExpertsPerPass;
   const int64_t t0 = (int64_t)blk * kRouterTokensPerBlock;
   const int64_t t1 = min(p.T, t0 + kRouterTokensPerBlock);
-  float s = 0.0f;
+  float s[kRouterExpertsPerPass];
+#pragma unroll
+  for (int k = 0; k < kRouterExpertsPerPass; ++k) s[k] = 0.0f;
+  // the block's selections and logit gradients staged in LDS once
+  __shared__ int32_t ssel[2 * kRouterTokensPerBlock];
+  __shared__ float sdl[2 * kRouterTokensPerBlock];
+  for (int j = threadIdx.x; j < 2 * (int)(t1 - t0); j += 256) {
+    ssel[j] = p.sel[2 * t0 + j];
+    sdl[j] = p.dl[2 * t0 + j];
+  }
+  __syncthreads();
+  if (i >= p.d) return;
+#pragma unroll 4
   for (int64_t t = t0; t < t1; ++t) {
-    const float c = p.sel[2 * t] == e ? p.dl[2 * t] : (p.sel[2 * t + 1] == e ? p.dl[2 * t + 1] : 0.0f);
+    const int tl = (int)(t - t0);
+    const int e0 = ssel[2 * tl] - eg, e1 = ssel[2 * tl + 1] - eg;  // (the pair's experts differ)
+    const float d0 = sdl[2 * tl], d1 = sdl[2 * tl + 1];
     float x;
     if constexpr (ND == LC_FP32) x = static_cast<const float *>(p.n)[t * p.d + i];
     else if constexpr (ND == LC_BF16) x = (float)static_cast<const __bf16 *>(p.n)[t * p.d + i];
     else x = (float)static_cast<const _Float16 *>(p.n)[t * p.d + i];
-    s += c * x;
+#pragma unroll
+    for (int k = 0; k < kRouterExpertsPerPass; ++k) {
+      const float c = k == e0 ? d0 : (k == e1 ? d1 : 0.0f);
+      s[k] += c * x;
+    }
   }
-  p.partial[((int64_t)blk * p.E + e) * p.d + i] = s;
+#pragma unroll
+  for (int k = 0; k < kRouterExpertsPerPass; ++k)
+    if (eg + k < p.E) p.partial[((int64_t)blk * p.E + eg + k) * p.d + i] = s[k];
 }
 
 __global__ __launch_bounds__(256) void moe_router_final_kernel(RouterGradP p) {
@@ -423,7 +446,9 @@ lc_status moe_router_grad_launch(const void *n, int n_dt, const int32_t *sel, co
   RouterGradP p{n, sel, dl, scratch, g, T, d, E, n_dt, nblk};
   with_dtype(n_dt, [&](auto nd) {
     hipLaunchKernelGGL((moe_router_partial_kernel<decltype(nd)::value>),
-                       dim3((unsigned)((d + 255) / 256), (unsigned)nblk, (unsigned)E), dim3(256), 0, s, p);
+                       dim3((unsigned)((d + 255) / 256), (unsigned)nblk,
+                            (unsigned)((E + kRouterExpertsPerPass - 1) / kRouterExpertsPerPass)),
+                       dim3(256), 0, s, p);
   });
   LC_TRY(check_launch("moe_router_partial_kernel"));
   hipLaunchKernelGGL(moe_router_final_kernel, dim3((unsigned)(((int64_t)E * d + 255) / 256)),

@@ -99,7 +99,7 @@ struct DispatchP {
 constexpr int kDispatchThreads = 1024;
 
 __global__ __launch_bounds__(kDispatchThreads) void moe_dispatch_kernel(DispatchP p) {
-  __shared__ int cnt[65], run[64], wtot[kDispatchThreads / 64];
+  __shared__ int cnt[65], run[64];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (tid < 65) cnt[tid] = 0;
   __syncthreads();
@@ -132,34 +132,44 @@ __global__ __launch_bounds__(kDispatchThreads) void moe_dispatch_kernel(Dispatch
     p.perm[r] = 0;
     p.wrow[r] = 0.0f;
   }
+  // pairs in token order, kDispatchThreads tokens at a time: each wave counts
+  // its pairs of every expert with one ballot per expert (no barrier between
+  // experts), then each thread places its (at most two) pairs after the
+  // earlier waves' and lanes' pairs of the same expert
+  __shared__ int wcnt[64][kDispatchThreads / 64];
   const unsigned long long below = (1ull << lane) - 1ull;
   for (int base = 0; base < p.T; base += kDispatchThreads) {
     const int t = base + tid;
     const bool valid = t < p.T;
     const int a = valid ? p.sel[2 * t] : -1, b0 = valid ? p.sel[2 * t + 1] : -1;
     const int b = b0 == a ? -1 : b0;
+    unsigned long long bal_a = 0, bal_b = 0;
     for (int e = 0; e < p.E; ++e) {
-      const bool f = valid && (a == e || b == e);
-      const unsigned long long bal = __ballot(f);
-      if (lane == 0) wtot[wv] = __popcll(bal);
-      __syncthreads();
-      int pre = 0, tot = 0;
-      for (int i = 0; i < kDispatchThreads / 64; ++i) {
-        const int c = wtot[i];
-        pre += i < wv ? c : 0;
-        tot += c;
-      }
-      if (f) {
-        const int pos = run[e] + pre + __popcll(bal & below);
-        const int k = a == e ? 0 : 1;
+      const unsigned long long bal = __ballot(valid && (a == e || b == e));
+      if (lane == 0) wcnt[e][wv] = __popcll(bal);
+      if (a == e) bal_a = bal;
+      if (b == e) bal_b = bal;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int e = k == 0 ? a : b;
+      if (valid && e >= 0 && e < p.E) {
+        int pre = 0;
+        for (int i = 0; i < wv; ++i) pre += wcnt[e][i];
+        const int pos = run[e] + pre + __popcll((k == 0 ? bal_a : bal_b) & below);
         p.perm[pos] = t;
         p.wrow[pos] = p.w[2 * t + k];
         p.rowpos[2 * t + k] = pos;
       }
-      __syncthreads();
-      if (tid == 0) run[e] += tot;
-      __syncthreads();
     }
+    __syncthreads();
+    if (tid < p.E) {
+      int tot = 0;
+      for (int i = 0; i < kDispatchThreads / 64; ++i) tot += wcnt[tid][i];
+      run[tid] += tot;
+    }
+    __syncthreads();
   }
 }
 

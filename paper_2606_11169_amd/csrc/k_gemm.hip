@@ -279,7 +279,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmP p) {
 
   // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
   // contiguous run of tiles, then walk tiles in groups of p.group tile-rows
-  // (4 or 8, chosen by the host) so that neighbouring workgroups share A rows
+  // (chosen by the host) so that neighbouring workgroups share A rows
   // and B columns in the XCD's L2.
   int wg = blockIdx.x;
   const int nwg = gridDim.x;
@@ -719,9 +719,10 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
   p.tiles_m = (int)((a.M + BM - 1) / BM);
   p.tiles_n = a.epilogue == LC_EPI_SWIGLU ? (int)((a.N + BN / 2 - 1) / (BN / 2))
                                           : (int)((a.N + BN - 1) / BN);
-  // 4 tile-rows per group when the grid is wide (32 or more tile-columns),
-  // else 8: the faster walk measured on the stage's shapes
-  p.group = p.tiles_n >= 32 ? 4 : 8;
+  // 4 tile-rows per group: of 2, 4, 8 and 16, the fastest walk measured over
+  // the stage's shapes (8 ties it on most and is 1-2% slower on the
+  // narrow-grid dn2, dn1 and dW13 products; 2 and 16 are slower)
+  p.group = 4;
   p.gmode = a.group_mode;
   p.ngroups = a.group_mode == LC_GROUP_NONE ? 1 : a.n_groups;
   p.goff = a.group_offsets;

@@ -719,10 +719,12 @@ lc_status gemm_launch(const lc_gemm_args &a, hipStream_t s) {
   p.tiles_m = (int)((a.M + BM - 1) / BM);
   p.tiles_n = a.epilogue == LC_EPI_SWIGLU ? (int)((a.N + BN / 2 - 1) / (BN / 2))
                                           : (int)((a.N + BN - 1) / BN);
-  // 4 tile-rows per group: of 2, 4, 8 and 16, the fastest walk measured over
-  // the stage's shapes (8 ties it on most and is 1-2% slower on the
-  // narrow-grid dn2, dn1 and dW13 products; 2 and 16 are slower)
-  p.group = 4;
+  // 4 tile-rows per group, 3 when the grid has an odd number of tile-columns:
+  // the fastest walk measured over the stage's shapes among groups of 2 to 8
+  // and 16 (4 against 8: 1-2% faster on the 16-column dn2, dn1 and dW13
+  // products, equal on the rest; 3 against 4 on the 43-column SwiGLU backward
+  // and dW2 products: 1.5% and 3% faster)
+  p.group = (p.tiles_n & 1) ? 3 : 4;
   p.gmode = a.group_mode;
   p.ngroups = a.group_mode == LC_GROUP_NONE ? 1 : a.n_groups;
   p.goff = a.group_offsets;
